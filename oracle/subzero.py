@@ -1,0 +1,251 @@
+"""float64 reference of every step on the SubZero+ hot path (test infrastructure).
+
+Each function cites the passage of the paper it follows.  Readings of points
+where the paper is silent or ambiguous are marked READING and listed in the
+design notes of the repository.
+
+Pins (independent checks that this file is right) live in
+``tests/test_oracle_pins.py``.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+__all__ = [
+    "householder_qr", "haar_qr", "raw_qr_first_column",
+    "perturbation", "perturbed_weight", "perturbed_linear", "perturbed_linear_blocks",
+    "sq_loss", "central_estimate", "forward_estimate", "aggregate",
+    "adam_direction", "subspace_adam_update", "round_bf16", "tiny_run",
+]
+
+
+# ---------------------------------------------------------------------------
+# Subspace construction: Eq. 11 / Alg. 1 (HaarProjMatrix)
+# ---------------------------------------------------------------------------
+def householder_qr(A):
+    """Thin QR of a tall matrix by Householder reflections (textbook algorithm).
+
+    Returns (Q, R) with A = Q R, Q rows x r with orthonormal columns, R r x r
+    upper triangular.  The sign of each R_kk is whatever the reflector choice
+    gives (alpha = -sign(x_0) ||x||, the choice that avoids cancellation), i.e.
+    an implementation-dependent convention -- exactly the situation the paper's
+    sign correction addresses (Sec. "QR Subspace Construction with Sign
+    Correction").  A column that is already zero below and on the diagonal
+    gets no reflector and R_kk = 0.
+    """
+    A = np.array(A, dtype=np.float64, copy=True)
+    rows, r = A.shape
+    if rows < r:
+        raise ValueError("householder_qr needs rows >= columns")
+    vs = []
+    for k in range(r):
+        x = A[k:, k]
+        normx = math.sqrt(float(np.dot(x, x)))
+        if normx == 0.0:
+            vs.append(None)
+            continue
+        alpha = -math.copysign(normx, x[0])
+        v = x.copy()
+        v[0] -= alpha
+        v /= math.sqrt(float(np.dot(v, v)))
+        # H = I - 2 v v^T applied to the trailing block.
+        A[k:, k:] -= 2.0 * np.outer(v, v @ A[k:, k:])
+        A[k + 1:, k] = 0.0
+        vs.append(v)
+    R = np.triu(A[:r, :])
+    Q = np.zeros((rows, r), dtype=np.float64)
+    Q[:r, :r] = np.eye(r)
+    for k in reversed(range(r)):
+        v = vs[k]
+        if v is None:
+            continue
+        Q[k:, :] -= 2.0 * np.outer(v, v @ Q[k:, :])
+    return Q, R
+
+
+def haar_qr(Omega):
+    """Haar-distributed orthonormal factor: Eq. 11 / Alg. 1.
+
+    QR of the Gaussian matrix, then each column of Q is multiplied by the sign
+    of the matching diagonal entry of R, so that the corrected R has a positive
+    diagonal.  READING: sgn(0) := +1 (the paper leaves it undefined); a zero
+    diagonal entry is reported through ``rank_deficient_col`` (first such
+    column, or -1).
+
+    Returns (U, R_corrected, rank_deficient_col).
+    """
+    Q, R = householder_qr(Omega)
+    d = np.diag(R)
+    s = np.where(d < 0.0, -1.0, 1.0)
+    zero = np.nonzero(d == 0.0)[0]
+    return Q * s[None, :], R * s[:, None], (int(zero[0]) if zero.size else -1)
+
+
+def raw_qr_first_column(Omega):
+    """First column of Q from the same QR without the sign correction (negative control)."""
+    Q, _ = householder_qr(Omega)
+    return Q[:, 0]
+
+
+# ---------------------------------------------------------------------------
+# Perturbation: Eq. 4, Alg. 2 (PerturbParams), linear layer of Eq. 5
+# ---------------------------------------------------------------------------
+def perturbation(U, Z, V):
+    """Full-space perturbation U Z V^T of one matrix for one query (Eq. 4)."""
+    U = np.asarray(U, np.float64)
+    V = np.asarray(V, np.float64)
+    Z = np.asarray(Z, np.float64)
+    return U @ Z @ V.T
+
+
+def perturbed_weight(W, U, V, Z, sign, eps):
+    """W + sign * eps * U Z V^T, materialised (Alg. 2 with scale sign*eps)."""
+    return np.asarray(W, np.float64) + (sign * eps) * perturbation(U, Z, V)
+
+
+def perturbed_linear(X, W, U, V, Z, sign, eps):
+    """Output of a linear layer (nn.Linear layout, W is out x in) under the
+    perturbed weight: X (W + sign eps U Z V^T)^T (Eq. 5's forward, one layer)."""
+    Wp = perturbed_weight(W, U, V, Z, sign, eps)
+    return np.asarray(X, np.float64) @ Wp.T
+
+
+def perturbed_linear_blocks(Xb, W, U, V, Zs, blk_query, blk_sign, eps, rows=None):
+    """Blocks b = 0..nblk-1: Y_b = X_b (W + s_b eps U Z_{j(b)} V^T)^T.
+
+    ``Xb`` is a list of per-block activations (T x n).  ``rows`` optionally
+    restricts each block to a subset of its rows (the layer is row-wise, so
+    sampled rows are computed exactly as in the full product).
+    """
+    out = []
+    for b, X in enumerate(Xb):
+        Xr = np.asarray(X, np.float64) if rows is None else np.asarray(X, np.float64)[rows]
+        out.append(perturbed_linear(Xr, W, U, V, Zs[blk_query[b]], float(blk_sign[b]), eps))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Losses and the estimate: Eqs. 3, 5, 6; Alg. 3 query loop
+# ---------------------------------------------------------------------------
+def sq_loss(Y, Ystar):
+    """Squared loss of the Tiny configuration: 0.5 ||Y - Y*||_F^2 / T (T = rows)."""
+    D = np.asarray(Y, np.float64) - np.asarray(Ystar, np.float64)
+    return 0.5 * float(np.sum(D * D)) / D.shape[0]
+
+
+def central_estimate(Lp, Lm, eps):
+    """Central difference (L+ - L-) / (2 eps) per query (the two-point scheme of
+    Eq. 3, applied to every query; READING: the central scheme replaces the
+    forward difference of Eq. 6 / Alg. 3 for this hot path)."""
+    return (np.asarray(Lp, np.float64) - np.asarray(Lm, np.float64)) / (2.0 * eps)
+
+
+def forward_estimate(L, L0, eps):
+    """Forward difference rho_k = (l_k - l_0) / eps (Eq. 6, Alg. 3)."""
+    return (np.asarray(L, np.float64) - float(L0)) / eps
+
+
+def aggregate(g, Zs):
+    """Aggregated low-rank gradient Zbar = (1/K) sum_k rho_k Z^(k) (Sec. 3.1, Alg. 3)."""
+    g = np.asarray(g, np.float64)
+    Zs = np.asarray(Zs, np.float64)
+    acc = np.zeros(Zs.shape[1:], dtype=np.float64)
+    for k in range(len(g)):
+        acc += g[k] * Zs[k]
+    return acc / len(g)
+
+
+# ---------------------------------------------------------------------------
+# Subspace Adam: Eqs. 7-10
+# ---------------------------------------------------------------------------
+def adam_direction(M1, M2, Zbar, t, beta1, beta2, eps_adam):
+    """One step of Adam on the r x r aggregated gradient (Eqs. 7-9).
+
+    READING: t is the 1-based step index (the paper's loop counts from 0,
+    which would divide by zero in the bias correction).  Returns
+    (M1_new, M2_new, S) with S = Mhat / (sqrt(Vhat) + eps_adam), eps_adam
+    outside the square root.
+    """
+    if t < 1:
+        raise ValueError("Adam step index is 1-based")
+    Zbar = np.asarray(Zbar, np.float64)
+    M1n = beta1 * np.asarray(M1, np.float64) + (1.0 - beta1) * Zbar
+    M2n = beta2 * np.asarray(M2, np.float64) + (1.0 - beta2) * (Zbar * Zbar)
+    mhat = M1n / (1.0 - beta1 ** t)
+    vhat = M2n / (1.0 - beta2 ** t)
+    S = mhat / (np.sqrt(vhat) + eps_adam)
+    return M1n, M2n, S
+
+
+def subspace_adam_update(W, U, V, Zs, g, M1, M2, t, lr, beta1, beta2, eps_adam):
+    """Full once-per-step update of one matrix (Alg. 3 tail, Eqs. 7-10).
+
+    Zbar = (1/q) sum_j g_j Z_j; Adam in r x r; W_new = W - lr U S V^T (exact,
+    float64).  READING: the trailing factor of Eq. 10 is the n x r right
+    projection (dimension check), the denominator uses the r x r moment.
+    Returns dict(W=W_new, M1, M2, S, Zbar).
+    """
+    Zbar = aggregate(g, Zs)
+    M1n, M2n, S = adam_direction(M1, M2, Zbar, t, beta1, beta2, eps_adam)
+    Wn = np.asarray(W, np.float64) - lr * (np.asarray(U, np.float64) @ S @ np.asarray(V, np.float64).T)
+    return dict(W=Wn, M1=M1n, M2=M2n, S=S, Zbar=Zbar)
+
+
+# ---------------------------------------------------------------------------
+# bfloat16 storage rounding (format, not method): single rounding from float64
+# ---------------------------------------------------------------------------
+def round_bf16(x):
+    """Round float64 values to the nearest bfloat16 (8 significant bits), ties to even.
+
+    Written from the format definition: x = f 2^e with 0.5 <= |f| < 1; the
+    bf16 quantum at that binade is 2^(e-8); rint() rounds half to even.
+    Overflow/subnormal ranges are not needed for weights and are not handled.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    f, e = np.frexp(x)
+    q = np.ldexp(1.0, e - 8)
+    return np.rint(x / q) * q
+
+
+# ---------------------------------------------------------------------------
+# Tiny configuration end to end (Alg. 3 with the central estimate)
+# ---------------------------------------------------------------------------
+def tiny_run(inputs, omega_fn, z_fn, cfg, g_override=None, f32_state=False):
+    """Alg. 3 on the one-layer Tiny problem, float64.
+
+    inputs: dict(W, X, Ystar) arrays.  omega_fn(t) -> (Omega_U, Omega_V) for a
+    refresh at step t; z_fn(t) -> Z[q, r, r].  g_override(t, g) may replace
+    the estimates (teacher forcing).  Per step t = 0..steps-1: refresh if
+    t mod F == 0; for each query j the losses of W +- eps U Z_j V^T;
+    g_j = (L+ - L-)/(2 eps); Adam update with step index t+1.
+    Returns a list of per-step records.
+    """
+    W = np.asarray(inputs["W"], np.float64)
+    X = np.asarray(inputs["X"], np.float64)
+    Ystar = np.asarray(inputs["Ystar"], np.float64)
+    r, q, eps = cfg["r"], cfg["q"], cfg["eps"]
+    M1 = np.zeros((r, r))
+    M2 = np.zeros((r, r))
+    U = V = None
+    recs = []
+    for t in range(cfg["steps"]):
+        if t % cfg["F"] == 0:
+            ou, ov = omega_fn(t)
+            U, _, _ = haar_qr(ou)
+            V, _, _ = haar_qr(ov)
+        Zs = np.asarray(z_fn(t), np.float64)
+        Lp = np.array([sq_loss(perturbed_linear(X, W, U, V, Zs[j], +1.0, eps), Ystar) for j in range(q)])
+        Lm = np.array([sq_loss(perturbed_linear(X, W, U, V, Zs[j], -1.0, eps), Ystar) for j in range(q)])
+        g = central_estimate(Lp, Lm, eps)
+        if g_override is not None:
+            g = np.asarray(g_override(t, g), np.float64)
+        upd = subspace_adam_update(W, U, V, Zs, g, M1, M2, t + 1, cfg["lr"],
+                                   cfg["beta1"], cfg["beta2"], cfg["eps_adam"])
+        W_before = W
+        W, M1, M2 = upd["W"], upd["M1"], upd["M2"]
+        recs.append(dict(t=t, U=U, V=V, Z=Zs, Lp=Lp, Lm=Lm, g=g, S=upd["S"], Zbar=upd["Zbar"],
+                         W_before=W_before, W=W, M1=M1, M2=M2,
+                         loss=sq_loss(X @ W.T, Ystar)))
+    return recs

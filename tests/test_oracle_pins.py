@@ -1,0 +1,389 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Every test here checks the oracle against something other than itself:
+hand-derived values (tests/golden), closed forms, invariants, library special
+cases (LAPACK QR, Cholesky, Kronecker products, torch.optim.Adam) and exact
+distributions.  No GPU is used.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg
+import scipy.special
+import scipy.stats
+
+import oracle
+import zo_draws as zd
+
+RNG = np.random.default_rng(1234)
+
+
+def _orth(rows, r, seed):
+    Q, _ = np.linalg.qr(np.random.default_rng(seed).standard_normal((rows, r)))
+    return Q
+
+
+# --------------------------------------------------------------------------- QR
+def test_qr_hand_cases(golden_dir):
+    """Eq. 11 / Alg. 1: the sign-corrected thin QR equals the hand-derived unique factor."""
+    cases = json.load(open(os.path.join(golden_dir, "qr_hand.json")))["cases"]
+    for c in cases:
+        U, R, bad = oracle.haar_qr(np.array(c["omega"]))
+        np.testing.assert_allclose(U, np.array(c["Q"]), rtol=0, atol=1e-15, err_msg=c["name"])
+        np.testing.assert_allclose(R, np.array(c["R"]), rtol=0, atol=1e-15, err_msg=c["name"])
+        assert bad == -1
+
+
+@pytest.mark.parametrize("rows,r", [(200, 8), (50, 10), (33, 33), (1000, 64)])
+def test_qr_first_column_closed_form(rows, r):
+    """With diag(R) > 0 the first column is Omega[:,0] / ||Omega[:,0]|| exactly."""
+    Om = RNG.standard_normal((rows, r))
+    U, R, _ = oracle.haar_qr(Om)
+    np.testing.assert_allclose(U[:, 0], Om[:, 0] / np.linalg.norm(Om[:, 0]), rtol=0, atol=1e-14)
+    assert R[0, 0] == pytest.approx(np.linalg.norm(Om[:, 0]), rel=1e-14)
+
+
+@pytest.mark.parametrize("rows,r", [(64, 4), (512, 16), (300, 37), (2048, 64)])
+def test_qr_matches_cholesky_form(rows, r):
+    """Uniqueness: R = chol(Omega^T Omega)^T (positive diagonal) and Q = Omega R^-1."""
+    Om = RNG.standard_normal((rows, r))
+    U, R, _ = oracle.haar_qr(Om)
+    Rc = np.linalg.cholesky(Om.T @ Om).T
+    Qc = scipy.linalg.solve_triangular(Rc, Om.T, trans="T", lower=False).T
+    np.testing.assert_allclose(R, Rc, rtol=0, atol=1e-10 * np.abs(Rc).max())
+    np.testing.assert_allclose(U, Qc, rtol=0, atol=1e-10)
+
+
+@pytest.mark.parametrize("rows,r", [(100, 1), (256, 4), (512, 32), (4096, 64)])
+def test_qr_matches_lapack_with_sign_fix(rows, r):
+    """Library special case: LAPACK's thin QR followed by the column sign fix."""
+    Om = RNG.standard_normal((rows, r))
+    Ql, Rl = np.linalg.qr(Om, mode="reduced")
+    s = np.where(np.diag(Rl) < 0, -1.0, 1.0)
+    U, R, _ = oracle.haar_qr(Om)
+    np.testing.assert_allclose(U, Ql * s, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(R, Rl * s[:, None], rtol=0, atol=1e-12 * np.abs(Rl).max())
+
+
+@pytest.mark.parametrize("rows,r", [(512, 16), (777, 5), (2000, 64)])
+def test_qr_invariants(rows, r):
+    Om = RNG.standard_normal((rows, r))
+    U, R, bad = oracle.haar_qr(Om)
+    assert bad == -1
+    assert np.abs(U.T @ U - np.eye(r)).max() < 1e-13
+    assert np.abs(U @ R - Om).max() < 1e-12 * np.abs(Om).max()
+    assert np.all(np.diag(R) > 0)
+    assert np.abs(np.tril(U.T @ Om, -1)).max() < 1e-12
+
+
+def test_qr_rank_deficient_column_reported():
+    """READING of sgn(0): a zero column gives R_kk = 0, reported as rank-deficient."""
+    Om = RNG.standard_normal((40, 6))
+    Om[:, 3] = 0.0
+    U, R, bad = oracle.haar_qr(Om)
+    assert bad == 3
+    assert R[3, 3] == 0.0
+    # The other columns are still orthonormal and the factorisation still holds.
+    assert np.abs(U @ R - Om).max() < 1e-12
+
+
+def _coord_cdf(m):
+    """Exact CDF of one coordinate of a uniform unit vector in R^m:
+    x^2 ~ Beta(1/2, (m-1)/2) and the distribution is symmetric."""
+    def cdf(x):
+        x = np.asarray(x)
+        return 0.5 + 0.5 * np.sign(x) * scipy.special.betainc(0.5, (m - 1) / 2.0, x * x)
+    return cdf
+
+
+@pytest.mark.parametrize("seed", [0, 42])
+def test_haar_ks_appendix_setup(seed, golden_dir):
+    """Appendix Haar validation (Table 9 setup: m = 50, r = 10, 2000 trials).
+
+    The corrected first column must follow the exact Haar marginal (KS p > 0.05);
+    the uncorrected one (negative control) must be rejected.  Our draws differ
+    from the paper's, so the paper's D values are compared only in size.
+    """
+    g = json.load(open(os.path.join(golden_dir, "paper_haar_ks.json")))
+    m, r, n = g["m"], g["r"], g["trials"]
+    corr = np.empty(n)
+    raw = np.empty(n)
+    corr1 = np.empty(n)
+    for i in range(n):
+        Om = zd.draw(seed, "OMEGA_U", (99999, i), (m, r))
+        U, _, _ = oracle.haar_qr(Om)
+        corr[i] = U[0, 0]
+        corr1[i] = U[1, 0]
+        raw[i] = oracle.raw_qr_first_column(Om)[0]
+    cdf = _coord_cdf(m)
+    kc = scipy.stats.kstest(corr, cdf)
+    kc1 = scipy.stats.kstest(corr1, cdf)
+    kr = scipy.stats.kstest(raw, cdf)
+    assert kc.pvalue > 0.05 and kc1.pvalue > 0.05
+    assert kc.statistic < 2.5 * g["corrected"]["seed0"]["D"]
+    assert kr.pvalue < 1e-3
+    # Coordinate variance of a uniform unit vector is exactly 1/m.
+    var = float(np.mean(corr ** 2))
+    assert abs(var - 1.0 / m) < 4 * math.sqrt(2.0 / n) / m + 1e-12
+    assert g["theory_variance"] == pytest.approx(1.0 / m)
+
+
+# ------------------------------------------------------------- perturbed linear
+def test_perturbed_linear_hand_example():
+    """X = [1, 2], W = I, U = e1, V = e2, Z = 3, eps = 0.5: W+ = [[1, 1.5], [0, 1]], Y = [4, 2]."""
+    X = np.array([[1.0, 2.0]])
+    W = np.eye(2)
+    U = np.array([[1.0], [0.0]])
+    V = np.array([[0.0], [1.0]])
+    Z = np.array([[3.0]])
+    np.testing.assert_array_equal(oracle.perturbed_linear(X, W, U, V, Z, +1.0, 0.5), [[4.0, 2.0]])
+    np.testing.assert_array_equal(oracle.perturbed_linear(X, W, U, V, Z, -1.0, 0.5), [[-2.0, 2.0]])
+
+
+def _pl_case(T=37, m=48, n=64, r=5, seed=7):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((T, n))
+    W = 0.02 * rng.standard_normal((m, n))
+    U = _orth(m, r, seed + 1)
+    V = _orth(n, r, seed + 2)
+    Z = rng.standard_normal((r, r))
+    return X, W, U, V, Z
+
+
+def test_perturbed_linear_special_cases():
+    X, W, U, V, Z = _pl_case()
+    base = np.matmul(X, W.T)
+    np.testing.assert_allclose(oracle.perturbed_linear(X, W, U, V, Z, 1.0, 0.0), base, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(oracle.perturbed_linear(X, W, U, V, 0 * Z, -1.0, 1e-3), base, rtol=0, atol=1e-14)
+
+
+@pytest.mark.parametrize("eps", [1e-3, 1.0])
+def test_perturbed_linear_factored_identity(eps):
+    """X (W + s eps U Z V^T)^T = X W^T + s eps (X V)(U Z)^T (the route that never forms U Z V^T)."""
+    X, W, U, V, Z = _pl_case()
+    for s in (+1.0, -1.0):
+        fact = X @ W.T + s * eps * (X @ V) @ (U @ Z).T
+        np.testing.assert_allclose(oracle.perturbed_linear(X, W, U, V, Z, s, eps), fact, rtol=0, atol=1e-12)
+    yp = oracle.perturbed_linear(X, W, U, V, Z, 1.0, eps)
+    ym = oracle.perturbed_linear(X, W, U, V, Z, -1.0, eps)
+    np.testing.assert_allclose(yp + ym, 2 * X @ W.T, rtol=0, atol=1e-12)
+
+
+def test_lemma1_kronecker_and_norm():
+    """Lemma 1 of SubZero (restated in the Preliminaries): vec(U Z V^T) = (V kron U) vec(Z),
+    and with column-orthonormal U, V the Frobenius norm is preserved."""
+    _, _, U, V, Z = _pl_case(m=20, n=30, r=4)
+    P = oracle.perturbation(U, Z, V)
+    vec = lambda A: A.reshape(-1, order="F")
+    np.testing.assert_allclose(vec(P), np.kron(V, U) @ vec(Z), rtol=0, atol=1e-14)
+    assert np.linalg.norm(P) == pytest.approx(np.linalg.norm(Z), rel=1e-13)
+    K = np.kron(V, U)
+    assert np.abs(K.T @ K - np.eye(16)).max() < 1e-13
+
+
+def test_perturbed_linear_blocks_rows_subset():
+    X, W, U, V, Z = _pl_case(T=20)
+    Zs = np.stack([Z, 2 * Z])
+    Xb = [X, X[::-1].copy(), X, X]
+    full = oracle.perturbed_linear_blocks(Xb, W, U, V, Zs, [0, 0, 1, 1], [1, -1, 1, -1], 1e-2)
+    rows = np.array([0, 5, 19])
+    part = oracle.perturbed_linear_blocks(Xb, W, U, V, Zs, [0, 0, 1, 1], [1, -1, 1, -1], 1e-2, rows=rows)
+    for b in range(4):
+        np.testing.assert_array_equal(part[b], full[b][rows])
+    np.testing.assert_allclose(full[2], X @ (W + 1e-2 * U @ (2 * Z) @ V.T).T, atol=1e-13)
+
+
+# --------------------------------------------------------------- loss, estimate
+def test_sq_loss_hand():
+    assert oracle.sq_loss([[1.0, 2.0]], [[0.0, 0.0]]) == 2.5
+    assert oracle.sq_loss([[1.0], [3.0]], [[0.0], [1.0]]) == pytest.approx(0.5 * (1 + 4) / 2)
+
+
+def _quad_problem(T=64, m=32, n=48, r=4, seed=3):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((T, n))
+    W = 0.02 * rng.standard_normal((m, n))
+    Ys = X @ (W + 0.01 * rng.standard_normal((m, n))).T
+    U = _orth(m, r, seed + 10)
+    V = _orth(n, r, seed + 11)
+    grad = (X @ W.T - Ys).T @ X / T
+    return X, W, Ys, U, V, grad
+
+
+@pytest.mark.parametrize("eps", [1e-3, 1.0, 7.5])
+def test_central_difference_exact_on_quadratic(eps):
+    """On L(W) = 0.5||X W^T - Y*||^2 / T the central difference equals <grad L, U Z V^T>
+    exactly for every eps (the quadratic terms cancel)."""
+    X, W, Ys, U, V, grad = _quad_problem()
+    Z = np.random.default_rng(9).standard_normal((4, 4))
+    Lp = oracle.sq_loss(oracle.perturbed_linear(X, W, U, V, Z, 1.0, eps), Ys)
+    Lm = oracle.sq_loss(oracle.perturbed_linear(X, W, U, V, Z, -1.0, eps), Ys)
+    g = oracle.central_estimate([Lp], [Lm], eps)[0]
+    exact = float(np.sum(grad * (U @ Z @ V.T)))
+    assert g == pytest.approx(exact, rel=2e-9 if eps < 1e-2 else 1e-11, abs=1e-13)
+
+
+def test_estimator_unbiased_monte_carlo():
+    """E_Z[<grad L, U Z V^T> Z] = U^T grad L V (E[z z^T] = I); Monte Carlo with a 4-sigma bound."""
+    X, W, Ys, U, V, grad = _quad_problem()
+    target = U.T @ grad @ V
+    N = 20000
+    rng = np.random.default_rng(5)
+    Zs = rng.standard_normal((N, 4, 4))
+    # Exact central differences on a quadratic equal the directional derivative.
+    g = np.array([np.sum(grad * (U @ Z @ V.T)) for Z in Zs])
+    est = oracle.aggregate(g, Zs)
+    bound = 4 * np.linalg.norm(target) * math.sqrt((16 + 1) / N)
+    assert np.linalg.norm(est - target) < bound
+    # Through the oracle's own loss route on a subset of draws (same expectation).
+    sub = Zs[:200]
+    gl = [oracle.central_estimate([oracle.sq_loss(oracle.perturbed_linear(X, W, U, V, Z, 1, 1e-2), Ys)],
+                                  [oracle.sq_loss(oracle.perturbed_linear(X, W, U, V, Z, -1, 1e-2), Ys)], 1e-2)[0]
+          for Z in sub]
+    np.testing.assert_allclose(gl, g[:200], rtol=1e-8, atol=1e-12)
+
+
+def test_forward_difference_unbiased_on_quadratic():
+    """Eq. 6's forward difference: on a quadratic, E[(L(W+eps D)-L(W))/eps Z] is also U^T grad V
+    (the eps^2 term is even in Z, its product with Z has zero mean)."""
+    X, W, Ys, U, V, grad = _quad_problem(r=2)
+    target = U.T @ grad @ V
+    N = 20000
+    Zs = np.random.default_rng(8).standard_normal((N, 2, 2))
+    eps = 1e-3
+    L0 = oracle.sq_loss(X @ W.T, Ys)
+    XWt = X @ W.T - Ys
+    # Closed-form loss of the perturbed weight keeps this fast: L(W+eps D) = 0.5||R + eps X D^T||^2/T.
+    XV = X @ V
+    Ls = np.array([0.5 * np.sum((XWt + eps * XV @ (U @ Z).T) ** 2) / X.shape[0] for Z in Zs[:2000]])
+    Lchk = np.array([oracle.sq_loss(oracle.perturbed_linear(X, W, U, V, Z, 1, eps), Ys) for Z in Zs[:20]])
+    np.testing.assert_allclose(Ls[:20], Lchk, rtol=1e-13)
+    rho = oracle.forward_estimate(Ls, L0, eps)
+    est = oracle.aggregate(rho, Zs[:2000])
+    assert np.linalg.norm(est - target) < 4 * np.linalg.norm(target) * math.sqrt(5 / 2000) + 1e-6
+
+
+def test_aggregate_one_hot_and_linearity():
+    Zs = RNG.standard_normal((5, 3, 3))
+    np.testing.assert_allclose(oracle.aggregate([0, 0, 5.0, 0, 0], Zs), Zs[2], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(oracle.aggregate(np.ones(5), Zs), Zs.mean(0), rtol=0, atol=1e-15)
+
+
+# ------------------------------------------------------------------------- Adam
+def test_adam_first_step_closed_form():
+    """Step 1: Mhat = Zbar, Vhat = Zbar^2, so S = Zbar / (|Zbar| + eps_adam) whatever the betas."""
+    Zb = RNG.standard_normal((6, 6))
+    for b1, b2 in [(0.9, 0.999), (0.9, 0.95), (0.0, 0.0), (0.5, 0.3)]:
+        _, _, S = oracle.adam_direction(np.zeros((6, 6)), np.zeros((6, 6)), Zb, 1, b1, b2, 1e-8)
+        np.testing.assert_allclose(S, Zb / (np.abs(Zb) + 1e-8), rtol=1e-14, atol=0)
+
+
+def test_adam_zero_betas_every_step():
+    M1 = RNG.standard_normal((4, 4))
+    M2 = RNG.random((4, 4))
+    Zb = RNG.standard_normal((4, 4))
+    for t in (1, 2, 17):
+        _, _, S = oracle.adam_direction(M1, M2, Zb, t, 0.0, 0.0, 1e-8)
+        np.testing.assert_allclose(S, Zb / (np.abs(Zb) + 1e-8), rtol=1e-14)
+
+
+def test_adam_step_index_is_one_based():
+    with pytest.raises(ValueError):
+        oracle.adam_direction(np.zeros((2, 2)), np.zeros((2, 2)), np.ones((2, 2)), 0, 0.9, 0.95, 1e-8)
+
+
+def test_adam_matches_torch_optim():
+    """Library special case: torch.optim.Adam on an r x r parameter with gradient Zbar_t moves the
+    parameter by exactly -lr * S_t each step (Eqs. 7-10 are Adam in the r x r space)."""
+    torch = pytest.importorskip("torch")
+    r, lr, b1, b2, ea = 5, 1e-2, 0.9, 0.95, 1e-8
+    p = torch.zeros((r, r), dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([p], lr=lr, betas=(b1, b2), eps=ea)
+    M1 = np.zeros((r, r))
+    M2 = np.zeros((r, r))
+    rng = np.random.default_rng(11)
+    for t in range(1, 8):
+        Zb = rng.standard_normal((r, r)) * (10.0 ** rng.integers(-3, 2))
+        before = p.detach().clone().numpy()
+        p.grad = torch.from_numpy(Zb.copy())
+        opt.step()
+        M1, M2, S = oracle.adam_direction(M1, M2, Zb, t, b1, b2, ea)
+        np.testing.assert_allclose(p.detach().numpy() - before, -lr * S, rtol=1e-9, atol=1e-15)
+
+
+def test_update_invariants():
+    """U^T (W_new - W_old) V = -lr S and rank(W_new - W_old) <= r."""
+    m, n, r, q = 40, 56, 4, 3
+    U, V = _orth(m, r, 1), _orth(n, r, 2)
+    W = 0.02 * RNG.standard_normal((m, n))
+    Zs = RNG.standard_normal((q, r, r))
+    g = RNG.standard_normal(q)
+    out = oracle.subspace_adam_update(W, U, V, Zs, g, np.zeros((r, r)), np.zeros((r, r)), 1, 1e-2, 0.9, 0.95, 1e-8)
+    D = out["W"] - W
+    np.testing.assert_allclose(U.T @ D @ V, -1e-2 * out["S"], rtol=0, atol=1e-15)
+    assert np.linalg.matrix_rank(D, tol=1e-12) <= r
+    np.testing.assert_allclose(out["Zbar"], np.tensordot(g, Zs, 1) / q, rtol=1e-14)
+
+
+def test_zero_estimates_leave_w_unchanged():
+    m, n, r, q = 16, 24, 3, 4
+    U, V = _orth(m, r, 3), _orth(n, r, 4)
+    W = RNG.standard_normal((m, n))
+    out = oracle.subspace_adam_update(W, U, V, RNG.standard_normal((q, r, r)), np.zeros(q),
+                                      np.zeros((r, r)), np.zeros((r, r)), 1, 1e-2, 0.9, 0.95, 1e-8)
+    np.testing.assert_array_equal(out["W"], W)
+
+
+# ------------------------------------------------------------------ bf16 format
+def test_round_bf16_hand_cases(golden_dir):
+    cases = json.load(open(os.path.join(golden_dir, "bf16_rounding.json")))["cases"]
+    for c in cases:
+        assert oracle.round_bf16(c["x_value"]) == c["bf16"], c["x"]
+
+
+def test_round_bf16_matches_torch_on_fp32_inputs():
+    """For float32-representable inputs one rounding to bf16 is torch's float32->bfloat16 cast."""
+    torch = pytest.importorskip("torch")
+    x32 = (RNG.standard_normal(200000) * 10.0 ** RNG.uniform(-6, 3, 200000)).astype(np.float32)
+    ref = torch.from_numpy(x32).to(torch.bfloat16).to(torch.float32).numpy().astype(np.float64)
+    np.testing.assert_array_equal(oracle.round_bf16(x32.astype(np.float64)), ref)
+
+
+def test_fp32_in_place_restore_is_not_exact():
+    """Alg. 2 adds then subtracts eps U Z V^T in place; in float32 that does not give W back
+    bit for bit (why the GPU path never writes W during the queries)."""
+    m, n, r = 256, 512, 4
+    W = zd.f32(zd.draw(0, "W0", (0,), (m, n), 0.02))
+    U, V = _orth(m, r, 5).astype(np.float32), _orth(n, r, 6).astype(np.float32)
+    D = (1e-3 * (U @ RNG.standard_normal((r, r)).astype(np.float32) @ V.T)).astype(np.float32)
+    back = (W + D) - D
+    assert np.count_nonzero(back != W) > 0
+
+
+# ------------------------------------------------------------------------ Tiny
+def test_tiny_loop_teacher_forced_zero_is_identity():
+    c = dict(zd.TINY, steps=3)
+    inp = zd.tiny_inputs(0)
+    recs = oracle.tiny_run(inp, lambda t: zd.omega_pair(0, t, 0, c["m"], c["n"], c["r"]),
+                           lambda t: zd.z_draws(0, t, 0, c["q"], c["r"]), c,
+                           g_override=lambda t, g: np.zeros_like(g))
+    np.testing.assert_array_equal(recs[-1]["W"], inp["W"].astype(np.float64))
+
+
+def test_tiny_loop_decreases_loss():
+    c = zd.TINY
+    inp = zd.tiny_inputs(0)
+    recs = oracle.tiny_run(inp, lambda t: zd.omega_pair(0, t, 0, c["m"], c["n"], c["r"]),
+                           lambda t: zd.z_draws(0, t, 0, c["q"], c["r"]), c)
+    L0 = oracle.sq_loss(inp["X"].astype(np.float64) @ inp["W"].astype(np.float64).T, inp["Ystar"])
+    assert recs[-1]["loss"] < L0
+    # The g's are exact directional derivatives of a quadratic (checked above), so each g_j equals
+    # <grad L(W_t), U Z_j V^T> up to the float64 cancellation of the difference.
+    rec = recs[7]
+    X = inp["X"].astype(np.float64)
+    grad = (X @ rec["W_before"].T - inp["Ystar"]).T @ X / X.shape[0]
+    exact = [np.sum(grad * (rec["U"] @ Z @ rec["V"].T)) for Z in rec["Z"]]
+    np.testing.assert_allclose(rec["g"], exact, rtol=1e-6, atol=1e-9)
