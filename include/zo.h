@@ -1,0 +1,212 @@
+/*
+ * zo.h -- C ABI of the SubZero+ hot path on AMD Instinct MI355X (gfx950).
+ *
+ * SubZero+ (arXiv 2608.15665) fine-tunes every weight matrix W_i (m x n, the
+ * out x in layout of a linear layer) with zeroth-order estimates taken inside
+ * a rank-r subspace spanned by column-orthonormal U_i (m x r) and V_i (n x r).
+ * Three operations dominate its cost and are exported here:
+ *
+ *   zo_subspace_refresh      Haar-distributed U, V: thin QR of Gaussian panels
+ *                            with column signs fixed so diag(R) > 0
+ *                            (Eq. 11, Alg. 1).
+ *   zo_perturbed_linear      the linear layer under the query perturbations
+ *                            W +- eps U Z_j V^T (Eq. 4, Alg. 2, the forward of
+ *                            Eq. 5) without forming the perturbed weight.
+ *   zo_subspace_adam_update  aggregate the per-query estimates, run Adam on the
+ *                            r x r state and apply W <- W - lr U S V^T
+ *                            (Eqs. 6-10, tail of Alg. 3).
+ *
+ * plus two small helpers for a squared-error loss and the central difference.
+ *
+ * Conventions (all entry points)
+ *   - Every tensor argument is DEVICE memory owned by the caller; the library
+ *     allocates nothing.  Scratch space comes from the caller's `workspace`
+ *     (device memory, 256-byte aligned, size from the matching *_workspace()
+ *     query).  Descriptor arrays (zo_panel, zo_update_item, blk_query,
+ *     blk_sign) are HOST memory read during the call only.
+ *   - Matrices are row-major and dense (leading dimension = number of
+ *     columns).  bf16 tensors hold IEEE bfloat16 bit patterns (uint16_t).
+ *     bf16 tensors must be 16-byte aligned; fp32 tensors 4-byte aligned.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default
+ *     stream).  No call synchronises; results are ready when the stream is.
+ *   - Return value: a zo_status.  Argument errors are detected on the host
+ *     before anything is enqueued; the call then returns ZO_ERR_INVALID_ARG /
+ *     ZO_ERR_UNSUPPORTED / ZO_ERR_WORKSPACE, launches nothing, and
+ *     zo_last_error_detail() (thread-local) says what was wrong.  A failed
+ *     launch returns ZO_ERR_HIP.
+ *   - Results are deterministic: no atomics take part in any reduction.
+ */
+#ifndef ZO_H
+#define ZO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ZO_ABI_VERSION 1
+#define ZO_MAX_RANK 128   /* r limit of zo_perturbed_linear and the update   */
+#define ZO_MAX_QR_RANK 64 /* r limit of zo_subspace_refresh                  */
+#define ZO_MAX_BLOCKS 256 /* nblk limit of zo_perturbed_linear               */
+#define ZO_MAX_QUERIES 256
+
+typedef enum {
+  ZO_OK = 0,
+  ZO_ERR_INVALID_ARG = 1,
+  ZO_ERR_UNSUPPORTED = 2,
+  ZO_ERR_RANK_DEFICIENT = 3,
+  ZO_ERR_NONFINITE = 4,
+  ZO_ERR_HIP = 5,
+  ZO_ERR_WORKSPACE = 6
+} zo_status;
+
+typedef enum { ZO_F32 = 0, ZO_BF16 = 1 } zo_dtype;
+
+int zo_abi_version(void);
+const char* zo_status_str(int status);
+/* Text of the last error raised on the calling thread ("" if none). */
+const char* zo_last_error_detail(void);
+
+/* ------------------------------------------------------------------------
+ * Subspace refresh -- Eq. 11 and Alg. 1 (HaarProjMatrix).
+ *
+ * For each panel p (rows_p x r, rows_p >= r): Omega_p = Q_p R_p with
+ * Q_p^T Q_p = I and R_p upper triangular with a POSITIVE diagonal, i.e. the
+ * Q of any thin QR with each column multiplied by the sign of the matching
+ * R diagonal entry.  This factor is unique, and for Gaussian Omega it is
+ * Haar distributed.  Computed by Householder reflections in float64 (tall
+ * panels as a tree of row blocks); outputs rounded once to float32.
+ *
+ *   omega   device, rows x r fp32, row-major; read only.
+ *   q       device, rows x r fp32 output; may alias omega.
+ *   r_diag  device, r fp32 output (diag of the corrected R, > 0); nullable.
+ *   info    device, `count` ints, nullable: info[p] = 0, or k+1 when the
+ *           first zero diagonal entry of R_p is at column k (Omega_p rank
+ *           deficient).  Such a column gets sign +1 (sgn(0) := +1); its Q
+ *           column is not meaningful.
+ * Limits: 1 <= r <= ZO_MAX_QR_RANK, rows <= 2^26.  Panels of one call share
+ * r; rows may differ.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int rows;
+  const float* omega;
+  float* q;
+  float* r_diag;
+} zo_panel;
+
+size_t zo_subspace_refresh_workspace(int count, const zo_panel* panels, int r);
+int zo_subspace_refresh(int count, const zo_panel* panels, int r, int* info,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Perturbed linear -- Eq. 4 inside the forward of Eq. 5 (Alg. 2 + Alg. 3).
+ *
+ * For every block b = 0..nblk-1 (one query j = blk_query[b] with sign
+ * s = blk_sign[b] in {+1, -1, 0}):
+ *
+ *     Y_b = X_b (W + s eps U Z_j V^T)^T
+ *         = X_b W^T + (X_b V) (s eps U Z_j)^T
+ *
+ * computed in the second form: W is only read (bitwise unchanged), the
+ * m x n perturbed weight is never formed.
+ *
+ *   T            rows (tokens) per block; m, n: W is m x n (out x in).
+ *   X            device, block b starts at X + b * x_block_stride elements,
+ *                each block T x n.  x_block_stride = 0: all blocks share one
+ *                X (the first layer of a network); otherwise >= T*n.
+ *   W            device, m x n.  in_dtype ZO_BF16 or ZO_F32 for X and W.
+ *   U, V         device fp32, m x r and n x r (column-orthonormal).
+ *   Z            device fp32, q x r x r (Z_j row-major).
+ *   blk_query    host, nblk ints in [0, q).
+ *   blk_sign     host, nblk int8 in {+1, -1, 0}.
+ *   Y            device, nblk blocks of T x m, contiguous; out_dtype ZO_BF16
+ *                or ZO_F32 (fp32 inputs require fp32 output).
+ * Arithmetic: bf16 inputs use bf16 MFMA with fp32 accumulation; the rank-r
+ * term uses bf16 operands (X_b V and s eps U Z_j rounded to bf16) added into
+ * the same accumulator; outputs rounded to nearest even.  fp32 inputs use
+ * fp32 FMA throughout.
+ * Limits: 1 <= r <= ZO_MAX_RANK, 1 <= q <= ZO_MAX_QUERIES, 1 <= nblk <=
+ * ZO_MAX_BLOCKS; bf16 inputs need m % 8 == 0 and n % 8 == 0.
+ * ------------------------------------------------------------------------ */
+size_t zo_perturbed_linear_workspace(int T, int m, int n, int r, int q, int nblk,
+                                     long long x_block_stride, int in_dtype);
+int zo_perturbed_linear(int T, int m, int n, int r, int q, int nblk,
+                        const int* blk_query, const int8_t* blk_sign, float eps,
+                        int in_dtype, const void* X, long long x_block_stride,
+                        const void* W, const float* U, const float* V,
+                        const float* Z, int out_dtype, void* Y,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Subspace Adam update -- Eqs. 6-10 and the tail of Alg. 3.
+ *
+ * With q global estimates g_j (shared by every matrix, e.g. the central
+ * differences (L+_j - L-_j) / (2 eps)), for each item:
+ *
+ *     Zbar = (1/q) sum_j g_j Z_j                          (r x r)
+ *     M1  <- beta1 M1 + (1 - beta1) Zbar                  (Eq. 7)
+ *     M2  <- beta2 M2 + (1 - beta2) Zbar * Zbar           (Eq. 8)
+ *     S    = (M1 / (1 - beta1^t)) / (sqrt(M2 / (1 - beta2^t)) + eps_adam)
+ *     W   <- W - lr U S V^T                               (Eq. 10)
+ *
+ * t >= 1 is the 1-based Adam step.  The r x r work is float64 inside; the
+ * moments are stored fp32.  The m x n product is accumulated in fp32
+ * (bf16 W: MFMA on a hi+lo bf16 split of lr U S and V; fp32 W: fp32 FMA),
+ * added to W in fp32 and rounded to nearest even when W is bf16.
+ *
+ *   W          device m x n (w_dtype), updated in place.
+ *   U, V, Z    device fp32: m x r, n x r, q x r x r.
+ *   M1, M2     device fp32 r x r, updated in place.
+ *   zbar_out   device fp32 r x r, nullable: Zbar.
+ *   w_f32_out  device fp32 m x n, nullable: the new W before its storage
+ *              rounding (a check hook).
+ *   g          device fp32, q values.
+ *   nonfinite_flag  device int, nullable.  If Zbar or S of an item has a
+ *              non-finite entry, that item's W, M1 and M2 are left untouched
+ *              and *nonfinite_flag is set to 1 (never cleared here).
+ * Limits: 1 <= r <= ZO_MAX_RANK, 1 <= q <= ZO_MAX_QUERIES; bf16 W needs
+ * n % 8 == 0.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int m, n;
+  void* W;
+  const float* U;
+  const float* V;
+  const float* Z;
+  float* M1;
+  float* M2;
+  float* zbar_out;
+  float* w_f32_out;
+} zo_update_item;
+
+size_t zo_subspace_adam_update_workspace(int count, const zo_update_item* items,
+                                         int r, int q, int w_dtype);
+int zo_subspace_adam_update(int count, const zo_update_item* items, int w_dtype,
+                            int r, int q, const float* g, int t, float lr,
+                            float beta1, float beta2, float eps_adam,
+                            int* nonfinite_flag, void* workspace,
+                            size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Squared-error loss per block (the loss of a one-layer regression model):
+ * out[b] = 0.5 * sum((Y_b - Ystar)^2) / T, float64 accumulation in a fixed
+ * order.  Y: nblk blocks of T x m (dtype), Ystar: T x m (same dtype), out:
+ * device float64 [nblk].
+ * ------------------------------------------------------------------------ */
+size_t zo_sq_loss_workspace(int nblk, int T, int m);
+int zo_sq_loss(int nblk, int T, int m, int dtype, const void* Y,
+               const void* Ystar, double* out, void* workspace,
+               size_t ws_bytes, void* stream);
+
+/* Central difference of Eq. 3 for every query:
+ * g[j] = (L[2j] - L[2j+1]) / (2 eps), L device float64 [2q] (block 2j is the
+ * + perturbation, 2j+1 the - one), g device fp32 [q]; float64 arithmetic. */
+int zo_combine_central(int q, const double* L, float eps, float* g,
+                       void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ZO_H */

@@ -1,0 +1,296 @@
+"""ctypes binding of libzo (the C ABI declared in include/zo.h).
+
+Argument marshalling only: every computation runs in the library's HIP
+kernels.  Tensors are torch tensors on the GPU (PyTorch provides device
+memory and the current stream); they are checked for device, dtype and
+contiguity and handed over as raw pointers.  There is no CPU fallback: if
+libzo.so is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional, Sequence
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libzo.so")
+
+ZO_F32, ZO_BF16 = 0, 1
+ZO_MAX_RANK = 128
+ZO_MAX_QR_RANK = 64
+ZO_MAX_BLOCKS = 256
+STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "rank deficient",
+          4: "non-finite value", 5: "HIP runtime error", 6: "workspace too small"}
+
+ABI_SYMBOLS = (
+    "zo_abi_version", "zo_status_str", "zo_last_error_detail",
+    "zo_subspace_refresh_workspace", "zo_subspace_refresh",
+    "zo_perturbed_linear_workspace", "zo_perturbed_linear",
+    "zo_subspace_adam_update_workspace", "zo_subspace_adam_update",
+    "zo_sq_loss_workspace", "zo_sq_loss", "zo_combine_central",
+)
+
+
+class ZoError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"libzo: {STATUS.get(status, status)}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+class Panel(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int), ("omega", ctypes.c_void_p),
+                ("q", ctypes.c_void_p), ("r_diag", ctypes.c_void_p)]
+
+
+class UpdateItem(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int), ("n", ctypes.c_int), ("W", ctypes.c_void_p),
+                ("U", ctypes.c_void_p), ("V", ctypes.c_void_p), ("Z", ctypes.c_void_p),
+                ("M1", ctypes.c_void_p), ("M2", ctypes.c_void_p),
+                ("zbar_out", ctypes.c_void_p), ("w_f32_out", ctypes.c_void_p)]
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libzo.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                                   "`python -m paper_2608_15665_amd._build` (or __graft_entry__.build())")
+            L = ctypes.CDLL(LIB_PATH)
+            c_int, c_vp, c_sz, c_f, c_ll = (ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
+                                           ctypes.c_float, ctypes.c_longlong)
+            L.zo_abi_version.restype = c_int
+            L.zo_status_str.restype = ctypes.c_char_p
+            L.zo_status_str.argtypes = [c_int]
+            L.zo_last_error_detail.restype = ctypes.c_char_p
+            L.zo_subspace_refresh_workspace.restype = c_sz
+            L.zo_subspace_refresh_workspace.argtypes = [c_int, ctypes.POINTER(Panel), c_int]
+            L.zo_subspace_refresh.restype = c_int
+            L.zo_subspace_refresh.argtypes = [c_int, ctypes.POINTER(Panel), c_int, c_vp, c_vp, c_sz, c_vp]
+            L.zo_perturbed_linear_workspace.restype = c_sz
+            L.zo_perturbed_linear_workspace.argtypes = [c_int] * 6 + [c_ll, c_int]
+            L.zo_perturbed_linear.restype = c_int
+            L.zo_perturbed_linear.argtypes = ([c_int] * 6 + [ctypes.POINTER(ctypes.c_int),
+                                               ctypes.POINTER(ctypes.c_int8), c_f, c_int, c_vp, c_ll,
+                                               c_vp, c_vp, c_vp, c_vp, c_int, c_vp, c_vp, c_sz, c_vp])
+            L.zo_subspace_adam_update_workspace.restype = c_sz
+            L.zo_subspace_adam_update_workspace.argtypes = [c_int, ctypes.POINTER(UpdateItem), c_int,
+                                                            c_int, c_int]
+            L.zo_subspace_adam_update.restype = c_int
+            L.zo_subspace_adam_update.argtypes = [c_int, ctypes.POINTER(UpdateItem), c_int, c_int, c_int,
+                                                  c_vp, c_int, c_f, c_f, c_f, c_f, c_vp, c_vp, c_sz, c_vp]
+            L.zo_sq_loss_workspace.restype = c_sz
+            L.zo_sq_loss_workspace.argtypes = [c_int, c_int, c_int]
+            L.zo_sq_loss.restype = c_int
+            L.zo_sq_loss.argtypes = [c_int, c_int, c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+            L.zo_combine_central.restype = c_int
+            L.zo_combine_central.argtypes = [c_int, c_vp, c_f, c_vp, c_vp]
+            _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise ZoError(status, lib().zo_last_error_detail().decode())
+
+
+def _stream_handle() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, numel=None) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on the GPU (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must hold {numel} elements (got {t.numel()})")
+    return t
+
+
+_DT = {torch.float32: ZO_F32, torch.bfloat16: ZO_BF16}
+
+
+class Workspace:
+    """Grow-only device scratch buffer, one per (device, stream).
+
+    Calls enqueued on one stream run in order, so reusing one buffer between
+    them is safe; calls on different streams get different buffers.
+    """
+    _bufs: dict = {}
+
+    @classmethod
+    def get(cls, nbytes: int) -> torch.Tensor:
+        dev = torch.cuda.current_device()
+        key = (dev, _stream_handle())
+        buf = cls._bufs.get(key)
+        if buf is None or buf.numel() < nbytes:
+            buf = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=f"cuda:{dev}")
+            cls._bufs[key] = buf
+        return buf
+
+    @classmethod
+    def clear(cls):
+        cls._bufs.clear()
+
+
+# ---------------------------------------------------------------------------
+def abi_version() -> int:
+    return lib().zo_abi_version()
+
+
+def subspace_refresh(omegas: Sequence[torch.Tensor], r: int, out: Optional[Sequence[torch.Tensor]] = None,
+                     r_diag: Optional[Sequence[torch.Tensor]] = None, info: Optional[torch.Tensor] = None):
+    """Haar factors Q_p of the Gaussian panels Omega_p (rows_p x r, fp32).  See zo_subspace_refresh."""
+    n = len(omegas)
+    if out is None:
+        out = [torch.empty_like(o) for o in omegas]
+    arr = (Panel * max(n, 1))()
+    for p, om in enumerate(omegas):
+        _need(om, f"omega[{p}]", torch.float32)
+        if om.dim() != 2 or om.shape[1] != r:
+            raise ValueError(f"omega[{p}] must be rows x {r}")
+        _need(out[p], f"out[{p}]", torch.float32, om.numel())
+        rd = None
+        if r_diag is not None:
+            rd = _need(r_diag[p], f"r_diag[{p}]", torch.float32, r)
+        arr[p] = Panel(int(om.shape[0]), om.data_ptr(), out[p].data_ptr(), _ptr(rd))
+    if info is not None:
+        _need(info, "info", torch.int32, n)
+    L = lib()
+    ws_n = L.zo_subspace_refresh_workspace(n, arr, r)
+    if ws_n == 0 and n > 0:
+        _check(L.zo_subspace_refresh(n, arr, r, None, None, 0, None))  # raises with the reason
+    ws = Workspace.get(ws_n)
+    _check(L.zo_subspace_refresh(n, arr, r, _ptr(info), ws.data_ptr(), ws.numel(), _stream_handle()))
+    return out
+
+
+def perturbed_linear(X: torch.Tensor, W: torch.Tensor, U: torch.Tensor, V: torch.Tensor, Z: torch.Tensor,
+                     blk_query: Sequence[int], blk_sign: Sequence[int], eps: float, T: int,
+                     x_block_stride: Optional[int] = None, out_dtype=None, Y: Optional[torch.Tensor] = None):
+    """Y_b = X_b (W + s_b eps U Z_{j(b)} V^T)^T for every block b.  See zo_perturbed_linear.
+
+    X holds the stacked blocks (nblk*T x n), or a single T x n block shared by
+    all blocks (x_block_stride = 0).  Returns Y (nblk*T x m).
+    """
+    nblk = len(blk_query)
+    if len(blk_sign) != nblk:
+        raise ValueError("blk_query and blk_sign differ in length")
+    m, n = W.shape
+    r = U.shape[1]
+    q = Z.shape[0]
+    dt = W.dtype
+    if dt not in _DT:
+        raise TypeError(f"unsupported dtype {dt}")
+    _need(W, "W", dt)
+    _need(X, "X", dt)
+    if x_block_stride is None:
+        x_block_stride = 0 if X.numel() == T * n else T * n
+    if X.numel() < (T * n if x_block_stride == 0 else x_block_stride * (nblk - 1) + T * n):
+        raise ValueError("X is too small for the block layout")
+    _need(U, "U", torch.float32, m * r)
+    _need(V, "V", torch.float32, n * r)
+    _need(Z, "Z", torch.float32, q * r * r)
+    out_dtype = dt if out_dtype is None else out_dtype
+    if Y is None:
+        Y = torch.empty((nblk * T, m), dtype=out_dtype, device=W.device)
+    _need(Y, "Y", out_dtype, nblk * T * m)
+    bq = (ctypes.c_int * nblk)(*[int(v) for v in blk_query])
+    bs = (ctypes.c_int8 * nblk)(*[int(v) for v in blk_sign])
+    L = lib()
+    ws_n = L.zo_perturbed_linear_workspace(T, m, n, r, q, nblk, x_block_stride, _DT[dt])
+    ws = Workspace.get(ws_n)
+    _check(L.zo_perturbed_linear(T, m, n, r, q, nblk, bq, bs, float(eps), _DT[dt], X.data_ptr(),
+                                 x_block_stride, W.data_ptr(), U.data_ptr(), V.data_ptr(), Z.data_ptr(),
+                                 _DT[out_dtype], Y.data_ptr(), ws.data_ptr(), ws.numel(), _stream_handle()))
+    return Y
+
+
+def subspace_adam_update(items: Sequence[dict], g: torch.Tensor, t: int, lr: float, beta1: float,
+                         beta2: float, eps_adam: float, nonfinite_flag: Optional[torch.Tensor] = None):
+    """Subspace Adam step for every item (dict with W, U, V, Z, M1, M2 and optional
+    zbar_out, w_f32_out).  See zo_subspace_adam_update."""
+    n = len(items)
+    if n == 0:
+        return
+    dt = items[0]["W"].dtype
+    if dt not in _DT:
+        raise TypeError(f"unsupported dtype {dt}")
+    r = items[0]["U"].shape[1]
+    q = items[0]["Z"].shape[0]
+    _need(g, "g", torch.float32, q)
+    arr = (UpdateItem * n)()
+    for i, it in enumerate(items):
+        W = _need(it["W"], f"W[{i}]", dt)
+        m, nn = W.shape
+        _need(it["U"], f"U[{i}]", torch.float32, m * r)
+        _need(it["V"], f"V[{i}]", torch.float32, nn * r)
+        _need(it["Z"], f"Z[{i}]", torch.float32, q * r * r)
+        _need(it["M1"], f"M1[{i}]", torch.float32, r * r)
+        _need(it["M2"], f"M2[{i}]", torch.float32, r * r)
+        zb = it.get("zbar_out")
+        wo = it.get("w_f32_out")
+        if zb is not None:
+            _need(zb, f"zbar_out[{i}]", torch.float32, r * r)
+        if wo is not None:
+            _need(wo, f"w_f32_out[{i}]", torch.float32, m * nn)
+        arr[i] = UpdateItem(m, nn, W.data_ptr(), it["U"].data_ptr(), it["V"].data_ptr(), it["Z"].data_ptr(),
+                            it["M1"].data_ptr(), it["M2"].data_ptr(), _ptr(zb), _ptr(wo))
+    if nonfinite_flag is not None:
+        _need(nonfinite_flag, "nonfinite_flag", torch.int32, 1)
+    L = lib()
+    ws_n = L.zo_subspace_adam_update_workspace(n, arr, r, q, _DT[dt])
+    if ws_n == 0:
+        _check(L.zo_subspace_adam_update(n, arr, _DT[dt], r, q, g.data_ptr(), t, lr, beta1, beta2,
+                                         eps_adam, None, None, 0, None))
+    ws = Workspace.get(ws_n)
+    _check(L.zo_subspace_adam_update(n, arr, _DT[dt], r, q, g.data_ptr(), int(t), float(lr), float(beta1),
+                                     float(beta2), float(eps_adam), _ptr(nonfinite_flag), ws.data_ptr(),
+                                     ws.numel(), _stream_handle()))
+
+
+def sq_loss(Y: torch.Tensor, Ystar: torch.Tensor, nblk: int, T: int, out: Optional[torch.Tensor] = None):
+    """Per-block 0.5 ||Y_b - Y*||^2 / T as a float64 device tensor [nblk]."""
+    dt = Y.dtype
+    m = Ystar.shape[-1]
+    _need(Y, "Y", dt, nblk * T * m)
+    _need(Ystar, "Ystar", dt, T * m)
+    if out is None:
+        out = torch.empty(nblk, dtype=torch.float64, device=Y.device)
+    _need(out, "out", torch.float64, nblk)
+    L = lib()
+    ws = Workspace.get(L.zo_sq_loss_workspace(nblk, T, m))
+    _check(L.zo_sq_loss(nblk, T, m, _DT[dt], Y.data_ptr(), Ystar.data_ptr(), out.data_ptr(),
+                        ws.data_ptr(), ws.numel(), _stream_handle()))
+    return out
+
+
+def combine_central(Lpm: torch.Tensor, eps: float, out: Optional[torch.Tensor] = None):
+    """g_j = (L[2j] - L[2j+1]) / (2 eps) as float32 [q]."""
+    _need(Lpm, "L", torch.float64)
+    q = Lpm.numel() // 2
+    if out is None:
+        out = torch.empty(q, dtype=torch.float32, device=Lpm.device)
+    _need(out, "g", torch.float32, q)
+    _check(lib().zo_combine_central(q, Lpm.data_ptr(), float(eps), out.data_ptr(), _stream_handle()))
+    return out

@@ -1,0 +1,262 @@
+// C ABI of libzo: argument validation on the host, then the launchers.
+// Nothing here allocates device memory or synchronises the stream.
+#include "zo_internal.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+namespace {
+thread_local char g_detail[512] = "";
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+#define ZO_CHECK(cond, ...)           \
+  do {                                \
+    if (!(cond)) {                    \
+      zo_set_error(__VA_ARGS__);      \
+      return ZO_ERR_INVALID_ARG;      \
+    }                                 \
+  } while (0)
+
+}  // namespace
+
+void zo_set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_detail, sizeof(g_detail), fmt, ap);
+  va_end(ap);
+}
+
+int zo_hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ZO_OK;
+  zo_set_error("%s: %s", what, hipGetErrorString(e));
+  return ZO_ERR_HIP;
+}
+
+extern "C" {
+
+int zo_abi_version(void) { return ZO_ABI_VERSION; }
+
+const char* zo_status_str(int s) {
+  switch (s) {
+    case ZO_OK: return "ok";
+    case ZO_ERR_INVALID_ARG: return "invalid argument";
+    case ZO_ERR_UNSUPPORTED: return "unsupported";
+    case ZO_ERR_RANK_DEFICIENT: return "rank deficient";
+    case ZO_ERR_NONFINITE: return "non-finite value";
+    case ZO_ERR_HIP: return "HIP runtime error";
+    case ZO_ERR_WORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+const char* zo_last_error_detail(void) { return g_detail; }
+
+// ------------------------------------------------------------------ refresh
+static int check_refresh(int count, const zo_panel* panels, int r) {
+  ZO_CHECK(count >= 0, "refresh: count = %d < 0", count);
+  ZO_CHECK(count == 0 || panels, "refresh: panels is NULL");
+  if (r > ZO_MAX_QR_RANK && r <= ZO_MAX_RANK) {
+    zo_set_error("refresh: r = %d above the QR limit %d", r, ZO_MAX_QR_RANK);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  ZO_CHECK(r >= 1 && r <= ZO_MAX_QR_RANK, "refresh: r = %d outside [1, %d]", r, ZO_MAX_QR_RANK);
+  for (int p = 0; p < count; ++p) {
+    const zo_panel& pn = panels[p];
+    ZO_CHECK(pn.rows >= r, "refresh: panel %d has rows = %d < r = %d", p, pn.rows, r);
+    ZO_CHECK(pn.rows <= (1 << 26), "refresh: panel %d rows = %d too large", p, pn.rows);
+    ZO_CHECK(pn.omega && pn.q, "refresh: panel %d has a NULL omega or q", p);
+    ZO_CHECK(aligned(pn.omega, 4) && aligned(pn.q, 4) && aligned(pn.r_diag, 4),
+             "refresh: panel %d pointer not 4-byte aligned", p);
+  }
+  return ZO_OK;
+}
+
+size_t zo_subspace_refresh_workspace(int count, const zo_panel* panels, int r) {
+  if (check_refresh(count, panels, r) != ZO_OK) return 0;
+  size_t need = 0;
+  zo_refresh_launch(count, panels, r, nullptr, nullptr, 0, nullptr, &need);
+  return need;
+}
+
+int zo_subspace_refresh(int count, const zo_panel* panels, int r, int* info, void* workspace,
+                        size_t ws_bytes, void* stream) {
+  int st = check_refresh(count, panels, r);
+  if (st != ZO_OK) return st;
+  if (count == 0) return ZO_OK;
+  size_t need = 0;
+  zo_refresh_launch(count, panels, r, nullptr, nullptr, 0, nullptr, &need);
+  if (ws_bytes < need || (need && !workspace)) {
+    zo_set_error("refresh: workspace %zu bytes < required %zu", ws_bytes, need);
+    return ZO_ERR_WORKSPACE;
+  }
+  ZO_CHECK(aligned(workspace, 256), "refresh: workspace not 256-byte aligned");
+  return zo_refresh_launch(count, panels, r, info, workspace, ws_bytes, (hipStream_t)stream,
+                           nullptr);
+}
+
+// --------------------------------------------------------- perturbed linear
+static int check_plinear(int T, int m, int n, int r, int q, int nblk, long long xs, int in_dtype) {
+  ZO_CHECK(T >= 1 && m >= 1 && n >= 1, "perturbed_linear: T, m, n must be >= 1 (got %d, %d, %d)",
+           T, m, n);
+  ZO_CHECK(r >= 1 && r <= ZO_MAX_RANK, "perturbed_linear: r = %d outside [1, %d]", r, ZO_MAX_RANK);
+  ZO_CHECK(q >= 1 && q <= ZO_MAX_QUERIES, "perturbed_linear: q = %d outside [1, %d]", q,
+           ZO_MAX_QUERIES);
+  ZO_CHECK(nblk >= 1 && nblk <= ZO_MAX_BLOCKS, "perturbed_linear: nblk = %d outside [1, %d]", nblk,
+           ZO_MAX_BLOCKS);
+  ZO_CHECK(in_dtype == ZO_F32 || in_dtype == ZO_BF16, "perturbed_linear: bad in_dtype %d",
+           in_dtype);
+  ZO_CHECK(xs == 0 || xs >= (long long)T * n,
+           "perturbed_linear: x_block_stride = %lld must be 0 or >= T*n", xs);
+  ZO_CHECK((long long)T * nblk < (1LL << 31), "perturbed_linear: T * nblk too large");
+  if (in_dtype == ZO_BF16) {
+    ZO_CHECK(m % 8 == 0 && n % 8 == 0, "perturbed_linear: bf16 needs m %% 8 == 0 and n %% 8 == 0 "
+             "(got m = %d, n = %d)", m, n);
+    ZO_CHECK(xs % 8 == 0, "perturbed_linear: bf16 x_block_stride must be a multiple of 8");
+  }
+  return ZO_OK;
+}
+
+size_t zo_perturbed_linear_workspace(int T, int m, int n, int r, int q, int nblk,
+                                     long long x_block_stride, int in_dtype) {
+  if (check_plinear(T, m, n, r, q, nblk, x_block_stride, in_dtype) != ZO_OK) return 0;
+  PlinearPlan p;
+  zo_plinear_plan(&p, T, m, n, r, q, nblk, x_block_stride, in_dtype, in_dtype);
+  return p.ws_total;
+}
+
+int zo_perturbed_linear(int T, int m, int n, int r, int q, int nblk, const int* blk_query,
+                        const int8_t* blk_sign, float eps, int in_dtype, const void* X,
+                        long long x_block_stride, const void* W, const float* U, const float* V,
+                        const float* Z, int out_dtype, void* Y, void* workspace, size_t ws_bytes,
+                        void* stream) {
+  int st = check_plinear(T, m, n, r, q, nblk, x_block_stride, in_dtype);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(blk_query && blk_sign, "perturbed_linear: blk_query / blk_sign is NULL");
+  for (int b = 0; b < nblk; ++b) {
+    ZO_CHECK(blk_query[b] >= 0 && blk_query[b] < q, "perturbed_linear: blk_query[%d] = %d outside "
+             "[0, %d)", b, blk_query[b], q);
+    ZO_CHECK(blk_sign[b] >= -1 && blk_sign[b] <= 1, "perturbed_linear: blk_sign[%d] = %d not in "
+             "{-1, 0, 1}", b, (int)blk_sign[b]);
+  }
+  ZO_CHECK(isfinite(eps), "perturbed_linear: eps is not finite");
+  ZO_CHECK(X && W && U && V && Z && Y, "perturbed_linear: NULL tensor argument");
+  ZO_CHECK(out_dtype == ZO_F32 || out_dtype == ZO_BF16, "perturbed_linear: bad out_dtype %d",
+           out_dtype);
+  if (in_dtype == ZO_F32 && out_dtype != ZO_F32) {
+    zo_set_error("perturbed_linear: fp32 inputs need fp32 output");
+    return ZO_ERR_UNSUPPORTED;
+  }
+  if (in_dtype == ZO_BF16) {
+    ZO_CHECK(aligned(X, 16) && aligned(W, 16) && aligned(Y, 16),
+             "perturbed_linear: bf16 X, W and Y must be 16-byte aligned");
+  } else {
+    ZO_CHECK(aligned(X, 4) && aligned(W, 4) && aligned(Y, 4),
+             "perturbed_linear: fp32 tensors must be 4-byte aligned");
+  }
+  ZO_CHECK(aligned(U, 4) && aligned(V, 4) && aligned(Z, 4), "perturbed_linear: U, V, Z alignment");
+  PlinearPlan p;
+  zo_plinear_plan(&p, T, m, n, r, q, nblk, x_block_stride, in_dtype, out_dtype);
+  if (ws_bytes < p.ws_total || !workspace) {
+    zo_set_error("perturbed_linear: workspace %zu bytes < required %zu", ws_bytes, p.ws_total);
+    return ZO_ERR_WORKSPACE;
+  }
+  ZO_CHECK(aligned(workspace, 256), "perturbed_linear: workspace not 256-byte aligned");
+  return zo_plinear_launch(p, blk_query, blk_sign, eps, X, W, U, V, Z, Y, workspace,
+                           (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------ update
+static int check_update(int count, const zo_update_item* items, int r, int q, int w_dtype) {
+  ZO_CHECK(count >= 0, "update: count = %d < 0", count);
+  ZO_CHECK(count == 0 || items, "update: items is NULL");
+  ZO_CHECK(r >= 1 && r <= ZO_MAX_RANK, "update: r = %d outside [1, %d]", r, ZO_MAX_RANK);
+  ZO_CHECK(q >= 1 && q <= ZO_MAX_QUERIES, "update: q = %d outside [1, %d]", q, ZO_MAX_QUERIES);
+  ZO_CHECK(w_dtype == ZO_F32 || w_dtype == ZO_BF16, "update: bad w_dtype %d", w_dtype);
+  for (int i = 0; i < count; ++i) {
+    const zo_update_item& it = items[i];
+    ZO_CHECK(it.m >= 1 && it.n >= 1, "update: item %d has m = %d, n = %d", i, it.m, it.n);
+    ZO_CHECK((long long)it.m * it.n < (1LL << 40), "update: item %d too large", i);
+    ZO_CHECK(it.W && it.U && it.V && it.Z && it.M1 && it.M2, "update: item %d has a NULL tensor", i);
+    if (w_dtype == ZO_BF16) {
+      ZO_CHECK(it.n % 8 == 0, "update: bf16 W needs n %% 8 == 0 (item %d, n = %d)", i, it.n);
+      ZO_CHECK(aligned(it.W, 16) && aligned(it.w_f32_out, 16),
+               "update: item %d W / w_f32_out not 16-byte aligned", i);
+      ZO_CHECK((long long)((it.m + 127) / 128) * ((it.n + 255) / 256) < (1LL << 30),
+               "update: item %d too large", i);
+    } else {
+      ZO_CHECK(aligned(it.W, 4) && aligned(it.w_f32_out, 4), "update: item %d alignment", i);
+      ZO_CHECK((long long)it.m * it.n < (1LL << 38), "update: item %d too large", i);
+    }
+  }
+  return ZO_OK;
+}
+
+size_t zo_subspace_adam_update_workspace(int count, const zo_update_item* items, int r, int q,
+                                         int w_dtype) {
+  if (check_update(count, items, r, q, w_dtype) != ZO_OK) return 0;
+  size_t need = 0;
+  zo_update_launch(count, items, w_dtype, r, q, nullptr, 1, 0.f, 0.f, 0.f, 0.f, nullptr, nullptr,
+                   0, nullptr, &need);
+  return need;
+}
+
+int zo_subspace_adam_update(int count, const zo_update_item* items, int w_dtype, int r, int q,
+                            const float* g, int t, float lr, float beta1, float beta2,
+                            float eps_adam, int* nonfinite_flag, void* workspace, size_t ws_bytes,
+                            void* stream) {
+  int st = check_update(count, items, r, q, w_dtype);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(g, "update: g is NULL");
+  ZO_CHECK(t >= 1, "update: Adam step t = %d must be >= 1", t);
+  ZO_CHECK(isfinite(lr), "update: lr is not finite");
+  ZO_CHECK(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f,
+           "update: betas must lie in [0, 1)");
+  ZO_CHECK(eps_adam >= 0.f && isfinite(eps_adam), "update: eps_adam must be finite and >= 0");
+  if (count == 0) return ZO_OK;
+  size_t need = 0;
+  zo_update_launch(count, items, w_dtype, r, q, nullptr, 1, 0.f, 0.f, 0.f, 0.f, nullptr, nullptr,
+                   0, nullptr, &need);
+  if (ws_bytes < need || !workspace) {
+    zo_set_error("update: workspace %zu bytes < required %zu", ws_bytes, need);
+    return ZO_ERR_WORKSPACE;
+  }
+  ZO_CHECK(aligned(workspace, 256), "update: workspace not 256-byte aligned");
+  return zo_update_launch(count, items, w_dtype, r, q, g, t, lr, beta1, beta2, eps_adam,
+                          nonfinite_flag, workspace, ws_bytes, (hipStream_t)stream, nullptr);
+}
+
+// ------------------------------------------------------------------- losses
+size_t zo_sq_loss_workspace(int nblk, int T, int m) {
+  if (nblk < 1 || T < 1 || m < 1) return 0;
+  size_t need = 0;
+  zo_sq_loss_launch(nblk, T, m, ZO_F32, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &need);
+  return need;
+}
+
+int zo_sq_loss(int nblk, int T, int m, int dtype, const void* Y, const void* Ystar, double* out,
+               void* workspace, size_t ws_bytes, void* stream) {
+  ZO_CHECK(nblk >= 1 && T >= 1 && m >= 1, "sq_loss: nblk, T, m must be >= 1");
+  ZO_CHECK(nblk <= 65535, "sq_loss: nblk = %d too large", nblk);
+  ZO_CHECK(dtype == ZO_F32 || dtype == ZO_BF16, "sq_loss: bad dtype %d", dtype);
+  ZO_CHECK(Y && Ystar && out, "sq_loss: NULL tensor argument");
+  size_t need = 0;
+  zo_sq_loss_launch(nblk, T, m, dtype, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &need);
+  if (ws_bytes < need || !workspace) {
+    zo_set_error("sq_loss: workspace %zu bytes < required %zu", ws_bytes, need);
+    return ZO_ERR_WORKSPACE;
+  }
+  return zo_sq_loss_launch(nblk, T, m, dtype, Y, Ystar, out, workspace, ws_bytes,
+                           (hipStream_t)stream, nullptr);
+}
+
+int zo_combine_central(int q, const double* L, float eps, float* g, void* stream) {
+  ZO_CHECK(q >= 1, "combine_central: q = %d < 1", q);
+  ZO_CHECK(L && g, "combine_central: NULL tensor argument");
+  ZO_CHECK(isfinite(eps) && eps != 0.f, "combine_central: eps must be finite and non-zero");
+  return zo_combine_central_launch(q, L, eps, g, (hipStream_t)stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,530 @@
+// Perturbed linear layer of SubZero+ (Eq. 4 inside the forward of Eq. 5).
+//
+//   Y_b = X_b W^T + (X_b V) (s_b eps U Z_{j(b)})^T
+//
+// Launches per call (bf16 inputs):
+//   1. k_transpose_v : V (n x r fp32) -> Vt2 (2 rp x n bf16): rows [0, rp) the
+//                      high bf16 part of V^T, rows [rp, 2 rp) the low part
+//                      (V = hi + lo to ~16 bits); rp = r rounded up to 16.
+//   2. P2 = X_x Vt2^T: the n -> rp projection of every distinct X block, as
+//                      two fp32 halves (one GEMM launch, narrow A operand).
+//   3. k_pcombine    : P = P2_hi + P2_lo, written as the K segment
+//                      [P_hi | P_hi | P_lo] (bf16, 3 rp wide).
+//   4. k_bprime      : B_b = s_b eps U Z_{j(b)} (fp32) written as the K segment
+//                      [B_hi | B_lo | B_hi] (bf16, 3 rp wide), every block.
+//   5. main GEMM     : Y_b = X_b W^T + P_{x(b)} B_b^T, the rank-r term added as
+//                      one more 3 rp-deep K segment into the same fp32
+//                      accumulators: hi*hi + hi*lo + lo*hi, so the correction
+//                      carries ~2^-16 relative error instead of the 2^-8 of
+//                      plain bf16 operands.
+// fp32 inputs: Vt (rp x n), P = X Vt^T and B_b in fp32, fp32 FMA throughout.
+//
+// bf16 GEMM: one workgroup computes a BM x BN tile of Y_b^T (BM output
+// columns, BN tokens) with v_mfma_f32_32x32x16_bf16.  The A operand is the
+// W tile (rows = output columns), the B operand the X tile (rows = tokens);
+// both are K-contiguous, staged through LDS in 128-byte rows with an XOR
+// swizzle of the 16-byte chunks, double buffered.  Accumulator lane layout of
+// the 32x32 MFMA: lane l holds token (l % 32) and output columns
+// 8a + 4(l / 32) + {0,1,2,3}, a = 0..3, so each lane stores 4 adjacent
+// outputs.  Workgroup ids are remapped so that the tiles one XCD runs
+// concurrently are contiguous, then grouped 8 token tiles deep so the tiles
+// in flight on an XCD share their W and X panels in that XCD's L2.
+#include "zo_internal.h"
+
+namespace {
+
+constexpr int BK = 64;  // bf16 elements per K tile = 128 bytes per LDS row
+
+// Swizzle of the 16-byte chunk index within a 128-byte LDS row; conflict free
+// for ds_read_b128 of 8 or 16 consecutive rows at one logical chunk.
+__device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ ((row & 1) << 2)) & 7; }
+
+struct GemmArgs {
+  const bf16_t* A;            // rows_a x K (shared by all blocks)
+  const bf16_t* B;            // per block rows_b x K
+  long long b_block_stride;   // elements; 0 = shared
+  int rows_a, rows_b, K, nblk;
+  const bf16_t* ca;           // correction A operand: per block rows_a x rc
+  long long ca_block_stride;
+  const bf16_t* cb;           // correction B operand: per block rows_b x rc
+  long long cb_block_stride;
+  int rc;                     // multiple of 16; 0 = no correction
+  void* Y;                    // per block rows_b x ldy
+  long long y_block_stride;
+  int ldy, out_bf16;
+  int tiles_a, tiles_b, total_tiles;
+};
+
+template <int WM, int WN, int TM, int TN>
+__global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int BM = WM * TM * 32;
+  constexpr int BN = WN * TN * 32;
+  constexpr int CA = BM * 8 / NT;
+  constexpr int CB = BN * 8 / NT;
+  constexpr int RSTEP = NT / 8;
+  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0, "tile/thread mismatch");
+  static_assert(RSTEP % 16 == 0, "swizzle must be invariant over the row step");
+  __shared__ __attribute__((aligned(16))) char lds[2 * (BM + BN) * 128];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % WM;
+  const int wn = wave / WM;
+
+  // XCD-aware remap: hardware deals workgroup w to XCD w % 8; give each XCD a
+  // contiguous range of logical tiles.
+  const int w = blockIdx.x;
+  const int nt = a.total_tiles;
+  const int xcd = w & 7, widx = w >> 3;
+  const int lt = xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
+  // Grouped raster: 8 token tiles (across blocks) per column sweep.
+  constexpr int GROUP = 8;
+  const int total_bt = a.nblk * a.tiles_b;
+  const int per_group = GROUP * a.tiles_a;
+  const int grp = lt / per_group;
+  const int first = grp * GROUP;
+  const int gsize = min(GROUP, total_bt - first);
+  const int rem = lt - grp * per_group;
+  const int bt = first + rem % gsize;
+  const int at = rem / gsize;
+  const int blk = bt / a.tiles_b;
+  const int t0 = (bt % a.tiles_b) * BN;
+  const int m0 = at * BM;
+
+  const bf16_t* __restrict__ Ag = a.A;
+  const bf16_t* __restrict__ Bg = a.B + (long long)blk * a.b_block_stride;
+
+  const int lrow = tid >> 3;
+  const int kc = tid & 7;
+  const int pc = kc ^ swz(lrow);
+
+  u32x4 ra[CA], rb[CB];
+  auto load_tiles = [&](int k0) {
+    const int kk = k0 + kc * 8;
+    const bool kin = kk < a.K;
+#pragma unroll
+    for (int i = 0; i < CA; ++i) {
+      const int row = m0 + lrow + RSTEP * i;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (kin && row < a.rows_a) v = *(const u32x4*)(Ag + (size_t)row * a.K + kk);
+      ra[i] = v;
+    }
+#pragma unroll
+    for (int i = 0; i < CB; ++i) {
+      const int row = t0 + lrow + RSTEP * i;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (kin && row < a.rows_b) v = *(const u32x4*)(Bg + (size_t)row * a.K + kk);
+      rb[i] = v;
+    }
+  };
+  auto store_tiles = [&](int buf) {
+    char* la = lds + buf * (BM + BN) * 128;
+    char* lb = la + BM * 128;
+#pragma unroll
+    for (int i = 0; i < CA; ++i) *(u32x4*)(la + (lrow + RSTEP * i) * 128 + pc * 16) = ra[i];
+#pragma unroll
+    for (int i = 0; i < CB; ++i) *(u32x4*)(lb + (lrow + RSTEP * i) * 128 + pc * 16) = rb[i];
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int fr = lane & 31;
+  const int fh = lane >> 5;
+  const int fsw = swz(fr);
+  auto compute = [&](int buf) {
+    const char* la = lds + buf * (BM + BN) * 128;
+    const char* lb = la + BM * 128;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int ch = ((ks * 2 + fh) ^ fsw) * 16;
+      bf16x8 fa[TM], fb[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        fa[i] = *(const bf16x8*)(la + (wm * TM * 32 + i * 32 + fr) * 128 + ch);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        fb[j] = *(const bf16x8*)(lb + (wn * TN * 32 + j * 32 + fr) * 128 + ch);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  const int nk = (a.K + BK - 1) / BK;
+  load_tiles(0);
+  store_tiles(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) load_tiles((kt + 1) * BK);
+    compute(cur);
+    if (kt + 1 < nk) store_tiles(cur ^ 1);
+    __syncthreads();
+  }
+
+  // Rank-rc correction: one more K segment with operands read straight from
+  // global memory (16 bytes per lane per fragment).
+  if (a.rc > 0) {
+    const bf16_t* __restrict__ Cg = a.ca + (long long)blk * a.ca_block_stride;
+    const bf16_t* __restrict__ Dg = a.cb + (long long)blk * a.cb_block_stride;
+    for (int k0 = 0; k0 < a.rc; k0 += 16) {
+      bf16x8 fa[TM], fb[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int row = m0 + wm * TM * 32 + i * 32 + fr;
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (row < a.rows_a) v = *(const u32x4*)(Cg + (size_t)row * a.rc + k0 + fh * 8);
+        fa[i] = __builtin_bit_cast(bf16x8, v);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int row = t0 + wn * TN * 32 + j * 32 + fr;
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (row < a.rows_b) v = *(const u32x4*)(Dg + (size_t)row * a.rc + k0 + fh * 8);
+        fb[j] = __builtin_bit_cast(bf16x8, v);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  // Store: lane holds token fr (+32j) and 4 adjacent output columns per a.
+  char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (a.out_bf16 ? 2 : 4);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int tok = t0 + wn * TN * 32 + j * 32 + fr;
+    if (tok >= a.rows_b) continue;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int col = m0 + wm * TM * 32 + i * 32 + q4 * 8 + fh * 4;
+        if (col >= a.rows_a) continue;
+        const float v0 = acc[i][j][q4 * 4 + 0], v1 = acc[i][j][q4 * 4 + 1];
+        const float v2 = acc[i][j][q4 * 4 + 2], v3 = acc[i][j][q4 * 4 + 3];
+        if (a.out_bf16) {
+          u32x2 pk = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+          *(u32x2*)(Yb + ((size_t)tok * a.ldy + col) * 2) = pk;
+        } else {
+          f32x4 pk = {v0, v1, v2, v3};
+          *(f32x4*)(Yb + ((size_t)tok * a.ldy + col) * 4) = pk;
+        }
+      }
+    }
+  }
+}
+
+// fp32 path: plain 64x64 tile GEMM, fp32 FMA, with the same correction term.
+struct F32Args {
+  const float* A;  // rows_a x K
+  const float* B;  // per block rows_b x K
+  long long b_block_stride;
+  int rows_a, rows_b, K;
+  const float* ca;  // per block rows_a x rc
+  long long ca_block_stride;
+  const float* cb;  // per block rows_b x rc
+  long long cb_block_stride;
+  int rc;
+  float* Y;
+  long long y_block_stride;
+  int ldy;
+};
+
+__global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
+  __shared__ float sb[16][68];
+  __shared__ float sa[16][68];
+  const int blk = blockIdx.z;
+  const int t0 = blockIdx.y * 64;
+  const int c0 = blockIdx.x * 64;
+  const float* __restrict__ B = a.B + (long long)blk * a.b_block_stride;
+  const float* __restrict__ A = a.A;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+  for (int k0 = 0; k0 < a.K; k0 += 16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = threadIdx.x + 256 * i;
+      const int row = e >> 4, kk = e & 15;
+      const int k = k0 + kk;
+      sb[kk][row] = (t0 + row < a.rows_b && k < a.K) ? B[(size_t)(t0 + row) * a.K + k] : 0.f;
+      sa[kk][row] = (c0 + row < a.rows_a && k < a.K) ? A[(size_t)(c0 + row) * a.K + k] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(sb[kk][ty * 4 + i], sa[kk][tx * 4 + j], acc[i][j]);
+    __syncthreads();
+  }
+  if (a.rc > 0) {
+    const float* __restrict__ C = a.ca + (long long)blk * a.ca_block_stride;
+    const float* __restrict__ D = a.cb + (long long)blk * a.cb_block_stride;
+    for (int c = 0; c < a.rc; ++c) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = t0 + ty * 4 + i;
+        const float p = tok < a.rows_b ? D[(size_t)tok * a.rc + c] : 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int col = c0 + tx * 4 + j;
+          const float q = col < a.rows_a ? C[(size_t)col * a.rc + c] : 0.f;
+          acc[i][j] = fmaf(p, q, acc[i][j]);
+        }
+      }
+    }
+  }
+  float* Y = a.Y + (long long)blk * a.y_block_stride;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tok = t0 + ty * 4 + i;
+    if (tok >= a.rows_b) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = c0 + tx * 4 + j;
+      if (col < a.rows_a) Y[(size_t)tok * a.ldy + col] = acc[i][j];
+    }
+  }
+}
+
+// Vt[a][k] = V[k][a] for a < r, 0 for r <= a < rp.  bf16: hi part in rows
+// [0, rp), low part (V - hi, rounded) in rows [rp, 2 rp).
+__global__ __launch_bounds__(256) void k_transpose_v(const float* __restrict__ V, int n, int r,
+                                                      int rp, void* Vt, int out_bf16) {
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long long)rp * n) return;
+  const int a = (int)(idx / n), k = (int)(idx % n);
+  const float v = a < r ? V[(size_t)k * r + a] : 0.f;
+  if (out_bf16) {
+    const bf16_t hi = f32_to_bf16(v);
+    ((bf16_t*)Vt)[idx] = hi;
+    ((bf16_t*)Vt)[(long long)rp * n + idx] = f32_to_bf16(v - bf16_to_f32(hi));
+  } else {
+    ((float*)Vt)[idx] = v;
+  }
+}
+
+// P = P2[:, :rp] + P2[:, rp:] (fp32), written as [P_hi | P_hi | P_lo] (bf16, 3 rp wide).
+__global__ __launch_bounds__(256) void k_pcombine(const float* __restrict__ P2, long long rows,
+                                                   int rp, bf16_t* __restrict__ Pc) {
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= rows * rp) return;
+  const long long t = idx / rp;
+  const int a = (int)(idx % rp);
+  const float p = P2[t * 2 * rp + a] + P2[t * 2 * rp + rp + a];
+  const bf16_t hi = f32_to_bf16(p);
+  const bf16_t lo = f32_to_bf16(p - bf16_to_f32(hi));
+  bf16_t* o = Pc + t * 3 * rp;
+  o[a] = hi;
+  o[rp + a] = hi;
+  o[2 * rp + a] = lo;
+}
+
+// Query table of a call: j(b) and s(b) packed as j | (s + 1) << 16.
+struct BlkTable {
+  int code[ZO_MAX_BLOCKS];
+};
+
+// B_b[i][a] = s_b eps sum_c U[i][c] Z_{j(b)}[c][a] (a < r; 0 for r <= a < rp).
+// fp32 output: m x rp per block.  bf16 output: m x 3 rp per block as
+// [B_hi | B_lo | B_hi].
+__global__ __launch_bounds__(256) void k_bprime(const float* __restrict__ U,
+                                                const float* __restrict__ Z, int m, int r,
+                                                int rp, int nblk, float eps, BlkTable tab,
+                                                void* Bp, int out_bf16) {
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  const long long per = (long long)m * rp;
+  if (idx >= per * nblk) return;
+  const int b = (int)(idx / per);
+  const long long rem = idx - (long long)b * per;
+  const int i = (int)(rem / rp), a = (int)(rem % rp);
+  float v = 0.f;
+  if (a < r) {
+    const int code = tab.code[b];
+    const int j = code & 0xffff;
+    const float s = (float)((code >> 16) - 1);
+    const float* __restrict__ Zj = Z + (size_t)j * r * r;
+    const float* __restrict__ Ui = U + (size_t)i * r;
+    float acc = 0.f;
+    for (int c = 0; c < r; ++c) acc = fmaf(Ui[c], Zj[c * r + a], acc);
+    v = s * eps * acc;
+  }
+  if (out_bf16) {
+    const bf16_t hi = f32_to_bf16(v);
+    const bf16_t lo = f32_to_bf16(v - bf16_to_f32(hi));
+    bf16_t* o = (bf16_t*)Bp + ((long long)b * m + i) * 3 * rp;
+    o[a] = hi;
+    o[rp + a] = lo;
+    o[2 * rp + a] = hi;
+  } else {
+    ((float*)Bp)[idx] = v;
+  }
+}
+
+template <int WM, int WN, int TM, int TN>
+int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
+  constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
+  a.tiles_a = (a.rows_a + BM - 1) / BM;
+  a.tiles_b = (a.rows_b + BN - 1) / BN;
+  const long long total = (long long)a.tiles_a * a.tiles_b * a.nblk;
+  if (total <= 0) return ZO_OK;
+  if (total > 0x7fffffffLL) {
+    zo_set_error("perturbed linear: too many tiles (%lld)", total);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  a.total_tiles = (int)total;
+  hipLaunchKernelGGL((k_gemm_bf16<WM, WN, TM, TN>), dim3(a.total_tiles), dim3(WM * WN * 64), 0,
+                     stream, a);
+  return zo_hip_status(hipGetLastError(), "k_gemm_bf16");
+}
+
+}  // namespace
+
+int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
+                    long long x_block_stride, int in_dtype, int out_dtype) {
+  p->T = T;
+  p->m = m;
+  p->n = n;
+  p->r = r;
+  p->rp = (r + 15) / 16 * 16;
+  p->q = q;
+  p->nblk = nblk;
+  p->x_block_stride = x_block_stride;
+  p->nx = x_block_stride == 0 ? 1 : nblk;
+  p->in_bf16 = in_dtype == ZO_BF16;
+  p->out_bf16 = out_dtype == ZO_BF16;
+  const size_t rows = (size_t)p->nx * T;
+  if (p->in_bf16) {
+    p->ws_vt = zo_align256((size_t)2 * p->rp * n * 2);       // Vt hi and lo, bf16
+    p->ws_p2 = zo_align256(rows * 2 * p->rp * 4);            // X Vt2^T, fp32
+    p->ws_p = zo_align256(rows * 3 * p->rp * 2);             // [P_hi | P_hi | P_lo]
+    p->ws_bp = zo_align256((size_t)nblk * m * 3 * p->rp * 2);  // [B_hi | B_lo | B_hi]
+  } else {
+    p->ws_vt = zo_align256((size_t)p->rp * n * 4);
+    p->ws_p2 = 0;
+    p->ws_p = zo_align256(rows * p->rp * 4);
+    p->ws_bp = zo_align256((size_t)nblk * m * p->rp * 4);
+  }
+  p->ws_total = p->ws_vt + p->ws_p2 + p->ws_p + p->ws_bp;
+  return ZO_OK;
+}
+
+int zo_plinear_launch(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
+                      float eps, const void* X, const void* W, const float* U, const float* V,
+                      const float* Z, void* Y, void* ws, hipStream_t stream) {
+  WsCarver wc(ws);
+  void* vt = wc.take(p.ws_vt);
+  void* p2 = p.ws_p2 ? wc.take(p.ws_p2) : nullptr;
+  void* pp = wc.take(p.ws_p);
+  void* bp = wc.take(p.ws_bp);
+  int st;
+
+  {
+    const long long total = (long long)p.rp * p.n;
+    hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                       V, p.n, p.r, p.rp, vt, p.in_bf16);
+    if ((st = zo_hip_status(hipGetLastError(), "k_transpose_v")) != ZO_OK) return st;
+  }
+  {
+    BlkTable tab;
+    for (int b = 0; b < p.nblk; ++b) tab.code[b] = blk_query[b] | ((int)(blk_sign[b] + 1) << 16);
+    const long long total = (long long)p.nblk * p.m * p.rp;
+    hipLaunchKernelGGL(k_bprime, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, U, Z,
+                       p.m, p.r, p.rp, p.nblk, eps, tab, bp, p.in_bf16);
+    if ((st = zo_hip_status(hipGetLastError(), "k_bprime")) != ZO_OK) return st;
+  }
+  const long long xs = p.x_block_stride;
+  if (p.in_bf16) {
+    GemmArgs g{};
+    g.A = (const bf16_t*)vt;
+    g.B = (const bf16_t*)X;
+    g.b_block_stride = xs;
+    g.rows_a = 2 * p.rp;
+    g.rows_b = p.T;
+    g.K = p.n;
+    g.nblk = p.nx;
+    g.rc = 0;
+    g.Y = p2;
+    g.y_block_stride = (long long)p.T * 2 * p.rp;
+    g.ldy = 2 * p.rp;
+    g.out_bf16 = 0;
+    if ((st = launch_gemm_bf16<1, 4, 2, 2>(g, stream)) != ZO_OK) return st;
+    const long long prow = (long long)p.nx * p.T;
+    hipLaunchKernelGGL(k_pcombine, dim3((unsigned)((prow * p.rp + 255) / 256)), dim3(256), 0, stream,
+                       (const float*)p2, prow, p.rp, (bf16_t*)pp);
+    if ((st = zo_hip_status(hipGetLastError(), "k_pcombine")) != ZO_OK) return st;
+
+    GemmArgs h{};
+    h.A = (const bf16_t*)W;
+    h.B = (const bf16_t*)X;
+    h.b_block_stride = xs;
+    h.rows_a = p.m;
+    h.rows_b = p.T;
+    h.K = p.n;
+    h.nblk = p.nblk;
+    h.ca = (const bf16_t*)bp;
+    h.ca_block_stride = (long long)p.m * 3 * p.rp;
+    h.cb = (const bf16_t*)pp;
+    h.cb_block_stride = p.nx == 1 ? 0 : (long long)p.T * 3 * p.rp;
+    h.rc = 3 * p.rp;
+    h.Y = Y;
+    h.y_block_stride = (long long)p.T * p.m;
+    h.ldy = p.m;
+    h.out_bf16 = p.out_bf16;
+    return launch_gemm_bf16<2, 4, 4, 2>(h, stream);
+  }
+  {
+    F32Args g{};
+    g.A = (const float*)vt;
+    g.B = (const float*)X;
+    g.b_block_stride = xs;
+    g.rows_a = p.rp;
+    g.rows_b = p.T;
+    g.K = p.n;
+    g.rc = 0;
+    g.Y = (float*)pp;
+    g.y_block_stride = (long long)p.T * p.rp;
+    g.ldy = p.rp;
+    dim3 grid((p.rp + 63) / 64, (p.T + 63) / 64, p.nx);
+    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, stream, g);
+    if ((st = zo_hip_status(hipGetLastError(), "k_gemm_f32 (projection)")) != ZO_OK) return st;
+  }
+  {
+    F32Args h{};
+    h.A = (const float*)W;
+    h.B = (const float*)X;
+    h.b_block_stride = xs;
+    h.rows_a = p.m;
+    h.rows_b = p.T;
+    h.K = p.n;
+    h.ca = (const float*)bp;
+    h.ca_block_stride = (long long)p.m * p.rp;
+    h.cb = (const float*)pp;
+    h.cb_block_stride = p.nx == 1 ? 0 : (long long)p.T * p.rp;
+    h.rc = p.rp;
+    h.Y = (float*)Y;
+    h.y_block_stride = (long long)p.T * p.m;
+    h.ldy = p.m;
+    dim3 grid((p.m + 63) / 64, (p.T + 63) / 64, p.nblk);
+    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, stream, h);
+    return zo_hip_status(hipGetLastError(), "k_gemm_f32");
+  }
+}

@@ -1,0 +1,83 @@
+// Internal declarations shared by the HIP sources of libzo (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "zo.h"
+
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------- host side
+void zo_set_error(const char* fmt, ...);
+int zo_hip_status(hipError_t e, const char* what);
+
+static inline size_t zo_align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Carves consecutive 256-byte aligned regions out of a workspace.
+struct WsCarver {
+  char* base;
+  size_t off;
+  explicit WsCarver(void* p) : base((char*)p), off(0) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + off : nullptr;
+    off += zo_align256(bytes);
+    return p;
+  }
+};
+
+// ---------------------------------------------------------------- device side
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// Round to nearest even; NaN stays NaN (quiet).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// ---------------------------------------------------------------- launchers
+// Perturbed linear (zo_gemm.hip).
+struct PlinearPlan {
+  int T, m, n, r, rp, q, nblk, nx;  // nx: number of distinct X blocks (1 or nblk)
+  long long x_block_stride;
+  int in_bf16, out_bf16;
+  size_t ws_vt, ws_p2, ws_p, ws_bp;  // bytes of each workspace region
+  size_t ws_total;
+};
+int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
+                    long long x_block_stride, int in_dtype, int out_dtype);
+int zo_plinear_launch(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
+                      float eps, const void* X, const void* W, const float* U,
+                      const float* V, const float* Z, void* Y, void* ws,
+                      hipStream_t stream);
+
+// Subspace Adam update (zo_update.hip).
+int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r, int q,
+                     const float* g, int t, float lr, float beta1, float beta2,
+                     float eps_adam, int* nonfinite_flag, void* ws, size_t ws_bytes,
+                     hipStream_t stream, size_t* ws_needed);
+
+// Householder TSQR refresh (zo_qr.hip).
+int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void* ws,
+                      size_t ws_bytes, hipStream_t stream, size_t* ws_needed);
+
+// Loss helpers (zo_loss.hip).
+int zo_sq_loss_launch(int nblk, int T, int m, int dtype, const void* Y, const void* Ystar,
+                      double* out, void* ws, size_t ws_bytes, hipStream_t stream,
+                      size_t* ws_needed);
+int zo_combine_central_launch(int q, const double* L, float eps, float* g,
+                              hipStream_t stream);

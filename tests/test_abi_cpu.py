@@ -1,0 +1,133 @@
+"""The C ABI on the host: every symbol include/zo.h declares is exported, and
+argument errors are reported before anything is launched (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_15665_amd as zo
+from paper_2608_15665_amd._lib import Panel, UpdateItem
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "zo.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(zo_\w+)\s*\(", src)))
+
+
+def test_header_declares_the_abi():
+    fns = header_functions()
+    assert set(fns) == set(zo.ABI_SYMBOLS), fns
+
+
+def test_library_exports_every_declared_symbol():
+    L = zo.lib()
+    for name in header_functions():
+        assert hasattr(L, name), name
+    assert zo.abi_version() == 1
+
+
+def test_struct_layouts_match_header():
+    # zo_panel: int + 3 pointers; zo_update_item: 2 ints + 8 pointers.
+    assert ctypes.sizeof(Panel) == 32
+    assert ctypes.sizeof(UpdateItem) == 8 + 8 * 8
+
+
+def _detail():
+    return zo.lib().zo_last_error_detail().decode()
+
+
+def test_status_strings():
+    L = zo.lib()
+    assert L.zo_status_str(0) == b"ok"
+    assert L.zo_status_str(6) == b"workspace too small"
+
+
+@pytest.mark.parametrize("args,needle", [
+    (dict(T=0), "T, m, n"),
+    (dict(r=0), "r = 0"),
+    (dict(r=129), "r = 129"),
+    (dict(q=0), "q = 0"),
+    (dict(nblk=257), "nblk = 257"),
+    (dict(m=12), "m % 8"),
+    (dict(n=20), "n % 8"),
+    (dict(xs=5), "x_block_stride"),
+    (dict(blk_query=[0, 5]), "blk_query[1]"),
+    (dict(blk_sign=[1, 2]), "blk_sign[1]"),
+    (dict(in_dtype=7), "in_dtype"),
+])
+def test_perturbed_linear_validation(args, needle):
+    p = dict(T=16, m=32, n=64, r=4, q=2, nblk=2, blk_query=[0, 1], blk_sign=[1, -1], xs=0, in_dtype=1)
+    p.update(args)
+    nb = p["nblk"]
+    bq = (ctypes.c_int * max(nb, 2))(*(p["blk_query"] + [0] * (max(nb, 2) - 2)))
+    bs = (ctypes.c_int8 * max(nb, 2))(*(p["blk_sign"] + [1] * (max(nb, 2) - 2)))
+    fake = 1 << 20  # never dereferenced: validation fails first
+    st = zo.lib().zo_perturbed_linear(p["T"], p["m"], p["n"], p["r"], p["q"], nb, bq, bs, 1e-3,
+                                      p["in_dtype"], fake, p["xs"], fake, fake, fake, fake, 1, fake,
+                                      fake, 1 << 30, None)
+    assert st == 1, (st, _detail())
+    assert needle in _detail()
+
+
+def test_perturbed_linear_rejects_small_workspace_and_nulls():
+    L = zo.lib()
+    bq = (ctypes.c_int * 2)(0, 0)
+    bs = (ctypes.c_int8 * 2)(1, -1)
+    fake = 1 << 20
+    need = L.zo_perturbed_linear_workspace(16, 32, 64, 4, 1, 2, 0, 1)
+    assert need > 0
+    st = L.zo_perturbed_linear(16, 32, 64, 4, 1, 2, bq, bs, 1e-3, 1, fake, 0, fake, fake, fake, fake, 1,
+                               fake, fake, need - 1, None)
+    assert st == 6 and "workspace" in _detail()
+    st = L.zo_perturbed_linear(16, 32, 64, 4, 1, 2, bq, bs, 1e-3, 1, None, 0, fake, fake, fake, fake, 1,
+                               fake, fake, need, None)
+    assert st == 1 and "NULL" in _detail()
+    # fp32 inputs with bf16 output is unsupported
+    st = L.zo_perturbed_linear(16, 32, 64, 4, 1, 2, bq, bs, 1e-3, 0, fake, 0, fake, fake, fake, fake, 1,
+                               fake, fake, need, None)
+    assert st == 2
+
+
+def test_refresh_validation():
+    L = zo.lib()
+    fake = 1 << 20
+    arr = (Panel * 2)(Panel(10, fake, fake, None), Panel(3, fake, fake, None))
+    assert L.zo_subspace_refresh(2, arr, 4, None, fake, 1 << 30, None) == 1
+    assert "rows = 3 < r = 4" in _detail()
+    assert L.zo_subspace_refresh(1, arr, 100, None, fake, 1 << 30, None) == 2  # above the QR rank limit
+    assert L.zo_subspace_refresh(1, arr, 0, None, fake, 1 << 30, None) == 1
+    assert L.zo_subspace_refresh_workspace(1, arr, 4) > 0
+    assert L.zo_subspace_refresh(1, arr, 4, None, fake, 16, None) == 6
+
+
+def test_update_validation():
+    L = zo.lib()
+    fake = 1 << 20
+    it = UpdateItem(8, 12, fake, fake, fake, fake, fake, fake, None, None)
+    arr = (UpdateItem * 1)(it)
+    assert L.zo_subspace_adam_update(1, arr, 1, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, fake,
+                                     1 << 30, None) == 1
+    assert "n % 8" in _detail()
+    it2 = UpdateItem(8, 16, fake, fake, fake, fake, fake, fake, None, None)
+    arr2 = (UpdateItem * 1)(it2)
+    assert L.zo_subspace_adam_update(1, arr2, 1, 4, 2, fake, 0, 1e-2, 0.9, 0.95, 1e-8, None, fake,
+                                     1 << 30, None) == 1
+    assert "t = 0" in _detail()
+    assert L.zo_subspace_adam_update(1, arr2, 1, 4, 2, fake, 1, 1e-2, 1.0, 0.95, 1e-8, None, fake,
+                                     1 << 30, None) == 1
+    need = L.zo_subspace_adam_update_workspace(1, arr2, 4, 2, 1)
+    assert need > 0
+    assert L.zo_subspace_adam_update(1, arr2, 1, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, fake,
+                                     need - 1, None) == 6
+
+
+def test_loss_validation():
+    L = zo.lib()
+    fake = 1 << 20
+    assert L.zo_sq_loss(0, 4, 4, 0, fake, fake, fake, fake, 1 << 20, None) == 1
+    assert L.zo_combine_central(2, fake, 0.0, fake, None) == 1
+    assert L.zo_sq_loss_workspace(2, 64, 256) > 0

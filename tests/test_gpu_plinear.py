@@ -1,0 +1,185 @@
+"""Parity of zo_perturbed_linear (HIP) with the float64 oracle (Eq. 4 in the forward of Eq. 5).
+
+The oracle materialises W + s eps U Z V^T; the GPU never does.  Tolerances
+(floored relative error e(a, b, tau) = max |a-b| / max(|b|, tau rms(b))):
+fp32 paths e(., ., 1) <= 1e-5; bf16 outputs e(., ., 1e-3) <= 1e-2 and
+normwise <= 1e-2 (bf16 rounding of the output alone reaches 2^-9 relative).
+"""
+import hashlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_15665_amd as zo
+import zo_draws as zd
+from _common import dev_bf16, dev_f32, ferr, host, normwise, orth
+
+pytestmark = pytest.mark.gpu
+
+
+def make_case(T, m, n, r, q, nblk, shared_x, bf16, seed=0, wsig=0.02):
+    """Inputs on host (exact float64 values the GPU receives) and on device.
+
+    Block b's activations are the base block X0 with its rows rolled by
+    b * floor(T / nblk) (zd.block_roll_rows); the stacked device tensor is built
+    with the same roll on the device so the host keeps only X0.
+    """
+    W64 = zd.draw(seed, "W0", (m, n), (m, n), wsig)
+    X0 = zd.draw(seed, "X", (T, n, 0), (T, n))
+    if bf16:
+        Wb, Wv = zd.as_bf16_values(W64)
+        X0b, X0v = zd.as_bf16_values(X0)
+        Wd, X0d = dev_bf16(Wb), dev_bf16(X0b)
+    else:
+        Wv = zd.f32(W64).astype(np.float64)
+        X0v = zd.f32(X0).astype(np.float64)
+        Wd, X0d = dev_f32(Wv), dev_f32(X0v)
+    step = T // nblk
+    if shared_x:
+        Xd, xs = X0d, 0
+    else:
+        Xd, xs = torch.cat([torch.roll(X0d, b * step, 0) for b in range(nblk)]).contiguous(), T * n
+    U = orth(seed, (1, m, r), m, r)
+    V = orth(seed, (2, n, r), n, r)
+    Z = zd.z_draws(seed, 0, 0, q, r)
+    bq = [b // 2 % q for b in range(nblk)]
+    bs = [1 if b % 2 == 0 else -1 for b in range(nblk)]
+    shift = [0 if shared_x else b * step for b in range(nblk)]
+    return dict(T=T, m=m, n=n, r=r, q=q, nblk=nblk, Wv=Wv, X0v=X0v, shift=shift, U=U, V=V, Z=Z,
+                bq=bq, bs=bs, Wd=Wd, Xd=Xd, Ud=dev_f32(U), Vd=dev_f32(V), Zd=dev_f32(Z), xs=xs)
+
+
+def xblock(c, b, rows=None):
+    """float64 activations of block b (optionally only the given rows)."""
+    T = c["T"]
+    idx = np.arange(T) if rows is None else np.asarray(rows)
+    return c["X0v"][(idx - c["shift"][b]) % T]
+
+
+def run_gpu(c, eps, out_dtype=None):
+    Y = zo.perturbed_linear(c["Xd"], c["Wd"], c["Ud"], c["Vd"], c["Zd"], c["bq"], c["bs"], eps, c["T"],
+                            x_block_stride=c["xs"], out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    return host(Y).reshape(c["nblk"], c["T"], c["m"])
+
+
+def run_oracle(c, eps, blocks=None, rows=None):
+    blocks = range(c["nblk"]) if blocks is None else blocks
+    out = []
+    for b in blocks:
+        out += oracle.perturbed_linear_blocks([xblock(c, b, rows)], c["Wv"], c["U"].astype(np.float64),
+                                              c["V"].astype(np.float64), c["Z"].astype(np.float64),
+                                              [c["bq"][b]], [c["bs"][b]], eps)
+    return out
+
+
+@pytest.mark.parametrize("T,m,n,r,q,nblk,shared", [
+    (64, 256, 512, 4, 4, 8, True),      # the Tiny configuration's layer
+    (37, 50, 70, 5, 3, 6, False),       # ragged everything
+    (1, 3, 1, 1, 1, 1, False),          # degenerate sizes
+    (130, 72, 300, 20, 2, 4, True),
+])
+def test_fp32_parity(T, m, n, r, q, nblk, shared):
+    c = make_case(T, m, n, r, q, nblk, shared, bf16=False)
+    Y = run_gpu(c, 1e-3)
+    ref = run_oracle(c, 1e-3)
+    for b in range(nblk):
+        assert ferr(Y[b], ref[b], 1.0) <= 1e-5, b
+
+
+@pytest.mark.parametrize("T,m,n,r,q,nblk,shared", [
+    (300, 264, 200, 16, 2, 4, False),   # ragged token, column and K tails; several tiles
+    (256, 512, 512, 64, 4, 8, False),   # exact tiles, r = 64
+    (96, 520, 136, 24, 3, 6, True),     # r not a multiple of 16, shared X
+    (513, 256, 1024, 4, 1, 2, False),   # one row past a tile
+    (8, 8, 8, 1, 1, 1, True),           # smallest legal bf16 shape
+])
+@pytest.mark.parametrize("out", ["bf16", "f32"])
+def test_bf16_parity(T, m, n, r, q, nblk, shared, out):
+    c = make_case(T, m, n, r, q, nblk, shared, bf16=True)
+    Y = run_gpu(c, 1e-3, out_dtype=torch.bfloat16 if out == "bf16" else torch.float32)
+    ref = run_oracle(c, 1e-3)
+    for b in range(nblk):
+        assert ferr(Y[b], ref[b], 1e-3) <= 1e-2, b
+        assert normwise(Y[b], ref[b]) <= 1e-2, b
+        if out == "f32":
+            # fp32 accumulation of exact bf16 products: far inside the bf16 bound.
+            assert ferr(Y[b], ref[b], 1.0) <= 1e-4, b
+
+
+def test_bf16_eps_one_correction_visible():
+    """At eps = 1 the rank-r term is large enough to be checked through bf16 outputs."""
+    c = make_case(200, 128, 256, 8, 2, 4, False, bf16=True)
+    Y = run_gpu(c, 1.0)
+    ref = run_oracle(c, 1.0)
+    base = [xblock(c, b) @ c["Wv"].T for b in range(4)]
+    for b in range(4):
+        assert normwise(Y[b], ref[b]) <= 1e-2
+        assert normwise(base[b], ref[b]) > 5e-2  # the correction matters at this eps
+
+
+def test_correction_channel_fp32_out():
+    """X_{2j} = X_{2j+1}: (Y+ - Y-)/(2 eps) isolates (X V)(U Z_j)^T, which a kernel that dropped
+    or mis-signed the rank-r term would fail (it is below bf16 resolution of Y)."""
+    T, m, n, r, q = 256, 256, 512, 16, 3
+    c = make_case(T, m, n, r, q, 2 * q, False, bf16=True)
+    X0 = c["X0v"]
+    c["Xd"] = torch.cat([c["Xd"][:T]] * (2 * q)).contiguous()  # block 0 (unrolled) for every block
+    c["bq"] = [b // 2 for b in range(2 * q)]
+    eps = 1e-3
+    Y = run_gpu(c, eps, out_dtype=torch.float32)
+    U, V = c["U"].astype(np.float64), c["V"].astype(np.float64)
+    for j in range(q):
+        d = (Y[2 * j] - Y[2 * j + 1]) / (2 * eps)
+        exact = (X0 @ V) @ (U @ c["Z"][j].astype(np.float64)).T
+        assert normwise(d, exact) <= 1e-2, j
+        assert ferr(d, exact, 1e-1) <= 5e-2, j
+
+
+def test_w_bitwise_unchanged():
+    """W is read only: its bytes are identical after the 2q queries (no in-place perturb/unperturb)."""
+    c = make_case(128, 256, 256, 16, 4, 8, False, bf16=True)
+    h0 = hashlib.sha256(c["Wd"].view(torch.int16).cpu().numpy().tobytes()).hexdigest()
+    for _ in range(3):
+        run_gpu(c, 1e-3)
+    h1 = hashlib.sha256(c["Wd"].view(torch.int16).cpu().numpy().tobytes()).hexdigest()
+    assert h0 == h1
+
+
+def test_zero_eps_is_plain_gemm():
+    c = make_case(128, 256, 192, 8, 2, 4, False, bf16=True)
+    Y = run_gpu(c, 0.0, out_dtype=torch.float32)
+    for b in range(4):
+        plain = np.matmul(xblock(c, b), c["Wv"].T)
+        assert ferr(Y[b], plain, 1.0) <= 1e-4
+
+
+def test_deterministic_repeat():
+    c = make_case(300, 264, 200, 16, 2, 4, False, bf16=True)
+    a = run_gpu(c, 1e-3)
+    b = run_gpu(c, 1e-3)
+    assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("name", ["fc1", "fc2"])
+def test_opt13b_full_size_sampled(name):
+    """The OPT-13B-shaped layer at full size (T = 8192, q = 8, 16 blocks, r = 64) in the launch
+    configuration the benchmark times; sampled token rows checked against the oracle row by row."""
+    cfg = zd.CONFIGS["opt-13b"]
+    m, n = {"fc1": (20480, 5120), "fc2": (5120, 20480)}[name]
+    T, r, q = cfg["T"], cfg["r"], cfg["q"]
+    nblk = 2 * q
+    c = make_case(T, m, n, r, q, nblk, False, bf16=True)
+    Y = zo.perturbed_linear(c["Xd"], c["Wd"], c["Ud"], c["Vd"], c["Zd"], c["bq"], c["bs"], 1e-3, T,
+                            x_block_stride=c["xs"])
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 255, 256, 4097, T - 1])
+    blocks = [0, 1, 7, nblk - 1]
+    Yh = Y.view(nblk, T, m)
+    for b in blocks:
+        got = host(Yh[b][torch.from_numpy(rows).cuda()])
+        ref = run_oracle(c, 1e-3, blocks=[b], rows=rows)[0]
+        assert ferr(got, ref, 1e-3) <= 1e-2, b
+        assert normwise(got, ref) <= 1e-2, b

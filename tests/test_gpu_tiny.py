@@ -1,0 +1,114 @@
+"""The Tiny configuration end to end on the GPU (Alg. 3 with central differences):
+W 256 x 512 fp32, X 64 x 512, r = 4, q = 4, eps = 1e-3, lr = 1e-2, beta = (0.9, 0.999),
+20 steps, refresh every 5 steps, seed 0.  Every step runs only library calls:
+refresh -> perturbed linear (8 blocks, shared X) -> squared loss -> central
+difference -> subspace Adam update.
+
+The loss differences cancel catastrophically (L ~ 6.4 while L+ - L- ~ 1e-4), so
+g carries ~1e-3 relative fp32 noise.  Teacher forcing (both sides use the
+oracle's g) checks the rest of the step at the fp32 bar; the free-running run
+is checked with bounds derived from that noise.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_15665_amd as zo
+import zo_draws as zd
+from _common import dev_f32, ferr, host
+
+pytestmark = pytest.mark.gpu
+
+C = zd.TINY
+
+
+def omega(t):
+    return zd.omega_pair(C["seed"], t, 0, C["m"], C["n"], C["r"])
+
+
+def zdraw(t):
+    return zd.z_draws(C["seed"], t, 0, C["q"], C["r"])
+
+
+class GpuTiny:
+    def __init__(self, inp):
+        self.W = dev_f32(inp["W"])
+        self.X = dev_f32(inp["X"])
+        self.Ys = dev_f32(inp["Ystar"])
+        r = C["r"]
+        self.U = torch.empty((C["m"], r), dtype=torch.float32, device="cuda")
+        self.V = torch.empty((C["n"], r), dtype=torch.float32, device="cuda")
+        self.M1 = torch.zeros((r, r), dtype=torch.float32, device="cuda")
+        self.M2 = torch.zeros((r, r), dtype=torch.float32, device="cuda")
+        self.bq = [b // 2 for b in range(2 * C["q"])]
+        self.bs = [1 if b % 2 == 0 else -1 for b in range(2 * C["q"])]
+
+    def step(self, t, g_override=None):
+        if t % C["F"] == 0:
+            ou, ov = omega(t)
+            zo.subspace_refresh([dev_f32(ou), dev_f32(ov)], C["r"], out=[self.U, self.V])
+        Z = dev_f32(zdraw(t))
+        Y = zo.perturbed_linear(self.X, self.W, self.U, self.V, Z, self.bq, self.bs, C["eps"], C["T"],
+                                x_block_stride=0)
+        L = zo.sq_loss(Y, self.Ys, 2 * C["q"], C["T"])
+        g = zo.combine_central(L, C["eps"])
+        if g_override is not None:
+            g = dev_f32(g_override)
+        zo.subspace_adam_update([dict(W=self.W, U=self.U, V=self.V, Z=Z, M1=self.M1, M2=self.M2)], g, t + 1,
+                                C["lr"], C["beta1"], C["beta2"], C["eps_adam"])
+        torch.cuda.synchronize()
+        return host(L), host(g)
+
+
+def f32cfg():
+    c = dict(C)
+    for k in ("eps", "lr", "beta1", "beta2", "eps_adam"):
+        c[k] = float(np.float32(c[k]))
+    return c
+
+
+def test_tiny_teacher_forced():
+    inp = zd.tiny_inputs(C["seed"])
+    recs = oracle.tiny_run(inp, omega, zdraw, f32cfg())
+    gpu = GpuTiny(inp)
+    for t, rec in enumerate(recs):
+        L, g = gpu.step(t, g_override=rec["g"].astype(np.float32))
+        Lp, Lm = L[0::2], L[1::2]
+        assert ferr(Lp, rec["Lp"], 1.0) <= 1e-5 and ferr(Lm, rec["Lm"], 1.0) <= 1e-5, t
+        # The GPU's own estimate differs from the oracle's by the fp32 cancellation noise only.
+        assert ferr(g, rec["g"], 1.0) <= 5e-2, t
+        W = host(gpu.W)
+        assert ferr(W, rec["W"], 1.0) <= 1e-5, t
+
+
+def test_tiny_free_running():
+    inp = zd.tiny_inputs(C["seed"])
+    recs = oracle.tiny_run(inp, omega, zdraw, f32cfg())
+    gpu = GpuTiny(inp)
+    for t in range(C["steps"]):
+        gpu.step(t)
+    W = host(gpu.W)
+    X = inp["X"].astype(np.float64)
+    loss = oracle.sq_loss(X @ W.T, inp["Ystar"])
+    L0 = oracle.sq_loss(X @ inp["W"].astype(np.float64).T, inp["Ystar"])
+    assert abs(loss - recs[-1]["loss"]) <= 1e-4 * recs[-1]["loss"]
+    assert ferr(W, recs[-1]["W"], 1.0) <= 1e-3
+    assert loss < L0
+
+
+def test_central_difference_exact_at_eps_one():
+    """On the quadratic loss the central difference equals <grad L, U Z V^T> exactly for any eps;
+    at eps = 1 the fp32 cancellation is small enough for a 1e-5 check of the GPU chain."""
+    inp = zd.tiny_inputs(C["seed"])
+    gpu = GpuTiny(inp)
+    ou, ov = omega(0)
+    zo.subspace_refresh([dev_f32(ou), dev_f32(ov)], C["r"], out=[gpu.U, gpu.V])
+    Zh = zdraw(0)
+    Y = zo.perturbed_linear(gpu.X, gpu.W, gpu.U, gpu.V, dev_f32(Zh), gpu.bq, gpu.bs, 1.0, C["T"], x_block_stride=0)
+    g = host(zo.combine_central(zo.sq_loss(Y, gpu.Ys, 2 * C["q"], C["T"]), 1.0))
+    U, V = host(gpu.U), host(gpu.V)
+    X, W = inp["X"].astype(np.float64), inp["W"].astype(np.float64)
+    grad = (X @ W.T - inp["Ystar"]).T @ X / C["T"]
+    exact = np.array([np.sum(grad * (U @ Zh[j].astype(np.float64) @ V.T)) for j in range(C["q"])])
+    assert ferr(g, exact, 1.0) <= 1e-5
