@@ -1,0 +1,295 @@
+#!/usr/bin/env python3
+"""Throughput of the SubZero+ hot path on one MI355X (OPT-13B-shaped stack).
+
+One step is Alg. 3 with central differences over the whole synthetic stack:
+  - subspace refresh of every U_i, V_i when t mod F == 0 (Eq. 11, Alg. 1);
+  - for every weight matrix: the perturbed linear over the 2q query blocks
+    (Eq. 4; prepare = the rank-r operands, apply = the fused GEMM);
+  - the per-block squared loss of the last matrix's outputs against a fixed
+    target and the central difference g_j (Eq. 3 per query);
+  - the subspace Adam update of every matrix (Eqs. 6-10).
+All inputs are synthetic, seeded, and resident in HBM before timing starts.
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "perturbed-linear TFLOP/s (% MFMA peak); subspace update GB/s (% HBM peak)"
+PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 4 SIMD x 1024 FLOP/clk x 2.4 GHz, dense
+PEAK_HBM_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic_opt13b.json")
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2608_15665_amd", "csrc", f) for f in ("zo_gemm.hip", "zo_internal.h")]
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def plinear_flops(T, m, n, r, q):
+    """Algorithmic FLOPs of one matrix's perturbed linear per step (all 2q blocks):
+    the X_b V projections, the q products U Z_j, the main products and the rank-r terms."""
+    return 2 * q * (2 * T * m * n + 2 * T * n * r + 2 * T * r * m) + q * 2 * m * r * r
+
+
+def apply_flops(T, m, n, r, q):
+    """Algorithmic FLOPs of the fused GEMM launch alone: X_b W^T and the rank-r term."""
+    return 2 * q * (2 * T * m * n + 2 * T * r * m)
+
+
+def update_bytes(m, n, r, q):
+    """Algorithmic HBM bytes of one matrix's update: bf16 W read + write, fp32 U and V,
+    the q fp32 Z_j, and the two fp32 moments read + write."""
+    return 4 * m * n + 4 * r * (m + n) + 4 * q * r * r + 16 * r * r
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for p in GEMM_SOURCES:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def copy_calibration():
+    """A plain device copy of known size (for scaling the FETCH_SIZE / WRITE_SIZE counters)."""
+    import torch
+    nbytes = 1 << 30
+    a = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").normal_()
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes,
+                      "launches": 3}))
+
+
+def cpu_baseline(cfg, seed, budget_s):
+    """The float64 oracle on a bounded sample of the same workload, on this host's cores."""
+    import numpy as np
+    import oracle
+    import zo_draws as zd
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    T, r, q = cfg["T"], cfg["r"], cfg["q"]
+    m, n = cfg["mats"][0][1], cfg["mats"][0][2]
+    S = 256
+    W = zd.as_bf16_values(zd.draw(seed, "W0", (m, n), (m, n), 0.02))[1]
+    X0 = zd.as_bf16_values(zd.draw(seed, "X", (T, n, 0), (S, n)))[1]
+    U, _ = np.linalg.qr(zd.draw(seed, "OMEGA_U", (0, m), (m, r)))
+    V, _ = np.linalg.qr(zd.draw(seed, "OMEGA_V", (0, n), (n, r)))
+    Z = zd.z_draws(seed, 0, 0, q, r).astype(np.float64)
+    flops = 0.0
+    nb = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s and nb < 64:
+        j, s = (nb // 2) % q, (1 if nb % 2 == 0 else -1)
+        oracle.perturbed_linear(X0, W, U, V, Z[j], s, 1e-3)
+        flops += 2 * S * m * n + 2 * S * n * r + 2 * S * r * m + 2 * m * r * r
+        nb += 1
+    dt = time.perf_counter() - t0
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 oracle (materialised W + s eps U Z V^T, then X W'^T) on {nb} query blocks "
+                      f"x {S} token rows of the {m}x{n} layer; algorithmic FLOPs of that sample / {dt:.1f} s; "
+                      f"{len(os.sched_getaffinity(0))} host cores visible"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="opt-13b", choices=["opt-1.3b", "llama-7b", "opt-13b"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scale)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the multi-GPU "
+              "path (sharding by query, one all-gather of 2q losses per step) is a design, not built.",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2608_15665_amd as zo
+    import zo_draws as zd
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    torch.cuda.set_device(0)
+    zo.lib()
+    cfg = zd.CONFIGS[args.config]
+    T, r, q = cfg["T"], cfg["r"], cfg["q"]
+    nblk = 2 * q
+    L = cfg["layers"]
+    eps, lr, b1, b2, ea, F = cfg["eps"], cfg["lr"], cfg["beta1"], cfg["beta2"], cfg["eps_adam"], cfg["F"]
+    seed = args.seed
+    dev = "cuda"
+    bf16 = torch.bfloat16
+    t_setup = time.perf_counter()
+
+    def to_bf16(a64):
+        bits = zd.bf16_bits(zd.f32(a64))
+        return torch.from_numpy(bits.view(np.int16)).view(bf16).to(dev)
+
+    # Weights: one host draw per distinct shape; layer l holds it rolled by l rows (device side).
+    shapes = sorted({(m, n) for _, m, n in cfg["mats"]})
+    Wbase = {s: to_bf16(zd.draw(seed, "W0", s, s, 0.02)) for s in shapes}
+    # Activations: one base block per distinct n; block b rolled by b*floor(T/nblk) rows.
+    ns = sorted({n for _, _, n in cfg["mats"]})
+    X = {}
+    for n in ns:
+        x0 = to_bf16(zd.draw(seed, "X", (T, n, 0), (T, n)))
+        X[n] = torch.cat([torch.roll(x0, b * (T // nblk), 0) for b in range(nblk)]).contiguous()
+        del x0
+    Y = {m: torch.empty((nblk * T, m), dtype=bf16, device=dev) for m in sorted({m for _, m, _ in cfg["mats"]})}
+    rows_set = sorted({m for _, m, _ in cfg["mats"]} | set(ns))
+    Obase = {rw: torch.from_numpy(zd.f32(zd.draw(seed, "OMEGA_U", (rw, r), (rw, r)))).to(dev) for rw in rows_set}
+    mats = []
+    for l in range(L):
+        for k, (name, m, n) in enumerate(cfg["mats"]):
+            idx = len(mats)
+            mats.append(dict(
+                name=f"{name}{l}", m=m, n=n,
+                W=torch.roll(Wbase[(m, n)], l, 0).contiguous(),
+                OU=torch.roll(Obase[m], 2 * idx, 0).contiguous(), OV=torch.roll(Obase[n], 2 * idx + 1, 0).contiguous(),
+                U=torch.empty((m, r), dtype=torch.float32, device=dev),
+                V=torch.empty((n, r), dtype=torch.float32, device=dev),
+                M1=torch.zeros((r, r), dtype=torch.float32, device=dev),
+                M2=torch.zeros((r, r), dtype=torch.float32, device=dev)))
+    del Wbase, Obase
+    nsteps = args.warmup + args.steps
+    Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(len(mats))])
+                                   for t in range(nsteps)])).to(dev)  # [step, mat, q, r, r]
+    m_last = cfg["mats"][-1][1]
+    Ystar = to_bf16(zd.draw(seed, "X", (T, m_last, 1), (T, m_last)))
+    bq = [b // 2 for b in range(nblk)]
+    bs = [1 if b % 2 == 0 else -1 for b in range(nblk)]
+    ws_need = max(zo.lib().zo_perturbed_linear_workspace(T, m, n, r, q, nblk, T * n, zo.ZO_BF16) for m, n in shapes)
+    ws = torch.empty(ws_need, dtype=torch.uint8, device=dev)
+    plins = [[zo.PerturbedLinear(X[mt["n"]], mt["W"], mt["U"], mt["V"], Z[t, i], bq, bs, eps, T,
+                                 x_block_stride=T * mt["n"], Y=Y[mt["m"]], workspace=ws)
+              for i, mt in enumerate(mats)] for t in range(nsteps)]
+    items = [[dict(W=mt["W"], U=mt["U"], V=mt["V"], Z=Z[t, i], M1=mt["M1"], M2=mt["M2"])
+              for i, mt in enumerate(mats)] for t in range(nsteps)]
+    torch.cuda.synchronize()
+    log(f"setup {time.perf_counter() - t_setup:.1f} s; {len(mats)} matrices; "
+        f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB on device")
+
+    Ev = lambda: torch.cuda.Event(enable_timing=True)
+    recs = []
+
+    def step(t, s):
+        """One SubZero+ step; s indexes the pre-drawn Z (step t of the run)."""
+        rec = {"gemm": [], "prep": [], "upd": None, "refresh": None}
+        if t % F == 0:
+            e0, e1 = Ev(), Ev()
+            e0.record()
+            zo.subspace_refresh([mt["OU"] for mt in mats] + [mt["OV"] for mt in mats], r,
+                                out=[mt["U"] for mt in mats] + [mt["V"] for mt in mats])
+            e1.record()
+            rec["refresh"] = (e0, e1)
+        for i, mt in enumerate(mats):
+            pl = plins[s][i]
+            e0, e1, e2 = Ev(), Ev(), Ev()
+            e0.record()
+            pl.prepare()
+            e1.record()
+            pl.apply()
+            e2.record()
+            rec["prep"].append((e0, e1))
+            rec["gemm"].append((e1, e2, mt["m"], mt["n"]))
+        Lb = zo.sq_loss(Y[m_last], Ystar, nblk, T)
+        g = zo.combine_central(Lb, eps)
+        e0, e1 = Ev(), Ev()
+        e0.record()
+        zo.subspace_adam_update(items[s], g, t + 1, lr, b1, b2, ea)
+        e1.record()
+        rec["upd"] = (e0, e1)
+        return rec
+
+    # Warm-up runs steps t = 0.. (t = 0 refreshes U, V); the moments are then reset and the
+    # timed steps run t = 0..K-1 again, so the timed window holds exactly one refresh.
+    for s in range(args.warmup):
+        step(s, s)
+        torch.cuda.synchronize()
+        log(f"warmup step {s} done")
+    for mt in mats:
+        mt["M1"].zero_()
+        mt["M2"].zero_()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        recs.append(step(k, args.warmup + k))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"timed {args.steps} steps in {t1 - t0:.2f} s")
+
+    step_flops = sum(plinear_flops(T, mt["m"], mt["n"], r, q) for mt in mats)
+    value = step_flops * args.steps / (t1 - t0) / 1e12
+    gemm_ms = sum(a.elapsed_time(b) for rc in recs for a, b, _, _ in rc["gemm"])
+    gemm_flops = sum(apply_flops(T, m, n, r, q) for rc in recs for _, _, m, n in rc["gemm"])
+    n_gemm = sum(len(rc["gemm"]) for rc in recs)
+    prep_ms = sum(a.elapsed_time(b) for rc in recs for a, b in rc["prep"])
+    upd_ms = sum(rc["upd"][0].elapsed_time(rc["upd"][1]) for rc in recs)
+    upd_bytes = sum(update_bytes(mt["m"], mt["n"], r, q) for mt in mats) * args.steps
+    ref_ms = [rc["refresh"][0].elapsed_time(rc["refresh"][1]) for rc in recs if rc["refresh"]]
+    per_shape = {}
+    for rc in recs:
+        for a, b, m, n in rc["gemm"]:
+            d = per_shape.setdefault(f"{m}x{n}", [0.0, 0.0, 0])
+            d[0] += a.elapsed_time(b)
+            d[1] += apply_flops(T, m, n, r, q)
+            d[2] += 1
+    achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        tr = json.load(open(TRAFFIC_FILE))
+        if tr.get("source_hash") == source_hash():
+            traffic = tr.get("bytes_per_launch")
+    upd_gbps = upd_bytes / (upd_ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round((t1 - t0) / args.steps * 1e3, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{args.config}-shaped stack: {L} layers x "
+                               + ", ".join(f"{nm} {m}x{n}" for nm, m, n in cfg["mats"])
+                               + f"; {nblk} query blocks (q={q}, +/-) of T={T} tokens; r={r}; bf16 W and X",
+                   "layers": L, "matrices": len(mats), "T": T, "r": r, "q": q, "blocks": nblk, "refresh_every": F},
+        "roofline": {"kernel": "k_gemm_bf16 (zo_perturbed_linear_apply)", "bound": "mfma",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                     "launches": n_gemm, "avg_launch_ms": round(gemm_ms / n_gemm, 4),
+                     "flops_per_launch_avg": gemm_flops / n_gemm},
+        "update": {"kernel": "zo_subspace_adam_update (k_adam_rr + k_us + k_update_bf16)", "bound": "hbm",
+                   "achieved": round(upd_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                   "frac": round(upd_gbps / PEAK_HBM_GBPS, 4), "ms_per_step": round(upd_ms / args.steps, 3)},
+        "prepare_ms_per_step": round(prep_ms / args.steps, 3),
+        "refresh_ms": round(ref_ms[0], 3) if ref_ms else None,
+        "gemm_by_shape": {k: {"tflops": round(v[1] / (v[0] * 1e-3) / 1e12, 1), "avg_ms": round(v[0] / v[2], 3)}
+                          for k, v in per_shape.items()},
+    }
+    if not args.no_cpu_baseline:
+        del plins, items, X, Y, ws
+        torch.cuda.empty_cache()
+        out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

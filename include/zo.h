@@ -123,10 +123,12 @@ int zo_subspace_refresh(int count, const zo_panel* panels, int r, int* info,
  *   blk_sign     host, nblk int8 in {+1, -1, 0}.
  *   Y            device, nblk blocks of T x m, contiguous; out_dtype ZO_BF16
  *                or ZO_F32 (fp32 inputs require fp32 output).
- * Arithmetic: bf16 inputs use bf16 MFMA with fp32 accumulation; the rank-r
- * term uses bf16 operands (X_b V and s eps U Z_j rounded to bf16) added into
- * the same accumulator; outputs rounded to nearest even.  fp32 inputs use
- * fp32 FMA throughout.
+ * Arithmetic: bf16 inputs use bf16 MFMA with fp32 accumulation.  The rank-r
+ * term is added into the same accumulators with its operands X_b V and
+ * s eps U Z_j each carried as a high + low pair of bf16 (about 16
+ * significant bits; X_b V itself formed from the same split of V), so it is
+ * ~2^-16 accurate relative to its own size.  Outputs rounded to nearest
+ * even.  fp32 inputs use fp32 FMA throughout.
  * Limits: 1 <= r <= ZO_MAX_RANK, 1 <= q <= ZO_MAX_QUERIES, 1 <= nblk <=
  * ZO_MAX_BLOCKS; bf16 inputs need m % 8 == 0 and n % 8 == 0.
  * ------------------------------------------------------------------------ */
@@ -138,6 +140,25 @@ int zo_perturbed_linear(int T, int m, int n, int r, int q, int nblk,
                         const void* W, const float* U, const float* V,
                         const float* Z, int out_dtype, void* Y,
                         void* workspace, size_t ws_bytes, void* stream);
+
+/* The same operation in two phases (zo_perturbed_linear = prepare + apply):
+ *   prepare  forms the rank-r operands X_b V and s_b eps U Z_{j(b)} in the
+ *            workspace (small launches; reads X once);
+ *   apply    one GEMM launch: Y_b = X_b W^T plus the prepared rank-r term.
+ * apply must be given the same dimensions, X and workspace as the prepare
+ * it follows on the same stream, with the workspace untouched in between.
+ * Arguments, limits and errors as for zo_perturbed_linear. */
+int zo_perturbed_linear_prepare(int T, int m, int n, int r, int q, int nblk,
+                                const int* blk_query, const int8_t* blk_sign,
+                                float eps, int in_dtype, const void* X,
+                                long long x_block_stride, const float* U,
+                                const float* V, const float* Z, void* workspace,
+                                size_t ws_bytes, void* stream);
+int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk,
+                              int in_dtype, const void* X,
+                              long long x_block_stride, const void* W,
+                              int out_dtype, void* Y, void* workspace,
+                              size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Subspace Adam update -- Eqs. 6-10 and the tail of Alg. 3.

@@ -9,9 +9,9 @@ of include/zo.h); this package only binds it.  Entry points:
     sq_loss, combine_central   loss helpers for a one-layer regression model
 """
 from ._lib import (ZO_BF16, ZO_F32, ZO_MAX_BLOCKS, ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH,
-                   Workspace, ZoError, abi_version, combine_central, lib, perturbed_linear, sq_loss,
+                   PerturbedLinear, Workspace, ZoError, abi_version, combine_central, lib, perturbed_linear, sq_loss,
                    subspace_adam_update, subspace_refresh)
 
 __all__ = ["ZO_BF16", "ZO_F32", "ZO_MAX_BLOCKS", "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH",
-           "Workspace", "ZoError", "abi_version", "combine_central", "lib", "perturbed_linear", "sq_loss",
+           "PerturbedLinear", "Workspace", "ZoError", "abi_version", "combine_central", "lib", "perturbed_linear", "sq_loss",
            "subspace_adam_update", "subspace_refresh"]

@@ -29,6 +29,7 @@ ABI_SYMBOLS = (
     "zo_abi_version", "zo_status_str", "zo_last_error_detail",
     "zo_subspace_refresh_workspace", "zo_subspace_refresh",
     "zo_perturbed_linear_workspace", "zo_perturbed_linear",
+    "zo_perturbed_linear_prepare", "zo_perturbed_linear_apply",
     "zo_subspace_adam_update_workspace", "zo_subspace_adam_update",
     "zo_sq_loss_workspace", "zo_sq_loss", "zo_combine_central",
 )
@@ -84,6 +85,13 @@ def lib() -> ctypes.CDLL:
             L.zo_perturbed_linear.argtypes = ([c_int] * 6 + [ctypes.POINTER(ctypes.c_int),
                                                ctypes.POINTER(ctypes.c_int8), c_f, c_int, c_vp, c_ll,
                                                c_vp, c_vp, c_vp, c_vp, c_int, c_vp, c_vp, c_sz, c_vp])
+            L.zo_perturbed_linear_prepare.restype = c_int
+            L.zo_perturbed_linear_prepare.argtypes = ([c_int] * 6 + [ctypes.POINTER(ctypes.c_int),
+                                                       ctypes.POINTER(ctypes.c_int8), c_f, c_int, c_vp,
+                                                       c_ll, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp])
+            L.zo_perturbed_linear_apply.restype = c_int
+            L.zo_perturbed_linear_apply.argtypes = [c_int] * 7 + [c_vp, c_ll, c_vp, c_int, c_vp, c_vp, c_sz,
+                                                                  c_vp]
             L.zo_subspace_adam_update_workspace.restype = c_sz
             L.zo_subspace_adam_update_workspace.argtypes = [c_int, ctypes.POINTER(UpdateItem), c_int,
                                                             c_int, c_int]
@@ -185,6 +193,73 @@ def subspace_refresh(omegas: Sequence[torch.Tensor], r: int, out: Optional[Seque
     return out
 
 
+class PerturbedLinear:
+    """One perturbed-linear problem (shapes, blocks, eps) with its arguments checked once.
+
+    __call__ runs prepare + apply; prepare()/apply() run the two phases
+    separately (same workspace, same stream, in that order).
+    """
+
+    def __init__(self, X: torch.Tensor, W: torch.Tensor, U: torch.Tensor, V: torch.Tensor, Z: torch.Tensor,
+                 blk_query: Sequence[int], blk_sign: Sequence[int], eps: float, T: int,
+                 x_block_stride: Optional[int] = None, out_dtype=None, Y: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None):
+        nblk = len(blk_query)
+        if len(blk_sign) != nblk:
+            raise ValueError("blk_query and blk_sign differ in length")
+        m, n = W.shape
+        r = U.shape[1]
+        q = Z.shape[0]
+        dt = W.dtype
+        if dt not in _DT:
+            raise TypeError(f"unsupported dtype {dt}")
+        _need(W, "W", dt)
+        _need(X, "X", dt)
+        if x_block_stride is None:
+            x_block_stride = 0 if X.numel() == T * n else T * n
+        if X.numel() < (T * n if x_block_stride == 0 else x_block_stride * (nblk - 1) + T * n):
+            raise ValueError("X is too small for the block layout")
+        _need(U, "U", torch.float32, m * r)
+        _need(V, "V", torch.float32, n * r)
+        _need(Z, "Z", torch.float32, q * r * r)
+        out_dtype = dt if out_dtype is None else out_dtype
+        if Y is None:
+            Y = torch.empty((nblk * T, m), dtype=out_dtype, device=W.device)
+        _need(Y, "Y", out_dtype, nblk * T * m)
+        self.dims = (T, m, n, r, q, nblk)
+        self.bq = (ctypes.c_int * nblk)(*[int(v) for v in blk_query])
+        self.bs = (ctypes.c_int8 * nblk)(*[int(v) for v in blk_sign])
+        self.eps = float(eps)
+        self.dt, self.odt = _DT[dt], _DT[out_dtype]
+        self.xs = int(x_block_stride)
+        self.X, self.W, self.U, self.V, self.Z, self.Y = X, W, U, V, Z, Y
+        need = lib().zo_perturbed_linear_workspace(T, m, n, r, q, nblk, self.xs, self.dt)
+        if workspace is None:
+            workspace = Workspace.get(need)
+        _need(workspace, "workspace", torch.uint8)
+        if workspace.numel() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, {need} needed")
+        self.ws = workspace
+
+    def prepare(self):
+        _check(lib().zo_perturbed_linear_prepare(*self.dims, self.bq, self.bs, self.eps, self.dt, self.X.data_ptr(),
+                                                 self.xs, self.U.data_ptr(), self.V.data_ptr(), self.Z.data_ptr(),
+                                                 self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
+
+    def apply(self):
+        _check(lib().zo_perturbed_linear_apply(*self.dims, self.dt, self.X.data_ptr(), self.xs, self.W.data_ptr(),
+                                               self.odt, self.Y.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+                                               _stream_handle()))
+        return self.Y
+
+    def __call__(self):
+        _check(lib().zo_perturbed_linear(*self.dims, self.bq, self.bs, self.eps, self.dt, self.X.data_ptr(), self.xs,
+                                         self.W.data_ptr(), self.U.data_ptr(), self.V.data_ptr(), self.Z.data_ptr(),
+                                         self.odt, self.Y.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+                                         _stream_handle()))
+        return self.Y
+
+
 def perturbed_linear(X: torch.Tensor, W: torch.Tensor, U: torch.Tensor, V: torch.Tensor, Z: torch.Tensor,
                      blk_query: Sequence[int], blk_sign: Sequence[int], eps: float, T: int,
                      x_block_stride: Optional[int] = None, out_dtype=None, Y: Optional[torch.Tensor] = None):
@@ -193,37 +268,7 @@ def perturbed_linear(X: torch.Tensor, W: torch.Tensor, U: torch.Tensor, V: torch
     X holds the stacked blocks (nblk*T x n), or a single T x n block shared by
     all blocks (x_block_stride = 0).  Returns Y (nblk*T x m).
     """
-    nblk = len(blk_query)
-    if len(blk_sign) != nblk:
-        raise ValueError("blk_query and blk_sign differ in length")
-    m, n = W.shape
-    r = U.shape[1]
-    q = Z.shape[0]
-    dt = W.dtype
-    if dt not in _DT:
-        raise TypeError(f"unsupported dtype {dt}")
-    _need(W, "W", dt)
-    _need(X, "X", dt)
-    if x_block_stride is None:
-        x_block_stride = 0 if X.numel() == T * n else T * n
-    if X.numel() < (T * n if x_block_stride == 0 else x_block_stride * (nblk - 1) + T * n):
-        raise ValueError("X is too small for the block layout")
-    _need(U, "U", torch.float32, m * r)
-    _need(V, "V", torch.float32, n * r)
-    _need(Z, "Z", torch.float32, q * r * r)
-    out_dtype = dt if out_dtype is None else out_dtype
-    if Y is None:
-        Y = torch.empty((nblk * T, m), dtype=out_dtype, device=W.device)
-    _need(Y, "Y", out_dtype, nblk * T * m)
-    bq = (ctypes.c_int * nblk)(*[int(v) for v in blk_query])
-    bs = (ctypes.c_int8 * nblk)(*[int(v) for v in blk_sign])
-    L = lib()
-    ws_n = L.zo_perturbed_linear_workspace(T, m, n, r, q, nblk, x_block_stride, _DT[dt])
-    ws = Workspace.get(ws_n)
-    _check(L.zo_perturbed_linear(T, m, n, r, q, nblk, bq, bs, float(eps), _DT[dt], X.data_ptr(),
-                                 x_block_stride, W.data_ptr(), U.data_ptr(), V.data_ptr(), Z.data_ptr(),
-                                 _DT[out_dtype], Y.data_ptr(), ws.data_ptr(), ws.numel(), _stream_handle()))
-    return Y
+    return PerturbedLinear(X, W, U, V, Z, blk_query, blk_sign, eps, T, x_block_stride, out_dtype, Y)()
 
 
 def subspace_adam_update(items: Sequence[dict], g: torch.Tensor, t: int, lr: float, beta1: float,

@@ -127,13 +127,32 @@ size_t zo_perturbed_linear_workspace(int T, int m, int n, int r, int q, int nblk
   return p.ws_total;
 }
 
-int zo_perturbed_linear(int T, int m, int n, int r, int q, int nblk, const int* blk_query,
-                        const int8_t* blk_sign, float eps, int in_dtype, const void* X,
-                        long long x_block_stride, const void* W, const float* U, const float* V,
-                        const float* Z, int out_dtype, void* Y, void* workspace, size_t ws_bytes,
-                        void* stream) {
-  int st = check_plinear(T, m, n, r, q, nblk, x_block_stride, in_dtype);
+static int check_plinear_call(int T, int m, int n, int r, int q, int nblk, long long xs,
+                              int in_dtype, int out_dtype, const void* X, const void* W,
+                              const void* Y, void* workspace, size_t ws_bytes, PlinearPlan* p) {
+  int st = check_plinear(T, m, n, r, q, nblk, xs, in_dtype);
   if (st != ZO_OK) return st;
+  ZO_CHECK(out_dtype == ZO_F32 || out_dtype == ZO_BF16, "perturbed_linear: bad out_dtype %d",
+           out_dtype);
+  if (in_dtype == ZO_F32 && out_dtype != ZO_F32) {
+    zo_set_error("perturbed_linear: fp32 inputs need fp32 output");
+    return ZO_ERR_UNSUPPORTED;
+  }
+  ZO_CHECK(X, "perturbed_linear: NULL tensor argument (X)");
+  const size_t al = in_dtype == ZO_BF16 ? 16 : 4;
+  ZO_CHECK(aligned(X, al) && aligned(W, al) && aligned(Y, al),
+           "perturbed_linear: X, W and Y must be %zu-byte aligned", al);
+  zo_plinear_plan(p, T, m, n, r, q, nblk, xs, in_dtype, out_dtype);
+  if (ws_bytes < p->ws_total || !workspace) {
+    zo_set_error("perturbed_linear: workspace %zu bytes < required %zu", ws_bytes, p->ws_total);
+    return ZO_ERR_WORKSPACE;
+  }
+  ZO_CHECK(aligned(workspace, 256), "perturbed_linear: workspace not 256-byte aligned");
+  return ZO_OK;
+}
+
+static int check_blocks(int q, int nblk, const int* blk_query, const int8_t* blk_sign, float eps,
+                        const float* U, const float* V, const float* Z) {
   ZO_CHECK(blk_query && blk_sign, "perturbed_linear: blk_query / blk_sign is NULL");
   for (int b = 0; b < nblk; ++b) {
     ZO_CHECK(blk_query[b] >= 0 && blk_query[b] < q, "perturbed_linear: blk_query[%d] = %d outside "
@@ -142,30 +161,55 @@ int zo_perturbed_linear(int T, int m, int n, int r, int q, int nblk, const int* 
              "{-1, 0, 1}", b, (int)blk_sign[b]);
   }
   ZO_CHECK(isfinite(eps), "perturbed_linear: eps is not finite");
-  ZO_CHECK(X && W && U && V && Z && Y, "perturbed_linear: NULL tensor argument");
-  ZO_CHECK(out_dtype == ZO_F32 || out_dtype == ZO_BF16, "perturbed_linear: bad out_dtype %d",
-           out_dtype);
-  if (in_dtype == ZO_F32 && out_dtype != ZO_F32) {
-    zo_set_error("perturbed_linear: fp32 inputs need fp32 output");
-    return ZO_ERR_UNSUPPORTED;
-  }
-  if (in_dtype == ZO_BF16) {
-    ZO_CHECK(aligned(X, 16) && aligned(W, 16) && aligned(Y, 16),
-             "perturbed_linear: bf16 X, W and Y must be 16-byte aligned");
-  } else {
-    ZO_CHECK(aligned(X, 4) && aligned(W, 4) && aligned(Y, 4),
-             "perturbed_linear: fp32 tensors must be 4-byte aligned");
-  }
+  ZO_CHECK(U && V && Z, "perturbed_linear: NULL tensor argument (U, V or Z)");
   ZO_CHECK(aligned(U, 4) && aligned(V, 4) && aligned(Z, 4), "perturbed_linear: U, V, Z alignment");
+  return ZO_OK;
+}
+
+int zo_perturbed_linear(int T, int m, int n, int r, int q, int nblk, const int* blk_query,
+                        const int8_t* blk_sign, float eps, int in_dtype, const void* X,
+                        long long x_block_stride, const void* W, const float* U, const float* V,
+                        const float* Z, int out_dtype, void* Y, void* workspace, size_t ws_bytes,
+                        void* stream) {
   PlinearPlan p;
-  zo_plinear_plan(&p, T, m, n, r, q, nblk, x_block_stride, in_dtype, out_dtype);
-  if (ws_bytes < p.ws_total || !workspace) {
-    zo_set_error("perturbed_linear: workspace %zu bytes < required %zu", ws_bytes, p.ws_total);
-    return ZO_ERR_WORKSPACE;
-  }
-  ZO_CHECK(aligned(workspace, 256), "perturbed_linear: workspace not 256-byte aligned");
-  return zo_plinear_launch(p, blk_query, blk_sign, eps, X, W, U, V, Z, Y, workspace,
-                           (hipStream_t)stream);
+  int st = check_plinear(T, m, n, r, q, nblk, x_block_stride, in_dtype);
+  if (st != ZO_OK) return st;
+  if ((st = check_blocks(q, nblk, blk_query, blk_sign, eps, U, V, Z)) != ZO_OK) return st;
+  ZO_CHECK(W && Y, "perturbed_linear: NULL tensor argument (W or Y)");
+  st = check_plinear_call(T, m, n, r, q, nblk, x_block_stride, in_dtype, out_dtype, X, W, Y,
+                          workspace, ws_bytes, &p);
+  if (st != ZO_OK) return st;
+  st = zo_plinear_prepare(p, blk_query, blk_sign, eps, X, U, V, Z, workspace, (hipStream_t)stream);
+  if (st != ZO_OK) return st;
+  return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream);
+}
+
+int zo_perturbed_linear_prepare(int T, int m, int n, int r, int q, int nblk,
+                                const int* blk_query, const int8_t* blk_sign, float eps,
+                                int in_dtype, const void* X, long long x_block_stride,
+                                const float* U, const float* V, const float* Z, void* workspace,
+                                size_t ws_bytes, void* stream) {
+  PlinearPlan p;
+  int st = check_plinear(T, m, n, r, q, nblk, x_block_stride, in_dtype);
+  if (st != ZO_OK) return st;
+  if ((st = check_blocks(q, nblk, blk_query, blk_sign, eps, U, V, Z)) != ZO_OK) return st;
+  // The output dtype does not enter the prepared operands.
+  st = check_plinear_call(T, m, n, r, q, nblk, x_block_stride, in_dtype, in_dtype, X, nullptr,
+                          nullptr, workspace, ws_bytes, &p);
+  if (st != ZO_OK) return st;
+  return zo_plinear_prepare(p, blk_query, blk_sign, eps, X, U, V, Z, workspace, (hipStream_t)stream);
+}
+
+int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk, int in_dtype,
+                              const void* X, long long x_block_stride, const void* W,
+                              int out_dtype, void* Y, void* workspace, size_t ws_bytes,
+                              void* stream) {
+  PlinearPlan p;
+  ZO_CHECK(W && Y, "perturbed_linear: NULL tensor argument (W or Y)");
+  int st = check_plinear_call(T, m, n, r, q, nblk, x_block_stride, in_dtype, out_dtype, X, W, Y,
+                              workspace, ws_bytes, &p);
+  if (st != ZO_OK) return st;
+  return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ update

@@ -427,16 +427,15 @@ int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
   return ZO_OK;
 }
 
-int zo_plinear_launch(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
-                      float eps, const void* X, const void* W, const float* U, const float* V,
-                      const float* Z, void* Y, void* ws, hipStream_t stream) {
+int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
+                       float eps, const void* X, const float* U, const float* V, const float* Z,
+                       void* ws, hipStream_t stream) {
   WsCarver wc(ws);
   void* vt = wc.take(p.ws_vt);
   void* p2 = p.ws_p2 ? wc.take(p.ws_p2) : nullptr;
   void* pp = wc.take(p.ws_p);
   void* bp = wc.take(p.ws_bp);
   int st;
-
   {
     const long long total = (long long)p.rp * p.n;
     hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
@@ -470,8 +469,33 @@ int zo_plinear_launch(const PlinearPlan& p, const int* blk_query, const int8_t* 
     const long long prow = (long long)p.nx * p.T;
     hipLaunchKernelGGL(k_pcombine, dim3((unsigned)((prow * p.rp + 255) / 256)), dim3(256), 0, stream,
                        (const float*)p2, prow, p.rp, (bf16_t*)pp);
-    if ((st = zo_hip_status(hipGetLastError(), "k_pcombine")) != ZO_OK) return st;
+    return zo_hip_status(hipGetLastError(), "k_pcombine");
+  }
+  F32Args g{};
+  g.A = (const float*)vt;
+  g.B = (const float*)X;
+  g.b_block_stride = xs;
+  g.rows_a = p.rp;
+  g.rows_b = p.T;
+  g.K = p.n;
+  g.rc = 0;
+  g.Y = (float*)pp;
+  g.y_block_stride = (long long)p.T * p.rp;
+  g.ldy = p.rp;
+  dim3 grid((p.rp + 63) / 64, (p.T + 63) / 64, p.nx);
+  hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, stream, g);
+  return zo_hip_status(hipGetLastError(), "k_gemm_f32 (projection)");
+}
 
+int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
+                     hipStream_t stream) {
+  WsCarver wc(ws);
+  wc.take(p.ws_vt);
+  if (p.ws_p2) wc.take(p.ws_p2);
+  void* pp = wc.take(p.ws_p);
+  void* bp = wc.take(p.ws_bp);
+  const long long xs = p.x_block_stride;
+  if (p.in_bf16) {
     GemmArgs h{};
     h.A = (const bf16_t*)W;
     h.B = (const bf16_t*)X;
@@ -491,40 +515,22 @@ int zo_plinear_launch(const PlinearPlan& p, const int* blk_query, const int8_t* 
     h.out_bf16 = p.out_bf16;
     return launch_gemm_bf16<2, 4, 4, 2>(h, stream);
   }
-  {
-    F32Args g{};
-    g.A = (const float*)vt;
-    g.B = (const float*)X;
-    g.b_block_stride = xs;
-    g.rows_a = p.rp;
-    g.rows_b = p.T;
-    g.K = p.n;
-    g.rc = 0;
-    g.Y = (float*)pp;
-    g.y_block_stride = (long long)p.T * p.rp;
-    g.ldy = p.rp;
-    dim3 grid((p.rp + 63) / 64, (p.T + 63) / 64, p.nx);
-    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, stream, g);
-    if ((st = zo_hip_status(hipGetLastError(), "k_gemm_f32 (projection)")) != ZO_OK) return st;
-  }
-  {
-    F32Args h{};
-    h.A = (const float*)W;
-    h.B = (const float*)X;
-    h.b_block_stride = xs;
-    h.rows_a = p.m;
-    h.rows_b = p.T;
-    h.K = p.n;
-    h.ca = (const float*)bp;
-    h.ca_block_stride = (long long)p.m * p.rp;
-    h.cb = (const float*)pp;
-    h.cb_block_stride = p.nx == 1 ? 0 : (long long)p.T * p.rp;
-    h.rc = p.rp;
-    h.Y = (float*)Y;
-    h.y_block_stride = (long long)p.T * p.m;
-    h.ldy = p.m;
-    dim3 grid((p.m + 63) / 64, (p.T + 63) / 64, p.nblk);
-    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, stream, h);
-    return zo_hip_status(hipGetLastError(), "k_gemm_f32");
-  }
+  F32Args h{};
+  h.A = (const float*)W;
+  h.B = (const float*)X;
+  h.b_block_stride = xs;
+  h.rows_a = p.m;
+  h.rows_b = p.T;
+  h.K = p.n;
+  h.ca = (const float*)bp;
+  h.ca_block_stride = (long long)p.m * p.rp;
+  h.cb = (const float*)pp;
+  h.cb_block_stride = p.nx == 1 ? 0 : (long long)p.T * p.rp;
+  h.rc = p.rp;
+  h.Y = (float*)Y;
+  h.y_block_stride = (long long)p.T * p.m;
+  h.ldy = p.m;
+  dim3 grid((p.m + 63) / 64, (p.T + 63) / 64, p.nblk);
+  hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, stream, h);
+  return zo_hip_status(hipGetLastError(), "k_gemm_f32");
 }

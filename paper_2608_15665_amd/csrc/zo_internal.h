@@ -60,10 +60,11 @@ struct PlinearPlan {
 };
 int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
                     long long x_block_stride, int in_dtype, int out_dtype);
-int zo_plinear_launch(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
-                      float eps, const void* X, const void* W, const float* U,
-                      const float* V, const float* Z, void* Y, void* ws,
-                      hipStream_t stream);
+int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
+                       float eps, const void* X, const float* U, const float* V,
+                       const float* Z, void* ws, hipStream_t stream);
+int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
+                     hipStream_t stream);
 
 // Subspace Adam update (zo_update.hip).
 int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r, int q,

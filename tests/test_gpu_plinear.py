@@ -183,3 +183,16 @@ def test_opt13b_full_size_sampled(name):
         ref = run_oracle(c, 1e-3, blocks=[b], rows=rows)[0]
         assert ferr(got, ref, 1e-3) <= 1e-2, b
         assert normwise(got, ref) <= 1e-2, b
+
+
+@pytest.mark.parametrize("bf16", [True, False])
+def test_prepare_apply_equals_one_call(bf16):
+    """zo_perturbed_linear_prepare + zo_perturbed_linear_apply is the one-call result, bit for bit."""
+    c = make_case(300, 264, 200, 16, 2, 4, False, bf16=bf16)
+    one = run_gpu(c, 1e-3)
+    pl = zo.PerturbedLinear(c["Xd"], c["Wd"], c["Ud"], c["Vd"], c["Zd"], c["bq"], c["bs"], 1e-3, c["T"],
+                            x_block_stride=c["xs"])
+    pl.prepare()
+    Y = pl.apply()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(Y).reshape(one.shape), one)
