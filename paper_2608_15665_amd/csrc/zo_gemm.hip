@@ -396,6 +396,184 @@ int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
   return zo_hip_status(hipGetLastError(), "k_gemm_bf16");
 }
 
+
+// ---------------------------------------------------------------------------
+// Main GEMM for K % 32 == 0: the kernel every model-shaped call takes.
+//
+// 256 x 256 output tile per workgroup of 4 waves (one per SIMD), each wave a
+// 128 x 128 sub-tile held in 16 accumulators of the 32x32x16 MFMA (256 AGPRs).
+// K is walked in tiles of 32 (64-byte LDS rows) through a 4-stage LDS ring
+// filled by direct global->LDS loads (global_load_lds_dwordx4: 16 rows x 64 B
+// per instruction, 8 per wave per tile).  Row r of a tile keeps its 16-byte
+// chunk c at position c ^ g(r), g(r) = ((r >> 2) ^ (r & 2)) & 3, which makes the
+// fragment reads conflict free for 8- and 16-lane LDS passes.
+//
+// One barrier per k-tile, in its middle: before it each wave has waited for
+// its own loads of tile kt+1; after it, tile kt+3 is issued into the stage
+// tile kt-1 used (read by everyone before this barrier) and the first
+// fragments of tile kt+1 are read while the second half of tile kt's MFMAs
+// run.  The loop body has no branches (the tail re-issues the last tile into
+// a free stage), so the instruction scheduler interleaves MFMAs with LDS reads
+// and DMA issues as requested by the sched_group_barrier sequence.
+//
+// The rank-rc correction is rc/32 more k-tiles through the same pipeline,
+// with the A operand taken from ca (per block, rows_a x rc) and the B operand
+// from cb (per block, rows_b x rc).  Rows past rows_a / rows_b are loaded
+// from the last valid row (never stored).
+__device__ __forceinline__ int g4(int r) { return ((r >> 2) ^ (r & 2)) & 3; }
+
+__global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
+  constexpr int STAGES = 4;
+  constexpr int BM = 256, BN = 256, RB = 64;               // RB: bytes per LDS row (32 bf16)
+  constexpr int TILE_BYTES = (BM + BN) * RB;                // 32 KB per stage
+  __shared__ __attribute__((aligned(1024))) char lds[STAGES * TILE_BYTES];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+
+  const int w = blockIdx.x;
+  const int nt = a.total_tiles;
+  const int xcd = w & 7, widx = w >> 3;
+  const int lt = xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
+  constexpr int GROUP = 8;
+  const int total_bt = a.nblk * a.tiles_b;
+  const int per_group = GROUP * a.tiles_a;
+  const int grp = lt / per_group;
+  const int first = grp * GROUP;
+  const int gsize = min(GROUP, total_bt - first);
+  const int rem = lt - grp * per_group;
+  const int bt = first + rem % gsize;
+  const int at = rem / gsize;
+  const int blk = bt / a.tiles_b;
+  const int t0 = (bt % a.tiles_b) * BN;
+  const int m0 = at * BM;
+
+  const int NKM = a.K / 32;
+  const int NTK = NKM + a.rc / 32;
+  const bf16_t* Bblk = a.B + (long long)blk * a.b_block_stride;
+  const bf16_t* Cblk = a.ca + (long long)blk * a.ca_block_stride;
+  const bf16_t* Dblk = a.cb + (long long)blk * a.cb_block_stride;
+  // DMA lane mapping: row 16 (wave + 4 i) + lane/4, physical chunk lane%4.
+  const int dr = lane >> 2;
+  const int dkc = (lane & 3) ^ g4(dr);
+  int ra[4], rb[4];  // clamped source rows of this lane's four A and four B loads
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 16 * (wave + 4 * i) + dr;
+    ra[i] = min(m0 + row, a.rows_a - 1);
+    rb[i] = min(t0 + row, a.rows_b - 1);
+  }
+  auto issue = [&](int kt) {
+    char* st = lds + (kt % STAGES) * TILE_BYTES + 16 * wave * RB;
+    const bool main = kt < NKM;
+    const bf16_t* baseA = main ? a.A : Cblk;
+    const bf16_t* baseB = main ? Bblk : Dblk;
+    const int ld = main ? a.K : a.rc;
+    const int ko = (main ? kt : kt - NKM) * 32 + dkc * 8;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(baseA + (size_t)ra[i] * ld + ko),
+                                       (lds_ptr_t)(st + 64 * i * RB), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(baseB + (size_t)rb[i] * ld + ko),
+                                       (lds_ptr_t)(st + BM * RB + 64 * i * RB), 16, 0, 0);
+  };
+  const int fr = lane & 31, fh = lane >> 5;
+  const int fg = g4(fr);
+  const int offA = (wm * 128 + fr) * RB, offB = BM * RB + (wn * 128 + fr) * RB;
+  auto frags = [&](int kt, int s, bf16x8* fa, bf16x8* fb) {
+    const char* st = lds + (kt % STAGES) * TILE_BYTES;
+    const int ch = ((2 * s + fh) ^ fg) * 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) fa[i] = *(const bf16x8*)(st + offA + i * 32 * RB + ch);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)(st + offB + j * 32 * RB + ch);
+  };
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
+
+  issue(0);
+  issue(min(1, NTK - 1));
+  issue(min(2, NTK - 1));
+  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");  // tile 0 of this wave landed
+  __syncthreads();                                    // ... and of every wave
+  bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
+  frags(0, 0, f0a, f0b);
+  for (int kt = 0; kt < NTK; ++kt) {
+    frags(kt, 1, f1a, f1b);
+    mma(f0a, f0b);
+    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // this wave's loads of tile kt+1 landed
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");                      // no memory access moves across
+    issue(min(kt + 3, NTK - 1));
+    frags(kt + 1, 0, f0a, f0b);
+    mma(f1a, f1b);
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 global->LDS load
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain the tail loads before exit
+
+  char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (a.out_bf16 ? 2 : 4);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int tok = t0 + wn * 128 + j * 32 + fr;
+    if (tok >= a.rows_b) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int col = m0 + wm * 128 + i * 32 + q4 * 8 + fh * 4;
+        if (col >= a.rows_a) continue;
+        const float v0 = acc[i][j][q4 * 4 + 0], v1 = acc[i][j][q4 * 4 + 1];
+        const float v2 = acc[i][j][q4 * 4 + 2], v3 = acc[i][j][q4 * 4 + 3];
+        if (a.out_bf16) {
+          u32x2 pk = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+          *(u32x2*)(Yb + ((size_t)tok * a.ldy + col) * 2) = pk;
+        } else {
+          f32x4 pk = {v0, v1, v2, v3};
+          *(f32x4*)(Yb + ((size_t)tok * a.ldy + col) * 4) = pk;
+        }
+      }
+    }
+  }
+}
+
+int launch_gemm_main(GemmArgs a, hipStream_t stream) {
+  a.tiles_a = (a.rows_a + 255) / 256;
+  a.tiles_b = (a.rows_b + 255) / 256;
+  const long long total = (long long)a.tiles_a * a.tiles_b * a.nblk;
+  if (total <= 0) return ZO_OK;
+  if (total > 0x7fffffffLL) {
+    zo_set_error("perturbed linear: too many tiles (%lld)", total);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  a.total_tiles = (int)total;
+  hipLaunchKernelGGL(k_gemm_main, dim3(a.total_tiles), dim3(256), 0, stream, a);
+  return zo_hip_status(hipGetLastError(), "k_gemm_main");
+}
+
 }  // namespace
 
 int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
@@ -404,7 +582,8 @@ int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
   p->m = m;
   p->n = n;
   p->r = r;
-  p->rp = (r + 15) / 16 * 16;
+  // bf16: a multiple of 32 so the 3 rp-deep rank-r segment is whole 32-wide k-tiles.
+  p->rp = in_dtype == ZO_BF16 ? (r + 31) / 32 * 32 : (r + 15) / 16 * 16;
   p->q = q;
   p->nblk = nblk;
   p->x_block_stride = x_block_stride;
@@ -513,6 +692,7 @@ int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y
     h.y_block_stride = (long long)p.T * p.m;
     h.ldy = p.m;
     h.out_bf16 = p.out_bf16;
+    if (p.n % 32 == 0) return launch_gemm_main(h, stream);
     return launch_gemm_bf16<2, 4, 4, 2>(h, stream);
   }
   F32Args h{};
