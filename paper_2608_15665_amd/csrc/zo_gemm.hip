@@ -409,12 +409,14 @@ int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
 // fragment reads conflict free for 8- and 16-lane LDS passes.
 //
 // One barrier per k-tile, in its middle: before it each wave has waited for
-// its own loads of tile kt+1; after it, tile kt+3 is issued into the stage
-// tile kt-1 used (read by everyone before this barrier) and the first
-// fragments of tile kt+1 are read while the second half of tile kt's MFMAs
-// run.  The loop body has no branches (the tail re-issues the last tile into
-// a free stage), so the instruction scheduler interleaves MFMAs with LDS reads
-// and DMA issues as requested by the sched_group_barrier sequence.
+// its own loads of tile kt+1 and its own reads of tile kt; after it, the
+// loads of tile kt+4 start into tile kt's stage (half right away, half in the
+// next iteration's first half, so load issue is spread over the loop) and
+// the first fragments of tile kt+1 are read while the second half of tile
+// kt's MFMAs run.  Loads therefore have three iterations to land.  The tail
+// re-issues the last tile into its own stage (identical bytes), which keeps
+// the loop body free of data-dependent branches so the instruction scheduler
+// follows the sched_group_barrier interleave of MFMAs, LDS reads and loads.
 //
 // The rank-rc correction is rc/32 more k-tiles through the same pipeline,
 // with the A operand taken from ca (per block, rows_a x rc) and the B operand
@@ -463,21 +465,19 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     ra[i] = min(m0 + row, a.rows_a - 1);
     rb[i] = min(t0 + row, a.rows_b - 1);
   }
-  auto issue = [&](int kt) {
-    char* st = lds + (kt % STAGES) * TILE_BYTES + 16 * wave * RB;
+  // One half of a tile's loads: part 0 the A rows (W, or the rank-r operand of W's side),
+  // part 1 the B rows (X, or the rank-r operand of X's side); 4 loads per lane each.
+  auto issue_part = [&](int kt, int part) {
+    char* st = lds + (kt % STAGES) * TILE_BYTES + 16 * wave * RB + part * BM * RB;
     const bool main = kt < NKM;
-    const bf16_t* baseA = main ? a.A : Cblk;
-    const bf16_t* baseB = main ? Bblk : Dblk;
+    const bf16_t* base = part ? (main ? Bblk : Dblk) : (main ? a.A : Cblk);
+    const int* rr = part ? rb : ra;
     const int ld = main ? a.K : a.rc;
     const int ko = (main ? kt : kt - NKM) * 32 + dkc * 8;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(baseA + (size_t)ra[i] * ld + ko),
+      __builtin_amdgcn_global_load_lds((const void*)(base + (size_t)rr[i] * ld + ko),
                                        (lds_ptr_t)(st + 64 * i * RB), 16, 0, 0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(baseB + (size_t)rb[i] * ld + ko),
-                                       (lds_ptr_t)(st + BM * RB + 64 * i * RB), 16, 0, 0);
   };
   const int fr = lane & 31, fh = lane >> 5;
   const int fg = g4(fr);
@@ -505,33 +505,42 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
 
-  issue(0);
-  issue(min(1, NTK - 1));
-  issue(min(2, NTK - 1));
-  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");  // tile 0 of this wave landed
-  __syncthreads();                                    // ... and of every wave
+  // Prologue: tiles 0..3 issued in full; wait for tile 0.
+  for (int t = 0; t < 4; ++t) {
+    issue_part(min(t, NTK - 1), 0);
+    issue_part(min(t, NTK - 1), 1);
+  }
+  asm volatile("s_waitcnt vmcnt(24)" ::: "memory");  // this wave's loads of tile 0 landed
+  __syncthreads();                                    // ... and every wave's
   bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
   frags(0, 0, f0a, f0b);
+  // Tile kt+4 reuses tile kt's stage: its part 0 is issued right after barrier(kt) (every wave
+  // has finished reading tile kt: each waits for its own reads before the barrier), its part 1
+  // in the first half of iteration kt+1.  So at barrier(kt) the loads outstanding are, in issue
+  // order, tile kt+1, kt+2, kt+3 (8 each): waiting down to 16 leaves tile kt+1 complete.
   for (int kt = 0; kt < NTK; ++kt) {
     frags(kt, 1, f1a, f1b);
+    if (kt >= 1) issue_part(min(kt + 3, NTK - 1), 1);
     mma(f0a, f0b);
-    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // this wave's loads of tile kt+1 landed
+    for (int i = 0; i < 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // 2 LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 global->LDS load
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");                      // no memory access moves across
-    issue(min(kt + 3, NTK - 1));
+    issue_part(min(kt + 4, NTK - 1), 0);
     frags(kt + 1, 0, f0a, f0b);
     mma(f1a, f1b);
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+    for (int i = 0; i < 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 global->LDS load
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // 2 LDS reads
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 12, 0);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain the tail loads before exit
 
