@@ -1,54 +1,68 @@
 // Subspace Adam update of SubZero+ (Eqs. 6-10, tail of Alg. 3).
 //
 // Three launches per chunk of up to ITEMS_PER_LAUNCH matrices:
-//   k_adam_rr   one workgroup per matrix: Zbar = (1/q) sum_j g_j Z_j, the two
-//               r x r moments (Eqs. 7-8), the bias-corrected direction S
-//               (Eq. 9, Adam form), all in float64; writes M1, M2 (fp32) and
-//               S (float64, workspace) -- or, if any entry is non-finite,
-//               leaves the state alone, raises the flag and marks the item
-//               skipped.
-//   k_us        L = lr U S (m x rp) and V (n x rp), zero padded to rp columns.
-//               bf16 W: each as a hi + lo pair of bf16 (x = hi + lo to about
-//               16 significant bits); fp32 W: L in fp32.
+//   k_adam_rr   256 entries of one matrix per workgroup: Zbar = (1/q) sum_j g_j Z_j,
+//               the two r x r moments (Eqs. 7-8) and the bias-corrected direction S
+//               (Eq. 9, Adam form), all in float64.  S and the new moments go to
+//               the workspace with one non-finite flag per workgroup; Zbar goes
+//               to zbar_out.
+//   k_us        Reads the item's flags: if any entry was non-finite the item is
+//               skipped (state untouched).  Otherwise commits the new moments and
+//               forms L = lr U S (m x rp; tiles of 128 rows, register-blocked fp32
+//               FMA) and, for bf16 W, the hi/lo split of V (n x rp); padding
+//               columns are zero.  bf16 W: L and V as hi + lo bf16 pairs (x = hi + lo
+//               to about 16 significant bits); fp32 W: L in fp32, V read as is.
 //   k_update_*  W <- W - L V^T in place.
 //
 // bf16 W (k_update_bf16): memory bound -- 4 bytes of HBM traffic per weight
 // against 2 r MACs.  At r = 64 that is 32 FLOP/B, above the fp32 VALU ridge
 // of the chip, so the rank-r product runs on v_mfma_f32_16x16x32_bf16 as
-// hi*hi + hi*lo + lo*hi (3 MFMAs per 32-deep K step).  Each wave owns a strip
-// of 64 columns whose V fragments stay in registers, and walks down rows 16
-// at a time.  The A operand rows are the strip's columns in a permuted order
-// so that the 16 accumulator values a lane ends with are 16 ADJACENT columns
-// of one row: the lane reads and writes its W values as two 16-byte vectors.
+// hi*hi + lo*hi + hi*lo (3 MFMAs per 32-deep K step).  Each wave owns a strip
+// of 64 columns whose V fragments stay in registers and walks its rows 16 at a
+// time; the L rows are staged once per workgroup in LDS.
+//
+// Every W, L and V access of k_update_bf16 is a buffer instruction whose
+// descriptor covers exactly the workgroup's rows: rows past the edge and
+// columns past n (given an out-of-range offset) read as zero and drop their
+// stores in hardware, so the loop has no branches around memory operations
+// and the compiler can count the loads in flight exactly.  W is read NS steps
+// ahead and the next L chunk one chunk ahead.
 #include "zo_internal.h"
 
 namespace {
 
 constexpr int ITEMS_PER_LAUNCH = 16;
-constexpr int UPD_ROWS = 128;  // rows per workgroup (8 steps of 16 per wave)
+constexpr int UPD_ROWS = 512;  // rows per workgroup
 constexpr int UPD_COLS = 256;  // columns per workgroup (4 waves x 64)
+constexpr int US_ROWS = 128;   // rows of L per k_us workgroup
+constexpr unsigned OOB = 0x80000000u;  // buffer offset beyond every descriptor used here
+constexpr int RSRC_CFG = 0x00020000;   // buffer descriptor word 3: 32-bit raw access
 
 struct ItemRR {
   const float* Z;
-  float* M1;
-  float* M2;
+  const float* M1;
+  const float* M2;
   float* zbar_out;
-  double* S;  // workspace, r x r
-  int* skip;  // workspace
+  double* S;    // workspace, r x r
+  float* M1n;   // workspace, r x r
+  float* M2n;   // workspace, r x r
+  int* flags;   // workspace, one per workgroup of the item
 };
 struct RRArgs {
   ItemRR it[ITEMS_PER_LAUNCH];
   const float* g;
   int* nonfinite_flag;
-  int r, q;
+  int r, q, aw;  // aw: workgroups per item
   double beta1, beta2, eps_adam, bc1, bc2;
 };
 
 __global__ __launch_bounds__(256) void k_adam_rr(RRArgs a) {
-  const ItemRR& it = a.it[blockIdx.x];
+  const ItemRR& it = a.it[blockIdx.x / a.aw];
+  const int w = blockIdx.x % a.aw;
   const int rr = a.r * a.r;
+  const int e = w * 256 + threadIdx.x;
   int bad = 0;
-  for (int e = threadIdx.x; e < rr; e += 256) {
+  if (e < rr) {
     double zb = 0.0;
     for (int j = 0; j < a.q; ++j) zb += (double)a.g[j] * (double)it.Z[(size_t)j * rr + e];
     zb /= (double)a.q;
@@ -57,81 +71,147 @@ __global__ __launch_bounds__(256) void k_adam_rr(RRArgs a) {
     const double s = (m1 / a.bc1) / (sqrt(m2 / a.bc2) + a.eps_adam);
     if (!isfinite(zb) || !isfinite(s)) bad = 1;
     if (it.zbar_out) it.zbar_out[e] = (float)zb;
+    it.S[e] = s;
+    it.M1n[e] = (float)m1;
+    it.M2n[e] = (float)m2;
   }
   bad = __syncthreads_or(bad);
-  if (bad) {
-    if (threadIdx.x == 0) {
-      *it.skip = 1;
-      if (a.nonfinite_flag) *a.nonfinite_flag = 1;
-    }
-    return;
+  if (threadIdx.x == 0) {
+    it.flags[w] = bad;
+    if (bad && a.nonfinite_flag) *a.nonfinite_flag = 1;
   }
-  // Second pass writes the state, recomputed identically.  Element e is read
-  // and written by the same thread only, so no barrier is needed.
-  for (int e = threadIdx.x; e < rr; e += 256) {
-    double zb = 0.0;
-    for (int j = 0; j < a.q; ++j) zb += (double)a.g[j] * (double)it.Z[(size_t)j * rr + e];
-    zb /= (double)a.q;
-    const double m1 = a.beta1 * (double)it.M1[e] + (1.0 - a.beta1) * zb;
-    const double m2 = a.beta2 * (double)it.M2[e] + (1.0 - a.beta2) * zb * zb;
-    it.S[e] = (m1 / a.bc1) / (sqrt(m2 / a.bc2) + a.eps_adam);
-    it.M1[e] = (float)m1;
-    it.M2[e] = (float)m2;
-  }
-  if (threadIdx.x == 0) *it.skip = 0;
 }
 
 struct ItemUS {
   const float* U;
   const float* V;
   const double* S;
-  const int* skip;
-  void* L;   // bf16: hi then lo (2 x m x rp); fp32: m x rp
+  const float* M1n;
+  const float* M2n;
+  float* M1;
+  float* M2;
+  const int* flags;
+  int* skip;
+  void* L;   // bf16: m rows of [hi (rp) | lo (rp)]; fp32: m x rp
   void* Vs;  // bf16: hi then lo (2 x n x rp); unused for fp32
   int m, n;
-  long long begin;  // first flat index of this item in the launch
+  int wg_begin;  // first workgroup of this item in the launch
+  int l_tiles;   // workgroups forming L (US_ROWS rows each); then V tiles (64 rows each)
+  int n_wg;      // all workgroups of the item
 };
 struct USArgs {
   ItemUS it[ITEMS_PER_LAUNCH];
-  int count, r, rp, bf16;
+  int count, r, rp, bf16, aw;
   float lr;
-  long long total;
 };
 
+// L = lr U S for rows i0 .. i0+127 of one item: 32 columns of K at a time, U
+// (transposed) and S staged in LDS as fp32; each thread owns 4 rows x rp/8
+// adjacent columns.  Or the hi/lo split of 64 rows of V.
+template <int RPK>
 __global__ __launch_bounds__(256) void k_us(USArgs a) {
-  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= a.total) return;
+  constexpr int RP = 32 * RPK;
+  constexpr int CPT = RP / 8;  // columns per thread
+  __shared__ __attribute__((aligned(16))) float Ut[32][US_ROWS + 4];
+  __shared__ __attribute__((aligned(16))) float Sl[32][RP];
   int k = 0;
-  while (k + 1 < a.count && idx >= a.it[k + 1].begin) ++k;
+  while (k + 1 < a.count && (int)blockIdx.x >= a.it[k + 1].wg_begin) ++k;
   const ItemUS& it = a.it[k];
-  if (*it.skip) return;
-  const long long e = idx - it.begin;
-  const long long nl = (long long)it.m * a.rp;
-  if (e < nl) {
-    const int i = (int)(e / a.rp), c = (int)(e % a.rp);
-    float v = 0.f;
-    if (c < a.r) {
-      double acc = 0.0;
-      for (int t = 0; t < a.r; ++t) acc += (double)it.U[(size_t)i * a.r + t] * it.S[t * a.r + c];
-      v = (float)((double)a.lr * acc);
+  const int local = blockIdx.x - it.wg_begin;
+  const int r = a.r, tid = threadIdx.x;
+  int bad = 0;
+  for (int w = tid; w < a.aw; w += 256) bad |= it.flags[w];
+  bad = __syncthreads_or(bad);
+  if (local == 0 && tid == 0) *it.skip = bad;
+  if (bad) return;
+  const int rr = r * r;
+  for (int e = local * 256 + tid; e < rr; e += it.n_wg * 256) {
+    it.M1[e] = it.M1n[e];
+    it.M2[e] = it.M2n[e];
+  }
+  if (local < it.l_tiles) {
+    const int i0 = local * US_ROWS;
+    const int tr = tid >> 3, tc = tid & 7;
+    float acc[4][CPT];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+      for (int y = 0; y < CPT; ++y) acc[x][y] = 0.f;
+    for (int kc = 0; kc < RPK; ++kc) {
+      if (kc) __syncthreads();
+      for (int x = tid; x < 32 * US_ROWS; x += 256) {
+        const int i = x >> 5, kk = x & 31, t = kc * 32 + kk;
+        Ut[kk][i] = (i0 + i < it.m && t < r) ? it.U[(size_t)(i0 + i) * r + t] : 0.f;
+      }
+      for (int x = tid; x < 32 * RP; x += 256) {
+        const int kk = x / RP, c = x % RP, t = kc * 32 + kk;
+        Sl[kk][c] = (t < r && c < r) ? (float)it.S[t * r + c] : 0.f;
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int kk = 0; kk < 32; ++kk) {
+        const f32x4 u = *(const f32x4*)&Ut[kk][tr * 4];
+        float s[CPT];
+#pragma unroll
+        for (int y = 0; y < CPT; y += 4) {
+          const f32x4 sv = *(const f32x4*)&Sl[kk][tc * CPT + y];
+          s[y] = sv[0];
+          s[y + 1] = sv[1];
+          s[y + 2] = sv[2];
+          s[y + 3] = sv[3];
+        }
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+          for (int y = 0; y < CPT; ++y) acc[x][y] = fmaf(u[x], s[y], acc[x][y]);
+      }
     }
-    if (a.bf16) {
-      const bf16_t hi = f32_to_bf16(v);
-      const bf16_t lo = f32_to_bf16(v - bf16_to_f32(hi));
-      ((bf16_t*)it.L)[e] = hi;
-      ((bf16_t*)it.L)[nl + e] = lo;
-    } else {
-      ((float*)it.L)[e] = v;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int i = i0 + tr * 4 + x;
+      if (i >= it.m) break;
+      if (a.bf16) {
+        bf16_t* Lh = (bf16_t*)it.L + (size_t)i * 2 * RP + tc * CPT;
+        bf16_t* Ll = Lh + RP;
+#pragma unroll
+        for (int y = 0; y < CPT; y += 4) {
+          float v[4], lo[4];
+#pragma unroll
+          for (int z = 0; z < 4; ++z) {
+            v[z] = a.lr * acc[x][y + z];
+            lo[z] = v[z] - bf16_to_f32(f32_to_bf16(v[z]));
+          }
+          *(u32x2*)(Lh + y) = (u32x2){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+          *(u32x2*)(Ll + y) = (u32x2){pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
+        }
+      } else {
+        // fp32 W keeps L unpadded: m x rp with rp == r.
+        float* Lf = (float*)it.L + (size_t)i * a.rp;
+#pragma unroll
+        for (int y = 0; y < CPT; ++y)
+          if (tc * CPT + y < a.rp) Lf[tc * CPT + y] = a.lr * acc[x][y];
+      }
     }
   } else {
-    const long long f = e - nl;  // only launched for bf16
-    const int i = (int)(f / a.rp), c = (int)(f % a.rp);
-    const float v = c < a.r ? it.V[(size_t)i * a.r + c] : 0.f;
-    const bf16_t hi = f32_to_bf16(v);
-    const bf16_t lo = f32_to_bf16(v - bf16_to_f32(hi));
-    const long long nv = (long long)it.n * a.rp;
-    ((bf16_t*)it.Vs)[f] = hi;
-    ((bf16_t*)it.Vs)[nv + f] = lo;
+    constexpr int G = RP / 8;  // 8-column groups per row
+    const int k0 = (local - it.l_tiles) * 64;
+    bf16_t* Vh = (bf16_t*)it.Vs;
+    bf16_t* Vl = Vh + (size_t)it.n * RP;
+    for (int x = tid; x < 64 * G; x += 256) {
+      const int row = k0 + x / G, c0 = (x % G) * 8;
+      if (row >= it.n) break;
+      float v[8], lo[8];
+#pragma unroll
+      for (int z = 0; z < 8; ++z) {
+        v[z] = c0 + z < r ? it.V[(size_t)row * r + c0 + z] : 0.f;
+        lo[z] = v[z] - bf16_to_f32(f32_to_bf16(v[z]));
+      }
+      *(u32x4*)(Vh + (size_t)row * RP + c0) = (u32x4){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                      pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+      *(u32x4*)(Vl + (size_t)row * RP + c0) =
+          (u32x4){pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]), pack_bf16x2(lo[4], lo[5]),
+                  pack_bf16x2(lo[6], lo[7])};
+    }
   }
 }
 
@@ -149,15 +229,44 @@ struct UpdArgs {
   int count, r, rp;
 };
 
-__device__ __forceinline__ bf16x8 ld_frag(const bf16_t* p, bool ok) {
-  u32x4 v = {0u, 0u, 0u, 0u};
-  if (ok) v = *(const u32x4*)p;
-  return __builtin_bit_cast(bf16x8, v);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)bytes, RSRC_CFG);
+}
+__device__ __forceinline__ u32x4 bload(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, unsigned off, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)off, 0, 0);
 }
 
-template <int RPK>  // rp = 32 * RPK
+__device__ __forceinline__ u32x2 bload2(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore2(__amdgpu_buffer_rsrc_t r, unsigned off, u32x2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, (int)off, 0, 0);
+}
+
+// Workgroup tile: UPD_ROWS rows x 256 columns (4 waves x 64 columns), walked in
+// chunks of CH = 16 NS rows.  Per chunk: the chunk's L rows (loaded a chunk
+// earlier into registers) go to LDS, the next chunk's L is requested, and each
+// of the NS steps multiplies 16 rows, stores them and requests the same step of
+// the next chunk.  The MFMA takes L rows as its A operand and V columns as its
+// B operand, column j of tile t being W column 4 j + t of the wave's strip: a
+// lane ends with 4 ADJACENT columns of rows 4 g .. 4 g + 3 (g = lane / 16),
+// so each memory instruction of a wave covers 4 rows x 128 contiguous bytes --
+// whole cache lines.  The prologue issues range-dropped stores in place of each
+// step's stores so that the count of memory operations between a load and its
+// use is the same on entry as in the steady state.
+template <int RPK, bool HOOK>
 __global__ __launch_bounds__(256) void k_update_bf16(UpdArgs a) {
   constexpr int RP = 32 * RPK;
+  constexpr int NS = RPK == 1 ? 4 : 2;  // W prefetch depth in 16-row steps
+  constexpr int CH = 16 * NS;           // rows per L chunk
+  constexpr int LROW = RP * 4 + 16;     // bytes per staged L row [hi | lo] (+16: conflict-free reads)
+  constexpr int V16 = RP * 4 / 16;      // 16-byte pieces per L row
+  constexpr int NL = CH * V16 / 256;    // L pieces per thread per chunk
+  static_assert(NL * 256 == CH * V16, "L chunk must split evenly over 256 threads");
+  __shared__ __attribute__((aligned(16))) char Ls[CH * LROW];
   int k = 0;
   while (k + 1 < a.count && (int)blockIdx.x >= a.it[k + 1].wg_begin) ++k;
   const ItemUpd& it = a.it[k];
@@ -165,94 +274,123 @@ __global__ __launch_bounds__(256) void k_update_bf16(UpdArgs a) {
   const int local = blockIdx.x - it.wg_begin;
   const int strip = local % it.strips;
   const int rchunk = local / it.strips;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int m = it.m, n = it.n;
   const int col0 = strip * UPD_COLS + wave * 64;
   const int row0 = rchunk * UPD_ROWS;
-  const int m = it.m, n = it.n;
-  if (col0 >= n) return;
+  const int rows = min(UPD_ROWS, m - row0);
+  const int nch = (rows + CH - 1) / CH;
 
-  const bf16_t* __restrict__ Lh = (const bf16_t*)it.L;
-  const bf16_t* __restrict__ Ll = Lh + (size_t)m * RP;
-  const bf16_t* __restrict__ Vh = (const bf16_t*)it.Vs;
-  const bf16_t* __restrict__ Vl = Vh + (size_t)n * RP;
-  const int l16 = lane & 15, g = lane >> 4;
+  const __amdgpu_buffer_rsrc_t rl =
+      rsrc((const bf16_t*)it.L + (size_t)row0 * 2 * RP, (unsigned)rows * RP * 4);
+  const __amdgpu_buffer_rsrc_t rv = rsrc(it.Vs, (unsigned)n * RP * 4);
+  bf16_t* Wt = (bf16_t*)it.W + (size_t)row0 * n;
+  const __amdgpu_buffer_rsrc_t rw = rsrc(Wt, (unsigned)rows * n * 2);
+  __amdgpu_buffer_rsrc_t ro = rw;
+  if (HOOK) ro = rsrc(it.wout + (size_t)row0 * n, (unsigned)rows * n * 4);
 
-  // V fragments of the strip (A operand): row rho = l16 of tile t is column
-  // col0 + 16 (rho / 4) + 4 t + rho % 4.
+  // V fragments of the strip (B operand): column j = l16 of tile t is W column
+  // col0 + 4 j + t.
+  const int cb = col0 + 4 * l16;
   bf16x8 vh[RPK][4], vl[RPK][4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const int col = col0 + 16 * (l16 >> 2) + 4 * t + (l16 & 3);
-    const bool ok = col < n;
 #pragma unroll
     for (int kk = 0; kk < RPK; ++kk) {
-      const size_t off = (size_t)col * RP + kk * 32 + g * 8;
-      vh[kk][t] = ld_frag(Vh + off, ok);
-      vl[kk][t] = ld_frag(Vl + off, ok);
+      const bool ok = cb + t < n;
+      const unsigned off = (unsigned)(((cb + t) * RP + kk * 32 + g * 8) * 2);
+      vh[kk][t] = __builtin_bit_cast(bf16x8, bload(rv, ok ? off : OOB));
+      vl[kk][t] = __builtin_bit_cast(bf16x8, bload(rv, ok ? off + (unsigned)n * RP * 2 : OOB));
     }
   }
+  // The fragments are complete before the loop: a wait inside it would
+  // otherwise count them as possibly in flight on every iteration.
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
 
-  bf16_t* __restrict__ W = (bf16_t*)it.W;
-  const int cbase = col0 + 16 * g;  // this lane's 16 adjacent columns
-  const bool c0ok = cbase < n, c1ok = cbase + 8 < n;
-  const int rend = min(row0 + UPD_ROWS, m);
-  for (int rs = row0; rs < rend; rs += 16) {
-    const int row = rs + l16;
-    const bool rok = row < m;
-    bf16x8 uh[RPK], ul[RPK];
+  // This lane's W pieces: rows 4 g + v (v = 0..3) of each step, columns cb .. cb+3
+  // (n % 8 == 0, so the 4 columns are all in range or all out).
+  const unsigned stepw = (unsigned)(16 * n * 2);
+  unsigned wo[4], ho[4];
 #pragma unroll
-    for (int kk = 0; kk < RPK; ++kk) {
-      const size_t off = (size_t)row * RP + kk * 32 + g * 8;
-      uh[kk] = ld_frag(Lh + off, rok);
-      ul[kk] = ld_frag(Ll + off, rok);
+  for (int v = 0; v < 4; ++v) {
+    wo[v] = cb < n ? (unsigned)(((4 * g + v) * n + cb) * 2) : OOB;
+    ho[v] = cb < n ? (unsigned)(((4 * g + v) * n + cb) * 4) : OOB;
+  }
+
+  // This thread's L pieces: (row, 16-byte column) of a chunk.
+  unsigned lo_g[NL];
+  int lo_s[NL];
+#pragma unroll
+  for (int x = 0; x < NL; ++x) {
+    const int p = tid + 256 * x;
+    const int rrow = p / V16, c16 = p % V16;
+    lo_g[x] = (unsigned)(rrow * RP * 4 + c16 * 16);
+    lo_s[x] = rrow * LROW + c16 * 16;
+  }
+  const unsigned chunk_l = (unsigned)(CH * RP * 4);
+
+  u32x4 lreg[NL];
+  u32x2 wb[NS][4];
+#pragma unroll
+  for (int x = 0; x < NL; ++x) lreg[x] = bload(rl, lo_g[x]);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    // Distinct offsets keep the compiler from merging the dropped stores.
+#pragma unroll
+    for (int v = 0; v < 4; ++v) bstore2(rw, OOB + 32 * s + 8 * v, (u32x2){0u, 0u});
+    if (HOOK) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) bstore(ro, OOB + 64 * s + 16 * v, (u32x4){0u, 0u, 0u, 0u});
     }
-    u32x4 w0 = {0u, 0u, 0u, 0u}, w1 = {0u, 0u, 0u, 0u};
-    bf16_t* wp = W + (size_t)row * n + cbase;
-    if (rok && c0ok) w0 = *(const u32x4*)wp;
-    if (rok && c1ok) w1 = *(const u32x4*)(wp + 8);
-    f32x4 acc[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      acc[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    for (int v = 0; v < 4; ++v) wb[s][v] = bload2(rw, wo[v] + s * stepw);
+  }
+
+  for (int c = 0; c < nch; ++c) {
+    __syncthreads();  // every wave is done with the previous chunk's L
+#pragma unroll
+    for (int x = 0; x < NL; ++x) *(u32x4*)(Ls + lo_s[x]) = lreg[x];
+    __syncthreads();
+#pragma unroll
+    for (int x = 0; x < NL; ++x) lreg[x] = bload(rl, lo_g[x] + (c + 1) * chunk_l);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      bf16x8 uh[RPK], ul[RPK];
 #pragma unroll
       for (int kk = 0; kk < RPK; ++kk) {
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh[kk][t], uh[kk], acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh[kk][t], ul[kk], acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vl[kk][t], uh[kk], acc[t], 0, 0, 0);
+        const char* lp = Ls + (s * 16 + l16) * LROW + (kk * 32 + g * 8) * 2;
+        uh[kk] = *(const bf16x8*)lp;
+        ul[kk] = *(const bf16x8*)(lp + RP * 2);
       }
-    }
-    // acc[t][c] is column cbase + 4 t + c.
-    uint32_t wv[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
-    float nv[16];
+      f32x4 acc[4];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const uint32_t word = wv[e >> 1];
-      const float old = __uint_as_float((e & 1) ? (word & 0xffff0000u) : (word << 16));
-      nv[e] = old - acc[e >> 2][e & 3];
-    }
-    if (rok) {
-      if (c0ok) {
-        u32x4 o = {pack_bf16x2(nv[0], nv[1]), pack_bf16x2(nv[2], nv[3]), pack_bf16x2(nv[4], nv[5]),
-                   pack_bf16x2(nv[6], nv[7])};
-        *(u32x4*)wp = o;
-      }
-      if (c1ok) {
-        u32x4 o = {pack_bf16x2(nv[8], nv[9]), pack_bf16x2(nv[10], nv[11]),
-                   pack_bf16x2(nv[12], nv[13]), pack_bf16x2(nv[14], nv[15])};
-        *(u32x4*)(wp + 8) = o;
-      }
-      if (it.wout) {
-        float* fo = it.wout + (size_t)row * n + cbase;
-        if (c0ok) {
-          *(f32x4*)fo = (f32x4){nv[0], nv[1], nv[2], nv[3]};
-          *(f32x4*)(fo + 4) = (f32x4){nv[4], nv[5], nv[6], nv[7]};
-        }
-        if (c1ok) {
-          *(f32x4*)(fo + 8) = (f32x4){nv[8], nv[9], nv[10], nv[11]};
-          *(f32x4*)(fo + 12) = (f32x4){nv[12], nv[13], nv[14], nv[15]};
+      for (int t = 0; t < 4; ++t) {
+        acc[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < RPK; ++kk) {
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(uh[kk], vh[kk][t], acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ul[kk], vh[kk][t], acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(uh[kk], vl[kk][t], acc[t], 0, 0, 0);
         }
       }
+      // acc[t][v] is row 4 g + v, column cb + t.
+      const unsigned d = (unsigned)(c * NS + s) * stepw;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const uint32_t w0 = wb[s][v][0], w1 = wb[s][v][1];
+        const float n0 = __uint_as_float(w0 << 16) - acc[0][v];
+        const float n1 = __uint_as_float(w0 & 0xffff0000u) - acc[1][v];
+        const float n2 = __uint_as_float(w1 << 16) - acc[2][v];
+        const float n3 = __uint_as_float(w1 & 0xffff0000u) - acc[3][v];
+        bstore2(rw, wo[v] + d, (u32x2){pack_bf16x2(n0, n1), pack_bf16x2(n2, n3)});
+        if (HOOK) bstore(ro, ho[v] + 2 * d, __builtin_bit_cast(u32x4, (f32x4){n0, n1, n2, n3}));
+      }
+      const unsigned dn = (unsigned)((c + 1) * NS + s) * stepw;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) wb[s][v] = bload2(rw, wo[v] + dn);
     }
   }
 }
@@ -277,16 +415,26 @@ __global__ __launch_bounds__(256) void k_update_f32(UpdArgs a) {
 }
 
 struct Layout {
-  size_t s, skip, L, Vs, total;
+  size_t s, mom, flags, skip, L, Vs, total;
 };
-Layout item_layout(int m, int n, int r, int rp, int bf16) {
+Layout item_layout(int m, int n, int r, int rp, int bf16, int aw) {
   Layout l;
   l.s = zo_align256((size_t)r * r * 8);
+  l.mom = zo_align256((size_t)r * r * 4);
+  l.flags = zo_align256((size_t)aw * 4);
   l.skip = 256;
-  l.L = zo_align256((size_t)m * rp * (bf16 ? 4 : 4));  // bf16: hi+lo; fp32: one
+  l.L = zo_align256((size_t)m * rp * 4);  // bf16: hi+lo; fp32: one
   l.Vs = bf16 ? zo_align256((size_t)n * rp * 4) : 0;
-  l.total = l.s + l.skip + l.L + l.Vs;
+  l.total = l.s + 2 * l.mom + l.flags + l.skip + l.L + l.Vs;
   return l;
+}
+
+template <int RPK>
+void launch_update_bf16(bool hook, int wg, hipStream_t stream, const UpdArgs& pa) {
+  if (hook)
+    hipLaunchKernelGGL((k_update_bf16<RPK, true>), dim3(wg), dim3(256), 0, stream, pa);
+  else
+    hipLaunchKernelGGL((k_update_bf16<RPK, false>), dim3(wg), dim3(256), 0, stream, pa);
 }
 
 }  // namespace
@@ -297,8 +445,9 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
                      size_t* ws_needed) {
   const int bf16 = w_dtype == ZO_BF16;
   const int rp = bf16 ? (r + 31) / 32 * 32 : r;
+  const int aw = (r * r + 255) / 256;
   size_t need = 0;
-  for (int i = 0; i < count; ++i) need += item_layout(items[i].m, items[i].n, r, rp, bf16).total;
+  for (int i = 0; i < count; ++i) need += item_layout(items[i].m, items[i].n, r, rp, bf16, aw).total;
   if (ws_needed) *ws_needed = need;
   if (!ws) return ZO_OK;
   if (ws_bytes < need) {
@@ -320,6 +469,7 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
     ra.nonfinite_flag = nonfinite_flag;
     ra.r = r;
     ra.q = q;
+    ra.aw = aw;
     ra.beta1 = beta1;
     ra.beta2 = beta2;
     ra.eps_adam = eps_adam;
@@ -329,19 +479,27 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
     ua.r = pa.r = r;
     ua.rp = pa.rp = rp;
     ua.bf16 = bf16;
+    ua.aw = aw;
     ua.lr = lr;
-    long long us_total = 0;
+    int us_wg = 0;
     int wg_total = 0;
+    bool hook = false;
     for (int k = 0; k < cn; ++k) {
       const zo_update_item& src = items[c0 + k];
-      const Layout lay = item_layout(src.m, src.n, r, rp, bf16);
+      const Layout lay = item_layout(src.m, src.n, r, rp, bf16, aw);
       double* S = (double*)wc.take(lay.s);
+      float* M1n = (float*)wc.take(lay.mom);
+      float* M2n = (float*)wc.take(lay.mom);
+      int* flags = (int*)wc.take(lay.flags);
       int* skip = (int*)wc.take(lay.skip);
       void* L = wc.take(lay.L);
       void* Vs = lay.Vs ? wc.take(lay.Vs) : nullptr;
-      ra.it[k] = ItemRR{src.Z, src.M1, src.M2, src.zbar_out, S, skip};
-      ua.it[k] = ItemUS{src.U, src.V, S, skip, L, Vs, src.m, src.n, us_total};
-      us_total += (long long)src.m * rp + (bf16 ? (long long)src.n * rp : 0);
+      ra.it[k] = ItemRR{src.Z, src.M1, src.M2, src.zbar_out, S, M1n, M2n, flags};
+      const int lt = (src.m + US_ROWS - 1) / US_ROWS;
+      const int vt = bf16 ? (src.n + 63) / 64 : 0;
+      ua.it[k] = ItemUS{src.U, src.V, S, M1n, M2n, src.M1, src.M2, flags, skip, L, Vs,
+                        src.m, src.n, us_wg, lt, lt + vt};
+      us_wg += lt + vt;
       ItemUpd u{};
       u.W = src.W;
       u.wout = src.w_f32_out;
@@ -358,22 +516,27 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
         u.strips = 1;
         wg_total += (int)(((long long)src.m * src.n + 255) / 256);
       }
+      hook = hook || src.w_f32_out;
       pa.it[k] = u;
     }
-    ua.total = us_total;
-    hipLaunchKernelGGL(k_adam_rr, dim3(cn), dim3(256), 0, stream, ra);
+    hipLaunchKernelGGL(k_adam_rr, dim3(cn * aw), dim3(256), 0, stream, ra);
     if ((st = zo_hip_status(hipGetLastError(), "k_adam_rr")) != ZO_OK) return st;
-    hipLaunchKernelGGL(k_us, dim3((unsigned)((us_total + 255) / 256)), dim3(256), 0, stream, ua);
+    switch ((rp + 31) / 32) {
+      case 1: hipLaunchKernelGGL(k_us<1>, dim3(us_wg), dim3(256), 0, stream, ua); break;
+      case 2: hipLaunchKernelGGL(k_us<2>, dim3(us_wg), dim3(256), 0, stream, ua); break;
+      case 3: hipLaunchKernelGGL(k_us<3>, dim3(us_wg), dim3(256), 0, stream, ua); break;
+      default: hipLaunchKernelGGL(k_us<4>, dim3(us_wg), dim3(256), 0, stream, ua); break;
+    }
     if ((st = zo_hip_status(hipGetLastError(), "k_us")) != ZO_OK) return st;
     if (wg_total > 0) {
       if (!bf16) {
         hipLaunchKernelGGL(k_update_f32, dim3(wg_total), dim3(256), 0, stream, pa);
       } else {
         switch (rp / 32) {
-          case 1: hipLaunchKernelGGL(k_update_bf16<1>, dim3(wg_total), dim3(256), 0, stream, pa); break;
-          case 2: hipLaunchKernelGGL(k_update_bf16<2>, dim3(wg_total), dim3(256), 0, stream, pa); break;
-          case 3: hipLaunchKernelGGL(k_update_bf16<3>, dim3(wg_total), dim3(256), 0, stream, pa); break;
-          default: hipLaunchKernelGGL(k_update_bf16<4>, dim3(wg_total), dim3(256), 0, stream, pa); break;
+          case 1: launch_update_bf16<1>(hook, wg_total, stream, pa); break;
+          case 2: launch_update_bf16<2>(hook, wg_total, stream, pa); break;
+          case 3: launch_update_bf16<3>(hook, wg_total, stream, pa); break;
+          default: launch_update_bf16<4>(hook, wg_total, stream, pa); break;
         }
       }
       if ((st = zo_hip_status(hipGetLastError(), "k_update")) != ZO_OK) return st;
