@@ -16,6 +16,7 @@ import numpy as np
 __all__ = [
     "householder_qr", "haar_qr", "raw_qr_first_column",
     "perturbation", "perturbed_weight", "perturbed_linear", "perturbed_linear_blocks",
+    "lora_perturbed_factors", "lora_perturbed_linear", "lora_perturbed_linear_blocks",
     "sq_loss", "central_estimate", "forward_estimate", "aggregate",
     "adam_direction", "subspace_adam_update", "round_bf16", "tiny_run",
 ]
@@ -123,6 +124,50 @@ def perturbed_linear_blocks(Xb, W, U, V, Zs, blk_query, blk_sign, eps, rows=None
     for b, X in enumerate(Xb):
         Xr = np.asarray(X, np.float64) if rows is None else np.asarray(X, np.float64)[rows]
         out.append(perturbed_linear(Xr, W, U, V, Zs[blk_query[b]], float(blk_sign[b]), eps))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# LoRA scheme: the trainable parameters are the two adapter factors
+# (Sec. "Algorithm" -- SubZero+ applies to the trainable parameters of each
+# scheme; Sec. "Experiments" -- LoRA with r = 8, alpha = 16)
+# ---------------------------------------------------------------------------
+def lora_perturbed_factors(A, UA, VA, ZA, B, UB, VB, ZB, sign, eps):
+    """Both adapter factors under one query, each in its own subspace (Eq. 4
+    applied to every trainable matrix, Alg. 2):
+
+        A' = A + sign eps U_A Z_A V_A^T   (r_L x n),
+        B' = B + sign eps U_B Z_B V_B^T   (m x r_L).
+
+    READING: the two factors of a layer take part in the same query with the
+    same sign, as every trainable matrix does in Alg. 3.
+    """
+    return (perturbed_weight(A, UA, VA, ZA, sign, eps),
+            perturbed_weight(B, UB, VB, ZB, sign, eps))
+
+
+def lora_perturbed_linear(X, W, A, UA, VA, ZA, B, UB, VB, ZB, sign, eps, scale):
+    """Output of a LoRA-adapted linear layer under one query, materialised:
+    X (W + scale B' A')^T with the frozen base W (out x in).
+
+    READING: scale = alpha / r_L, the usual LoRA scaling (2 for r_L = 8,
+    alpha = 16).
+    """
+    Ap, Bp = lora_perturbed_factors(A, UA, VA, ZA, B, UB, VB, ZB, sign, eps)
+    Weff = np.asarray(W, np.float64) + scale * (Bp @ Ap)
+    return np.asarray(X, np.float64) @ Weff.T
+
+
+def lora_perturbed_linear_blocks(Xb, W, A, UA, VA, ZAs, B, UB, VB, ZBs, blk_query, blk_sign,
+                                 eps, scale, rows=None):
+    """Blocks b = 0..nblk-1 of the LoRA layer: query j(b), sign s(b); ``rows``
+    optionally restricts each block to a subset of its rows."""
+    out = []
+    for b, X in enumerate(Xb):
+        Xr = np.asarray(X, np.float64) if rows is None else np.asarray(X, np.float64)[rows]
+        j = blk_query[b]
+        out.append(lora_perturbed_linear(Xr, W, A, UA, VA, ZAs[j], B, UB, VB, ZBs[j],
+                                         float(blk_sign[b]), eps, scale))
     return out
 
 

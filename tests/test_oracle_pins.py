@@ -196,6 +196,126 @@ def test_perturbed_linear_blocks_rows_subset():
     np.testing.assert_allclose(full[2], X @ (W + 1e-2 * U @ (2 * Z) @ V.T).T, atol=1e-13)
 
 
+# ------------------------------------------------------------------ LoRA scheme
+def test_lora_hand_example():
+    """Worked by hand: n = 2, m = r_L = r = 1, W = 0, X = [1, 2], A = [1, 0], B = [[2]],
+    U_A = U_B = V_B = [[1]], V_A = e2, Z_A = 3, Z_B = -1, eps = 0.5, scale = 2.
+    s = +1: A' = [1, 1.5], B' = 1.5, W_eff = 2 * 1.5 * A' = [3, 4.5], Y = 3 + 9 = 12.
+    s = -1: A' = [1, -1.5], B' = 2.5, W_eff = [5, -7.5], Y = 5 - 15 = -10."""
+    X = np.array([[1.0, 2.0]])
+    W = np.zeros((1, 2))
+    A = np.array([[1.0, 0.0]])
+    B = np.array([[2.0]])
+    one = np.array([[1.0]])
+    VA = np.array([[0.0], [1.0]])
+    args = (X, W, A, one, VA, np.array([[3.0]]), B, one, one, np.array([[-1.0]]))
+    np.testing.assert_array_equal(oracle.lora_perturbed_linear(*args, +1.0, 0.5, 2.0), [[12.0]])
+    np.testing.assert_array_equal(oracle.lora_perturbed_linear(*args, -1.0, 0.5, 2.0), [[-10.0]])
+
+
+def _lora_case(T=9, m=7, n=11, rl=3, r=2, seed=11, zero_b=False):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((T, n))
+    W = 0.02 * rng.standard_normal((m, n))
+    A = 0.02 * rng.standard_normal((rl, n))
+    B = np.zeros((m, rl)) if zero_b else 0.02 * rng.standard_normal((m, rl))
+    UA, VA = _orth(rl, r, seed + 1), _orth(n, r, seed + 2)
+    UB, VB = _orth(m, r, seed + 3), _orth(rl, r, seed + 4)
+    ZA, ZB = rng.standard_normal((r, r)), rng.standard_normal((r, r))
+    return X, W, A, UA, VA, ZA, B, UB, VB, ZB
+
+
+def test_lora_brute_force_loops():
+    """Element-by-element loops over the definition on a tiny case."""
+    X, W, A, UA, VA, ZA, B, UB, VB, ZB = _lora_case(T=3, m=4, n=5, rl=2, r=2)
+    s, eps, scale = -1.0, 0.3, 2.0
+    T, n = X.shape
+    m, rl = B.shape
+    r = UA.shape[1]
+    Ap = np.zeros((rl, n))
+    for c in range(rl):
+        for k in range(n):
+            acc = A[c, k]
+            for e in range(r):
+                for f in range(r):
+                    acc += s * eps * UA[c, e] * ZA[e, f] * VA[k, f]
+            Ap[c, k] = acc
+    Bp = np.zeros((m, rl))
+    for i in range(m):
+        for c in range(rl):
+            acc = B[i, c]
+            for e in range(r):
+                for f in range(r):
+                    acc += s * eps * UB[i, e] * ZB[e, f] * VB[c, f]
+            Bp[i, c] = acc
+    Y = np.zeros((T, m))
+    for t in range(T):
+        for i in range(m):
+            acc = 0.0
+            for k in range(n):
+                w = W[i, k]
+                for c in range(rl):
+                    w += scale * Bp[i, c] * Ap[c, k]
+                acc += X[t, k] * w
+            Y[t, i] = acc
+    got = oracle.lora_perturbed_linear(X, W, A, UA, VA, ZA, B, UB, VB, ZB, s, eps, scale)
+    np.testing.assert_allclose(got, Y, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("eps", [1e-3, 0.5])
+def test_lora_output_is_quadratic_in_eps(eps):
+    """Both factors are affine in eps, so Y(s eps) = Y0 + s eps Y1 + eps^2 Y2 exactly:
+    the even part isolates the product of the two perturbations and the odd part the two
+    first-order terms.  A factor left unperturbed, or perturbed with the opposite sign,
+    breaks one of the two."""
+    X, W, A, UA, VA, ZA, B, UB, VB, ZB = _lora_case()
+    scale = 2.0
+    f = lambda s, e: oracle.lora_perturbed_linear(X, W, A, UA, VA, ZA, B, UB, VB, ZB, s, e, scale)
+    PA = UA @ ZA @ VA.T
+    PB = UB @ ZB @ VB.T
+    Y0 = X @ (W + scale * B @ A).T
+    Y1 = scale * X @ (B @ PA + PB @ A).T
+    Y2 = scale * X @ (PB @ PA).T
+    np.testing.assert_allclose(f(1.0, 0.0), Y0, rtol=0, atol=1e-14)
+    np.testing.assert_allclose((f(1.0, eps) - f(-1.0, eps)) / (2 * eps), Y1, rtol=0, atol=1e-10)
+    np.testing.assert_allclose((f(1.0, eps) + f(-1.0, eps)) / 2 - Y0, eps ** 2 * Y2, rtol=0, atol=1e-14)
+
+
+def test_lora_reduces_to_full_tuning_case():
+    """With A = I (r_L = n), Z_A = 0 and B = 0 the adapter is B' itself, so the layer is the
+    full-tuning perturbed linear with Z scaled by the LoRA scale."""
+    X, W, _, UA, VA, ZA, _, _, _, ZB = _lora_case(n=6, rl=6)
+    m, n = W.shape
+    UB, VB = _orth(m, 2, 5), _orth(n, 2, 6)
+    A = np.eye(n)
+    B = np.zeros((m, n))
+    for s in (1.0, -1.0):
+        got = oracle.lora_perturbed_linear(X, W, A, UA, VA, 0 * ZA, B, UB, VB, ZB, s, 1e-2, 2.0)
+        ref = oracle.perturbed_linear(X, W, UB, VB, 2.0 * ZB, s, 1e-2)
+        np.testing.assert_allclose(got, ref, rtol=0, atol=1e-14)
+
+
+def test_lora_zero_b_first_order_only_through_b():
+    """Paper initialisation B = 0 with Z_A = 0: the branch is exactly linear in eps and
+    equals scale * s eps X A^T (U_B Z_B V_B^T)^T."""
+    X, W, A, UA, VA, ZA, B, UB, VB, ZB = _lora_case(zero_b=True)
+    for s in (1.0, -1.0):
+        got = oracle.lora_perturbed_linear(X, W, A, UA, VA, 0 * ZA, B, UB, VB, ZB, s, 0.25, 2.0)
+        lin = X @ W.T + 2.0 * s * 0.25 * X @ A.T @ (UB @ ZB @ VB.T).T
+        np.testing.assert_allclose(got, lin, rtol=0, atol=1e-14)
+
+
+def test_lora_blocks_use_their_query_and_sign():
+    X, W, A, UA, VA, ZA, B, UB, VB, ZB = _lora_case()
+    ZAs, ZBs = np.stack([ZA, -2 * ZA]), np.stack([ZB, 3 * ZB])
+    Xb = [X, X[::-1].copy(), X]
+    out = oracle.lora_perturbed_linear_blocks(Xb, W, A, UA, VA, ZAs, B, UB, VB, ZBs, [1, 0, 1],
+                                              [-1, 1, 0], 1e-2, 2.0, rows=np.array([0, 4]))
+    ref0 = oracle.lora_perturbed_linear(X, W, A, UA, VA, -2 * ZA, B, UB, VB, 3 * ZB, -1.0, 1e-2, 2.0)
+    np.testing.assert_array_equal(out[0], ref0[[0, 4]])
+    np.testing.assert_allclose(out[2], (X @ (W + 2.0 * B @ A).T)[[0, 4]], rtol=0, atol=1e-14)
+
+
 # --------------------------------------------------------------- loss, estimate
 def test_sq_loss_hand():
     assert oracle.sq_loss([[1.0, 2.0]], [[0.0, 0.0]]) == 2.5
