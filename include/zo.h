@@ -161,6 +161,70 @@ int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk,
                               size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Perturbed linear of a LoRA-adapted layer -- Eq. 4 and Alg. 2 applied to
+ * the two trainable adapter factors (the LoRA scheme of the experiments,
+ * r_L = 8, alpha = 16), inside the forward of Eq. 5.
+ *
+ * The frozen base W (m x n) carries the adapter A (rl x n) and B (m x rl);
+ * each factor has its own rank-r subspace and coefficients.  For every block
+ * b (query j = blk_query[b], sign s = blk_sign[b]):
+ *
+ *     A'  = A + s eps U_A Z_A,j V_A^T          B' = B + s eps U_B Z_B,j V_B^T
+ *     Y_b = X_b (W + scale B' A')^T            (scale = alpha / rl)
+ *
+ * computed without forming W + scale B' A' or A', as the frozen-base GEMM
+ * plus a rank-(rl + r) term: X_b [A^T | V_A] times
+ * scale [B' | s eps B' U_A Z_A,j] (the second factor is m x (rl + r) per
+ * block).  W, A and B are only read.
+ *
+ *   T, m, n, q, nblk, blk_query, blk_sign, eps, in_dtype, X, x_block_stride,
+ *   W, out_dtype, Y   as for zo_perturbed_linear.
+ *   rl          adapter rank (rows of A, columns of B).
+ *   r           subspace rank of each factor.
+ *   scale       the adapter scaling alpha / rl.
+ *   A, B        device fp32, rl x n and m x rl (row-major).
+ *   U_A, V_A    device fp32, rl x r and n x r.
+ *   U_B, V_B    device fp32, m x r and rl x r.
+ *   Z_A, Z_B    device fp32, q x r x r each.
+ * Arithmetic as for zo_perturbed_linear with rank rl + r (the adapter
+ * operands enter the bf16 GEMM as high + low bf16 pairs).
+ * Limits: rl >= 1, r >= 1, rl + r <= ZO_MAX_RANK; the rest as for
+ * zo_perturbed_linear.
+ *
+ * The two-phase form: zo_lora_perturbed_linear_prepare fills the workspace;
+ * then zo_perturbed_linear_apply with rank rl + r (same T, m, n, q, nblk, X,
+ * x_block_stride, in_dtype and workspace, on the same stream) adds the
+ * frozen-base GEMM and writes Y.  Workspace size:
+ * zo_lora_perturbed_linear_workspace (equal to the full-tuning size at rank
+ * rl + r).
+ * ------------------------------------------------------------------------ */
+size_t zo_lora_perturbed_linear_workspace(int T, int m, int n, int rl, int r,
+                                          int q, int nblk,
+                                          long long x_block_stride,
+                                          int in_dtype);
+int zo_lora_perturbed_linear(int T, int m, int n, int rl, int r, int q,
+                             int nblk, const int* blk_query,
+                             const int8_t* blk_sign, float eps, float scale,
+                             int in_dtype, const void* X,
+                             long long x_block_stride, const void* W,
+                             const float* A, const float* U_A,
+                             const float* V_A, const float* Z_A,
+                             const float* B, const float* U_B,
+                             const float* V_B, const float* Z_B,
+                             int out_dtype, void* Y, void* workspace,
+                             size_t ws_bytes, void* stream);
+int zo_lora_perturbed_linear_prepare(int T, int m, int n, int rl, int r, int q,
+                                     int nblk, const int* blk_query,
+                                     const int8_t* blk_sign, float eps,
+                                     float scale, int in_dtype, const void* X,
+                                     long long x_block_stride, const float* A,
+                                     const float* U_A, const float* V_A,
+                                     const float* Z_A, const float* B,
+                                     const float* U_B, const float* V_B,
+                                     const float* Z_B, void* workspace,
+                                     size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Subspace Adam update -- Eqs. 6-10 and the tail of Alg. 3.
  *
  * With q global estimates g_j (shared by every matrix, e.g. the central

@@ -3,15 +3,17 @@
 The computation lives in libzo.so (hand-written HIP kernels behind the C ABI
 of include/zo.h); this package only binds it.  Entry points:
 
-    subspace_refresh      Haar factors of Gaussian panels (Eq. 11, Alg. 1)
-    perturbed_linear      X_b (W +- eps U Z_j V^T)^T for all query blocks (Eq. 4)
-    subspace_adam_update  subspace Adam and W <- W - lr U S V^T (Eqs. 6-10)
+    subspace_refresh       Haar factors of Gaussian panels (Eq. 11, Alg. 1)
+    perturbed_linear       X_b (W +- eps U Z_j V^T)^T for all query blocks (Eq. 4)
+    lora_perturbed_linear  the same for a LoRA-adapted layer: both adapter factors
+                           perturbed in their own subspaces
+    subspace_adam_update   subspace Adam and W <- W - lr U S V^T (Eqs. 6-10)
     sq_loss, combine_central   loss helpers for a one-layer regression model
 """
 from ._lib import (ZO_BF16, ZO_F32, ZO_MAX_BLOCKS, ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH,
-                   PerturbedLinear, Workspace, ZoError, abi_version, combine_central, lib, perturbed_linear, sq_loss,
-                   subspace_adam_update, subspace_refresh)
+                   LoraPerturbedLinear, PerturbedLinear, Workspace, ZoError, abi_version, combine_central, lib,
+                   lora_perturbed_linear, perturbed_linear, sq_loss, subspace_adam_update, subspace_refresh)
 
 __all__ = ["ZO_BF16", "ZO_F32", "ZO_MAX_BLOCKS", "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH",
-           "PerturbedLinear", "Workspace", "ZoError", "abi_version", "combine_central", "lib", "perturbed_linear", "sq_loss",
-           "subspace_adam_update", "subspace_refresh"]
+           "LoraPerturbedLinear", "PerturbedLinear", "Workspace", "ZoError", "abi_version", "combine_central", "lib",
+           "lora_perturbed_linear", "perturbed_linear", "sq_loss", "subspace_adam_update", "subspace_refresh"]

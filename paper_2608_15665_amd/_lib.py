@@ -30,6 +30,8 @@ ABI_SYMBOLS = (
     "zo_subspace_refresh_workspace", "zo_subspace_refresh",
     "zo_perturbed_linear_workspace", "zo_perturbed_linear",
     "zo_perturbed_linear_prepare", "zo_perturbed_linear_apply",
+    "zo_lora_perturbed_linear_workspace", "zo_lora_perturbed_linear",
+    "zo_lora_perturbed_linear_prepare",
     "zo_subspace_adam_update_workspace", "zo_subspace_adam_update",
     "zo_sq_loss_workspace", "zo_sq_loss", "zo_combine_central",
 )
@@ -92,6 +94,16 @@ def lib() -> ctypes.CDLL:
             L.zo_perturbed_linear_apply.restype = c_int
             L.zo_perturbed_linear_apply.argtypes = [c_int] * 7 + [c_vp, c_ll, c_vp, c_int, c_vp, c_vp, c_sz,
                                                                   c_vp]
+            L.zo_lora_perturbed_linear_workspace.restype = c_sz
+            L.zo_lora_perturbed_linear_workspace.argtypes = [c_int] * 7 + [c_ll, c_int]
+            L.zo_lora_perturbed_linear.restype = c_int
+            L.zo_lora_perturbed_linear.argtypes = ([c_int] * 7 + [ctypes.POINTER(ctypes.c_int),
+                                                    ctypes.POINTER(ctypes.c_int8), c_f, c_f, c_int, c_vp,
+                                                    c_ll, c_vp] + [c_vp] * 8 + [c_int, c_vp, c_vp, c_sz, c_vp])
+            L.zo_lora_perturbed_linear_prepare.restype = c_int
+            L.zo_lora_perturbed_linear_prepare.argtypes = ([c_int] * 7 + [ctypes.POINTER(ctypes.c_int),
+                                                            ctypes.POINTER(ctypes.c_int8), c_f, c_f, c_int,
+                                                            c_vp, c_ll] + [c_vp] * 8 + [c_vp, c_sz, c_vp])
             L.zo_subspace_adam_update_workspace.restype = c_sz
             L.zo_subspace_adam_update_workspace.argtypes = [c_int, ctypes.POINTER(UpdateItem), c_int,
                                                             c_int, c_int]
@@ -269,6 +281,92 @@ def perturbed_linear(X: torch.Tensor, W: torch.Tensor, U: torch.Tensor, V: torch
     all blocks (x_block_stride = 0).  Returns Y (nblk*T x m).
     """
     return PerturbedLinear(X, W, U, V, Z, blk_query, blk_sign, eps, T, x_block_stride, out_dtype, Y)()
+
+
+class LoraPerturbedLinear:
+    """One perturbed LoRA-adapted layer (frozen base W, adapter A: rl x n, B: m x rl, each factor
+    with its own subspace U_*, V_* and coefficients Z_*).  See zo_lora_perturbed_linear.
+
+    __call__ runs prepare + apply; prepare()/apply() run the two phases separately (apply is
+    zo_perturbed_linear_apply at rank rl + r).
+    """
+
+    def __init__(self, X: torch.Tensor, W: torch.Tensor, A: torch.Tensor, UA: torch.Tensor, VA: torch.Tensor,
+                 ZA: torch.Tensor, B: torch.Tensor, UB: torch.Tensor, VB: torch.Tensor, ZB: torch.Tensor,
+                 blk_query: Sequence[int], blk_sign: Sequence[int], eps: float, scale: float, T: int,
+                 x_block_stride: Optional[int] = None, out_dtype=None, Y: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None):
+        nblk = len(blk_query)
+        if len(blk_sign) != nblk:
+            raise ValueError("blk_query and blk_sign differ in length")
+        m, n = W.shape
+        rl = A.shape[0]
+        r = UA.shape[1]
+        q = ZA.shape[0]
+        dt = W.dtype
+        if dt not in _DT:
+            raise TypeError(f"unsupported dtype {dt}")
+        _need(W, "W", dt)
+        _need(X, "X", dt)
+        if x_block_stride is None:
+            x_block_stride = 0 if X.numel() == T * n else T * n
+        if X.numel() < (T * n if x_block_stride == 0 else x_block_stride * (nblk - 1) + T * n):
+            raise ValueError("X is too small for the block layout")
+        _need(A, "A", torch.float32, rl * n)
+        _need(B, "B", torch.float32, m * rl)
+        _need(UA, "U_A", torch.float32, rl * r)
+        _need(VA, "V_A", torch.float32, n * r)
+        _need(UB, "U_B", torch.float32, m * r)
+        _need(VB, "V_B", torch.float32, rl * r)
+        _need(ZA, "Z_A", torch.float32, q * r * r)
+        _need(ZB, "Z_B", torch.float32, q * r * r)
+        out_dtype = dt if out_dtype is None else out_dtype
+        if Y is None:
+            Y = torch.empty((nblk * T, m), dtype=out_dtype, device=W.device)
+        _need(Y, "Y", out_dtype, nblk * T * m)
+        self.T, self.m, self.n, self.rl, self.r, self.q, self.nblk = T, m, n, rl, r, q, nblk
+        self.bq = (ctypes.c_int * nblk)(*[int(v) for v in blk_query])
+        self.bs = (ctypes.c_int8 * nblk)(*[int(v) for v in blk_sign])
+        self.eps, self.scale = float(eps), float(scale)
+        self.dt, self.odt = _DT[dt], _DT[out_dtype]
+        self.xs = int(x_block_stride)
+        self.X, self.W, self.Y = X, W, Y
+        self.factors = (A, UA, VA, ZA, B, UB, VB, ZB)
+        need = lib().zo_lora_perturbed_linear_workspace(T, m, n, rl, r, q, nblk, self.xs, self.dt)
+        if workspace is None:
+            workspace = Workspace.get(need)
+        _need(workspace, "workspace", torch.uint8)
+        if workspace.numel() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, {need} needed")
+        self.ws = workspace
+
+    def _dims(self):
+        return (self.T, self.m, self.n, self.rl, self.r, self.q, self.nblk)
+
+    def prepare(self):
+        _check(lib().zo_lora_perturbed_linear_prepare(
+            *self._dims(), self.bq, self.bs, self.eps, self.scale, self.dt, self.X.data_ptr(), self.xs,
+            *[f.data_ptr() for f in self.factors], self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
+
+    def apply(self):
+        _check(lib().zo_perturbed_linear_apply(
+            self.T, self.m, self.n, self.rl + self.r, self.q, self.nblk, self.dt, self.X.data_ptr(), self.xs,
+            self.W.data_ptr(), self.odt, self.Y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
+        return self.Y
+
+    def __call__(self):
+        _check(lib().zo_lora_perturbed_linear(
+            *self._dims(), self.bq, self.bs, self.eps, self.scale, self.dt, self.X.data_ptr(), self.xs,
+            self.W.data_ptr(), *[f.data_ptr() for f in self.factors], self.odt, self.Y.data_ptr(),
+            self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
+        return self.Y
+
+
+def lora_perturbed_linear(X, W, A, UA, VA, ZA, B, UB, VB, ZB, blk_query, blk_sign, eps, scale, T,
+                          x_block_stride=None, out_dtype=None, Y=None):
+    """Y_b = X_b (W + scale B'_b A'_b)^T for every block b.  See zo_lora_perturbed_linear."""
+    return LoraPerturbedLinear(X, W, A, UA, VA, ZA, B, UB, VB, ZB, blk_query, blk_sign, eps, scale, T,
+                               x_block_stride, out_dtype, Y)()
 
 
 def subspace_adam_update(items: Sequence[dict], g: torch.Tensor, t: int, lr: float, beta1: float,

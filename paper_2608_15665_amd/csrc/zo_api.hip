@@ -212,6 +212,78 @@ int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk, int i
   return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream);
 }
 
+// ------------------------------------------------------------- LoRA scheme
+static int check_lora(int T, int m, int n, int rl, int r, int q, int nblk, long long xs,
+                      int in_dtype) {
+  ZO_CHECK(rl >= 1 && r >= 1 && rl + r <= ZO_MAX_RANK,
+           "lora_perturbed_linear: r_L = %d, r = %d (need both >= 1, r_L + r <= %d)", rl, r,
+           ZO_MAX_RANK);
+  return check_plinear(T, m, n, rl + r, q, nblk, xs, in_dtype);
+}
+
+static int check_lora_factors(int q, int nblk, const int* blk_query, const int8_t* blk_sign,
+                              float eps, float scale, const float* A, const float* UA,
+                              const float* VA, const float* ZA, const float* B, const float* UB,
+                              const float* VB, const float* ZB) {
+  int st = check_blocks(q, nblk, blk_query, blk_sign, eps, UA, VA, ZA);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(isfinite(scale), "lora_perturbed_linear: scale is not finite");
+  ZO_CHECK(A && B && UB && VB && ZB, "lora_perturbed_linear: NULL tensor argument (A, B, U_B, V_B "
+           "or Z_B)");
+  ZO_CHECK(aligned(A, 4) && aligned(B, 4) && aligned(UB, 4) && aligned(VB, 4) && aligned(ZB, 4),
+           "lora_perturbed_linear: adapter tensors must be 4-byte aligned");
+  return ZO_OK;
+}
+
+size_t zo_lora_perturbed_linear_workspace(int T, int m, int n, int rl, int r, int q, int nblk,
+                                          long long x_block_stride, int in_dtype) {
+  if (check_lora(T, m, n, rl, r, q, nblk, x_block_stride, in_dtype) != ZO_OK) return 0;
+  PlinearPlan p;
+  zo_plinear_plan(&p, T, m, n, rl + r, q, nblk, x_block_stride, in_dtype, in_dtype);
+  return p.ws_total;
+}
+
+int zo_lora_perturbed_linear_prepare(int T, int m, int n, int rl, int r, int q, int nblk,
+                                     const int* blk_query, const int8_t* blk_sign, float eps,
+                                     float scale, int in_dtype, const void* X,
+                                     long long x_block_stride, const float* A, const float* UA,
+                                     const float* VA, const float* ZA, const float* B,
+                                     const float* UB, const float* VB, const float* ZB,
+                                     void* workspace, size_t ws_bytes, void* stream) {
+  PlinearPlan p;
+  int st = check_lora(T, m, n, rl, r, q, nblk, x_block_stride, in_dtype);
+  if (st != ZO_OK) return st;
+  st = check_lora_factors(q, nblk, blk_query, blk_sign, eps, scale, A, UA, VA, ZA, B, UB, VB, ZB);
+  if (st != ZO_OK) return st;
+  st = check_plinear_call(T, m, n, rl + r, q, nblk, x_block_stride, in_dtype, in_dtype, X, nullptr,
+                          nullptr, workspace, ws_bytes, &p);
+  if (st != ZO_OK) return st;
+  return zo_lora_prepare(p, rl, r, blk_query, blk_sign, eps, scale, X, A, UA, VA, ZA, B, UB, VB,
+                         ZB, workspace, (hipStream_t)stream);
+}
+
+int zo_lora_perturbed_linear(int T, int m, int n, int rl, int r, int q, int nblk,
+                             const int* blk_query, const int8_t* blk_sign, float eps, float scale,
+                             int in_dtype, const void* X, long long x_block_stride, const void* W,
+                             const float* A, const float* UA, const float* VA, const float* ZA,
+                             const float* B, const float* UB, const float* VB, const float* ZB,
+                             int out_dtype, void* Y, void* workspace, size_t ws_bytes,
+                             void* stream) {
+  PlinearPlan p;
+  int st = check_lora(T, m, n, rl, r, q, nblk, x_block_stride, in_dtype);
+  if (st != ZO_OK) return st;
+  st = check_lora_factors(q, nblk, blk_query, blk_sign, eps, scale, A, UA, VA, ZA, B, UB, VB, ZB);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(W && Y, "lora_perturbed_linear: NULL tensor argument (W or Y)");
+  st = check_plinear_call(T, m, n, rl + r, q, nblk, x_block_stride, in_dtype, out_dtype, X, W, Y,
+                          workspace, ws_bytes, &p);
+  if (st != ZO_OK) return st;
+  st = zo_lora_prepare(p, rl, r, blk_query, blk_sign, eps, scale, X, A, UA, VA, ZA, B, UB, VB, ZB,
+                       workspace, (hipStream_t)stream);
+  if (st != ZO_OK) return st;
+  return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream);
+}
+
 // ------------------------------------------------------------------ update
 static int check_update(int count, const zo_update_item* items, int r, int q, int w_dtype) {
   ZO_CHECK(count >= 0, "update: count = %d < 0", count);

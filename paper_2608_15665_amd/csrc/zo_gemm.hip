@@ -338,11 +338,6 @@ __global__ __launch_bounds__(256) void k_pcombine(const float* __restrict__ P2, 
   o[2 * rp + a] = lo;
 }
 
-// Query table of a call: j(b) and s(b) packed as j | (s + 1) << 16.
-struct BlkTable {
-  int code[ZO_MAX_BLOCKS];
-};
-
 // B_b[i][a] = s_b eps sum_c U[i][c] Z_{j(b)}[c][a] (a < r; 0 for r <= a < rp).
 // fp32 output: m x rp per block.  bf16 output: m x 3 rp per block as
 // [B_hi | B_lo | B_hi].
@@ -615,29 +610,49 @@ int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
   return ZO_OK;
 }
 
+BlkTable zo_blk_table(int nblk, const int* blk_query, const int8_t* blk_sign) {
+  BlkTable tab;
+  for (int b = 0; b < nblk; ++b) tab.code[b] = blk_query[b] | ((int)(blk_sign[b] + 1) << 16);
+  return tab;
+}
+
+PlinearWs zo_plinear_ws(const PlinearPlan& p, void* ws) {
+  WsCarver wc(ws);
+  PlinearWs w;
+  w.vt = wc.take(p.ws_vt);
+  w.p2 = p.ws_p2 ? wc.take(p.ws_p2) : nullptr;
+  w.pp = wc.take(p.ws_p);
+  w.bp = wc.take(p.ws_bp);
+  return w;
+}
+
 int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
                        float eps, const void* X, const float* U, const float* V, const float* Z,
                        void* ws, hipStream_t stream) {
-  WsCarver wc(ws);
-  void* vt = wc.take(p.ws_vt);
-  void* p2 = p.ws_p2 ? wc.take(p.ws_p2) : nullptr;
-  void* pp = wc.take(p.ws_p);
-  void* bp = wc.take(p.ws_bp);
+  const PlinearWs w = zo_plinear_ws(p, ws);
   int st;
   {
     const long long total = (long long)p.rp * p.n;
     hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
-                       V, p.n, p.r, p.rp, vt, p.in_bf16);
+                       V, p.n, p.r, p.rp, w.vt, p.in_bf16);
     if ((st = zo_hip_status(hipGetLastError(), "k_transpose_v")) != ZO_OK) return st;
   }
   {
-    BlkTable tab;
-    for (int b = 0; b < p.nblk; ++b) tab.code[b] = blk_query[b] | ((int)(blk_sign[b] + 1) << 16);
+    const BlkTable tab = zo_blk_table(p.nblk, blk_query, blk_sign);
     const long long total = (long long)p.nblk * p.m * p.rp;
     hipLaunchKernelGGL(k_bprime, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, U, Z,
-                       p.m, p.r, p.rp, p.nblk, eps, tab, bp, p.in_bf16);
+                       p.m, p.r, p.rp, p.nblk, eps, tab, w.bp, p.in_bf16);
     if ((st = zo_hip_status(hipGetLastError(), "k_bprime")) != ZO_OK) return st;
   }
+  return zo_plinear_project(p, X, ws, stream);
+}
+
+int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_t stream) {
+  const PlinearWs w = zo_plinear_ws(p, ws);
+  void* vt = w.vt;
+  void* p2 = w.p2;
+  void* pp = w.pp;
+  int st;
   const long long xs = p.x_block_stride;
   if (p.in_bf16) {
     GemmArgs g{};
@@ -677,11 +692,9 @@ int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t*
 
 int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
                      hipStream_t stream) {
-  WsCarver wc(ws);
-  wc.take(p.ws_vt);
-  if (p.ws_p2) wc.take(p.ws_p2);
-  void* pp = wc.take(p.ws_p);
-  void* bp = wc.take(p.ws_bp);
+  const PlinearWs w = zo_plinear_ws(p, ws);
+  void* pp = w.pp;
+  void* bp = w.bp;
   const long long xs = p.x_block_stride;
   if (p.in_bf16) {
     GemmArgs h{};

@@ -61,6 +61,28 @@ struct PlinearPlan {
 };
 int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
                     long long x_block_stride, int in_dtype, int out_dtype);
+// Workspace regions of a plan, in carving order.
+struct PlinearWs {
+  void* vt;  // right factor, transposed: bf16 2 rp x n (hi rows, then lo rows); fp32 rp x n
+  void* p2;  // bf16 inputs: X_b Vt^T in fp32, 2 rp wide (nullptr for fp32)
+  void* pp;  // left correction operand per X block: bf16 [P_hi | P_hi | P_lo]; fp32 rp wide
+  void* bp;  // right correction operand per block: bf16 [B_hi | B_lo | B_hi]; fp32 rp wide
+};
+PlinearWs zo_plinear_ws(const PlinearPlan& p, void* ws);
+// Query table of a call: j(b) and s(b) packed as j | (s + 1) << 16.
+struct BlkTable {
+  int code[ZO_MAX_BLOCKS];
+};
+BlkTable zo_blk_table(int nblk, const int* blk_query, const int8_t* blk_sign);
+// P = X_b Vt^T for every distinct X block, from the vt region already filled.
+int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_t stream);
+// LoRA scheme: fills vt with [A ; V_A^T] and bp with the per-block right factor
+// (plan rank r = rl + rs), then projects.
+int zo_lora_prepare(const PlinearPlan& p, int rl, int rs, const int* blk_query,
+                    const int8_t* blk_sign, float eps, float scale, const void* X, const float* A,
+                    const float* UA, const float* VA, const float* ZA, const float* B,
+                    const float* UB, const float* VB, const float* ZB, void* ws,
+                    hipStream_t stream);
 int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
                        float eps, const void* X, const float* U, const float* V,
                        const float* Z, void* ws, hipStream_t stream);

@@ -92,6 +92,32 @@ def test_perturbed_linear_rejects_small_workspace_and_nulls():
     assert st == 2
 
 
+def test_lora_validation_and_workspace():
+    """The LoRA entry points share the full-tuning plan at rank rl + r and reject bad ranks,
+    non-finite scale and NULL adapter tensors before launching anything."""
+    L = zo.lib()
+    bq = (ctypes.c_int * 2)(0, 0)
+    bs = (ctypes.c_int8 * 2)(1, -1)
+    fake = 1 << 20
+    need = L.zo_lora_perturbed_linear_workspace(16, 32, 64, 8, 4, 1, 2, 0, 1)
+    assert need == L.zo_perturbed_linear_workspace(16, 32, 64, 12, 1, 2, 0, 1) > 0
+    assert L.zo_lora_perturbed_linear_workspace(16, 32, 64, 120, 9, 1, 2, 0, 1) == 0
+    f8 = [fake] * 8
+    st = L.zo_lora_perturbed_linear(16, 32, 64, 0, 4, 1, 2, bq, bs, 1e-3, 2.0, 1, fake, 0, fake, *f8, 1,
+                                    fake, fake, need, None)
+    assert st == 1 and "r_L" in _detail()
+    st = L.zo_lora_perturbed_linear(16, 32, 64, 8, 4, 1, 2, bq, bs, 1e-3, float("inf"), 1, fake, 0, fake,
+                                    *f8, 1, fake, fake, need, None)
+    assert st == 1 and "scale" in _detail()
+    f8n = [fake] * 4 + [None] + [fake] * 3
+    st = L.zo_lora_perturbed_linear_prepare(16, 32, 64, 8, 4, 1, 2, bq, bs, 1e-3, 2.0, 1, fake, 0, *f8n,
+                                            fake, need, None)
+    assert st == 1 and "NULL" in _detail()
+    st = L.zo_lora_perturbed_linear_prepare(16, 32, 64, 8, 4, 1, 2, bq, bs, 1e-3, 2.0, 1, fake, 0, *f8,
+                                            fake, need - 1, None)
+    assert st == 6
+
+
 def test_refresh_validation():
     L = zo.lib()
     fake = 1 << 20

@@ -163,20 +163,32 @@ def test_deterministic_repeat():
     assert np.array_equal(a, b)
 
 
-@pytest.mark.parametrize("name", ["fc1", "fc2"])
-def test_opt13b_full_size_sampled(name):
-    """The OPT-13B-shaped layer at full size (T = 8192, q = 8, 16 blocks, r = 64) in the launch
-    configuration the benchmark times; sampled token rows checked against the oracle row by row."""
-    cfg = zd.CONFIGS["opt-13b"]
-    m, n = {"fc1": (20480, 5120), "fc2": (5120, 20480)}[name]
+def _distinct_shapes(cfg):
+    seen = []
+    for _, m, n in cfg["mats"]:
+        if (m, n) not in seen:
+            seen.append((m, n))
+    return seen
+
+
+FULL_SIZE = [(name, m, n) for name in ("opt-1.3b", "llama-7b", "opt-13b")
+             for m, n in _distinct_shapes(zd.CONFIGS[name])]
+
+
+@pytest.mark.parametrize("name,m,n", FULL_SIZE)
+def test_full_size_sampled(name, m, n):
+    """Every distinct matrix shape of the OPT-1.3B, LLaMA-7B and OPT-13B stacks at full size
+    (T tokens per block, 2q blocks, the config's r) in the launch configuration the benchmark
+    times; sampled token rows of several blocks checked against the oracle row by row."""
+    cfg = zd.CONFIGS[name]
     T, r, q = cfg["T"], cfg["r"], cfg["q"]
     nblk = 2 * q
     c = make_case(T, m, n, r, q, nblk, False, bf16=True)
     Y = zo.perturbed_linear(c["Xd"], c["Wd"], c["Ud"], c["Vd"], c["Zd"], c["bq"], c["bs"], 1e-3, T,
                             x_block_stride=c["xs"])
     torch.cuda.synchronize()
-    rows = np.array([0, 1, 255, 256, 4097, T - 1])
-    blocks = [0, 1, 7, nblk - 1]
+    rows = np.array([0, 1, 255, 256, T // 2 + 1, T - 1])
+    blocks = sorted({0, 1, nblk // 2 - 1, nblk - 1})
     Yh = Y.view(nblk, T, m)
     for b in blocks:
         got = host(Yh[b][torch.from_numpy(rows).cuda()])

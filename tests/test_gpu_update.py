@@ -153,18 +153,25 @@ def test_batched_heterogeneous_items():
         check_item(it, ref, True)
 
 
-def test_opt13b_fc1_full_size_sampled():
-    """Full-size OPT-13B fc1 update (20480 x 5120, r = 64, q = 8); sampled rows vs the oracle."""
-    m, n, r, q = 20480, 5120, 64, 8
-    it = make_item(5, (20480,), m, n, r, q, True, True)
-    g = zd.f32(zd.draw(5, "G", (20480,), (q,), 1e-2))
-    zo.subspace_adam_update([it["dev"]], dev_f32(g), 3, 1e-3, 0.9, 0.95, 1e-8)
+@pytest.mark.parametrize("name,m,n", [("opt-1.3b", 8192, 2048), ("llama-7b", 11008, 4096),
+                                       ("llama-7b", 4096, 11008), ("opt-13b", 20480, 5120),
+                                       ("opt-13b", 5120, 20480)])
+def test_full_size_sampled(name, m, n):
+    """Full-size update of the largest matrices of each stack (the config's r, q, lr, betas);
+    sampled rows vs the oracle."""
+    cfg = zd.CONFIGS[name]
+    r, q, lr, b1, b2 = cfg["r"], cfg["q"], cfg["lr"], cfg["beta1"], cfg["beta2"]
+    it = make_item(5, (m, n), m, n, r, q, True, True)
+    g = zd.f32(zd.draw(5, "G", (m, n), (q,), 1e-2))
+    zo.subspace_adam_update([it["dev"]], dev_f32(g), 3, lr, b1, b2, 1e-8)
     torch.cuda.synchronize()
-    rows = np.array([0, 1, 127, 128, 10000, m - 1])
+    rows = np.array([0, 1, 127, 128, m // 2 + 3, m - 1])
     Zbar = oracle.aggregate(g.astype(np.float64), it["Z"])
-    _, _, S = oracle.adam_direction(it["M1h"], it["M2h"], Zbar, 3, F32(0.9), F32(0.95), F32(1e-8))
-    W_rows = it["Wv"][rows] - F32(1e-3) * (it["U"][rows].astype(np.float64) @ S @ it["V"].astype(np.float64).T)
+    _, _, S = oracle.adam_direction(it["M1h"], it["M2h"], Zbar, 3, F32(b1), F32(b2), F32(1e-8))
+    W_rows = it["Wv"][rows] - F32(lr) * (it["U"][rows].astype(np.float64) @ S @ it["V"].astype(np.float64).T)
     got_hook = host(it["dev"]["w_f32_out"][torch.from_numpy(rows).cuda()])
     got_w = host(it["dev"]["W"][torch.from_numpy(rows).cuda()])
     assert ferr(got_hook, W_rows, 1.0) <= 5e-5
     assert check_bf16_storage(got_w, got_hook, W_rows) < 1e-2
+    np.testing.assert_allclose(host(it["dev"]["M1"]), oracle.adam_direction(
+        it["M1h"], it["M2h"], Zbar, 3, F32(b1), F32(b2), F32(1e-8))[0], rtol=1e-6, atol=1e-12)
