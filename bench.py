@@ -28,7 +28,7 @@ METRIC = "perturbed-linear TFLOP/s (% MFMA peak); subspace update GB/s (% HBM pe
 PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 4 SIMD x 1024 FLOP/clk x 2.4 GHz, dense
 PEAK_HBM_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic_opt13b.json")
-GEMM_SOURCES = [os.path.join(ROOT, "paper_2608_15665_amd", "csrc", f) for f in ("zo_gemm.hip", "zo_internal.h")]
+CSRC = os.path.join(ROOT, "paper_2608_15665_amd", "csrc")
 
 
 def log(msg):
@@ -46,16 +46,41 @@ def apply_flops(T, m, n, r, q):
     return 2 * q * (2 * T * m * n + 2 * T * r * m)
 
 
-def update_bytes(m, n, r, q):
-    """Algorithmic HBM bytes of one matrix's update: bf16 W read + write, fp32 U and V,
-    the q fp32 Z_j, and the two fp32 moments read + write."""
-    return 4 * m * n + 4 * r * (m + n) + 4 * q * r * r + 16 * r * r
+def lora_flops(T, m, n, rl, r, q):
+    """Algorithmic FLOPs of one LoRA-adapted layer per step (all 2q blocks): the frozen-base
+    products, the X_b [A^T | V_A] projections and the rank-(rl + r) terms, and the per-block
+    right factors scale [B' | s eps B' U_A Z_A]."""
+    re = rl + r
+    return 2 * q * (2 * T * m * n + 2 * T * n * re + 2 * T * re * m) + 2 * q * m * (2 * r * rl + 2 * rl * r)
+
+
+def lora_apply_flops(T, m, n, rl, r, q):
+    return 2 * q * (2 * T * m * n + 2 * T * (rl + r) * m)
+
+
+def update_bytes(m, n, r, q, wbytes=2):
+    """Algorithmic HBM bytes of one matrix's update: W read + write (bf16, or fp32 for the
+    adapter factors), fp32 U and V, the q fp32 Z_j, and the two fp32 moments read + write."""
+    return 2 * wbytes * m * n + 4 * r * (m + n) + 4 * q * r * r + 16 * r * r
+
+
+def _region(text, start, end):
+    i = text.index(start)
+    return text[i:text.index(end, i) + len(end)]
 
 
 def source_hash():
+    """Hash of the source text the dominant kernel is built from: its argument struct, the
+    kernel with its launcher, and the bf16 rounding helpers its epilogue uses."""
+    gemm = open(os.path.join(CSRC, "zo_gemm.hip")).read()
+    inc = open(os.path.join(CSRC, "zo_internal.h")).read()
+    parts = [_region(gemm, "struct GemmArgs {", "};"),
+             _region(gemm, "__device__ __forceinline__ int g4(int r)", 'hipGetLastError(), "k_gemm_main");\n}'),
+             _region(inc, "__device__ __forceinline__ bf16_t f32_to_bf16(", "}"),
+             _region(inc, "__device__ __forceinline__ uint32_t pack_bf16x2(", "}")]
     h = hashlib.sha256()
-    for p in GEMM_SOURCES:
-        h.update(open(p, "rb").read())
+    for p in parts:
+        h.update(p.encode())
     return h.hexdigest()[:16]
 
 
@@ -72,7 +97,7 @@ def copy_calibration():
                       "launches": 3}))
 
 
-def cpu_baseline(cfg, seed, budget_s):
+def cpu_baseline(cfg, seed, budget_s, mat, lora):
     """The float64 oracle on a bounded sample of the same workload, on this host's cores."""
     import numpy as np
     import oracle
@@ -83,7 +108,8 @@ def cpu_baseline(cfg, seed, budget_s):
     except Exception:  # pragma: no cover
         threads = 1
     T, r, q = cfg["T"], cfg["r"], cfg["q"]
-    m, n = cfg["mats"][0][1], cfg["mats"][0][2]
+    m, n = mat[1], mat[2]
+    rl, scale = zd.QWEN_LORA_RANK, zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
     S = 256
     W = zd.as_bf16_values(zd.draw(seed, "W0", (m, n), (m, n), 0.02))[1]
     X0 = zd.as_bf16_values(zd.draw(seed, "X", (T, n, 0), (S, n)))[1]
@@ -93,14 +119,26 @@ def cpu_baseline(cfg, seed, budget_s):
     flops = 0.0
     nb = 0
     t0 = time.perf_counter()
+    if lora:
+        A = zd.f32(zd.draw(seed, "LORA_A", (0,), (rl, n), 0.02)).astype(np.float64)
+        B = np.zeros((m, rl))
+        UA, _ = np.linalg.qr(zd.draw(seed, "OMEGA_U", (1, rl), (rl, r)))
+        VB, _ = np.linalg.qr(zd.draw(seed, "OMEGA_V", (1, rl), (rl, r)))
     while time.perf_counter() - t0 < budget_s and nb < 64:
         j, s = (nb // 2) % q, (1 if nb % 2 == 0 else -1)
-        oracle.perturbed_linear(X0, W, U, V, Z[j], s, 1e-3)
-        flops += 2 * S * m * n + 2 * S * n * r + 2 * S * r * m + 2 * m * r * r
+        if lora:
+            oracle.lora_perturbed_linear(X0, W, A, UA, V, Z[j], B, U, VB, Z[(j + 1) % q], s, 1e-3, scale)
+            re = rl + r
+            flops += 2 * S * m * n + 2 * S * n * re + 2 * S * re * m + 2 * m * (2 * r * rl + 2 * rl * r)
+        else:
+            oracle.perturbed_linear(X0, W, U, V, Z[j], s, 1e-3)
+            flops += 2 * S * m * n + 2 * S * n * r + 2 * S * r * m + 2 * m * r * r
         nb += 1
     dt = time.perf_counter() - t0
+    what = ("materialised A', B' and W + scale B' A', then X W'^T" if lora
+            else "materialised W + s eps U Z V^T, then X W'^T")
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"float64 oracle (materialised W + s eps U Z V^T, then X W'^T) on {nb} query blocks "
+            "sample": f"float64 oracle ({what}) on {nb} query blocks "
                       f"x {S} token rows of the {m}x{n} layer; algorithmic FLOPs of that sample / {dt:.1f} s; "
                       f"{len(os.sched_getaffinity(0))} host cores visible"}
 
@@ -110,7 +148,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", default="opt-13b", choices=["opt-1.3b", "llama-7b", "opt-13b"])
+    ap.add_argument("--config", default="opt-13b", choices=["opt-1.3b", "llama-7b", "opt-13b", "qwen-32b-lora"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -134,10 +172,12 @@ def main():
     torch.cuda.set_device(0)
     zo.lib()
     cfg = zd.CONFIGS[args.config]
+    lora = args.config.endswith("-lora")
     T, r, q = cfg["T"], cfg["r"], cfg["q"]
     nblk = 2 * q
     L = cfg["layers"]
     eps, lr, b1, b2, ea, F = cfg["eps"], cfg["lr"], cfg["beta1"], cfg["beta2"], cfg["eps_adam"], cfg["F"]
+    rl, scale = zd.QWEN_LORA_RANK, zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
     seed = args.seed
     dev = "cuda"
     bf16 = torch.bfloat16
@@ -147,48 +187,80 @@ def main():
         bits = zd.bf16_bits(zd.f32(a64))
         return torch.from_numpy(bits.view(np.int16)).view(bf16).to(dev)
 
+    def f32dev(a64):
+        return torch.from_numpy(zd.f32(a64)).to(dev)
+
+    # The perturbed matrices: every weight (full tuning) or the adapted q and v projections (LoRA).
+    unit_mats = [mt for mt in cfg["mats"] if not lora or mt[0] in ("q", "v")]
     # Weights: one host draw per distinct shape; layer l holds it rolled by l rows (device side).
-    shapes = sorted({(m, n) for _, m, n in cfg["mats"]})
-    Wbase = {s: to_bf16(zd.draw(seed, "W0", s, s, 0.02)) for s in shapes}
+    shapes = sorted({(m, n) for _, m, n in unit_mats})
+    Wbase = {sh: to_bf16(zd.draw(seed, "W0", sh, sh, 0.02)) for sh in shapes}
     # Activations: one base block per distinct n; block b rolled by b*floor(T/nblk) rows.
-    ns = sorted({n for _, _, n in cfg["mats"]})
+    ns = sorted({n for _, _, n in unit_mats})
     X = {}
     for n in ns:
         x0 = to_bf16(zd.draw(seed, "X", (T, n, 0), (T, n)))
         X[n] = torch.cat([torch.roll(x0, b * (T // nblk), 0) for b in range(nblk)]).contiguous()
         del x0
-    Y = {m: torch.empty((nblk * T, m), dtype=bf16, device=dev) for m in sorted({m for _, m, _ in cfg["mats"]})}
-    rows_set = sorted({m for _, m, _ in cfg["mats"]} | set(ns))
-    Obase = {rw: torch.from_numpy(zd.f32(zd.draw(seed, "OMEGA_U", (rw, r), (rw, r)))).to(dev) for rw in rows_set}
-    mats = []
+    Y = {m: torch.empty((nblk * T, m), dtype=bf16, device=dev) for m in sorted({m for _, m, _ in unit_mats})}
+    rows_set = sorted({m for _, m, _ in unit_mats} | set(ns) | ({rl} if lora else set()))
+    Obase = {rw: f32dev(zd.draw(seed, "OMEGA_U", (rw, r), (rw, r))) for rw in rows_set}
+    zeros_rr = lambda: torch.zeros((r, r), dtype=torch.float32, device=dev)
+    units, omegas, qouts = [], [], []
     for l in range(L):
-        for k, (name, m, n) in enumerate(cfg["mats"]):
-            idx = len(mats)
-            mats.append(dict(
-                name=f"{name}{l}", m=m, n=n,
-                W=torch.roll(Wbase[(m, n)], l, 0).contiguous(),
-                OU=torch.roll(Obase[m], 2 * idx, 0).contiguous(), OV=torch.roll(Obase[n], 2 * idx + 1, 0).contiguous(),
-                U=torch.empty((m, r), dtype=torch.float32, device=dev),
-                V=torch.empty((n, r), dtype=torch.float32, device=dev),
-                M1=torch.zeros((r, r), dtype=torch.float32, device=dev),
-                M2=torch.zeros((r, r), dtype=torch.float32, device=dev)))
+        for name, m, n in unit_mats:
+            idx = len(units)
+            u = dict(name=f"{name}{l}", m=m, n=n, W=torch.roll(Wbase[(m, n)], l, 0).contiguous())
+            # Panels (rows x r Gaussian inputs of the refresh) and their Haar factors.
+            prow = [("UA", rl), ("VA", n), ("UB", m), ("VB", rl)] if lora else [("U", m), ("V", n)]
+            for k, (key, rw) in enumerate(prow):
+                omegas.append(torch.roll(Obase[rw], len(prow) * idx + k, 0).contiguous())
+                u[key] = torch.empty((rw, r), dtype=torch.float32, device=dev)
+                qouts.append(u[key])
+            if lora:
+                u["A"] = f32dev(zd.draw(seed, "LORA_A", (idx,), (rl, n), 0.02))
+                u["B"] = torch.zeros((m, rl), dtype=torch.float32, device=dev)  # the usual LoRA start
+                u["mom"] = [(zeros_rr(), zeros_rr()), (zeros_rr(), zeros_rr())]
+            else:
+                u["mom"] = [(zeros_rr(), zeros_rr())]
+            units.append(u)
     del Wbase, Obase
     nsteps = args.warmup + args.steps
-    Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(len(mats))])
-                                   for t in range(nsteps)])).to(dev)  # [step, mat, q, r, r]
-    m_last = cfg["mats"][-1][1]
+    zper = 2 if lora else 1  # coefficient sets per unit (one per perturbed factor)
+    Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(zper * len(units))])
+                                   for t in range(nsteps)])).to(dev)  # [step, factor, q, r, r]
+    m_last = unit_mats[-1][1]
     Ystar = to_bf16(zd.draw(seed, "X", (T, m_last, 1), (T, m_last)))
     bq = [b // 2 for b in range(nblk)]
     bs = [1 if b % 2 == 0 else -1 for b in range(nblk)]
-    ws_need = max(zo.lib().zo_perturbed_linear_workspace(T, m, n, r, q, nblk, T * n, zo.ZO_BF16) for m, n in shapes)
+    if lora:
+        ws_need = max(zo.lib().zo_lora_perturbed_linear_workspace(T, m, n, rl, r, q, nblk, T * n, zo.ZO_BF16)
+                      for m, n in shapes)
+    else:
+        ws_need = max(zo.lib().zo_perturbed_linear_workspace(T, m, n, r, q, nblk, T * n, zo.ZO_BF16)
+                      for m, n in shapes)
     ws = torch.empty(ws_need, dtype=torch.uint8, device=dev)
-    plins = [[zo.PerturbedLinear(X[mt["n"]], mt["W"], mt["U"], mt["V"], Z[t, i], bq, bs, eps, T,
-                                 x_block_stride=T * mt["n"], Y=Y[mt["m"]], workspace=ws)
-              for i, mt in enumerate(mats)] for t in range(nsteps)]
-    items = [[dict(W=mt["W"], U=mt["U"], V=mt["V"], Z=Z[t, i], M1=mt["M1"], M2=mt["M2"])
-              for i, mt in enumerate(mats)] for t in range(nsteps)]
+
+    def make_layer(t, i, u):
+        if lora:
+            return zo.LoraPerturbedLinear(X[u["n"]], u["W"], u["A"], u["UA"], u["VA"], Z[t, 2 * i], u["B"], u["UB"],
+                                          u["VB"], Z[t, 2 * i + 1], bq, bs, eps, scale, T,
+                                          x_block_stride=T * u["n"], Y=Y[u["m"]], workspace=ws)
+        return zo.PerturbedLinear(X[u["n"]], u["W"], u["U"], u["V"], Z[t, i], bq, bs, eps, T,
+                                  x_block_stride=T * u["n"], Y=Y[u["m"]], workspace=ws)
+
+    def make_items(t, i, u):
+        if lora:
+            (a1, a2), (c1, c2) = u["mom"]
+            return [dict(W=u["A"], U=u["UA"], V=u["VA"], Z=Z[t, 2 * i], M1=a1, M2=a2),
+                    dict(W=u["B"], U=u["UB"], V=u["VB"], Z=Z[t, 2 * i + 1], M1=c1, M2=c2)]
+        (m1, m2), = u["mom"]
+        return [dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, i], M1=m1, M2=m2)]
+
+    plins = [[make_layer(t, i, u) for i, u in enumerate(units)] for t in range(nsteps)]
+    items = [[it for i, u in enumerate(units) for it in make_items(t, i, u)] for t in range(nsteps)]
     torch.cuda.synchronize()
-    log(f"setup {time.perf_counter() - t_setup:.1f} s; {len(mats)} matrices; "
+    log(f"setup {time.perf_counter() - t_setup:.1f} s; {len(units)} perturbed layers; "
         f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB on device")
 
     Ev = lambda: torch.cuda.Event(enable_timing=True)
@@ -200,11 +272,10 @@ def main():
         if t % F == 0:
             e0, e1 = Ev(), Ev()
             e0.record()
-            zo.subspace_refresh([mt["OU"] for mt in mats] + [mt["OV"] for mt in mats], r,
-                                out=[mt["U"] for mt in mats] + [mt["V"] for mt in mats])
+            zo.subspace_refresh(omegas, r, out=qouts)
             e1.record()
             rec["refresh"] = (e0, e1)
-        for i, mt in enumerate(mats):
+        for i, mt in enumerate(units):
             pl = plins[s][i]
             e0, e1, e2 = Ev(), Ev(), Ev()
             e0.record()
@@ -229,9 +300,10 @@ def main():
         step(s, s)
         torch.cuda.synchronize()
         log(f"warmup step {s} done")
-    for mt in mats:
-        mt["M1"].zero_()
-        mt["M2"].zero_()
+    for u in units:
+        for m1, m2 in u["mom"]:
+            m1.zero_()
+            m2.zero_()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -240,21 +312,29 @@ def main():
     t1 = time.perf_counter()
     log(f"timed {args.steps} steps in {t1 - t0:.2f} s")
 
-    step_flops = sum(plinear_flops(T, mt["m"], mt["n"], r, q) for mt in mats)
+    if lora:
+        layer_flops = lambda m, n: lora_flops(T, m, n, rl, r, q)
+        launch_flops = lambda m, n: lora_apply_flops(T, m, n, rl, r, q)
+        unit_bytes = lambda m, n: update_bytes(rl, n, r, q, 4) + update_bytes(m, rl, r, q, 4)
+    else:
+        layer_flops = lambda m, n: plinear_flops(T, m, n, r, q)
+        launch_flops = lambda m, n: apply_flops(T, m, n, r, q)
+        unit_bytes = lambda m, n: update_bytes(m, n, r, q)
+    step_flops = sum(layer_flops(u["m"], u["n"]) for u in units)
     value = step_flops * args.steps / (t1 - t0) / 1e12
     gemm_ms = sum(a.elapsed_time(b) for rc in recs for a, b, _, _ in rc["gemm"])
-    gemm_flops = sum(apply_flops(T, m, n, r, q) for rc in recs for _, _, m, n in rc["gemm"])
+    gemm_flops = sum(launch_flops(m, n) for rc in recs for _, _, m, n in rc["gemm"])
     n_gemm = sum(len(rc["gemm"]) for rc in recs)
     prep_ms = sum(a.elapsed_time(b) for rc in recs for a, b in rc["prep"])
     upd_ms = sum(rc["upd"][0].elapsed_time(rc["upd"][1]) for rc in recs)
-    upd_bytes = sum(update_bytes(mt["m"], mt["n"], r, q) for mt in mats) * args.steps
+    upd_bytes = sum(unit_bytes(u["m"], u["n"]) for u in units) * args.steps
     ref_ms = [rc["refresh"][0].elapsed_time(rc["refresh"][1]) for rc in recs if rc["refresh"]]
     per_shape = {}
     for rc in recs:
         for a, b, m, n in rc["gemm"]:
             d = per_shape.setdefault(f"{m}x{n}", [0.0, 0.0, 0])
             d[0] += a.elapsed_time(b)
-            d[1] += apply_flops(T, m, n, r, q)
+            d[1] += launch_flops(m, n)
             d[2] += 1
     achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
     traffic = None
@@ -267,16 +347,20 @@ def main():
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round((t1 - t0) / args.steps * 1e3, 2), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": f"{args.config}-shaped stack: {L} layers x "
-                               + ", ".join(f"{nm} {m}x{n}" for nm, m, n in cfg["mats"])
-                               + f"; {nblk} query blocks (q={q}, +/-) of T={T} tokens; r={r}; bf16 W and X",
-                   "layers": L, "matrices": len(mats), "T": T, "r": r, "q": q, "blocks": nblk, "refresh_every": F},
-        "roofline": {"kernel": "k_gemm_bf16 (zo_perturbed_linear_apply)", "bound": "mfma",
+        "config": {"workload": (f"{args.config}-shaped stack: {L} layers x "
+                                + ", ".join(f"{nm} {m}x{n}" for nm, m, n in unit_mats)
+                                + (f" (frozen bf16 base, fp32 LoRA adapter r_L={rl}, alpha={int(scale * rl)}, "
+                                   f"each factor in its own subspace)" if lora else "")
+                                + f"; {nblk} query blocks (q={q}, +/-) of T={T} tokens; r={r}; bf16 W and X"),
+                   "layers": L, "perturbed_layers": len(units), "T": T, "r": r, "q": q, "blocks": nblk,
+                   "refresh_every": F},
+        "roofline": {"kernel": "k_gemm_main (zo_perturbed_linear_apply)", "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "launches": n_gemm, "avg_launch_ms": round(gemm_ms / n_gemm, 4),
                      "flops_per_launch_avg": gemm_flops / n_gemm},
-        "update": {"kernel": "zo_subspace_adam_update (k_adam_rr + k_us + k_update_bf16)", "bound": "hbm",
+        "update": {"kernel": "zo_subspace_adam_update (k_adam_rr + k_us + "
+                             + ("k_update_f32, fp32 adapter factors)" if lora else "k_update_bf16)"), "bound": "hbm",
                    "achieved": round(upd_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                    "frac": round(upd_gbps / PEAK_HBM_GBPS, 4), "ms_per_step": round(upd_ms / args.steps, 3)},
         "prepare_ms_per_step": round(prep_ms / args.steps, 3),
@@ -285,9 +369,9 @@ def main():
                           for k, v in per_shape.items()},
     }
     if not args.no_cpu_baseline:
-        del plins, items, X, Y, ws
+        del plins, items, X, Y, ws, units
         torch.cuda.empty_cache()
-        out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget, unit_mats[0], lora)
     print(json.dumps(out), flush=True)
 
 
