@@ -341,36 +341,107 @@ __global__ __launch_bounds__(256) void k_pcombine(const float* __restrict__ P2, 
 // B_b[i][a] = s_b eps sum_c U[i][c] Z_{j(b)}[c][a] (a < r; 0 for r <= a < rp).
 // fp32 output: m x rp per block.  bf16 output: m x 3 rp per block as
 // [B_hi | B_lo | B_hi].
+// One workgroup forms C = eps U Z_j for 128 rows and one query j (U rows and Z_j
+// staged in LDS 32 columns of K at a time; each thread owns 4 rows x rp/8
+// adjacent columns), then writes s_b C for every block b of query j.  The
+// bf16 split is odd in its argument (round to nearest even is symmetric), so
+// the blocks of one query share one product.
+constexpr int BP_ROWS = 128;
+
+template <int RPK>
 __global__ __launch_bounds__(256) void k_bprime(const float* __restrict__ U,
                                                 const float* __restrict__ Z, int m, int r,
                                                 int rp, int nblk, float eps, BlkTable tab,
                                                 void* Bp, int out_bf16) {
-  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-  const long long per = (long long)m * rp;
-  if (idx >= per * nblk) return;
-  const int b = (int)(idx / per);
-  const long long rem = idx - (long long)b * per;
-  const int i = (int)(rem / rp), a = (int)(rem % rp);
-  float v = 0.f;
-  if (a < r) {
-    const int code = tab.code[b];
-    const int j = code & 0xffff;
-    const float s = (float)((code >> 16) - 1);
-    const float* __restrict__ Zj = Z + (size_t)j * r * r;
-    const float* __restrict__ Ui = U + (size_t)i * r;
-    float acc = 0.f;
-    for (int c = 0; c < r; ++c) acc = fmaf(Ui[c], Zj[c * r + a], acc);
-    v = s * eps * acc;
+  constexpr int RP = 32 * RPK;
+  constexpr int CPT = RP / 8;
+  __shared__ __attribute__((aligned(16))) float Ut[32][BP_ROWS + 4];
+  __shared__ __attribute__((aligned(16))) float Zl[32][RP];
+  const int j = blockIdx.y;
+  const int i0 = blockIdx.x * BP_ROWS;
+  const int tid = threadIdx.x, tr = tid >> 3, tc = tid & 7;
+  const float* __restrict__ Zj = Z + (size_t)j * r * r;
+  float acc[4][CPT];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < CPT; ++y) acc[x][y] = 0.f;
+  for (int kc = 0; kc < RPK; ++kc) {
+    if (kc) __syncthreads();
+    for (int x = tid; x < 32 * BP_ROWS; x += 256) {
+      const int i = x >> 5, kk = x & 31, t = kc * 32 + kk;
+      Ut[kk][i] = (i0 + i < m && t < r) ? U[(size_t)(i0 + i) * r + t] : 0.f;
+    }
+    for (int x = tid; x < 32 * RP; x += 256) {
+      const int kk = x / RP, c = x % RP, t = kc * 32 + kk;
+      Zl[kk][c] = (t < r && c < r) ? Zj[t * r + c] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int kk = 0; kk < 32; ++kk) {
+      const f32x4 u = *(const f32x4*)&Ut[kk][tr * 4];
+#pragma unroll
+      for (int y = 0; y < CPT; y += 4) {
+        const f32x4 z = *(const f32x4*)&Zl[kk][tc * CPT + y];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          acc[x][y] = fmaf(u[x], z[0], acc[x][y]);
+          acc[x][y + 1] = fmaf(u[x], z[1], acc[x][y + 1]);
+          acc[x][y + 2] = fmaf(u[x], z[2], acc[x][y + 2]);
+          acc[x][y + 3] = fmaf(u[x], z[3], acc[x][y + 3]);
+        }
+      }
+    }
   }
+  // hi / lo of eps C (the sign is applied per block below).
+  uint32_t hp[4][CPT / 2], lp[4][CPT / 2];
+  float v[4][CPT];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < CPT; ++y) v[x][y] = eps * acc[x][y];
   if (out_bf16) {
-    const bf16_t hi = f32_to_bf16(v);
-    const bf16_t lo = f32_to_bf16(v - bf16_to_f32(hi));
-    bf16_t* o = (bf16_t*)Bp + ((long long)b * m + i) * 3 * rp;
-    o[a] = hi;
-    o[rp + a] = lo;
-    o[2 * rp + a] = hi;
-  } else {
-    ((float*)Bp)[idx] = v;
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+      for (int y = 0; y < CPT; y += 2) {
+        const float a0 = v[x][y], a1 = v[x][y + 1];
+        hp[x][y / 2] = pack_bf16x2(a0, a1);
+        lp[x][y / 2] = pack_bf16x2(a0 - bf16_to_f32(f32_to_bf16(a0)), a1 - bf16_to_f32(f32_to_bf16(a1)));
+      }
+  }
+  for (int b = 0; b < nblk; ++b) {
+    const int code = tab.code[b];
+    if ((code & 0xffff) != j) continue;
+    const int s = (code >> 16) - 1;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int i = i0 + tr * 4 + x;
+      if (i >= m) break;
+      if (out_bf16) {
+        // Negation flips the sign bits; zero times the sign is +0.
+        const uint32_t flip = s < 0 ? 0x80008000u : 0u;
+        bf16_t* o = (bf16_t*)Bp + ((long long)b * m + i) * 3 * rp + tc * CPT;
+#pragma unroll
+        for (int y = 0; y < CPT; y += 4) {
+          uint32_t h0 = hp[x][y / 2], h1 = hp[x][y / 2 + 1], l0 = lp[x][y / 2], l1 = lp[x][y / 2 + 1];
+          if (s == 0) {
+            h0 = h1 = l0 = l1 = 0u;
+          } else {
+            h0 ^= flip; h1 ^= flip; l0 ^= flip; l1 ^= flip;
+          }
+          *(u32x2*)(o + y) = (u32x2){h0, h1};
+          *(u32x2*)(o + rp + y) = (u32x2){l0, l1};
+          *(u32x2*)(o + 2 * rp + y) = (u32x2){h0, h1};
+        }
+      } else {
+        // fp32 keeps rp == round16(r) wide rows; RP may exceed rp.
+        float* o = (float*)Bp + ((long long)b * m + i) * rp;
+#pragma unroll
+        for (int y = 0; y < CPT; ++y)
+          if (tc * CPT + y < rp) o[tc * CPT + y] = (float)s * v[x][y];
+      }
+    }
   }
 }
 
@@ -639,9 +710,17 @@ int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t*
   }
   {
     const BlkTable tab = zo_blk_table(p.nblk, blk_query, blk_sign);
-    const long long total = (long long)p.nblk * p.m * p.rp;
-    hipLaunchKernelGGL(k_bprime, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, U, Z,
-                       p.m, p.r, p.rp, p.nblk, eps, tab, w.bp, p.in_bf16);
+    const dim3 grid((unsigned)((p.m + BP_ROWS - 1) / BP_ROWS), (unsigned)p.q);
+    switch ((p.r + 31) / 32) {
+      case 1: hipLaunchKernelGGL(k_bprime<1>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+                                 eps, tab, w.bp, p.in_bf16); break;
+      case 2: hipLaunchKernelGGL(k_bprime<2>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+                                 eps, tab, w.bp, p.in_bf16); break;
+      case 3: hipLaunchKernelGGL(k_bprime<3>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+                                 eps, tab, w.bp, p.in_bf16); break;
+      default: hipLaunchKernelGGL(k_bprime<4>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+                                  eps, tab, w.bp, p.in_bf16); break;
+    }
     if ((st = zo_hip_status(hipGetLastError(), "k_bprime")) != ZO_OK) return st;
   }
   return zo_plinear_project(p, X, ws, stream);
