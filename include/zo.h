@@ -76,16 +76,21 @@ const char* zo_last_error_detail(void);
  * Q_p^T Q_p = I and R_p upper triangular with a POSITIVE diagonal, i.e. the
  * Q of any thin QR with each column multiplied by the sign of the matching
  * R diagonal entry.  This factor is unique, and for Gaussian Omega it is
- * Haar distributed.  Computed by Householder reflections in float64 (tall
- * panels as a tree of row blocks); outputs rounded once to float32.
+ * Haar distributed.  Computed in float64 by CholeskyQR2 (R1 = chol(O^T O),
+ * Q1 = O R1^-1, R2 = chol(Q1^T Q1), Q = Q1 R2^-1), whose Cholesky factors
+ * have a positive diagonal, so the sign correction is built in; outputs
+ * rounded once to float32.  Accurate to working precision while
+ * cond(Omega)^2 * 1e-16 << 1, which Gaussian panels with rows >= r meet
+ * with overwhelming probability.  Bitwise reproducible.
  *
  *   omega   device, rows x r fp32, row-major; read only.
  *   q       device, rows x r fp32 output; may alias omega.
  *   r_diag  device, r fp32 output (diag of the corrected R, > 0); nullable.
  *   info    device, `count` ints, nullable: info[p] = 0, or k+1 when the
- *           first zero diagonal entry of R_p is at column k (Omega_p rank
- *           deficient).  Such a column gets sign +1 (sgn(0) := +1); its Q
- *           column is not meaningful.
+ *           first Cholesky pivot that is not positive is at column k
+ *           (Omega_p rank deficient; an exactly zero column gives this).
+ *           R_kk is then reported as 0, the Q column is zero and the other
+ *           columns are formed as if column k were absent.
  * Limits: 1 <= r <= ZO_MAX_QR_RANK, rows <= 2^26.  Panels of one call share
  * r; rows may differ.
  * ------------------------------------------------------------------------ */

@@ -2,353 +2,332 @@
 // (Eq. 11, Alg. 1) -- thin QR with each column of Q multiplied by the sign of
 // the matching diagonal entry of R, so the corrected R has diag(R) > 0.
 //
-// Tall-skinny QR as a reduction tree (TSQR) of Householder factorisations,
-// float64 throughout:
-//   up pass    level 0: each leaf is a block of at most BMAX rows of the
-//              panel; level l >= 1: each node stacks the R factors (r x r) of
-//              up to G children.  A node loads its block into LDS
-//              (column-major float64), runs r Householder steps (one wave
-//              per trailing column: dot product by wave reduction, then the
-//              rank-1 update), writes its R, then forms its explicit Q in
-//              place by backward accumulation and writes it.
-//   down pass  from the root: the root's Q is multiplied by diag(s),
-//              s_k = sgn(R_kk) with sgn(0) = +1; every child's Q is
-//              multiplied by its r x r slice of the parent's final Q.  The
-//              leaves write the float32 panel output.
-// The final Q equals the panel's unique thin-QR factor with positive
-// diag(R), whatever sign convention the reflectors use.
+// That corrected factor is the unique Q with Q^T Q = I and Omega = Q R,
+// diag(R) > 0.  It is computed here by CholeskyQR2 in float64 (Fukaya,
+// Nakatsukasa, Yanagisawa, Yamamoto, 2014): R1 = chol(Omega^T Omega),
+// Q1 = Omega R1^-1, R2 = chol(Q1^T Q1), Q = Q1 R2^-1, R = R2 R1.  A Cholesky
+// factor has a positive diagonal, so the sign correction is built in.  The
+// second pass restores orthogonality to working precision whenever
+// cond(Omega)^2 u << 1, which Gaussian panels with rows >= r satisfy with
+// overwhelming probability (their condition number is about
+// (sqrt(rows) + sqrt(r)) / (sqrt(rows) - sqrt(r))).
+//
+// Five launches per batch of panels, all float64 with fixed-order sums (the
+// result is bitwise reproducible):
+//   k_cqr_rows<0>  per chunk of CHUNK rows: partial Omega^T Omega
+//   k_cqr_chol     per panel: sum of the partials, Cholesky -> R1, and
+//                  X1 = R1^-1 (rows of the identity through forward substitution)
+//   k_cqr_rows<1>  per chunk: Q1 = Omega X1, partial Q1^T Q1
+//   k_cqr_chol     per panel: R2, X2 = R2^-1, M = X1 X2; diag(R) = diag(R2) diag(R1); info
+//   k_cqr_rows<2>  per chunk: Q = Omega M, written as fp32
+// The row passes are small dense products (4 x 4 register tiles, operands in LDS).
+// A pivot that is not positive marks the panel rank deficient at that column
+// (an exactly zero column gives a zero pivot): R's row there is zero, the Q
+// column is zero, and the other columns are formed as if it were absent.
 #include "zo_internal.h"
 
 #include <vector>
 
 namespace {
 
-constexpr int NT = 256;
-constexpr int LDS_DOUBLES = 16384;  // 128 KB node block (plus padding of the leading dimension)
-constexpr int MAX_LEAF_ROWS = 1024;
-constexpr int MAX_FANIN = 16;
-constexpr int PANELS_PER_LAUNCH = 16;  // keeps the kernel-argument struct under 2 KB
+constexpr int ROWS_WG = 128;     // rows held per pass of a workgroup (one per thread)
+constexpr int CHUNK = 1024;      // rows per workgroup (8 passes of ROWS_WG)
+constexpr int PANELS_PER_LAUNCH = 48;
 
-struct QrEntry {
+struct CqrPanel {
   const float* omega;
   float* q;
   float* r_diag;
   int* info;
-  double* Qn;         // Q of this level's nodes
-  double* Rn;         // R of this level's nodes (r x r each)
-  const double* Rc;   // children's R (up pass, level >= 1)
-  const double* Mp;   // parent's final Q (down pass, below the top)
-  double* Qf;         // this level's final Q (down pass, level >= 1)
-  int rows, nodes, child_nodes, G, leaf_base, leaf_extra, is_top, wg_begin;
+  double* part;  // partial Gram matrices, one RP x RP per chunk
+  double* R1;    // RP x RP: R1 (its diagonal is needed at the end)
+  double* X1;    // RP x RP: R1^-1
+  double* M;     // RP x RP: R1^-1 R2^-1
+  int rows, chunk_begin;
 };
-struct QrArgs {
-  QrEntry e[PANELS_PER_LAUNCH];
-  int count, r, level;
+struct CqrArgs {
+  CqrPanel p[PANELS_PER_LAUNCH];
+  int count, r;
 };
 
-__device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
-}
-
-__device__ __forceinline__ int find_entry(const QrArgs& a) {
+__device__ __forceinline__ int find_panel(const CqrArgs& a, int wg) {
   int k = 0;
-  while (k + 1 < a.count && (int)blockIdx.x >= a.e[k + 1].wg_begin) ++k;
+  while (k + 1 < a.count && wg >= a.p[k + 1].chunk_begin) ++k;
   return k;
 }
 
-__device__ __forceinline__ void leaf_rows(const QrEntry& e, int node, int* rs, int* nr) {
-  *rs = node * e.leaf_base + min(node, e.leaf_extra);
-  *nr = e.leaf_base + (node < e.leaf_extra ? 1 : 0);
-}
-
-// Householder QR of the nr x r block in LDS (column-major, leading dim ld).
-// On return the upper triangle holds R, the reflector vectors (v_0 = 1
-// implied) sit below the diagonal and tau[] holds their scalars.
-__device__ void householder_lds(double* A, int ld, int nr, int r, double* tau, double* red) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int k = 0; k < r; ++k) {
-    double* ck = A + (size_t)k * ld;
-    double s = 0.0;
-    for (int i = k + 1 + tid; i < nr; i += NT) s += ck[i] * ck[i];
-    s = wave_sum(s);
-    if (lane == 0) red[wave] = s;
-    __syncthreads();
-    if (tid == 0) {
-      const double xn2 = (red[0] + red[1]) + (red[2] + red[3]);
-      const double alpha = ck[k];
-      double t = 0.0, scale = 0.0, beta = alpha;
-      if (xn2 > 0.0) {
-        beta = -copysign(sqrt(alpha * alpha + xn2), alpha);
-        t = (beta - alpha) / beta;
-        scale = 1.0 / (alpha - beta);
-      }
-      tau[k] = t;
-      red[4] = scale;
-      ck[k] = beta;
+// Y = X Mx for a block of ROWS_WG rows (X, Y in rowbuf, Mx RP x RP in LDS);
+// each thread owns RK tiles of 4 rows x 4 columns.
+template <int RP>
+__device__ __forceinline__ void block_product(double (*rowbuf)[RP + 1], const double* Mx) {
+  constexpr int CG = RP / 4;                 // column groups
+  constexpr int TPT = ROWS_WG / 4 * CG / ROWS_WG;  // tiles per thread (= RP / 16)
+  const int tid = threadIdx.x;
+  double acc[TPT][4][4];
+#pragma unroll
+  for (int t = 0; t < TPT; ++t)
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[t][u][v] = 0.0;
+  for (int k = 0; k < RP; ++k) {
+#pragma unroll
+    for (int t = 0; t < TPT; ++t) {
+      const int tile = tid + t * ROWS_WG, rg = tile / CG, cg = tile % CG;
+      double a[4], m[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a[u] = rowbuf[4 * rg + u][k];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) m[v] = Mx[k * RP + 4 * cg + v];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[t][u][v] = fma(a[u], m[v], acc[t][u][v]);
     }
-    __syncthreads();
-    const double scale = red[4];
-    const double tk = tau[k];
-    if (tk != 0.0)
-      for (int i = k + 1 + tid; i < nr; i += NT) ck[i] *= scale;
-    __syncthreads();
-    if (tk != 0.0) {
-      for (int j = k + 1 + wave; j < r; j += NT / 64) {
-        double* cj = A + (size_t)j * ld;
-        double w = 0.0;
-        for (int i = k + 1 + lane; i < nr; i += 64) w += ck[i] * cj[i];
-        w = wave_sum(w) + cj[k];
-        const double tw = tk * w;
-        for (int i = k + 1 + lane; i < nr; i += 64) cj[i] -= tw * ck[i];
-        if (lane == 0) cj[k] -= tw;
-      }
-    }
-    __syncthreads();
   }
-}
-
-// Explicit thin Q (nr x r) from the reflectors, in place (backward accumulation).
-__device__ void form_q_lds(double* A, int ld, int nr, int r, const double* tau) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int k = r - 1; k >= 0; --k) {
-    double* ck = A + (size_t)k * ld;
-    const double tk = tau[k];
-    if (tk != 0.0) {
-      for (int j = k + 1 + wave; j < r; j += NT / 64) {
-        double* cj = A + (size_t)j * ld;
-        double w = 0.0;
-        for (int i = k + 1 + lane; i < nr; i += 64) w += ck[i] * cj[i];
-        w = wave_sum(w) + cj[k];
-        const double tw = tk * w;
-        for (int i = k + 1 + lane; i < nr; i += 64) cj[i] -= tw * ck[i];
-        if (lane == 0) cj[k] -= tw;
-      }
-    }
-    __syncthreads();
-    for (int i = tid; i < nr; i += NT) {
-      double v;
-      if (i < k) v = 0.0;
-      else if (i == k) v = 1.0 - tk;
-      else v = -tk * ck[i];
-      ck[i] = v;
-    }
-    __syncthreads();
-  }
-}
-
-__global__ __launch_bounds__(NT) void k_qr_up(QrArgs a) {
-  __shared__ double A[LDS_DOUBLES + ZO_MAX_QR_RANK];
-  __shared__ double tau[ZO_MAX_QR_RANK];
-  __shared__ double red[8];
-  const QrEntry& e = a.e[find_entry(a)];
-  const int node = blockIdx.x - e.wg_begin;
-  const int r = a.r, tid = threadIdx.x;
-  int nr, ld;
-  double* qout;
-  if (a.level == 0) {
-    int rs;
-    leaf_rows(e, node, &rs, &nr);
-    ld = nr | 1;  // odd leading dimension: column-strided LDS access spreads over banks
-    for (int x = tid; x < nr * r; x += NT) {
-      const int i = x / r, c = x % r;
-      A[(size_t)c * ld + i] = (double)e.omega[(size_t)(rs + i) * r + c];
-    }
-    qout = e.Qn + (size_t)rs * r;
-  } else {
-    const int c0 = node * e.G;
-    const int c1 = min(c0 + e.G, e.child_nodes);
-    nr = (c1 - c0) * r;
-    ld = nr | 1;
-    const double* src = e.Rc + (size_t)c0 * r * r;  // stacked r x r row-major blocks
-    for (int x = tid; x < nr * r; x += NT) {
-      const int i = x / r, c = x % r;
-      A[(size_t)c * ld + i] = src[x];
-    }
-    qout = e.Qn + (size_t)node * e.G * r * r;
+  __syncthreads();  // every thread has read its rows of X
+#pragma unroll
+  for (int t = 0; t < TPT; ++t) {
+    const int tile = tid + t * ROWS_WG, rg = tile / CG, cg = tile % CG;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) rowbuf[4 * rg + u][4 * cg + v] = acc[t][u][v];
   }
   __syncthreads();
-  householder_lds(A, ld, nr, r, tau, red);
-  double* Rout = e.Rn + (size_t)node * r * r;
-  for (int x = tid; x < r * r; x += NT) {
-    const int i = x / r, c = x % r;
-    Rout[x] = i <= c ? A[(size_t)c * ld + i] : 0.0;
+}
+
+// PASS 0: partial Omega^T Omega of this chunk.  PASS 1: partial Q1^T Q1 with
+// Q1 = Omega X1.  PASS 2: Q = Omega M written as fp32.  Rows move between
+// global memory and LDS as contiguous blocks.
+template <int RK, int PASS>
+__global__ __launch_bounds__(ROWS_WG) void k_cqr_rows(CqrArgs a) {
+  constexpr int RP = 16 * RK;
+  constexpr int NB = RP / 4;                  // 4 x 4 blocks per side
+  constexpr int NBLK = NB * (NB + 1) / 2;     // upper-triangular blocks
+  constexpr int BPT = (NBLK + ROWS_WG - 1) / ROWS_WG;
+  __shared__ double Mx[PASS == 0 ? 1 : RP * RP];
+  __shared__ double rowbuf[ROWS_WG][RP + 1];
+  const CqrPanel& P = a.p[find_panel(a, blockIdx.x)];
+  const int chunk = blockIdx.x - P.chunk_begin;
+  const int r = a.r, tid = threadIdx.x;
+  if (PASS >= 1) {
+    const double* src = PASS == 1 ? P.X1 : P.M;
+    for (int x = tid; x < RP * RP; x += ROWS_WG) Mx[x] = src[x];
   }
-  if (e.is_top && tid == 0) {
+  // Padding columns r .. RP-1 stay zero in every row.
+  for (int x = tid; x < ROWS_WG * (RP - r); x += ROWS_WG) rowbuf[x / (RP - r)][r + x % (RP - r)] = 0.0;
+  // Gram blocks owned by this thread: (bi, bj) with bi <= bj, enumerated row-major.
+  int bi[BPT], bj[BPT];
+  double g[BPT][4][4];
+#pragma unroll
+  for (int t = 0; t < BPT; ++t) {
+    int b = tid + t * ROWS_WG, ii = 0;
+    if (b >= NBLK) b = -1;
+    if (b >= 0) {
+      int rem = b;
+      while (rem >= NB - ii) { rem -= NB - ii; ++ii; }
+      bi[t] = ii;
+      bj[t] = ii + rem;
+    } else {
+      bi[t] = bj[t] = -1;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) g[t][u][v] = 0.0;
+  }
+  const int row_end = min((chunk + 1) * CHUNK, P.rows);
+  for (int base = chunk * CHUNK; base < row_end; base += ROWS_WG) {
+    const int nrow = min(ROWS_WG, row_end - base);
+    __syncthreads();  // the previous block's rows have been consumed
+    {
+      const float* src = P.omega + (size_t)base * r;
+      for (int x = tid; x < nrow * r; x += ROWS_WG) rowbuf[x / r][x % r] = (double)src[x];
+      // Rows past the panel's end multiply as zeros.
+      for (int x = tid; x < (ROWS_WG - nrow) * r; x += ROWS_WG) rowbuf[nrow + x / r][x % r] = 0.0;
+    }
+    __syncthreads();
+    if (PASS >= 1) block_product<RP>(rowbuf, Mx);
+    if (PASS == 2) {
+      float* dst = P.q + (size_t)base * r;
+      for (int x = tid; x < nrow * r; x += ROWS_WG) dst[x] = (float)rowbuf[x / r][x % r];
+      continue;
+    }
+    for (int rr = 0; rr < nrow; ++rr) {
+      const double* row = rowbuf[rr];
+#pragma unroll
+      for (int t = 0; t < BPT; ++t) {
+        if (bi[t] < 0) continue;
+        double u[4], v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          u[e] = row[4 * bi[t] + e];
+          v[e] = row[4 * bj[t] + e];
+        }
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) g[t][p][q] = fma(u[p], v[q], g[t][p][q]);
+      }
+    }
+  }
+  if (PASS == 2) return;
+  double* out = P.part + (size_t)chunk * RP * RP;
+#pragma unroll
+  for (int t = 0; t < BPT; ++t) {
+    if (bi[t] < 0) continue;
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) out[(size_t)(4 * bi[t] + p) * RP + 4 * bj[t] + q] = g[t][p][q];
+  }
+}
+
+// Sum of the chunk partials (upper triangle, chunk order) and the Cholesky
+// factor G = R^T R, row by row: R_kk = sqrt(G_kk - sum_{i<k} R_ik^2),
+// R_kj = (G_kj - sum_{i<k} R_ik R_ij) / R_kk (a pivot that is not positive
+// gives a zero row).  Then X = R^-1 row by row: row i of X is e_i pushed
+// through the forward substitution x_j = (x_j - sum_{l<j} x_l R_lj) / R_jj
+// (zero where R_jj = 0), so Omega X is exactly that substitution applied to
+// Omega's rows.  FINAL: this is R2; M = X1 X2, diag(R) = diag(R2) diag(R1), info.
+template <int RK, bool FINAL>
+__global__ __launch_bounds__(256) void k_cqr_chol(CqrArgs a) {
+  constexpr int RP = 16 * RK;
+  __shared__ double G[RP * RP];
+  __shared__ double X[RP * RP];
+  __shared__ double inv[RP];
+  const CqrPanel& P = a.p[blockIdx.x];
+  const int r = a.r, tid = threadIdx.x;
+  const int nchunk = (P.rows + CHUNK - 1) / CHUNK;
+  for (int x = tid; x < RP * RP; x += 256) {
+    const int i = x / RP, j = x % RP;
+    double s = 0.0;
+    if (i <= j && j < r)
+      for (int c = 0; c < nchunk; ++c) s += P.part[(size_t)c * RP * RP + x];
+    G[x] = s;
+  }
+  __syncthreads();
+  for (int k = 0; k < r; ++k) {
+    if (tid == 0) {
+      double d = G[k * RP + k];
+      for (int i = 0; i < k; ++i) d = fma(-G[i * RP + k], G[i * RP + k], d);
+      G[k * RP + k] = d > 0.0 ? sqrt(d) : 0.0;
+    }
+    __syncthreads();
+    const double rkk = G[k * RP + k];
+    for (int j = k + 1 + tid; j < r; j += 256) {
+      double s = G[k * RP + j];
+      for (int i = 0; i < k; ++i) s = fma(-G[i * RP + k], G[i * RP + j], s);
+      G[k * RP + j] = rkk > 0.0 ? s / rkk : 0.0;
+    }
+    __syncthreads();
+  }
+  for (int j = tid; j < RP; j += 256) {
+    const double d = j < r ? G[j * RP + j] : 0.0;
+    inv[j] = d > 0.0 ? 1.0 / d : 0.0;
+  }
+  __syncthreads();
+  if (tid < RP) {
+    double x[RP];
+#pragma unroll
+    for (int j = 0; j < RP; ++j) {
+      double s = j == tid ? 1.0 : 0.0;
+#pragma unroll
+      for (int l = 0; l < j; ++l) s = fma(-x[l], G[l * RP + j], s);
+      x[j] = s * inv[j];
+    }
+#pragma unroll
+    for (int j = 0; j < RP; ++j) X[tid * RP + j] = x[j];
+  }
+  __syncthreads();
+  if (!FINAL) {
+    for (int x = tid; x < RP * RP; x += 256) {
+      const int i = x / RP, j = x % RP;
+      P.R1[x] = i <= j ? G[x] : 0.0;
+      P.X1[x] = X[x];
+    }
+    return;
+  }
+  for (int x = tid; x < RP * RP; x += 256) {
+    const int i = x / RP, j = x % RP;
+    double s = 0.0;
+    for (int k = 0; k < RP; ++k) s = fma(P.X1[i * RP + k], X[k * RP + j], s);
+    P.M[x] = s;
+  }
+  if (tid == 0) {
     int bad = 0;
     for (int k = 0; k < r; ++k) {
-      const double d = A[(size_t)k * ld + k];
-      if (e.r_diag) e.r_diag[k] = (float)fabs(d);
+      const double d = G[k * RP + k] * P.R1[k * RP + k];
+      if (P.r_diag) P.r_diag[k] = (float)d;
       if (d == 0.0 && bad == 0) bad = k + 1;
     }
-    if (e.info) *e.info = bad;
-  }
-  __syncthreads();
-  form_q_lds(A, ld, nr, r, tau);
-  for (int x = tid; x < nr * r; x += NT) {
-    const int i = x / r, c = x % r;
-    qout[x] = A[(size_t)c * ld + i];
+    if (P.info) *P.info = bad;
   }
 }
 
-__global__ __launch_bounds__(NT) void k_qr_down(QrArgs a) {
-  __shared__ double M[ZO_MAX_QR_RANK * ZO_MAX_QR_RANK];
-  const QrEntry& e = a.e[find_entry(a)];
-  const int node = blockIdx.x - e.wg_begin;
-  const int r = a.r, tid = threadIdx.x;
-  if (e.is_top) {
-    const double* R = e.Rn;  // the root's R
-    for (int x = tid; x < r * r; x += NT) {
-      const int i = x / r, c = x % r;
-      M[x] = i == c ? (R[(size_t)i * r + i] < 0.0 ? -1.0 : 1.0) : 0.0;
-    }
-  } else {
-    const int p = node / e.G, cl = node % e.G;
-    const double* src = e.Mp + ((size_t)p * e.G + cl) * r * r;
-    for (int x = tid; x < r * r; x += NT) M[x] = src[x];
-  }
-  __syncthreads();
-  int nr;
-  const double* Qsrc;
-  if (a.level == 0) {
-    int rs;
-    leaf_rows(e, node, &rs, &nr);
-    Qsrc = e.Qn + (size_t)rs * r;
-    float* out = e.q + (size_t)rs * r;
-    for (int x = tid; x < nr * r; x += NT) {
-      const int i = x / r, c = x % r;
-      const double* qi = Qsrc + (size_t)i * r;
-      double s = 0.0;
-      for (int k = 0; k < r; ++k) s += qi[k] * M[k * r + c];
-      out[x] = (float)s;
-    }
-  } else {
-    const int c0 = node * e.G;
-    const int c1 = min(c0 + e.G, e.child_nodes);
-    nr = (c1 - c0) * r;
-    Qsrc = e.Qn + (size_t)node * e.G * r * r;
-    double* out = e.Qf + (size_t)node * e.G * r * r;
-    for (int x = tid; x < nr * r; x += NT) {
-      const int i = x / r, c = x % r;
-      const double* qi = Qsrc + (size_t)i * r;
-      double s = 0.0;
-      for (int k = 0; k < r; ++k) s += qi[k] * M[k * r + c];
-      out[x] = s;
-    }
-  }
+size_t panel_ws(int rows, int RP) {
+  const size_t nchunk = (size_t)(rows + CHUNK - 1) / CHUNK;
+  return zo_align256(nchunk * RP * RP * 8) + 3 * zo_align256((size_t)RP * RP * 8);
 }
 
-struct PanelPlan {
-  int rows, nleaf, G, top, leaf_base, leaf_extra;
-  std::vector<int> nodes;           // per level
-  std::vector<size_t> q_off, r_off, qf_off;  // doubles, per level
-  size_t q_total, r_total, qf_total;
-};
-
-PanelPlan plan_panel(int rows, int r) {
-  PanelPlan p;
-  p.rows = rows;
-  int bmax = LDS_DOUBLES / r;
-  if (bmax > MAX_LEAF_ROWS) bmax = MAX_LEAF_ROWS;
-  p.G = bmax / r;
-  if (p.G > MAX_FANIN) p.G = MAX_FANIN;
-  p.nleaf = (rows + bmax - 1) / bmax;
-  p.leaf_base = rows / p.nleaf;
-  p.leaf_extra = rows % p.nleaf;
-  p.nodes.push_back(p.nleaf);
-  while (p.nodes.back() > 1) p.nodes.push_back((p.nodes.back() + p.G - 1) / p.G);
-  p.top = (int)p.nodes.size() - 1;
-  size_t q = 0, rr = 0, qf = 0;
-  for (int l = 0; l <= p.top; ++l) {
-    p.q_off.push_back(q);
-    p.r_off.push_back(rr);
-    p.qf_off.push_back(qf);
-    if (l == 0) {
-      q += (size_t)rows * r;
-    } else {
-      q += (size_t)p.nodes[l] * p.G * r * r;
-      qf += (size_t)p.nodes[l] * p.G * r * r;
-    }
-    rr += (size_t)p.nodes[l] * r * r;
-  }
-  p.q_total = q;
-  p.r_total = rr;
-  p.qf_total = qf;
-  return p;
+template <int RK>
+int run_batch(const CqrArgs& ca, int wg, hipStream_t stream) {
+  int st;
+  hipLaunchKernelGGL((k_cqr_rows<RK, 0>), dim3(wg), dim3(ROWS_WG), 0, stream, ca);
+  if ((st = zo_hip_status(hipGetLastError(), "k_cqr_rows")) != ZO_OK) return st;
+  hipLaunchKernelGGL((k_cqr_chol<RK, false>), dim3(ca.count), dim3(256), 0, stream, ca);
+  if ((st = zo_hip_status(hipGetLastError(), "k_cqr_chol")) != ZO_OK) return st;
+  hipLaunchKernelGGL((k_cqr_rows<RK, 1>), dim3(wg), dim3(ROWS_WG), 0, stream, ca);
+  if ((st = zo_hip_status(hipGetLastError(), "k_cqr_rows")) != ZO_OK) return st;
+  hipLaunchKernelGGL((k_cqr_chol<RK, true>), dim3(ca.count), dim3(256), 0, stream, ca);
+  if ((st = zo_hip_status(hipGetLastError(), "k_cqr_chol")) != ZO_OK) return st;
+  hipLaunchKernelGGL((k_cqr_rows<RK, 2>), dim3(wg), dim3(ROWS_WG), 0, stream, ca);
+  return zo_hip_status(hipGetLastError(), "k_cqr_rows");
 }
 
 }  // namespace
 
 int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void* ws,
                       size_t ws_bytes, hipStream_t stream, size_t* ws_needed) {
-  std::vector<PanelPlan> plans;
-  plans.reserve(count);
+  const int RK = (r + 15) / 16;
+  const int RP = 16 * RK;
   size_t need = 0;
-  int max_top = 0;
-  for (int p = 0; p < count; ++p) {
-    plans.push_back(plan_panel(panels[p].rows, r));
-    const PanelPlan& pl = plans.back();
-    need += zo_align256(pl.q_total * 8) + zo_align256(pl.r_total * 8) + zo_align256(pl.qf_total * 8);
-    if (pl.top > max_top) max_top = pl.top;
-  }
+  for (int p = 0; p < count; ++p) need += panel_ws(panels[p].rows, RP);
   if (ws_needed) *ws_needed = need;
   if (!ws) return ZO_OK;
   if (ws_bytes < need) {
     zo_set_error("refresh: workspace %zu bytes < required %zu", ws_bytes, need);
     return ZO_ERR_WORKSPACE;
   }
-  std::vector<double*> qb(count), rb(count), qfb(count);
   WsCarver wc(ws);
-  for (int p = 0; p < count; ++p) {
-    qb[p] = (double*)wc.take(plans[p].q_total * 8);
-    rb[p] = (double*)wc.take(plans[p].r_total * 8);
-    qfb[p] = (double*)wc.take(plans[p].qf_total * 8);
-  }
   int st;
-  // Up pass, level by level; down pass from the highest root to the leaves.
-  for (int pass = 0; pass < 2; ++pass) {
-    for (int step = 0; step <= max_top; ++step) {
-      const int level = pass == 0 ? step : max_top - step;
-      for (int c0 = 0; c0 < count; c0 += PANELS_PER_LAUNCH) {
-        QrArgs qa{};
-        qa.r = r;
-        qa.level = level;
-        int n = 0, wg = 0;
-        for (int p = c0; p < count && p < c0 + PANELS_PER_LAUNCH; ++p) {
-          const PanelPlan& pl = plans[p];
-          if (level > pl.top) continue;
-          QrEntry e{};
-          e.omega = panels[p].omega;
-          e.q = panels[p].q;
-          e.r_diag = panels[p].r_diag;
-          e.info = info ? info + p : nullptr;
-          e.Qn = qb[p] + pl.q_off[level];
-          e.Rn = rb[p] + pl.r_off[level];
-          e.Rc = level > 0 ? rb[p] + pl.r_off[level - 1] : nullptr;
-          e.Mp = level < pl.top ? qfb[p] + pl.qf_off[level + 1] : nullptr;
-          e.Qf = level > 0 ? qfb[p] + pl.qf_off[level] : nullptr;
-          e.rows = pl.rows;
-          e.nodes = pl.nodes[level];
-          e.child_nodes = level > 0 ? pl.nodes[level - 1] : 0;
-          e.G = pl.G;
-          e.leaf_base = pl.leaf_base;
-          e.leaf_extra = pl.leaf_extra;
-          e.is_top = level == pl.top;
-          e.wg_begin = wg;
-          wg += e.nodes;
-          qa.e[n++] = e;
-        }
-        if (n == 0) continue;
-        qa.count = n;
-        if (pass == 0)
-          hipLaunchKernelGGL(k_qr_up, dim3(wg), dim3(NT), 0, stream, qa);
-        else
-          hipLaunchKernelGGL(k_qr_down, dim3(wg), dim3(NT), 0, stream, qa);
-        if ((st = zo_hip_status(hipGetLastError(), pass == 0 ? "k_qr_up" : "k_qr_down")) != ZO_OK)
-          return st;
-      }
+  for (int c0 = 0; c0 < count; c0 += PANELS_PER_LAUNCH) {
+    CqrArgs ca{};
+    ca.r = r;
+    int wg = 0;
+    for (int p = c0; p < count && p < c0 + PANELS_PER_LAUNCH; ++p) {
+      CqrPanel& e = ca.p[ca.count++];
+      const int nchunk = (panels[p].rows + CHUNK - 1) / CHUNK;
+      e.omega = panels[p].omega;
+      e.q = panels[p].q;
+      e.r_diag = panels[p].r_diag;
+      e.info = info ? info + p : nullptr;
+      e.part = (double*)wc.take((size_t)nchunk * RP * RP * 8);
+      e.R1 = (double*)wc.take((size_t)RP * RP * 8);
+      e.X1 = (double*)wc.take((size_t)RP * RP * 8);
+      e.M = (double*)wc.take((size_t)RP * RP * 8);
+      e.rows = panels[p].rows;
+      e.chunk_begin = wg;
+      wg += nchunk;
     }
+    switch (RK) {
+      case 1: st = run_batch<1>(ca, wg, stream); break;
+      case 2: st = run_batch<2>(ca, wg, stream); break;
+      case 3: st = run_batch<3>(ca, wg, stream); break;
+      default: st = run_batch<4>(ca, wg, stream); break;
+    }
+    if (st != ZO_OK) return st;
   }
   return ZO_OK;
 }
