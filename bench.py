@@ -35,27 +35,29 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def plinear_flops(T, m, n, r, q):
-    """Algorithmic FLOPs of one matrix's perturbed linear per step (all 2q blocks):
-    the X_b V projections, the q products U Z_j, the main products and the rank-r terms."""
-    return 2 * q * (2 * T * m * n + 2 * T * n * r + 2 * T * r * m) + q * 2 * m * r * r
+def plinear_flops(T, m, n, r, q, nblk, nsigned):
+    """Algorithmic FLOPs of one matrix's perturbed linear per step: the main products of all
+    nblk blocks, the X_b V projections of all blocks, the rank-r terms of the nsigned perturbed
+    blocks and the q products U Z_j."""
+    return nblk * (2 * T * m * n + 2 * T * n * r) + nsigned * 2 * T * r * m + q * 2 * m * r * r
 
 
-def apply_flops(T, m, n, r, q):
-    """Algorithmic FLOPs of the fused GEMM launch alone: X_b W^T and the rank-r term."""
-    return 2 * q * (2 * T * m * n + 2 * T * r * m)
+def apply_flops(T, m, n, r, q, nblk, nsigned):
+    """Algorithmic FLOPs of the fused GEMM launch alone: X_b W^T and the rank-r terms."""
+    return nblk * 2 * T * m * n + nsigned * 2 * T * r * m
 
 
-def lora_flops(T, m, n, rl, r, q):
-    """Algorithmic FLOPs of one LoRA-adapted layer per step (all 2q blocks): the frozen-base
-    products, the X_b [A^T | V_A] projections and the rank-(rl + r) terms, and the per-block
+def lora_flops(T, m, n, rl, r, q, nblk, nsigned):
+    """Algorithmic FLOPs of one LoRA-adapted layer per step: the frozen-base products, the
+    X_b [A^T | V_A] projections, the rank-(rl + r) terms of the perturbed blocks, and the per-block
     right factors scale [B' | s eps B' U_A Z_A]."""
     re = rl + r
-    return 2 * q * (2 * T * m * n + 2 * T * n * re + 2 * T * re * m) + 2 * q * m * (2 * r * rl + 2 * rl * r)
+    return (nblk * (2 * T * m * n + 2 * T * n * re) + nsigned * 2 * T * re * m
+            + nsigned * m * (2 * r * rl + 2 * rl * r))
 
 
-def lora_apply_flops(T, m, n, rl, r, q):
-    return 2 * q * (2 * T * m * n + 2 * T * (rl + r) * m)
+def lora_apply_flops(T, m, n, rl, r, q, nblk, nsigned):
+    return nblk * 2 * T * m * n + nsigned * 2 * T * (rl + r) * m
 
 
 def update_bytes(m, n, r, q, wbytes=2):
@@ -149,6 +151,9 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="opt-13b", choices=["opt-1.3b", "llama-7b", "opt-13b", "qwen-32b-lora"])
+    ap.add_argument("--estimator", default="central", choices=["central", "forward"],
+                    help="central: 2q blocks (+/-); forward: a baseline block and q perturbed blocks (Eq. 6)")
+    ap.add_argument("--queries", type=int, default=0, help="queries per step (default: the config's q)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -174,7 +179,16 @@ def main():
     cfg = zd.CONFIGS[args.config]
     lora = args.config.endswith("-lora")
     T, r, q = cfg["T"], cfg["r"], cfg["q"]
-    nblk = 2 * q
+    if args.queries:
+        q = args.queries
+    forward = args.estimator == "forward"
+    # Query blocks: central -- (j, +), (j, -); forward -- the baseline (sign 0), then (j, +).
+    if forward:
+        bq, bs = [0] + list(range(q)), [0] + [1] * q
+    else:
+        bq, bs = [b // 2 for b in range(2 * q)], [1 if b % 2 == 0 else -1 for b in range(2 * q)]
+    nblk = len(bq)
+    nsigned = sum(1 for v in bs if v != 0)
     L = cfg["layers"]
     eps, lr, b1, b2, ea, F = cfg["eps"], cfg["lr"], cfg["beta1"], cfg["beta2"], cfg["eps_adam"], cfg["F"]
     rl, scale = zd.QWEN_LORA_RANK, zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
@@ -231,8 +245,6 @@ def main():
                                    for t in range(nsteps)])).to(dev)  # [step, factor, q, r, r]
     m_last = unit_mats[-1][1]
     Ystar = to_bf16(zd.draw(seed, "X", (T, m_last, 1), (T, m_last)))
-    bq = [b // 2 for b in range(nblk)]
-    bs = [1 if b % 2 == 0 else -1 for b in range(nblk)]
     if lora:
         ws_need = max(zo.lib().zo_lora_perturbed_linear_workspace(T, m, n, rl, r, q, nblk, T * n, zo.ZO_BF16)
                       for m, n in shapes)
@@ -286,7 +298,7 @@ def main():
             rec["prep"].append((e0, e1))
             rec["gemm"].append((e1, e2, mt["m"], mt["n"]))
         Lb = zo.sq_loss(Y[m_last], Ystar, nblk, T)
-        g = zo.combine_central(Lb, eps)
+        g = zo.combine_forward(Lb, eps) if forward else zo.combine_central(Lb, eps)
         e0, e1 = Ev(), Ev()
         e0.record()
         zo.subspace_adam_update(items[s], g, t + 1, lr, b1, b2, ea)
@@ -313,12 +325,12 @@ def main():
     log(f"timed {args.steps} steps in {t1 - t0:.2f} s")
 
     if lora:
-        layer_flops = lambda m, n: lora_flops(T, m, n, rl, r, q)
-        launch_flops = lambda m, n: lora_apply_flops(T, m, n, rl, r, q)
+        layer_flops = lambda m, n: lora_flops(T, m, n, rl, r, q, nblk, nsigned)
+        launch_flops = lambda m, n: lora_apply_flops(T, m, n, rl, r, q, nblk, nsigned)
         unit_bytes = lambda m, n: update_bytes(rl, n, r, q, 4) + update_bytes(m, rl, r, q, 4)
     else:
-        layer_flops = lambda m, n: plinear_flops(T, m, n, r, q)
-        launch_flops = lambda m, n: apply_flops(T, m, n, r, q)
+        layer_flops = lambda m, n: plinear_flops(T, m, n, r, q, nblk, nsigned)
+        launch_flops = lambda m, n: apply_flops(T, m, n, r, q, nblk, nsigned)
         unit_bytes = lambda m, n: update_bytes(m, n, r, q)
     step_flops = sum(layer_flops(u["m"], u["n"]) for u in units)
     value = step_flops * args.steps / (t1 - t0) / 1e12
@@ -340,7 +352,7 @@ def main():
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         tr = json.load(open(TRAFFIC_FILE))
-        if tr.get("source_hash") == source_hash():
+        if tr.get("source_hash") == source_hash() and tr.get("workload_key") == f"{args.config}/{args.estimator}/q={q}":
             traffic = tr.get("bytes_per_launch")
     upd_gbps = upd_bytes / (upd_ms * 1e-3) / 1e9
     out = {
@@ -351,8 +363,11 @@ def main():
                                 + ", ".join(f"{nm} {m}x{n}" for nm, m, n in unit_mats)
                                 + (f" (frozen bf16 base, fp32 LoRA adapter r_L={rl}, alpha={int(scale * rl)}, "
                                    f"each factor in its own subspace)" if lora else "")
-                                + f"; {nblk} query blocks (q={q}, +/-) of T={T} tokens; r={r}; bf16 W and X"),
+                                + (f"; {nblk} blocks (baseline + q={q} forward queries)" if forward
+                                   else f"; {nblk} query blocks (q={q}, +/-)")
+                                + f" of T={T} tokens; r={r}; bf16 W and X"),
                    "layers": L, "perturbed_layers": len(units), "T": T, "r": r, "q": q, "blocks": nblk,
+                   "estimator": args.estimator,
                    "refresh_every": F},
         "roofline": {"kernel": "k_gemm_main (zo_perturbed_linear_apply)", "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",

@@ -296,6 +296,13 @@ int zo_sq_loss(int nblk, int T, int m, int dtype, const void* Y,
 int zo_combine_central(int q, const double* L, float eps, float* g,
                        void* stream);
 
+/* Forward difference of Eq. 6 (Alg. 3's estimator, one baseline and q
+ * perturbed forwards): g[j] = (L[1 + j] - L[0]) / eps, L device float64
+ * [q + 1] (block 0 is the unperturbed baseline, blk_sign 0; block 1 + j is
+ * query j with sign +1), g device fp32 [q]; float64 arithmetic. */
+int zo_combine_forward(int q, const double* L, float eps, float* g,
+                       void* stream);
+
 #ifdef __cplusplus
 }
 #endif

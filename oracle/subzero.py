@@ -257,14 +257,16 @@ def round_bf16(x):
 # ---------------------------------------------------------------------------
 # Tiny configuration end to end (Alg. 3 with the central estimate)
 # ---------------------------------------------------------------------------
-def tiny_run(inputs, omega_fn, z_fn, cfg, g_override=None, f32_state=False):
+def tiny_run(inputs, omega_fn, z_fn, cfg, g_override=None, f32_state=False, estimator="central"):
     """Alg. 3 on the one-layer Tiny problem, float64.
 
     inputs: dict(W, X, Ystar) arrays.  omega_fn(t) -> (Omega_U, Omega_V) for a
     refresh at step t; z_fn(t) -> Z[q, r, r].  g_override(t, g) may replace
     the estimates (teacher forcing).  Per step t = 0..steps-1: refresh if
-    t mod F == 0; for each query j the losses of W +- eps U Z_j V^T;
-    g_j = (L+ - L-)/(2 eps); Adam update with step index t+1.
+    t mod F == 0; for each query j the loss of W + eps U Z_j V^T and either
+    the loss of W - eps U Z_j V^T, g_j = (L+ - L-)/(2 eps) (estimator
+    "central"), or the baseline loss of W, g_j = (L+ - L0)/eps (estimator
+    "forward", Eq. 6); Adam update with step index t+1.
     Returns a list of per-step records.
     """
     W = np.asarray(inputs["W"], np.float64)
@@ -282,15 +284,21 @@ def tiny_run(inputs, omega_fn, z_fn, cfg, g_override=None, f32_state=False):
             V, _, _ = haar_qr(ov)
         Zs = np.asarray(z_fn(t), np.float64)
         Lp = np.array([sq_loss(perturbed_linear(X, W, U, V, Zs[j], +1.0, eps), Ystar) for j in range(q)])
-        Lm = np.array([sq_loss(perturbed_linear(X, W, U, V, Zs[j], -1.0, eps), Ystar) for j in range(q)])
-        g = central_estimate(Lp, Lm, eps)
+        if estimator == "forward":
+            Lm = None
+            L0 = sq_loss(X @ W.T, Ystar)
+            g = forward_estimate(Lp, L0, eps)
+        else:
+            Lm = np.array([sq_loss(perturbed_linear(X, W, U, V, Zs[j], -1.0, eps), Ystar) for j in range(q)])
+            L0 = None
+            g = central_estimate(Lp, Lm, eps)
         if g_override is not None:
             g = np.asarray(g_override(t, g), np.float64)
         upd = subspace_adam_update(W, U, V, Zs, g, M1, M2, t + 1, cfg["lr"],
                                    cfg["beta1"], cfg["beta2"], cfg["eps_adam"])
         W_before = W
         W, M1, M2 = upd["W"], upd["M1"], upd["M2"]
-        recs.append(dict(t=t, U=U, V=V, Z=Zs, Lp=Lp, Lm=Lm, g=g, S=upd["S"], Zbar=upd["Zbar"],
+        recs.append(dict(t=t, U=U, V=V, Z=Zs, Lp=Lp, Lm=Lm, L0=L0, g=g, S=upd["S"], Zbar=upd["Zbar"],
                          W_before=W_before, W=W, M1=M1, M2=M2,
                          loss=sq_loss(X @ W.T, Ystar)))
     return recs

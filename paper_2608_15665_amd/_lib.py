@@ -33,7 +33,7 @@ ABI_SYMBOLS = (
     "zo_lora_perturbed_linear_workspace", "zo_lora_perturbed_linear",
     "zo_lora_perturbed_linear_prepare",
     "zo_subspace_adam_update_workspace", "zo_subspace_adam_update",
-    "zo_sq_loss_workspace", "zo_sq_loss", "zo_combine_central",
+    "zo_sq_loss_workspace", "zo_sq_loss", "zo_combine_central", "zo_combine_forward",
 )
 
 
@@ -116,6 +116,8 @@ def lib() -> ctypes.CDLL:
             L.zo_sq_loss.argtypes = [c_int, c_int, c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
             L.zo_combine_central.restype = c_int
             L.zo_combine_central.argtypes = [c_int, c_vp, c_f, c_vp, c_vp]
+            L.zo_combine_forward.restype = c_int
+            L.zo_combine_forward.argtypes = [c_int, c_vp, c_f, c_vp, c_vp]
             _lib = L
     return _lib
 
@@ -436,4 +438,15 @@ def combine_central(Lpm: torch.Tensor, eps: float, out: Optional[torch.Tensor] =
         out = torch.empty(q, dtype=torch.float32, device=Lpm.device)
     _need(out, "g", torch.float32, q)
     _check(lib().zo_combine_central(q, Lpm.data_ptr(), float(eps), out.data_ptr(), _stream_handle()))
+    return out
+
+
+def combine_forward(L: torch.Tensor, eps: float, out: Optional[torch.Tensor] = None):
+    """g_j = (L[1 + j] - L[0]) / eps as float32 [q] (L[0]: the baseline block)."""
+    _need(L, "L", torch.float64)
+    q = L.numel() - 1
+    if out is None:
+        out = torch.empty(q, dtype=torch.float32, device=L.device)
+    _need(out, "g", torch.float32, q)
+    _check(lib().zo_combine_forward(q, L.data_ptr(), float(eps), out.data_ptr(), _stream_handle()))
     return out

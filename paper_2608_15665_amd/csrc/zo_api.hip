@@ -375,4 +375,11 @@ int zo_combine_central(int q, const double* L, float eps, float* g, void* stream
   return zo_combine_central_launch(q, L, eps, g, (hipStream_t)stream);
 }
 
+int zo_combine_forward(int q, const double* L, float eps, float* g, void* stream) {
+  ZO_CHECK(q >= 1, "combine_forward: q = %d < 1", q);
+  ZO_CHECK(L && g, "combine_forward: NULL tensor argument");
+  ZO_CHECK(isfinite(eps) && eps != 0.f, "combine_forward: eps must be finite and non-zero");
+  return zo_combine_forward_launch(q, L, eps, g, (hipStream_t)stream);
+}
+
 }  // extern "C"

@@ -105,3 +105,4 @@ int zo_sq_loss_launch(int nblk, int T, int m, int dtype, const void* Y, const vo
                       size_t* ws_needed);
 int zo_combine_central_launch(int q, const double* L, float eps, float* g,
                               hipStream_t stream);
+int zo_combine_forward_launch(int q, const double* L, float eps, float* g, hipStream_t stream);

@@ -50,6 +50,11 @@ __global__ void k_central(int q, const double* L, float eps, float* g) {
   if (j < q) g[j] = (float)((L[2 * j] - L[2 * j + 1]) / (2.0 * (double)eps));
 }
 
+__global__ void k_forward(int q, const double* L, float eps, float* g) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j < q) g[j] = (float)((L[1 + j] - L[0]) / (double)eps);
+}
+
 }  // namespace
 
 int zo_sq_loss_launch(int nblk, int T, int m, int dtype, const void* Y, const void* Ystar,
@@ -77,4 +82,9 @@ int zo_sq_loss_launch(int nblk, int T, int m, int dtype, const void* Y, const vo
 int zo_combine_central_launch(int q, const double* L, float eps, float* g, hipStream_t stream) {
   hipLaunchKernelGGL(k_central, dim3((q + 63) / 64), dim3(64), 0, stream, q, L, eps, g);
   return zo_hip_status(hipGetLastError(), "k_central");
+}
+
+int zo_combine_forward_launch(int q, const double* L, float eps, float* g, hipStream_t stream) {
+  hipLaunchKernelGGL(k_forward, dim3((q + 63) / 64), dim3(64), 0, stream, q, L, eps, g);
+  return zo_hip_status(hipGetLastError(), "k_forward");
 }

@@ -1,4 +1,5 @@
-"""The Tiny configuration end to end on the GPU (Alg. 3 with central differences):
+"""The Tiny configuration end to end on the GPU (Alg. 3 with central differences, and with
+Alg. 3's forward difference against a baseline block):
 W 256 x 512 fp32, X 64 x 512, r = 4, q = 4, eps = 1e-3, lr = 1e-2, beta = (0.9, 0.999),
 20 steps, refresh every 5 steps, seed 0.  Every step runs only library calls:
 refresh -> perturbed linear (8 blocks, shared X) -> squared loss -> central
@@ -32,7 +33,10 @@ def zdraw(t):
 
 
 class GpuTiny:
-    def __init__(self, inp):
+    """forward=False: blocks (j, +), (j, -) per query (central difference); forward=True:
+    block 0 the unperturbed baseline (sign 0), block 1 + j query j with sign + (Eq. 6)."""
+
+    def __init__(self, inp, forward=False):
         self.W = dev_f32(inp["W"])
         self.X = dev_f32(inp["X"])
         self.Ys = dev_f32(inp["Ystar"])
@@ -41,8 +45,13 @@ class GpuTiny:
         self.V = torch.empty((C["n"], r), dtype=torch.float32, device="cuda")
         self.M1 = torch.zeros((r, r), dtype=torch.float32, device="cuda")
         self.M2 = torch.zeros((r, r), dtype=torch.float32, device="cuda")
-        self.bq = [b // 2 for b in range(2 * C["q"])]
-        self.bs = [1 if b % 2 == 0 else -1 for b in range(2 * C["q"])]
+        self.forward = forward
+        if forward:
+            self.bq = [0] + list(range(C["q"]))
+            self.bs = [0] + [1] * C["q"]
+        else:
+            self.bq = [b // 2 for b in range(2 * C["q"])]
+            self.bs = [1 if b % 2 == 0 else -1 for b in range(2 * C["q"])]
 
     def step(self, t, g_override=None):
         if t % C["F"] == 0:
@@ -51,8 +60,8 @@ class GpuTiny:
         Z = dev_f32(zdraw(t))
         Y = zo.perturbed_linear(self.X, self.W, self.U, self.V, Z, self.bq, self.bs, C["eps"], C["T"],
                                 x_block_stride=0)
-        L = zo.sq_loss(Y, self.Ys, 2 * C["q"], C["T"])
-        g = zo.combine_central(L, C["eps"])
+        L = zo.sq_loss(Y, self.Ys, len(self.bq), C["T"])
+        g = zo.combine_forward(L, C["eps"]) if self.forward else zo.combine_central(L, C["eps"])
         if g_override is not None:
             g = dev_f32(g_override)
         zo.subspace_adam_update([dict(W=self.W, U=self.U, V=self.V, Z=Z, M1=self.M1, M2=self.M2)], g, t + 1,
@@ -112,3 +121,35 @@ def test_central_difference_exact_at_eps_one():
     grad = (X @ W.T - inp["Ystar"]).T @ X / C["T"]
     exact = np.array([np.sum(grad * (U @ Zh[j].astype(np.float64) @ V.T)) for j in range(C["q"])])
     assert ferr(g, exact, 1.0) <= 1e-5
+
+
+def test_tiny_forward_teacher_forced():
+    """Alg. 3's own estimator: one baseline block (blk_sign 0) and q perturbed blocks per step,
+    g_j = (L_j - L_0) / eps on the device (zo_combine_forward)."""
+    inp = zd.tiny_inputs(C["seed"])
+    recs = oracle.tiny_run(inp, omega, zdraw, f32cfg(), estimator="forward")
+    gpu = GpuTiny(inp, forward=True)
+    for t, rec in enumerate(recs):
+        L, g = gpu.step(t, g_override=rec["g"].astype(np.float32))
+        assert ferr(L[:1], [rec["L0"]], 1.0) <= 1e-5 and ferr(L[1:], rec["Lp"], 1.0) <= 1e-5, t
+        assert ferr(g, rec["g"], 1.0) <= 5e-2, t
+        assert ferr(host(gpu.W), rec["W"], 1.0) <= 1e-5, t
+
+
+def test_forward_difference_closed_form_at_eps_one():
+    """On the quadratic loss the forward difference is <grad L, P> + (eps / 2) ||X P^T||^2 / T
+    exactly (P = U Z V^T); at eps = 1 the GPU chain is held to 1e-5."""
+    inp = zd.tiny_inputs(C["seed"])
+    gpu = GpuTiny(inp, forward=True)
+    ou, ov = omega(0)
+    zo.subspace_refresh([dev_f32(ou), dev_f32(ov)], C["r"], out=[gpu.U, gpu.V])
+    Zh = zdraw(0)
+    Y = zo.perturbed_linear(gpu.X, gpu.W, gpu.U, gpu.V, dev_f32(Zh), gpu.bq, gpu.bs, 1.0, C["T"], x_block_stride=0)
+    g = host(zo.combine_forward(zo.sq_loss(Y, gpu.Ys, C["q"] + 1, C["T"]), 1.0))
+    U, V = host(gpu.U), host(gpu.V)
+    X, W = inp["X"].astype(np.float64), inp["W"].astype(np.float64)
+    grad = (X @ W.T - inp["Ystar"]).T @ X / C["T"]
+    P = [U @ Zh[j].astype(np.float64) @ V.T for j in range(C["q"])]
+    exact = np.array([np.sum(grad * p) + 0.5 * np.sum((X @ p.T) ** 2) / C["T"] for p in P])
+    assert ferr(g, exact, 1.0) <= 1e-5
+

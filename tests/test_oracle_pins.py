@@ -386,6 +386,38 @@ def test_forward_difference_unbiased_on_quadratic():
     assert np.linalg.norm(est - target) < 4 * np.linalg.norm(target) * math.sqrt(5 / 2000) + 1e-6
 
 
+@pytest.mark.parametrize("eps", [1e-3, 0.5])
+def test_forward_difference_closed_form_on_quadratic(eps):
+    """Eq. 6 on the quadratic L(W) = 0.5||X W^T - Y*||^2 / T: with P = U Z V^T,
+    (L(W + eps P) - L(W)) / eps = <grad L, P> + (eps / 2) ||X P^T||^2 / T exactly."""
+    X, W, Ys, U, V, grad = _quad_problem(r=3)
+    Z = np.random.default_rng(31).standard_normal((3, 3))
+    P = U @ Z @ V.T
+    L0 = oracle.sq_loss(X @ W.T, Ys)
+    L1 = oracle.sq_loss(oracle.perturbed_linear(X, W, U, V, Z, 1.0, eps), Ys)
+    rho = oracle.forward_estimate(np.array([L1]), L0, eps)[0]
+    exact = np.sum(grad * P) + 0.5 * eps * np.sum((X @ P.T) ** 2) / X.shape[0]
+    assert rho == pytest.approx(exact, rel=1e-7 if eps < 1e-2 else 1e-11, abs=1e-12)
+
+
+def test_tiny_forward_run_matches_its_definition():
+    """The forward-difference variant of the Tiny loop: each step's g is (L(W + eps U Z_j V^T) - L(W)) / eps
+    of that step's W, and a teacher-forced zero estimate leaves W unchanged."""
+    inp = zd.tiny_inputs(0)
+    cfg = dict(zd.TINY, steps=3)
+    om = lambda t: zd.omega_pair(0, t, 0, cfg["m"], cfg["n"], cfg["r"])
+    zf = lambda t: zd.z_draws(0, t, 0, cfg["q"], cfg["r"])
+    recs = oracle.tiny_run(inp, om, zf, cfg, estimator="forward")
+    X, Ys = inp["X"].astype(np.float64), inp["Ystar"]
+    for rec in recs:
+        L0 = oracle.sq_loss(X @ rec["W_before"].T, Ys)
+        assert rec["L0"] == pytest.approx(L0, rel=1e-15)
+        np.testing.assert_allclose(rec["g"], (rec["Lp"] - L0) / cfg["eps"], rtol=1e-12)
+        assert rec["Lm"] is None
+    zero = oracle.tiny_run(inp, om, zf, cfg, estimator="forward", g_override=lambda t, g: np.zeros_like(g))
+    np.testing.assert_array_equal(zero[-1]["W"], inp["W"].astype(np.float64))
+
+
 def test_aggregate_one_hot_and_linearity():
     Zs = RNG.standard_normal((5, 3, 3))
     np.testing.assert_allclose(oracle.aggregate([0, 0, 5.0, 0, 0], Zs), Zs[2], rtol=0, atol=1e-15)
