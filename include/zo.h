@@ -280,6 +280,24 @@ int zo_subspace_adam_update(int count, const zo_update_item* items, int w_dtype,
                             size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Subspace SGD update -- the "SubZero+/SGD" variant of the experiments and,
+ * with q = 1, SubZero's own update (Sec. "Preliminaries": W <- W - eta g
+ * U Z V^T).  For each item:
+ *
+ *     Zbar = (1/q) sum_j g_j Z_j,     W <- W - lr U Zbar V^T
+ *
+ * Arguments, arithmetic, workspace rules and the non-finite guard as for
+ * zo_subspace_adam_update; M1 and M2 are neither read nor written (may be
+ * NULL).  zo_subspace_sgd_update_workspace gives the workspace size.
+ * ------------------------------------------------------------------------ */
+size_t zo_subspace_sgd_update_workspace(int count, const zo_update_item* items,
+                                        int r, int q, int w_dtype);
+int zo_subspace_sgd_update(int count, const zo_update_item* items, int w_dtype,
+                           int r, int q, const float* g, float lr,
+                           int* nonfinite_flag, void* workspace,
+                           size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Squared-error loss per block (the loss of a one-layer regression model):
  * out[b] = 0.5 * sum((Y_b - Ystar)^2) / T, float64 accumulation in a fixed
  * order.  Y: nblk blocks of T x m (dtype), Ystar: T x m (same dtype), out:

@@ -18,7 +18,7 @@ __all__ = [
     "perturbation", "perturbed_weight", "perturbed_linear", "perturbed_linear_blocks",
     "lora_perturbed_factors", "lora_perturbed_linear", "lora_perturbed_linear_blocks",
     "sq_loss", "central_estimate", "forward_estimate", "aggregate",
-    "adam_direction", "subspace_adam_update", "round_bf16", "tiny_run",
+    "adam_direction", "subspace_adam_update", "subspace_sgd_update", "round_bf16", "tiny_run",
 ]
 
 
@@ -241,6 +241,16 @@ def subspace_adam_update(W, U, V, Zs, g, M1, M2, t, lr, beta1, beta2, eps_adam):
 # ---------------------------------------------------------------------------
 # bfloat16 storage rounding (format, not method): single rounding from float64
 # ---------------------------------------------------------------------------
+def subspace_sgd_update(W, U, V, Zs, g, lr):
+    """Plain SGD in the subspace (the "SubZero+/SGD" rows of the experiments; with q = 1
+    SubZero's update W - eta rho U Z V^T of Sec. "Preliminaries"):
+    Zbar = (1/q) sum_j g_j Z_j, W_new = W - lr U Zbar V^T (exact, float64).
+    Returns dict(W=W_new, Zbar)."""
+    Zbar = aggregate(g, Zs)
+    W_new = np.asarray(W, np.float64) - lr * (np.asarray(U, np.float64) @ Zbar @ np.asarray(V, np.float64).T)
+    return dict(W=W_new, Zbar=Zbar)
+
+
 def round_bf16(x):
     """Round float64 values to the nearest bfloat16 (8 significant bits), ties to even.
 

@@ -8,15 +8,18 @@ of include/zo.h); this package only binds it.  Entry points:
     lora_perturbed_linear  the same for a LoRA-adapted layer: both adapter factors
                            perturbed in their own subspaces
     subspace_adam_update   subspace Adam and W <- W - lr U S V^T (Eqs. 6-10)
+    subspace_sgd_update    plain subspace SGD, W <- W - lr U Zbar V^T
     sq_loss, combine_central, combine_forward   loss and estimate helpers (central
                            difference, or forward difference against a baseline block)
 """
 from ._lib import (ZO_BF16, ZO_F32, ZO_MAX_BLOCKS, ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH,
                    LoraPerturbedLinear, PerturbedLinear, Workspace, ZoError, abi_version, combine_central,
                    combine_forward, lib,
-                   lora_perturbed_linear, perturbed_linear, sq_loss, subspace_adam_update, subspace_refresh)
+                   lora_perturbed_linear, perturbed_linear, sq_loss, subspace_adam_update, subspace_refresh,
+                   subspace_sgd_update)
 
 __all__ = ["ZO_BF16", "ZO_F32", "ZO_MAX_BLOCKS", "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH",
            "LoraPerturbedLinear", "PerturbedLinear", "Workspace", "ZoError", "abi_version", "combine_central",
            "combine_forward", "lib",
-           "lora_perturbed_linear", "perturbed_linear", "sq_loss", "subspace_adam_update", "subspace_refresh"]
+           "lora_perturbed_linear", "perturbed_linear", "sq_loss", "subspace_adam_update", "subspace_refresh",
+           "subspace_sgd_update"]

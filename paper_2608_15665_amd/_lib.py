@@ -33,6 +33,7 @@ ABI_SYMBOLS = (
     "zo_lora_perturbed_linear_workspace", "zo_lora_perturbed_linear",
     "zo_lora_perturbed_linear_prepare",
     "zo_subspace_adam_update_workspace", "zo_subspace_adam_update",
+    "zo_subspace_sgd_update_workspace", "zo_subspace_sgd_update",
     "zo_sq_loss_workspace", "zo_sq_loss", "zo_combine_central", "zo_combine_forward",
 )
 
@@ -110,6 +111,12 @@ def lib() -> ctypes.CDLL:
             L.zo_subspace_adam_update.restype = c_int
             L.zo_subspace_adam_update.argtypes = [c_int, ctypes.POINTER(UpdateItem), c_int, c_int, c_int,
                                                   c_vp, c_int, c_f, c_f, c_f, c_f, c_vp, c_vp, c_sz, c_vp]
+            L.zo_subspace_sgd_update_workspace.restype = c_sz
+            L.zo_subspace_sgd_update_workspace.argtypes = [c_int, ctypes.POINTER(UpdateItem), c_int,
+                                                           c_int, c_int]
+            L.zo_subspace_sgd_update.restype = c_int
+            L.zo_subspace_sgd_update.argtypes = [c_int, ctypes.POINTER(UpdateItem), c_int, c_int, c_int,
+                                                 c_vp, c_f, c_vp, c_vp, c_sz, c_vp]
             L.zo_sq_loss_workspace.restype = c_sz
             L.zo_sq_loss_workspace.argtypes = [c_int, c_int, c_int]
             L.zo_sq_loss.restype = c_int
@@ -371,13 +378,8 @@ def lora_perturbed_linear(X, W, A, UA, VA, ZA, B, UB, VB, ZB, blk_query, blk_sig
                                x_block_stride, out_dtype, Y)()
 
 
-def subspace_adam_update(items: Sequence[dict], g: torch.Tensor, t: int, lr: float, beta1: float,
-                         beta2: float, eps_adam: float, nonfinite_flag: Optional[torch.Tensor] = None):
-    """Subspace Adam step for every item (dict with W, U, V, Z, M1, M2 and optional
-    zbar_out, w_f32_out).  See zo_subspace_adam_update."""
+def _update_items(items: Sequence[dict], g: torch.Tensor, moments: bool):
     n = len(items)
-    if n == 0:
-        return
     dt = items[0]["W"].dtype
     if dt not in _DT:
         raise TypeError(f"unsupported dtype {dt}")
@@ -391,8 +393,11 @@ def subspace_adam_update(items: Sequence[dict], g: torch.Tensor, t: int, lr: flo
         _need(it["U"], f"U[{i}]", torch.float32, m * r)
         _need(it["V"], f"V[{i}]", torch.float32, nn * r)
         _need(it["Z"], f"Z[{i}]", torch.float32, q * r * r)
-        _need(it["M1"], f"M1[{i}]", torch.float32, r * r)
-        _need(it["M2"], f"M2[{i}]", torch.float32, r * r)
+        m1, m2 = it.get("M1"), it.get("M2")
+        if moments or m1 is not None:
+            _need(m1, f"M1[{i}]", torch.float32, r * r)
+        if moments or m2 is not None:
+            _need(m2, f"M2[{i}]", torch.float32, r * r)
         zb = it.get("zbar_out")
         wo = it.get("w_f32_out")
         if zb is not None:
@@ -400,18 +405,48 @@ def subspace_adam_update(items: Sequence[dict], g: torch.Tensor, t: int, lr: flo
         if wo is not None:
             _need(wo, f"w_f32_out[{i}]", torch.float32, m * nn)
         arr[i] = UpdateItem(m, nn, W.data_ptr(), it["U"].data_ptr(), it["V"].data_ptr(), it["Z"].data_ptr(),
-                            it["M1"].data_ptr(), it["M2"].data_ptr(), _ptr(zb), _ptr(wo))
+                            _ptr(m1), _ptr(m2), _ptr(zb), _ptr(wo))
+    return arr, _DT[dt], r, q
+
+
+def subspace_adam_update(items: Sequence[dict], g: torch.Tensor, t: int, lr: float, beta1: float,
+                         beta2: float, eps_adam: float, nonfinite_flag: Optional[torch.Tensor] = None):
+    """Subspace Adam step for every item (dict with W, U, V, Z, M1, M2 and optional
+    zbar_out, w_f32_out).  See zo_subspace_adam_update."""
+    n = len(items)
+    if n == 0:
+        return
+    arr, dt, r, q = _update_items(items, g, True)
     if nonfinite_flag is not None:
         _need(nonfinite_flag, "nonfinite_flag", torch.int32, 1)
     L = lib()
-    ws_n = L.zo_subspace_adam_update_workspace(n, arr, r, q, _DT[dt])
+    ws_n = L.zo_subspace_adam_update_workspace(n, arr, r, q, dt)
     if ws_n == 0:
-        _check(L.zo_subspace_adam_update(n, arr, _DT[dt], r, q, g.data_ptr(), t, lr, beta1, beta2,
+        _check(L.zo_subspace_adam_update(n, arr, dt, r, q, g.data_ptr(), t, lr, beta1, beta2,
                                          eps_adam, None, None, 0, None))
     ws = Workspace.get(ws_n)
-    _check(L.zo_subspace_adam_update(n, arr, _DT[dt], r, q, g.data_ptr(), int(t), float(lr), float(beta1),
+    _check(L.zo_subspace_adam_update(n, arr, dt, r, q, g.data_ptr(), int(t), float(lr), float(beta1),
                                      float(beta2), float(eps_adam), _ptr(nonfinite_flag), ws.data_ptr(),
                                      ws.numel(), _stream_handle()))
+
+
+def subspace_sgd_update(items: Sequence[dict], g: torch.Tensor, lr: float,
+                        nonfinite_flag: Optional[torch.Tensor] = None):
+    """Subspace SGD step W <- W - lr U Zbar V^T for every item (dict with W, U, V, Z and optional
+    zbar_out, w_f32_out; moments not used).  See zo_subspace_sgd_update."""
+    n = len(items)
+    if n == 0:
+        return
+    arr, dt, r, q = _update_items(items, g, False)
+    if nonfinite_flag is not None:
+        _need(nonfinite_flag, "nonfinite_flag", torch.int32, 1)
+    L = lib()
+    ws_n = L.zo_subspace_sgd_update_workspace(n, arr, r, q, dt)
+    if ws_n == 0:
+        _check(L.zo_subspace_sgd_update(n, arr, dt, r, q, g.data_ptr(), lr, None, None, 0, None))
+    ws = Workspace.get(ws_n)
+    _check(L.zo_subspace_sgd_update(n, arr, dt, r, q, g.data_ptr(), float(lr), _ptr(nonfinite_flag),
+                                    ws.data_ptr(), ws.numel(), _stream_handle()))
 
 
 def sq_loss(Y: torch.Tensor, Ystar: torch.Tensor, nblk: int, T: int, out: Optional[torch.Tensor] = None):

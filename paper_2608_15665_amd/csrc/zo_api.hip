@@ -285,7 +285,8 @@ int zo_lora_perturbed_linear(int T, int m, int n, int rl, int r, int q, int nblk
 }
 
 // ------------------------------------------------------------------ update
-static int check_update(int count, const zo_update_item* items, int r, int q, int w_dtype) {
+static int check_update(int count, const zo_update_item* items, int r, int q, int w_dtype,
+                        bool moments = true) {
   ZO_CHECK(count >= 0, "update: count = %d < 0", count);
   ZO_CHECK(count == 0 || items, "update: items is NULL");
   ZO_CHECK(r >= 1 && r <= ZO_MAX_RANK, "update: r = %d outside [1, %d]", r, ZO_MAX_RANK);
@@ -295,7 +296,8 @@ static int check_update(int count, const zo_update_item* items, int r, int q, in
     const zo_update_item& it = items[i];
     ZO_CHECK(it.m >= 1 && it.n >= 1, "update: item %d has m = %d, n = %d", i, it.m, it.n);
     ZO_CHECK((long long)it.m * it.n < (1LL << 40), "update: item %d too large", i);
-    ZO_CHECK(it.W && it.U && it.V && it.Z && it.M1 && it.M2, "update: item %d has a NULL tensor", i);
+    ZO_CHECK(it.W && it.U && it.V && it.Z, "update: item %d has a NULL tensor", i);
+    ZO_CHECK(!moments || (it.M1 && it.M2), "update: item %d has a NULL moment", i);
     if (w_dtype == ZO_BF16) {
       ZO_CHECK(it.n % 8 == 0, "update: bf16 W needs n %% 8 == 0 (item %d, n = %d)", i, it.n);
       ZO_CHECK(aligned(it.W, 16) && aligned(it.w_f32_out, 16),
@@ -314,8 +316,8 @@ size_t zo_subspace_adam_update_workspace(int count, const zo_update_item* items,
                                          int w_dtype) {
   if (check_update(count, items, r, q, w_dtype) != ZO_OK) return 0;
   size_t need = 0;
-  zo_update_launch(count, items, w_dtype, r, q, nullptr, 1, 0.f, 0.f, 0.f, 0.f, nullptr, nullptr,
-                   0, nullptr, &need);
+  zo_update_launch(count, items, w_dtype, r, q, nullptr, 1, 0.f, 0.f, 0.f, 0.f, 0, nullptr,
+                   nullptr, 0, nullptr, &need);
   return need;
 }
 
@@ -333,14 +335,43 @@ int zo_subspace_adam_update(int count, const zo_update_item* items, int w_dtype,
   ZO_CHECK(eps_adam >= 0.f && isfinite(eps_adam), "update: eps_adam must be finite and >= 0");
   if (count == 0) return ZO_OK;
   size_t need = 0;
-  zo_update_launch(count, items, w_dtype, r, q, nullptr, 1, 0.f, 0.f, 0.f, 0.f, nullptr, nullptr,
-                   0, nullptr, &need);
+  zo_update_launch(count, items, w_dtype, r, q, nullptr, 1, 0.f, 0.f, 0.f, 0.f, 0, nullptr,
+                   nullptr, 0, nullptr, &need);
   if (ws_bytes < need || !workspace) {
     zo_set_error("update: workspace %zu bytes < required %zu", ws_bytes, need);
     return ZO_ERR_WORKSPACE;
   }
   ZO_CHECK(aligned(workspace, 256), "update: workspace not 256-byte aligned");
-  return zo_update_launch(count, items, w_dtype, r, q, g, t, lr, beta1, beta2, eps_adam,
+  return zo_update_launch(count, items, w_dtype, r, q, g, t, lr, beta1, beta2, eps_adam, 0,
+                          nonfinite_flag, workspace, ws_bytes, (hipStream_t)stream, nullptr);
+}
+
+size_t zo_subspace_sgd_update_workspace(int count, const zo_update_item* items, int r, int q,
+                                        int w_dtype) {
+  if (check_update(count, items, r, q, w_dtype, false) != ZO_OK) return 0;
+  size_t need = 0;
+  zo_update_launch(count, items, w_dtype, r, q, nullptr, 1, 0.f, 0.f, 0.f, 0.f, 1, nullptr,
+                   nullptr, 0, nullptr, &need);
+  return need;
+}
+
+int zo_subspace_sgd_update(int count, const zo_update_item* items, int w_dtype, int r, int q,
+                           const float* g, float lr, int* nonfinite_flag, void* workspace,
+                           size_t ws_bytes, void* stream) {
+  int st = check_update(count, items, r, q, w_dtype, false);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(g, "update: g is NULL");
+  ZO_CHECK(isfinite(lr), "update: lr is not finite");
+  if (count == 0) return ZO_OK;
+  size_t need = 0;
+  zo_update_launch(count, items, w_dtype, r, q, nullptr, 1, 0.f, 0.f, 0.f, 0.f, 1, nullptr,
+                   nullptr, 0, nullptr, &need);
+  if (ws_bytes < need || !workspace) {
+    zo_set_error("update: workspace %zu bytes < required %zu", ws_bytes, need);
+    return ZO_ERR_WORKSPACE;
+  }
+  ZO_CHECK(aligned(workspace, 256), "update: workspace not 256-byte aligned");
+  return zo_update_launch(count, items, w_dtype, r, q, g, 1, lr, 0.f, 0.f, 0.f, 1,
                           nonfinite_flag, workspace, ws_bytes, (hipStream_t)stream, nullptr);
 }
 

@@ -89,13 +89,14 @@ int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t*
 int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
                      hipStream_t stream);
 
-// Subspace Adam update (zo_update.hip).
+// Subspace update (zo_update.hip): Adam (sgd = 0) or plain SGD in the subspace (sgd = 1,
+// S = Zbar; the moments are neither read nor written).
 int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r, int q,
                      const float* g, int t, float lr, float beta1, float beta2,
-                     float eps_adam, int* nonfinite_flag, void* ws, size_t ws_bytes,
+                     float eps_adam, int sgd, int* nonfinite_flag, void* ws, size_t ws_bytes,
                      hipStream_t stream, size_t* ws_needed);
 
-// Householder TSQR refresh (zo_qr.hip).
+// Subspace refresh, CholeskyQR2 (zo_qr.hip).
 int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void* ws,
                       size_t ws_bytes, hipStream_t stream, size_t* ws_needed);
 

@@ -1,4 +1,6 @@
-// Subspace Adam update of SubZero+ (Eqs. 6-10, tail of Alg. 3).
+// Subspace Adam update of SubZero+ (Eqs. 6-10, tail of Alg. 3), and the plain
+// subspace SGD update it is compared with (S = Zbar, no moments; SubZero's own
+// update when q = 1).
 //
 // Three launches per chunk of up to ITEMS_PER_LAUNCH matrices:
 //   k_adam_rr   256 entries of one matrix per workgroup: Zbar = (1/q) sum_j g_j Z_j,
@@ -53,6 +55,7 @@ struct RRArgs {
   const float* g;
   int* nonfinite_flag;
   int r, q, aw;  // aw: workgroups per item
+  int sgd;       // 1: S = Zbar, no moments
   double beta1, beta2, eps_adam, bc1, bc2;
 };
 
@@ -66,14 +69,17 @@ __global__ __launch_bounds__(256) void k_adam_rr(RRArgs a) {
     double zb = 0.0;
     for (int j = 0; j < a.q; ++j) zb += (double)a.g[j] * (double)it.Z[(size_t)j * rr + e];
     zb /= (double)a.q;
-    const double m1 = a.beta1 * (double)it.M1[e] + (1.0 - a.beta1) * zb;
-    const double m2 = a.beta2 * (double)it.M2[e] + (1.0 - a.beta2) * zb * zb;
-    const double s = (m1 / a.bc1) / (sqrt(m2 / a.bc2) + a.eps_adam);
+    double s = zb;
+    if (!a.sgd) {
+      const double m1 = a.beta1 * (double)it.M1[e] + (1.0 - a.beta1) * zb;
+      const double m2 = a.beta2 * (double)it.M2[e] + (1.0 - a.beta2) * zb * zb;
+      s = (m1 / a.bc1) / (sqrt(m2 / a.bc2) + a.eps_adam);
+      it.M1n[e] = (float)m1;
+      it.M2n[e] = (float)m2;
+    }
     if (!isfinite(zb) || !isfinite(s)) bad = 1;
     if (it.zbar_out) it.zbar_out[e] = (float)zb;
     it.S[e] = s;
-    it.M1n[e] = (float)m1;
-    it.M2n[e] = (float)m2;
   }
   bad = __syncthreads_or(bad);
   if (threadIdx.x == 0) {
@@ -101,7 +107,7 @@ struct ItemUS {
 };
 struct USArgs {
   ItemUS it[ITEMS_PER_LAUNCH];
-  int count, r, rp, bf16, aw;
+  int count, r, rp, bf16, aw, sgd;
   float lr;
 };
 
@@ -125,9 +131,11 @@ __global__ __launch_bounds__(256) void k_us(USArgs a) {
   if (local == 0 && tid == 0) *it.skip = bad;
   if (bad) return;
   const int rr = r * r;
-  for (int e = local * 256 + tid; e < rr; e += it.n_wg * 256) {
-    it.M1[e] = it.M1n[e];
-    it.M2[e] = it.M2n[e];
+  if (!a.sgd) {
+    for (int e = local * 256 + tid; e < rr; e += it.n_wg * 256) {
+      it.M1[e] = it.M1n[e];
+      it.M2[e] = it.M2n[e];
+    }
   }
   if (local < it.l_tiles) {
     const int i0 = local * US_ROWS;
@@ -441,7 +449,7 @@ void launch_update_bf16(bool hook, int wg, hipStream_t stream, const UpdArgs& pa
 
 int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r, int q,
                      const float* g, int t, float lr, float beta1, float beta2, float eps_adam,
-                     int* nonfinite_flag, void* ws, size_t ws_bytes, hipStream_t stream,
+                     int sgd, int* nonfinite_flag, void* ws, size_t ws_bytes, hipStream_t stream,
                      size_t* ws_needed) {
   const int bf16 = w_dtype == ZO_BF16;
   const int rp = bf16 ? (r + 31) / 32 * 32 : r;
@@ -470,6 +478,7 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
     ra.r = r;
     ra.q = q;
     ra.aw = aw;
+    ra.sgd = sgd;
     ra.beta1 = beta1;
     ra.beta2 = beta2;
     ra.eps_adam = eps_adam;
@@ -480,6 +489,7 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
     ua.rp = pa.rp = rp;
     ua.bf16 = bf16;
     ua.aw = aw;
+    ua.sgd = sgd;
     ua.lr = lr;
     int us_wg = 0;
     int wg_total = 0;

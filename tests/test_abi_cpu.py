@@ -151,6 +151,23 @@ def test_update_validation():
                                      need - 1, None) == 6
 
 
+def test_sgd_update_validation():
+    """The SGD update accepts NULL moments (the Adam update does not) and checks the rest alike."""
+    L = zo.lib()
+    fake = 1 << 20
+    no_mom = UpdateItem(8, 16, fake, fake, fake, fake, None, None, None, None)
+    arr = (UpdateItem * 1)(no_mom)
+    need = L.zo_subspace_sgd_update_workspace(1, arr, 4, 2, 1)
+    assert need > 0
+    assert L.zo_subspace_adam_update_workspace(1, arr, 4, 2, 1) == 0
+    assert L.zo_subspace_adam_update(1, arr, 1, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, fake,
+                                     1 << 30, None) == 1
+    assert "moment" in _detail()
+    assert L.zo_subspace_sgd_update(1, arr, 1, 4, 2, fake, float("nan"), None, fake, 1 << 30, None) == 1
+    assert "lr" in _detail()
+    assert L.zo_subspace_sgd_update(1, arr, 1, 4, 2, fake, 1e-2, None, fake, need - 1, None) == 6
+
+
 def test_loss_validation():
     L = zo.lib()
     fake = 1 << 20

@@ -175,3 +175,46 @@ def test_full_size_sampled(name, m, n):
     assert check_bf16_storage(got_w, got_hook, W_rows) < 1e-2
     np.testing.assert_allclose(host(it["dev"]["M1"]), oracle.adam_direction(
         it["M1h"], it["M2h"], Zbar, 3, F32(b1), F32(b2), F32(1e-8))[0], rtol=1e-6, atol=1e-12)
+
+
+@pytest.mark.parametrize("bf16", [True, False])
+@pytest.mark.parametrize("m,n,r,q", [(300, 264, 16, 4), (512, 1024, 64, 8), (129, 72, 5, 1)])
+def test_sgd_update_parity(bf16, m, n, r, q):
+    """Subspace SGD (S = Zbar; q = 1 is SubZero's update): the same bars as the Adam update;
+    moments given to the call are left untouched."""
+    if bf16 and n % 8:
+        pytest.skip("bf16 W needs n % 8 == 0")
+    it = make_item(11, (m, n, 7), m, n, r, q, bf16, moments=True)
+    g = zd.f32(zd.draw(11, "G", (m, n, 7), (q,), 1e-2))
+    M1_before = host(it["dev"]["M1"]).copy()
+    zo.subspace_sgd_update([it["dev"]], dev_f32(g), 1e-3)
+    torch.cuda.synchronize()
+    ref = oracle.subspace_sgd_update(it["Wv"], it["U"], it["V"], it["Z"], g.astype(np.float64), F32(1e-3))
+    got_hook = host(it["dev"]["w_f32_out"])
+    got_w = host(it["dev"]["W"])
+    if bf16:
+        assert ferr(got_hook, ref["W"], 1.0) <= 5e-5
+        assert check_bf16_storage(got_w, got_hook, ref["W"]) < 1e-2
+        assert normwise(got_w, ref["W"]) <= 2e-3
+    else:
+        assert ferr(got_w, ref["W"], 1.0) <= 1e-5
+    np.testing.assert_allclose(host(it["dev"]["zbar_out"]), ref["Zbar"], rtol=1e-6, atol=1e-9)
+    np.testing.assert_array_equal(host(it["dev"]["M1"]), M1_before)
+
+
+def test_sgd_update_without_moments_and_nonfinite_guard():
+    m, n, r, q = 256, 512, 16, 4
+    it = make_item(12, (m, n), m, n, r, q, True)
+    dev = {k: v for k, v in it["dev"].items() if k not in ("M1", "M2")}
+    W0 = host(dev["W"]).copy()
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    g = dev_f32(np.array([1.0, np.nan, 0.5, 0.0], np.float32))
+    zo.subspace_sgd_update([dev], g, 1e-2, nonfinite_flag=flag)
+    torch.cuda.synchronize()
+    assert int(flag.item()) == 1
+    np.testing.assert_array_equal(host(dev["W"]), W0)
+    g = zd.f32(zd.draw(12, "G", (m, n), (q,), 1e-2))
+    zo.subspace_sgd_update([dev], dev_f32(g), 1e-2)
+    torch.cuda.synchronize()
+    ref = oracle.subspace_sgd_update(it["Wv"], it["U"], it["V"], it["Z"], g.astype(np.float64), F32(1e-2))
+    assert ferr(host(dev["w_f32_out"]), ref["W"], 1.0) <= 5e-5

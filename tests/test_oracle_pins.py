@@ -490,6 +490,25 @@ def test_zero_estimates_leave_w_unchanged():
 
 
 # ------------------------------------------------------------------ bf16 format
+def test_sgd_update_single_query_is_subzero_step():
+    """q = 1: W - lr g U Z V^T (SubZero's update), and U^T (W_new - W) V = -lr Zbar for any q."""
+    rng = np.random.default_rng(21)
+    m, n, r = 30, 20, 3
+    W = rng.standard_normal((m, n))
+    U, V = _orth(m, r, 1), _orth(n, r, 2)
+    Z = rng.standard_normal((1, r, r))
+    out = oracle.subspace_sgd_update(W, U, V, Z, [0.7], 0.1)
+    np.testing.assert_allclose(out["W"], W - 0.1 * 0.7 * U @ Z[0] @ V.T, rtol=0, atol=1e-14)
+    Zs = rng.standard_normal((4, r, r))
+    g = rng.standard_normal(4)
+    out = oracle.subspace_sgd_update(W, U, V, Zs, g, 0.05)
+    Zbar = np.einsum("j,jab->ab", g, Zs) / 4
+    np.testing.assert_allclose(U.T @ (out["W"] - W) @ V, -0.05 * Zbar, rtol=0, atol=1e-13)
+    assert np.linalg.matrix_rank(out["W"] - W, tol=1e-10) <= r
+    zero = oracle.subspace_sgd_update(W, U, V, Zs, np.zeros(4), 0.05)
+    np.testing.assert_array_equal(zero["W"], W)
+
+
 def test_round_bf16_hand_cases(golden_dir):
     cases = json.load(open(os.path.join(golden_dir, "bf16_rounding.json")))["cases"]
     for c in cases:
