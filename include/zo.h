@@ -257,7 +257,8 @@ int zo_lora_perturbed_linear_prepare(int T, int m, int n, int rl, int r, int q,
  *              non-finite entry, that item's W, M1 and M2 are left untouched
  *              and *nonfinite_flag is set to 1 (never cleared here).
  * Limits: 1 <= r <= ZO_MAX_RANK, 1 <= q <= ZO_MAX_QUERIES; bf16 W needs
- * n % 8 == 0.
+ * n % 8 == 0 and n <= 2^20 (a 512-row tile of W and of w_f32_out must stay
+ * under 2^31 bytes).
  * ------------------------------------------------------------------------ */
 typedef struct {
   int m, n;

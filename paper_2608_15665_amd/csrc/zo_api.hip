@@ -300,6 +300,7 @@ static int check_update(int count, const zo_update_item* items, int r, int q, in
     ZO_CHECK(!moments || (it.M1 && it.M2), "update: item %d has a NULL moment", i);
     if (w_dtype == ZO_BF16) {
       ZO_CHECK(it.n % 8 == 0, "update: bf16 W needs n %% 8 == 0 (item %d, n = %d)", i, it.n);
+      ZO_CHECK(it.n <= (1 << 20), "update: bf16 W needs n <= %d (item %d, n = %d)", 1 << 20, i, it.n);
       ZO_CHECK(aligned(it.W, 16) && aligned(it.w_f32_out, 16),
                "update: item %d W / w_f32_out not 16-byte aligned", i);
       ZO_CHECK((long long)((it.m + 127) / 128) * ((it.n + 255) / 256) < (1LL << 30),

@@ -145,6 +145,10 @@ def test_update_validation():
     assert "t = 0" in _detail()
     assert L.zo_subspace_adam_update(1, arr2, 1, 4, 2, fake, 1, 1e-2, 1.0, 0.95, 1e-8, None, fake,
                                      1 << 30, None) == 1
+    wide = (UpdateItem * 1)(UpdateItem(8, (1 << 20) + 8, fake, fake, fake, fake, fake, fake, None, None))
+    assert L.zo_subspace_adam_update(1, wide, 1, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, fake,
+                                     1 << 30, None) == 1
+    assert "n <=" in _detail()
     need = L.zo_subspace_adam_update_workspace(1, arr2, 4, 2, 1)
     assert need > 0
     assert L.zo_subspace_adam_update(1, arr2, 1, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, fake,
