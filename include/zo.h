@@ -48,7 +48,7 @@ extern "C" {
 
 #define ZO_ABI_VERSION 1
 #define ZO_MAX_RANK 128   /* r limit of zo_perturbed_linear and the update   */
-#define ZO_MAX_QR_RANK 64 /* r limit of zo_subspace_refresh                  */
+#define ZO_MAX_QR_RANK 128 /* r limit of zo_subspace_refresh                 */
 #define ZO_MAX_BLOCKS 256 /* nblk limit of zo_perturbed_linear               */
 #define ZO_MAX_QUERIES 256
 

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_PKG, "libzo.so")
 
 ZO_F32, ZO_BF16 = 0, 1
 ZO_MAX_RANK = 128
-ZO_MAX_QR_RANK = 64
+ZO_MAX_QR_RANK = 128
 ZO_MAX_BLOCKS = 256
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "rank deficient",
           4: "non-finite value", 5: "HIP runtime error", 6: "workspace too small"}

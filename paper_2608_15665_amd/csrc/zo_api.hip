@@ -58,10 +58,6 @@ const char* zo_last_error_detail(void) { return g_detail; }
 static int check_refresh(int count, const zo_panel* panels, int r) {
   ZO_CHECK(count >= 0, "refresh: count = %d < 0", count);
   ZO_CHECK(count == 0 || panels, "refresh: panels is NULL");
-  if (r > ZO_MAX_QR_RANK && r <= ZO_MAX_RANK) {
-    zo_set_error("refresh: r = %d above the QR limit %d", r, ZO_MAX_QR_RANK);
-    return ZO_ERR_UNSUPPORTED;
-  }
   ZO_CHECK(r >= 1 && r <= ZO_MAX_QR_RANK, "refresh: r = %d outside [1, %d]", r, ZO_MAX_QR_RANK);
   for (int p = 0; p < count; ++p) {
     const zo_panel& pn = panels[p];

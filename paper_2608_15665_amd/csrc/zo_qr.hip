@@ -286,14 +286,266 @@ int run_batch(const CqrArgs& ca, int wg, hipStream_t stream) {
   return zo_hip_status(hipGetLastError(), "k_cqr_rows");
 }
 
+// ---------------------------------------------------------------- 64 < r <= 128
+// Wide panels are padded to RP = 128.  Neither an RP x RP operand next to a
+// 128-row block nor a thread-private row of R^-1 fits at that width, so the
+// same five launches are arranged differently:
+//   rows: 256 threads, 64 rows in LDS at a time; the product Omega Mx streams
+//         Mx through LDS 32 rows of K at a time (4 x 4 register tiles, two per
+//         thread); the chunk's partial Gram is stored as its 528 upper 4 x 4
+//         blocks.
+//   chol: one RP x (RP + 1) LDS array holds R in its upper part (R_ij at
+//         [i][j + 1]) and R^-1 transposed in its lower part (X_ij at [j][i]).
+//         Cholesky and the inverse are right-looking: after column k is final,
+//         every later entry takes its fused update from it.  Each entry sees
+//         the same updates in the same order (k = 0, 1, ...) as the left-looking
+//         sums of the narrow kernel, with the same zero-pivot rule.
+constexpr int BIG_RP = 128;
+constexpr int BIG_NT = 256;
+constexpr int BIG_RW = 64;                      // rows per pass
+constexpr int BIG_KC = 32;                      // K rows of Mx staged at a time
+constexpr int BIG_NB = BIG_RP / 4;              // 4 x 4 blocks per side
+constexpr int BIG_NBLK = BIG_NB * (BIG_NB + 1) / 2;
+
+// Index of upper block (bi <= bj) in row-major order over the upper triangle.
+__device__ __forceinline__ int big_blk(int bi, int bj) {
+  return bi * BIG_NB - bi * (bi - 1) / 2 + (bj - bi);
+}
+
+template <int PASS>
+__global__ __launch_bounds__(BIG_NT) void k_cqr_rows_big(CqrArgs a) {
+  constexpr int RP = BIG_RP, NB = BIG_NB, NBLK = BIG_NBLK;
+  constexpr int BPT = (NBLK + BIG_NT - 1) / BIG_NT;
+  __shared__ __attribute__((aligned(16))) double rowbuf[BIG_RW][RP + 1];
+  __shared__ __attribute__((aligned(16))) double Mk[PASS == 0 ? 2 : BIG_KC * RP];
+  const CqrPanel& P = a.p[find_panel(a, blockIdx.x)];
+  const int chunk = blockIdx.x - P.chunk_begin;
+  const int r = a.r, tid = threadIdx.x;
+  for (int x = tid; x < BIG_RW * (RP - r); x += BIG_NT)
+    rowbuf[x / (RP - r)][r + x % (RP - r)] = 0.0;
+  int bi[BPT], bj[BPT];
+  double g[BPT][4][4];
+#pragma unroll
+  for (int t = 0; t < BPT; ++t) {
+    int b = tid + t * BIG_NT, ii = 0;
+    if (b >= NBLK) b = -1;
+    if (b >= 0) {
+      int rem = b;
+      while (rem >= NB - ii) { rem -= NB - ii; ++ii; }
+      bi[t] = ii;
+      bj[t] = ii + rem;
+    } else {
+      bi[t] = bj[t] = -1;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) g[t][u][v] = 0.0;
+  }
+  // Product tiles: column group cg, row groups rg0 and rg0 + 8.
+  const int cg = tid & 31, rg0 = tid >> 5;
+  const int nkc = (r + BIG_KC - 1) / BIG_KC;
+  const double* Msrc = PASS == 1 ? P.X1 : P.M;
+  const int row_end = min((chunk + 1) * CHUNK, P.rows);
+  for (int base = chunk * CHUNK; base < row_end; base += BIG_RW) {
+    const int nrow = min(BIG_RW, row_end - base);
+    __syncthreads();  // the previous block's rows have been consumed
+    {
+      const float* src = P.omega + (size_t)base * r;
+      for (int x = tid; x < nrow * r; x += BIG_NT) rowbuf[x / r][x % r] = (double)src[x];
+      for (int x = tid; x < (BIG_RW - nrow) * r; x += BIG_NT) rowbuf[nrow + x / r][x % r] = 0.0;
+    }
+    if (PASS >= 1) {
+      double acc[2][4][4];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) acc[t][u][v] = 0.0;
+      for (int kc = 0; kc < nkc; ++kc) {
+        __syncthreads();  // rows stored / previous Mk slice consumed
+        for (int x = tid; x < BIG_KC * RP; x += BIG_NT) Mk[x] = Msrc[(size_t)kc * BIG_KC * RP + x];
+        __syncthreads();
+#pragma unroll 4
+        for (int kk = 0; kk < BIG_KC; ++kk) {
+          const int k = kc * BIG_KC + kk;
+          const double2 m01 = *(const double2*)&Mk[kk * RP + 4 * cg];
+          const double2 m23 = *(const double2*)&Mk[kk * RP + 4 * cg + 2];
+          const double m[4] = {m01.x, m01.y, m23.x, m23.y};
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const int rg = rg0 + 8 * t;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const double av = rowbuf[4 * rg + u][k];
+#pragma unroll
+              for (int v = 0; v < 4; ++v) acc[t][u][v] = fma(av, m[v], acc[t][u][v]);
+            }
+          }
+        }
+      }
+      __syncthreads();  // every thread has read its rows of Omega
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int rg = rg0 + 8 * t;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) rowbuf[4 * rg + u][4 * cg + v] = acc[t][u][v];
+      }
+    }
+    __syncthreads();
+    if (PASS == 2) {
+      float* dst = P.q + (size_t)base * r;
+      for (int x = tid; x < nrow * r; x += BIG_NT) dst[x] = (float)rowbuf[x / r][x % r];
+      continue;
+    }
+    for (int rr = 0; rr < nrow; ++rr) {
+      const double* row = rowbuf[rr];
+#pragma unroll
+      for (int t = 0; t < BPT; ++t) {
+        if (bi[t] < 0) continue;
+        double u[4], v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          u[e] = row[4 * bi[t] + e];
+          v[e] = row[4 * bj[t] + e];
+        }
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) g[t][p][q] = fma(u[p], v[q], g[t][p][q]);
+      }
+    }
+  }
+  if (PASS == 2) return;
+  double* out = P.part + (size_t)chunk * NBLK * 16;
+#pragma unroll
+  for (int t = 0; t < BPT; ++t) {
+    if (bi[t] < 0) continue;
+    double* o = out + (size_t)big_blk(bi[t], bj[t]) * 16;
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[p * 4 + q] = g[t][p][q];
+  }
+}
+
+template <bool FINAL>
+__global__ __launch_bounds__(BIG_NT) void k_cqr_chol_big(CqrArgs a) {
+  constexpr int RP = BIG_RP, NBLK = BIG_NBLK;
+  __shared__ double A[RP][RP + 1];  // R_ij at [i][j + 1], X_ij at [j][i]  (i <= j)
+  __shared__ double inv[RP];
+  __shared__ double dg[RP];
+  const CqrPanel& P = a.p[blockIdx.x];
+  const int r = a.r, tid = threadIdx.x;
+  const int nchunk = (P.rows + CHUNK - 1) / CHUNK;
+  for (int x = tid; x < RP * RP; x += BIG_NT) {
+    const int i = x / RP, j = x % RP;
+    if (i > j) continue;
+    double s = 0.0;
+    if (j < r) {
+      const size_t e = (size_t)big_blk(i >> 2, j >> 2) * 16 + (i & 3) * 4 + (j & 3);
+      for (int c = 0; c < nchunk; ++c) s += P.part[(size_t)c * NBLK * 16 + e];
+    }
+    A[i][j + 1] = s;
+    A[j][i] = (i == j && i < r) ? 1.0 : 0.0;
+  }
+  __syncthreads();
+  // Cholesky: G = R^T R, right-looking.
+  for (int k = 0; k < r; ++k) {
+    if (tid == 0) {
+      const double d = A[k][k + 1];
+      A[k][k + 1] = d > 0.0 ? sqrt(d) : 0.0;
+    }
+    __syncthreads();
+    const double rkk = A[k][k + 1];
+    for (int j = k + 1 + tid; j < r; j += BIG_NT) A[k][j + 1] = rkk > 0.0 ? A[k][j + 1] / rkk : 0.0;
+    __syncthreads();
+    for (int i = k + 1 + (tid >> 5); i < r; i += BIG_NT / 32) {
+      const double rki = A[k][i + 1];
+      for (int j = i + (tid & 31); j < r; j += 32) A[i][j + 1] = fma(-rki, A[k][j + 1], A[i][j + 1]);
+    }
+    __syncthreads();
+  }
+  for (int j = tid; j < RP; j += BIG_NT) {
+    const double d = j < r ? A[j][j + 1] : 0.0;
+    inv[j] = d > 0.0 ? 1.0 / d : 0.0;
+  }
+  __syncthreads();
+  // X = R^-1: rows of the identity through the forward substitution, column by
+  // column; X_ij = 0 for i > j, and column j is final once scaled by 1 / R_jj.
+  for (int j = 0; j < r; ++j) {
+    for (int i = tid; i <= j; i += BIG_NT) A[j][i] *= inv[j];
+    __syncthreads();
+    for (int jj = j + 1 + (tid >> 5); jj < r; jj += BIG_NT / 32) {
+      const double rjj = A[j][jj + 1];
+      for (int i = tid & 31; i <= j; i += 32) A[jj][i] = fma(-A[j][i], rjj, A[jj][i]);
+    }
+    __syncthreads();
+  }
+  if (!FINAL) {
+    for (int x = tid; x < RP * RP; x += BIG_NT) {
+      const int i = x / RP, j = x % RP;
+      P.R1[x] = i <= j ? A[i][j + 1] : 0.0;
+      P.X1[x] = i <= j ? A[j][i] : 0.0;
+    }
+    return;
+  }
+  for (int k = tid; k < RP; k += BIG_NT) dg[k] = A[k][k + 1];
+  __syncthreads();
+  // R2 is no longer needed: X1 takes its place, then M = X1 X2.
+  for (int x = tid; x < RP * RP; x += BIG_NT) {
+    const int i = x / RP, j = x % RP;
+    if (i <= j) A[i][j + 1] = P.X1[x];
+  }
+  __syncthreads();
+  for (int x = tid; x < RP * RP; x += BIG_NT) {
+    const int i = x / RP, j = x % RP;
+    double s = 0.0;
+    for (int k = i; k <= j; ++k) s = fma(A[i][k + 1], A[j][k], s);
+    P.M[x] = s;
+  }
+  if (tid == 0) {
+    int bad = 0;
+    for (int k = 0; k < r; ++k) {
+      const double d = dg[k] * P.R1[k * RP + k];
+      if (P.r_diag) P.r_diag[k] = (float)d;
+      if (d == 0.0 && bad == 0) bad = k + 1;
+    }
+    if (P.info) *P.info = bad;
+  }
+}
+
+size_t panel_ws_big(int rows) {
+  const size_t nchunk = (size_t)(rows + CHUNK - 1) / CHUNK;
+  return zo_align256(nchunk * BIG_NBLK * 16 * 8) + 3 * zo_align256((size_t)BIG_RP * BIG_RP * 8);
+}
+
+int run_batch_big(const CqrArgs& ca, int wg, hipStream_t stream) {
+  int st;
+  hipLaunchKernelGGL(k_cqr_rows_big<0>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
+  if ((st = zo_hip_status(hipGetLastError(), "k_cqr_rows_big")) != ZO_OK) return st;
+  hipLaunchKernelGGL(k_cqr_chol_big<false>, dim3(ca.count), dim3(BIG_NT), 0, stream, ca);
+  if ((st = zo_hip_status(hipGetLastError(), "k_cqr_chol_big")) != ZO_OK) return st;
+  hipLaunchKernelGGL(k_cqr_rows_big<1>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
+  if ((st = zo_hip_status(hipGetLastError(), "k_cqr_rows_big")) != ZO_OK) return st;
+  hipLaunchKernelGGL(k_cqr_chol_big<true>, dim3(ca.count), dim3(BIG_NT), 0, stream, ca);
+  if ((st = zo_hip_status(hipGetLastError(), "k_cqr_chol_big")) != ZO_OK) return st;
+  hipLaunchKernelGGL(k_cqr_rows_big<2>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
+  return zo_hip_status(hipGetLastError(), "k_cqr_rows_big");
+}
+
 }  // namespace
 
 int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void* ws,
                       size_t ws_bytes, hipStream_t stream, size_t* ws_needed) {
-  const int RK = (r + 15) / 16;
+  const bool big = r > 64;
+  const int RK = big ? BIG_RP / 16 : (r + 15) / 16;
   const int RP = 16 * RK;
   size_t need = 0;
-  for (int p = 0; p < count; ++p) need += panel_ws(panels[p].rows, RP);
+  for (int p = 0; p < count; ++p) need += big ? panel_ws_big(panels[p].rows) : panel_ws(panels[p].rows, RP);
   if (ws_needed) *ws_needed = need;
   if (!ws) return ZO_OK;
   if (ws_bytes < need) {
@@ -313,7 +565,7 @@ int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void*
       e.q = panels[p].q;
       e.r_diag = panels[p].r_diag;
       e.info = info ? info + p : nullptr;
-      e.part = (double*)wc.take((size_t)nchunk * RP * RP * 8);
+      e.part = (double*)wc.take((size_t)nchunk * (big ? BIG_NBLK * 16 : RP * RP) * 8);
       e.R1 = (double*)wc.take((size_t)RP * RP * 8);
       e.X1 = (double*)wc.take((size_t)RP * RP * 8);
       e.M = (double*)wc.take((size_t)RP * RP * 8);
@@ -321,7 +573,8 @@ int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void*
       e.chunk_begin = wg;
       wg += nchunk;
     }
-    switch (RK) {
+    switch (big ? 0 : RK) {
+      case 0: st = run_batch_big(ca, wg, stream); break;
       case 1: st = run_batch<1>(ca, wg, stream); break;
       case 2: st = run_batch<2>(ca, wg, stream); break;
       case 3: st = run_batch<3>(ca, wg, stream); break;

@@ -124,7 +124,7 @@ def test_refresh_validation():
     arr = (Panel * 2)(Panel(10, fake, fake, None), Panel(3, fake, fake, None))
     assert L.zo_subspace_refresh(2, arr, 4, None, fake, 1 << 30, None) == 1
     assert "rows = 3 < r = 4" in _detail()
-    assert L.zo_subspace_refresh(1, arr, 100, None, fake, 1 << 30, None) == 2  # above the QR rank limit
+    assert L.zo_subspace_refresh(1, arr, 129, None, fake, 1 << 30, None) == 1  # above the rank limit
     assert L.zo_subspace_refresh(1, arr, 0, None, fake, 1 << 30, None) == 1
     assert L.zo_subspace_refresh_workspace(1, arr, 4) > 0
     assert L.zo_subspace_refresh(1, arr, 4, None, fake, 16, None) == 6

@@ -80,6 +80,7 @@ def run_oracle(c, eps, blocks=None, rows=None):
     (37, 50, 70, 5, 3, 6, False),       # ragged everything
     (1, 3, 1, 1, 1, 1, False),          # degenerate sizes
     (130, 72, 300, 20, 2, 4, True),
+    (64, 200, 300, 128, 2, 4, False),   # r = 128, the paper's full-tuning rank
 ])
 def test_fp32_parity(T, m, n, r, q, nblk, shared):
     c = make_case(T, m, n, r, q, nblk, shared, bf16=False)
@@ -95,6 +96,8 @@ def test_fp32_parity(T, m, n, r, q, nblk, shared):
     (96, 520, 136, 24, 3, 6, True),     # r not a multiple of 16, shared X
     (513, 256, 1024, 4, 1, 2, False),   # one row past a tile
     (8, 8, 8, 1, 1, 1, True),           # smallest legal bf16 shape
+    (192, 256, 384, 128, 2, 4, False),  # r = 128, the paper's full-tuning rank
+    (100, 136, 264, 100, 3, 6, True),   # r = 100 padded to 128
 ])
 @pytest.mark.parametrize("out", ["bf16", "f32"])
 def test_bf16_parity(T, m, n, r, q, nblk, shared, out):
@@ -120,10 +123,11 @@ def test_bf16_eps_one_correction_visible():
         assert normwise(base[b], ref[b]) > 5e-2  # the correction matters at this eps
 
 
-def test_correction_channel_fp32_out():
+@pytest.mark.parametrize("r", [16, 128])
+def test_correction_channel_fp32_out(r):
     """X_{2j} = X_{2j+1}: (Y+ - Y-)/(2 eps) isolates (X V)(U Z_j)^T, which a kernel that dropped
     or mis-signed the rank-r term would fail (it is below bf16 resolution of Y)."""
-    T, m, n, r, q = 256, 256, 512, 16, 3
+    T, m, n, q = 256, 256, 512, 3
     c = make_case(T, m, n, r, q, 2 * q, False, bf16=True)
     X0 = c["X0v"]
     c["Xd"] = torch.cat([c["Xd"][:T]] * (2 * q)).contiguous()  # block 0 (unrolled) for every block
@@ -175,13 +179,18 @@ FULL_SIZE = [(name, m, n) for name in ("opt-1.3b", "llama-7b", "opt-13b")
              for m, n in _distinct_shapes(zd.CONFIGS[name])]
 
 
-@pytest.mark.parametrize("name,m,n", FULL_SIZE)
-def test_full_size_sampled(name, m, n):
+FULL_SIZE_R128 = [("opt-13b", m, n, 128) for m, n in _distinct_shapes(zd.CONFIGS["opt-13b"])]
+
+
+@pytest.mark.parametrize("name,m,n,rank", [(*x, None) for x in FULL_SIZE] + FULL_SIZE_R128)
+def test_full_size_sampled(name, m, n, rank):
     """Every distinct matrix shape of the OPT-1.3B, LLaMA-7B and OPT-13B stacks at full size
-    (T tokens per block, 2q blocks, the config's r) in the launch configuration the benchmark
-    times; sampled token rows of several blocks checked against the oracle row by row."""
+    (T tokens per block, 2q blocks, the config's r; the OPT-13B shapes also at the paper's
+    full-tuning rank r = 128) in the launch configuration the benchmark times; sampled token
+    rows of several blocks checked against the oracle row by row."""
     cfg = zd.CONFIGS[name]
-    T, r, q = cfg["T"], cfg["r"], cfg["q"]
+    T, q = cfg["T"], cfg["q"]
+    r = rank or cfg["r"]
     nblk = 2 * q
     c = make_case(T, m, n, r, q, nblk, False, bf16=True)
     Y = zo.perturbed_linear(c["Xd"], c["Wd"], c["Ud"], c["Vd"], c["Zd"], c["bq"], c["bs"], 1e-3, T,

@@ -47,6 +47,8 @@ def check(Q, rd, Om):
     (5120, 64), (20480, 64),             # OPT-13B
     (8, 4), (27648, 4),                  # Qwen LoRA factors
     (64, 64), (65, 64), (257, 64), (300, 37), (1, 1), (1025, 3),
+    (5120, 128), (20480, 128),           # the paper's full-tuning rank at OPT-13B sizes
+    (128, 128), (65, 65), (300, 100), (1025, 96), (2049, 72), (4096, 24),
 ])
 def test_refresh_parity(rows, r):
     Om = zd.f32(zd.draw(0, "OMEGA_U", (rows, r), (rows, r)))
@@ -65,19 +67,38 @@ def test_refresh_batched_mixed_rows_inplace():
         check(q, d, om)
 
 
-def test_refresh_rank_deficient_flag():
-    r = 6
+def test_refresh_batched_wide_rank():
+    """r = 128 over 50 panels of mixed rows (two launches of the wide kernels)."""
+    r = 128
+    rows = [128, 300, 2048, 1100, 129] * 10
+    Oms = [zd.f32(zd.draw(4, "OMEGA_V", (i,), (rw, r))) for i, rw in enumerate(rows)]
+    Q, rd, info = run(Oms, r, inplace=True)
+    assert np.all(info == 0)
+    for q, d, om in zip(Q, rd, Oms):
+        check(q, d, om)
+
+
+@pytest.mark.parametrize("r,zero_col", [(6, 3), (128, 70), (100, 0)])
+def test_refresh_rank_deficient_flag(r, zero_col):
     Om = zd.f32(zd.draw(2, "OMEGA_U", (0,), (500, r)))
-    Om[:, 3] = 0.0
+    Om[:, zero_col] = 0.0
     Q, rd, info = run([Om], r)
-    assert info[0] == 4  # first zero diagonal at column 3
-    assert rd[0][3] == 0.0
+    assert info[0] == zero_col + 1  # first zero diagonal at that column
+    assert rd[0][zero_col] == 0.0
+    assert np.all(Q[0][:, zero_col] == 0.0)
+    # The other columns are the Haar factor of the panel without that column.
+    keep = [c for c in range(r) if c != zero_col]
+    U, R, bad = oracle.haar_qr(np.delete(Om, zero_col, axis=1).astype(np.float64))
+    assert bad == -1
+    assert ferr(Q[0][:, keep], U, 1.0) <= 1e-5
+    np.testing.assert_allclose(rd[0][keep], np.diag(R), rtol=1e-5)
 
 
-def test_refresh_deterministic():
-    Om = zd.f32(zd.draw(3, "OMEGA_U", (0,), (5120, 64)))
-    a = run([Om], 64)[0][0]
-    b = run([Om], 64)[0][0]
+@pytest.mark.parametrize("rows,r", [(5120, 64), (5120, 128)])
+def test_refresh_deterministic(rows, r):
+    Om = zd.f32(zd.draw(3, "OMEGA_U", (0,), (rows, r)))
+    a = run([Om], r)[0][0]
+    b = run([Om], r)[0][0]
     assert np.array_equal(a, b)
 
 
