@@ -99,7 +99,7 @@ def copy_calibration():
                       "launches": 3}))
 
 
-def cpu_baseline(cfg, seed, budget_s, mat, lora):
+def cpu_baseline(cfg, seed, budget_s, mat, lora, r):
     """The float64 oracle on a bounded sample of the same workload, on this host's cores."""
     import numpy as np
     import oracle
@@ -109,7 +109,7 @@ def cpu_baseline(cfg, seed, budget_s, mat, lora):
         threads = max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
     except Exception:  # pragma: no cover
         threads = 1
-    T, r, q = cfg["T"], cfg["r"], cfg["q"]
+    T, q = cfg["T"], cfg["q"]
     m, n = mat[1], mat[2]
     rl, scale = zd.QWEN_LORA_RANK, zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
     S = 256
@@ -154,6 +154,7 @@ def main():
     ap.add_argument("--estimator", default="central", choices=["central", "forward"],
                     help="central: 2q blocks (+/-); forward: a baseline block and q perturbed blocks (Eq. 6)")
     ap.add_argument("--queries", type=int, default=0, help="queries per step (default: the config's q)")
+    ap.add_argument("--rank", type=int, default=0, help="subspace rank r (default: the config's r)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -181,6 +182,8 @@ def main():
     T, r, q = cfg["T"], cfg["r"], cfg["q"]
     if args.queries:
         q = args.queries
+    if args.rank:
+        r = args.rank
     forward = args.estimator == "forward"
     # Query blocks: central -- (j, +), (j, -); forward -- the baseline (sign 0), then (j, +).
     if forward:
@@ -352,7 +355,7 @@ def main():
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         tr = json.load(open(TRAFFIC_FILE))
-        if tr.get("source_hash") == source_hash() and tr.get("workload_key") == f"{args.config}/{args.estimator}/q={q}":
+        if tr.get("source_hash") == source_hash() and tr.get("workload_key") == f"{args.config}/{args.estimator}/q={q}/r={r}":
             traffic = tr.get("bytes_per_launch")
     upd_gbps = upd_bytes / (upd_ms * 1e-3) / 1e9
     out = {
@@ -386,7 +389,7 @@ def main():
     if not args.no_cpu_baseline:
         del plins, items, X, Y, ws, units
         torch.cuda.empty_cache()
-        out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget, unit_mats[0], lora)
+        out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget, unit_mats[0], lora, r)
     print(json.dumps(out), flush=True)
 
 
