@@ -72,14 +72,19 @@ def _region(text, start, end):
 
 
 def source_hash():
-    """Hash of the source text the dominant kernel is built from: its argument struct, the
-    kernel with its launcher, and the bf16 rounding helpers its epilogue uses."""
+    """Hash of the source text the dominant kernel is built from: its argument struct, its
+    MFMA and store helpers, the kernel with its launcher, and the 16-bit rounding helpers its
+    epilogue uses."""
     gemm = open(os.path.join(CSRC, "zo_gemm.hip")).read()
     inc = open(os.path.join(CSRC, "zo_internal.h")).read()
     parts = [_region(gemm, "struct GemmArgs {", "};"),
+             _region(gemm, "template <int OUT>\n__device__ __forceinline__ void store4(", "\n}\n"),
+             _region(gemm, "__device__ __forceinline__ f32x16 mfma32(", "\n}\n"),
              _region(gemm, "__device__ __forceinline__ int g4(int r)", 'hipGetLastError(), "k_gemm_main");\n}'),
-             _region(inc, "__device__ __forceinline__ bf16_t f32_to_bf16(", "}"),
-             _region(inc, "__device__ __forceinline__ uint32_t pack_bf16x2(", "}")]
+             _region(inc, "__device__ __forceinline__ bf16_t f32_to_bf16(", "\n}\n"),
+             _region(inc, "__device__ __forceinline__ uint32_t pack_bf16x2(", "\n}\n"),
+             _region(inc, "__device__ __forceinline__ uint16_t f32_to_f16(", "\n}\n"),
+             _region(inc, "__device__ __forceinline__ uint32_t pack_f16x2(", "\n}\n")]
     h = hashlib.sha256()
     for p in parts:
         h.update(p.encode())
@@ -99,7 +104,7 @@ def copy_calibration():
                       "launches": 3}))
 
 
-def cpu_baseline(cfg, seed, budget_s, mat, lora, r):
+def cpu_baseline(cfg, seed, budget_s, mat, lora, r, f16=False):
     """The float64 oracle on a bounded sample of the same workload, on this host's cores."""
     import numpy as np
     import oracle
@@ -113,8 +118,9 @@ def cpu_baseline(cfg, seed, budget_s, mat, lora, r):
     m, n = mat[1], mat[2]
     rl, scale = zd.QWEN_LORA_RANK, zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
     S = 256
-    W = zd.as_bf16_values(zd.draw(seed, "W0", (m, n), (m, n), 0.02))[1]
-    X0 = zd.as_bf16_values(zd.draw(seed, "X", (T, n, 0), (S, n)))[1]
+    cast = zd.as_f16_values if f16 else zd.as_bf16_values
+    W = cast(zd.draw(seed, "W0", (m, n), (m, n), 0.02))[1]
+    X0 = cast(zd.draw(seed, "X", (T, n, 0), (S, n)))[1]
     U, _ = np.linalg.qr(zd.draw(seed, "OMEGA_U", (0, m), (m, r)))
     V, _ = np.linalg.qr(zd.draw(seed, "OMEGA_V", (0, n), (n, r)))
     Z = zd.z_draws(seed, 0, 0, q, r).astype(np.float64)
@@ -155,6 +161,8 @@ def main():
                     help="central: 2q blocks (+/-); forward: a baseline block and q perturbed blocks (Eq. 6)")
     ap.add_argument("--queries", type=int, default=0, help="queries per step (default: the config's q)")
     ap.add_argument("--rank", type=int, default=0, help="subspace rank r (default: the config's r)")
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "fp16"],
+                    help="weights and activations (fp16: the paper's precision for OPT-13B)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -197,12 +205,17 @@ def main():
     rl, scale = zd.QWEN_LORA_RANK, zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
     seed = args.seed
     dev = "cuda"
-    bf16 = torch.bfloat16
+    f16 = args.dtype == "fp16"
+    dt16 = torch.float16 if f16 else torch.bfloat16
+    zdt = zo.ZO_F16 if f16 else zo.ZO_BF16
     t_setup = time.perf_counter()
 
     def to_bf16(a64):
+        """A float64 host draw as a device tensor of the run's 16-bit type."""
+        if f16:
+            return torch.from_numpy(zd.as_f16_values(a64)[0]).to(dev)
         bits = zd.bf16_bits(zd.f32(a64))
-        return torch.from_numpy(bits.view(np.int16)).view(bf16).to(dev)
+        return torch.from_numpy(bits.view(np.int16)).view(dt16).to(dev)
 
     def f32dev(a64):
         return torch.from_numpy(zd.f32(a64)).to(dev)
@@ -219,7 +232,7 @@ def main():
         x0 = to_bf16(zd.draw(seed, "X", (T, n, 0), (T, n)))
         X[n] = torch.cat([torch.roll(x0, b * (T // nblk), 0) for b in range(nblk)]).contiguous()
         del x0
-    Y = {m: torch.empty((nblk * T, m), dtype=bf16, device=dev) for m in sorted({m for _, m, _ in unit_mats})}
+    Y = {m: torch.empty((nblk * T, m), dtype=dt16, device=dev) for m in sorted({m for _, m, _ in unit_mats})}
     rows_set = sorted({m for _, m, _ in unit_mats} | set(ns) | ({rl} if lora else set()))
     Obase = {rw: f32dev(zd.draw(seed, "OMEGA_U", (rw, r), (rw, r))) for rw in rows_set}
     zeros_rr = lambda: torch.zeros((r, r), dtype=torch.float32, device=dev)
@@ -249,10 +262,10 @@ def main():
     m_last = unit_mats[-1][1]
     Ystar = to_bf16(zd.draw(seed, "X", (T, m_last, 1), (T, m_last)))
     if lora:
-        ws_need = max(zo.lib().zo_lora_perturbed_linear_workspace(T, m, n, rl, r, q, nblk, T * n, zo.ZO_BF16)
+        ws_need = max(zo.lib().zo_lora_perturbed_linear_workspace(T, m, n, rl, r, q, nblk, T * n, zdt)
                       for m, n in shapes)
     else:
-        ws_need = max(zo.lib().zo_perturbed_linear_workspace(T, m, n, r, q, nblk, T * n, zo.ZO_BF16)
+        ws_need = max(zo.lib().zo_perturbed_linear_workspace(T, m, n, r, q, nblk, T * n, zdt)
                       for m, n in shapes)
     ws = torch.empty(ws_need, dtype=torch.uint8, device=dev)
 
@@ -355,20 +368,21 @@ def main():
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         tr = json.load(open(TRAFFIC_FILE))
-        if tr.get("source_hash") == source_hash() and tr.get("workload_key") == f"{args.config}/{args.estimator}/q={q}/r={r}":
+        key = f"{args.config}/{args.estimator}/q={q}/r={r}/{args.dtype}"
+        if tr.get("source_hash") == source_hash() and tr.get("workload_key") == key:
             traffic = tr.get("bytes_per_launch")
     upd_gbps = upd_bytes / (upd_ms * 1e-3) / 1e9
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round((t1 - t0) / args.steps * 1e3, 2), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": args.dtype, "data": "synthetic",
         "config": {"workload": (f"{args.config}-shaped stack: {L} layers x "
                                 + ", ".join(f"{nm} {m}x{n}" for nm, m, n in unit_mats)
-                                + (f" (frozen bf16 base, fp32 LoRA adapter r_L={rl}, alpha={int(scale * rl)}, "
+                                + (f" (frozen {args.dtype} base, fp32 LoRA adapter r_L={rl}, alpha={int(scale * rl)}, "
                                    f"each factor in its own subspace)" if lora else "")
                                 + (f"; {nblk} blocks (baseline + q={q} forward queries)" if forward
                                    else f"; {nblk} query blocks (q={q}, +/-)")
-                                + f" of T={T} tokens; r={r}; bf16 W and X"),
+                                + f" of T={T} tokens; r={r}; {args.dtype} W and X"),
                    "layers": L, "perturbed_layers": len(units), "T": T, "r": r, "q": q, "blocks": nblk,
                    "estimator": args.estimator,
                    "refresh_every": F},
@@ -389,7 +403,7 @@ def main():
     if not args.no_cpu_baseline:
         del plins, items, X, Y, ws, units
         torch.cuda.empty_cache()
-        out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget, unit_mats[0], lora, r)
+        out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget, unit_mats[0], lora, r, f16)
     print(json.dumps(out), flush=True)
 
 

@@ -62,7 +62,7 @@ typedef enum {
   ZO_ERR_WORKSPACE = 6
 } zo_status;
 
-typedef enum { ZO_F32 = 0, ZO_BF16 = 1 } zo_dtype;
+typedef enum { ZO_F32 = 0, ZO_BF16 = 1, ZO_F16 = 2 } zo_dtype;
 
 int zo_abi_version(void);
 const char* zo_status_str(int status);
@@ -121,21 +121,26 @@ int zo_subspace_refresh(int count, const zo_panel* panels, int r, int* info,
  *   X            device, block b starts at X + b * x_block_stride elements,
  *                each block T x n.  x_block_stride = 0: all blocks share one
  *                X (the first layer of a network); otherwise >= T*n.
- *   W            device, m x n.  in_dtype ZO_BF16 or ZO_F32 for X and W.
+ *   W            device, m x n.  in_dtype ZO_BF16, ZO_F16 or ZO_F32 for X
+ *                and W.
  *   U, V         device fp32, m x r and n x r (column-orthonormal).
  *   Z            device fp32, q x r x r (Z_j row-major).
  *   blk_query    host, nblk ints in [0, q).
  *   blk_sign     host, nblk int8 in {+1, -1, 0}.
- *   Y            device, nblk blocks of T x m, contiguous; out_dtype ZO_BF16
- *                or ZO_F32 (fp32 inputs require fp32 output).
- * Arithmetic: bf16 inputs use bf16 MFMA with fp32 accumulation.  The rank-r
- * term is added into the same accumulators with its operands X_b V and
- * s eps U Z_j each carried as a high + low pair of bf16 (about 16
- * significant bits; X_b V itself formed from the same split of V), so it is
- * ~2^-16 accurate relative to its own size.  Outputs rounded to nearest
- * even.  fp32 inputs use fp32 FMA throughout.
+ *   Y            device, nblk blocks of T x m, contiguous; out_dtype is
+ *                in_dtype or ZO_F32 (fp32 inputs require fp32 output).
+ * Arithmetic: bf16 (fp16) inputs use bf16 (fp16) MFMA for X_b W^T with fp32
+ * accumulation.  The rank-r term is added into the same accumulators with
+ * its operands X_b V and s eps U Z_j each carried as a high + low pair of
+ * bf16 (about 16 significant bits, and bf16's range: eps U Z_j entries sit
+ * near fp16's smallest normal), so it is ~2^-16 accurate relative to its own
+ * size.  X_b V itself is formed by the input type's MFMA from a high + low
+ * split of V (for fp16, of 256 V, scaled back exactly).  Outputs rounded to
+ * nearest even.  fp32 inputs use fp32 FMA throughout.
  * Limits: 1 <= r <= ZO_MAX_RANK, 1 <= q <= ZO_MAX_QUERIES, 1 <= nblk <=
- * ZO_MAX_BLOCKS; bf16 inputs need m % 8 == 0 and n % 8 == 0.
+ * ZO_MAX_BLOCKS; 16-bit inputs need m % 8 == 0 and n % 8 == 0; fp16 inputs
+ * need |V| < 255 entrywise (a column-orthonormal V has |V| <= 1; larger
+ * entries overflow the scaled split to infinity).
  * ------------------------------------------------------------------------ */
 size_t zo_perturbed_linear_workspace(int T, int m, int n, int r, int q, int nblk,
                                      long long x_block_stride, int in_dtype);
@@ -192,7 +197,9 @@ int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk,
  *   U_B, V_B    device fp32, m x r and rl x r.
  *   Z_A, Z_B    device fp32, q x r x r each.
  * Arithmetic as for zo_perturbed_linear with rank rl + r (the adapter
- * operands enter the bf16 GEMM as high + low bf16 pairs).
+ * operands enter the GEMM as high + low bf16 pairs; with fp16 inputs the
+ * projection's right factor [A ; V_A^T] needs entries below 255 in
+ * magnitude).
  * Limits: rl >= 1, r >= 1, rl + r <= ZO_MAX_RANK; the rest as for
  * zo_perturbed_linear.
  *
@@ -243,8 +250,9 @@ int zo_lora_perturbed_linear_prepare(int T, int m, int n, int rl, int r, int q,
  *
  * t >= 1 is the 1-based Adam step.  The r x r work is float64 inside; the
  * moments are stored fp32.  The m x n product is accumulated in fp32
- * (bf16 W: MFMA on a hi+lo bf16 split of lr U S and V; fp32 W: fp32 FMA),
- * added to W in fp32 and rounded to nearest even when W is bf16.
+ * (bf16 or fp16 W: MFMA on a hi+lo bf16 split of lr U S and V; fp32 W: fp32
+ * FMA), added to W in fp32 and rounded to nearest even when W is bf16 or
+ * fp16 (fp16 overflows to infinity, as IEEE rounding does).
  *
  *   W          device m x n (w_dtype), updated in place.
  *   U, V, Z    device fp32: m x r, n x r, q x r x r.
@@ -256,7 +264,7 @@ int zo_lora_perturbed_linear_prepare(int T, int m, int n, int rl, int r, int q,
  *   nonfinite_flag  device int, nullable.  If Zbar or S of an item has a
  *              non-finite entry, that item's W, M1 and M2 are left untouched
  *              and *nonfinite_flag is set to 1 (never cleared here).
- * Limits: 1 <= r <= ZO_MAX_RANK, 1 <= q <= ZO_MAX_QUERIES; bf16 W needs
+ * Limits: 1 <= r <= ZO_MAX_RANK, 1 <= q <= ZO_MAX_QUERIES; 16-bit W needs
  * n % 8 == 0 and n <= 2^20 (a 512-row tile of W and of w_f32_out must stay
  * under 2^31 bytes).
  * ------------------------------------------------------------------------ */
@@ -301,8 +309,8 @@ int zo_subspace_sgd_update(int count, const zo_update_item* items, int w_dtype,
 /* ------------------------------------------------------------------------
  * Squared-error loss per block (the loss of a one-layer regression model):
  * out[b] = 0.5 * sum((Y_b - Ystar)^2) / T, float64 accumulation in a fixed
- * order.  Y: nblk blocks of T x m (dtype), Ystar: T x m (same dtype), out:
- * device float64 [nblk].
+ * order.  Y: nblk blocks of T x m (dtype: ZO_F32, ZO_BF16 or ZO_F16), Ystar:
+ * T x m (same dtype), out: device float64 [nblk].
  * ------------------------------------------------------------------------ */
 size_t zo_sq_loss_workspace(int nblk, int T, int m);
 int zo_sq_loss(int nblk, int T, int m, int dtype, const void* Y,

@@ -18,7 +18,7 @@ __all__ = [
     "perturbation", "perturbed_weight", "perturbed_linear", "perturbed_linear_blocks",
     "lora_perturbed_factors", "lora_perturbed_linear", "lora_perturbed_linear_blocks",
     "sq_loss", "central_estimate", "forward_estimate", "aggregate",
-    "adam_direction", "subspace_adam_update", "subspace_sgd_update", "round_bf16", "tiny_run",
+    "adam_direction", "subspace_adam_update", "subspace_sgd_update", "round_bf16", "round_f16", "tiny_run",
 ]
 
 
@@ -262,6 +262,21 @@ def round_bf16(x):
     f, e = np.frexp(x)
     q = np.ldexp(1.0, e - 8)
     return np.rint(x / q) * q
+
+
+def round_f16(x):
+    """Round float64 values to the nearest IEEE binary16 value, ties to even.
+
+    Written from the format definition: 11 significant bits, so the quantum
+    in the binade [2^(e-1), 2^e) is 2^(e-11); below the smallest normal
+    2^-14 the quantum stays 2^-24 (subnormals); a result beyond the largest
+    finite value (2 - 2^-10) 2^15 = 65504 becomes an infinity of x's sign.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    f, e = np.frexp(x)
+    q = np.ldexp(1.0, np.maximum(e - 11, -24))
+    y = np.rint(x / q) * q
+    return np.where(np.abs(y) > 65504.0, np.copysign(np.inf, x), y)
 
 
 # ---------------------------------------------------------------------------

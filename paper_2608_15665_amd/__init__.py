@@ -12,13 +12,13 @@ of include/zo.h); this package only binds it.  Entry points:
     sq_loss, combine_central, combine_forward   loss and estimate helpers (central
                            difference, or forward difference against a baseline block)
 """
-from ._lib import (ZO_BF16, ZO_F32, ZO_MAX_BLOCKS, ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH,
+from ._lib import (ZO_BF16, ZO_F16, ZO_F32, ZO_MAX_BLOCKS, ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH,
                    LoraPerturbedLinear, PerturbedLinear, Workspace, ZoError, abi_version, combine_central,
                    combine_forward, lib,
                    lora_perturbed_linear, perturbed_linear, sq_loss, subspace_adam_update, subspace_refresh,
                    subspace_sgd_update)
 
-__all__ = ["ZO_BF16", "ZO_F32", "ZO_MAX_BLOCKS", "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH",
+__all__ = ["ZO_BF16", "ZO_F16", "ZO_F32", "ZO_MAX_BLOCKS", "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH",
            "LoraPerturbedLinear", "PerturbedLinear", "Workspace", "ZoError", "abi_version", "combine_central",
            "combine_forward", "lib",
            "lora_perturbed_linear", "perturbed_linear", "sq_loss", "subspace_adam_update", "subspace_refresh",

@@ -18,7 +18,7 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libzo.so")
 
-ZO_F32, ZO_BF16 = 0, 1
+ZO_F32, ZO_BF16, ZO_F16 = 0, 1, 2
 ZO_MAX_RANK = 128
 ZO_MAX_QR_RANK = 128
 ZO_MAX_BLOCKS = 256
@@ -156,7 +156,7 @@ def _need(t: torch.Tensor, name: str, dtype=None, numel=None) -> torch.Tensor:
     return t
 
 
-_DT = {torch.float32: ZO_F32, torch.bfloat16: ZO_BF16}
+_DT = {torch.float32: ZO_F32, torch.bfloat16: ZO_BF16, torch.float16: ZO_F16}
 
 
 class Workspace:

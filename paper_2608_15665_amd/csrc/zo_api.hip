@@ -102,15 +102,15 @@ static int check_plinear(int T, int m, int n, int r, int q, int nblk, long long 
            ZO_MAX_QUERIES);
   ZO_CHECK(nblk >= 1 && nblk <= ZO_MAX_BLOCKS, "perturbed_linear: nblk = %d outside [1, %d]", nblk,
            ZO_MAX_BLOCKS);
-  ZO_CHECK(in_dtype == ZO_F32 || in_dtype == ZO_BF16, "perturbed_linear: bad in_dtype %d",
-           in_dtype);
+  ZO_CHECK(in_dtype == ZO_F32 || in_dtype == ZO_BF16 || in_dtype == ZO_F16,
+           "perturbed_linear: bad in_dtype %d", in_dtype);
   ZO_CHECK(xs == 0 || xs >= (long long)T * n,
            "perturbed_linear: x_block_stride = %lld must be 0 or >= T*n", xs);
   ZO_CHECK((long long)T * nblk < (1LL << 31), "perturbed_linear: T * nblk too large");
-  if (in_dtype == ZO_BF16) {
-    ZO_CHECK(m % 8 == 0 && n % 8 == 0, "perturbed_linear: bf16 needs m %% 8 == 0 and n %% 8 == 0 "
-             "(got m = %d, n = %d)", m, n);
-    ZO_CHECK(xs % 8 == 0, "perturbed_linear: bf16 x_block_stride must be a multiple of 8");
+  if (in_dtype != ZO_F32) {
+    ZO_CHECK(m % 8 == 0 && n % 8 == 0, "perturbed_linear: 16-bit inputs need m %% 8 == 0 and "
+             "n %% 8 == 0 (got m = %d, n = %d)", m, n);
+    ZO_CHECK(xs % 8 == 0, "perturbed_linear: 16-bit x_block_stride must be a multiple of 8");
   }
   return ZO_OK;
 }
@@ -128,14 +128,14 @@ static int check_plinear_call(int T, int m, int n, int r, int q, int nblk, long 
                               const void* Y, void* workspace, size_t ws_bytes, PlinearPlan* p) {
   int st = check_plinear(T, m, n, r, q, nblk, xs, in_dtype);
   if (st != ZO_OK) return st;
-  ZO_CHECK(out_dtype == ZO_F32 || out_dtype == ZO_BF16, "perturbed_linear: bad out_dtype %d",
-           out_dtype);
-  if (in_dtype == ZO_F32 && out_dtype != ZO_F32) {
-    zo_set_error("perturbed_linear: fp32 inputs need fp32 output");
+  ZO_CHECK(out_dtype == ZO_F32 || out_dtype == ZO_BF16 || out_dtype == ZO_F16,
+           "perturbed_linear: bad out_dtype %d", out_dtype);
+  if (out_dtype != ZO_F32 && out_dtype != in_dtype) {
+    zo_set_error("perturbed_linear: out_dtype %d must be in_dtype (%d) or fp32", out_dtype, in_dtype);
     return ZO_ERR_UNSUPPORTED;
   }
   ZO_CHECK(X, "perturbed_linear: NULL tensor argument (X)");
-  const size_t al = in_dtype == ZO_BF16 ? 16 : 4;
+  const size_t al = in_dtype != ZO_F32 ? 16 : 4;
   ZO_CHECK(aligned(X, al) && aligned(W, al) && aligned(Y, al),
            "perturbed_linear: X, W and Y must be %zu-byte aligned", al);
   zo_plinear_plan(p, T, m, n, r, q, nblk, xs, in_dtype, out_dtype);
@@ -287,16 +287,18 @@ static int check_update(int count, const zo_update_item* items, int r, int q, in
   ZO_CHECK(count == 0 || items, "update: items is NULL");
   ZO_CHECK(r >= 1 && r <= ZO_MAX_RANK, "update: r = %d outside [1, %d]", r, ZO_MAX_RANK);
   ZO_CHECK(q >= 1 && q <= ZO_MAX_QUERIES, "update: q = %d outside [1, %d]", q, ZO_MAX_QUERIES);
-  ZO_CHECK(w_dtype == ZO_F32 || w_dtype == ZO_BF16, "update: bad w_dtype %d", w_dtype);
+  ZO_CHECK(w_dtype == ZO_F32 || w_dtype == ZO_BF16 || w_dtype == ZO_F16, "update: bad w_dtype %d",
+           w_dtype);
   for (int i = 0; i < count; ++i) {
     const zo_update_item& it = items[i];
     ZO_CHECK(it.m >= 1 && it.n >= 1, "update: item %d has m = %d, n = %d", i, it.m, it.n);
     ZO_CHECK((long long)it.m * it.n < (1LL << 40), "update: item %d too large", i);
     ZO_CHECK(it.W && it.U && it.V && it.Z, "update: item %d has a NULL tensor", i);
     ZO_CHECK(!moments || (it.M1 && it.M2), "update: item %d has a NULL moment", i);
-    if (w_dtype == ZO_BF16) {
-      ZO_CHECK(it.n % 8 == 0, "update: bf16 W needs n %% 8 == 0 (item %d, n = %d)", i, it.n);
-      ZO_CHECK(it.n <= (1 << 20), "update: bf16 W needs n <= %d (item %d, n = %d)", 1 << 20, i, it.n);
+    if (w_dtype != ZO_F32) {
+      ZO_CHECK(it.n % 8 == 0, "update: 16-bit W needs n %% 8 == 0 (item %d, n = %d)", i, it.n);
+      ZO_CHECK(it.n <= (1 << 20), "update: 16-bit W needs n <= %d (item %d, n = %d)", 1 << 20, i,
+               it.n);
       ZO_CHECK(aligned(it.W, 16) && aligned(it.w_f32_out, 16),
                "update: item %d W / w_f32_out not 16-byte aligned", i);
       ZO_CHECK((long long)((it.m + 127) / 128) * ((it.n + 255) / 256) < (1LL << 30),
@@ -384,7 +386,7 @@ int zo_sq_loss(int nblk, int T, int m, int dtype, const void* Y, const void* Yst
                void* workspace, size_t ws_bytes, void* stream) {
   ZO_CHECK(nblk >= 1 && T >= 1 && m >= 1, "sq_loss: nblk, T, m must be >= 1");
   ZO_CHECK(nblk <= 65535, "sq_loss: nblk = %d too large", nblk);
-  ZO_CHECK(dtype == ZO_F32 || dtype == ZO_BF16, "sq_loss: bad dtype %d", dtype);
+  ZO_CHECK(dtype == ZO_F32 || dtype == ZO_BF16 || dtype == ZO_F16, "sq_loss: bad dtype %d", dtype);
   ZO_CHECK(Y && Ystar && out, "sq_loss: NULL tensor argument");
   size_t need = 0;
   zo_sq_loss_launch(nblk, T, m, dtype, nullptr, nullptr, nullptr, nullptr, 0, nullptr, &need);

@@ -17,6 +17,12 @@
 //                      accumulators: hi*hi + hi*lo + lo*hi, so the correction
 //                      carries ~2^-16 relative error instead of the 2^-8 of
 //                      plain bf16 operands.
+// fp16 inputs: the same launches.  X W^T runs on the fp16 MFMA; the rank-r
+// segment keeps its bf16 hi/lo operands (eps U Z_j entries are near fp16's
+// smallest normal, and bf16 has fp32's range) on the bf16 MFMA, as more
+// k-tiles of the same pipeline.  The projection X_x Vt2^T runs on the fp16
+// MFMA with Vt2 the fp16 hi/lo split of 256 V (the low parts of entries near
+// 1/sqrt(n) then stay normal); k_pcombine multiplies by 1/256 (exact).
 // fp32 inputs: Vt (rp x n), P = X Vt^T and B_b in fp32, fp32 FMA throughout.
 //
 // bf16 GEMM: one workgroup computes a BM x BN tile of Y_b^T (BM output
@@ -30,6 +36,8 @@
 // concurrently are contiguous, then grouped 8 token tiles deep so the tiles
 // in flight on an XCD share their W and X panels in that XCD's L2.
 #include "zo_internal.h"
+
+#include <type_traits>
 
 namespace {
 
@@ -51,11 +59,44 @@ struct GemmArgs {
   int rc;                     // multiple of 16; 0 = no correction
   void* Y;                    // per block rows_b x ldy
   long long y_block_stride;
-  int ldy, out_bf16;
+  int ldy, out_dtype;          // zo_dtype of Y
   int tiles_a, tiles_b, total_tiles;
 };
 
-template <int WM, int WN, int TM, int TN>
+// Four fp32 accumulator values as element idx.. of an OUT-typed (zo_dtype) array.
+template <int OUT>
+__device__ __forceinline__ void store4(char* base, size_t idx, float v0, float v1, float v2,
+                                       float v3) {
+  if constexpr (OUT == ZO_BF16)
+    *(u32x2*)(base + idx * 2) = (u32x2){pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+  else if constexpr (OUT == ZO_F16)
+    *(u32x2*)(base + idx * 2) = (u32x2){pack_f16x2(v0, v1), pack_f16x2(v2, v3)};
+  else
+    *(f32x4*)(base + idx * 4) = (f32x4){v0, v1, v2, v3};
+}
+
+// The same with the output type chosen at run time (kernels with few accumulators).
+__device__ __forceinline__ void store4_rt(char* base, size_t idx, int out_dtype, float v0, float v1,
+                                          float v2, float v3) {
+  if (out_dtype == ZO_BF16)
+    store4<ZO_BF16>(base, idx, v0, v1, v2, v3);
+  else if (out_dtype == ZO_F16)
+    store4<ZO_F16>(base, idx, v0, v1, v2, v3);
+  else
+    store4<ZO_F32>(base, idx, v0, v1, v2, v3);
+}
+
+// 32x32x16 MFMA on 16-byte fragments of eight 16-bit values: fp16 or bf16.
+template <bool F16>
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+template <int WM, int WN, int TM, int TN, bool F16>
 __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
   constexpr int NT = WM * WN * 64;
   constexpr int BM = WM * TM * 32;
@@ -155,8 +196,7 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32<F16>(fa[i], fb[j], acc[i][j]);
     }
   };
 
@@ -173,7 +213,7 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
   }
 
   // Rank-rc correction: one more K segment with operands read straight from
-  // global memory (16 bytes per lane per fragment).
+  // global memory (16 bytes per lane per fragment); bf16 for every input type.
   if (a.rc > 0) {
     const bf16_t* __restrict__ Cg = a.ca + (long long)blk * a.ca_block_stride;
     const bf16_t* __restrict__ Dg = a.cb + (long long)blk * a.cb_block_stride;
@@ -202,7 +242,7 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
   }
 
   // Store: lane holds token fr (+32j) and 4 adjacent output columns per a.
-  char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (a.out_bf16 ? 2 : 4);
+  char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (a.out_dtype == ZO_F32 ? 4 : 2);
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int tok = t0 + wn * TN * 32 + j * 32 + fr;
@@ -213,15 +253,8 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
       for (int q4 = 0; q4 < 4; ++q4) {
         const int col = m0 + wm * TM * 32 + i * 32 + q4 * 8 + fh * 4;
         if (col >= a.rows_a) continue;
-        const float v0 = acc[i][j][q4 * 4 + 0], v1 = acc[i][j][q4 * 4 + 1];
-        const float v2 = acc[i][j][q4 * 4 + 2], v3 = acc[i][j][q4 * 4 + 3];
-        if (a.out_bf16) {
-          u32x2 pk = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-          *(u32x2*)(Yb + ((size_t)tok * a.ldy + col) * 2) = pk;
-        } else {
-          f32x4 pk = {v0, v1, v2, v3};
-          *(f32x4*)(Yb + ((size_t)tok * a.ldy + col) * 4) = pk;
-        }
+        store4_rt(Yb, (size_t)tok * a.ldy + col, a.out_dtype, acc[i][j][q4 * 4 + 0],
+                  acc[i][j][q4 * 4 + 1], acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
       }
     }
   }
@@ -305,31 +338,26 @@ __global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
   }
 }
 
-// Vt[a][k] = V[k][a] for a < r, 0 for r <= a < rp.  bf16: hi part in rows
-// [0, rp), low part (V - hi, rounded) in rows [rp, 2 rp).
+// Vt[a][k] = V[k][a] for a < r, 0 for r <= a < rp.  16-bit: hi part in rows
+// [0, rp), low part (V - hi, rounded) in rows [rp, 2 rp); fp16 splits 256 V.
 __global__ __launch_bounds__(256) void k_transpose_v(const float* __restrict__ V, int n, int r,
-                                                      int rp, void* Vt, int out_bf16) {
+                                                      int rp, void* Vt, int dtype) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long long)rp * n) return;
   const int a = (int)(idx / n), k = (int)(idx % n);
   const float v = a < r ? V[(size_t)k * r + a] : 0.f;
-  if (out_bf16) {
-    const bf16_t hi = f32_to_bf16(v);
-    ((bf16_t*)Vt)[idx] = hi;
-    ((bf16_t*)Vt)[(long long)rp * n + idx] = f32_to_bf16(v - bf16_to_f32(hi));
-  } else {
-    ((float*)Vt)[idx] = v;
-  }
+  put_split(Vt, idx, (long long)rp * n, v, dtype);
 }
 
-// P = P2[:, :rp] + P2[:, rp:] (fp32), written as [P_hi | P_hi | P_lo] (bf16, 3 rp wide).
+// P = (P2[:, :rp] + P2[:, rp:]) * unscale (fp32; unscale a power of two),
+// written as [P_hi | P_hi | P_lo] (bf16, 3 rp wide).
 __global__ __launch_bounds__(256) void k_pcombine(const float* __restrict__ P2, long long rows,
-                                                   int rp, bf16_t* __restrict__ Pc) {
+                                                   int rp, float unscale, bf16_t* __restrict__ Pc) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= rows * rp) return;
   const long long t = idx / rp;
   const int a = (int)(idx % rp);
-  const float p = P2[t * 2 * rp + a] + P2[t * 2 * rp + rp + a];
+  const float p = (P2[t * 2 * rp + a] + P2[t * 2 * rp + rp + a]) * unscale;
   const bf16_t hi = f32_to_bf16(p);
   const bf16_t lo = f32_to_bf16(p - bf16_to_f32(hi));
   bf16_t* o = Pc + t * 3 * rp;
@@ -445,7 +473,7 @@ __global__ __launch_bounds__(256) void k_bprime(const float* __restrict__ U,
   }
 }
 
-template <int WM, int WN, int TM, int TN>
+template <int WM, int WN, int TM, int TN, bool F16>
 int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
   constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
   a.tiles_a = (a.rows_a + BM - 1) / BM;
@@ -457,7 +485,7 @@ int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
     return ZO_ERR_UNSUPPORTED;
   }
   a.total_tiles = (int)total;
-  hipLaunchKernelGGL((k_gemm_bf16<WM, WN, TM, TN>), dim3(a.total_tiles), dim3(WM * WN * 64), 0,
+  hipLaunchKernelGGL((k_gemm_bf16<WM, WN, TM, TN, F16>), dim3(a.total_tiles), dim3(WM * WN * 64), 0,
                      stream, a);
   return zo_hip_status(hipGetLastError(), "k_gemm_bf16");
 }
@@ -487,9 +515,16 @@ int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
 // The rank-rc correction is rc/32 more k-tiles through the same pipeline,
 // with the A operand taken from ca (per block, rows_a x rc) and the B operand
 // from cb (per block, rows_b x rc).  Rows past rows_a / rows_b are loaded
-// from the last valid row (never stored).
+// from the last valid row (never stored).  F16: the main k-tiles run the fp16
+// MFMA and the correction k-tiles (bf16 hi/lo operands) the bf16 MFMA, as two
+// loops over the same body; the loads do not depend on the element type.
+// OUT (zo_dtype of Y) is a template parameter: with all 256 accumulators live,
+// one store path per instantiation keeps the epilogue free of per-store
+// branches (a run-time choice there made the compiler keep spilled VGPR
+// copies of the accumulators, one of which it stored wrongly).
 __device__ __forceinline__ int g4(int r) { return ((r >> 2) ^ (r & 2)) & 3; }
 
+template <bool F16, int OUT>
 __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   constexpr int STAGES = 4;
   constexpr int BM = 256, BN = 256, RB = 64;               // RB: bytes per LDS row (32 bf16)
@@ -563,12 +598,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-  auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+  auto mma = [&](const bf16x8* fa, const bf16x8* fb, auto f16) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32<decltype(f16)::value>(fa[i], fb[j], acc[i][j]);
   };
 
   // Prologue: tiles 0..3 issued in full; wait for tile 0.
@@ -584,10 +618,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   // has finished reading tile kt: each waits for its own reads before the barrier), its part 1
   // in the first half of iteration kt+1.  So at barrier(kt) the loads outstanding are, in issue
   // order, tile kt+1, kt+2, kt+3 (8 each): waiting down to 16 leaves tile kt+1 complete.
-  for (int kt = 0; kt < NTK; ++kt) {
+  auto body = [&](int kt, auto f16) {
     frags(kt, 1, f1a, f1b);
     if (kt >= 1) issue_part(min(kt + 3, NTK - 1), 1);
-    mma(f0a, f0b);
+    mma(f0a, f0b, f16);
     for (int i = 0; i < 4; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // 2 LDS reads
@@ -600,17 +634,24 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     asm volatile("" ::: "memory");                      // no memory access moves across
     issue_part(min(kt + 4, NTK - 1), 0);
     frags(kt + 1, 0, f0a, f0b);
-    mma(f1a, f1b);
+    mma(f1a, f1b, f16);
     for (int i = 0; i < 4; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 global->LDS load
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // 2 LDS reads
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 12, 0);
+  };
+  if constexpr (F16) {
+    int kt = 0;
+    for (; kt < NKM; ++kt) body(kt, std::true_type{});
+    for (; kt < NTK; ++kt) body(kt, std::false_type{});
+  } else {
+    for (int kt = 0; kt < NTK; ++kt) body(kt, std::false_type{});
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain the tail loads before exit
 
-  char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (a.out_bf16 ? 2 : 4);
+  char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (OUT == ZO_F32 ? 4 : 2);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int tok = t0 + wn * 128 + j * 32 + fr;
@@ -621,21 +662,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
       for (int q4 = 0; q4 < 4; ++q4) {
         const int col = m0 + wm * 128 + i * 32 + q4 * 8 + fh * 4;
         if (col >= a.rows_a) continue;
-        const float v0 = acc[i][j][q4 * 4 + 0], v1 = acc[i][j][q4 * 4 + 1];
-        const float v2 = acc[i][j][q4 * 4 + 2], v3 = acc[i][j][q4 * 4 + 3];
-        if (a.out_bf16) {
-          u32x2 pk = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-          *(u32x2*)(Yb + ((size_t)tok * a.ldy + col) * 2) = pk;
-        } else {
-          f32x4 pk = {v0, v1, v2, v3};
-          *(f32x4*)(Yb + ((size_t)tok * a.ldy + col) * 4) = pk;
-        }
+        store4<OUT>(Yb, (size_t)tok * a.ldy + col, acc[i][j][q4 * 4 + 0], acc[i][j][q4 * 4 + 1],
+                    acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
       }
     }
   }
 }
 
-int launch_gemm_main(GemmArgs a, hipStream_t stream) {
+int launch_gemm_main(GemmArgs a, bool f16, hipStream_t stream) {
   a.tiles_a = (a.rows_a + 255) / 256;
   a.tiles_b = (a.rows_b + 255) / 256;
   const long long total = (long long)a.tiles_a * a.tiles_b * a.nblk;
@@ -645,7 +679,17 @@ int launch_gemm_main(GemmArgs a, hipStream_t stream) {
     return ZO_ERR_UNSUPPORTED;
   }
   a.total_tiles = (int)total;
-  hipLaunchKernelGGL(k_gemm_main, dim3(a.total_tiles), dim3(256), 0, stream, a);
+  const dim3 grid(a.total_tiles), block(256);
+  if (a.out_dtype == ZO_F32) {
+    if (f16)
+      hipLaunchKernelGGL((k_gemm_main<true, ZO_F32>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((k_gemm_main<false, ZO_F32>), grid, block, 0, stream, a);
+  } else if (f16) {
+    hipLaunchKernelGGL((k_gemm_main<true, ZO_F16>), grid, block, 0, stream, a);
+  } else {
+    hipLaunchKernelGGL((k_gemm_main<false, ZO_BF16>), grid, block, 0, stream, a);
+  }
   return zo_hip_status(hipGetLastError(), "k_gemm_main");
 }
 
@@ -657,16 +701,17 @@ int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
   p->m = m;
   p->n = n;
   p->r = r;
-  // bf16: a multiple of 32 so the 3 rp-deep rank-r segment is whole 32-wide k-tiles.
-  p->rp = in_dtype == ZO_BF16 ? (r + 31) / 32 * 32 : (r + 15) / 16 * 16;
+  p->in16 = in_dtype != ZO_F32;
+  p->in_dtype = in_dtype;
+  p->out_dtype = out_dtype;
+  // 16-bit: a multiple of 32 so the 3 rp-deep rank-r segment is whole 32-wide k-tiles.
+  p->rp = p->in16 ? (r + 31) / 32 * 32 : (r + 15) / 16 * 16;
   p->q = q;
   p->nblk = nblk;
   p->x_block_stride = x_block_stride;
   p->nx = x_block_stride == 0 ? 1 : nblk;
-  p->in_bf16 = in_dtype == ZO_BF16;
-  p->out_bf16 = out_dtype == ZO_BF16;
   const size_t rows = (size_t)p->nx * T;
-  if (p->in_bf16) {
+  if (p->in16) {
     p->ws_vt = zo_align256((size_t)2 * p->rp * n * 2);       // Vt hi and lo, bf16
     p->ws_p2 = zo_align256(rows * 2 * p->rp * 4);            // X Vt2^T, fp32
     p->ws_p = zo_align256(rows * 3 * p->rp * 2);             // [P_hi | P_hi | P_lo]
@@ -705,7 +750,7 @@ int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t*
   {
     const long long total = (long long)p.rp * p.n;
     hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
-                       V, p.n, p.r, p.rp, w.vt, p.in_bf16);
+                       V, p.n, p.r, p.rp, w.vt, p.in_dtype);
     if ((st = zo_hip_status(hipGetLastError(), "k_transpose_v")) != ZO_OK) return st;
   }
   {
@@ -713,13 +758,13 @@ int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t*
     const dim3 grid((unsigned)((p.m + BP_ROWS - 1) / BP_ROWS), (unsigned)p.q);
     switch ((p.r + 31) / 32) {
       case 1: hipLaunchKernelGGL(k_bprime<1>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                 eps, tab, w.bp, p.in_bf16); break;
+                                 eps, tab, w.bp, p.in16); break;
       case 2: hipLaunchKernelGGL(k_bprime<2>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                 eps, tab, w.bp, p.in_bf16); break;
+                                 eps, tab, w.bp, p.in16); break;
       case 3: hipLaunchKernelGGL(k_bprime<3>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                 eps, tab, w.bp, p.in_bf16); break;
+                                 eps, tab, w.bp, p.in16); break;
       default: hipLaunchKernelGGL(k_bprime<4>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                  eps, tab, w.bp, p.in_bf16); break;
+                                  eps, tab, w.bp, p.in16); break;
     }
     if ((st = zo_hip_status(hipGetLastError(), "k_bprime")) != ZO_OK) return st;
   }
@@ -733,7 +778,7 @@ int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_
   void* pp = w.pp;
   int st;
   const long long xs = p.x_block_stride;
-  if (p.in_bf16) {
+  if (p.in16) {
     GemmArgs g{};
     g.A = (const bf16_t*)vt;
     g.B = (const bf16_t*)X;
@@ -746,11 +791,13 @@ int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_
     g.Y = p2;
     g.y_block_stride = (long long)p.T * 2 * p.rp;
     g.ldy = 2 * p.rp;
-    g.out_bf16 = 0;
-    if ((st = launch_gemm_bf16<1, 4, 2, 2>(g, stream)) != ZO_OK) return st;
+    g.out_dtype = ZO_F32;
+    const bool f16 = p.in_dtype == ZO_F16;
+    st = f16 ? launch_gemm_bf16<1, 4, 2, 2, true>(g, stream) : launch_gemm_bf16<1, 4, 2, 2, false>(g, stream);
+    if (st != ZO_OK) return st;
     const long long prow = (long long)p.nx * p.T;
     hipLaunchKernelGGL(k_pcombine, dim3((unsigned)((prow * p.rp + 255) / 256)), dim3(256), 0, stream,
-                       (const float*)p2, prow, p.rp, (bf16_t*)pp);
+                       (const float*)p2, prow, p.rp, f16 ? 1.f / ZO_F16_RSCALE : 1.f, (bf16_t*)pp);
     return zo_hip_status(hipGetLastError(), "k_pcombine");
   }
   F32Args g{};
@@ -775,7 +822,7 @@ int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y
   void* pp = w.pp;
   void* bp = w.bp;
   const long long xs = p.x_block_stride;
-  if (p.in_bf16) {
+  if (p.in16) {
     GemmArgs h{};
     h.A = (const bf16_t*)W;
     h.B = (const bf16_t*)X;
@@ -792,9 +839,10 @@ int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y
     h.Y = Y;
     h.y_block_stride = (long long)p.T * p.m;
     h.ldy = p.m;
-    h.out_bf16 = p.out_bf16;
-    if (p.n % 32 == 0) return launch_gemm_main(h, stream);
-    return launch_gemm_bf16<2, 4, 4, 2>(h, stream);
+    h.out_dtype = p.out_dtype;
+    const bool f16 = p.in_dtype == ZO_F16;
+    if (p.n % 32 == 0) return launch_gemm_main(h, f16, stream);
+    return f16 ? launch_gemm_bf16<2, 4, 4, 2, true>(h, stream) : launch_gemm_bf16<2, 4, 4, 2, false>(h, stream);
   }
   F32Args h{};
   h.A = (const float*)W;

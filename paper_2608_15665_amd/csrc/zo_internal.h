@@ -9,6 +9,7 @@
 
 typedef uint16_t bf16_t;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -50,12 +51,49 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
+// IEEE binary16: conversion from fp32 rounds to nearest even (v_cvt_f16_f32
+// under the default mode), overflowing to infinity.
+__device__ __forceinline__ float f16_to_f32(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+__device__ __forceinline__ uint16_t f32_to_f16(float f) {
+  return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  return (uint32_t)f32_to_f16(lo) | ((uint32_t)f32_to_f16(hi) << 16);
+}
+
+// fp16 inputs: the projection's right factor (V, or LoRA's [A ; V_A^T]) is
+// split into fp16 hi + lo after scaling by this power of two, so that the low
+// parts of entries near 1/sqrt(n) stay normal numbers; the projection undoes
+// it exactly.  Entries must stay below 65504 / 256 in magnitude.
+constexpr float ZO_F16_RSCALE = 256.f;
+
+// Element idx of the projection's right factor: fp32 as is; 16-bit as a hi
+// part at idx and the rounded remainder at lo_off + idx (fp16: of 256 v).
+__device__ __forceinline__ void put_split(void* Vt, long long idx, long long lo_off, float v,
+                                          int dtype) {
+  if (dtype == ZO_BF16) {
+    const bf16_t hi = f32_to_bf16(v);
+    ((bf16_t*)Vt)[idx] = hi;
+    ((bf16_t*)Vt)[lo_off + idx] = f32_to_bf16(v - bf16_to_f32(hi));
+  } else if (dtype == ZO_F16) {
+    const float x = v * ZO_F16_RSCALE;
+    const uint16_t hi = f32_to_f16(x);
+    ((uint16_t*)Vt)[idx] = hi;
+    ((uint16_t*)Vt)[lo_off + idx] = f32_to_f16(x - f16_to_f32(hi));
+  } else {
+    ((float*)Vt)[idx] = v;
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 // Perturbed linear (zo_gemm.hip).
 struct PlinearPlan {
   int T, m, n, r, rp, q, nblk, nx;  // nx: number of distinct X blocks (1 or nblk)
   long long x_block_stride;
-  int in_bf16, out_bf16;
+  int in16;                 // 16-bit inputs (bf16 or fp16): MFMA path
+  int in_dtype, out_dtype;  // zo_dtype values
   size_t ws_vt, ws_p2, ws_p, ws_bp;  // bytes of each workspace region
   size_t ws_total;
 };

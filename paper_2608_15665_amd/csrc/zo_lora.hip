@@ -16,10 +16,11 @@
 namespace {
 
 // Vt rows a < rl: A[a][:]; rows rl <= a < rl + rs: V_A[:][a - rl]; zero up to rp.
-// bf16: hi part in rows [0, rp), low part (x - hi, rounded) in rows [rp, 2 rp).
+// 16-bit: hi part in rows [0, rp), low part (x - hi, rounded) in rows [rp, 2 rp);
+// fp16 splits 256 x (the projection scales back exactly).
 __global__ __launch_bounds__(256) void k_lora_vt(const float* __restrict__ A,
                                                  const float* __restrict__ VA, int n, int rl,
-                                                 int rs, int rp, void* Vt, int out_bf16) {
+                                                 int rs, int rp, void* Vt, int dtype) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long long)rp * n) return;
   const int a = (int)(idx / n), k = (int)(idx % n);
@@ -28,13 +29,7 @@ __global__ __launch_bounds__(256) void k_lora_vt(const float* __restrict__ A,
     v = A[(size_t)a * n + k];
   else if (a < rl + rs)
     v = VA[(size_t)k * rs + (a - rl)];
-  if (out_bf16) {
-    const bf16_t hi = f32_to_bf16(v);
-    ((bf16_t*)Vt)[idx] = hi;
-    ((bf16_t*)Vt)[(long long)rp * n + idx] = f32_to_bf16(v - bf16_to_f32(hi));
-  } else {
-    ((float*)Vt)[idx] = v;
-  }
+  put_split(Vt, idx, (long long)rp * n, v, dtype);
 }
 
 // B'[i][c] = B[i][c] + s eps sum_e U_B[i][e] sum_f Z_B[e][f] V_B[c][f].
@@ -106,7 +101,7 @@ int zo_lora_prepare(const PlinearPlan& p, int rl, int rs, const int* blk_query,
   {
     const long long total = (long long)p.rp * p.n;
     hipLaunchKernelGGL(k_lora_vt, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, A,
-                       VA, p.n, rl, rs, p.rp, w.vt, p.in_bf16);
+                       VA, p.n, rl, rs, p.rp, w.vt, p.in_dtype);
     if ((st = zo_hip_status(hipGetLastError(), "k_lora_vt")) != ZO_OK) return st;
   }
   {
@@ -114,7 +109,7 @@ int zo_lora_prepare(const PlinearPlan& p, int rl, int rs, const int* blk_query,
     const long long total = (long long)p.nblk * p.m * p.rp;
     hipLaunchKernelGGL(k_lora_bprime, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
                        B, UB, VB, ZB, UA, ZA, p.m, rl, rs, p.rp, p.nblk, eps, scale, tab, w.bp,
-                       p.in_bf16);
+                       p.in16);
     if ((st = zo_hip_status(hipGetLastError(), "k_lora_bprime")) != ZO_OK) return st;
   }
   return zo_plinear_project(p, X, ws, stream);

@@ -7,7 +7,7 @@ namespace {
 
 constexpr int LOSS_CHUNK = 65536;  // elements per workgroup
 
-__global__ __launch_bounds__(256) void k_sq_partial(const void* Y, const void* Ystar, int bf16,
+__global__ __launch_bounds__(256) void k_sq_partial(const void* Y, const void* Ystar, int dtype,
                                                     long long per_block, int nchunk,
                                                     double* partial) {
   __shared__ double red[4];
@@ -15,11 +15,18 @@ __global__ __launch_bounds__(256) void k_sq_partial(const void* Y, const void* Y
   const long long lo = (long long)c * LOSS_CHUNK;
   const long long hi = min(lo + (long long)LOSS_CHUNK, per_block);
   double s = 0.0;
-  if (bf16) {
+  if (dtype == ZO_BF16) {
     const bf16_t* y = (const bf16_t*)Y + (long long)b * per_block;
     const bf16_t* ys = (const bf16_t*)Ystar;
     for (long long e = lo + threadIdx.x; e < hi; e += 256) {
       const double d = (double)bf16_to_f32(y[e]) - (double)bf16_to_f32(ys[e]);
+      s += d * d;
+    }
+  } else if (dtype == ZO_F16) {
+    const uint16_t* y = (const uint16_t*)Y + (long long)b * per_block;
+    const uint16_t* ys = (const uint16_t*)Ystar;
+    for (long long e = lo + threadIdx.x; e < hi; e += 256) {
+      const double d = (double)f16_to_f32(y[e]) - (double)f16_to_f32(ys[e]);
       s += d * d;
     }
   } else {
@@ -71,7 +78,7 @@ int zo_sq_loss_launch(int nblk, int T, int m, int dtype, const void* Y, const vo
   }
   double* partial = (double*)ws;
   hipLaunchKernelGGL(k_sq_partial, dim3(nchunk, nblk), dim3(256), 0, stream, Y, Ystar,
-                     dtype == ZO_BF16, per, nchunk, partial);
+                     dtype, per, nchunk, partial);
   int st = zo_hip_status(hipGetLastError(), "k_sq_partial");
   if (st != ZO_OK) return st;
   hipLaunchKernelGGL(k_sq_final, dim3((nblk + 63) / 64), dim3(64), 0, stream, partial, nchunk,

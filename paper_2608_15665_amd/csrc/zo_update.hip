@@ -11,12 +11,15 @@
 //   k_us        Reads the item's flags: if any entry was non-finite the item is
 //               skipped (state untouched).  Otherwise commits the new moments and
 //               forms L = lr U S (m x rp; tiles of 128 rows, register-blocked fp32
-//               FMA) and, for bf16 W, the hi/lo split of V (n x rp); padding
-//               columns are zero.  bf16 W: L and V as hi + lo bf16 pairs (x = hi + lo
-//               to about 16 significant bits); fp32 W: L in fp32, V read as is.
+//               FMA) and, for 16-bit W, the hi/lo split of V (n x rp); padding
+//               columns are zero.  16-bit W: L and V as hi + lo bf16 pairs (x = hi +
+//               lo to about 16 significant bits, with fp32's range); fp32 W: L in
+//               fp32, V read as is.
 //   k_update_*  W <- W - L V^T in place.
 //
-// bf16 W (k_update_bf16): memory bound -- 4 bytes of HBM traffic per weight
+// bf16 or fp16 W (k_update_bf16, the W type a template parameter: it changes
+// only the conversion of W to fp32 and the rounding of the result back, both
+// to nearest even): memory bound -- 4 bytes of HBM traffic per weight
 // against 2 r MACs.  At r = 64 that is 32 FLOP/B, above the fp32 VALU ridge
 // of the chip, so the rank-r product runs on v_mfma_f32_16x16x32_bf16 as
 // hi*hi + lo*hi + hi*lo (3 MFMAs per 32-deep K step).  Each wave owns a strip
@@ -265,7 +268,7 @@ __device__ __forceinline__ void bstore2(__amdgpu_buffer_rsrc_t r, unsigned off, 
 // whole cache lines.  The prologue issues range-dropped stores in place of each
 // step's stores so that the count of memory operations between a load and its
 // use is the same on entry as in the steady state.
-template <int RPK, bool HOOK>
+template <int RPK, bool HOOK, bool WF16>
 __global__ __launch_bounds__(256) void k_update_bf16(UpdArgs a) {
   constexpr int RP = 32 * RPK;
   constexpr int NS = RPK == 1 ? 4 : 2;  // W prefetch depth in 16-row steps
@@ -389,11 +392,20 @@ __global__ __launch_bounds__(256) void k_update_bf16(UpdArgs a) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const uint32_t w0 = wb[s][v][0], w1 = wb[s][v][1];
-        const float n0 = __uint_as_float(w0 << 16) - acc[0][v];
-        const float n1 = __uint_as_float(w0 & 0xffff0000u) - acc[1][v];
-        const float n2 = __uint_as_float(w1 << 16) - acc[2][v];
-        const float n3 = __uint_as_float(w1 & 0xffff0000u) - acc[3][v];
-        bstore2(rw, wo[v] + d, (u32x2){pack_bf16x2(n0, n1), pack_bf16x2(n2, n3)});
+        float n0, n1, n2, n3;
+        if constexpr (WF16) {
+          n0 = f16_to_f32((uint16_t)w0) - acc[0][v];
+          n1 = f16_to_f32((uint16_t)(w0 >> 16)) - acc[1][v];
+          n2 = f16_to_f32((uint16_t)w1) - acc[2][v];
+          n3 = f16_to_f32((uint16_t)(w1 >> 16)) - acc[3][v];
+          bstore2(rw, wo[v] + d, (u32x2){pack_f16x2(n0, n1), pack_f16x2(n2, n3)});
+        } else {
+          n0 = __uint_as_float(w0 << 16) - acc[0][v];
+          n1 = __uint_as_float(w0 & 0xffff0000u) - acc[1][v];
+          n2 = __uint_as_float(w1 << 16) - acc[2][v];
+          n3 = __uint_as_float(w1 & 0xffff0000u) - acc[3][v];
+          bstore2(rw, wo[v] + d, (u32x2){pack_bf16x2(n0, n1), pack_bf16x2(n2, n3)});
+        }
         if (HOOK) bstore(ro, ho[v] + 2 * d, __builtin_bit_cast(u32x4, (f32x4){n0, n1, n2, n3}));
       }
       const unsigned dn = (unsigned)((c + 1) * NS + s) * stepw;
@@ -437,12 +449,20 @@ Layout item_layout(int m, int n, int r, int rp, int bf16, int aw) {
   return l;
 }
 
-template <int RPK>
-void launch_update_bf16(bool hook, int wg, hipStream_t stream, const UpdArgs& pa) {
+template <int RPK, bool WF16>
+void launch_update_w16(bool hook, int wg, hipStream_t stream, const UpdArgs& pa) {
   if (hook)
-    hipLaunchKernelGGL((k_update_bf16<RPK, true>), dim3(wg), dim3(256), 0, stream, pa);
+    hipLaunchKernelGGL((k_update_bf16<RPK, true, WF16>), dim3(wg), dim3(256), 0, stream, pa);
   else
-    hipLaunchKernelGGL((k_update_bf16<RPK, false>), dim3(wg), dim3(256), 0, stream, pa);
+    hipLaunchKernelGGL((k_update_bf16<RPK, false, WF16>), dim3(wg), dim3(256), 0, stream, pa);
+}
+
+template <int RPK>
+void launch_update_bf16(bool hook, bool wf16, int wg, hipStream_t stream, const UpdArgs& pa) {
+  if (wf16)
+    launch_update_w16<RPK, true>(hook, wg, stream, pa);
+  else
+    launch_update_w16<RPK, false>(hook, wg, stream, pa);
 }
 
 }  // namespace
@@ -451,7 +471,9 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
                      const float* g, int t, float lr, float beta1, float beta2, float eps_adam,
                      int sgd, int* nonfinite_flag, void* ws, size_t ws_bytes, hipStream_t stream,
                      size_t* ws_needed) {
-  const int bf16 = w_dtype == ZO_BF16;
+  // 16-bit W (bf16 or fp16) takes the MFMA path: L and V as hi+lo bf16 pairs.
+  const int bf16 = w_dtype != ZO_F32;
+  const bool wf16 = w_dtype == ZO_F16;
   const int rp = bf16 ? (r + 31) / 32 * 32 : r;
   const int aw = (r * r + 255) / 256;
   size_t need = 0;
@@ -543,10 +565,10 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
         hipLaunchKernelGGL(k_update_f32, dim3(wg_total), dim3(256), 0, stream, pa);
       } else {
         switch (rp / 32) {
-          case 1: launch_update_bf16<1>(hook, wg_total, stream, pa); break;
-          case 2: launch_update_bf16<2>(hook, wg_total, stream, pa); break;
-          case 3: launch_update_bf16<3>(hook, wg_total, stream, pa); break;
-          default: launch_update_bf16<4>(hook, wg_total, stream, pa); break;
+          case 1: launch_update_bf16<1>(hook, wf16, wg_total, stream, pa); break;
+          case 2: launch_update_bf16<2>(hook, wf16, wg_total, stream, pa); break;
+          case 3: launch_update_bf16<3>(hook, wf16, wg_total, stream, pa); break;
+          default: launch_update_bf16<4>(hook, wf16, wg_total, stream, pa); break;
         }
       }
       if ((st = zo_hip_status(hipGetLastError(), "k_update")) != ZO_OK) return st;

@@ -37,6 +37,11 @@ def dev_bf16(bits):
     return torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16)).view(torch.bfloat16).cuda()
 
 
+def dev_f16(h):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(h, dtype=np.float16)).cuda()
+
+
 def host_bf16_values(t):
     """float64 values of a bf16 device tensor."""
     import torch

@@ -58,6 +58,9 @@ def test_status_strings():
     (dict(blk_query=[0, 5]), "blk_query[1]"),
     (dict(blk_sign=[1, 2]), "blk_sign[1]"),
     (dict(in_dtype=7), "in_dtype"),
+    (dict(in_dtype=3), "in_dtype"),
+    (dict(in_dtype=2, m=12), "m % 8"),      # fp16 shares the 16-bit limits
+    (dict(in_dtype=2, xs=1028), "x_block_stride"),
 ])
 def test_perturbed_linear_validation(args, needle):
     p = dict(T=16, m=32, n=64, r=4, q=2, nblk=2, blk_query=[0, 1], blk_sign=[1, -1], xs=0, in_dtype=1)
@@ -90,6 +93,13 @@ def test_perturbed_linear_rejects_small_workspace_and_nulls():
     st = L.zo_perturbed_linear(16, 32, 64, 4, 1, 2, bq, bs, 1e-3, 0, fake, 0, fake, fake, fake, fake, 1,
                                fake, fake, need, None)
     assert st == 2
+    # The output is the input type or fp32: fp16 in with bf16 out, bf16 in with fp16 out are not.
+    need16 = L.zo_perturbed_linear_workspace(16, 32, 64, 4, 1, 2, 0, 2)
+    assert need16 == need  # fp16 takes the same workspace layout as bf16
+    for in_dt, out_dt in ((2, 1), (1, 2)):
+        st = L.zo_perturbed_linear(16, 32, 64, 4, 1, 2, bq, bs, 1e-3, in_dt, fake, 0, fake, fake, fake, fake,
+                                   out_dt, fake, fake, need, None)
+        assert st == 2 and "out_dtype" in _detail()
 
 
 def test_lora_validation_and_workspace():
@@ -151,6 +161,14 @@ def test_update_validation():
     assert "n <=" in _detail()
     need = L.zo_subspace_adam_update_workspace(1, arr2, 4, 2, 1)
     assert need > 0
+    # fp16 W: the same limits and workspace as bf16; other dtypes rejected.
+    assert L.zo_subspace_adam_update_workspace(1, arr2, 4, 2, 2) == need
+    assert L.zo_subspace_adam_update(1, arr, 2, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, fake,
+                                     1 << 30, None) == 1
+    assert "n % 8" in _detail()
+    assert L.zo_subspace_adam_update(1, arr2, 3, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, fake,
+                                     1 << 30, None) == 1
+    assert "w_dtype" in _detail()
     assert L.zo_subspace_adam_update(1, arr2, 1, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, fake,
                                      need - 1, None) == 6
 
@@ -176,5 +194,7 @@ def test_loss_validation():
     L = zo.lib()
     fake = 1 << 20
     assert L.zo_sq_loss(0, 4, 4, 0, fake, fake, fake, fake, 1 << 20, None) == 1
+    assert L.zo_sq_loss(2, 4, 4, 3, fake, fake, fake, fake, 1 << 20, None) == 1
+    assert "dtype" in _detail()
     assert L.zo_combine_central(2, fake, 0.0, fake, None) == 1
     assert L.zo_sq_loss_workspace(2, 64, 256) > 0

@@ -17,17 +17,22 @@ import torch
 import oracle
 import paper_2608_15665_amd as zo
 import zo_draws as zd
-from _common import dev_bf16, dev_f32, ferr, host, normwise, orth
+from _common import dev_bf16, dev_f16, dev_f32, ferr, host, normwise, orth
 
 pytestmark = pytest.mark.gpu
 
 SCALE = zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
 
 
-def make_case(T, m, n, rl, r, q, nblk, shared_x, bf16, zero_b=False, seed=0, same_x_pairs=False):
+def make_case(T, m, n, rl, r, q, nblk, shared_x, bf16, zero_b=False, seed=0, same_x_pairs=False, f16=False):
+    """The frozen base W and X are bf16 (bf16=True), fp16 (f16=True) or fp32."""
     W64 = zd.draw(seed, "W0", (m, n), (m, n), 0.02)
     X0 = zd.draw(seed, "X", (T, n, 0), (T, n))
-    if bf16:
+    if f16:
+        Wh, Wv = zd.as_f16_values(W64)
+        X0h, X0v = zd.as_f16_values(X0)
+        Wd, X0d = dev_f16(Wh), dev_f16(X0h)
+    elif bf16:
         Wb, Wv = zd.as_bf16_values(W64)
         X0b, X0v = zd.as_bf16_values(X0)
         Wd, X0d = dev_bf16(Wb), dev_bf16(X0b)
@@ -118,6 +123,24 @@ def test_bf16_parity(T, m, n, rl, r, q, nblk, shared, zero_b, out):
             assert ferr(Y[b], ref[b], 1.0) <= 1e-4, b
 
 
+@pytest.mark.parametrize("T,m,n,rl,r,q,nblk,shared,zero_b", [
+    (300, 264, 200, 8, 4, 2, 4, False, False),   # ragged tails (generic tile kernel)
+    (256, 1024, 512, 8, 4, 4, 8, False, True),   # v-projection-like m, B = 0 (main kernel)
+    (96, 520, 136, 16, 8, 3, 6, True, False),    # wider adapter, shared X
+])
+@pytest.mark.parametrize("out", ["f16", "f32"])
+def test_f16_parity(T, m, n, rl, r, q, nblk, shared, zero_b, out):
+    """fp16 frozen base (the paper's precision for its LoRA runs)."""
+    c = make_case(T, m, n, rl, r, q, nblk, shared, bf16=False, zero_b=zero_b, f16=True)
+    Y = run_gpu(c, 1e-3, out_dtype=torch.float16 if out == "f16" else torch.float32)
+    ref = run_oracle(c, 1e-3)
+    for b in range(nblk):
+        assert ferr(Y[b], ref[b], 1e-3) <= 1e-2, b
+        assert normwise(Y[b], ref[b]) <= 2e-3, b
+        if out == "f32":
+            assert ferr(Y[b], ref[b], 1.0) <= 1e-4, b
+
+
 def test_bf16_eps_one_adapter_visible():
     """At eps = 1 with a non-zero B the adapter branch and both perturbations are large enough
     to be checked through bf16 outputs."""
@@ -132,12 +155,14 @@ def test_bf16_eps_one_adapter_visible():
 
 
 @pytest.mark.parametrize("zero_b", [True, False])
-def test_adapter_channel_fp32_out(zero_b):
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_adapter_channel_fp32_out(zero_b, dt):
     """X_{2j} = X_{2j+1}: (Y+ - Y-)/(2 eps) is the odd part of the branch,
     scale X [(U_A Z_A V_A^T)^T B^T + A^T (U_B Z_B V_B^T)^T], which a kernel that dropped or
-    mis-signed either perturbation would fail (it is below bf16 resolution of Y)."""
+    mis-signed either perturbation would fail (it is below 16-bit resolution of Y)."""
     T, m, n, rl, r, q = 256, 256, 512, 8, 4, 3
-    c = make_case(T, m, n, rl, r, q, 2 * q, False, bf16=True, zero_b=zero_b, same_x_pairs=True)
+    c = make_case(T, m, n, rl, r, q, 2 * q, False, bf16=dt == "bf16", zero_b=zero_b, same_x_pairs=True,
+                  f16=dt == "f16")
     eps = 1e-3
     Y = run_gpu(c, eps, out_dtype=torch.float32)
     h = c["h"]
@@ -151,9 +176,10 @@ def test_adapter_channel_fp32_out(zero_b):
         assert ferr(d, odd, 1e-1) <= 5e-2, j
 
 
-def test_frozen_tensors_bitwise_unchanged():
-    c = make_case(128, 256, 256, 8, 4, 4, 8, False, bf16=True)
-    hs = lambda t: hashlib.sha256(t.contiguous().view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32)
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_frozen_tensors_bitwise_unchanged(dt):
+    c = make_case(128, 256, 256, 8, 4, 4, 8, False, bf16=dt == "bf16", f16=dt == "f16")
+    hs = lambda t: hashlib.sha256(t.contiguous().view(torch.int16 if t.element_size() == 2 else torch.int32)
                                   .cpu().numpy().tobytes()).hexdigest()
     before = [hs(c["Wd"]), hs(c["d"]["A"]), hs(c["d"]["B"])]
     for _ in range(3):
@@ -161,9 +187,9 @@ def test_frozen_tensors_bitwise_unchanged():
     assert before == [hs(c["Wd"]), hs(c["d"]["A"]), hs(c["d"]["B"])]
 
 
-@pytest.mark.parametrize("bf16", [True, False])
-def test_prepare_apply_equals_one_call(bf16):
-    c = make_case(300, 264, 200, 8, 4, 2, 4, False, bf16=bf16)
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
+def test_prepare_apply_equals_one_call(dt):
+    c = make_case(300, 264, 200, 8, 4, 2, 4, False, bf16=dt == "bf16", f16=dt == "f16")
     one = run_gpu(c, 1e-3)
     pl = layer(c, 1e-3)
     pl.prepare()

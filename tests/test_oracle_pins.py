@@ -523,6 +523,30 @@ def test_round_bf16_matches_torch_on_fp32_inputs():
     np.testing.assert_array_equal(oracle.round_bf16(x32.astype(np.float64)), ref)
 
 
+def test_round_f16_hand_cases(golden_dir):
+    cases = json.load(open(os.path.join(golden_dir, "f16_rounding.json")))["cases"]
+    for c in cases:
+        got = oracle.round_f16(c["x_value"])
+        assert got == float(c["f16"]), c["x"]
+        assert np.signbit(got) == np.signbit(float(c["f16"])) or float(c["f16"]) == 0.0, c["x"]
+
+
+def test_round_f16_matches_library_casts():
+    """One rounding float64 -> binary16 is numpy's float16 cast, over normal, subnormal and
+    overflowing magnitudes; on float32-representable inputs it is also torch's float32 ->
+    float16 cast (torch's float64 -> float16 goes through float32, a double rounding)."""
+    torch = pytest.importorskip("torch")
+    x = RNG.standard_normal(200000) * 10.0 ** RNG.uniform(-9, 5.2, 200000)
+    with np.errstate(over="ignore"):
+        ref_np = x.astype(np.float16).astype(np.float64)
+    got = oracle.round_f16(x)
+    np.testing.assert_array_equal(got, ref_np)
+    assert np.isinf(got).any() and (np.abs(got[np.isfinite(got)]) < 2.0 ** -14).any()
+    x32 = x.astype(np.float32)
+    ref_t = torch.from_numpy(x32).to(torch.float16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(oracle.round_f16(x32.astype(np.float64)), ref_t)
+
+
 def test_fp32_in_place_restore_is_not_exact():
     """Alg. 2 adds then subtracts eps U Z V^T in place; in float32 that does not give W back
     bit for bit (why the GPU path never writes W during the queries)."""

@@ -111,6 +111,13 @@ def as_bf16_values(a64: np.ndarray):
     return bits, bf16_to_f32(bits).astype(np.float64)
 
 
+def as_f16_values(a64: np.ndarray):
+    """Cast a float64 draw to IEEE binary16 via float32 (both steps round to nearest even):
+    returns (float16 array, exact float64 values of it)."""
+    h = f32(a64).astype(np.float16)
+    return h, h.astype(np.float64)
+
+
 def sha256(a: np.ndarray) -> str:
     return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
 
