@@ -39,6 +39,7 @@ namespace {
 constexpr int ITEMS_PER_LAUNCH = 16;
 constexpr int UPD_ROWS = 512;  // rows per workgroup
 constexpr int UPD_COLS = 256;  // columns per workgroup (4 waves x 64)
+constexpr int UPD_GROUP = 4;   // row chunks per raster group
 constexpr int US_ROWS = 128;   // rows of L per k_us workgroup
 constexpr unsigned OOB = 0x80000000u;  // buffer offset beyond every descriptor used here
 constexpr int RSRC_CFG = 0x00020000;   // buffer descriptor word 3: 32-bit raw access
@@ -233,11 +234,12 @@ struct ItemUpd {
   const void* Vs;  // bf16 path: split V; fp32 path: V itself (n x r)
   const int* skip;
   int m, n;
-  int strips, wg_begin;
+  int strips, rchunks, wg_begin;  // bf16 path: 256-column strips x 512-row chunks
 };
 struct UpdArgs {
   ItemUpd it[ITEMS_PER_LAUNCH];
   int count, r, rp;
+  int total_wg;
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, unsigned bytes) {
@@ -278,13 +280,26 @@ __global__ __launch_bounds__(256) void k_update_bf16(UpdArgs a) {
   constexpr int NL = CH * V16 / 256;    // L pieces per thread per chunk
   static_assert(NL * 256 == CH * V16, "L chunk must split evenly over 256 threads");
   __shared__ __attribute__((aligned(16))) char Ls[CH * LROW];
+  // The hardware deals workgroup w to XCD w % 8.  Each XCD gets a contiguous
+  // range of tiles, rastered in groups of UPD_GROUP row chunks: within a group
+  // the row chunk runs fastest, then the strip.  The ~32 workgroups an XCD runs
+  // at once then cover about 4 row chunks x 8 strips, so each chunk's L rows
+  // (128 KB at r = 64) and each strip's V fragments (64 KB) come from its L2
+  // after the first read, instead of once per workgroup.
+  const int w = blockIdx.x, nt = a.total_wg;
+  const int xcd = w & 7, widx = w >> 3;
+  const int lt = xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
   int k = 0;
-  while (k + 1 < a.count && (int)blockIdx.x >= a.it[k + 1].wg_begin) ++k;
+  while (k + 1 < a.count && lt >= a.it[k + 1].wg_begin) ++k;
   const ItemUpd& it = a.it[k];
   if (*it.skip) return;
-  const int local = blockIdx.x - it.wg_begin;
-  const int strip = local % it.strips;
-  const int rchunk = local / it.strips;
+  const int local = lt - it.wg_begin;
+  const int per_group = UPD_GROUP * it.strips;
+  const int grp = local / per_group;
+  const int gsize = min(UPD_GROUP, it.rchunks - grp * UPD_GROUP);
+  const int rem = local - grp * per_group;
+  const int rchunk = grp * UPD_GROUP + rem % gsize;
+  const int strip = rem / gsize;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -543,9 +558,10 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
       u.wg_begin = wg_total;
       if (bf16) {
         u.strips = (src.n + UPD_COLS - 1) / UPD_COLS;
-        wg_total += u.strips * ((src.m + UPD_ROWS - 1) / UPD_ROWS);
+        u.rchunks = (src.m + UPD_ROWS - 1) / UPD_ROWS;
+        wg_total += u.strips * u.rchunks;
       } else {
-        u.strips = 1;
+        u.strips = u.rchunks = 1;
         wg_total += (int)(((long long)src.m * src.n + 255) / 256);
       }
       hook = hook || src.w_f32_out;
@@ -560,6 +576,7 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
       default: hipLaunchKernelGGL(k_us<4>, dim3(us_wg), dim3(256), 0, stream, ua); break;
     }
     if ((st = zo_hip_status(hipGetLastError(), "k_us")) != ZO_OK) return st;
+    pa.total_wg = wg_total;
     if (wg_total > 0) {
       if (!bf16) {
         hipLaunchKernelGGL(k_update_f32, dim3(wg_total), dim3(256), 0, stream, pa);
