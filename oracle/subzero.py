@@ -17,6 +17,7 @@ __all__ = [
     "householder_qr", "haar_qr", "raw_qr_first_column",
     "perturbation", "perturbed_weight", "perturbed_linear", "perturbed_linear_blocks",
     "lora_perturbed_factors", "lora_perturbed_linear", "lora_perturbed_linear_blocks",
+    "layer_norm", "causal_attention", "DECODER_MATS", "decoder_layer",
     "sq_loss", "central_estimate", "forward_estimate", "aggregate",
     "adam_direction", "subspace_adam_update", "subspace_sgd_update", "round_bf16", "round_f16", "tiny_run",
 ]
@@ -169,6 +170,67 @@ def lora_perturbed_linear_blocks(Xb, W, A, UA, VA, ZAs, B, UB, VB, ZBs, blk_quer
         out.append(lora_perturbed_linear(Xr, W, A, UA, VA, ZAs[j], B, UB, VB, ZBs[j],
                                          float(blk_sign[b]), eps, scale))
     return out
+
+
+# ---------------------------------------------------------------------------
+# The network whose loss each query evaluates (Eq. 5; Alg. 3 query loop): a
+# pre-LN decoder layer of the OPT family with every weight matrix perturbed
+# ---------------------------------------------------------------------------
+def layer_norm(X, gamma, beta, eps_ln=1e-5):
+    """Row-wise layer normalisation (x - mean) / sqrt(var + eps_ln) * gamma + beta, with the
+    population variance of each row (the normalisation inside the OPT decoder layers the
+    paper fine-tunes).  READING: eps_ln = 1e-5."""
+    X = np.asarray(X, np.float64)
+    mu = X.mean(axis=1, keepdims=True)
+    var = ((X - mu) ** 2).mean(axis=1, keepdims=True)
+    return (X - mu) / np.sqrt(var + eps_ln) * np.asarray(gamma, np.float64) + np.asarray(beta, np.float64)
+
+
+def causal_attention(Q, K, V, heads, seq_len):
+    """Multi-head causal self-attention of one block of T token rows holding T / seq_len
+    sequences one after another: for each sequence and head h (columns h dh .. (h+1) dh - 1,
+    dh = d / heads), query t attends to keys t' <= t of its own sequence with weights
+    softmax_t'(q_t . k_t' / sqrt(dh)) and returns the weighted sum of the v_t'."""
+    Q, K, V = (np.asarray(a, np.float64) for a in (Q, K, V))
+    T, d = Q.shape
+    dh = d // heads
+    O = np.zeros_like(Q)
+    future = np.triu(np.ones((seq_len, seq_len), dtype=bool), 1)
+    for s0 in range(0, T, seq_len):
+        rows = slice(s0, s0 + seq_len)
+        for h in range(heads):
+            c = slice(h * dh, (h + 1) * dh)
+            S = Q[rows, c] @ K[rows, c].T / math.sqrt(dh)
+            S[future] = -np.inf
+            S = S - S.max(axis=1, keepdims=True)
+            P = np.exp(S)
+            P = P / P.sum(axis=1, keepdims=True)
+            O[rows, c] = P @ V[rows, c]
+    return O
+
+
+DECODER_MATS = ("q", "k", "v", "o", "fc1", "fc2")
+
+
+def decoder_layer(H, layer, sign, eps, j, heads, seq_len, store=None, eps_ln=1e-5):
+    """One pre-LN decoder layer under query j with sign s: each of its six weight matrices W
+    (q, k, v, o, fc1, fc2; each with its own U, V and coefficients Z_j) enters as
+    W + s eps U Z_j V^T (Eq. 4), and
+        A = LN1(H);   Q, K, V = A Wq'^T, A Wk'^T, A Wv'^T;   C = attention(Q, K, V)
+        H2 = H + C Wo'^T;   F = relu(LN2(H2) W1'^T);   H3 = H2 + F W2'^T.
+    ``store`` (optional) rounds each tensor the layer writes to memory, at the points where
+    a device path stores one (e.g. round_bf16); all arithmetic is float64.
+    READING: no biases (the perturbed parameters are the weight matrices); ReLU, as in OPT."""
+    st = store if store is not None else (lambda x: x)
+    lin = lambda X, name: perturbed_linear(X, layer[name]["W"], layer[name]["U"], layer[name]["V"],
+                                           layer[name]["Z"][j], sign, eps)
+    A = st(layer_norm(H, layer["ln1_g"], layer["ln1_b"], eps_ln))
+    Q, K, Vv = st(lin(A, "q")), st(lin(A, "k")), st(lin(A, "v"))
+    C = st(causal_attention(Q, K, Vv, heads, seq_len))
+    H2 = st(np.asarray(H, np.float64) + lin(C, "o"))
+    A2 = st(layer_norm(H2, layer["ln2_g"], layer["ln2_b"], eps_ln))
+    F = st(np.maximum(lin(A2, "fc1"), 0.0))
+    return st(H2 + lin(F, "fc2"))
 
 
 # ---------------------------------------------------------------------------

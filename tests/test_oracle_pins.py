@@ -582,3 +582,133 @@ def test_tiny_loop_decreases_loss():
     grad = (X @ rec["W_before"].T - inp["Ystar"]).T @ X / X.shape[0]
     exact = [np.sum(grad * (rec["U"] @ Z @ rec["V"].T)) for Z in rec["Z"]]
     np.testing.assert_allclose(rec["g"], exact, rtol=1e-6, atol=1e-9)
+
+
+# ---------------------------------------------------------------------------
+# The decoder layer the queries run through (Eq. 5 inside Alg. 3)
+# ---------------------------------------------------------------------------
+def test_layer_norm_hand_case(golden_dir):
+    c = json.load(open(os.path.join(golden_dir, "layernorm_hand.json")))
+    x = np.array([c["x"]])
+    n = oracle.layer_norm(x, np.ones(4), np.zeros(4), c["eps_ln"])[0]
+    np.testing.assert_allclose(n, c["normalised"], rtol=0, atol=1e-15)
+    y = oracle.layer_norm(x, np.array(c["gamma"]), np.array(c["beta"]), c["eps_ln"])[0]
+    np.testing.assert_allclose(y, c["y"], rtol=0, atol=1e-15)
+
+
+def test_layer_norm_closed_forms_and_torch():
+    torch = pytest.importorskip("torch")
+    X = RNG.standard_normal((37, 96)) * 3.0 + RNG.standard_normal((37, 1))
+    eps_ln = 1e-5
+    Y = oracle.layer_norm(X, np.ones(96), np.zeros(96), eps_ln)
+    var = X.var(axis=1)
+    np.testing.assert_allclose(Y.mean(axis=1), 0.0, atol=1e-13)
+    np.testing.assert_allclose((Y ** 2).mean(axis=1), var / (var + eps_ln), rtol=1e-12)
+    # eps = 0: invariant to a positive scale and a shift of each row.
+    a, c = RNG.uniform(0.5, 4.0, (37, 1)), RNG.standard_normal((37, 1))
+    np.testing.assert_allclose(oracle.layer_norm(a * X + c, np.ones(96), np.zeros(96), 0.0),
+                               oracle.layer_norm(X, np.ones(96), np.zeros(96), 0.0), atol=1e-12)
+    g, b = RNG.standard_normal(96), RNG.standard_normal(96)
+    ref = torch.nn.functional.layer_norm(torch.from_numpy(X), (96,), torch.from_numpy(g), torch.from_numpy(b),
+                                         eps_ln).numpy()
+    np.testing.assert_allclose(oracle.layer_norm(X, g, b, eps_ln), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_causal_attention_matches_torch_sdpa():
+    torch = pytest.importorskip("torch")
+    S, L, heads, dh = 3, 20, 4, 16
+    Q, K, V = (RNG.standard_normal((S * L, heads * dh)) for _ in range(3))
+    got = oracle.causal_attention(Q, K, V, heads, L)
+    to4 = lambda A: torch.from_numpy(A).reshape(S, L, heads, dh).permute(0, 2, 1, 3)
+    ref = torch.nn.functional.scaled_dot_product_attention(to4(Q), to4(K), to4(V), is_causal=True)
+    ref = ref.permute(0, 2, 1, 3).reshape(S * L, heads * dh).numpy()
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_causal_attention_closed_forms():
+    S, L, heads, dh = 2, 12, 2, 16
+    Q, K, V = (RNG.standard_normal((S * L, heads * dh)) for _ in range(3))
+    O = oracle.causal_attention(Q, K, V, heads, L)
+    # The first token of each sequence sees only itself.
+    for s0 in range(0, S * L, L):
+        np.testing.assert_allclose(O[s0], V[s0], rtol=0, atol=1e-15)
+    # Q = 0: uniform weights over the visible keys, i.e. prefix means of V per sequence.
+    O0 = oracle.causal_attention(np.zeros_like(Q), K, V, heads, L)
+    for s0 in range(0, S * L, L):
+        pref = np.cumsum(V[s0:s0 + L], axis=0) / np.arange(1, L + 1)[:, None]
+        np.testing.assert_allclose(O0[s0:s0 + L], pref, rtol=1e-13, atol=1e-13)
+    # One-hot keys k_t = e_t and q_t = lam e_t: logit a = lam / sqrt(dh) on the diagonal, 0 off it,
+    # so o_t = (e^a v_t + sum_{t' < t} v_t') / (e^a + t).
+    lam = 3.0
+    Kh = np.zeros((L, dh)); Kh[np.arange(L), np.arange(L)] = 1.0
+    Vh = RNG.standard_normal((L, dh))
+    Oh = oracle.causal_attention(lam * Kh, Kh, Vh, 1, L)
+    ea = math.exp(lam / math.sqrt(dh))
+    for t in range(L):
+        np.testing.assert_allclose(Oh[t], (ea * Vh[t] + Vh[:t].sum(axis=0)) / (ea + t), rtol=1e-13, atol=1e-14)
+    # Sequences do not see each other.
+    V2 = V.copy(); V2[L:] += 1.0
+    np.testing.assert_array_equal(oracle.causal_attention(Q, K, V2, heads, L)[:L], O[:L])
+
+
+def _decoder_params(seed, d, ffn, r, q, zero=False):
+    shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "fc1": (ffn, d), "fc2": (d, ffn)}
+    layer = {}
+    for i, (nm, (m, n)) in enumerate(shapes.items()):
+        W = np.zeros((m, n)) if zero else zd.draw(seed, "W0", (i, m, n), (m, n), 0.05)
+        U, _ = np.linalg.qr(zd.draw(seed, "OMEGA_U", (i, m), (m, r)))
+        V, _ = np.linalg.qr(zd.draw(seed, "OMEGA_V", (i, n), (n, r)))
+        layer[nm] = dict(W=W, U=U, V=V, Z=zd.z_draws(seed, 0, i, q, r).astype(np.float64))
+    layer["ln1_g"], layer["ln1_b"] = 1.0 + 0.1 * RNG.standard_normal(d), 0.1 * RNG.standard_normal(d)
+    layer["ln2_g"], layer["ln2_b"] = 1.0 + 0.1 * RNG.standard_normal(d), 0.1 * RNG.standard_normal(d)
+    return layer
+
+
+def test_decoder_layer_zero_weights_is_identity():
+    d, ffn, r, q = 32, 64, 4, 2
+    layer = _decoder_params(1, d, ffn, r, q, zero=True)
+    H = RNG.standard_normal((24, d))
+    np.testing.assert_array_equal(oracle.decoder_layer(H, layer, 1.0, 0.0, 0, 4, 8), H)
+
+
+def test_decoder_layer_single_token_sequences():
+    """seq_len = 1: attention returns V, so H2 = H + (LN1(H) Wv'^T) Wo'^T, written out with the
+    perturbed weights formed directly from Eq. 4."""
+    d, ffn, r, q = 32, 64, 4, 2
+    layer = _decoder_params(2, d, ffn, r, q)
+    H = RNG.standard_normal((10, d))
+    s, eps, j = -1.0, 0.3, 1
+    Wp = {nm: layer[nm]["W"] + s * eps * layer[nm]["U"] @ layer[nm]["Z"][j] @ layer[nm]["V"].T
+          for nm in oracle.DECODER_MATS}
+    mu = H.mean(1, keepdims=True); sd = np.sqrt(H.var(1, keepdims=True) + 1e-5)
+    A = (H - mu) / sd * layer["ln1_g"] + layer["ln1_b"]
+    H2 = H + (A @ Wp["v"].T) @ Wp["o"].T
+    mu2 = H2.mean(1, keepdims=True); sd2 = np.sqrt(H2.var(1, keepdims=True) + 1e-5)
+    A2 = (H2 - mu2) / sd2 * layer["ln2_g"] + layer["ln2_b"]
+    H3 = H2 + np.maximum(A2 @ Wp["fc1"].T, 0.0) @ Wp["fc2"].T
+    np.testing.assert_allclose(oracle.decoder_layer(H, layer, s, eps, j, 4, 1), H3, rtol=1e-12, atol=1e-12)
+
+
+def test_decoder_layer_matches_torch_modules():
+    """The layer against torch's own layer_norm, scaled_dot_product_attention and relu in float64,
+    with the perturbed weights formed from Eq. 4."""
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    d, ffn, r, q, heads, L, S = 64, 128, 4, 3, 4, 10, 3
+    layer = _decoder_params(3, d, ffn, r, q)
+    H = RNG.standard_normal((S * L, d))
+    s, eps, j = 1.0, 0.05, 2
+    Wp = {nm: torch.from_numpy(layer[nm]["W"] + s * eps * layer[nm]["U"] @ layer[nm]["Z"][j] @ layer[nm]["V"].T)
+          for nm in oracle.DECODER_MATS}
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    Ht = t(H)
+    A = F.layer_norm(Ht, (d,), t(layer["ln1_g"]), t(layer["ln1_b"]), 1e-5)
+    heads4 = lambda X: X.reshape(S, L, heads, d // heads).permute(0, 2, 1, 3)
+    C = F.scaled_dot_product_attention(heads4(F.linear(A, Wp["q"])), heads4(F.linear(A, Wp["k"])),
+                                       heads4(F.linear(A, Wp["v"])), is_causal=True)
+    C = C.permute(0, 2, 1, 3).reshape(S * L, d)
+    H2 = Ht + F.linear(C, Wp["o"])
+    A2 = F.layer_norm(H2, (d,), t(layer["ln2_g"]), t(layer["ln2_b"]), 1e-5)
+    H3 = H2 + F.linear(F.relu(F.linear(A2, Wp["fc1"])), Wp["fc2"])
+    np.testing.assert_allclose(oracle.decoder_layer(H, layer, s, eps, j, heads, L), H3.numpy(),
+                               rtol=1e-11, atol=1e-11)
