@@ -63,6 +63,8 @@ typedef enum {
 } zo_status;
 
 typedef enum { ZO_F32 = 0, ZO_BF16 = 1, ZO_F16 = 2 } zo_dtype;
+/* Epilogues fused into the perturbed linear's output (zo_perturbed_linear_apply_ex). */
+typedef enum { ZO_EPI_NONE = 0, ZO_EPI_RELU = 1, ZO_EPI_RESIDUAL = 2 } zo_epilogue;
 
 int zo_abi_version(void);
 const char* zo_status_str(int status);
@@ -170,6 +172,23 @@ int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk,
                               int out_dtype, void* Y, void* workspace,
                               size_t ws_bytes, void* stream);
 
+/* apply with a fused epilogue on the fp32 result, before its one rounding to
+ * out_dtype -- the operations that follow a linear inside the decoder layer
+ * of the network the queries evaluate (the forward of Eq. 5):
+ *   ZO_EPI_NONE      Y_b = result (zo_perturbed_linear_apply);
+ *   ZO_EPI_RELU      Y_b = max(result, 0);
+ *   ZO_EPI_RESIDUAL  Y_b = R_b + result, R_b at R + b * r_block_stride
+ *                    elements (0: one R for every block), out_dtype, T x m
+ *                    rows of stride m.  R may be Y itself.
+ * Limits as for zo_perturbed_linear_apply; with 16-bit outputs R is 16-byte
+ * aligned and r_block_stride a multiple of 8 (0 or >= T*m). */
+int zo_perturbed_linear_apply_ex(int T, int m, int n, int r, int q, int nblk,
+                                 int in_dtype, const void* X,
+                                 long long x_block_stride, const void* W,
+                                 int out_dtype, void* Y, int epilogue,
+                                 const void* R, long long r_block_stride,
+                                 void* workspace, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------
  * Perturbed linear of a LoRA-adapted layer -- Eq. 4 and Alg. 2 applied to
  * the two trainable adapter factors (the LoRA scheme of the experiments,
@@ -235,6 +254,77 @@ int zo_lora_perturbed_linear_prepare(int T, int m, int n, int rl, int r, int q,
                                      const float* U_B, const float* V_B,
                                      const float* Z_B, void* workspace,
                                      size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * The network a query evaluates -- the forward inside Eq. 5 (each query's
+ * loss is that of the whole model with every matrix perturbed, Alg. 3), as a
+ * pre-LN decoder layer of the OPT family:
+ *
+ *   A = LN1(H);   Q, K, V = A Wq'^T, A Wk'^T, A Wv'^T;   C = attention(Q, K, V)
+ *   H2 = H + C Wo'^T;   F = relu(LN2(H2) W1'^T);   H_out = H2 + F W2'^T
+ *
+ * with each W' = W + s eps U Z_j V^T for block b's query j and sign s (Eq. 4;
+ * each matrix has its own U, V, Z).  No biases (the perturbed parameters are
+ * the weight matrices).
+ * ------------------------------------------------------------------------ */
+
+/* Row-wise layer normalisation: Y = (X - mean) / sqrt(var + eps_ln) * gamma +
+ * beta per row of d elements, population variance, statistics in fp32.
+ * X, Y: rows x d (dtype, may alias); gamma, beta: device fp32 [d].
+ * Limits: d % 8 == 0; 16-byte aligned pointers. */
+int zo_layernorm(long long rows, int d, int dtype, const void* X,
+                 const float* gamma, const float* beta, float eps_ln, void* Y,
+                 void* stream);
+
+/* Multi-head causal self-attention.  Q, K, V, O: nblk blocks of T rows x d
+ * (dtype bf16 or fp16, row-major, contiguous blocks); each block holds
+ * T / seq_len sequences one after another; head h is columns h dh ..
+ * (h+1) dh - 1 (dh = d / heads).  Query t of a sequence attends to its keys
+ * t' <= t with weights softmax(q_t . k_t' / sqrt(dh)).  fp32 softmax; the
+ * products run on the MFMA with P as a hi + lo 16-bit pair (~2^-16 relative
+ * before the output's rounding to dtype).
+ * Limits: T % seq_len == 0; dh = 64 or 128; 16-byte aligned pointers. */
+int zo_causal_attention(int nblk, int T, int seq_len, int d, int heads,
+                        int dtype, const void* Q, const void* K, const void* V,
+                        void* O, void* stream);
+
+/* One perturbed matrix: W (m x n, the layer's dtype), U (m x r), V (n x r)
+ * and Z (q x r x r) fp32. */
+typedef struct {
+  const void* W;
+  const float* U;
+  const float* V;
+  const float* Z;
+} zo_matrix;
+
+/* A decoder layer: q, k, v, o (d x d), fc1 (ffn x d), fc2 (d x ffn), and the
+ * two layer norms' gamma / beta (device fp32 [d]). */
+typedef struct {
+  zo_matrix q, k, v, o, fc1, fc2;
+  const float* ln1_gamma;
+  const float* ln1_beta;
+  const float* ln2_gamma;
+  const float* ln2_beta;
+} zo_decoder_layer;
+
+/* The layer for all nblk blocks at once (block b: query blk_query[b], sign
+ * blk_sign[b], as for zo_perturbed_linear).  H: the layer input, one T x d
+ * for every block (h_block_stride = 0: the model's first layer) or nblk
+ * contiguous blocks (h_block_stride = T*d); H_out: nblk blocks of T x d (may
+ * alias H when h_block_stride = T*d).  The six products are perturbed
+ * linears (zo_perturbed_linear_apply_ex: ReLU after fc1, the residuals fused
+ * into o and fc2); intermediate activations are stored in dtype in the
+ * workspace (zo_decoder_layer_workspace bytes).
+ * Limits: dtype bf16 or fp16; those of zo_causal_attention and of
+ * zo_perturbed_linear for each matrix. */
+size_t zo_decoder_layer_workspace(int T, int seq_len, int d, int heads, int ffn,
+                                  int r, int q, int nblk, int dtype);
+int zo_decoder_layer_forward(int T, int seq_len, int d, int heads, int ffn,
+                             int r, int q, int nblk, const int* blk_query,
+                             const int8_t* blk_sign, float eps, float eps_ln,
+                             int dtype, const void* H, long long h_block_stride,
+                             const zo_decoder_layer* layer, void* H_out,
+                             void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Subspace Adam update -- Eqs. 6-10 and the tail of Alg. 3.

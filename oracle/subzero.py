@@ -212,14 +212,15 @@ def causal_attention(Q, K, V, heads, seq_len):
 DECODER_MATS = ("q", "k", "v", "o", "fc1", "fc2")
 
 
-def decoder_layer(H, layer, sign, eps, j, heads, seq_len, store=None, eps_ln=1e-5):
+def decoder_layer(H, layer, sign, eps, j, heads, seq_len, store=None, eps_ln=1e-5, trace=None):
     """One pre-LN decoder layer under query j with sign s: each of its six weight matrices W
     (q, k, v, o, fc1, fc2; each with its own U, V and coefficients Z_j) enters as
     W + s eps U Z_j V^T (Eq. 4), and
         A = LN1(H);   Q, K, V = A Wq'^T, A Wk'^T, A Wv'^T;   C = attention(Q, K, V)
         H2 = H + C Wo'^T;   F = relu(LN2(H2) W1'^T);   H3 = H2 + F W2'^T.
     ``store`` (optional) rounds each tensor the layer writes to memory, at the points where
-    a device path stores one (e.g. round_bf16); all arithmetic is float64.
+    a device path stores one (e.g. round_bf16); all arithmetic is float64.  ``trace`` (an
+    optional dict) receives the stored intermediates A, Q, K, V, C, H2, A2, F.
     READING: no biases (the perturbed parameters are the weight matrices); ReLU, as in OPT."""
     st = store if store is not None else (lambda x: x)
     lin = lambda X, name: perturbed_linear(X, layer[name]["W"], layer[name]["U"], layer[name]["V"],
@@ -230,6 +231,8 @@ def decoder_layer(H, layer, sign, eps, j, heads, seq_len, store=None, eps_ln=1e-
     H2 = st(np.asarray(H, np.float64) + lin(C, "o"))
     A2 = st(layer_norm(H2, layer["ln2_g"], layer["ln2_b"], eps_ln))
     F = st(np.maximum(lin(A2, "fc1"), 0.0))
+    if trace is not None:
+        trace.update(A=A, Q=Q, K=K, V=Vv, C=C, H2=H2, A2=A2, F=F)
     return st(H2 + lin(F, "fc2"))
 
 

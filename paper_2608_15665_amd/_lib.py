@@ -35,7 +35,21 @@ ABI_SYMBOLS = (
     "zo_subspace_adam_update_workspace", "zo_subspace_adam_update",
     "zo_subspace_sgd_update_workspace", "zo_subspace_sgd_update",
     "zo_sq_loss_workspace", "zo_sq_loss", "zo_combine_central", "zo_combine_forward",
+    "zo_perturbed_linear_apply_ex", "zo_layernorm", "zo_causal_attention",
+    "zo_decoder_layer_workspace", "zo_decoder_layer_forward",
 )
+ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL = 0, 1, 2
+
+
+class Matrix(ctypes.Structure):
+    """zo_matrix: one perturbed matrix (device pointers)."""
+    _fields_ = [("W", ctypes.c_void_p), ("U", ctypes.c_void_p), ("V", ctypes.c_void_p), ("Z", ctypes.c_void_p)]
+
+
+class DecoderLayerDesc(ctypes.Structure):
+    """zo_decoder_layer: six perturbed matrices and the two layer norms' parameters."""
+    _fields_ = [(nm, Matrix) for nm in ("q", "k", "v", "o", "fc1", "fc2")] + [
+        (nm, ctypes.c_void_p) for nm in ("ln1_gamma", "ln1_beta", "ln2_gamma", "ln2_beta")]
 
 
 class ZoError(RuntimeError):
@@ -125,6 +139,20 @@ def lib() -> ctypes.CDLL:
             L.zo_combine_central.argtypes = [c_int, c_vp, c_f, c_vp, c_vp]
             L.zo_combine_forward.restype = c_int
             L.zo_combine_forward.argtypes = [c_int, c_vp, c_f, c_vp, c_vp]
+            L.zo_perturbed_linear_apply_ex.restype = c_int
+            L.zo_perturbed_linear_apply_ex.argtypes = ([c_int] * 7 + [c_vp, c_ll, c_vp, c_int, c_vp, c_int, c_vp,
+                                                                      c_ll, c_vp, c_sz, c_vp])
+            L.zo_layernorm.restype = c_int
+            L.zo_layernorm.argtypes = [c_ll, c_int, c_int, c_vp, c_vp, c_vp, c_f, c_vp, c_vp]
+            L.zo_causal_attention.restype = c_int
+            L.zo_causal_attention.argtypes = [c_int] * 6 + [c_vp] * 5
+            L.zo_decoder_layer_workspace.restype = c_sz
+            L.zo_decoder_layer_workspace.argtypes = [c_int] * 9
+            L.zo_decoder_layer_forward.restype = c_int
+            L.zo_decoder_layer_forward.argtypes = ([c_int] * 8 + [ctypes.POINTER(ctypes.c_int),
+                                                                  ctypes.POINTER(ctypes.c_int8), c_f, c_f, c_int,
+                                                                  c_vp, c_ll, ctypes.POINTER(DecoderLayerDesc),
+                                                                  c_vp, c_vp, c_sz, c_vp])
             _lib = L
     return _lib
 
@@ -267,10 +295,21 @@ class PerturbedLinear:
                                                  self.xs, self.U.data_ptr(), self.V.data_ptr(), self.Z.data_ptr(),
                                                  self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
 
-    def apply(self):
-        _check(lib().zo_perturbed_linear_apply(*self.dims, self.dt, self.X.data_ptr(), self.xs, self.W.data_ptr(),
-                                               self.odt, self.Y.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
-                                               _stream_handle()))
+    def apply(self, epilogue: int = ZO_EPI_NONE, R: Optional[torch.Tensor] = None,
+              r_block_stride: Optional[int] = None):
+        """The fused GEMM (zo_perturbed_linear_apply_ex): epilogue ZO_EPI_RELU, or ZO_EPI_RESIDUAL
+        adding R (Y's type; one T x m block shared by all blocks, or nblk blocks)."""
+        T, m = self.dims[0], self.dims[1]
+        nblk = self.dims[5]
+        rs = 0
+        if epilogue == ZO_EPI_RESIDUAL:
+            _need(R, "R", self.Y.dtype)
+            rs = r_block_stride if r_block_stride is not None else (0 if R.numel() == T * m else T * m)
+            if R.numel() < (T * m if rs == 0 else rs * (nblk - 1) + T * m):
+                raise ValueError("R is too small for the block layout")
+        _check(lib().zo_perturbed_linear_apply_ex(*self.dims, self.dt, self.X.data_ptr(), self.xs, self.W.data_ptr(),
+                                                  self.odt, self.Y.data_ptr(), int(epilogue), _ptr(R), int(rs),
+                                                  self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
         return self.Y
 
     def __call__(self):
@@ -290,6 +329,106 @@ def perturbed_linear(X: torch.Tensor, W: torch.Tensor, U: torch.Tensor, V: torch
     all blocks (x_block_stride = 0).  Returns Y (nblk*T x m).
     """
     return PerturbedLinear(X, W, U, V, Z, blk_query, blk_sign, eps, T, x_block_stride, out_dtype, Y)()
+
+
+def layernorm(X: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor, eps_ln: float = 1e-5,
+              out: Optional[torch.Tensor] = None):
+    """Row-wise layer normalisation of X (rows x d).  See zo_layernorm."""
+    d = X.shape[-1]
+    _need(X, "X", X.dtype)
+    if X.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {X.dtype}")
+    _need(gamma, "gamma", torch.float32, d)
+    _need(beta, "beta", torch.float32, d)
+    if out is None:
+        out = torch.empty_like(X)
+    _need(out, "out", X.dtype, X.numel())
+    _check(lib().zo_layernorm(X.numel() // d, d, _DT[X.dtype], X.data_ptr(), gamma.data_ptr(), beta.data_ptr(),
+                              float(eps_ln), out.data_ptr(), _stream_handle()))
+    return out
+
+
+def causal_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, nblk: int, T: int, seq_len: int,
+                     heads: int, out: Optional[torch.Tensor] = None):
+    """Multi-head causal self-attention of nblk blocks of T rows (T / seq_len sequences each).
+    See zo_causal_attention."""
+    d = Q.shape[-1]
+    for nm, t in (("Q", Q), ("K", K), ("V", V)):
+        _need(t, nm, Q.dtype, nblk * T * d)
+    if out is None:
+        out = torch.empty_like(Q)
+    _need(out, "out", Q.dtype, nblk * T * d)
+    _check(lib().zo_causal_attention(nblk, T, seq_len, d, heads, _DT[Q.dtype], Q.data_ptr(), K.data_ptr(),
+                                     V.data_ptr(), out.data_ptr(), _stream_handle()))
+    return out
+
+
+class DecoderLayer:
+    """A pre-LN decoder layer whose six matrices are perturbed per block.  See
+    zo_decoder_layer_forward.  ``mats`` maps q, k, v, o, fc1, fc2 to dicts with W (the
+    layer's dtype), U, V, Z (fp32); ``ln`` holds ln1_gamma, ln1_beta, ln2_gamma, ln2_beta."""
+
+    NAMES = ("q", "k", "v", "o", "fc1", "fc2")
+
+    def __init__(self, mats: dict, ln: dict, blk_query: Sequence[int], blk_sign: Sequence[int], eps: float,
+                 T: int, seq_len: int, heads: int, eps_ln: float = 1e-5, workspace: Optional[torch.Tensor] = None):
+        nblk = len(blk_query)
+        if len(blk_sign) != nblk:
+            raise ValueError("blk_query and blk_sign differ in length")
+        Wq = mats["q"]["W"]
+        d = Wq.shape[0]
+        ffn = mats["fc1"]["W"].shape[0]
+        r = mats["q"]["U"].shape[1]
+        q = mats["q"]["Z"].shape[0]
+        dt = Wq.dtype
+        if dt not in _DT:
+            raise TypeError(f"unsupported dtype {dt}")
+        shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "fc1": (ffn, d), "fc2": (d, ffn)}
+        desc = DecoderLayerDesc()
+        for nm in self.NAMES:
+            m, n = shapes[nm]
+            mt = mats[nm]
+            _need(mt["W"], f"{nm}.W", dt, m * n)
+            _need(mt["U"], f"{nm}.U", torch.float32, m * r)
+            _need(mt["V"], f"{nm}.V", torch.float32, n * r)
+            _need(mt["Z"], f"{nm}.Z", torch.float32, q * r * r)
+            setattr(desc, nm, Matrix(mt["W"].data_ptr(), mt["U"].data_ptr(), mt["V"].data_ptr(), mt["Z"].data_ptr()))
+        for nm in ("ln1_gamma", "ln1_beta", "ln2_gamma", "ln2_beta"):
+            _need(ln[nm], nm, torch.float32, d)
+            setattr(desc, nm, ln[nm].data_ptr())
+        self.desc, self.keep = desc, (mats, ln)
+        self.dims = (T, seq_len, d, heads, ffn, r, q, nblk)
+        self.bq = (ctypes.c_int * nblk)(*[int(v) for v in blk_query])
+        self.bs = (ctypes.c_int8 * nblk)(*[int(v) for v in blk_sign])
+        self.eps, self.eps_ln, self.dt, self.dtype = float(eps), float(eps_ln), _DT[dt], dt
+        need = lib().zo_decoder_layer_workspace(*self.dims, self.dt)
+        if need == 0:
+            _check(lib().zo_decoder_layer_forward(*self.dims, self.bq, self.bs, self.eps, self.eps_ln, self.dt,
+                                                  None, 0, ctypes.byref(self.desc), None, None, 0, None))
+        if workspace is None:
+            workspace = Workspace.get(need)
+        _need(workspace, "workspace", torch.uint8)
+        if workspace.numel() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, {need} needed")
+        self.ws = workspace
+
+    def __call__(self, H: torch.Tensor, out: Optional[torch.Tensor] = None):
+        """H: one T x d input shared by all blocks, or nblk blocks; returns nblk blocks of T x d."""
+        T, d, nblk = self.dims[0], self.dims[2], self.dims[7]
+        _need(H, "H", self.dtype)
+        if H.numel() == T * d:
+            hs = 0
+        elif H.numel() == nblk * T * d:
+            hs = T * d
+        else:
+            raise ValueError("H must hold T*d or nblk*T*d elements")
+        if out is None:
+            out = torch.empty((nblk * T, d), dtype=self.dtype, device=H.device)
+        _need(out, "out", self.dtype, nblk * T * d)
+        _check(lib().zo_decoder_layer_forward(*self.dims, self.bq, self.bs, self.eps, self.eps_ln, self.dt,
+                                              H.data_ptr(), hs, ctypes.byref(self.desc), out.data_ptr(),
+                                              self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
+        return out
 
 
 class LoraPerturbedLinear:

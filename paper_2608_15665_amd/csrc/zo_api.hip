@@ -196,16 +196,37 @@ int zo_perturbed_linear_prepare(int T, int m, int n, int r, int q, int nblk,
   return zo_plinear_prepare(p, blk_query, blk_sign, eps, X, U, V, Z, workspace, (hipStream_t)stream);
 }
 
+int zo_perturbed_linear_apply_ex(int T, int m, int n, int r, int q, int nblk, int in_dtype,
+                                 const void* X, long long x_block_stride, const void* W,
+                                 int out_dtype, void* Y, int epilogue, const void* R,
+                                 long long r_block_stride, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  PlinearPlan p;
+  ZO_CHECK(W && Y, "perturbed_linear: NULL tensor argument (W or Y)");
+  ZO_CHECK(epilogue == ZO_EPI_NONE || epilogue == ZO_EPI_RELU || epilogue == ZO_EPI_RESIDUAL,
+           "perturbed_linear: bad epilogue %d", epilogue);
+  if (epilogue == ZO_EPI_RESIDUAL) {
+    ZO_CHECK(R, "perturbed_linear: residual epilogue with a NULL R");
+    ZO_CHECK(r_block_stride == 0 || r_block_stride >= (long long)T * m,
+             "perturbed_linear: r_block_stride = %lld must be 0 or >= T*m", r_block_stride);
+    ZO_CHECK(out_dtype == ZO_F32 || r_block_stride % 8 == 0,
+             "perturbed_linear: 16-bit r_block_stride must be a multiple of 8");
+    ZO_CHECK(aligned(R, out_dtype == ZO_F32 ? 4 : 16), "perturbed_linear: R alignment");
+  }
+  int st = check_plinear_call(T, m, n, r, q, nblk, x_block_stride, in_dtype, out_dtype, X, W, Y,
+                              workspace, ws_bytes, &p);
+  if (st != ZO_OK) return st;
+  return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream, epilogue,
+                          epilogue == ZO_EPI_RESIDUAL ? R : nullptr, r_block_stride);
+}
+
 int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk, int in_dtype,
                               const void* X, long long x_block_stride, const void* W,
                               int out_dtype, void* Y, void* workspace, size_t ws_bytes,
                               void* stream) {
-  PlinearPlan p;
-  ZO_CHECK(W && Y, "perturbed_linear: NULL tensor argument (W or Y)");
-  int st = check_plinear_call(T, m, n, r, q, nblk, x_block_stride, in_dtype, out_dtype, X, W, Y,
-                              workspace, ws_bytes, &p);
-  if (st != ZO_OK) return st;
-  return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream);
+  return zo_perturbed_linear_apply_ex(T, m, n, r, q, nblk, in_dtype, X, x_block_stride, W,
+                                      out_dtype, Y, ZO_EPI_NONE, nullptr, 0, workspace, ws_bytes,
+                                      stream);
 }
 
 // ------------------------------------------------------------- LoRA scheme
@@ -278,6 +299,157 @@ int zo_lora_perturbed_linear(int T, int m, int n, int rl, int r, int q, int nblk
                        workspace, (hipStream_t)stream);
   if (st != ZO_OK) return st;
   return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream);
+}
+
+// ------------------------------------------------------- decoder layer
+int zo_layernorm(long long rows, int d, int dtype, const void* X, const float* gamma,
+                 const float* beta, float eps_ln, void* Y, void* stream) {
+  ZO_CHECK(rows >= 0 && d >= 8 && d % 8 == 0, "layernorm: rows = %lld, d = %d (need d %% 8 == 0)",
+           rows, d);
+  ZO_CHECK(dtype == ZO_F32 || dtype == ZO_BF16 || dtype == ZO_F16, "layernorm: bad dtype %d", dtype);
+  ZO_CHECK(isfinite(eps_ln) && eps_ln >= 0.f, "layernorm: eps_ln must be finite and >= 0");
+  if (rows == 0) return ZO_OK;
+  ZO_CHECK(X && Y && gamma && beta, "layernorm: NULL tensor argument");
+  ZO_CHECK(aligned(X, 16) && aligned(Y, 16) && aligned(gamma, 16) && aligned(beta, 16),
+           "layernorm: X, Y, gamma, beta must be 16-byte aligned");
+  return zo_layernorm_launch(rows, d, dtype, X, gamma, beta, eps_ln, Y, (hipStream_t)stream);
+}
+
+static int check_attention(int nblk, int T, int seq_len, int d, int heads, int dtype) {
+  ZO_CHECK(nblk >= 1 && T >= 1 && seq_len >= 1 && T % seq_len == 0,
+           "attention: nblk = %d, T = %d, seq_len = %d (need T %% seq_len == 0)", nblk, T, seq_len);
+  ZO_CHECK(heads >= 1 && d % heads == 0, "attention: d = %d not a multiple of heads = %d", d, heads);
+  if (dtype != ZO_BF16 && dtype != ZO_F16) {
+    zo_set_error("attention: dtype %d unsupported (bf16 or fp16)", dtype);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  const int dh = d / heads;
+  if (dh != 64 && dh != 128) {
+    zo_set_error("attention: head dim %d unsupported (64 or 128)", dh);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  ZO_CHECK((long long)nblk * T * d < (1LL << 40), "attention: tensors too large");
+  return ZO_OK;
+}
+
+int zo_causal_attention(int nblk, int T, int seq_len, int d, int heads, int dtype, const void* Q,
+                        const void* K, const void* V, void* O, void* stream) {
+  int st = check_attention(nblk, T, seq_len, d, heads, dtype);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(Q && K && V && O, "attention: NULL tensor argument");
+  ZO_CHECK(aligned(Q, 16) && aligned(K, 16) && aligned(V, 16) && aligned(O, 16),
+           "attention: Q, K, V, O must be 16-byte aligned");
+  return zo_attention_launch(nblk, T, seq_len, d, heads, dtype, Q, K, V, O, (hipStream_t)stream);
+}
+
+namespace {
+struct DecoderWs {
+  char *A, *Qb, *Kb, *Vb, *C, *H2, *F, *lin;
+  size_t total;
+};
+// The largest perturbed-linear workspace of the layer's six matrices.
+size_t decoder_lin_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype) {
+  const int shapes[3][2] = {{d, d}, {ffn, d}, {d, ffn}};
+  size_t need = 0;
+  for (const auto& sh : shapes) {
+    PlinearPlan p;
+    zo_plinear_plan(&p, T, sh[0], sh[1], r, q, nblk, (long long)T * sh[1], dtype, dtype);
+    need = p.ws_total > need ? p.ws_total : need;
+  }
+  return need;
+}
+DecoderWs decoder_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype, void* base) {
+  const size_t es = dtype == ZO_F32 ? 4 : 2;
+  const size_t act = zo_align256((size_t)nblk * T * d * es);
+  WsCarver wc(base);
+  DecoderWs w;
+  w.A = (char*)wc.take(act);
+  w.Qb = (char*)wc.take(act);
+  w.Kb = (char*)wc.take(act);
+  w.Vb = (char*)wc.take(act);
+  w.C = (char*)wc.take(act);
+  w.H2 = (char*)wc.take(act);
+  w.F = (char*)wc.take((size_t)nblk * T * ffn * es);
+  w.lin = (char*)wc.take(decoder_lin_ws(T, d, ffn, r, q, nblk, dtype));
+  w.total = wc.off;
+  return w;
+}
+int check_decoder(int T, int seq_len, int d, int heads, int ffn, int r, int q, int nblk, int dtype) {
+  int st = check_attention(nblk, T, seq_len, d, heads, dtype);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(ffn >= 8 && ffn % 8 == 0, "decoder: ffn = %d must be a positive multiple of 8", ffn);
+  if ((st = check_plinear(T, d, d, r, q, nblk, (long long)T * d, dtype)) != ZO_OK) return st;
+  if ((st = check_plinear(T, ffn, d, r, q, nblk, (long long)T * d, dtype)) != ZO_OK) return st;
+  return check_plinear(T, d, ffn, r, q, nblk, (long long)T * ffn, dtype);
+}
+}  // namespace
+
+size_t zo_decoder_layer_workspace(int T, int seq_len, int d, int heads, int ffn, int r, int q,
+                                  int nblk, int dtype) {
+  if (check_decoder(T, seq_len, d, heads, ffn, r, q, nblk, dtype) != ZO_OK) return 0;
+  return decoder_ws(T, d, ffn, r, q, nblk, dtype, nullptr).total;
+}
+
+int zo_decoder_layer_forward(int T, int seq_len, int d, int heads, int ffn, int r, int q, int nblk,
+                             const int* blk_query, const int8_t* blk_sign, float eps, float eps_ln,
+                             int dtype, const void* H, long long h_block_stride,
+                             const zo_decoder_layer* layer, void* H_out, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  int st = check_decoder(T, seq_len, d, heads, ffn, r, q, nblk, dtype);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(layer && H && H_out, "decoder: NULL argument (layer, H or H_out)");
+  ZO_CHECK(h_block_stride == 0 || h_block_stride == (long long)T * d,
+           "decoder: h_block_stride = %lld must be 0 (one H for every block) or T*d", h_block_stride);
+  ZO_CHECK(isfinite(eps_ln) && eps_ln >= 0.f, "decoder: eps_ln must be finite and >= 0");
+  const zo_matrix* mats[6] = {&layer->q, &layer->k, &layer->v, &layer->o, &layer->fc1, &layer->fc2};
+  const char* names[6] = {"q", "k", "v", "o", "fc1", "fc2"};
+  for (int i = 0; i < 6; ++i) {
+    if ((st = check_blocks(q, nblk, blk_query, blk_sign, eps, mats[i]->U, mats[i]->V, mats[i]->Z)) != ZO_OK)
+      return st;
+    ZO_CHECK(mats[i]->W && aligned(mats[i]->W, 16), "decoder: %s W is NULL or not 16-byte aligned", names[i]);
+  }
+  ZO_CHECK(layer->ln1_gamma && layer->ln1_beta && layer->ln2_gamma && layer->ln2_beta,
+           "decoder: NULL layer-norm parameter");
+  ZO_CHECK(aligned(layer->ln1_gamma, 16) && aligned(layer->ln1_beta, 16) &&
+               aligned(layer->ln2_gamma, 16) && aligned(layer->ln2_beta, 16),
+           "decoder: layer-norm parameters must be 16-byte aligned");
+  ZO_CHECK(aligned(H, 16) && aligned(H_out, 16), "decoder: H and H_out must be 16-byte aligned");
+  const DecoderWs need = decoder_ws(T, d, ffn, r, q, nblk, dtype, nullptr);
+  if (!workspace || ws_bytes < need.total) {
+    zo_set_error("decoder: workspace %zu bytes < required %zu", ws_bytes, need.total);
+    return ZO_ERR_WORKSPACE;
+  }
+  ZO_CHECK(aligned(workspace, 256), "decoder: workspace not 256-byte aligned");
+  const DecoderWs w = decoder_ws(T, d, ffn, r, q, nblk, dtype, workspace);
+  hipStream_t s = (hipStream_t)stream;
+  const long long Td = (long long)T * d, Tf = (long long)T * ffn;
+  const bool shared = h_block_stride == 0;
+  // One perturbed linear: prepare (X V, s eps U Z_j) then the fused GEMM.
+  auto lin = [&](const zo_matrix* mt, int m, int n, const void* X, long long xs, void* Y, int epi,
+                 const void* R, long long rs) -> int {
+    PlinearPlan p;
+    zo_plinear_plan(&p, T, m, n, r, q, nblk, xs, dtype, dtype);
+    int e = zo_plinear_prepare(p, blk_query, blk_sign, eps, X, mt->U, mt->V, mt->Z, w.lin, s);
+    if (e != ZO_OK) return e;
+    return zo_plinear_apply(p, X, mt->W, Y, w.lin, s, epi, R, rs);
+  };
+  // A = LN1(H): once when every block shares H.
+  if ((st = zo_layernorm_launch(shared ? T : (long long)nblk * T, d, dtype, H, layer->ln1_gamma,
+                                layer->ln1_beta, eps_ln, w.A, s)) != ZO_OK)
+    return st;
+  const long long as = shared ? 0 : Td;
+  if ((st = lin(&layer->q, d, d, w.A, as, w.Qb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  if ((st = lin(&layer->k, d, d, w.A, as, w.Kb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  if ((st = lin(&layer->v, d, d, w.A, as, w.Vb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
+    return st;
+  // H2 = H + C Wo'^T;  A = LN2(H2);  F = relu(A W1'^T);  H_out = H2 + F W2'^T.
+  if ((st = lin(&layer->o, d, d, w.C, Td, w.H2, ZO_EPI_RESIDUAL, H, h_block_stride)) != ZO_OK) return st;
+  if ((st = zo_layernorm_launch((long long)nblk * T, d, dtype, w.H2, layer->ln2_gamma, layer->ln2_beta,
+                                eps_ln, w.A, s)) != ZO_OK)
+    return st;
+  if ((st = lin(&layer->fc1, ffn, d, w.A, Td, w.F, ZO_EPI_RELU, nullptr, 0)) != ZO_OK) return st;
+  return lin(&layer->fc2, d, ffn, w.F, Tf, H_out, ZO_EPI_RESIDUAL, w.H2, Td);
 }
 
 // ------------------------------------------------------------------ update

@@ -1,0 +1,339 @@
+// The network a SubZero+ query evaluates (the forward inside Eq. 5 / the query
+// loop of Alg. 3), as a pre-LN decoder layer of the OPT family whose six weight
+// matrices are all perturbed in their own subspaces (Eq. 4):
+//   A = LN1(H);  Q, K, V = A Wq'^T, A Wk'^T, A Wv'^T;  C = causal attention;
+//   H2 = H + C Wo'^T;  F = relu(LN2(H2) W1'^T);  H3 = H2 + F W2'^T.
+// The six products are the perturbed linears of zo_gemm.hip (the ReLU and the
+// residual additions fused into their epilogues); this file adds the row
+// normalisation, the attention, and the host sequence of one layer.
+//
+// k_layernorm: one wave per row, three passes over the row (sum, squared
+// deviations, output); the row stays in L1/L2 after the first, so HBM sees
+// one read and one write.  Statistics in fp32 with fixed-order wave sums.
+//
+// k_attention<F16, DH>: one workgroup (4 waves) per (block, sequence, head,
+// 64-query tile); keys in tiles of 64 through LDS, online softmax in fp32.
+// Each wave owns 16 queries and computes the transposed products, which keeps
+// every step in registers:
+//   S^T = K Q^T  (v_mfma_f32_16x16x32: A = K rows from LDS, B = the wave's Q
+//                 rows held in registers); lane (l16, g) of a 16 x 16 result
+//                 holds query l16 and keys 4g .. 4g+3, so a query's softmax
+//                 statistics are a sum over its lane and the 4 lanes l16 + 16g;
+//   O^T += V^T P^T, 32 keys per MFMA.  The MFMA's k slots of lane group g are
+//                 given the keys that lane already holds for P (4g .. 4g+3 of
+//                 each of two 16-key tiles); V^T's fragment takes the same keys
+//                 from a transposed LDS copy of the V tile.  A sum over k does
+//                 not depend on how the k slots are assigned to keys, as long
+//                 as both operands use the same assignment.
+// P enters as a hi + lo pair of 16-bit values (two MFMAs), so the product is
+// ~2^-16 accurate before the output's rounding; P is computed as
+// 2^(s - m + 12) (the common factor 2^12 cancels in the normalisation and keeps
+// fp16 low parts out of the subnormal range).
+#include "zo_internal.h"
+
+#include <type_traits>
+
+namespace {
+
+// ---------------------------------------------------------------- layer norm
+template <int DT>
+__device__ __forceinline__ void load8(const void* X, size_t idx, float* v) {
+  if constexpr (DT == ZO_F32) {
+    const f32x4 a = *(const f32x4*)((const float*)X + idx);
+    const f32x4 b = *(const f32x4*)((const float*)X + idx + 4);
+    v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
+    v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
+  } else {
+    const u32x4 u = *(const u32x4*)((const uint16_t*)X + idx);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (DT == ZO_BF16) {
+        v[2 * e] = bf16_to_f32((bf16_t)u[e]);
+        v[2 * e + 1] = bf16_to_f32((bf16_t)(u[e] >> 16));
+      } else {
+        v[2 * e] = f16_to_f32((uint16_t)u[e]);
+        v[2 * e + 1] = f16_to_f32((uint16_t)(u[e] >> 16));
+      }
+    }
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ void store8(void* Y, size_t idx, const float* v) {
+  if constexpr (DT == ZO_F32) {
+    *(f32x4*)((float*)Y + idx) = (f32x4){v[0], v[1], v[2], v[3]};
+    *(f32x4*)((float*)Y + idx + 4) = (f32x4){v[4], v[5], v[6], v[7]};
+  } else if constexpr (DT == ZO_BF16) {
+    *(u32x4*)((uint16_t*)Y + idx) = (u32x4){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                            pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+  } else {
+    *(u32x4*)((uint16_t*)Y + idx) = (u32x4){pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3]),
+                                            pack_f16x2(v[4], v[5]), pack_f16x2(v[6], v[7])};
+  }
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Rows of d elements (d % 8 == 0), 4 rows per workgroup, one per wave.
+template <int DT>
+__global__ __launch_bounds__(256) void k_layernorm(const void* __restrict__ X,
+                                                   const float* __restrict__ gamma,
+                                                   const float* __restrict__ beta, void* Y,
+                                                   long long rows, int d, float eps_ln) {
+  const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const size_t base = (size_t)row * d;
+  float v[8];
+  float s = 0.f;
+  for (int c = lane * 8; c < d; c += 512) {
+    load8<DT>(X, base + c, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s += v[e];
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.f;
+  for (int c = lane * 8; c < d; c += 512) {
+    load8<DT>(X, base + c, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q = fmaf(v[e] - mean, v[e] - mean, q);
+  }
+  const float rstd = 1.f / sqrtf(wave_sum(q) / (float)d + eps_ln);
+  for (int c = lane * 8; c < d; c += 512) {
+    load8<DT>(X, base + c, v);
+    const f32x4 g0 = *(const f32x4*)(gamma + c), g1 = *(const f32x4*)(gamma + c + 4);
+    const f32x4 b0 = *(const f32x4*)(beta + c), b1 = *(const f32x4*)(beta + c + 4);
+    const float g[8] = {g0[0], g0[1], g0[2], g0[3], g1[0], g1[1], g1[2], g1[3]};
+    const float b[8] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = fmaf((v[e] - mean) * rstd, g[e], b[e]);
+    store8<DT>(Y, base + c, v);
+  }
+}
+
+// ---------------------------------------------------------------- attention
+constexpr int AT_Q = 64;   // queries per workgroup (16 per wave)
+constexpr int AT_K = 64;   // keys per tile
+
+struct AttnArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  void* O;
+  int T, seq_len, d, heads, qtiles;  // qtiles = ceil(seq_len / AT_Q)
+  float scale_log2;                  // log2(e) / sqrt(dh)
+};
+
+template <bool F16>
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+template <bool F16>
+__device__ __forceinline__ uint16_t to16(float x) {
+  if constexpr (F16)
+    return f32_to_f16(x);
+  else
+    return f32_to_bf16(x);
+}
+template <bool F16>
+__device__ __forceinline__ float from16(uint16_t h) {
+  if constexpr (F16)
+    return f16_to_f32(h);
+  else
+    return bf16_to_f32(h);
+}
+
+template <bool F16, int DH>
+__global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
+  constexpr int KS = DH / 32;         // 32-deep k steps of Q K^T
+  constexpr int DT = DH / 16;         // 16-dim tiles of the output
+  constexpr int KROW = DH + 8;        // LDS row of the K tile (elements), padded
+  constexpr int VROW = AT_K + 8;      // LDS row of the transposed V tile (elements)
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[AT_K * KROW];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[DH * VROW];
+
+  // Workgroup -> (block, sequence, head, query tile).
+  int w = blockIdx.x;
+  const int qt = w % a.qtiles;
+  w /= a.qtiles;
+  const int head = w % a.heads;
+  w /= a.heads;
+  const int nseq = a.T / a.seq_len;
+  const int seq = w % nseq;
+  const int blk = w / nseq;
+  const long long row0 = (long long)blk * a.T + (long long)seq * a.seq_len;  // first row of the sequence
+  const int col0 = head * DH;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int q0 = qt * AT_Q;                // first query of the tile (within the sequence)
+  const int myq = q0 + wave * 16 + l16;    // this lane's query
+  const int myq_c = min(myq, a.seq_len - 1);
+
+  // The wave's Q rows as the B operand of S^T = K Q^T (k = head dims).
+  bf16x8 qf[KS];
+  {
+    const uint16_t* qp = (const uint16_t*)a.Q + (size_t)(row0 + myq_c) * a.d + col0 + 8 * g;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) qf[kk] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + 32 * kk));
+  }
+
+  f32x4 o[DT];
+#pragma unroll
+  for (int t = 0; t < DT; ++t) o[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  float mrow = -1e30f;  // running max of this lane's query (log2 units)
+  float lsum = 0.f;     // this lane's part of the running sum
+
+  const int kend = min(a.seq_len, q0 + AT_Q);  // keys beyond the tile's last query are never seen
+  for (int k0 = 0; k0 < kend; k0 += AT_K) {
+    __syncthreads();  // the previous tile has been consumed
+    // K tile rows and the transposed V tile; rows past the sequence are clamped
+    // to its last row (their keys are masked below).
+    for (int x = tid; x < AT_K * (DH / 8); x += 256) {
+      const int kr = x / (DH / 8), c8 = (x % (DH / 8)) * 8;
+      const int key = min(k0 + kr, a.seq_len - 1);
+      const size_t gi = (size_t)(row0 + key) * a.d + col0 + c8;
+      *(u32x4*)&Ks[kr * KROW + c8] = *(const u32x4*)((const uint16_t*)a.K + gi);
+      const u32x4 vv = *(const u32x4*)((const uint16_t*)a.V + gi);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        Vt[(c8 + 2 * e) * VROW + kr] = (uint16_t)vv[e];
+        Vt[(c8 + 2 * e + 1) * VROW + kr] = (uint16_t)(vv[e] >> 16);
+      }
+    }
+    __syncthreads();
+
+    // S^T for 4 key subtiles of 16: st[t][i] = key k0 + 16 t + 4 g + i, query myq.
+    f32x4 st[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      st[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const bf16x8 kf = *(const bf16x8*)&Ks[(16 * t + l16) * KROW + 32 * kk + 8 * g];
+        st[t] = mfma16<F16>(kf, qf[kk], st[t]);
+      }
+    }
+    // Scale to log2 units, mask keys after the query (and past the sequence).
+    float tmax = -1e30f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = k0 + 16 * t + 4 * g + i;
+        const float sv = key <= myq ? st[t][i] * a.scale_log2 : -INFINITY;
+        st[t][i] = sv;
+        tmax = fmaxf(tmax, sv);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float mnew = fmaxf(mrow, tmax);
+    const float alpha = exp2f(mrow - mnew);
+    mrow = mnew;
+    lsum *= alpha;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) o[t] *= alpha;
+    // P = 2^(s - m + 12) as hi + lo 16-bit pairs in the B-operand order of the P V MFMA.
+    uint32_t ph[4][2], pl[4][2];
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; i += 2) {
+        const float p0 = exp2f(st[t][i] - mnew + 12.f), p1 = exp2f(st[t][i + 1] - mnew + 12.f);
+        lsum += p0 + p1;
+        const uint16_t h0 = to16<F16>(p0), h1 = to16<F16>(p1);
+        ph[t][i / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        pl[t][i / 2] = (uint32_t)to16<F16>(p0 - from16<F16>(h0)) |
+                       ((uint32_t)to16<F16>(p1 - from16<F16>(h1)) << 16);
+      }
+    // O^T += V^T P^T over two 32-key chunks c (subtiles 2c and 2c+1): lane group g's
+    // k slots are keys 32c + 4g + (0..3) and 32c + 16 + 4g + (0..3).
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const bf16x8 bh = __builtin_bit_cast(
+          bf16x8, (u32x4){ph[2 * c][0], ph[2 * c][1], ph[2 * c + 1][0], ph[2 * c + 1][1]});
+      const bf16x8 bl = __builtin_bit_cast(
+          bf16x8, (u32x4){pl[2 * c][0], pl[2 * c][1], pl[2 * c + 1][0], pl[2 * c + 1][1]});
+#pragma unroll
+      for (int t = 0; t < DT; ++t) {
+        const uint16_t* vr = &Vt[(16 * t + l16) * VROW + 32 * c + 4 * g];
+        const u32x2 v0 = *(const u32x2*)vr, v1 = *(const u32x2*)(vr + 16);
+        const bf16x8 af = __builtin_bit_cast(bf16x8, (u32x4){v0[0], v0[1], v1[0], v1[1]});
+        o[t] = mfma16<F16>(af, bh, o[t]);
+        o[t] = mfma16<F16>(af, bl, o[t]);
+      }
+    }
+  }
+  // Normalise by the row sum (over the 4 lane groups) and store dims 16 t + 4 g .. +3.
+  float l = lsum + __shfl_xor(lsum, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (myq >= a.seq_len) return;
+  const float inv = 1.f / l;
+  uint16_t* op = (uint16_t*)a.O + (size_t)(row0 + myq) * a.d + col0 + 4 * g;
+#pragma unroll
+  for (int t = 0; t < DT; ++t) {
+    const float y0 = o[t][0] * inv, y1 = o[t][1] * inv, y2 = o[t][2] * inv, y3 = o[t][3] * inv;
+    const u32x2 pk = F16 ? (u32x2){pack_f16x2(y0, y1), pack_f16x2(y2, y3)}
+                         : (u32x2){pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
+    *(u32x2*)(op + 16 * t) = pk;
+  }
+}
+
+}  // namespace
+
+int zo_layernorm_launch(long long rows, int d, int dtype, const void* X, const float* gamma,
+                        const float* beta, float eps_ln, void* Y, hipStream_t stream) {
+  if (rows <= 0) return ZO_OK;
+  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  if (dtype == ZO_BF16)
+    hipLaunchKernelGGL(k_layernorm<ZO_BF16>, grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  else if (dtype == ZO_F16)
+    hipLaunchKernelGGL(k_layernorm<ZO_F16>, grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  else
+    hipLaunchKernelGGL(k_layernorm<ZO_F32>, grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  return zo_hip_status(hipGetLastError(), "k_layernorm");
+}
+
+int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int dtype, const void* Q,
+                        const void* K, const void* V, void* O, hipStream_t stream) {
+  AttnArgs a;
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.O = O;
+  a.T = T;
+  a.seq_len = seq_len;
+  a.d = d;
+  a.heads = heads;
+  a.qtiles = (seq_len + AT_Q - 1) / AT_Q;
+  const int dh = d / heads;
+  a.scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
+  const long long wg = (long long)nblk * (T / seq_len) * heads * a.qtiles;
+  if (wg <= 0) return ZO_OK;
+  if (wg > 0x7fffffffLL) {
+    zo_set_error("attention: too many workgroups (%lld)", wg);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  const dim3 grid((unsigned)wg), block(256);
+  const bool f16 = dtype == ZO_F16;
+  if (dh == 64) {
+    if (f16)
+      hipLaunchKernelGGL((k_attention<true, 64>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((k_attention<false, 64>), grid, block, 0, stream, a);
+  } else {
+    if (f16)
+      hipLaunchKernelGGL((k_attention<true, 128>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((k_attention<false, 128>), grid, block, 0, stream, a);
+  }
+  return zo_hip_status(hipGetLastError(), "k_attention");
+}

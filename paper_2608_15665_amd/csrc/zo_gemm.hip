@@ -60,6 +60,9 @@ struct GemmArgs {
   void* Y;                    // per block rows_b x ldy
   long long y_block_stride;
   int ldy, out_dtype;          // zo_dtype of Y
+  int epi;                     // zo_epilogue
+  const void* R;               // ZO_EPI_RESIDUAL: added to Y, same type and layout (ldy)
+  long long r_block_stride;    // elements; 0 = one R shared by all blocks
   int tiles_a, tiles_b, total_tiles;
 };
 
@@ -75,15 +78,58 @@ __device__ __forceinline__ void store4(char* base, size_t idx, float v0, float v
     *(f32x4*)(base + idx * 4) = (f32x4){v0, v1, v2, v3};
 }
 
-// The same with the output type chosen at run time (kernels with few accumulators).
-__device__ __forceinline__ void store4_rt(char* base, size_t idx, int out_dtype, float v0, float v1,
-                                          float v2, float v3) {
-  if (out_dtype == ZO_BF16)
-    store4<ZO_BF16>(base, idx, v0, v1, v2, v3);
-  else if (out_dtype == ZO_F16)
-    store4<ZO_F16>(base, idx, v0, v1, v2, v3);
+// Four OUT-typed values at element idx.. as fp32, added to v0..v3.
+template <int OUT>
+__device__ __forceinline__ void add4(const char* base, size_t idx, float& v0, float& v1, float& v2,
+                                     float& v3) {
+  if constexpr (OUT == ZO_F32) {
+    const f32x4 r = *(const f32x4*)(base + idx * 4);
+    v0 += r[0]; v1 += r[1]; v2 += r[2]; v3 += r[3];
+  } else {
+    const u32x2 r = *(const u32x2*)(base + idx * 2);
+    if constexpr (OUT == ZO_BF16) {
+      v0 += bf16_to_f32((bf16_t)r[0]); v1 += bf16_to_f32((bf16_t)(r[0] >> 16));
+      v2 += bf16_to_f32((bf16_t)r[1]); v3 += bf16_to_f32((bf16_t)(r[1] >> 16));
+    } else {
+      v0 += f16_to_f32((uint16_t)r[0]); v1 += f16_to_f32((uint16_t)(r[0] >> 16));
+      v2 += f16_to_f32((uint16_t)r[1]); v3 += f16_to_f32((uint16_t)(r[1] >> 16));
+    }
+  }
+}
+
+// The fused epilogue on four fp32 accumulator values, then the store: ReLU, or the
+// residual R (same layout as Y) added before the single rounding to OUT.
+template <int OUT, int EPI>
+__device__ __forceinline__ void finish4(char* Yb, const char* Rb, size_t idx, float v0, float v1,
+                                        float v2, float v3) {
+  if constexpr (EPI == ZO_EPI_RELU) {
+    v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f);
+  } else if constexpr (EPI == ZO_EPI_RESIDUAL) {
+    add4<OUT>(Rb, idx, v0, v1, v2, v3);
+  }
+  store4<OUT>(Yb, idx, v0, v1, v2, v3);
+}
+
+// The same with the output type and epilogue chosen at run time (kernels with few
+// accumulators live).
+template <int OUT>
+__device__ __forceinline__ void finish4_epi(char* Yb, const char* Rb, size_t idx, int epi, float v0,
+                                            float v1, float v2, float v3) {
+  if (epi == ZO_EPI_RELU)
+    finish4<OUT, ZO_EPI_RELU>(Yb, Rb, idx, v0, v1, v2, v3);
+  else if (epi == ZO_EPI_RESIDUAL)
+    finish4<OUT, ZO_EPI_RESIDUAL>(Yb, Rb, idx, v0, v1, v2, v3);
   else
-    store4<ZO_F32>(base, idx, v0, v1, v2, v3);
+    finish4<OUT, ZO_EPI_NONE>(Yb, Rb, idx, v0, v1, v2, v3);
+}
+__device__ __forceinline__ void finish4_rt(char* Yb, const char* Rb, size_t idx, int out_dtype,
+                                           int epi, float v0, float v1, float v2, float v3) {
+  if (out_dtype == ZO_BF16)
+    finish4_epi<ZO_BF16>(Yb, Rb, idx, epi, v0, v1, v2, v3);
+  else if (out_dtype == ZO_F16)
+    finish4_epi<ZO_F16>(Yb, Rb, idx, epi, v0, v1, v2, v3);
+  else
+    finish4_epi<ZO_F32>(Yb, Rb, idx, epi, v0, v1, v2, v3);
 }
 
 // 32x32x16 MFMA on 16-byte fragments of eight 16-bit values: fp16 or bf16.
@@ -242,7 +288,9 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
   }
 
   // Store: lane holds token fr (+32j) and 4 adjacent output columns per a.
-  char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (a.out_dtype == ZO_F32 ? 4 : 2);
+  const int osz = a.out_dtype == ZO_F32 ? 4 : 2;
+  char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * osz;
+  const char* Rb = (const char*)a.R + (long long)blk * a.r_block_stride * osz;
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int tok = t0 + wn * TN * 32 + j * 32 + fr;
@@ -253,8 +301,8 @@ __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
       for (int q4 = 0; q4 < 4; ++q4) {
         const int col = m0 + wm * TM * 32 + i * 32 + q4 * 8 + fh * 4;
         if (col >= a.rows_a) continue;
-        store4_rt(Yb, (size_t)tok * a.ldy + col, a.out_dtype, acc[i][j][q4 * 4 + 0],
-                  acc[i][j][q4 * 4 + 1], acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
+        finish4_rt(Yb, Rb, (size_t)tok * a.ldy + col, a.out_dtype, a.epi, acc[i][j][q4 * 4 + 0],
+                   acc[i][j][q4 * 4 + 1], acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
       }
     }
   }
@@ -274,6 +322,9 @@ struct F32Args {
   float* Y;
   long long y_block_stride;
   int ldy;
+  int epi;                    // zo_epilogue
+  const float* R;             // ZO_EPI_RESIDUAL: added to Y (same layout)
+  long long r_block_stride;
 };
 
 __global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
@@ -326,6 +377,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
     }
   }
   float* Y = a.Y + (long long)blk * a.y_block_stride;
+  const float* R = a.R + (long long)blk * a.r_block_stride;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int tok = t0 + ty * 4 + i;
@@ -333,7 +385,11 @@ __global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int col = c0 + tx * 4 + j;
-      if (col < a.rows_a) Y[(size_t)tok * a.ldy + col] = acc[i][j];
+      if (col >= a.rows_a) continue;
+      float v = acc[i][j];
+      if (a.epi == ZO_EPI_RELU) v = fmaxf(v, 0.f);
+      if (a.epi == ZO_EPI_RESIDUAL) v += R[(size_t)tok * a.ldy + col];
+      Y[(size_t)tok * a.ldy + col] = v;
     }
   }
 }
@@ -518,13 +574,13 @@ int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
 // from the last valid row (never stored).  F16: the main k-tiles run the fp16
 // MFMA and the correction k-tiles (bf16 hi/lo operands) the bf16 MFMA, as two
 // loops over the same body; the loads do not depend on the element type.
-// OUT (zo_dtype of Y) is a template parameter: with all 256 accumulators live,
-// one store path per instantiation keeps the epilogue free of per-store
-// branches (a run-time choice there made the compiler keep spilled VGPR
-// copies of the accumulators, one of which it stored wrongly).
+// OUT (zo_dtype of Y) and EPI (zo_epilogue) are template parameters: with all
+// 256 accumulators live, one store path per instantiation keeps the epilogue
+// free of per-store branches (a run-time choice there made the compiler keep
+// spilled VGPR copies of the accumulators, one of which it stored wrongly).
 __device__ __forceinline__ int g4(int r) { return ((r >> 2) ^ (r & 2)) & 3; }
 
-template <bool F16, int OUT>
+template <bool F16, int OUT, int EPI>
 __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   constexpr int STAGES = 4;
   constexpr int BM = 256, BN = 256, RB = 64;               // RB: bytes per LDS row (32 bf16)
@@ -652,6 +708,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain the tail loads before exit
 
   char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (OUT == ZO_F32 ? 4 : 2);
+  const char* Rb = (const char*)a.R + (long long)blk * a.r_block_stride * (OUT == ZO_F32 ? 4 : 2);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int tok = t0 + wn * 128 + j * 32 + fr;
@@ -662,11 +719,21 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
       for (int q4 = 0; q4 < 4; ++q4) {
         const int col = m0 + wm * 128 + i * 32 + q4 * 8 + fh * 4;
         if (col >= a.rows_a) continue;
-        store4<OUT>(Yb, (size_t)tok * a.ldy + col, acc[i][j][q4 * 4 + 0], acc[i][j][q4 * 4 + 1],
-                    acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
+        finish4<OUT, EPI>(Yb, Rb, (size_t)tok * a.ldy + col, acc[i][j][q4 * 4 + 0],
+                          acc[i][j][q4 * 4 + 1], acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
       }
     }
   }
+}
+
+template <bool F16, int OUT>
+void launch_main_epi(const GemmArgs& a, dim3 grid, hipStream_t stream) {
+  if (a.epi == ZO_EPI_RELU)
+    hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_RELU>), grid, dim3(256), 0, stream, a);
+  else if (a.epi == ZO_EPI_RESIDUAL)
+    hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_RESIDUAL>), grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_NONE>), grid, dim3(256), 0, stream, a);
 }
 
 int launch_gemm_main(GemmArgs a, bool f16, hipStream_t stream) {
@@ -679,16 +746,16 @@ int launch_gemm_main(GemmArgs a, bool f16, hipStream_t stream) {
     return ZO_ERR_UNSUPPORTED;
   }
   a.total_tiles = (int)total;
-  const dim3 grid(a.total_tiles), block(256);
+  const dim3 grid(a.total_tiles);
   if (a.out_dtype == ZO_F32) {
     if (f16)
-      hipLaunchKernelGGL((k_gemm_main<true, ZO_F32>), grid, block, 0, stream, a);
+      launch_main_epi<true, ZO_F32>(a, grid, stream);
     else
-      hipLaunchKernelGGL((k_gemm_main<false, ZO_F32>), grid, block, 0, stream, a);
+      launch_main_epi<false, ZO_F32>(a, grid, stream);
   } else if (f16) {
-    hipLaunchKernelGGL((k_gemm_main<true, ZO_F16>), grid, block, 0, stream, a);
+    launch_main_epi<true, ZO_F16>(a, grid, stream);
   } else {
-    hipLaunchKernelGGL((k_gemm_main<false, ZO_BF16>), grid, block, 0, stream, a);
+    launch_main_epi<false, ZO_BF16>(a, grid, stream);
   }
   return zo_hip_status(hipGetLastError(), "k_gemm_main");
 }
@@ -817,7 +884,7 @@ int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_
 }
 
 int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
-                     hipStream_t stream) {
+                     hipStream_t stream, int epi, const void* R, long long r_block_stride) {
   const PlinearWs w = zo_plinear_ws(p, ws);
   void* pp = w.pp;
   void* bp = w.bp;
@@ -840,6 +907,9 @@ int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y
     h.y_block_stride = (long long)p.T * p.m;
     h.ldy = p.m;
     h.out_dtype = p.out_dtype;
+    h.epi = epi;
+    h.R = R;
+    h.r_block_stride = r_block_stride;
     const bool f16 = p.in_dtype == ZO_F16;
     if (p.n % 32 == 0) return launch_gemm_main(h, f16, stream);
     return f16 ? launch_gemm_bf16<2, 4, 4, 2, true>(h, stream) : launch_gemm_bf16<2, 4, 4, 2, false>(h, stream);
@@ -859,6 +929,9 @@ int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y
   h.Y = (float*)Y;
   h.y_block_stride = (long long)p.T * p.m;
   h.ldy = p.m;
+  h.epi = epi;
+  h.R = (const float*)R;
+  h.r_block_stride = r_block_stride;
   dim3 grid((p.m + 63) / 64, (p.T + 63) / 64, p.nblk);
   hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, stream, h);
   return zo_hip_status(hipGetLastError(), "k_gemm_f32");

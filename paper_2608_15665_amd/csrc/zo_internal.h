@@ -124,8 +124,14 @@ int zo_lora_prepare(const PlinearPlan& p, int rl, int rs, const int* blk_query,
 int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
                        float eps, const void* X, const float* U, const float* V,
                        const float* Z, void* ws, hipStream_t stream);
+// Decoder-layer pieces (zo_decoder.hip).
+int zo_layernorm_launch(long long rows, int d, int dtype, const void* X, const float* gamma,
+                        const float* beta, float eps_ln, void* Y, hipStream_t stream);
+int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int dtype, const void* Q,
+                        const void* K, const void* V, void* O, hipStream_t stream);
 int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
-                     hipStream_t stream);
+                     hipStream_t stream, int epi = ZO_EPI_NONE, const void* R = nullptr,
+                     long long r_block_stride = 0);
 
 // Subspace update (zo_update.hip): Adam (sgd = 0) or plain SGD in the subspace (sgd = 1,
 // S = Zbar; the moments are neither read nor written).

@@ -198,3 +198,48 @@ def test_loss_validation():
     assert "dtype" in _detail()
     assert L.zo_combine_central(2, fake, 0.0, fake, None) == 1
     assert L.zo_sq_loss_workspace(2, 64, 256) > 0
+
+
+def test_decoder_entry_points_validation():
+    """Layer norm, attention, the fused-epilogue apply and the decoder layer reject bad
+    arguments before launching anything (no GPU touched)."""
+    L = zo.lib()
+    fake = 1 << 20
+    assert L.zo_layernorm(4, 12, 1, fake, fake, fake, 1e-5, fake, None) == 1 and "d % 8" in _detail()
+    assert L.zo_layernorm(4, 16, 5, fake, fake, fake, 1e-5, fake, None) == 1 and "dtype" in _detail()
+    assert L.zo_layernorm(4, 16, 1, fake, fake, fake, -1.0, fake, None) == 1 and "eps_ln" in _detail()
+    assert L.zo_layernorm(0, 16, 1, None, None, None, 1e-5, None, None) == 0  # nothing to do
+    assert L.zo_causal_attention(1, 100, 30, 256, 2, 1, fake, fake, fake, fake, None) == 1
+    assert "seq_len" in _detail()
+    assert L.zo_causal_attention(1, 128, 64, 256, 8, 1, fake, fake, fake, fake, None) == 2  # dh = 32
+    assert "head dim" in _detail()
+    assert L.zo_causal_attention(1, 128, 64, 256, 2, 0, fake, fake, fake, fake, None) == 2  # fp32
+    assert L.zo_causal_attention(1, 128, 64, 256, 2, 1, None, fake, fake, fake, None) == 1
+    # apply_ex: bad epilogue; residual without R; misaligned residual stride
+    bq = (ctypes.c_int * 2)(0, 0)
+    bs = (ctypes.c_int8 * 2)(1, -1)
+    need = L.zo_perturbed_linear_workspace(16, 32, 64, 4, 1, 2, 0, 1)
+    st = L.zo_perturbed_linear_apply_ex(16, 32, 64, 4, 1, 2, 1, fake, 0, fake, 1, fake, 7, None, 0, fake, need,
+                                        None)
+    assert st == 1 and "epilogue" in _detail()
+    st = L.zo_perturbed_linear_apply_ex(16, 32, 64, 4, 1, 2, 1, fake, 0, fake, 1, fake, 2, None, 0, fake, need,
+                                        None)
+    assert st == 1 and "NULL R" in _detail()
+    st = L.zo_perturbed_linear_apply_ex(16, 32, 64, 4, 1, 2, 1, fake, 0, fake, 1, fake, 2, fake, 514, fake, need,
+                                        None)
+    assert st == 1 and "r_block_stride" in _detail()
+    # decoder layer: sizes, dtype, block layout of H
+    assert L.zo_decoder_layer_workspace(128, 64, 256, 2, 512, 8, 2, 4, 1) > 0
+    assert L.zo_decoder_layer_workspace(128, 64, 256, 2, 512, 8, 2, 4, 2) > 0
+    assert L.zo_decoder_layer_workspace(128, 64, 256, 2, 512, 8, 2, 4, 0) == 0   # fp32: no attention kernel
+    assert L.zo_decoder_layer_workspace(128, 60, 256, 2, 512, 8, 2, 4, 1) == 0   # T % seq_len
+    assert L.zo_decoder_layer_workspace(128, 64, 256, 2, 500, 8, 2, 4, 1) == 0   # ffn % 8
+    layer = zo._lib.DecoderLayerDesc()
+    bq4 = (ctypes.c_int * 4)(0, 0, 1, 1)
+    bs4 = (ctypes.c_int8 * 4)(1, -1, 1, -1)
+    st = L.zo_decoder_layer_forward(128, 64, 256, 2, 512, 8, 2, 4, bq4, bs4, 1e-3, 1e-5, 1, fake, 0,
+                                    ctypes.byref(layer), fake, fake, 1 << 40, None)
+    assert st == 1 and "NULL" in _detail()  # the matrices of the layer are NULL
+    st = L.zo_decoder_layer_forward(128, 64, 256, 2, 512, 8, 2, 4, bq4, bs4, 1e-3, 1e-5, 1, fake, 5,
+                                    ctypes.byref(layer), fake, fake, 1 << 40, None)
+    assert st == 1 and "h_block_stride" in _detail()
