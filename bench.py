@@ -151,6 +151,175 @@ def cpu_baseline(cfg, seed, budget_s, mat, lora, r, f16=False):
                       f"{len(os.sched_getaffinity(0))} host cores visible"}
 
 
+def attention_flops(T, seq_len, heads, dh, nblk):
+    """Algorithmic FLOPs of causal attention per layer: q.k and p.v for the L(L+1)/2 visible
+    (query, key) pairs of each sequence and head, in every block."""
+    return nblk * (T // seq_len) * heads * 2 * 2 * dh * seq_len * (seq_len + 1) // 2
+
+
+def run_decoder(args):
+    """One SubZero+ step through real decoder layers: refresh (t mod F == 0), for every layer the
+    forward of all 2q blocks (zo_decoder_layer_forward: layer norm, the six perturbed linears
+    with fused ReLU / residuals, causal attention), the squared loss of the last hidden state
+    against a fixed target, the estimate, and the subspace Adam update of all 6 L matrices."""
+    import numpy as np
+    import torch
+
+    import paper_2608_15665_amd as zo
+    import zo_draws as zd
+
+    cfg = zd.CONFIGS[args.config]
+    dec = cfg.get("decoder")
+    if not dec:
+        print(f"bench.py: --model decoder needs an OPT-shaped config (got {args.config})", file=sys.stderr)
+        sys.exit(2)
+    T, r, q = cfg["T"], cfg["r"], cfg["q"]
+    if args.queries:
+        q = args.queries
+    if args.rank:
+        r = args.rank
+    d, heads, ffn, L = dec["d"], dec["heads"], dec["ffn"], dec["seq_len"]
+    layers = cfg["layers"]
+    forward = args.estimator == "forward"
+    if forward:
+        bq, bs = [0] + list(range(q)), [0] + [1] * q
+    else:
+        bq, bs = [b // 2 for b in range(2 * q)], [1 if b % 2 == 0 else -1 for b in range(2 * q)]
+    nblk = len(bq)
+    nsigned = sum(1 for v in bs if v != 0)
+    eps, lr, b1, b2, ea, F = cfg["eps"], cfg["lr"], cfg["beta1"], cfg["beta2"], cfg["eps_adam"], cfg["F"]
+    seed, dev = args.seed, "cuda"
+    f16 = args.dtype == "fp16"
+    dt16 = torch.float16 if f16 else torch.bfloat16
+    t_setup = time.perf_counter()
+
+    def to16(a64):
+        if f16:
+            return torch.from_numpy(zd.as_f16_values(a64)[0]).to(dev)
+        return torch.from_numpy(zd.bf16_bits(zd.f32(a64)).view(np.int16)).view(dt16).to(dev)
+
+    shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "fc1": (ffn, d), "fc2": (d, ffn)}
+    Wbase = {sh: to16(zd.draw(seed, "W0", sh, sh, 0.02)) for sh in set(shapes.values())}
+    rows_set = sorted({d, ffn})
+    Obase = {rw: torch.from_numpy(zd.f32(zd.draw(seed, "OMEGA_U", (rw, r), (rw, r)))).to(dev) for rw in rows_set}
+    nsteps = args.warmup + args.steps
+    mats, omegas, qouts, lns = [], [], [], []
+    for l in range(layers):
+        lm = {}
+        for nm, (m, n) in shapes.items():
+            idx = len(mats) * 6 + len(lm)
+            u = dict(W=torch.roll(Wbase[(m, n)], l, 0).contiguous(),
+                     U=torch.empty((m, r), dtype=torch.float32, device=dev),
+                     V=torch.empty((n, r), dtype=torch.float32, device=dev),
+                     M1=torch.zeros((r, r), dtype=torch.float32, device=dev),
+                     M2=torch.zeros((r, r), dtype=torch.float32, device=dev), m=m, n=n)
+            for key, rw in (("U", m), ("V", n)):
+                omegas.append(torch.roll(Obase[rw], 2 * idx + (key == "V"), 0).contiguous())
+                qouts.append(u[key])
+            lm[nm] = u
+        mats.append(lm)
+        g = torch.from_numpy(zd.f32(1.0 + 0.05 * zd.draw(seed, "W0", (l, 1), (4, d)))).to(dev)
+        lns.append(dict(ln1_gamma=g[0].contiguous(), ln1_beta=(g[1] - 1.0).contiguous(),
+                        ln2_gamma=g[2].contiguous(), ln2_beta=(g[3] - 1.0).contiguous()))
+    del Wbase, Obase
+    nmat = 6 * layers
+    Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(nmat)])
+                                   for t in range(nsteps)])).to(dev)  # [step, matrix, q, r, r]
+    H0 = to16(zd.draw(seed, "X", (T, d, 0), (T, d)))
+    Ystar = to16(zd.draw(seed, "X", (T, d, 1), (T, d)))
+    Hbuf = [torch.empty((nblk * T, d), dtype=dt16, device=dev) for _ in range(2)]
+
+    def layer_obj(t, l):
+        lm = {nm: dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, 6 * l + i]) for i, (nm, u) in enumerate(mats[l].items())}
+        return zo.DecoderLayer(lm, lns[l], bq, bs, eps, T, L, heads)
+
+    decs = [[layer_obj(t, l) for l in range(layers)] for t in range(nsteps)]
+    items = [[dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, 6 * l + i], M1=u["M1"], M2=u["M2"])
+              for l in range(layers) for i, u in enumerate(mats[l].values())] for t in range(nsteps)]
+    torch.cuda.synchronize()
+    log(f"setup {time.perf_counter() - t_setup:.1f} s; {layers} decoder layers; "
+        f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB on device")
+    Ev = lambda: torch.cuda.Event(enable_timing=True)
+    recs = []
+
+    def step(t, s):
+        rec = {"layers": [], "upd": None, "refresh": None}
+        if t % F == 0:
+            e0, e1 = Ev(), Ev()
+            e0.record()
+            zo.subspace_refresh(omegas, r, out=qouts)
+            e1.record()
+            rec["refresh"] = (e0, e1)
+        H = H0
+        for l in range(layers):
+            e0, e1 = Ev(), Ev()
+            e0.record()
+            H = decs[s][l](H, out=Hbuf[l % 2])
+            e1.record()
+            rec["layers"].append((e0, e1))
+        Lb = zo.sq_loss(H, Ystar, nblk, T)
+        g = zo.combine_forward(Lb, eps) if forward else zo.combine_central(Lb, eps)
+        e0, e1 = Ev(), Ev()
+        e0.record()
+        zo.subspace_adam_update(items[s], g, t + 1, lr, b1, b2, ea)
+        e1.record()
+        rec["upd"] = (e0, e1)
+        return rec
+
+    for s in range(args.warmup):
+        step(s, s)
+        torch.cuda.synchronize()
+        log(f"warmup step {s} done")
+    for lm in mats:
+        for u in lm.values():
+            u["M1"].zero_()
+            u["M2"].zero_()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        recs.append(step(k, args.warmup + k))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"timed {args.steps} steps in {t1 - t0:.2f} s")
+
+    lin_layer = sum(plinear_flops(T, m, n, r, q, nblk, nsigned) for m, n in shapes.values())
+    att_layer = attention_flops(T, L, heads, d // heads, nblk)
+    lin_step = lin_layer * layers
+    value = lin_step * args.steps / (t1 - t0) / 1e12
+    layer_ms = [a.elapsed_time(b) for rc in recs for a, b in rc["layers"]]
+    avg_layer = sum(layer_ms) / len(layer_ms)
+    achieved = (lin_layer + att_layer) / (avg_layer * 1e-3) / 1e12
+    upd_ms = sum(rc["upd"][0].elapsed_time(rc["upd"][1]) for rc in recs)
+    upd_bytes = sum(update_bytes(u["m"], u["n"], r, q) for lm in mats for u in lm.values()) * args.steps
+    upd_gbps = upd_bytes / (upd_ms * 1e-3) / 1e9
+    ref_ms = [rc["refresh"][0].elapsed_time(rc["refresh"][1]) for rc in recs if rc["refresh"]]
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round((t1 - t0) / args.steps * 1e3, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": args.dtype, "data": "synthetic",
+        "config": {"workload": (f"{args.config}-shaped decoder: {layers} pre-LN layers (d={d}, {heads} heads of "
+                                f"{d // heads}, ffn={ffn}, ReLU), every q, k, v, o, fc1, fc2 perturbed; "
+                                + (f"{nblk} blocks (baseline + q={q} forward queries)" if forward
+                                   else f"{nblk} query blocks (q={q}, +/-)")
+                                + f" of T={T} tokens ({T // L} sequences x {L}); r={r}; {args.dtype}; "
+                                  "value counts the perturbed-linear FLOPs of the step"),
+                   "layers": layers, "d": d, "heads": heads, "ffn": ffn, "seq_len": L, "T": T, "r": r, "q": q,
+                   "blocks": nblk, "estimator": args.estimator, "refresh_every": F},
+        "roofline": {"kernel": "zo_decoder_layer_forward (one layer: 2 layer norms, 6 fused perturbed GEMMs "
+                               "with their projections, causal attention)", "bound": "mfma",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "launches": len(layer_ms), "avg_launch_ms": round(avg_layer, 4),
+                     "flops_per_launch_avg": lin_layer + att_layer},
+        "attention_flops_per_layer": att_layer,
+        "update": {"kernel": "zo_subspace_adam_update (k_adam_rr + k_us + k_update_bf16)", "bound": "hbm",
+                   "achieved": round(upd_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                   "frac": round(upd_gbps / PEAK_HBM_GBPS, 4), "ms_per_step": round(upd_ms / args.steps, 3)},
+        "refresh_ms": round(ref_ms[0], 3) if ref_ms else None,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -163,6 +332,9 @@ def main():
     ap.add_argument("--rank", type=int, default=0, help="subspace rank r (default: the config's r)")
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "fp16"],
                     help="weights and activations (fp16: the paper's precision for OPT-13B)")
+    ap.add_argument("--model", default="stack", choices=["stack", "decoder"],
+                    help="stack: the perturbed linears of every matrix on synthetic activations; decoder: "
+                         "real pre-LN decoder-layer forwards (layer norm, causal attention, ReLU MLP, residuals)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -185,6 +357,9 @@ def main():
         return
     torch.cuda.set_device(0)
     zo.lib()
+    if args.model == "decoder":
+        run_decoder(args)
+        return
     cfg = zd.CONFIGS[args.config]
     lora = args.config.endswith("-lora")
     T, r, q = cfg["T"], cfg["r"], cfg["q"]

@@ -165,16 +165,17 @@ def z_draws(seed: int, t: int, mat: int, q: int, r: int) -> np.ndarray:
 # --------------------------------------------------------------------------
 # Model-shaped stacks (shapes only; weights are synthetic).
 # --------------------------------------------------------------------------
-def _stack(name, layers, mats, T, r, q, eps=1e-3, lr=1e-3, F=100, beta1=0.9, beta2=0.95):
+def _stack(name, layers, mats, T, r, q, eps=1e-3, lr=1e-3, F=100, beta1=0.9, beta2=0.95, decoder=None):
     return dict(name=name, layers=layers, mats=mats, T=T, r=r, q=q, eps=eps, lr=lr,
-                F=F, beta1=beta1, beta2=beta2, eps_adam=1e-8)
+                F=F, beta1=beta1, beta2=beta2, eps_adam=1e-8, decoder=decoder)
 
 
 CONFIGS = {
     "opt-1.3b": _stack("opt-1.3b", 24,
                        [("q", 2048, 2048), ("k", 2048, 2048), ("v", 2048, 2048),
                         ("o", 2048, 2048), ("fc1", 8192, 2048), ("fc2", 2048, 8192)],
-                       T=4096, r=16, q=4, F=500),
+                       T=4096, r=16, q=4, F=500,
+                       decoder=dict(d=2048, heads=32, ffn=8192, seq_len=256)),   # 16 sequences x 256
     "llama-7b": _stack("llama-7b", 32,
                        [("q", 4096, 4096), ("k", 4096, 4096), ("v", 4096, 4096),
                         ("o", 4096, 4096), ("gate", 11008, 4096), ("up", 11008, 4096),
@@ -183,7 +184,8 @@ CONFIGS = {
     "opt-13b": _stack("opt-13b", 40,
                       [("q", 5120, 5120), ("k", 5120, 5120), ("v", 5120, 5120),
                        ("o", 5120, 5120), ("fc1", 20480, 5120), ("fc2", 5120, 20480)],
-                      T=8192, r=64, q=8),
+                      T=8192, r=64, q=8,
+                      decoder=dict(d=5120, heads=40, ffn=20480, seq_len=512)),  # batch 16 x 512
     # LoRA on q and v of a frozen base; each factor has its own r=4 subspace.
     "qwen-32b-lora": _stack("qwen-32b-lora", 64,
                             [("q", 5120, 5120), ("k", 1024, 5120), ("v", 1024, 5120),
