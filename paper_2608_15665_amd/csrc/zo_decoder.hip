@@ -12,9 +12,12 @@
 // one read and one write.  Statistics in fp32 with fixed-order wave sums.
 //
 // k_attention<F16, DH>: one workgroup (4 waves) per (block, sequence, head,
-// 64-query tile); keys in tiles of 64 through LDS, online softmax in fp32.
-// Each wave owns 16 queries and computes the transposed products, which keeps
-// every step in registers:
+// tile of 64 AT_NG queries); keys in tiles of 64 through LDS (loaded into
+// registers a tile ahead; V transposed in registers into four-key rows),
+// online softmax in fp32.  Each wave owns AT_NG groups of 16 queries that
+// share every K and V fragment it reads from LDS (one group measured faster
+// than two at head dim 128: two need 256 VGPRs, one wave per SIMD), and
+// computes the transposed products, which keeps every step in registers:
 //   S^T = K Q^T  (v_mfma_f32_16x16x32: A = K rows from LDS, B = the wave's Q
 //                 rows held in registers); lane (l16, g) of a 16 x 16 result
 //                 holds query l16 and keys 4g .. 4g+3, so a query's softmax
@@ -116,8 +119,9 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* __restrict__ X,
 }
 
 // ---------------------------------------------------------------- attention
-constexpr int AT_Q = 64;   // queries per workgroup (16 per wave)
-constexpr int AT_K = 64;   // keys per tile
+constexpr int AT_NG = 1;               // 16-query groups per wave
+constexpr int AT_Q = 64 * AT_NG;       // queries per workgroup (4 waves)
+constexpr int AT_K = 64;               // keys per tile
 
 struct AttnArgs {
   const void* Q;
@@ -152,12 +156,21 @@ __device__ __forceinline__ float from16(uint16_t h) {
     return bf16_to_f32(h);
 }
 
+// Element e (0..7) of eight 16-bit values packed in a u32x4.
+__device__ __forceinline__ uint32_t half_of(u32x4 v, int e) {
+  return (e & 1) ? (v[e >> 1] >> 16) : (v[e >> 1] & 0xffffu);
+}
+
 template <bool F16, int DH>
 __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
   constexpr int KS = DH / 32;         // 32-deep k steps of Q K^T
   constexpr int DT = DH / 16;         // 16-dim tiles of the output
   constexpr int KROW = DH + 8;        // LDS row of the K tile (elements), padded
-  constexpr int VROW = AT_K + 8;      // LDS row of the transposed V tile (elements)
+  constexpr int VROW = AT_K + 4;      // LDS row of the transposed V tile (elements)
+  constexpr int C8 = DH / 8;          // 16-byte chunks per head row
+  constexpr int KCH = AT_K * C8 / 256;    // K chunks per thread per tile
+  constexpr int VIT = (AT_K / 4) * C8;    // V items (4 keys x 8 dims) per tile
+  static_assert(KCH * 256 == AT_K * C8 && VIT <= 256, "tile / thread mismatch");
   __shared__ __attribute__((aligned(16))) uint16_t Ks[AT_K * KROW];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[DH * VROW];
 
@@ -174,116 +187,168 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
   const int col0 = head * DH;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
-  const int q0 = qt * AT_Q;                // first query of the tile (within the sequence)
-  const int myq = q0 + wave * 16 + l16;    // this lane's query
-  const int myq_c = min(myq, a.seq_len - 1);
+  const int q0 = qt * AT_Q;  // first query of the tile (within the sequence)
+  const uint16_t* __restrict__ Kg = (const uint16_t*)a.K;
+  const uint16_t* __restrict__ Vg = (const uint16_t*)a.V;
 
-  // The wave's Q rows as the B operand of S^T = K Q^T (k = head dims).
-  bf16x8 qf[KS];
-  {
-    const uint16_t* qp = (const uint16_t*)a.Q + (size_t)(row0 + myq_c) * a.d + col0 + 8 * g;
+  // This lane's queries (one per group) and their rows as B operands of S^T = K Q^T.
+  int myq[AT_NG];
+  bf16x8 qf[AT_NG][KS];
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) qf[kk] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + 32 * kk));
+  for (int gq = 0; gq < AT_NG; ++gq) {
+    myq[gq] = q0 + wave * 16 * AT_NG + 16 * gq + l16;
+    const int qc = min(myq[gq], a.seq_len - 1);
+    const uint16_t* qp = (const uint16_t*)a.Q + (size_t)(row0 + qc) * a.d + col0 + 8 * g;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+      qf[gq][kk] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + 32 * kk));
   }
 
-  f32x4 o[DT];
+  f32x4 o[AT_NG][DT];
+  float mrow[AT_NG], lsum[AT_NG];
 #pragma unroll
-  for (int t = 0; t < DT; ++t) o[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  float mrow = -1e30f;  // running max of this lane's query (log2 units)
-  float lsum = 0.f;     // this lane's part of the running sum
+  for (int gq = 0; gq < AT_NG; ++gq) {
+#pragma unroll
+    for (int t = 0; t < DT; ++t) o[gq][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    mrow[gq] = -1e30f;  // running max (log2 units)
+    lsum[gq] = 0.f;     // this lane's part of the running sum
+  }
 
-  const int kend = min(a.seq_len, q0 + AT_Q);  // keys beyond the tile's last query are never seen
-  for (int k0 = 0; k0 < kend; k0 += AT_K) {
-    __syncthreads();  // the previous tile has been consumed
-    // K tile rows and the transposed V tile; rows past the sequence are clamped
-    // to its last row (their keys are masked below).
-    for (int x = tid; x < AT_K * (DH / 8); x += 256) {
-      const int kr = x / (DH / 8), c8 = (x % (DH / 8)) * 8;
-      const int key = min(k0 + kr, a.seq_len - 1);
-      const size_t gi = (size_t)(row0 + key) * a.d + col0 + c8;
-      *(u32x4*)&Ks[kr * KROW + c8] = *(const u32x4*)((const uint16_t*)a.K + gi);
-      const u32x4 vv = *(const u32x4*)((const uint16_t*)a.V + gi);
+  // K and V tiles are loaded into registers a tile ahead.  K: chunk x = tid + 256 c is key
+  // x / C8, dims 8 (x % C8).  V: item tid (< VIT) is keys 4 (tid / C8) .. +3, dims
+  // 8 (tid % C8) .. +7, transposed in registers into four-key rows of Vt.  Rows past the
+  // sequence are clamped to its last row (their keys are masked).
+  u32x4 kreg[KCH], vreg[4];
+  auto load_tile = [&](int k0) {
+#pragma unroll
+    for (int c = 0; c < KCH; ++c) {
+      const int x = tid + 256 * c;
+      const int key = min(k0 + x / C8, a.seq_len - 1);
+      kreg[c] = *(const u32x4*)(Kg + (size_t)(row0 + key) * a.d + col0 + 8 * (x % C8));
+    }
+    if (tid < VIT) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        Vt[(c8 + 2 * e) * VROW + kr] = (uint16_t)vv[e];
-        Vt[(c8 + 2 * e + 1) * VROW + kr] = (uint16_t)(vv[e] >> 16);
+        const int key = min(k0 + 4 * (tid / C8) + e, a.seq_len - 1);
+        vreg[e] = *(const u32x4*)(Vg + (size_t)(row0 + key) * a.d + col0 + 8 * (tid % C8));
       }
     }
-    __syncthreads();
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int c = 0; c < KCH; ++c) {
+      const int x = tid + 256 * c;
+      *(u32x4*)&Ks[(x / C8) * KROW + 8 * (x % C8)] = kreg[c];
+    }
+    if (tid < VIT) {
+      const int kb = 4 * (tid / C8), db = 8 * (tid % C8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t lo = half_of(vreg[0], e) | (half_of(vreg[1], e) << 16);
+        const uint32_t hi = half_of(vreg[2], e) | (half_of(vreg[3], e) << 16);
+        *(u32x2*)&Vt[(db + e) * VROW + kb] = (u32x2){lo, hi};
+      }
+    }
+  };
 
-    // S^T for 4 key subtiles of 16: st[t][i] = key k0 + 16 t + 4 g + i, query myq.
-    f32x4 st[4];
+  const int kend = min(a.seq_len, q0 + AT_Q);  // keys beyond the tile's last query are never seen
+  load_tile(0);
+  for (int k0 = 0; k0 < kend; k0 += AT_K) {
+    __syncthreads();  // the previous tile has been consumed
+    store_tile();
+    __syncthreads();
+    if (k0 + AT_K < kend) load_tile(k0 + AT_K);
+
+    // S^T for 4 key subtiles of 16: st[gq][t][i] = key k0 + 16 t + 4 g + i, query myq[gq].
+    f32x4 st[AT_NG][4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      st[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int gq = 0; gq < AT_NG; ++gq) st[gq][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
         const bf16x8 kf = *(const bf16x8*)&Ks[(16 * t + l16) * KROW + 32 * kk + 8 * g];
-        st[t] = mfma16<F16>(kf, qf[kk], st[t]);
+#pragma unroll
+        for (int gq = 0; gq < AT_NG; ++gq) st[gq][t] = mfma16<F16>(kf, qf[gq][kk], st[gq][t]);
       }
     }
-    // Scale to log2 units, mask keys after the query (and past the sequence).
-    float tmax = -1e30f;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = k0 + 16 * t + 4 * g + i;
-        const float sv = key <= myq ? st[t][i] * a.scale_log2 : -INFINITY;
-        st[t][i] = sv;
-        tmax = fmaxf(tmax, sv);
-      }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(mrow, tmax);
-    const float alpha = exp2f(mrow - mnew);
-    mrow = mnew;
-    lsum *= alpha;
-#pragma unroll
-    for (int t = 0; t < DT; ++t) o[t] *= alpha;
+    // Scale to log2 units, mask keys after the query (and past the sequence), online softmax,
     // P = 2^(s - m + 12) as hi + lo 16-bit pairs in the B-operand order of the P V MFMA.
-    uint32_t ph[4][2], pl[4][2];
+    uint32_t ph[AT_NG][4][2], pl[AT_NG][4][2];
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int gq = 0; gq < AT_NG; ++gq) {
+      float tmax = -1e30f;
 #pragma unroll
-      for (int i = 0; i < 4; i += 2) {
-        const float p0 = exp2f(st[t][i] - mnew + 12.f), p1 = exp2f(st[t][i + 1] - mnew + 12.f);
-        lsum += p0 + p1;
-        const uint16_t h0 = to16<F16>(p0), h1 = to16<F16>(p1);
-        ph[t][i / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        pl[t][i / 2] = (uint32_t)to16<F16>(p0 - from16<F16>(h0)) |
-                       ((uint32_t)to16<F16>(p1 - from16<F16>(h1)) << 16);
-      }
-    // O^T += V^T P^T over two 32-key chunks c (subtiles 2c and 2c+1): lane group g's
-    // k slots are keys 32c + 4g + (0..3) and 32c + 16 + 4g + (0..3).
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = k0 + 16 * t + 4 * g + i;
+          const float sv = key <= myq[gq] ? st[gq][t][i] * a.scale_log2 : -INFINITY;
+          st[gq][t][i] = sv;
+          tmax = fmaxf(tmax, sv);
+        }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      const float mnew = fmaxf(mrow[gq], tmax);
+      const float alpha = exp2f(mrow[gq] - mnew);
+      mrow[gq] = mnew;
+      lsum[gq] *= alpha;
+#pragma unroll
+      for (int t = 0; t < DT; ++t) o[gq][t] *= alpha;
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; i += 2) {
+          const float p0 = exp2f(st[gq][t][i] - mnew + 12.f), p1 = exp2f(st[gq][t][i + 1] - mnew + 12.f);
+          lsum[gq] += p0 + p1;
+          const uint16_t h0 = to16<F16>(p0), h1 = to16<F16>(p1);
+          ph[gq][t][i / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+          pl[gq][t][i / 2] = (uint32_t)to16<F16>(p0 - from16<F16>(h0)) |
+                             ((uint32_t)to16<F16>(p1 - from16<F16>(h1)) << 16);
+        }
+    }
+    // O^T += V^T P^T over two 32-key chunks c (subtiles 2c and 2c+1): lane group g's k slots
+    // are keys 32c + 4g + (0..3) and 32c + 16 + 4g + (0..3).  Each V^T fragment serves both
+    // query groups.
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const bf16x8 bh = __builtin_bit_cast(
-          bf16x8, (u32x4){ph[2 * c][0], ph[2 * c][1], ph[2 * c + 1][0], ph[2 * c + 1][1]});
-      const bf16x8 bl = __builtin_bit_cast(
-          bf16x8, (u32x4){pl[2 * c][0], pl[2 * c][1], pl[2 * c + 1][0], pl[2 * c + 1][1]});
+      bf16x8 bh[AT_NG], bl[AT_NG];
+#pragma unroll
+      for (int gq = 0; gq < AT_NG; ++gq) {
+        bh[gq] = __builtin_bit_cast(bf16x8, (u32x4){ph[gq][2 * c][0], ph[gq][2 * c][1], ph[gq][2 * c + 1][0],
+                                                    ph[gq][2 * c + 1][1]});
+        bl[gq] = __builtin_bit_cast(bf16x8, (u32x4){pl[gq][2 * c][0], pl[gq][2 * c][1], pl[gq][2 * c + 1][0],
+                                                    pl[gq][2 * c + 1][1]});
+      }
 #pragma unroll
       for (int t = 0; t < DT; ++t) {
         const uint16_t* vr = &Vt[(16 * t + l16) * VROW + 32 * c + 4 * g];
         const u32x2 v0 = *(const u32x2*)vr, v1 = *(const u32x2*)(vr + 16);
         const bf16x8 af = __builtin_bit_cast(bf16x8, (u32x4){v0[0], v0[1], v1[0], v1[1]});
-        o[t] = mfma16<F16>(af, bh, o[t]);
-        o[t] = mfma16<F16>(af, bl, o[t]);
+#pragma unroll
+        for (int gq = 0; gq < AT_NG; ++gq) {
+          o[gq][t] = mfma16<F16>(af, bh[gq], o[gq][t]);
+          o[gq][t] = mfma16<F16>(af, bl[gq], o[gq][t]);
+        }
       }
     }
   }
-  // Normalise by the row sum (over the 4 lane groups) and store dims 16 t + 4 g .. +3.
-  float l = lsum + __shfl_xor(lsum, 16, 64);
-  l += __shfl_xor(l, 32, 64);
-  if (myq >= a.seq_len) return;
-  const float inv = 1.f / l;
-  uint16_t* op = (uint16_t*)a.O + (size_t)(row0 + myq) * a.d + col0 + 4 * g;
+  // Normalise by the row sums (over the 4 lane groups) and store dims 16 t + 4 g .. +3.
 #pragma unroll
-  for (int t = 0; t < DT; ++t) {
-    const float y0 = o[t][0] * inv, y1 = o[t][1] * inv, y2 = o[t][2] * inv, y3 = o[t][3] * inv;
-    const u32x2 pk = F16 ? (u32x2){pack_f16x2(y0, y1), pack_f16x2(y2, y3)}
-                         : (u32x2){pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
-    *(u32x2*)(op + 16 * t) = pk;
+  for (int gq = 0; gq < AT_NG; ++gq) {
+    float l = lsum[gq] + __shfl_xor(lsum[gq], 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    if (myq[gq] >= a.seq_len) continue;
+    const float inv = 1.f / l;
+    uint16_t* op = (uint16_t*)a.O + (size_t)(row0 + myq[gq]) * a.d + col0 + 4 * g;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) {
+      const float y0 = o[gq][t][0] * inv, y1 = o[gq][t][1] * inv;
+      const float y2 = o[gq][t][2] * inv, y3 = o[gq][t][3] * inv;
+      const u32x2 pk = F16 ? (u32x2){pack_f16x2(y0, y1), pack_f16x2(y2, y3)}
+                           : (u32x2){pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
+      *(u32x2*)(op + 16 * t) = pk;
+    }
   }
 }
 
