@@ -243,3 +243,14 @@ def test_decoder_entry_points_validation():
     st = L.zo_decoder_layer_forward(128, 64, 256, 2, 512, 8, 2, 4, bq4, bs4, 1e-3, 1e-5, 1, fake, 5,
                                     ctypes.byref(layer), fake, fake, 1 << 40, None)
     assert st == 1 and "h_block_stride" in _detail()
+
+
+def test_empty_calls_are_no_ops():
+    """count = 0 refreshes and updates, and zero-row layer norms, succeed without launching."""
+    L = zo.lib()
+    fake = 1 << 20
+    assert L.zo_subspace_refresh(0, None, 4, None, None, 0, None) == 0
+    assert L.zo_subspace_refresh_workspace(0, None, 4) == 0
+    assert L.zo_subspace_adam_update(0, None, 1, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, None, 0, None) == 0
+    assert L.zo_subspace_sgd_update(0, None, 1, 4, 2, fake, 1e-2, None, None, 0, None) == 0
+    assert L.zo_layernorm(0, 64, 1, None, None, None, 1e-5, None, None) == 0

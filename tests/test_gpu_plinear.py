@@ -251,3 +251,34 @@ def test_prepare_apply_equals_one_call(dt):
     Y = pl.apply()
     torch.cuda.synchronize()
     assert np.array_equal(host(Y).reshape(one.shape), one)
+
+
+def test_max_blocks_and_queries():
+    """ZO_MAX_BLOCKS blocks over ZO_MAX_QUERIES queries (every block's query and sign decoded
+    from the per-call table), small T; every block against the oracle."""
+    T, m, n, r = 16, 64, 128, 4
+    nblk = zo.ZO_MAX_BLOCKS
+    q = 256
+    c = make_case(T, m, n, r, q, nblk, False, bf16=True)
+    c["bq"] = [(7 * b) % q for b in range(nblk)]
+    c["bs"] = [(1, -1, 0)[b % 3] for b in range(nblk)]
+    Y = run_gpu(c, 1e-1, out_dtype=torch.float32)
+    ref = run_oracle(c, 1e-1)
+    for b in range(nblk):
+        assert ferr(Y[b], ref[b], 1.0) <= 1e-4, b
+
+
+def test_forward_difference_layout_at_paper_k():
+    """The paper's K = 99 queries with a baseline block (nblk = 100: block 0 unperturbed, block
+    1 + k query k with sign +), as the forward estimator of Eq. 6 lays them out."""
+    T, m, n, r, q = 32, 128, 256, 8, 99
+    nblk = q + 1
+    c = make_case(T, m, n, r, q, nblk, True, bf16=True)
+    c["bq"] = [0] + list(range(q))
+    c["bs"] = [0] + [1] * q
+    Y = run_gpu(c, 1e-3, out_dtype=torch.float32)
+    ref = run_oracle(c, 1e-3)
+    for b in range(nblk):
+        assert ferr(Y[b], ref[b], 1.0) <= 1e-4, b
+    # the baseline block is the plain product X W^T
+    np.testing.assert_allclose(Y[0], c["X0v"] @ c["Wv"].T, rtol=0, atol=1e-4 * np.abs(Y[0]).max())

@@ -272,3 +272,15 @@ def test_sgd_update_without_moments_and_nonfinite_guard():
     torch.cuda.synchronize()
     ref = oracle.subspace_sgd_update(it["Wv"], it["U"], it["V"], it["Z"], g.astype(np.float64), F32(1e-2))
     assert ferr(host(dev["w_f32_out"]), ref["W"], 1.0) <= 5e-5
+
+
+def test_max_queries_aggregate():
+    """q = ZO_MAX_QUERIES coefficient matrices aggregated with their global estimates (Eq. 6)."""
+    m, n, r, q = 64, 128, 8, 256
+    it = make_item(31, (m, n, r), m, n, r, q, True, True)
+    g = zd.f32(zd.draw(31, "G", (m, n, r), (q,), 1e-2))
+    lr, b1, b2, ea = 1e-2, 0.9, 0.95, 1e-8
+    ref = expected(it, g.astype(np.float64), 2, lr, b1, b2, ea)
+    zo.subspace_adam_update([it["dev"]], dev_f32(g), 2, lr, b1, b2, ea)
+    torch.cuda.synchronize()
+    check_item(it, ref, True, lr)
