@@ -132,7 +132,7 @@ def cpu_baseline(cfg, seed, budget_s, mat, lora, r, f16=False):
         B = np.zeros((m, rl))
         UA, _ = np.linalg.qr(zd.draw(seed, "OMEGA_U", (1, rl), (rl, r)))
         VB, _ = np.linalg.qr(zd.draw(seed, "OMEGA_V", (1, rl), (rl, r)))
-    while time.perf_counter() - t0 < budget_s and nb < 64:
+    while time.perf_counter() - t0 < budget_s and nb < 4096:
         j, s = (nb // 2) % q, (1 if nb % 2 == 0 else -1)
         if lora:
             oracle.lora_perturbed_linear(X0, W, A, UA, V, Z[j], B, U, VB, Z[(j + 1) % q], s, 1e-3, scale)
