@@ -2,7 +2,11 @@
 // subspace SGD update it is compared with (S = Zbar, no moments; SubZero's own
 // update when q = 1).
 //
-// Three launches per chunk of up to ITEMS_PER_LAUNCH matrices:
+// One descriptor per matrix (Item) lives in the caller's workspace: small
+// k_fill_items launches copy FILL_ITEMS host descriptors each into that table
+// (kernel arguments only, nothing else touches host memory).  Then three
+// launches cover every matrix of the call at once, so the big update kernel
+// has one tail per call instead of one per group of matrices:
 //   k_adam_rr   256 entries of one matrix per workgroup: Zbar = (1/q) sum_j g_j Z_j,
 //               the two r x r moments (Eqs. 7-8) and the bias-corrected direction S
 //               (Eq. 9, Adam form), all in float64.  S and the new moments go to
@@ -32,11 +36,14 @@
 // stores in hardware, so the loop has no branches around memory operations
 // and the compiler can count the loads in flight exactly.  W is read NS steps
 // ahead and the next L chunk one chunk ahead.
+#include <vector>
+
 #include "zo_internal.h"
 
 namespace {
 
-constexpr int ITEMS_PER_LAUNCH = 16;
+constexpr int FILL_ITEMS = 16;           // descriptors per k_fill_items launch
+constexpr long long MAX_PASS_WG = 1 << 22; // workgroups per launch (x 256 threads < 2^32)
 constexpr int UPD_ROWS = 512;  // rows per workgroup
 constexpr int UPD_COLS = 256;  // columns per workgroup (4 waves x 64)
 constexpr int UPD_GROUP = 4;   // row chunks per raster group
@@ -44,18 +51,74 @@ constexpr int US_ROWS = 128;   // rows of L per k_us workgroup
 constexpr unsigned OOB = 0x80000000u;  // buffer offset beyond every descriptor used here
 constexpr int RSRC_CFG = 0x00020000;   // buffer descriptor word 3: 32-bit raw access
 
-struct ItemRR {
+// One matrix of the call.  Pointers marked (ws) are carved from the workspace.
+struct Item {
   const float* Z;
-  const float* M1;
-  const float* M2;
+  float* M1;        // moments: read by k_adam_rr, committed by k_us
+  float* M2;
   float* zbar_out;
-  double* S;    // workspace, r x r
-  float* M1n;   // workspace, r x r
-  float* M2n;   // workspace, r x r
-  int* flags;   // workspace, one per workgroup of the item
+  double* S;        // (ws) r x r
+  float* M1n;       // (ws) r x r
+  float* M2n;       // (ws) r x r
+  int* flags;       // (ws) one per k_adam_rr workgroup of the item
+  int* skip;        // (ws) set by k_us: the item had a non-finite entry
+  const float* U;
+  const float* V;
+  void* L;          // (ws) 16-bit W: m rows of [hi (rp) | lo (rp)] bf16; fp32 W: m x rp fp32
+  void* Vs;         // (ws) 16-bit W: hi then lo (2 x n x rp) bf16; unused for fp32 W
+  void* W;
+  float* wout;
+  int m, n;
+  int us_begin;     // first k_us workgroup of the item (over the whole call)
+  int l_tiles;      // k_us workgroups forming L (US_ROWS rows each); then V tiles (64 rows each)
+  int us_wg;        // all k_us workgroups of the item
+  int up_begin;     // first update workgroup of the item
+  int strips, rchunks;  // 16-bit W: 256-column strips x 512-row chunks
 };
+
+struct FillArgs {
+  Item it[FILL_ITEMS];
+  Item* dst;
+  int* us_begin;
+  int* up_begin;
+  int c0, cn;
+};
+
+// Copies one group of host descriptors (kernel arguments) into the workspace
+// table, one 32-bit word per thread, and fills the two workgroup-start arrays
+// searched by find_item.
+__global__ __launch_bounds__(256) void k_fill_items(FillArgs a) {
+  constexpr int WORDS = (int)(sizeof(Item) / 4);
+  static_assert(sizeof(Item) % 4 == 0, "Item must be a whole number of words");
+  const uint32_t* src = (const uint32_t*)a.it;
+  uint32_t* dst = (uint32_t*)(a.dst + a.c0);
+  for (int x = threadIdx.x; x < a.cn * WORDS; x += 256) dst[x] = src[x];
+  if (threadIdx.x < a.cn) {
+    a.us_begin[a.c0 + threadIdx.x] = a.it[threadIdx.x].us_begin;
+    a.up_begin[a.c0 + threadIdx.x] = a.it[threadIdx.x].up_begin;
+  }
+}
+
+// The item that workgroup b belongs to: the last k with begin[k] <= b
+// (begin is non-decreasing and begin[0] = 0 <= b).  A 64-way search: each
+// round one load per lane and a ballot, so 240 items take two rounds.
+__device__ __forceinline__ int find_item(const int* __restrict__ begin, int count, int b) {
+  const int lane = threadIdx.x & 63;
+  int lo = 0, len = count;
+  while (len > 64) {
+    const int step = (len + 63) >> 6;
+    const int off = lane * step;
+    const bool le = off < len && begin[lo + off] <= b;
+    const int c = __popcll(__ballot(le));
+    lo += (c - 1) * step;
+    len = min(step, len - (c - 1) * step);
+  }
+  const bool le = lane < len && begin[lo + lane] <= b;
+  return __builtin_amdgcn_readfirstlane(lo + __popcll(__ballot(le)) - 1);
+}
+
 struct RRArgs {
-  ItemRR it[ITEMS_PER_LAUNCH];
+  const Item* it;
   const float* g;
   int* nonfinite_flag;
   int r, q, aw;  // aw: workgroups per item
@@ -64,7 +127,7 @@ struct RRArgs {
 };
 
 __global__ __launch_bounds__(256) void k_adam_rr(RRArgs a) {
-  const ItemRR& it = a.it[blockIdx.x / a.aw];
+  const Item it = a.it[blockIdx.x / a.aw];
   const int w = blockIdx.x % a.aw;
   const int rr = a.r * a.r;
   const int e = w * 256 + threadIdx.x;
@@ -92,26 +155,11 @@ __global__ __launch_bounds__(256) void k_adam_rr(RRArgs a) {
   }
 }
 
-struct ItemUS {
-  const float* U;
-  const float* V;
-  const double* S;
-  const float* M1n;
-  const float* M2n;
-  float* M1;
-  float* M2;
-  const int* flags;
-  int* skip;
-  void* L;   // bf16: m rows of [hi (rp) | lo (rp)]; fp32: m x rp
-  void* Vs;  // bf16: hi then lo (2 x n x rp); unused for fp32
-  int m, n;
-  int wg_begin;  // first workgroup of this item in the launch
-  int l_tiles;   // workgroups forming L (US_ROWS rows each); then V tiles (64 rows each)
-  int n_wg;      // all workgroups of the item
-};
 struct USArgs {
-  ItemUS it[ITEMS_PER_LAUNCH];
+  const Item* it;
+  const int* begin;  // us_begin of every item
   int count, r, rp, bf16, aw, sgd;
+  int wg0;           // first workgroup of this launch over the whole call
   float lr;
 };
 
@@ -124,10 +172,9 @@ __global__ __launch_bounds__(256) void k_us(USArgs a) {
   constexpr int CPT = RP / 8;  // columns per thread
   __shared__ __attribute__((aligned(16))) float Ut[32][US_ROWS + 4];
   __shared__ __attribute__((aligned(16))) float Sl[32][RP];
-  int k = 0;
-  while (k + 1 < a.count && (int)blockIdx.x >= a.it[k + 1].wg_begin) ++k;
-  const ItemUS& it = a.it[k];
-  const int local = blockIdx.x - it.wg_begin;
+  const int b = a.wg0 + (int)blockIdx.x;
+  const Item it = a.it[find_item(a.begin, a.count, b)];
+  const int local = b - it.us_begin;
   const int r = a.r, tid = threadIdx.x;
   int bad = 0;
   for (int w = tid; w < a.aw; w += 256) bad |= it.flags[w];
@@ -136,7 +183,7 @@ __global__ __launch_bounds__(256) void k_us(USArgs a) {
   if (bad) return;
   const int rr = r * r;
   if (!a.sgd) {
-    for (int e = local * 256 + tid; e < rr; e += it.n_wg * 256) {
+    for (int e = local * 256 + tid; e < rr; e += it.us_wg * 256) {
       it.M1[e] = it.M1n[e];
       it.M2[e] = it.M2n[e];
     }
@@ -227,19 +274,12 @@ __global__ __launch_bounds__(256) void k_us(USArgs a) {
   }
 }
 
-struct ItemUpd {
-  void* W;
-  float* wout;
-  const void* L;
-  const void* Vs;  // bf16 path: split V; fp32 path: V itself (n x r)
-  const int* skip;
-  int m, n;
-  int strips, rchunks, wg_begin;  // bf16 path: 256-column strips x 512-row chunks
-};
 struct UpdArgs {
-  ItemUpd it[ITEMS_PER_LAUNCH];
+  const Item* it;
+  const int* begin;  // up_begin of every item
   int count, r, rp;
-  int total_wg;
+  int wg0;           // first workgroup of this launch over the whole call
+  int pass_wg;       // workgroups of this launch
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, unsigned bytes) {
@@ -286,14 +326,12 @@ __global__ __launch_bounds__(256) void k_update_bf16(UpdArgs a) {
   // at once then cover about 4 row chunks x 8 strips, so each chunk's L rows
   // (128 KB at r = 64) and each strip's V fragments (64 KB) come from its L2
   // after the first read, instead of once per workgroup.
-  const int w = blockIdx.x, nt = a.total_wg;
+  const int w = blockIdx.x, nt = a.pass_wg;
   const int xcd = w & 7, widx = w >> 3;
-  const int lt = xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
-  int k = 0;
-  while (k + 1 < a.count && lt >= a.it[k + 1].wg_begin) ++k;
-  const ItemUpd& it = a.it[k];
+  const int lt = a.wg0 + xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
+  const Item it = a.it[find_item(a.begin, a.count, lt)];
   if (*it.skip) return;
-  const int local = lt - it.wg_begin;
+  const int local = lt - it.up_begin;
   const int per_group = UPD_GROUP * it.strips;
   const int grp = local / per_group;
   const int gsize = min(UPD_GROUP, it.rchunks - grp * UPD_GROUP);
@@ -316,7 +354,8 @@ __global__ __launch_bounds__(256) void k_update_bf16(UpdArgs a) {
   bf16_t* Wt = (bf16_t*)it.W + (size_t)row0 * n;
   const __amdgpu_buffer_rsrc_t rw = rsrc(Wt, (unsigned)rows * n * 2);
   __amdgpu_buffer_rsrc_t ro = rw;
-  if (HOOK) ro = rsrc(it.wout + (size_t)row0 * n, (unsigned)rows * n * 4);
+  // Items without a hook buffer get an empty descriptor: their hook stores are dropped.
+  if (HOOK) ro = it.wout ? rsrc(it.wout + (size_t)row0 * n, (unsigned)rows * n * 4) : rsrc(Wt, 0u);
 
   // V fragments of the strip (B operand): column j = l16 of tile t is W column
   // col0 + 4 j + t.
@@ -432,15 +471,14 @@ __global__ __launch_bounds__(256) void k_update_bf16(UpdArgs a) {
 
 // fp32 W: one thread per weight, fp32 FMA over the r columns.
 __global__ __launch_bounds__(256) void k_update_f32(UpdArgs a) {
-  int k = 0;
-  while (k + 1 < a.count && (int)blockIdx.x >= a.it[k + 1].wg_begin) ++k;
-  const ItemUpd& it = a.it[k];
+  const int b = a.wg0 + (int)blockIdx.x;
+  const Item it = a.it[find_item(a.begin, a.count, b)];
   if (*it.skip) return;
-  const long long e = (long long)(blockIdx.x - it.wg_begin) * 256 + threadIdx.x;
+  const long long e = (long long)(b - it.up_begin) * 256 + threadIdx.x;
   if (e >= (long long)it.m * it.n) return;
   const int i = (int)(e / it.n), c = (int)(e % it.n);
   const float* L = (const float*)it.L;  // m x rp (rp = r)
-  const float* V = (const float*)it.Vs; // n x r
+  const float* V = it.V;               // n x r
   float d = 0.f;
   for (int t = 0; t < a.r; ++t) d = fmaf(L[(size_t)i * a.rp + t], V[(size_t)c * a.r + t], d);
   float* W = (float*)it.W;
@@ -491,7 +529,9 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
   const bool wf16 = w_dtype == ZO_F16;
   const int rp = bf16 ? (r + 31) / 32 * 32 : r;
   const int aw = (r * r + 255) / 256;
-  size_t need = 0;
+  // Workspace: the descriptor table and the two workgroup-start arrays, then
+  // each item's regions.
+  size_t need = zo_align256((size_t)count * sizeof(Item)) + 2 * zo_align256((size_t)count * 4);
   for (int i = 0; i < count; ++i) need += item_layout(items[i].m, items[i].n, r, rp, bf16, aw).total;
   if (ws_needed) *ws_needed = need;
   if (!ws) return ZO_OK;
@@ -503,93 +543,131 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
     zo_set_error("update: r = %d above %d", r, ZO_MAX_RANK);
     return ZO_ERR_UNSUPPORTED;
   }
+  if (count <= 0) return ZO_OK;
   WsCarver wc(ws);
-  int st;
-  for (int c0 = 0; c0 < count; c0 += ITEMS_PER_LAUNCH) {
-    const int cn = count - c0 < ITEMS_PER_LAUNCH ? count - c0 : ITEMS_PER_LAUNCH;
-    RRArgs ra{};
-    USArgs ua{};
-    UpdArgs pa{};
-    ra.g = g;
-    ra.nonfinite_flag = nonfinite_flag;
-    ra.r = r;
-    ra.q = q;
-    ra.aw = aw;
-    ra.sgd = sgd;
-    ra.beta1 = beta1;
-    ra.beta2 = beta2;
-    ra.eps_adam = eps_adam;
-    ra.bc1 = 1.0 - pow((double)beta1, (double)t);
-    ra.bc2 = 1.0 - pow((double)beta2, (double)t);
-    ua.count = pa.count = cn;
-    ua.r = pa.r = r;
-    ua.rp = pa.rp = rp;
-    ua.bf16 = bf16;
-    ua.aw = aw;
-    ua.sgd = sgd;
-    ua.lr = lr;
-    int us_wg = 0;
-    int wg_total = 0;
-    bool hook = false;
-    for (int k = 0; k < cn; ++k) {
-      const zo_update_item& src = items[c0 + k];
-      const Layout lay = item_layout(src.m, src.n, r, rp, bf16, aw);
-      double* S = (double*)wc.take(lay.s);
-      float* M1n = (float*)wc.take(lay.mom);
-      float* M2n = (float*)wc.take(lay.mom);
-      int* flags = (int*)wc.take(lay.flags);
-      int* skip = (int*)wc.take(lay.skip);
-      void* L = wc.take(lay.L);
-      void* Vs = lay.Vs ? wc.take(lay.Vs) : nullptr;
-      ra.it[k] = ItemRR{src.Z, src.M1, src.M2, src.zbar_out, S, M1n, M2n, flags};
-      const int lt = (src.m + US_ROWS - 1) / US_ROWS;
-      const int vt = bf16 ? (src.n + 63) / 64 : 0;
-      ua.it[k] = ItemUS{src.U, src.V, S, M1n, M2n, src.M1, src.M2, flags, skip, L, Vs,
-                        src.m, src.n, us_wg, lt, lt + vt};
-      us_wg += lt + vt;
-      ItemUpd u{};
-      u.W = src.W;
-      u.wout = src.w_f32_out;
-      u.L = L;
-      u.Vs = bf16 ? Vs : (const void*)src.V;
-      u.skip = skip;
-      u.m = src.m;
-      u.n = src.n;
-      u.wg_begin = wg_total;
-      if (bf16) {
-        u.strips = (src.n + UPD_COLS - 1) / UPD_COLS;
-        u.rchunks = (src.m + UPD_ROWS - 1) / UPD_ROWS;
-        wg_total += u.strips * u.rchunks;
-      } else {
-        u.strips = u.rchunks = 1;
-        wg_total += (int)(((long long)src.m * src.n + 255) / 256);
-      }
-      hook = hook || src.w_f32_out;
-      pa.it[k] = u;
+  Item* dtab = (Item*)wc.take((size_t)count * sizeof(Item));
+  int* us_begin = (int*)wc.take((size_t)count * 4);
+  int* up_begin = (int*)wc.take((size_t)count * 4);
+  std::vector<Item> tab((size_t)count);
+  long long us_total = 0, up_total = 0;
+  bool hook = false;
+  for (int k = 0; k < count; ++k) {
+    const zo_update_item& src = items[k];
+    const Layout lay = item_layout(src.m, src.n, r, rp, bf16, aw);
+    Item& it = tab[k];
+    it.Z = src.Z;
+    it.M1 = src.M1;
+    it.M2 = src.M2;
+    it.zbar_out = src.zbar_out;
+    it.S = (double*)wc.take(lay.s);
+    it.M1n = (float*)wc.take(lay.mom);
+    it.M2n = (float*)wc.take(lay.mom);
+    it.flags = (int*)wc.take(lay.flags);
+    it.skip = (int*)wc.take(lay.skip);
+    it.L = wc.take(lay.L);
+    it.Vs = lay.Vs ? wc.take(lay.Vs) : nullptr;
+    it.U = src.U;
+    it.V = src.V;
+    it.W = src.W;
+    it.wout = src.w_f32_out;
+    it.m = src.m;
+    it.n = src.n;
+    it.l_tiles = (src.m + US_ROWS - 1) / US_ROWS;
+    it.us_wg = it.l_tiles + (bf16 ? (src.n + 63) / 64 : 0);
+    it.us_begin = (int)us_total;
+    us_total += it.us_wg;
+    it.up_begin = (int)up_total;
+    if (bf16) {
+      it.strips = (src.n + UPD_COLS - 1) / UPD_COLS;
+      it.rchunks = (src.m + UPD_ROWS - 1) / UPD_ROWS;
+      up_total += (long long)it.strips * it.rchunks;
+    } else {
+      it.strips = it.rchunks = 1;
+      up_total += ((long long)src.m * src.n + 255) / 256;
     }
-    hipLaunchKernelGGL(k_adam_rr, dim3(cn * aw), dim3(256), 0, stream, ra);
-    if ((st = zo_hip_status(hipGetLastError(), "k_adam_rr")) != ZO_OK) return st;
+    if (us_total >= (1LL << 31) || up_total >= (1LL << 31)) {
+      zo_set_error("update: too many workgroups for one call (item %d); split the items", k);
+      return ZO_ERR_UNSUPPORTED;
+    }
+    hook = hook || src.w_f32_out;
+  }
+  if ((long long)count * aw > MAX_PASS_WG) {
+    zo_set_error("update: %d items above the %lld per call", count, MAX_PASS_WG / aw);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  int st;
+  for (int c0 = 0; c0 < count; c0 += FILL_ITEMS) {
+    FillArgs fa{};
+    fa.dst = dtab;
+    fa.us_begin = us_begin;
+    fa.up_begin = up_begin;
+    fa.c0 = c0;
+    fa.cn = count - c0 < FILL_ITEMS ? count - c0 : FILL_ITEMS;
+    for (int k = 0; k < fa.cn; ++k) fa.it[k] = tab[c0 + k];
+    hipLaunchKernelGGL(k_fill_items, dim3(1), dim3(256), 0, stream, fa);
+    if ((st = zo_hip_status(hipGetLastError(), "k_fill_items")) != ZO_OK) return st;
+  }
+
+  RRArgs ra{};
+  ra.it = dtab;
+  ra.g = g;
+  ra.nonfinite_flag = nonfinite_flag;
+  ra.r = r;
+  ra.q = q;
+  ra.aw = aw;
+  ra.sgd = sgd;
+  ra.beta1 = beta1;
+  ra.beta2 = beta2;
+  ra.eps_adam = eps_adam;
+  ra.bc1 = 1.0 - pow((double)beta1, (double)t);
+  ra.bc2 = 1.0 - pow((double)beta2, (double)t);
+  hipLaunchKernelGGL(k_adam_rr, dim3((unsigned)(count * aw)), dim3(256), 0, stream, ra);
+  if ((st = zo_hip_status(hipGetLastError(), "k_adam_rr")) != ZO_OK) return st;
+
+  USArgs ua{};
+  ua.it = dtab;
+  ua.begin = us_begin;
+  ua.count = count;
+  ua.r = r;
+  ua.rp = rp;
+  ua.bf16 = bf16;
+  ua.aw = aw;
+  ua.sgd = sgd;
+  ua.lr = lr;
+  for (long long w0 = 0; w0 < us_total; w0 += MAX_PASS_WG) {
+    const long long nw = us_total - w0 < MAX_PASS_WG ? us_total - w0 : MAX_PASS_WG;
+    ua.wg0 = (int)w0;
+    const dim3 grid((unsigned)nw);
     switch ((rp + 31) / 32) {
-      case 1: hipLaunchKernelGGL(k_us<1>, dim3(us_wg), dim3(256), 0, stream, ua); break;
-      case 2: hipLaunchKernelGGL(k_us<2>, dim3(us_wg), dim3(256), 0, stream, ua); break;
-      case 3: hipLaunchKernelGGL(k_us<3>, dim3(us_wg), dim3(256), 0, stream, ua); break;
-      default: hipLaunchKernelGGL(k_us<4>, dim3(us_wg), dim3(256), 0, stream, ua); break;
+      case 1: hipLaunchKernelGGL(k_us<1>, grid, dim3(256), 0, stream, ua); break;
+      case 2: hipLaunchKernelGGL(k_us<2>, grid, dim3(256), 0, stream, ua); break;
+      case 3: hipLaunchKernelGGL(k_us<3>, grid, dim3(256), 0, stream, ua); break;
+      default: hipLaunchKernelGGL(k_us<4>, grid, dim3(256), 0, stream, ua); break;
     }
     if ((st = zo_hip_status(hipGetLastError(), "k_us")) != ZO_OK) return st;
-    pa.total_wg = wg_total;
-    if (wg_total > 0) {
-      if (!bf16) {
-        hipLaunchKernelGGL(k_update_f32, dim3(wg_total), dim3(256), 0, stream, pa);
-      } else {
-        switch (rp / 32) {
-          case 1: launch_update_bf16<1>(hook, wf16, wg_total, stream, pa); break;
-          case 2: launch_update_bf16<2>(hook, wf16, wg_total, stream, pa); break;
-          case 3: launch_update_bf16<3>(hook, wf16, wg_total, stream, pa); break;
-          default: launch_update_bf16<4>(hook, wf16, wg_total, stream, pa); break;
-        }
+  }
+
+  UpdArgs pa{};
+  pa.it = dtab;
+  pa.begin = up_begin;
+  pa.count = count;
+  pa.r = r;
+  pa.rp = rp;
+  for (long long w0 = 0; w0 < up_total; w0 += MAX_PASS_WG) {
+    const long long nw = up_total - w0 < MAX_PASS_WG ? up_total - w0 : MAX_PASS_WG;
+    pa.wg0 = (int)w0;
+    pa.pass_wg = (int)nw;
+    if (!bf16) {
+      hipLaunchKernelGGL(k_update_f32, dim3((unsigned)nw), dim3(256), 0, stream, pa);
+    } else {
+      switch (rp / 32) {
+        case 1: launch_update_bf16<1>(hook, wf16, (int)nw, stream, pa); break;
+        case 2: launch_update_bf16<2>(hook, wf16, (int)nw, stream, pa); break;
+        case 3: launch_update_bf16<3>(hook, wf16, (int)nw, stream, pa); break;
+        default: launch_update_bf16<4>(hook, wf16, (int)nw, stream, pa); break;
       }
-      if ((st = zo_hip_status(hipGetLastError(), "k_update")) != ZO_OK) return st;
     }
+    if ((st = zo_hip_status(hipGetLastError(), "k_update")) != ZO_OK) return st;
   }
   return ZO_OK;
 }

@@ -184,7 +184,7 @@ def test_nonfinite_estimate_leaves_state_untouched():
 
 
 def test_batched_heterogeneous_items():
-    """More items than one launch holds, mixed shapes, one global g."""
+    """Mixed shapes in one call (more than one group of the descriptor fill), one global g."""
     r, q = 16, 4
     shapes = [(64 + 8 * i, 256 + 64 * (i % 3)) for i in range(21)]
     items = [make_item(4, (i,), m, n, r, q, True, i % 2 == 1) for i, (m, n) in enumerate(shapes)]
@@ -196,6 +196,40 @@ def test_batched_heterogeneous_items():
     assert int(flag.item()) == 0
     for it, ref in zip(items, refs):
         check_item(it, ref, True, 5e-3)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_many_items_mixed_hooks(dt):
+    """150 items in one call: the descriptor table takes ten fill launches and the workgroup ->
+    item search two rounds; every third item has no check hook and no zbar_out, so the
+    hook-writing kernel variant also runs items without a hook buffer."""
+    bf16 = dt == "bf16"
+    r, q, lr, t = 8, 2, 5e-3, 2
+    shapes = [(16 + 8 * (i % 7), 64 + 64 * (i % 3)) for i in range(150)]
+    items = [make_item(6, (i,), m, n, r, q, bf16, i % 2 == 1) for i, (m, n) in enumerate(shapes)]
+    for i, it in enumerate(items):
+        if i % 3 == 2:
+            it["dev"]["w_f32_out"] = None
+            it["dev"]["zbar_out"] = None
+    g = zd.f32(zd.draw(6, "G", (0,), (q,), 1e-2))
+    refs = [expected(it, g.astype(np.float64), t, lr, 0.9, 0.95, 1e-8) for it in items]
+    zo.subspace_adam_update([it["dev"] for it in items], dev_f32(g), t, lr, 0.9, 0.95, 1e-8)
+    torch.cuda.synchronize()
+    for i, (it, ref) in enumerate(zip(items, refs)):
+        if it["dev"]["w_f32_out"] is not None:
+            check_item(it, ref, bf16, lr)
+            continue
+        got_w = host(it["dev"]["W"])
+        if bf16:
+            # No hook: the stored value is RNE of a value within E of W_exact.
+            E = update_bound(it["U"], it["V"], ref["S"], lr, ref["W"])
+            half_ulp = np.maximum(np.exp2(np.frexp(got_w)[1] - 9.0), np.exp2(np.frexp(ref["W"])[1] - 9.0))
+            assert np.all(np.abs(got_w - ref["W"]) <= E + half_ulp), i
+            assert normwise(got_w, ref["W"]) <= 2e-3
+        else:
+            assert ferr(got_w, ref["W"], 1.0) <= 1e-5, i
+        np.testing.assert_allclose(host(it["dev"]["M1"]), ref["M1"], rtol=1e-6, atol=1e-12)
+        np.testing.assert_allclose(host(it["dev"]["M2"]), ref["M2"], rtol=1e-6, atol=1e-14)
 
 
 @pytest.mark.parametrize("name,m,n,rank,f16", [("opt-1.3b", 8192, 2048, None, False),
