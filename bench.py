@@ -104,6 +104,43 @@ def copy_calibration():
                       "launches": 3}))
 
 
+def practical_peaks(M, m, n, dt16):
+    """What library kernels reach on this GPU in the same run: a plain GEMM of one of the
+    workload's shapes (torch.matmul, i.e. hipBLASLt), a 2 GiB device copy and a 2 GiB in-place
+    read-modify-write (torch elementwise add).  Context for the roofline fractions."""
+    import torch
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, reps):
+        for _ in range(2):
+            fn()
+        a, b = ev(), ev()
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1)
+    X = torch.randn(M, n, device="cuda", generator=g).to(dt16)
+    W = (0.02 * torch.randn(m, n, device="cuda", generator=g)).to(dt16)
+    Y = torch.empty(M, m, device="cuda", dtype=dt16)
+    ms_gemm = timed(lambda: torch.matmul(X, W.t(), out=Y), 5)
+    del X, W, Y
+    nbytes = 1 << 31
+    a = torch.empty(nbytes // 2, dtype=dt16, device="cuda").normal_(generator=g)
+    b = torch.empty_like(a)
+    ms_copy = timed(lambda: b.copy_(a), 5)
+    ms_rmw = timed(lambda: a.add_(1.0), 5)
+    del a, b
+    torch.cuda.empty_cache()
+    return {"gemm_torch_matmul": {"shape": f"{M}x{m}x{n}", "tflops": round(2.0 * M * m * n / ms_gemm / 1e9, 1)},
+            "copy_2gib_gbs": round(2 * nbytes / ms_copy / 1e6, 1),
+            "inplace_rmw_2gib_gbs": round(2 * nbytes / ms_rmw / 1e6, 1)}
+
+
 def cpu_baseline(cfg, seed, budget_s, mat, lora, r, f16=False):
     """The float64 oracle on a bounded sample of the same workload, on this host's cores."""
     import numpy as np
@@ -338,6 +375,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the library GEMM / copy / read-modify-write reference timings")
     ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scale)")
     args = ap.parse_args()
 
@@ -575,9 +614,12 @@ def main():
         "gemm_by_shape": {k: {"tflops": round(v[1] / (v[0] * 1e-3) / 1e12, 1), "avg_ms": round(v[0] / v[2], 3)}
                           for k, v in per_shape.items()},
     }
+    del plins, items, X, Y, ws, units
+    torch.cuda.empty_cache()
+    if not args.no_peaks:
+        _, m0, n0 = unit_mats[0]
+        out["practical_peaks"] = practical_peaks(nblk * T, m0, n0, dt16)
     if not args.no_cpu_baseline:
-        del plins, items, X, Y, ws, units
-        torch.cuda.empty_cache()
         out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget, unit_mats[0], lora, r, f16)
     print(json.dumps(out), flush=True)
 

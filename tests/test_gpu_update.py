@@ -232,6 +232,23 @@ def test_many_items_mixed_hooks(dt):
         np.testing.assert_allclose(host(it["dev"]["M2"]), ref["M2"], rtol=1e-6, atol=1e-14)
 
 
+def test_thousands_of_items():
+    """4500 tiny items in one call: 282 fill launches and a three-round workgroup -> item search
+    (4500 > 64 * 64), for the bf16 path; every item checked against the oracle."""
+    r, q, lr, t = 4, 2, 1e-2, 1
+    shapes = [(8 + 8 * (i % 5), 8 + 8 * (i % 2)) for i in range(4500)]
+    items = [make_item(7, (i,), m, n, r, q, True, False) for i, (m, n) in enumerate(shapes)]
+    g = zd.f32(zd.draw(7, "G", (0,), (q,), 1e-2))
+    refs = [expected(it, g.astype(np.float64), t, lr, 0.9, 0.95, 1e-8) for it in items]
+    zo.subspace_adam_update([it["dev"] for it in items], dev_f32(g), t, lr, 0.9, 0.95, 1e-8)
+    torch.cuda.synchronize()
+    got_hook = host(torch.cat([it["dev"]["w_f32_out"].reshape(-1) for it in items]))
+    want = np.concatenate([ref["W"].reshape(-1) for ref in refs])
+    assert ferr(got_hook, want, 1.0) <= 5e-5
+    for i in (0, 1, 63, 64, 4095, 4096, 4499):
+        check_item(items[i], refs[i], True, lr)
+
+
 @pytest.mark.parametrize("name,m,n,rank,f16", [("opt-1.3b", 8192, 2048, None, False),
                                                 ("llama-7b", 11008, 4096, None, False),
                                                 ("llama-7b", 4096, 11008, None, False),
