@@ -8,8 +8,11 @@
 // normalisation, the attention, and the host sequence of one layer.
 //
 // k_layernorm: one wave per row, three passes over the row (sum, squared
-// deviations, output); the row stays in L1/L2 after the first, so HBM sees
-// one read and one write.  Statistics in fp32 with fixed-order wave sums.
+// deviations, output), statistics in fp32 with fixed-order wave sums.  Rows of
+// up to 8192 elements are read once into registers (k_layernorm_reg, NC
+// 512-element chunks, every load in flight at once); longer rows are re-read
+// by each pass from L1/L2 (k_layernorm).  Both do the same operations in the
+// same order, so their results are identical.
 //
 // k_attention<F16, DH>: one workgroup (4 waves) per (block, sequence, head,
 // tile of 64 AT_NG queries); keys in tiles of 64 through LDS (loaded into
@@ -115,6 +118,75 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* __restrict__ X,
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = fmaf((v[e] - mean) * rstd, g[e], b[e]);
     store8<DT>(Y, base + c, v);
+  }
+}
+
+// Rows of d <= 512 NC elements held in registers as loaded (8 elements per lane and chunk:
+// one 16-byte word for 16-bit types, two for fp32), widened to fp32 at each use (exact).
+template <int DT>
+struct Raw8 {
+  static constexpr int W = DT == ZO_F32 ? 2 : 1;
+  u32x4 w[W];
+  __device__ __forceinline__ void load(const void* X, size_t idx) {
+    const u32x4* p = DT == ZO_F32 ? (const u32x4*)((const float*)X + idx) : (const u32x4*)((const uint16_t*)X + idx);
+#pragma unroll
+    for (int i = 0; i < W; ++i) w[i] = p[i];
+  }
+  __device__ __forceinline__ float at(int e) const {
+    if constexpr (DT == ZO_F32) return __uint_as_float(w[e >> 2][e & 3]);
+    const uint32_t u = w[0][e >> 1];
+    const uint16_t h = (uint16_t)((e & 1) ? (u >> 16) : u);
+    if constexpr (DT == ZO_BF16) return bf16_to_f32((bf16_t)h);
+    return f16_to_f32(h);
+  }
+};
+
+template <int DT, int NC>
+__global__ __launch_bounds__(256) void k_layernorm_reg(const void* __restrict__ X,
+                                                       const float* __restrict__ gamma,
+                                                       const float* __restrict__ beta, void* Y,
+                                                       long long rows, int d, float eps_ln) {
+  const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const size_t base = (size_t)row * d;
+  Raw8<DT> v[NC];
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int c = lane * 8 + 512 * k;
+    if (c < d) v[k].load(X, base + c);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    if (lane * 8 + 512 * k < d) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += v[k].at(e);
+    }
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    if (lane * 8 + 512 * k < d) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) q = fmaf(v[k].at(e) - mean, v[k].at(e) - mean, q);
+    }
+  }
+  const float rstd = 1.f / sqrtf(wave_sum(q) / (float)d + eps_ln);
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int c = lane * 8 + 512 * k;
+    if (c < d) {
+      const f32x4 g0 = *(const f32x4*)(gamma + c), g1 = *(const f32x4*)(gamma + c + 4);
+      const f32x4 b0 = *(const f32x4*)(beta + c), b1 = *(const f32x4*)(beta + c + 4);
+      const float g[8] = {g0[0], g0[1], g0[2], g0[3], g1[0], g1[1], g1[2], g1[3]};
+      const float b[8] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = fmaf((v[k].at(e) - mean) * rstd, g[e], b[e]);
+      store8<DT>(Y, base + c, o);
+    }
   }
 }
 
@@ -352,6 +424,24 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
   }
 }
 
+// Register-resident rows in buckets of 2, 4, 8, 10 or 16 chunks of 512; longer rows re-read.
+template <int DT>
+void layernorm_dispatch(dim3 grid, dim3 block, hipStream_t stream, const void* X, const float* gamma,
+                        const float* beta, void* Y, long long rows, int d, float eps_ln) {
+  if (d <= 1024)
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 2>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  else if (d <= 2048)
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 4>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  else if (d <= 4096)
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 8>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  else if (d <= 5120)
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 10>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  else if (d <= 8192)
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 16>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  else
+    hipLaunchKernelGGL(k_layernorm<DT>, grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+}
+
 }  // namespace
 
 int zo_layernorm_launch(long long rows, int d, int dtype, const void* X, const float* gamma,
@@ -359,11 +449,11 @@ int zo_layernorm_launch(long long rows, int d, int dtype, const void* X, const f
   if (rows <= 0) return ZO_OK;
   const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
   if (dtype == ZO_BF16)
-    hipLaunchKernelGGL(k_layernorm<ZO_BF16>, grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    layernorm_dispatch<ZO_BF16>(grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else if (dtype == ZO_F16)
-    hipLaunchKernelGGL(k_layernorm<ZO_F16>, grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    layernorm_dispatch<ZO_F16>(grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else
-    hipLaunchKernelGGL(k_layernorm<ZO_F32>, grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    layernorm_dispatch<ZO_F32>(grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
   return zo_hip_status(hipGetLastError(), "k_layernorm");
 }
 

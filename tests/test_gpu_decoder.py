@@ -44,7 +44,9 @@ def check16(got, ref, what):
 
 # ------------------------------------------------------------------ layer norm
 @pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
-@pytest.mark.parametrize("rows,d", [(37, 96), (300, 5120), (5, 8), (64, 2048)])
+@pytest.mark.parametrize("rows,d", [(37, 96), (300, 5120), (5, 8), (64, 2048),
+                                    # every register bucket and its edges, and the re-reading path
+                                    (7, 1032), (9, 4096), (6, 5128), (5, 8192), (3, 8200)])
 def test_layernorm_parity(dt, rows, d):
     Xd, Xv = cast(zd.draw(7, "X", (rows, d), (rows, d)) * 2.0 + 0.5, dt)
     g = zd.f32(1.0 + 0.1 * zd.draw(7, "W0", (d, 1), (d,)))
