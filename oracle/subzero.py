@@ -18,6 +18,7 @@ __all__ = [
     "perturbation", "perturbed_weight", "perturbed_linear", "perturbed_linear_blocks",
     "lora_perturbed_factors", "lora_perturbed_linear", "lora_perturbed_linear_blocks",
     "layer_norm", "causal_attention", "DECODER_MATS", "decoder_layer",
+    "rms_norm", "rope", "silu", "LLAMA_MATS", "llama_layer",
     "sq_loss", "central_estimate", "forward_estimate", "aggregate",
     "adam_direction", "subspace_adam_update", "subspace_sgd_update", "round_bf16", "round_f16", "tiny_run",
 ]
@@ -234,6 +235,79 @@ def decoder_layer(H, layer, sign, eps, j, heads, seq_len, store=None, eps_ln=1e-
     if trace is not None:
         trace.update(A=A, Q=Q, K=K, V=Vv, C=C, H2=H2, A2=A2, F=F)
     return st(H2 + lin(F, "fc2"))
+
+
+# ---------------------------------------------------------------------------
+# The same for a decoder layer of the LLaMA family (the other full-tuning
+# family of the experiments): RMS normalisation, rotary positions, SwiGLU MLP
+# ---------------------------------------------------------------------------
+def rms_norm(X, gamma, eps_rms=1e-6):
+    """Row-wise RMS normalisation x / sqrt(mean(x^2) + eps_rms) * gamma (no centring, no bias).
+    READING: eps_rms = 1e-6."""
+    X = np.asarray(X, np.float64)
+    ms = (X * X).mean(axis=1, keepdims=True)
+    return X / np.sqrt(ms + eps_rms) * np.asarray(gamma, np.float64)
+
+
+def rope(X, seq_len, heads, base=10000.0):
+    """Rotary position embedding of query or key rows of one block (T token rows holding
+    T / seq_len sequences one after another; a row's position is its index within its
+    sequence).  In each head of dh = d / heads columns, dimension i < dh/2 and its partner
+    i + dh/2 are rotated together by the angle p * base^(-2i/dh):
+        (a, b) -> (a cos - b sin, b cos + a sin).
+    READING: the half-split pairing and base 10000 of the LLaMA checkpoints' usual form."""
+    X = np.asarray(X, np.float64)
+    T, d = X.shape
+    dh = d // heads
+    half = dh // 2
+    pos = (np.arange(T) % seq_len).astype(np.float64)
+    theta = base ** (-2.0 * np.arange(half, dtype=np.float64) / dh)
+    ang = pos[:, None] * theta[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    out = X.copy()
+    for h in range(heads):
+        a = X[:, h * dh:h * dh + half]
+        b = X[:, h * dh + half:(h + 1) * dh]
+        out[:, h * dh:h * dh + half] = a * c - b * s
+        out[:, h * dh + half:(h + 1) * dh] = b * c + a * s
+    return out
+
+
+def silu(x):
+    """x * sigmoid(x), the gate non-linearity of the SwiGLU MLP."""
+    x = np.asarray(x, np.float64)
+    return x / (1.0 + np.exp(-x))
+
+
+LLAMA_MATS = ("q", "k", "v", "o", "gate", "up", "down")
+
+
+def llama_layer(H, layer, sign, eps, j, heads, seq_len, store=None, eps_rms=1e-6, rope_base=10000.0,
+                trace=None):
+    """One pre-norm decoder layer of the LLaMA family under query j with sign s, each of its
+    seven weight matrices (q, k, v, o, gate, up, down; each with its own U, V and Z_j)
+    entering as W + s eps U Z_j V^T (Eq. 4):
+        A = RMS1(H);   Q = rope(A Wq'^T);  K = rope(A Wk'^T);  V = A Wv'^T
+        C = attention(Q, K, V);   H2 = H + C Wo'^T;   A2 = RMS2(H2)
+        F = silu(A2 Wg'^T) * (A2 Wu'^T);   H3 = H2 + F Wd'^T.
+    ``store`` rounds each tensor at the points where the device path stores one (Q and K
+    are stored before and after the rotation; the gate output before it enters F); all
+    arithmetic float64.  ``trace`` receives A, Q, K, V, C, H2, A2, G, F."""
+    st = store if store is not None else (lambda x: x)
+    lin = lambda X, name: perturbed_linear(X, layer[name]["W"], layer[name]["U"], layer[name]["V"],
+                                           layer[name]["Z"][j], sign, eps)
+    A = st(rms_norm(H, layer["rms1_g"], eps_rms))
+    Q = st(rope(st(lin(A, "q")), seq_len, heads, rope_base))
+    K = st(rope(st(lin(A, "k")), seq_len, heads, rope_base))
+    Vv = st(lin(A, "v"))
+    C = st(causal_attention(Q, K, Vv, heads, seq_len))
+    H2 = st(np.asarray(H, np.float64) + lin(C, "o"))
+    A2 = st(rms_norm(H2, layer["rms2_g"], eps_rms))
+    G = st(lin(A2, "gate"))
+    F = st(silu(G) * lin(A2, "up"))
+    if trace is not None:
+        trace.update(A=A, Q=Q, K=K, V=Vv, C=C, H2=H2, A2=A2, G=G, F=F)
+    return st(H2 + lin(F, "down"))
 
 
 # ---------------------------------------------------------------------------

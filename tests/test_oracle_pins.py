@@ -712,3 +712,135 @@ def test_decoder_layer_matches_torch_modules():
     H3 = H2 + F.linear(F.relu(F.linear(A2, Wp["fc1"])), Wp["fc2"])
     np.testing.assert_allclose(oracle.decoder_layer(H, layer, s, eps, j, heads, L), H3.numpy(),
                                rtol=1e-11, atol=1e-11)
+
+
+# ---------------------------------------------------------------------------
+# The LLaMA-family layer (RMS normalisation, rotary positions, SwiGLU MLP)
+# ---------------------------------------------------------------------------
+def test_rms_norm_hand_case_and_torch():
+    torch = pytest.importorskip("torch")
+    # (3, 4): mean square 12.5, so the row divides by sqrt(12.5).
+    np.testing.assert_allclose(oracle.rms_norm(np.array([[3.0, 4.0]]), np.ones(2), 0.0)[0],
+                               [0.848528137423857, 1.131370849898476], rtol=0, atol=1e-15)
+    X = RNG.standard_normal((29, 80)) * 2.0 + 0.5
+    g = 1.0 + 0.1 * RNG.standard_normal(80)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(X), (80,), torch.from_numpy(g), 1e-6).numpy()
+    np.testing.assert_allclose(oracle.rms_norm(X, g, 1e-6), ref, rtol=1e-13, atol=1e-13)
+    # eps = 0: invariant to a positive scale of each row (but not to a shift).
+    a = RNG.uniform(0.5, 4.0, (29, 1))
+    np.testing.assert_allclose(oracle.rms_norm(a * X, g, 0.0), oracle.rms_norm(X, g, 0.0), rtol=1e-13, atol=1e-13)
+    assert np.abs(oracle.rms_norm(X + 1.0, g, 0.0) - oracle.rms_norm(X, g, 0.0)).max() > 1e-2
+
+
+def test_rope_hand_cases_and_properties():
+    # One head of dh = 4: dimension 0 pairs with 2 (angle p * 1), dimension 1 with 3 (angle p * 0.01).
+    X = np.array([[1.0, 0.0, 0.0, 0.0], [1.0, 0.0, 0.0, 0.0], [0.0, 1.0, 0.0, 0.0], [0.0, 0.0, 2.0, 0.0]])
+    Y = oracle.rope(X, 4, 1)  # positions 0, 1, 2, 3
+    np.testing.assert_allclose(Y[0], [1.0, 0.0, 0.0, 0.0], atol=1e-16)
+    np.testing.assert_allclose(Y[1], [math.cos(1.0), 0.0, math.sin(1.0), 0.0], atol=1e-16)
+    np.testing.assert_allclose(Y[2], [0.0, math.cos(0.02), 0.0, math.sin(0.02)], atol=1e-16)
+    np.testing.assert_allclose(Y[3], [-2.0 * math.sin(3.0), 0.0, 2.0 * math.cos(3.0), 0.0], atol=1e-15)
+    L, heads, dh = 16, 3, 32
+    Q, K = RNG.standard_normal((L, heads * dh)), RNG.standard_normal((L, heads * dh))
+    Rq, Rk = oracle.rope(Q, L, heads), oracle.rope(K, L, heads)
+    # Rotations: every (i, i + dh/2) pair keeps its length; position 0 is untouched.
+    for h in range(heads):
+        a, b = slice(h * dh, h * dh + dh // 2), slice(h * dh + dh // 2, (h + 1) * dh)
+        np.testing.assert_allclose(Rq[:, a] ** 2 + Rq[:, b] ** 2, Q[:, a] ** 2 + Q[:, b] ** 2, rtol=1e-13)
+    np.testing.assert_array_equal(Rq[0], Q[0])
+    # Scores depend on positions only through their difference: q at p, k at s.
+    def score(p, s, h=1):
+        q = np.zeros((L, heads * dh)); k = np.zeros((L, heads * dh))
+        q[p], k[s] = Q[3], K[5]
+        qr, kr = oracle.rope(q, L, heads)[p], oracle.rope(k, L, heads)[s]
+        c = slice(h * dh, (h + 1) * dh)
+        return float(qr[c] @ kr[c])
+    np.testing.assert_allclose(score(9, 4), score(12, 7), rtol=1e-12)
+    assert abs(score(9, 4) - score(9, 6)) > 1e-3
+    # Positions restart with every sequence of the block.
+    np.testing.assert_array_equal(oracle.rope(np.vstack([Q, Q]), L, heads)[L:], Rq)
+
+
+def test_rope_matches_transformers():
+    torch = pytest.importorskip("torch")
+    ml = pytest.importorskip("transformers.models.llama.modeling_llama")
+    L, heads, dh, base = 12, 2, 16, 10000.0
+    Q, K = RNG.standard_normal((L, heads * dh)), RNG.standard_normal((L, heads * dh))
+    inv = 1.0 / base ** (torch.arange(0, dh, 2, dtype=torch.float64) / dh)
+    ang = torch.arange(L, dtype=torch.float64)[:, None] * inv[None, :]
+    emb = torch.cat([ang, ang], dim=-1)
+    to4 = lambda A: torch.from_numpy(A).reshape(1, L, heads, dh).permute(0, 2, 1, 3)
+    qr, kr = ml.apply_rotary_pos_emb(to4(Q), to4(K), emb.cos()[None], emb.sin()[None])
+    back = lambda A: A.permute(0, 2, 1, 3).reshape(L, heads * dh).numpy()
+    np.testing.assert_allclose(oracle.rope(Q, L, heads), back(qr), rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(oracle.rope(K, L, heads), back(kr), rtol=1e-13, atol=1e-13)
+
+
+def test_silu_closed_forms_and_torch():
+    torch = pytest.importorskip("torch")
+    x = RNG.standard_normal(200) * 4.0
+    np.testing.assert_allclose(oracle.silu(x) - oracle.silu(-x), x, rtol=1e-14, atol=1e-14)
+    assert oracle.silu(0.0) == 0.0
+    np.testing.assert_allclose(oracle.silu(x), torch.nn.functional.silu(torch.from_numpy(x)).numpy(), rtol=1e-14)
+
+
+def _llama_params(seed, d, ffn, r, q, zero=False):
+    shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "gate": (ffn, d), "up": (ffn, d), "down": (d, ffn)}
+    layer = {}
+    for i, (nm, (m, n)) in enumerate(shapes.items()):
+        W = np.zeros((m, n)) if zero else zd.draw(seed, "W0", (i, m, n), (m, n), 0.05)
+        U, _ = np.linalg.qr(zd.draw(seed, "OMEGA_U", (i, m), (m, r)))
+        V, _ = np.linalg.qr(zd.draw(seed, "OMEGA_V", (i, n), (n, r)))
+        layer[nm] = dict(W=W, U=U, V=V, Z=zd.z_draws(seed, 0, i, q, r).astype(np.float64))
+    layer["rms1_g"], layer["rms2_g"] = 1.0 + 0.1 * RNG.standard_normal(d), 1.0 + 0.1 * RNG.standard_normal(d)
+    return layer
+
+
+def test_llama_layer_zero_weights_and_causality():
+    d, ffn, r, q, heads, L = 32, 64, 4, 2, 4, 8
+    zero = _llama_params(4, d, ffn, r, q, zero=True)
+    H = RNG.standard_normal((3 * L, d))
+    np.testing.assert_array_equal(oracle.llama_layer(H, zero, 1.0, 0.0, 0, heads, L), H)
+    layer = _llama_params(5, d, ffn, r, q)
+    out = oracle.llama_layer(H, layer, -1.0, 0.2, 1, heads, L)
+    # Changing the last tokens of the second sequence leaves every earlier row as it was.
+    H2 = H.copy(); H2[L + 5:2 * L] += RNG.standard_normal((3, d))
+    out2 = oracle.llama_layer(H2, layer, -1.0, 0.2, 1, heads, L)
+    np.testing.assert_array_equal(out2[:L + 5], out[:L + 5])
+    np.testing.assert_array_equal(out2[2 * L:], out[2 * L:])
+    assert np.abs(out2[L + 5:2 * L] - out[L + 5:2 * L]).max() > 1e-3
+
+
+def test_llama_layer_matches_transformers():
+    """The layer against transformers' LlamaDecoderLayer (its RMS norm and rotary tables are
+    float32 inside, hence the 2e-6 bar), with the perturbed weights formed from Eq. 4."""
+    torch = pytest.importorskip("torch")
+    transformers = pytest.importorskip("transformers")
+    ml = pytest.importorskip("transformers.models.llama.modeling_llama")
+    d, ffn, r, q, heads, L, S = 64, 128, 4, 3, 4, 10, 3
+    layer = _llama_params(6, d, ffn, r, q)
+    H = RNG.standard_normal((S * L, d))
+    s, eps, j = 1.0, 0.05, 2
+    Wp = {nm: layer[nm]["W"] + s * eps * layer[nm]["U"] @ layer[nm]["Z"][j] @ layer[nm]["V"].T
+          for nm in oracle.LLAMA_MATS}
+    cfg = transformers.LlamaConfig(hidden_size=d, intermediate_size=ffn, num_attention_heads=heads,
+                                   num_key_value_heads=heads, rms_norm_eps=1e-6, attention_bias=False,
+                                   mlp_bias=False, hidden_act="silu", max_position_embeddings=4 * L)
+    cfg._attn_implementation = "sdpa"
+    mod = ml.LlamaDecoderLayer(cfg, 0).double()
+    rot = ml.LlamaRotaryEmbedding(cfg).double()
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    with torch.no_grad():
+        att, mlp = mod.self_attn, mod.mlp
+        for lin, nm in ((att.q_proj, "q"), (att.k_proj, "k"), (att.v_proj, "v"), (att.o_proj, "o"),
+                        (mlp.gate_proj, "gate"), (mlp.up_proj, "up"), (mlp.down_proj, "down")):
+            lin.weight.copy_(t(Wp[nm]))
+        mod.input_layernorm.weight.copy_(t(layer["rms1_g"]))
+        mod.post_attention_layernorm.weight.copy_(t(layer["rms2_g"]))
+        x = t(H).reshape(S, L, d)
+        pos = torch.arange(L).unsqueeze(0).expand(S, L)
+        out = mod(x, attention_mask=None, position_ids=pos, position_embeddings=rot(x, pos))
+        out = out[0] if isinstance(out, tuple) else out
+    ref = out.reshape(S * L, d).numpy()
+    got = oracle.llama_layer(H, layer, s, eps, j, heads, L)
+    np.testing.assert_allclose(got, ref, rtol=2e-6, atol=2e-6 * np.abs(ref).max())
