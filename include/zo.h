@@ -64,7 +64,7 @@ typedef enum {
 
 typedef enum { ZO_F32 = 0, ZO_BF16 = 1, ZO_F16 = 2 } zo_dtype;
 /* Epilogues fused into the perturbed linear's output (zo_perturbed_linear_apply_ex). */
-typedef enum { ZO_EPI_NONE = 0, ZO_EPI_RELU = 1, ZO_EPI_RESIDUAL = 2 } zo_epilogue;
+typedef enum { ZO_EPI_NONE = 0, ZO_EPI_RELU = 1, ZO_EPI_RESIDUAL = 2, ZO_EPI_SILU_MUL = 3 } zo_epilogue;
 
 int zo_abi_version(void);
 const char* zo_status_str(int status);
@@ -180,6 +180,9 @@ int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk,
  *   ZO_EPI_RESIDUAL  Y_b = R_b + result, R_b at R + b * r_block_stride
  *                    elements (0: one R for every block), out_dtype, T x m
  *                    rows of stride m.  R may be Y itself.
+ *   ZO_EPI_SILU_MUL  Y_b = silu(R_b) * result, silu(x) = x / (1 + e^-x), R_b
+ *                    laid out as for ZO_EPI_RESIDUAL (the gated MLP of the
+ *                    LLaMA-family layer: R is the gate projection's output).
  * Limits as for zo_perturbed_linear_apply; with 16-bit outputs R is 16-byte
  * aligned and r_block_stride a multiple of 8 (0 or >= T*m). */
 int zo_perturbed_linear_apply_ex(int T, int m, int n, int r, int q, int nblk,
@@ -276,6 +279,30 @@ int zo_layernorm(long long rows, int d, int dtype, const void* X,
                  const float* gamma, const float* beta, float eps_ln, void* Y,
                  void* stream);
 
+/* The same layer of the LLaMA family (pre-norm, RMS normalisation, rotary
+ * positions on queries and keys, SwiGLU MLP, no biases):
+ *
+ *   A = RMS1(H);   Q = rope(A Wq'^T);   K = rope(A Wk'^T);   V = A Wv'^T
+ *   C = attention(Q, K, V);   H2 = H + C Wo'^T;   A2 = RMS2(H2)
+ *   H_out = H2 + (silu(A2 Wg'^T) * (A2 Wu'^T)) Wd'^T
+ *
+ * Row-wise RMS normalisation: Y = X / sqrt(mean(X^2) + eps) * gamma per row of d
+ * elements, statistics in fp32.  X, Y: rows x d (dtype, may alias); gamma:
+ * device fp32 [d].  Limits: d % 8 == 0; 16-byte aligned pointers. */
+int zo_rmsnorm(long long rows, int d, int dtype, const void* X,
+               const float* gamma, float eps, void* Y, void* stream);
+
+/* Rotary position embedding, in place: X is rows x d (bf16 or fp16) holding
+ * sequences of seq_len rows one after another (a row's position p is its index
+ * within its sequence); in each head (dh = d / heads columns) dimension
+ * i < dh/2 and dimension i + dh/2 are rotated together by the angle
+ * p * base^(-2i/dh): (a, b) -> (a cos - b sin, b cos + a sin).  The angle is
+ * formed and reduced modulo 2 pi in fp64, its sine and cosine and the rotation
+ * taken in fp32, one rounding to the dtype.  Limits: rows % seq_len == 0;
+ * dh % 16 == 0; base > 1; 16-byte aligned X. */
+int zo_rope(long long rows, int seq_len, int d, int heads, int dtype, void* X,
+            float base, void* stream);
+
 /* Multi-head causal self-attention.  Q, K, V, O: nblk blocks of T rows x d
  * (dtype bf16 or fp16, row-major, contiguous blocks); each block holds
  * T / seq_len sequences one after another; head h is columns h dh ..
@@ -325,6 +352,32 @@ int zo_decoder_layer_forward(int T, int seq_len, int d, int heads, int ffn,
                              int dtype, const void* H, long long h_block_stride,
                              const zo_decoder_layer* layer, void* H_out,
                              void* workspace, size_t ws_bytes, void* stream);
+
+/* A LLaMA-family layer: q, k, v, o (d x d), gate, up (ffn x d), down
+ * (d x ffn), and the two RMS norms' gamma (device fp32 [d]). */
+typedef struct {
+  zo_matrix q, k, v, o, gate, up, down;
+  const float* rms1_gamma;
+  const float* rms2_gamma;
+} zo_llama_layer;
+
+/* The LLaMA-family layer for all nblk blocks at once; arguments as for
+ * zo_decoder_layer_forward, with eps_rms for the RMS norms and rope_base for
+ * the rotary angles.  The seven products are perturbed linears (the residuals
+ * fused into o and down, silu(gate) * up fused into up); intermediate
+ * activations are stored in dtype in the workspace
+ * (zo_llama_layer_workspace bytes).
+ * Limits: dtype bf16 or fp16; those of zo_causal_attention, of zo_rope and of
+ * zo_perturbed_linear for each matrix. */
+size_t zo_llama_layer_workspace(int T, int seq_len, int d, int heads, int ffn,
+                                int r, int q, int nblk, int dtype);
+int zo_llama_layer_forward(int T, int seq_len, int d, int heads, int ffn,
+                           int r, int q, int nblk, const int* blk_query,
+                           const int8_t* blk_sign, float eps, float eps_rms,
+                           float rope_base, int dtype, const void* H,
+                           long long h_block_stride, const zo_llama_layer* layer,
+                           void* H_out, void* workspace, size_t ws_bytes,
+                           void* stream);
 
 /* ------------------------------------------------------------------------
  * Subspace Adam update -- Eqs. 6-10 and the tail of Alg. 3.

@@ -11,19 +11,22 @@ of include/zo.h); this package only binds it.  Entry points:
     layernorm, causal_attention, DecoderLayer
                            the network a query evaluates (the forward of Eq. 5): a
                            pre-LN decoder layer with all six matrices perturbed
+    rmsnorm, rope, LlamaLayer
+                           the same for a LLaMA-family layer (RMS norms, rotary
+                           positions, SwiGLU MLP) with all seven matrices perturbed
     subspace_adam_update   subspace Adam and W <- W - lr U S V^T (Eqs. 6-10)
     subspace_sgd_update    plain subspace SGD, W <- W - lr U Zbar V^T
     sq_loss, combine_central, combine_forward   loss and estimate helpers (central
                            difference, or forward difference against a baseline block)
 """
-from ._lib import (ZO_BF16, ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL, ZO_F16, ZO_F32, ZO_MAX_BLOCKS,
-                   ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH, DecoderLayer, LoraPerturbedLinear,
-                   PerturbedLinear, Workspace, ZoError, abi_version, causal_attention, combine_central,
-                   combine_forward, layernorm, lib, lora_perturbed_linear, perturbed_linear, sq_loss,
-                   subspace_adam_update, subspace_refresh, subspace_sgd_update)
+from ._lib import (ZO_BF16, ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL, ZO_EPI_SILU_MUL, ZO_F16, ZO_F32, ZO_MAX_BLOCKS,
+                   ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH, DecoderLayer, LlamaLayer,
+                   LoraPerturbedLinear, PerturbedLinear, Workspace, ZoError, abi_version, causal_attention, combine_central,
+                   combine_forward, layernorm, lib, lora_perturbed_linear, perturbed_linear, rmsnorm, rope,
+                   sq_loss, subspace_adam_update, subspace_refresh, subspace_sgd_update)
 
-__all__ = ["ZO_BF16", "ZO_EPI_NONE", "ZO_EPI_RELU", "ZO_EPI_RESIDUAL", "ZO_F16", "ZO_F32", "ZO_MAX_BLOCKS",
-           "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH", "DecoderLayer", "LoraPerturbedLinear",
+__all__ = ["ZO_BF16", "ZO_EPI_NONE", "ZO_EPI_RELU", "ZO_EPI_RESIDUAL", "ZO_EPI_SILU_MUL", "ZO_F16", "ZO_F32", "ZO_MAX_BLOCKS",
+           "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH", "DecoderLayer", "LlamaLayer", "LoraPerturbedLinear",
            "PerturbedLinear", "Workspace", "ZoError", "abi_version", "causal_attention", "combine_central",
-           "combine_forward", "layernorm", "lib", "lora_perturbed_linear", "perturbed_linear", "sq_loss",
+           "combine_forward", "layernorm", "lib", "lora_perturbed_linear", "perturbed_linear", "rmsnorm", "rope", "sq_loss",
            "subspace_adam_update", "subspace_refresh", "subspace_sgd_update"]

@@ -37,8 +37,9 @@ ABI_SYMBOLS = (
     "zo_sq_loss_workspace", "zo_sq_loss", "zo_combine_central", "zo_combine_forward",
     "zo_perturbed_linear_apply_ex", "zo_layernorm", "zo_causal_attention",
     "zo_decoder_layer_workspace", "zo_decoder_layer_forward",
+    "zo_rmsnorm", "zo_rope", "zo_llama_layer_workspace", "zo_llama_layer_forward",
 )
-ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL = 0, 1, 2
+ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL, ZO_EPI_SILU_MUL = 0, 1, 2, 3
 
 
 class Matrix(ctypes.Structure):
@@ -50,6 +51,12 @@ class DecoderLayerDesc(ctypes.Structure):
     """zo_decoder_layer: six perturbed matrices and the two layer norms' parameters."""
     _fields_ = [(nm, Matrix) for nm in ("q", "k", "v", "o", "fc1", "fc2")] + [
         (nm, ctypes.c_void_p) for nm in ("ln1_gamma", "ln1_beta", "ln2_gamma", "ln2_beta")]
+
+
+class LlamaLayerDesc(ctypes.Structure):
+    """zo_llama_layer: seven perturbed matrices and the two RMS norms' gamma."""
+    _fields_ = [(nm, Matrix) for nm in ("q", "k", "v", "o", "gate", "up", "down")] + [
+        (nm, ctypes.c_void_p) for nm in ("rms1_gamma", "rms2_gamma")]
 
 
 class ZoError(RuntimeError):
@@ -153,6 +160,17 @@ def lib() -> ctypes.CDLL:
                                                                   ctypes.POINTER(ctypes.c_int8), c_f, c_f, c_int,
                                                                   c_vp, c_ll, ctypes.POINTER(DecoderLayerDesc),
                                                                   c_vp, c_vp, c_sz, c_vp])
+            L.zo_rmsnorm.restype = c_int
+            L.zo_rmsnorm.argtypes = [c_ll, c_int, c_int, c_vp, c_vp, c_f, c_vp, c_vp]
+            L.zo_rope.restype = c_int
+            L.zo_rope.argtypes = [c_ll, c_int, c_int, c_int, c_int, c_vp, c_f, c_vp]
+            L.zo_llama_layer_workspace.restype = c_sz
+            L.zo_llama_layer_workspace.argtypes = [c_int] * 9
+            L.zo_llama_layer_forward.restype = c_int
+            L.zo_llama_layer_forward.argtypes = ([c_int] * 8 + [ctypes.POINTER(ctypes.c_int),
+                                                                ctypes.POINTER(ctypes.c_int8), c_f, c_f, c_f, c_int,
+                                                                c_vp, c_ll, ctypes.POINTER(LlamaLayerDesc),
+                                                                c_vp, c_vp, c_sz, c_vp])
             _lib = L
     return _lib
 
@@ -297,12 +315,13 @@ class PerturbedLinear:
 
     def apply(self, epilogue: int = ZO_EPI_NONE, R: Optional[torch.Tensor] = None,
               r_block_stride: Optional[int] = None):
-        """The fused GEMM (zo_perturbed_linear_apply_ex): epilogue ZO_EPI_RELU, or ZO_EPI_RESIDUAL
-        adding R (Y's type; one T x m block shared by all blocks, or nblk blocks)."""
+        """The fused GEMM (zo_perturbed_linear_apply_ex): epilogue ZO_EPI_RELU, ZO_EPI_RESIDUAL
+        adding R, or ZO_EPI_SILU_MUL multiplying by silu(R) (R in Y's type; one T x m block shared
+        by all blocks, or nblk blocks)."""
         T, m = self.dims[0], self.dims[1]
         nblk = self.dims[5]
         rs = 0
-        if epilogue == ZO_EPI_RESIDUAL:
+        if epilogue in (ZO_EPI_RESIDUAL, ZO_EPI_SILU_MUL):
             _need(R, "R", self.Y.dtype)
             rs = r_block_stride if r_block_stride is not None else (0 if R.numel() == T * m else T * m)
             if R.numel() < (T * m if rs == 0 else rs * (nblk - 1) + T * m):
@@ -346,6 +365,33 @@ def layernorm(X: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor, eps_ln: 
     _check(lib().zo_layernorm(X.numel() // d, d, _DT[X.dtype], X.data_ptr(), gamma.data_ptr(), beta.data_ptr(),
                               float(eps_ln), out.data_ptr(), _stream_handle()))
     return out
+
+
+def rmsnorm(X: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-6, out: Optional[torch.Tensor] = None):
+    """Row-wise RMS normalisation of X (rows x d).  See zo_rmsnorm."""
+    d = X.shape[-1]
+    _need(X, "X", X.dtype)
+    if X.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {X.dtype}")
+    _need(gamma, "gamma", torch.float32, d)
+    if out is None:
+        out = torch.empty_like(X)
+    _need(out, "out", X.dtype, X.numel())
+    _check(lib().zo_rmsnorm(X.numel() // d, d, _DT[X.dtype], X.data_ptr(), gamma.data_ptr(), float(eps),
+                            out.data_ptr(), _stream_handle()))
+    return out
+
+
+def rope(X: torch.Tensor, seq_len: int, heads: int, base: float = 10000.0):
+    """Rotary position embedding of X (rows x d, sequences of seq_len rows), in place.
+    See zo_rope."""
+    d = X.shape[-1]
+    _need(X, "X", X.dtype)
+    if X.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {X.dtype}")
+    _check(lib().zo_rope(X.numel() // d, seq_len, d, heads, _DT[X.dtype], X.data_ptr(), float(base),
+                         _stream_handle()))
+    return X
 
 
 def causal_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, nblk: int, T: int, seq_len: int,
@@ -428,6 +474,78 @@ class DecoderLayer:
         _check(lib().zo_decoder_layer_forward(*self.dims, self.bq, self.bs, self.eps, self.eps_ln, self.dt,
                                               H.data_ptr(), hs, ctypes.byref(self.desc), out.data_ptr(),
                                               self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
+        return out
+
+
+class LlamaLayer:
+    """A LLaMA-family decoder layer (RMS norms, rotary positions, SwiGLU MLP) whose seven
+    matrices are perturbed per block.  See zo_llama_layer_forward.  ``mats`` maps q, k, v, o,
+    gate, up, down to dicts with W (the layer's dtype), U, V, Z (fp32); ``norms`` holds
+    rms1_gamma and rms2_gamma."""
+
+    NAMES = ("q", "k", "v", "o", "gate", "up", "down")
+
+    def __init__(self, mats: dict, norms: dict, blk_query: Sequence[int], blk_sign: Sequence[int], eps: float,
+                 T: int, seq_len: int, heads: int, eps_rms: float = 1e-6, rope_base: float = 10000.0,
+                 workspace: Optional[torch.Tensor] = None):
+        nblk = len(blk_query)
+        if len(blk_sign) != nblk:
+            raise ValueError("blk_query and blk_sign differ in length")
+        Wq = mats["q"]["W"]
+        d = Wq.shape[0]
+        ffn = mats["gate"]["W"].shape[0]
+        r = mats["q"]["U"].shape[1]
+        q = mats["q"]["Z"].shape[0]
+        dt = Wq.dtype
+        if dt not in _DT:
+            raise TypeError(f"unsupported dtype {dt}")
+        shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "gate": (ffn, d), "up": (ffn, d),
+                  "down": (d, ffn)}
+        desc = LlamaLayerDesc()
+        for nm in self.NAMES:
+            m, n = shapes[nm]
+            mt = mats[nm]
+            _need(mt["W"], f"{nm}.W", dt, m * n)
+            _need(mt["U"], f"{nm}.U", torch.float32, m * r)
+            _need(mt["V"], f"{nm}.V", torch.float32, n * r)
+            _need(mt["Z"], f"{nm}.Z", torch.float32, q * r * r)
+            setattr(desc, nm, Matrix(mt["W"].data_ptr(), mt["U"].data_ptr(), mt["V"].data_ptr(), mt["Z"].data_ptr()))
+        for nm in ("rms1_gamma", "rms2_gamma"):
+            _need(norms[nm], nm, torch.float32, d)
+            setattr(desc, nm, norms[nm].data_ptr())
+        self.desc, self.keep = desc, (mats, norms)
+        self.dims = (T, seq_len, d, heads, ffn, r, q, nblk)
+        self.bq = (ctypes.c_int * nblk)(*[int(v) for v in blk_query])
+        self.bs = (ctypes.c_int8 * nblk)(*[int(v) for v in blk_sign])
+        self.eps, self.eps_rms, self.base = float(eps), float(eps_rms), float(rope_base)
+        self.dt, self.dtype = _DT[dt], dt
+        need = lib().zo_llama_layer_workspace(*self.dims, self.dt)
+        if need == 0:
+            _check(lib().zo_llama_layer_forward(*self.dims, self.bq, self.bs, self.eps, self.eps_rms, self.base,
+                                                self.dt, None, 0, ctypes.byref(self.desc), None, None, 0, None))
+        if workspace is None:
+            workspace = Workspace.get(need)
+        _need(workspace, "workspace", torch.uint8)
+        if workspace.numel() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, {need} needed")
+        self.ws = workspace
+
+    def __call__(self, H: torch.Tensor, out: Optional[torch.Tensor] = None):
+        """H: one T x d input shared by all blocks, or nblk blocks; returns nblk blocks of T x d."""
+        T, d, nblk = self.dims[0], self.dims[2], self.dims[7]
+        _need(H, "H", self.dtype)
+        if H.numel() == T * d:
+            hs = 0
+        elif H.numel() == nblk * T * d:
+            hs = T * d
+        else:
+            raise ValueError("H must hold T*d or nblk*T*d elements")
+        if out is None:
+            out = torch.empty((nblk * T, d), dtype=self.dtype, device=H.device)
+        _need(out, "out", self.dtype, nblk * T * d)
+        _check(lib().zo_llama_layer_forward(*self.dims, self.bq, self.bs, self.eps, self.eps_rms, self.base,
+                                            self.dt, H.data_ptr(), hs, ctypes.byref(self.desc), out.data_ptr(),
+                                            self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
         return out
 
 

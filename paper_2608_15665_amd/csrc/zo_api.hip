@@ -203,10 +203,12 @@ int zo_perturbed_linear_apply_ex(int T, int m, int n, int r, int q, int nblk, in
                                  void* stream) {
   PlinearPlan p;
   ZO_CHECK(W && Y, "perturbed_linear: NULL tensor argument (W or Y)");
-  ZO_CHECK(epilogue == ZO_EPI_NONE || epilogue == ZO_EPI_RELU || epilogue == ZO_EPI_RESIDUAL,
+  ZO_CHECK(epilogue == ZO_EPI_NONE || epilogue == ZO_EPI_RELU || epilogue == ZO_EPI_RESIDUAL ||
+               epilogue == ZO_EPI_SILU_MUL,
            "perturbed_linear: bad epilogue %d", epilogue);
-  if (epilogue == ZO_EPI_RESIDUAL) {
-    ZO_CHECK(R, "perturbed_linear: residual epilogue with a NULL R");
+  const bool uses_r = epilogue == ZO_EPI_RESIDUAL || epilogue == ZO_EPI_SILU_MUL;
+  if (uses_r) {
+    ZO_CHECK(R, "perturbed_linear: epilogue %d with a NULL R", epilogue);
     ZO_CHECK(r_block_stride == 0 || r_block_stride >= (long long)T * m,
              "perturbed_linear: r_block_stride = %lld must be 0 or >= T*m", r_block_stride);
     ZO_CHECK(out_dtype == ZO_F32 || r_block_stride % 8 == 0,
@@ -216,8 +218,8 @@ int zo_perturbed_linear_apply_ex(int T, int m, int n, int r, int q, int nblk, in
   int st = check_plinear_call(T, m, n, r, q, nblk, x_block_stride, in_dtype, out_dtype, X, W, Y,
                               workspace, ws_bytes, &p);
   if (st != ZO_OK) return st;
-  return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream, epilogue,
-                          epilogue == ZO_EPI_RESIDUAL ? R : nullptr, r_block_stride);
+  return zo_plinear_apply(p, X, W, Y, workspace, (hipStream_t)stream, epilogue, uses_r ? R : nullptr,
+                          r_block_stride);
 }
 
 int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk, int in_dtype,
@@ -315,6 +317,40 @@ int zo_layernorm(long long rows, int d, int dtype, const void* X, const float* g
   return zo_layernorm_launch(rows, d, dtype, X, gamma, beta, eps_ln, Y, (hipStream_t)stream);
 }
 
+int zo_rmsnorm(long long rows, int d, int dtype, const void* X, const float* gamma, float eps,
+               void* Y, void* stream) {
+  ZO_CHECK(rows >= 0 && d >= 8 && d % 8 == 0, "rmsnorm: rows = %lld, d = %d (need d %% 8 == 0)", rows, d);
+  ZO_CHECK(dtype == ZO_F32 || dtype == ZO_BF16 || dtype == ZO_F16, "rmsnorm: bad dtype %d", dtype);
+  ZO_CHECK(isfinite(eps) && eps >= 0.f, "rmsnorm: eps must be finite and >= 0");
+  if (rows == 0) return ZO_OK;
+  ZO_CHECK(X && Y && gamma, "rmsnorm: NULL tensor argument");
+  ZO_CHECK(aligned(X, 16) && aligned(Y, 16) && aligned(gamma, 16),
+           "rmsnorm: X, Y, gamma must be 16-byte aligned");
+  return zo_layernorm_launch(rows, d, dtype, X, gamma, nullptr, eps, Y, (hipStream_t)stream, true);
+}
+
+static int check_rope(long long rows, int seq_len, int d, int heads, int dtype, float base) {
+  ZO_CHECK(rows >= 0 && seq_len >= 1 && rows % seq_len == 0,
+           "rope: rows = %lld, seq_len = %d (need rows %% seq_len == 0)", rows, seq_len);
+  ZO_CHECK(heads >= 1 && d >= 16 && d % heads == 0 && (d / heads) % 16 == 0,
+           "rope: d = %d, heads = %d (need a head dim that is a multiple of 16)", d, heads);
+  ZO_CHECK(isfinite(base) && base > 1.f, "rope: base must be finite and > 1");
+  if (dtype != ZO_BF16 && dtype != ZO_F16) {
+    zo_set_error("rope: dtype %d unsupported (bf16 or fp16)", dtype);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  return ZO_OK;
+}
+
+int zo_rope(long long rows, int seq_len, int d, int heads, int dtype, void* X, float base,
+            void* stream) {
+  int st = check_rope(rows, seq_len, d, heads, dtype, base);
+  if (st != ZO_OK) return st;
+  if (rows == 0) return ZO_OK;
+  ZO_CHECK(X && aligned(X, 16), "rope: X is NULL or not 16-byte aligned");
+  return zo_rope_launch(rows, seq_len, d, heads, dtype, X, base, (hipStream_t)stream);
+}
+
 static int check_attention(int nblk, int T, int seq_len, int d, int heads, int dtype) {
   ZO_CHECK(nblk >= 1 && T >= 1 && seq_len >= 1 && T % seq_len == 0,
            "attention: nblk = %d, T = %d, seq_len = %d (need T %% seq_len == 0)", nblk, T, seq_len);
@@ -348,7 +384,7 @@ struct DecoderWs {
   size_t total;
 };
 // The largest perturbed-linear workspace of the layer's six matrices.
-size_t decoder_lin_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype) {
+static size_t decoder_lin_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype) {
   const int shapes[3][2] = {{d, d}, {ffn, d}, {d, ffn}};
   size_t need = 0;
   for (const auto& sh : shapes) {
@@ -358,7 +394,7 @@ size_t decoder_lin_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype) 
   }
   return need;
 }
-DecoderWs decoder_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype, void* base) {
+static DecoderWs decoder_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype, void* base) {
   const size_t es = dtype == ZO_F32 ? 4 : 2;
   const size_t act = zo_align256((size_t)nblk * T * d * es);
   WsCarver wc(base);
@@ -374,7 +410,7 @@ DecoderWs decoder_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype, v
   w.total = wc.off;
   return w;
 }
-int check_decoder(int T, int seq_len, int d, int heads, int ffn, int r, int q, int nblk, int dtype) {
+static int check_decoder(int T, int seq_len, int d, int heads, int ffn, int r, int q, int nblk, int dtype) {
   int st = check_attention(nblk, T, seq_len, d, heads, dtype);
   if (st != ZO_OK) return st;
   ZO_CHECK(ffn >= 8 && ffn % 8 == 0, "decoder: ffn = %d must be a positive multiple of 8", ffn);
@@ -450,6 +486,102 @@ int zo_decoder_layer_forward(int T, int seq_len, int d, int heads, int ffn, int 
     return st;
   if ((st = lin(&layer->fc1, ffn, d, w.A, Td, w.F, ZO_EPI_RELU, nullptr, 0)) != ZO_OK) return st;
   return lin(&layer->fc2, d, ffn, w.F, Tf, H_out, ZO_EPI_RESIDUAL, w.H2, Td);
+}
+
+namespace {
+struct LlamaWs {
+  char *A, *Qb, *Kb, *Vb, *C, *H2, *G, *F, *lin;
+  size_t total;
+};
+// The largest perturbed-linear workspace of the layer's seven matrices (d x d, ffn x d, d x ffn).
+static LlamaWs llama_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype, void* base) {
+  const size_t es = dtype == ZO_F32 ? 4 : 2;
+  const size_t act = zo_align256((size_t)nblk * T * d * es);
+  const size_t wide = zo_align256((size_t)nblk * T * ffn * es);
+  WsCarver wc(base);
+  LlamaWs w;
+  w.A = (char*)wc.take(act);
+  w.Qb = (char*)wc.take(act);
+  w.Kb = (char*)wc.take(act);
+  w.Vb = (char*)wc.take(act);
+  w.C = (char*)wc.take(act);
+  w.H2 = (char*)wc.take(act);
+  w.G = (char*)wc.take(wide);
+  w.F = (char*)wc.take(wide);
+  w.lin = (char*)wc.take(decoder_lin_ws(T, d, ffn, r, q, nblk, dtype));
+  w.total = wc.off;
+  return w;
+}
+}  // namespace
+
+size_t zo_llama_layer_workspace(int T, int seq_len, int d, int heads, int ffn, int r, int q, int nblk,
+                                int dtype) {
+  if (check_decoder(T, seq_len, d, heads, ffn, r, q, nblk, dtype) != ZO_OK) return 0;
+  if (check_rope((long long)nblk * T, seq_len, d, heads, dtype, 10000.f) != ZO_OK) return 0;
+  return llama_ws(T, d, ffn, r, q, nblk, dtype, nullptr).total;
+}
+
+int zo_llama_layer_forward(int T, int seq_len, int d, int heads, int ffn, int r, int q, int nblk,
+                           const int* blk_query, const int8_t* blk_sign, float eps, float eps_rms,
+                           float rope_base, int dtype, const void* H, long long h_block_stride,
+                           const zo_llama_layer* layer, void* H_out, void* workspace, size_t ws_bytes,
+                           void* stream) {
+  int st = check_decoder(T, seq_len, d, heads, ffn, r, q, nblk, dtype);
+  if (st != ZO_OK) return st;
+  if ((st = check_rope((long long)nblk * T, seq_len, d, heads, dtype, rope_base)) != ZO_OK) return st;
+  ZO_CHECK(layer && H && H_out, "llama: NULL argument (layer, H or H_out)");
+  ZO_CHECK(h_block_stride == 0 || h_block_stride == (long long)T * d,
+           "llama: h_block_stride = %lld must be 0 (one H for every block) or T*d", h_block_stride);
+  ZO_CHECK(isfinite(eps_rms) && eps_rms >= 0.f, "llama: eps_rms must be finite and >= 0");
+  const zo_matrix* mats[7] = {&layer->q, &layer->k, &layer->v, &layer->o, &layer->gate, &layer->up, &layer->down};
+  const char* names[7] = {"q", "k", "v", "o", "gate", "up", "down"};
+  for (int i = 0; i < 7; ++i) {
+    if ((st = check_blocks(q, nblk, blk_query, blk_sign, eps, mats[i]->U, mats[i]->V, mats[i]->Z)) != ZO_OK)
+      return st;
+    ZO_CHECK(mats[i]->W && aligned(mats[i]->W, 16), "llama: %s W is NULL or not 16-byte aligned", names[i]);
+  }
+  ZO_CHECK(layer->rms1_gamma && layer->rms2_gamma, "llama: NULL RMS-norm parameter");
+  ZO_CHECK(aligned(layer->rms1_gamma, 16) && aligned(layer->rms2_gamma, 16),
+           "llama: RMS-norm parameters must be 16-byte aligned");
+  ZO_CHECK(aligned(H, 16) && aligned(H_out, 16), "llama: H and H_out must be 16-byte aligned");
+  const LlamaWs need = llama_ws(T, d, ffn, r, q, nblk, dtype, nullptr);
+  if (!workspace || ws_bytes < need.total) {
+    zo_set_error("llama: workspace %zu bytes < required %zu", ws_bytes, need.total);
+    return ZO_ERR_WORKSPACE;
+  }
+  ZO_CHECK(aligned(workspace, 256), "llama: workspace not 256-byte aligned");
+  const LlamaWs w = llama_ws(T, d, ffn, r, q, nblk, dtype, workspace);
+  hipStream_t s = (hipStream_t)stream;
+  const long long Td = (long long)T * d, Tf = (long long)T * ffn;
+  const long long rows = (long long)nblk * T;
+  const bool shared = h_block_stride == 0;
+  auto lin = [&](const zo_matrix* mt, int m, int n, const void* X, long long xs, void* Y, int epi,
+                 const void* R, long long rs) -> int {
+    PlinearPlan p;
+    zo_plinear_plan(&p, T, m, n, r, q, nblk, xs, dtype, dtype);
+    int e = zo_plinear_prepare(p, blk_query, blk_sign, eps, X, mt->U, mt->V, mt->Z, w.lin, s);
+    if (e != ZO_OK) return e;
+    return zo_plinear_apply(p, X, mt->W, Y, w.lin, s, epi, R, rs);
+  };
+  // A = RMS1(H): once when every block shares H.
+  if ((st = zo_layernorm_launch(shared ? T : rows, d, dtype, H, layer->rms1_gamma, nullptr, eps_rms, w.A, s,
+                                true)) != ZO_OK)
+    return st;
+  const long long as = shared ? 0 : Td;
+  if ((st = lin(&layer->q, d, d, w.A, as, w.Qb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  if ((st = lin(&layer->k, d, d, w.A, as, w.Kb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  if ((st = lin(&layer->v, d, d, w.A, as, w.Vb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  if ((st = zo_rope_launch(rows, seq_len, d, heads, dtype, w.Qb, rope_base, s)) != ZO_OK) return st;
+  if ((st = zo_rope_launch(rows, seq_len, d, heads, dtype, w.Kb, rope_base, s)) != ZO_OK) return st;
+  if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
+    return st;
+  // H2 = H + C Wo'^T;  A = RMS2(H2);  G = A Wg'^T;  F = silu(G) * (A Wu'^T);  H_out = H2 + F Wd'^T.
+  if ((st = lin(&layer->o, d, d, w.C, Td, w.H2, ZO_EPI_RESIDUAL, H, h_block_stride)) != ZO_OK) return st;
+  if ((st = zo_layernorm_launch(rows, d, dtype, w.H2, layer->rms2_gamma, nullptr, eps_rms, w.A, s, true)) != ZO_OK)
+    return st;
+  if ((st = lin(&layer->gate, ffn, d, w.A, Td, w.G, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  if ((st = lin(&layer->up, ffn, d, w.A, Td, w.F, ZO_EPI_SILU_MUL, w.G, Tf)) != ZO_OK) return st;
+  return lin(&layer->down, d, ffn, w.F, Tf, H_out, ZO_EPI_RESIDUAL, w.H2, Td);
 }
 
 // ------------------------------------------------------------------ update

@@ -8,7 +8,8 @@
 // normalisation, the attention, and the host sequence of one layer.
 //
 // k_layernorm: one wave per row, three passes over the row (sum, squared
-// deviations, output), statistics in fp32 with fixed-order wave sums.  Rows of
+// deviations, output; RMS normalisation skips the first), statistics in fp32
+// with fixed-order wave sums.  Rows of
 // up to 8192 elements are read once into registers (k_layernorm_reg, NC
 // 512-element chunks, every load in flight at once); longer rows are re-read
 // by each pass from L1/L2 (k_layernorm).  Both do the same operations in the
@@ -84,8 +85,10 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Rows of d elements (d % 8 == 0), 4 rows per workgroup, one per wave.
-template <int DT>
+// Rows of d elements (d % 8 == 0), 4 rows per workgroup, one per wave.  RMS: no centring
+// (the mean is taken as 0 and the sum pass skipped) and no beta (fmaf with 0 is the rounded
+// product), i.e. x / sqrt(mean(x^2) + eps) * gamma.
+template <int DT, bool RMS>
 __global__ __launch_bounds__(256) void k_layernorm(const void* __restrict__ X,
                                                    const float* __restrict__ gamma,
                                                    const float* __restrict__ beta, void* Y,
@@ -95,13 +98,16 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* __restrict__ X,
   const int lane = threadIdx.x & 63;
   const size_t base = (size_t)row * d;
   float v[8];
-  float s = 0.f;
-  for (int c = lane * 8; c < d; c += 512) {
-    load8<DT>(X, base + c, v);
+  float mean = 0.f;
+  if constexpr (!RMS) {
+    float s = 0.f;
+    for (int c = lane * 8; c < d; c += 512) {
+      load8<DT>(X, base + c, v);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s += v[e];
+      for (int e = 0; e < 8; ++e) s += v[e];
+    }
+    mean = wave_sum(s) / (float)d;
   }
-  const float mean = wave_sum(s) / (float)d;
   float q = 0.f;
   for (int c = lane * 8; c < d; c += 512) {
     load8<DT>(X, base + c, v);
@@ -112,7 +118,11 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* __restrict__ X,
   for (int c = lane * 8; c < d; c += 512) {
     load8<DT>(X, base + c, v);
     const f32x4 g0 = *(const f32x4*)(gamma + c), g1 = *(const f32x4*)(gamma + c + 4);
-    const f32x4 b0 = *(const f32x4*)(beta + c), b1 = *(const f32x4*)(beta + c + 4);
+    f32x4 b0 = {0.f, 0.f, 0.f, 0.f}, b1 = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (!RMS) {
+      b0 = *(const f32x4*)(beta + c);
+      b1 = *(const f32x4*)(beta + c + 4);
+    }
     const float g[8] = {g0[0], g0[1], g0[2], g0[3], g1[0], g1[1], g1[2], g1[3]};
     const float b[8] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
 #pragma unroll
@@ -141,7 +151,7 @@ struct Raw8 {
   }
 };
 
-template <int DT, int NC>
+template <int DT, int NC, bool RMS>
 __global__ __launch_bounds__(256) void k_layernorm_reg(const void* __restrict__ X,
                                                        const float* __restrict__ gamma,
                                                        const float* __restrict__ beta, void* Y,
@@ -156,15 +166,18 @@ __global__ __launch_bounds__(256) void k_layernorm_reg(const void* __restrict__ 
     const int c = lane * 8 + 512 * k;
     if (c < d) v[k].load(X, base + c);
   }
-  float s = 0.f;
+  float mean = 0.f;
+  if constexpr (!RMS) {
+    float s = 0.f;
 #pragma unroll
-  for (int k = 0; k < NC; ++k) {
-    if (lane * 8 + 512 * k < d) {
+    for (int k = 0; k < NC; ++k) {
+      if (lane * 8 + 512 * k < d) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s += v[k].at(e);
+        for (int e = 0; e < 8; ++e) s += v[k].at(e);
+      }
     }
+    mean = wave_sum(s) / (float)d;
   }
-  const float mean = wave_sum(s) / (float)d;
   float q = 0.f;
 #pragma unroll
   for (int k = 0; k < NC; ++k) {
@@ -179,7 +192,11 @@ __global__ __launch_bounds__(256) void k_layernorm_reg(const void* __restrict__ 
     const int c = lane * 8 + 512 * k;
     if (c < d) {
       const f32x4 g0 = *(const f32x4*)(gamma + c), g1 = *(const f32x4*)(gamma + c + 4);
-      const f32x4 b0 = *(const f32x4*)(beta + c), b1 = *(const f32x4*)(beta + c + 4);
+      f32x4 b0 = {0.f, 0.f, 0.f, 0.f}, b1 = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (!RMS) {
+        b0 = *(const f32x4*)(beta + c);
+        b1 = *(const f32x4*)(beta + c + 4);
+      }
       const float g[8] = {g0[0], g0[1], g0[2], g0[3], g1[0], g1[1], g1[2], g1[3]};
       const float b[8] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
       float o[8];
@@ -187,6 +204,49 @@ __global__ __launch_bounds__(256) void k_layernorm_reg(const void* __restrict__ 
       for (int e = 0; e < 8; ++e) o[e] = fmaf((v[k].at(e) - mean) * rstd, g[e], b[e]);
       store8<DT>(Y, base + c, o);
     }
+  }
+}
+
+// Rotary positions, in place.  A thread owns 8 dimensions i of the first half of one head
+// (and their partners dh/2 further on) in ROPE_RB consecutive rows.  The frequency
+// 2^(i k), k = -2 log2(base) / dh, is formed once per thread in fp64; each angle p 2^(i k)
+// is formed and reduced to [-pi, pi] in fp64, so that sincosf sees an argument that is
+// exact to fp32 rounding at any position (a direct fp32 product p * theta would carry an
+// absolute error of about p * 2^-24 radians: 2.4e-4 at p = 4095, a quarter of a bf16 ulp).
+constexpr int ROPE_RB = 8;
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_rope(void* X, long long rows, int seq_len, int d, int dh, double k) {
+  const int cpr = d / 16;   // (head, 8-dimension chunk) pairs per row
+  const int cph = dh / 16;  // chunks per half head
+  const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
+  const long long groups = (rows + ROPE_RB - 1) / ROPE_RB;
+  if (t >= groups * cpr) return;
+  const int cc = (int)(t % cpr);
+  const int h = cc / cph, c = cc % cph;
+  const long long r0 = (t / cpr) * ROPE_RB;
+  const long long r1 = r0 + ROPE_RB < rows ? r0 + ROPE_RB : rows;
+  double theta[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) theta[e] = exp2((double)(8 * c + e) * k);
+  constexpr double kTwoPi = 6.283185307179586, kInvTwoPi = 0.15915494309189535;
+  for (long long row = r0; row < r1; ++row) {
+    const double pos = (double)(row % seq_len);
+    const size_t ia = (size_t)row * d + (size_t)h * dh + 8 * c, ib = ia + dh / 2;
+    float a[8], b[8], na[8], nb[8];
+    load8<DT>(X, ia, a);
+    load8<DT>(X, ib, b);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const double ang = pos * theta[e];
+      const float red = (float)fma(-rint(ang * kInvTwoPi), kTwoPi, ang);
+      float sn, cs;
+      sincosf(red, &sn, &cs);
+      na[e] = a[e] * cs - b[e] * sn;
+      nb[e] = b[e] * cs + a[e] * sn;
+    }
+    store8<DT>(X, ia, na);
+    store8<DT>(X, ib, nb);
   }
 }
 
@@ -425,36 +485,64 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
 }
 
 // Register-resident rows in buckets of 2, 4, 8, 10 or 16 chunks of 512; longer rows re-read.
-template <int DT>
+template <int DT, bool RMS>
 void layernorm_dispatch(dim3 grid, dim3 block, hipStream_t stream, const void* X, const float* gamma,
                         const float* beta, void* Y, long long rows, int d, float eps_ln) {
   if (d <= 1024)
-    hipLaunchKernelGGL((k_layernorm_reg<DT, 2>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 2, RMS>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else if (d <= 2048)
-    hipLaunchKernelGGL((k_layernorm_reg<DT, 4>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 4, RMS>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else if (d <= 4096)
-    hipLaunchKernelGGL((k_layernorm_reg<DT, 8>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 8, RMS>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else if (d <= 5120)
-    hipLaunchKernelGGL((k_layernorm_reg<DT, 10>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 10, RMS>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else if (d <= 8192)
-    hipLaunchKernelGGL((k_layernorm_reg<DT, 16>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    hipLaunchKernelGGL((k_layernorm_reg<DT, 16, RMS>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else
-    hipLaunchKernelGGL(k_layernorm<DT>, grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    hipLaunchKernelGGL((k_layernorm<DT, RMS>), grid, block, 0, stream, X, gamma, beta, Y, rows, d, eps_ln);
+}
+
+template <int DT>
+void layernorm_dispatch_rms(bool rms, dim3 grid, dim3 block, hipStream_t stream, const void* X,
+                            const float* gamma, const float* beta, void* Y, long long rows, int d,
+                            float eps_ln) {
+  if (rms)
+    layernorm_dispatch<DT, true>(grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
+  else
+    layernorm_dispatch<DT, false>(grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
 }
 
 }  // namespace
 
 int zo_layernorm_launch(long long rows, int d, int dtype, const void* X, const float* gamma,
-                        const float* beta, float eps_ln, void* Y, hipStream_t stream) {
+                        const float* beta, float eps_ln, void* Y, hipStream_t stream, bool rms) {
   if (rows <= 0) return ZO_OK;
   const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
   if (dtype == ZO_BF16)
-    layernorm_dispatch<ZO_BF16>(grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    layernorm_dispatch_rms<ZO_BF16>(rms, grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else if (dtype == ZO_F16)
-    layernorm_dispatch<ZO_F16>(grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    layernorm_dispatch_rms<ZO_F16>(rms, grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
   else
-    layernorm_dispatch<ZO_F32>(grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
+    layernorm_dispatch_rms<ZO_F32>(rms, grid, block, stream, X, gamma, beta, Y, rows, d, eps_ln);
   return zo_hip_status(hipGetLastError(), "k_layernorm");
+}
+
+int zo_rope_launch(long long rows, int seq_len, int d, int heads, int dtype, void* X, float base,
+                   hipStream_t stream) {
+  const int dh = d / heads;
+  const long long threads = (rows + ROPE_RB - 1) / ROPE_RB * (d / 16);
+  if (threads <= 0) return ZO_OK;
+  const long long wg = (threads + 255) / 256;
+  if (wg > 0x7fffffffLL) {
+    zo_set_error("rope: too many rows (%lld)", rows);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  const double k = -2.0 * log2((double)base) / (double)dh;
+  if (dtype == ZO_BF16)
+    hipLaunchKernelGGL(k_rope<ZO_BF16>, dim3((unsigned)wg), dim3(256), 0, stream, X, rows, seq_len, d, dh, k);
+  else
+    hipLaunchKernelGGL(k_rope<ZO_F16>, dim3((unsigned)wg), dim3(256), 0, stream, X, rows, seq_len, d, dh, k);
+  return zo_hip_status(hipGetLastError(), "k_rope");
 }
 
 int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int dtype, const void* Q,

@@ -61,7 +61,7 @@ struct GemmArgs {
   long long y_block_stride;
   int ldy, out_dtype;          // zo_dtype of Y
   int epi;                     // zo_epilogue
-  const void* R;               // ZO_EPI_RESIDUAL: added to Y, same type and layout (ldy)
+  const void* R;               // ZO_EPI_RESIDUAL / SILU_MUL: same type and layout as Y (ldy)
   long long r_block_stride;    // elements; 0 = one R shared by all blocks
   int tiles_a, tiles_b, total_tiles;
 };
@@ -78,27 +78,42 @@ __device__ __forceinline__ void store4(char* base, size_t idx, float v0, float v
     *(f32x4*)(base + idx * 4) = (f32x4){v0, v1, v2, v3};
 }
 
+// Four OUT-typed values at element idx.. as fp32.
+template <int OUT>
+__device__ __forceinline__ f32x4 load4(const char* base, size_t idx) {
+  if constexpr (OUT == ZO_F32) {
+    return *(const f32x4*)(base + idx * 4);
+  } else {
+    const u32x2 r = *(const u32x2*)(base + idx * 2);
+    if constexpr (OUT == ZO_BF16)
+      return (f32x4){bf16_to_f32((bf16_t)r[0]), bf16_to_f32((bf16_t)(r[0] >> 16)),
+                     bf16_to_f32((bf16_t)r[1]), bf16_to_f32((bf16_t)(r[1] >> 16))};
+    else
+      return (f32x4){f16_to_f32((uint16_t)r[0]), f16_to_f32((uint16_t)(r[0] >> 16)),
+                     f16_to_f32((uint16_t)r[1]), f16_to_f32((uint16_t)(r[1] >> 16))};
+  }
+}
+
 // Four OUT-typed values at element idx.. as fp32, added to v0..v3.
 template <int OUT>
 __device__ __forceinline__ void add4(const char* base, size_t idx, float& v0, float& v1, float& v2,
                                      float& v3) {
-  if constexpr (OUT == ZO_F32) {
-    const f32x4 r = *(const f32x4*)(base + idx * 4);
-    v0 += r[0]; v1 += r[1]; v2 += r[2]; v3 += r[3];
-  } else {
-    const u32x2 r = *(const u32x2*)(base + idx * 2);
-    if constexpr (OUT == ZO_BF16) {
-      v0 += bf16_to_f32((bf16_t)r[0]); v1 += bf16_to_f32((bf16_t)(r[0] >> 16));
-      v2 += bf16_to_f32((bf16_t)r[1]); v3 += bf16_to_f32((bf16_t)(r[1] >> 16));
-    } else {
-      v0 += f16_to_f32((uint16_t)r[0]); v1 += f16_to_f32((uint16_t)(r[0] >> 16));
-      v2 += f16_to_f32((uint16_t)r[1]); v3 += f16_to_f32((uint16_t)(r[1] >> 16));
-    }
-  }
+  const f32x4 r = load4<OUT>(base, idx);
+  v0 += r[0]; v1 += r[1]; v2 += r[2]; v3 += r[3];
 }
 
-// The fused epilogue on four fp32 accumulator values, then the store: ReLU, or the
-// residual R (same layout as Y) added before the single rounding to OUT.
+__device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
+
+// v0..v3 multiplied by silu of the four OUT-typed values at element idx.. (fp32).
+template <int OUT>
+__device__ __forceinline__ void mul4_silu(const char* base, size_t idx, float& v0, float& v1, float& v2,
+                                          float& v3) {
+  const f32x4 r = load4<OUT>(base, idx);
+  v0 *= silu(r[0]); v1 *= silu(r[1]); v2 *= silu(r[2]); v3 *= silu(r[3]);
+}
+
+// The fused epilogue on four fp32 accumulator values, then the store: ReLU, the residual R
+// (same layout as Y) added, or the product with silu(R), before the single rounding to OUT.
 template <int OUT, int EPI>
 __device__ __forceinline__ void finish4(char* Yb, const char* Rb, size_t idx, float v0, float v1,
                                         float v2, float v3) {
@@ -106,6 +121,8 @@ __device__ __forceinline__ void finish4(char* Yb, const char* Rb, size_t idx, fl
     v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f);
   } else if constexpr (EPI == ZO_EPI_RESIDUAL) {
     add4<OUT>(Rb, idx, v0, v1, v2, v3);
+  } else if constexpr (EPI == ZO_EPI_SILU_MUL) {
+    mul4_silu<OUT>(Rb, idx, v0, v1, v2, v3);
   }
   store4<OUT>(Yb, idx, v0, v1, v2, v3);
 }
@@ -119,6 +136,8 @@ __device__ __forceinline__ void finish4_epi(char* Yb, const char* Rb, size_t idx
     finish4<OUT, ZO_EPI_RELU>(Yb, Rb, idx, v0, v1, v2, v3);
   else if (epi == ZO_EPI_RESIDUAL)
     finish4<OUT, ZO_EPI_RESIDUAL>(Yb, Rb, idx, v0, v1, v2, v3);
+  else if (epi == ZO_EPI_SILU_MUL)
+    finish4<OUT, ZO_EPI_SILU_MUL>(Yb, Rb, idx, v0, v1, v2, v3);
   else
     finish4<OUT, ZO_EPI_NONE>(Yb, Rb, idx, v0, v1, v2, v3);
 }
@@ -389,6 +408,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
       float v = acc[i][j];
       if (a.epi == ZO_EPI_RELU) v = fmaxf(v, 0.f);
       if (a.epi == ZO_EPI_RESIDUAL) v += R[(size_t)tok * a.ldy + col];
+      if (a.epi == ZO_EPI_SILU_MUL) v *= silu(R[(size_t)tok * a.ldy + col]);
       Y[(size_t)tok * a.ldy + col] = v;
     }
   }
@@ -732,6 +752,8 @@ void launch_main_epi(const GemmArgs& a, dim3 grid, hipStream_t stream) {
     hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_RELU>), grid, dim3(256), 0, stream, a);
   else if (a.epi == ZO_EPI_RESIDUAL)
     hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_RESIDUAL>), grid, dim3(256), 0, stream, a);
+  else if (a.epi == ZO_EPI_SILU_MUL)
+    hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_SILU_MUL>), grid, dim3(256), 0, stream, a);
   else
     hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_NONE>), grid, dim3(256), 0, stream, a);
 }

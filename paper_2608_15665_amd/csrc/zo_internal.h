@@ -128,7 +128,9 @@ int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t*
                        const float* Z, void* ws, hipStream_t stream);
 // Decoder-layer pieces (zo_decoder.hip).
 int zo_layernorm_launch(long long rows, int d, int dtype, const void* X, const float* gamma,
-                        const float* beta, float eps_ln, void* Y, hipStream_t stream);
+                        const float* beta, float eps_ln, void* Y, hipStream_t stream, bool rms = false);
+int zo_rope_launch(long long rows, int seq_len, int d, int heads, int dtype, void* X, float base,
+                   hipStream_t stream);
 int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int dtype, const void* Q,
                         const void* K, const void* V, void* O, hipStream_t stream);
 int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,

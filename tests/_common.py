@@ -54,3 +54,50 @@ def host(t):
     if t.dtype == torch.bfloat16:
         return host_bf16_values(t)
     return t.detach().cpu().numpy().astype(np.float64)
+
+
+def cast(a64, dt):
+    """(device tensor, exact float64 values) of a float64 array in dtype dt."""
+    if dt == "bf16":
+        bits, v = zd.as_bf16_values(a64)
+        return dev_bf16(bits), v
+    if dt == "f16":
+        h, v = zd.as_f16_values(a64)
+        return dev_f16(h), v
+    v = zd.f32(a64).astype(np.float64)
+    return dev_f32(v), v
+
+
+def rnd(dt):
+    """The oracle's rounding of a stored activation of type dt."""
+    import oracle
+    return oracle.round_f16 if dt == "f16" else oracle.round_bf16
+
+
+def check16(got, ref, what):
+    """The bar of one 16-bit rounding of a kernel's output: floored relative error <= 1e-2 at
+    floor 1e-3 rms, normwise <= 2e-3."""
+    assert ferr(got, ref, 1e-3) <= 1e-2, what
+    assert normwise(got, ref) <= 2e-3, what
+
+
+def ulp16(x, dt):
+    """Spacing of 16-bit values (fp16 with its subnormals, or bf16) at |x|."""
+    e = np.frexp(x)[1]
+    return np.ldexp(1.0, np.maximum(e - 11, -24)) if dt == "f16" else np.ldexp(1.0, e - 8)
+
+
+def check_attention(got, Q, K, V, heads, seq_len, dt, what):
+    """Causal attention held to the bar its arithmetic sets.  P enters the P V product as a
+    hi + lo pair of 16-bit values (relative error <= 2^-17 for bf16 pairs, less for fp16), and
+    the fp32 logits carry an absolute error of a few 2^-24 |q| |k|, which moves P by under
+    2^-16 relative at logits of a few hundred.  So before its rounding each output is within
+    2^-14 softmax(S) |V| (the same average taken of |V|, with margin) of the exact one, and
+    after it within one ulp more; blockwise it keeps the normwise bar of a single rounding."""
+    import oracle
+    ref = oracle.causal_attention(Q, K, V, heads, seq_len)
+    mag = oracle.causal_attention(Q, K, np.abs(V), heads, seq_len)
+    assert normwise(got, ref) <= 2e-3, what
+    bound = ulp16(ref, dt) + 2.0 ** -14 * mag
+    err = np.abs(np.asarray(got, np.float64) - ref)
+    assert np.all(err <= bound), (what, float(np.max(err / bound)))

@@ -245,6 +245,46 @@ def test_decoder_entry_points_validation():
     assert st == 1 and "h_block_stride" in _detail()
 
 
+def test_llama_entry_points_validation():
+    """RMS norm, rotary positions and the LLaMA-family layer reject bad arguments before
+    launching anything (no GPU touched)."""
+    L = zo.lib()
+    fake = 1 << 20
+    assert L.zo_rmsnorm(4, 12, 1, fake, fake, 1e-6, fake, None) == 1 and "d % 8" in _detail()
+    assert L.zo_rmsnorm(4, 16, 7, fake, fake, 1e-6, fake, None) == 1 and "dtype" in _detail()
+    assert L.zo_rmsnorm(4, 16, 1, fake, fake, float("nan"), fake, None) == 1 and "eps" in _detail()
+    assert L.zo_rmsnorm(4, 16, 1, fake, None, 1e-6, fake, None) == 1 and "NULL" in _detail()
+    assert L.zo_rmsnorm(4, 16, 1, fake + 2, fake, 1e-6, fake, None) == 1 and "aligned" in _detail()
+    assert L.zo_rope(100, 30, 256, 2, 1, fake, 1e4, None) == 1 and "seq_len" in _detail()
+    assert L.zo_rope(64, 64, 256, 32, 1, fake, 1e4, None) == 1 and "head dim" in _detail()  # dh = 8
+    assert L.zo_rope(0, 64, 240, 3, 1, None, 1e4, None) == 0   # dh = 80 passes the checks (nothing to do)
+    assert L.zo_rope(64, 64, 256, 2, 1, fake, 1.0, None) == 1 and "base" in _detail()
+    assert L.zo_rope(64, 64, 256, 2, 0, fake, 1e4, None) == 2 and "dtype" in _detail()  # fp32
+    assert L.zo_rope(64, 64, 256, 2, 1, fake + 2, 1e4, None) == 1 and "aligned" in _detail()
+    assert L.zo_llama_layer_workspace(128, 64, 256, 2, 512, 8, 2, 4, 1) > 0
+    assert L.zo_llama_layer_workspace(128, 64, 256, 2, 512, 8, 2, 4, 2) > 0
+    assert L.zo_llama_layer_workspace(128, 64, 256, 2, 512, 8, 2, 4, 0) == 0   # fp32: no attention kernel
+    assert L.zo_llama_layer_workspace(128, 60, 256, 2, 512, 8, 2, 4, 1) == 0   # T % seq_len
+    assert L.zo_llama_layer_workspace(128, 64, 256, 2, 500, 8, 2, 4, 1) == 0   # ffn % 8
+    # the LLaMA workspace holds the gate output beside the decoder's buffers
+    assert (L.zo_llama_layer_workspace(128, 64, 256, 2, 512, 8, 2, 4, 1)
+            > L.zo_decoder_layer_workspace(128, 64, 256, 2, 512, 8, 2, 4, 1))
+    layer = zo._lib.LlamaLayerDesc()
+    bq4 = (ctypes.c_int * 4)(0, 0, 1, 1)
+    bs4 = (ctypes.c_int8 * 4)(1, -1, 1, -1)
+    args = (128, 64, 256, 2, 512, 8, 2, 4, bq4, bs4, 1e-3, 1e-6, 1e4, 1, fake)
+    st = L.zo_llama_layer_forward(*args, 0, ctypes.byref(layer), fake, fake, 1 << 40, None)
+    assert st == 1 and "NULL" in _detail()  # the matrices of the layer are NULL
+    st = L.zo_llama_layer_forward(*args, 5, ctypes.byref(layer), fake, fake, 1 << 40, None)
+    assert st == 1 and "h_block_stride" in _detail()
+    bad_base = args[:12] + (0.5,) + args[13:]
+    st = L.zo_llama_layer_forward(*bad_base, 0, ctypes.byref(layer), fake, fake, 1 << 40, None)
+    assert st == 1 and "base" in _detail()
+    bad_rms = args[:11] + (-1.0,) + args[12:]
+    st = L.zo_llama_layer_forward(*bad_rms, 0, ctypes.byref(layer), fake, fake, 1 << 40, None)
+    assert st == 1 and "eps_rms" in _detail()
+
+
 def test_empty_calls_are_no_ops():
     """count = 0 refreshes and updates, and zero-row layer norms, succeed without launching."""
     L = zo.lib()
@@ -254,3 +294,5 @@ def test_empty_calls_are_no_ops():
     assert L.zo_subspace_adam_update(0, None, 1, 4, 2, fake, 1, 1e-2, 0.9, 0.95, 1e-8, None, None, 0, None) == 0
     assert L.zo_subspace_sgd_update(0, None, 1, 4, 2, fake, 1e-2, None, None, 0, None) == 0
     assert L.zo_layernorm(0, 64, 1, None, None, None, 1e-5, None, None) == 0
+    assert L.zo_rmsnorm(0, 64, 1, None, None, 1e-6, None, None) == 0
+    assert L.zo_rope(0, 64, 256, 2, 1, None, 1e4, None) == 0
