@@ -196,9 +196,11 @@ def attention_flops(T, seq_len, heads, dh, nblk):
 
 def run_decoder(args):
     """One SubZero+ step through real decoder layers: refresh (t mod F == 0), for every layer the
-    forward of all 2q blocks (zo_decoder_layer_forward: layer norm, the six perturbed linears
-    with fused ReLU / residuals, causal attention), the squared loss of the last hidden state
-    against a fixed target, the estimate, and the subspace Adam update of all 6 L matrices."""
+    forward of all 2q blocks (OPT family, zo_decoder_layer_forward: layer norm, the six perturbed
+    linears with fused ReLU / residuals, causal attention; LLaMA family, zo_llama_layer_forward:
+    RMS norm, rotary positions, the seven perturbed linears with the SwiGLU product and the
+    residuals fused), the squared loss of the last hidden state against a fixed target, the
+    estimate, and the subspace Adam update of every matrix of every layer."""
     import numpy as np
     import torch
 
@@ -208,8 +210,9 @@ def run_decoder(args):
     cfg = zd.CONFIGS[args.config]
     dec = cfg.get("decoder")
     if not dec:
-        print(f"bench.py: --model decoder needs an OPT-shaped config (got {args.config})", file=sys.stderr)
+        print(f"bench.py: --model decoder has no layer shape for {args.config}", file=sys.stderr)
         sys.exit(2)
+    llama = dec.get("family") == "llama"
     T, r, q = cfg["T"], cfg["r"], cfg["q"]
     if args.queries:
         q = args.queries
@@ -235,7 +238,12 @@ def run_decoder(args):
             return torch.from_numpy(zd.as_f16_values(a64)[0]).to(dev)
         return torch.from_numpy(zd.bf16_bits(zd.f32(a64)).view(np.int16)).view(dt16).to(dev)
 
-    shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "fc1": (ffn, d), "fc2": (d, ffn)}
+    if llama:
+        shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "gate": (ffn, d), "up": (ffn, d),
+                  "down": (d, ffn)}
+    else:
+        shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "fc1": (ffn, d), "fc2": (d, ffn)}
+    nper = len(shapes)
     Wbase = {sh: to16(zd.draw(seed, "W0", sh, sh, 0.02)) for sh in set(shapes.values())}
     rows_set = sorted({d, ffn})
     Obase = {rw: torch.from_numpy(zd.f32(zd.draw(seed, "OMEGA_U", (rw, r), (rw, r)))).to(dev) for rw in rows_set}
@@ -244,7 +252,7 @@ def run_decoder(args):
     for l in range(layers):
         lm = {}
         for nm, (m, n) in shapes.items():
-            idx = len(mats) * 6 + len(lm)
+            idx = len(mats) * nper + len(lm)
             u = dict(W=torch.roll(Wbase[(m, n)], l, 0).contiguous(),
                      U=torch.empty((m, r), dtype=torch.float32, device=dev),
                      V=torch.empty((n, r), dtype=torch.float32, device=dev),
@@ -256,10 +264,13 @@ def run_decoder(args):
             lm[nm] = u
         mats.append(lm)
         g = torch.from_numpy(zd.f32(1.0 + 0.05 * zd.draw(seed, "W0", (l, 1), (4, d)))).to(dev)
-        lns.append(dict(ln1_gamma=g[0].contiguous(), ln1_beta=(g[1] - 1.0).contiguous(),
-                        ln2_gamma=g[2].contiguous(), ln2_beta=(g[3] - 1.0).contiguous()))
+        if llama:
+            lns.append(dict(rms1_gamma=g[0].contiguous(), rms2_gamma=g[2].contiguous()))
+        else:
+            lns.append(dict(ln1_gamma=g[0].contiguous(), ln1_beta=(g[1] - 1.0).contiguous(),
+                            ln2_gamma=g[2].contiguous(), ln2_beta=(g[3] - 1.0).contiguous()))
     del Wbase, Obase
-    nmat = 6 * layers
+    nmat = nper * layers
     Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(nmat)])
                                    for t in range(nsteps)])).to(dev)  # [step, matrix, q, r, r]
     H0 = to16(zd.draw(seed, "X", (T, d, 0), (T, d)))
@@ -267,11 +278,14 @@ def run_decoder(args):
     Hbuf = [torch.empty((nblk * T, d), dtype=dt16, device=dev) for _ in range(2)]
 
     def layer_obj(t, l):
-        lm = {nm: dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, 6 * l + i]) for i, (nm, u) in enumerate(mats[l].items())}
+        lm = {nm: dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, nper * l + i])
+              for i, (nm, u) in enumerate(mats[l].items())}
+        if llama:
+            return zo.LlamaLayer(lm, lns[l], bq, bs, eps, T, L, heads)
         return zo.DecoderLayer(lm, lns[l], bq, bs, eps, T, L, heads)
 
     decs = [[layer_obj(t, l) for l in range(layers)] for t in range(nsteps)]
-    items = [[dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, 6 * l + i], M1=u["M1"], M2=u["M2"])
+    items = [[dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, nper * l + i], M1=u["M1"], M2=u["M2"])
               for l in range(layers) for i, u in enumerate(mats[l].values())] for t in range(nsteps)]
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s; {layers} decoder layers; "
@@ -334,16 +348,22 @@ def run_decoder(args):
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round((t1 - t0) / args.steps * 1e3, 2), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": args.dtype, "data": "synthetic",
-        "config": {"workload": (f"{args.config}-shaped decoder: {layers} pre-LN layers (d={d}, {heads} heads of "
-                                f"{d // heads}, ffn={ffn}, ReLU), every q, k, v, o, fc1, fc2 perturbed; "
+        "config": {"workload": (f"{args.config}-shaped decoder: {layers} "
+                                + ("pre-norm LLaMA-family layers (RMS norm, rotary positions, " if llama
+                                   else "pre-LN layers (")
+                                + f"d={d}, {heads} heads of {d // heads}, ffn={ffn}, "
+                                + ("SwiGLU), every q, k, v, o, gate, up, down perturbed; " if llama
+                                   else "ReLU), every q, k, v, o, fc1, fc2 perturbed; ")
                                 + (f"{nblk} blocks (baseline + q={q} forward queries)" if forward
                                    else f"{nblk} query blocks (q={q}, +/-)")
                                 + f" of T={T} tokens ({T // L} sequences x {L}); r={r}; {args.dtype}; "
                                   "value counts the perturbed-linear FLOPs of the step"),
                    "layers": layers, "d": d, "heads": heads, "ffn": ffn, "seq_len": L, "T": T, "r": r, "q": q,
                    "blocks": nblk, "estimator": args.estimator, "refresh_every": F},
-        "roofline": {"kernel": "zo_decoder_layer_forward (one layer: 2 layer norms, 6 fused perturbed GEMMs "
-                               "with their projections, causal attention)", "bound": "mfma",
+        "roofline": {"kernel": ("zo_llama_layer_forward (one layer: 2 RMS norms, 2 rotations, 7 fused "
+                                "perturbed GEMMs with their projections, causal attention)" if llama else
+                                "zo_decoder_layer_forward (one layer: 2 layer norms, 6 fused perturbed GEMMs "
+                                "with their projections, causal attention)"), "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "launches": len(layer_ms), "avg_launch_ms": round(avg_layer, 4),
@@ -371,7 +391,8 @@ def main():
                     help="weights and activations (fp16: the paper's precision for OPT-13B)")
     ap.add_argument("--model", default="stack", choices=["stack", "decoder"],
                     help="stack: the perturbed linears of every matrix on synthetic activations; decoder: "
-                         "real pre-LN decoder-layer forwards (layer norm, causal attention, ReLU MLP, residuals)")
+                         "real decoder-layer forwards (OPT: layer norm, causal attention, ReLU MLP; llama-7b: "
+                         "RMS norm, rotary positions, causal attention, SwiGLU MLP; residuals)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")

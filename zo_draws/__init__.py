@@ -180,7 +180,8 @@ CONFIGS = {
                        [("q", 4096, 4096), ("k", 4096, 4096), ("v", 4096, 4096),
                         ("o", 4096, 4096), ("gate", 11008, 4096), ("up", 11008, 4096),
                         ("down", 4096, 11008)],
-                       T=4096, r=32, q=4),
+                       T=4096, r=32, q=4,
+                       decoder=dict(d=4096, heads=32, ffn=11008, seq_len=256, family="llama")),  # 16 x 256
     "opt-13b": _stack("opt-13b", 40,
                       [("q", 5120, 5120), ("k", 5120, 5120), ("v", 5120, 5120),
                        ("o", 5120, 5120), ("fc1", 20480, 5120), ("fc2", 5120, 20480)],
