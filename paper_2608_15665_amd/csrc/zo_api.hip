@@ -380,7 +380,7 @@ int zo_causal_attention(int nblk, int T, int seq_len, int d, int heads, int dtyp
 
 namespace {
 struct DecoderWs {
-  char *A, *Qb, *Kb, *Vb, *C, *H2, *F, *lin;
+  char *A, *Qb, *Kb, *Vb, *C, *H2, *F, *lin[3], *grp;
   size_t total;
 };
 // The largest perturbed-linear workspace of the layer's six matrices.
@@ -394,6 +394,12 @@ static size_t decoder_lin_ws(int T, int d, int ffn, int r, int q, int nblk, int 
   }
   return need;
 }
+// The stacked projection of q, k, v (three matrices reading A, n = d).
+static size_t decoder_grp_ws(int T, int d, int r, int q, int nblk, int dtype) {
+  PlinearPlan p;
+  zo_plinear_plan(&p, T, d, d, r, q, nblk, (long long)T * d, dtype, dtype);
+  return zo_plinear_group_ws(p, 3);
+}
 static DecoderWs decoder_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype, void* base) {
   const size_t es = dtype == ZO_F32 ? 4 : 2;
   const size_t act = zo_align256((size_t)nblk * T * d * es);
@@ -406,7 +412,9 @@ static DecoderWs decoder_ws(int T, int d, int ffn, int r, int q, int nblk, int d
   w.C = (char*)wc.take(act);
   w.H2 = (char*)wc.take(act);
   w.F = (char*)wc.take((size_t)nblk * T * ffn * es);
-  w.lin = (char*)wc.take(decoder_lin_ws(T, d, ffn, r, q, nblk, dtype));
+  const size_t lin = decoder_lin_ws(T, d, ffn, r, q, nblk, dtype);
+  for (auto& l : w.lin) l = (char*)wc.take(lin);
+  w.grp = (char*)wc.take(decoder_grp_ws(T, d, r, q, nblk, dtype));
   w.total = wc.off;
   return w;
 }
@@ -417,6 +425,28 @@ static int check_decoder(int T, int seq_len, int d, int heads, int ffn, int r, i
   if ((st = check_plinear(T, d, d, r, q, nblk, (long long)T * d, dtype)) != ZO_OK) return st;
   if ((st = check_plinear(T, ffn, d, r, q, nblk, (long long)T * d, dtype)) != ZO_OK) return st;
   return check_plinear(T, d, ffn, r, q, nblk, (long long)T * ffn, dtype);
+}
+// Perturbed linears of one shape that read the same X: one stacked projection of X against
+// all their V factors, then each one's fused GEMM in order (epilogue epi[i] with R[i], rs[i];
+// a later one may read an earlier one's output as its R).
+static int lin_group(int T, int m, int n, int r, int q, int nblk, long long xs, int dtype,
+                     const int* blk_query, const int8_t* blk_sign, float eps, const void* X, int count,
+                     const zo_matrix* const* mats, void* const* Y, const int* epi, const void* const* R,
+                     const long long* rs, char* const* lin, void* grp, hipStream_t s) {
+  PlinearPlan p[3];
+  const float *U[3], *V[3], *Z[3];
+  void* ws[3];
+  for (int i = 0; i < count; ++i) {
+    zo_plinear_plan(&p[i], T, m, n, r, q, nblk, xs, dtype, dtype);
+    U[i] = mats[i]->U;
+    V[i] = mats[i]->V;
+    Z[i] = mats[i]->Z;
+    ws[i] = lin[i];
+  }
+  int st = zo_plinear_prepare_group(p, count, blk_query, blk_sign, eps, X, U, V, Z, ws, grp, s);
+  for (int i = 0; i < count && st == ZO_OK; ++i)
+    st = zo_plinear_apply(p[i], X, mats[i]->W, Y[i], ws[i], s, epi[i], R[i], rs[i]);
+  return st;
 }
 }  // namespace
 
@@ -465,18 +495,26 @@ int zo_decoder_layer_forward(int T, int seq_len, int d, int heads, int ffn, int 
                  const void* R, long long rs) -> int {
     PlinearPlan p;
     zo_plinear_plan(&p, T, m, n, r, q, nblk, xs, dtype, dtype);
-    int e = zo_plinear_prepare(p, blk_query, blk_sign, eps, X, mt->U, mt->V, mt->Z, w.lin, s);
+    int e = zo_plinear_prepare(p, blk_query, blk_sign, eps, X, mt->U, mt->V, mt->Z, w.lin[0], s);
     if (e != ZO_OK) return e;
-    return zo_plinear_apply(p, X, mt->W, Y, w.lin, s, epi, R, rs);
+    return zo_plinear_apply(p, X, mt->W, Y, w.lin[0], s, epi, R, rs);
   };
   // A = LN1(H): once when every block shares H.
   if ((st = zo_layernorm_launch(shared ? T : (long long)nblk * T, d, dtype, H, layer->ln1_gamma,
                                 layer->ln1_beta, eps_ln, w.A, s)) != ZO_OK)
     return st;
   const long long as = shared ? 0 : Td;
-  if ((st = lin(&layer->q, d, d, w.A, as, w.Qb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
-  if ((st = lin(&layer->k, d, d, w.A, as, w.Kb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
-  if ((st = lin(&layer->v, d, d, w.A, as, w.Vb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  // q, k, v read the same A: one stacked projection, then the three fused GEMMs.
+  {
+    const zo_matrix* const qkv[3] = {&layer->q, &layer->k, &layer->v};
+    void* const out[3] = {w.Qb, w.Kb, w.Vb};
+    const int epi[3] = {ZO_EPI_NONE, ZO_EPI_NONE, ZO_EPI_NONE};
+    const void* const R[3] = {nullptr, nullptr, nullptr};
+    const long long rs[3] = {0, 0, 0};
+    if ((st = lin_group(T, d, d, r, q, nblk, as, dtype, blk_query, blk_sign, eps, w.A, 3, qkv, out, epi, R, rs,
+                        w.lin, w.grp, s)) != ZO_OK)
+      return st;
+  }
   if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
     return st;
   // H2 = H + C Wo'^T;  A = LN2(H2);  F = relu(A W1'^T);  H_out = H2 + F W2'^T.
@@ -490,7 +528,7 @@ int zo_decoder_layer_forward(int T, int seq_len, int d, int heads, int ffn, int 
 
 namespace {
 struct LlamaWs {
-  char *A, *Qb, *Kb, *Vb, *C, *H2, *G, *F, *lin;
+  char *A, *Qb, *Kb, *Vb, *C, *H2, *G, *F, *lin[3], *grp;
   size_t total;
 };
 // The largest perturbed-linear workspace of the layer's seven matrices (d x d, ffn x d, d x ffn).
@@ -508,7 +546,9 @@ static LlamaWs llama_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype
   w.H2 = (char*)wc.take(act);
   w.G = (char*)wc.take(wide);
   w.F = (char*)wc.take(wide);
-  w.lin = (char*)wc.take(decoder_lin_ws(T, d, ffn, r, q, nblk, dtype));
+  const size_t lin = decoder_lin_ws(T, d, ffn, r, q, nblk, dtype);
+  for (auto& l : w.lin) l = (char*)wc.take(lin);
+  w.grp = (char*)wc.take(decoder_grp_ws(T, d, r, q, nblk, dtype));  // q, k, v (gate, up need less)
   w.total = wc.off;
   return w;
 }
@@ -559,18 +599,26 @@ int zo_llama_layer_forward(int T, int seq_len, int d, int heads, int ffn, int r,
                  const void* R, long long rs) -> int {
     PlinearPlan p;
     zo_plinear_plan(&p, T, m, n, r, q, nblk, xs, dtype, dtype);
-    int e = zo_plinear_prepare(p, blk_query, blk_sign, eps, X, mt->U, mt->V, mt->Z, w.lin, s);
+    int e = zo_plinear_prepare(p, blk_query, blk_sign, eps, X, mt->U, mt->V, mt->Z, w.lin[0], s);
     if (e != ZO_OK) return e;
-    return zo_plinear_apply(p, X, mt->W, Y, w.lin, s, epi, R, rs);
+    return zo_plinear_apply(p, X, mt->W, Y, w.lin[0], s, epi, R, rs);
   };
   // A = RMS1(H): once when every block shares H.
   if ((st = zo_layernorm_launch(shared ? T : rows, d, dtype, H, layer->rms1_gamma, nullptr, eps_rms, w.A, s,
                                 true)) != ZO_OK)
     return st;
   const long long as = shared ? 0 : Td;
-  if ((st = lin(&layer->q, d, d, w.A, as, w.Qb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
-  if ((st = lin(&layer->k, d, d, w.A, as, w.Kb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
-  if ((st = lin(&layer->v, d, d, w.A, as, w.Vb, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
+  // q, k, v read the same A: one stacked projection, then the three fused GEMMs.
+  {
+    const zo_matrix* const qkv[3] = {&layer->q, &layer->k, &layer->v};
+    void* const out[3] = {w.Qb, w.Kb, w.Vb};
+    const int epi[3] = {ZO_EPI_NONE, ZO_EPI_NONE, ZO_EPI_NONE};
+    const void* const R[3] = {nullptr, nullptr, nullptr};
+    const long long rs[3] = {0, 0, 0};
+    if ((st = lin_group(T, d, d, r, q, nblk, as, dtype, blk_query, blk_sign, eps, w.A, 3, qkv, out, epi, R, rs,
+                        w.lin, w.grp, s)) != ZO_OK)
+      return st;
+  }
   if ((st = zo_rope_launch(rows, seq_len, d, heads, dtype, w.Qb, rope_base, s)) != ZO_OK) return st;
   if ((st = zo_rope_launch(rows, seq_len, d, heads, dtype, w.Kb, rope_base, s)) != ZO_OK) return st;
   if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
@@ -579,8 +627,16 @@ int zo_llama_layer_forward(int T, int seq_len, int d, int heads, int ffn, int r,
   if ((st = lin(&layer->o, d, d, w.C, Td, w.H2, ZO_EPI_RESIDUAL, H, h_block_stride)) != ZO_OK) return st;
   if ((st = zo_layernorm_launch(rows, d, dtype, w.H2, layer->rms2_gamma, nullptr, eps_rms, w.A, s, true)) != ZO_OK)
     return st;
-  if ((st = lin(&layer->gate, ffn, d, w.A, Td, w.G, ZO_EPI_NONE, nullptr, 0)) != ZO_OK) return st;
-  if ((st = lin(&layer->up, ffn, d, w.A, Td, w.F, ZO_EPI_SILU_MUL, w.G, Tf)) != ZO_OK) return st;
+  {  // gate and up read the same A: one stacked projection; F = silu(G) * (A Wu'^T)
+    const zo_matrix* const gu[2] = {&layer->gate, &layer->up};
+    void* const out[2] = {w.G, w.F};
+    const int epi[2] = {ZO_EPI_NONE, ZO_EPI_SILU_MUL};
+    const void* const R[2] = {nullptr, w.G};
+    const long long rs[2] = {0, Tf};
+    if ((st = lin_group(T, ffn, d, r, q, nblk, Td, dtype, blk_query, blk_sign, eps, w.A, 2, gu, out, epi, R, rs,
+                        w.lin, w.grp, s)) != ZO_OK)
+      return st;
+  }
   return lin(&layer->down, d, ffn, w.F, Tf, H_out, ZO_EPI_RESIDUAL, w.H2, Td);
 }
 

@@ -102,7 +102,14 @@ __device__ __forceinline__ void add4(const char* base, size_t idx, float& v0, fl
   v0 += r[0]; v1 += r[1]; v2 += r[2]; v3 += r[3];
 }
 
-__device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
+// silu(x) = x / (1 + e^-x) from the hardware exponential and reciprocal (about 1 ulp each,
+// so a few fp32 ulps in all, far below the output's 16-bit rounding): the IEEE expf and
+// division cost ~28 VALU instructions per element, and the epilogue of a 256 x 256 tile
+// applies it to 256 values per lane while the matrix cores idle.  e^-x overflows to +inf
+// for x < -88, and the reciprocal then gives 0: silu(x) -> -0, its limit.
+__device__ __forceinline__ float silu(float x) {
+  return x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x * -1.4426950408889634f));
+}
 
 // v0..v3 multiplied by silu of the four OUT-typed values at element idx.. (fp32).
 template <int OUT>
@@ -425,15 +432,16 @@ __global__ __launch_bounds__(256) void k_transpose_v(const float* __restrict__ V
   put_split(Vt, idx, (long long)rp * n, v, dtype);
 }
 
-// P = (P2[:, :rp] + P2[:, rp:]) * unscale (fp32; unscale a power of two),
+// P = (P2[:, :rp] + P2[:, rp:]) * unscale (fp32; unscale a power of two; P2 rows ld2 apart),
 // written as [P_hi | P_hi | P_lo] (bf16, 3 rp wide).
 __global__ __launch_bounds__(256) void k_pcombine(const float* __restrict__ P2, long long rows,
-                                                   int rp, float unscale, bf16_t* __restrict__ Pc) {
+                                                   int rp, int ld2, float unscale,
+                                                   bf16_t* __restrict__ Pc) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= rows * rp) return;
   const long long t = idx / rp;
   const int a = (int)(idx % rp);
-  const float p = (P2[t * 2 * rp + a] + P2[t * 2 * rp + rp + a]) * unscale;
+  const float p = (P2[t * ld2 + a] + P2[t * ld2 + rp + a]) * unscale;
   const bf16_t hi = f32_to_bf16(p);
   const bf16_t lo = f32_to_bf16(p - bf16_to_f32(hi));
   bf16_t* o = Pc + t * 3 * rp;
@@ -831,33 +839,102 @@ PlinearWs zo_plinear_ws(const PlinearPlan& p, void* ws) {
   return w;
 }
 
+static int launch_transpose_v(const PlinearPlan& p, const float* V, void* vt, hipStream_t stream) {
+  const long long total = (long long)p.rp * p.n;
+  hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                     V, p.n, p.r, p.rp, vt, p.in_dtype);
+  return zo_hip_status(hipGetLastError(), "k_transpose_v");
+}
+
+static int launch_bprime(const PlinearPlan& p, const BlkTable& tab, float eps, const float* U,
+                         const float* Z, void* bp, hipStream_t stream) {
+  const dim3 grid((unsigned)((p.m + BP_ROWS - 1) / BP_ROWS), (unsigned)p.q);
+  switch ((p.r + 31) / 32) {
+    case 1: hipLaunchKernelGGL(k_bprime<1>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+                               eps, tab, bp, p.in16); break;
+    case 2: hipLaunchKernelGGL(k_bprime<2>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+                               eps, tab, bp, p.in16); break;
+    case 3: hipLaunchKernelGGL(k_bprime<3>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+                               eps, tab, bp, p.in16); break;
+    default: hipLaunchKernelGGL(k_bprime<4>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+                                eps, tab, bp, p.in16); break;
+  }
+  return zo_hip_status(hipGetLastError(), "k_bprime");
+}
+
 int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
                        float eps, const void* X, const float* U, const float* V, const float* Z,
                        void* ws, hipStream_t stream) {
   const PlinearWs w = zo_plinear_ws(p, ws);
   int st;
-  {
-    const long long total = (long long)p.rp * p.n;
-    hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
-                       V, p.n, p.r, p.rp, w.vt, p.in_dtype);
-    if ((st = zo_hip_status(hipGetLastError(), "k_transpose_v")) != ZO_OK) return st;
-  }
-  {
-    const BlkTable tab = zo_blk_table(p.nblk, blk_query, blk_sign);
-    const dim3 grid((unsigned)((p.m + BP_ROWS - 1) / BP_ROWS), (unsigned)p.q);
-    switch ((p.r + 31) / 32) {
-      case 1: hipLaunchKernelGGL(k_bprime<1>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                 eps, tab, w.bp, p.in16); break;
-      case 2: hipLaunchKernelGGL(k_bprime<2>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                 eps, tab, w.bp, p.in16); break;
-      case 3: hipLaunchKernelGGL(k_bprime<3>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                 eps, tab, w.bp, p.in16); break;
-      default: hipLaunchKernelGGL(k_bprime<4>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                  eps, tab, w.bp, p.in16); break;
-    }
-    if ((st = zo_hip_status(hipGetLastError(), "k_bprime")) != ZO_OK) return st;
-  }
+  if ((st = launch_transpose_v(p, V, w.vt, stream)) != ZO_OK) return st;
+  if ((st = launch_bprime(p, zo_blk_table(p.nblk, blk_query, blk_sign), eps, U, Z, w.bp, stream)) != ZO_OK)
+    return st;
   return zo_plinear_project(p, X, ws, stream);
+}
+
+// The 16-bit projection GEMM P2 = X_x Vt2^T of every distinct X block: A = vt (rows_a rows,
+// n deep), output fp32 rows_a wide.
+static int launch_projection(const PlinearPlan& p, const void* X, const void* vt, int rows_a, void* p2,
+                             hipStream_t stream) {
+  GemmArgs g{};
+  g.A = (const bf16_t*)vt;
+  g.B = (const bf16_t*)X;
+  g.b_block_stride = p.x_block_stride;
+  g.rows_a = rows_a;
+  g.rows_b = p.T;
+  g.K = p.n;
+  g.nblk = p.nx;
+  g.rc = 0;
+  g.Y = p2;
+  g.y_block_stride = (long long)p.T * rows_a;
+  g.ldy = rows_a;
+  g.out_dtype = ZO_F32;
+  return p.in_dtype == ZO_F16 ? launch_gemm_bf16<1, 4, 2, 2, true>(g, stream)
+                              : launch_gemm_bf16<1, 4, 2, 2, false>(g, stream);
+}
+
+static int launch_pcombine(const PlinearPlan& p, const float* p2, int ld2, void* pp, hipStream_t stream) {
+  const long long prow = (long long)p.nx * p.T;
+  hipLaunchKernelGGL(k_pcombine, dim3((unsigned)((prow * p.rp + 255) / 256)), dim3(256), 0, stream, p2,
+                     prow, p.rp, ld2, p.in_dtype == ZO_F16 ? 1.f / ZO_F16_RSCALE : 1.f, (bf16_t*)pp);
+  return zo_hip_status(hipGetLastError(), "k_pcombine");
+}
+
+size_t zo_plinear_group_ws(const PlinearPlan& p, int count) {
+  if (!p.in16 || count < 2) return 0;
+  return zo_align256((size_t)count * 2 * p.rp * p.n * 2) +
+         zo_align256((size_t)p.nx * p.T * count * 2 * p.rp * 4);
+}
+
+int zo_plinear_prepare_group(const PlinearPlan* plans, int count, const int* blk_query,
+                             const int8_t* blk_sign, float eps, const void* X, const float* const* U,
+                             const float* const* V, const float* const* Z, void* const* ws, void* gws,
+                             hipStream_t stream) {
+  int st;
+  if (count < 2 || !plans[0].in16) {
+    for (int i = 0; i < count; ++i)
+      if ((st = zo_plinear_prepare(plans[i], blk_query, blk_sign, eps, X, U[i], V[i], Z[i], ws[i], stream)) !=
+          ZO_OK)
+        return st;
+    return ZO_OK;
+  }
+  const PlinearPlan& p0 = plans[0];
+  const int w2 = 2 * p0.rp;  // rows of one matrix's Vt2 (a multiple of 64: whole projection tiles)
+  char* gvt = (char*)gws;
+  float* gp2 = (float*)(gvt + zo_align256((size_t)count * w2 * p0.n * 2));
+  const BlkTable tab = zo_blk_table(p0.nblk, blk_query, blk_sign);
+  for (int i = 0; i < count; ++i) {
+    const PlinearWs w = zo_plinear_ws(plans[i], ws[i]);
+    if ((st = launch_transpose_v(plans[i], V[i], gvt + (size_t)i * w2 * p0.n * 2, stream)) != ZO_OK) return st;
+    if ((st = launch_bprime(plans[i], tab, eps, U[i], Z[i], w.bp, stream)) != ZO_OK) return st;
+  }
+  if ((st = launch_projection(p0, X, gvt, count * w2, gp2, stream)) != ZO_OK) return st;
+  for (int i = 0; i < count; ++i)
+    if ((st = launch_pcombine(plans[i], gp2 + (size_t)i * w2, count * w2, zo_plinear_ws(plans[i], ws[i]).pp,
+                              stream)) != ZO_OK)
+      return st;
+  return ZO_OK;
 }
 
 int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_t stream) {
@@ -868,26 +945,8 @@ int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_
   int st;
   const long long xs = p.x_block_stride;
   if (p.in16) {
-    GemmArgs g{};
-    g.A = (const bf16_t*)vt;
-    g.B = (const bf16_t*)X;
-    g.b_block_stride = xs;
-    g.rows_a = 2 * p.rp;
-    g.rows_b = p.T;
-    g.K = p.n;
-    g.nblk = p.nx;
-    g.rc = 0;
-    g.Y = p2;
-    g.y_block_stride = (long long)p.T * 2 * p.rp;
-    g.ldy = 2 * p.rp;
-    g.out_dtype = ZO_F32;
-    const bool f16 = p.in_dtype == ZO_F16;
-    st = f16 ? launch_gemm_bf16<1, 4, 2, 2, true>(g, stream) : launch_gemm_bf16<1, 4, 2, 2, false>(g, stream);
-    if (st != ZO_OK) return st;
-    const long long prow = (long long)p.nx * p.T;
-    hipLaunchKernelGGL(k_pcombine, dim3((unsigned)((prow * p.rp + 255) / 256)), dim3(256), 0, stream,
-                       (const float*)p2, prow, p.rp, f16 ? 1.f / ZO_F16_RSCALE : 1.f, (bf16_t*)pp);
-    return zo_hip_status(hipGetLastError(), "k_pcombine");
+    if ((st = launch_projection(p, X, vt, 2 * p.rp, p2, stream)) != ZO_OK) return st;
+    return launch_pcombine(p, (const float*)p2, 2 * p.rp, pp, stream);
   }
   F32Args g{};
   g.A = (const float*)vt;

@@ -126,6 +126,17 @@ int zo_lora_prepare(const PlinearPlan& p, int rl, int rs, const int* blk_query,
 int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t* blk_sign,
                        float eps, const void* X, const float* U, const float* V,
                        const float* Z, void* ws, hipStream_t stream);
+// Prepare of `count` perturbed linears that read the same X (plans equal but for m; 16-bit):
+// their Vt2 factors stacked into one projection GEMM, so X is read once for all of them.
+// ws[i] is matrix i's own workspace (apply reads it afterwards); gws holds the stacked
+// factors and projections, zo_plinear_group_ws bytes.  Results are bitwise those of
+// separate prepares (every projection tile covers one matrix's rows).  fp32 plans, or
+// count < 2, take the separate prepares.
+size_t zo_plinear_group_ws(const PlinearPlan& p, int count);
+int zo_plinear_prepare_group(const PlinearPlan* plans, int count, const int* blk_query,
+                             const int8_t* blk_sign, float eps, const void* X, const float* const* U,
+                             const float* const* V, const float* const* Z, void* const* ws, void* gws,
+                             hipStream_t stream);
 // Decoder-layer pieces (zo_decoder.hip).
 int zo_layernorm_launch(long long rows, int d, int dtype, const void* X, const float* gamma,
                         const float* beta, float eps_ln, void* Y, hipStream_t stream, bool rms = false);
