@@ -890,8 +890,14 @@ static int launch_projection(const PlinearPlan& p, const void* X, const void* vt
   g.y_block_stride = (long long)p.T * rows_a;
   g.ldy = rows_a;
   g.out_dtype = ZO_F32;
-  return p.in_dtype == ZO_F16 ? launch_gemm_bf16<1, 4, 2, 2, true>(g, stream)
-                              : launch_gemm_bf16<1, 4, 2, 2, false>(g, stream);
+  // 64 x 256 tiles; 64 x 128 when that leaves fewer than two workgroups per CU (this pass
+  // streams X once, so it needs the whole chip's loads in flight).  Tile shapes change no
+  // element's arithmetic.
+  const long long tiles = (long long)p.nx * ((p.T + 255) / 256) * ((rows_a + 63) / 64);
+  const bool f16 = p.in_dtype == ZO_F16;
+  if (tiles < 512)
+    return f16 ? launch_gemm_bf16<1, 4, 2, 1, true>(g, stream) : launch_gemm_bf16<1, 4, 2, 1, false>(g, stream);
+  return f16 ? launch_gemm_bf16<1, 4, 2, 2, true>(g, stream) : launch_gemm_bf16<1, 4, 2, 2, false>(g, stream);
 }
 
 static int launch_pcombine(const PlinearPlan& p, const float* p2, int ld2, void* pp, hipStream_t stream) {
