@@ -30,6 +30,14 @@ HIPCC_FLAGS = [
 ]
 
 
+# Per-file additions.  zo_decoder.hip: its only MFMA kernel (attention) keeps fewer than 64
+# accumulators per lane, so their VGPR form avoids the AGPR round trips of every online-softmax
+# rescale (and leaves room for a third wave per SIMD).  The GEMMs elsewhere need the AGPRs.
+FILE_FLAGS = {
+    "zo_decoder.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
+
 def hipcc() -> str:
     for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if c and os.path.exists(c):
@@ -58,7 +66,8 @@ def build(verbose: bool = False) -> str:
     objs = [os.path.join(BUILD, os.path.basename(s)[:-4] + ".o") for s in srcs]
     jobs = max(1, min(len(srcs), int(os.environ.get("MAX_JOBS", "8"))))
     with ThreadPoolExecutor(max_workers=jobs) as ex:
-        list(ex.map(lambda so: _run([cc, *HIPCC_FLAGS, "-c", so[0], "-o", so[1]], verbose),
+        list(ex.map(lambda so: _run([cc, *HIPCC_FLAGS, *FILE_FLAGS.get(os.path.basename(so[0]), []), "-c",
+                                     so[0], "-o", so[1]], verbose),
                     zip(srcs, objs)))
     tmp = LIB + ".tmp"
     _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)

@@ -273,24 +273,36 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Two fp32 values rounded to nearest even into a packed pair of 16-bit values (one
+// v_cvt_pk_bf16_f32 / v_cvt_pk_f16_f32), and back.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 template <bool F16>
-__device__ __forceinline__ uint16_t to16(float x) {
+__device__ __forceinline__ uint32_t cvt_pk(float x, float y) {
   if constexpr (F16)
-    return f32_to_f16(x);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){x, y}, f16x2_t));
   else
-    return f32_to_bf16(x);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){x, y}, bf16x2_t));
 }
 template <bool F16>
-__device__ __forceinline__ float from16(uint16_t h) {
+__device__ __forceinline__ float unpk(uint32_t pk, int half) {
+  const uint16_t h = (uint16_t)(half ? pk >> 16 : pk);
   if constexpr (F16)
     return f16_to_f32(h);
   else
     return bf16_to_f32(h);
 }
 
-// Element e (0..7) of eight 16-bit values packed in a u32x4.
-__device__ __forceinline__ uint32_t half_of(u32x4 v, int e) {
-  return (e & 1) ? (v[e >> 1] >> 16) : (v[e >> 1] & 0xffffu);
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+// ds_read_b64_tr_b16: within each 16-lane group, lane i reads 4 consecutive 16-bit values
+// D[i][0..3] at its own address, and lane j receives D[j/4 + 4e][j%4] for e = 0..3.  With
+// lane i addressing row (r0 + i/4), columns c0 + 4 (i%4) of a row-major tile, lane j thus
+// receives column c0 + j of rows r0 .. r0+3: a transposed fragment.
+__device__ __forceinline__ u32x2 ds_read_tr(const uint16_t* p) {
+  const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4_t*)(p));
+  return __builtin_bit_cast(u32x2, v);
 }
 
 template <bool F16, int DH>
@@ -298,13 +310,13 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
   constexpr int KS = DH / 32;         // 32-deep k steps of Q K^T
   constexpr int DT = DH / 16;         // 16-dim tiles of the output
   constexpr int KROW = DH + 8;        // LDS row of the K tile (elements), padded
-  constexpr int VROW = AT_K + 4;      // LDS row of the transposed V tile (elements)
+  constexpr int VROW = DH + 16;       // LDS row of the V tile (elements): 16 rows of a
+                                      // transposed read fall on distinct banks
   constexpr int C8 = DH / 8;          // 16-byte chunks per head row
-  constexpr int KCH = AT_K * C8 / 256;    // K chunks per thread per tile
-  constexpr int VIT = (AT_K / 4) * C8;    // V items (4 keys x 8 dims) per tile
-  static_assert(KCH * 256 == AT_K * C8 && VIT <= 256, "tile / thread mismatch");
+  constexpr int KCH = AT_K * C8 / 256;    // K (and V) chunks per thread per tile
+  static_assert(KCH * 256 == AT_K * C8, "tile / thread mismatch");
   __shared__ __attribute__((aligned(16))) uint16_t Ks[AT_K * KROW];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[DH * VROW];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[AT_K * VROW];
 
   // Workgroup -> (block, sequence, head, query tile).
   int w = blockIdx.x;
@@ -335,6 +347,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
     for (int kk = 0; kk < KS; ++kk)
       qf[gq][kk] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + 32 * kk));
   }
+  const int wq0 = q0 + wave * 16 * AT_NG;  // the wave's first query
 
   f32x4 o[AT_NG][DT];
   float mrow[AT_NG], lsum[AT_NG];
@@ -342,28 +355,21 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
   for (int gq = 0; gq < AT_NG; ++gq) {
 #pragma unroll
     for (int t = 0; t < DT; ++t) o[gq][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    mrow[gq] = -1e30f;  // running max (log2 units)
+    mrow[gq] = -1e30f;  // running max of the raw logits
     lsum[gq] = 0.f;     // this lane's part of the running sum
   }
 
-  // K and V tiles are loaded into registers a tile ahead.  K: chunk x = tid + 256 c is key
-  // x / C8, dims 8 (x % C8).  V: item tid (< VIT) is keys 4 (tid / C8) .. +3, dims
-  // 8 (tid % C8) .. +7, transposed in registers into four-key rows of Vt.  Rows past the
-  // sequence are clamped to its last row (their keys are masked).
-  u32x4 kreg[KCH], vreg[4];
+  // K and V tiles are loaded into registers a tile ahead: chunk x = tid + 256 c is key x / C8,
+  // dims 8 (x % C8); both are stored row-major (V is read transposed by ds_read_tr).  Rows
+  // past the sequence are clamped to its last row (their keys are masked).
+  u32x4 kreg[KCH], vreg[KCH];
   auto load_tile = [&](int k0) {
 #pragma unroll
     for (int c = 0; c < KCH; ++c) {
       const int x = tid + 256 * c;
-      const int key = min(k0 + x / C8, a.seq_len - 1);
-      kreg[c] = *(const u32x4*)(Kg + (size_t)(row0 + key) * a.d + col0 + 8 * (x % C8));
-    }
-    if (tid < VIT) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = min(k0 + 4 * (tid / C8) + e, a.seq_len - 1);
-        vreg[e] = *(const u32x4*)(Vg + (size_t)(row0 + key) * a.d + col0 + 8 * (tid % C8));
-      }
+      const size_t off = (size_t)(row0 + min(k0 + x / C8, a.seq_len - 1)) * a.d + col0 + 8 * (x % C8);
+      kreg[c] = *(const u32x4*)(Kg + off);
+      vreg[c] = *(const u32x4*)(Vg + off);
     }
   };
   auto store_tile = [&]() {
@@ -371,15 +377,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
     for (int c = 0; c < KCH; ++c) {
       const int x = tid + 256 * c;
       *(u32x4*)&Ks[(x / C8) * KROW + 8 * (x % C8)] = kreg[c];
-    }
-    if (tid < VIT) {
-      const int kb = 4 * (tid / C8), db = 8 * (tid % C8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t lo = half_of(vreg[0], e) | (half_of(vreg[1], e) << 16);
-        const uint32_t hi = half_of(vreg[2], e) | (half_of(vreg[3], e) << 16);
-        *(u32x2*)&Vt[(db + e) * VROW + kb] = (u32x2){lo, hi};
-      }
+      *(u32x4*)&Vs[(x / C8) * VROW + 8 * (x % C8)] = vreg[c];
     }
   };
 
@@ -404,8 +402,13 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
         for (int gq = 0; gq < AT_NG; ++gq) st[gq][t] = mfma16<F16>(kf, qf[gq][kk], st[gq][t]);
       }
     }
-    // Scale to log2 units, mask keys after the query (and past the sequence), online softmax,
-    // P = 2^(s - m + 12) as hi + lo 16-bit pairs in the B-operand order of the P V MFMA.
+    // Mask keys after the query (only a tile that reaches past the wave's first query has
+    // any), online softmax on the raw logits, P = 2^((s - m) scale + 12) as hi + lo 16-bit
+    // pairs in the B-operand order of the P V MFMA.  The running maximum m moves only when
+    // some query of the wave has a logit more than 3 (log2 units) above it, so most tiles
+    // skip the rescale of O; P then stays below 2^15 (within fp16's range), and the first
+    // tile sets m to its row maximum, whose P is exactly 2^12.
+    const bool diag = k0 + AT_K - 1 > wq0;
     uint32_t ph[AT_NG][4][2], pl[AT_NG][4][2];
 #pragma unroll
     for (int gq = 0; gq < AT_NG; ++gq) {
@@ -414,34 +417,35 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = k0 + 16 * t + 4 * g + i;
-          const float sv = key <= myq[gq] ? st[gq][t][i] * a.scale_log2 : -INFINITY;
-          st[gq][t][i] = sv;
-          tmax = fmaxf(tmax, sv);
+          if (diag && k0 + 16 * t + 4 * g + i > myq[gq]) st[gq][t][i] = -INFINITY;
+          tmax = fmaxf(tmax, st[gq][t][i]);
         }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float mnew = fmaxf(mrow[gq], tmax);
-      const float alpha = exp2f(mrow[gq] - mnew);
-      mrow[gq] = mnew;
-      lsum[gq] *= alpha;
+      if (__ballot((tmax - mrow[gq]) * a.scale_log2 > 3.f)) {
+        const float mnew = fmaxf(mrow[gq], tmax);
+        const float alpha = __builtin_amdgcn_exp2f((mrow[gq] - mnew) * a.scale_log2);
+        mrow[gq] = mnew;
+        lsum[gq] *= alpha;
 #pragma unroll
-      for (int t = 0; t < DT; ++t) o[gq][t] *= alpha;
+        for (int t = 0; t < DT; ++t) o[gq][t] *= alpha;
+      }
+      const float m = mrow[gq];
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int i = 0; i < 4; i += 2) {
-          const float p0 = exp2f(st[gq][t][i] - mnew + 12.f), p1 = exp2f(st[gq][t][i + 1] - mnew + 12.f);
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(st[gq][t][i] - m, a.scale_log2, 12.f));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(st[gq][t][i + 1] - m, a.scale_log2, 12.f));
           lsum[gq] += p0 + p1;
-          const uint16_t h0 = to16<F16>(p0), h1 = to16<F16>(p1);
-          ph[gq][t][i / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-          pl[gq][t][i / 2] = (uint32_t)to16<F16>(p0 - from16<F16>(h0)) |
-                             ((uint32_t)to16<F16>(p1 - from16<F16>(h1)) << 16);
+          const uint32_t h = cvt_pk<F16>(p0, p1);
+          ph[gq][t][i / 2] = h;
+          pl[gq][t][i / 2] = cvt_pk<F16>(p0 - unpk<F16>(h, 0), p1 - unpk<F16>(h, 1));
         }
     }
     // O^T += V^T P^T over two 32-key chunks c (subtiles 2c and 2c+1): lane group g's k slots
-    // are keys 32c + 4g + (0..3) and 32c + 16 + 4g + (0..3).  Each V^T fragment serves both
-    // query groups.
+    // are keys 32c + 4g + (0..3) and 32c + 16 + 4g + (0..3); V^T's fragment (dim 16t + l16 of
+    // those keys) comes from two transposed reads of the row-major V tile.
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       bf16x8 bh[AT_NG], bl[AT_NG];
@@ -452,10 +456,10 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
         bl[gq] = __builtin_bit_cast(bf16x8, (u32x4){pl[gq][2 * c][0], pl[gq][2 * c][1], pl[gq][2 * c + 1][0],
                                                     pl[gq][2 * c + 1][1]});
       }
+      const uint16_t* vb = &Vs[(32 * c + 4 * g + (l16 >> 2)) * VROW + 4 * (l16 & 3)];
 #pragma unroll
       for (int t = 0; t < DT; ++t) {
-        const uint16_t* vr = &Vt[(16 * t + l16) * VROW + 32 * c + 4 * g];
-        const u32x2 v0 = *(const u32x2*)vr, v1 = *(const u32x2*)(vr + 16);
+        const u32x2 v0 = ds_read_tr(vb + 16 * t), v1 = ds_read_tr(vb + 16 * VROW + 16 * t);
         const bf16x8 af = __builtin_bit_cast(bf16x8, (u32x4){v0[0], v0[1], v1[0], v1[1]});
 #pragma unroll
         for (int gq = 0; gq < AT_NG; ++gq) {
