@@ -17,11 +17,12 @@
 //
 // k_attention<F16, DH>: one workgroup (4 waves) per (block, sequence, head,
 // tile of 64 AT_NG queries); keys in tiles of 64 through LDS (loaded into
-// registers a tile ahead; V transposed in registers into four-key rows),
-// online softmax in fp32.  Each wave owns AT_NG groups of 16 queries that
-// share every K and V fragment it reads from LDS (one group measured faster
-// than two at head dim 128: two need 256 VGPRs, one wave per SIMD), and
-// computes the transposed products, which keeps every step in registers:
+// registers a tile ahead, both K and V stored row-major), online softmax in
+// fp32.  Each wave owns AT_NG = 2 groups of 16 queries that share every K and
+// V fragment it reads from LDS (two groups measured 9-18 % faster than one once
+// the accumulators sit in VGPRs: 240 registers, two waves per SIMD), skips the
+// tiles whose keys all follow its queries, and computes the transposed
+// products, which keeps every step in registers:
 //   S^T = K Q^T  (v_mfma_f32_16x16x32: A = K rows from LDS, B = the wave's Q
 //                 rows held in registers); lane (l16, g) of a 16 x 16 result
 //                 holds query l16 and keys 4g .. 4g+3, so a query's softmax
@@ -29,13 +30,15 @@
 //   O^T += V^T P^T, 32 keys per MFMA.  The MFMA's k slots of lane group g are
 //                 given the keys that lane already holds for P (4g .. 4g+3 of
 //                 each of two 16-key tiles); V^T's fragment takes the same keys
-//                 from a transposed LDS copy of the V tile.  A sum over k does
-//                 not depend on how the k slots are assigned to keys, as long
-//                 as both operands use the same assignment.
+//                 from two transposed reads (ds_read_b64_tr_b16) of the
+//                 row-major V tile.  A sum over k does not depend on how the k
+//                 slots are assigned to keys, as long as both operands use the
+//                 same assignment.
 // P enters as a hi + lo pair of 16-bit values (two MFMAs), so the product is
 // ~2^-16 accurate before the output's rounding; P is computed as
-// 2^(s - m + 12) (the common factor 2^12 cancels in the normalisation and keeps
-// fp16 low parts out of the subnormal range).
+// 2^((s - m) scale + 12) on the raw logits s (the common factor cancels in the
+// normalisation and keeps fp16 low parts out of the subnormal range), with the
+// running maximum m moved only when a logit exceeds it by more than 2^3.
 #include "zo_internal.h"
 
 #include <type_traits>
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(256) void k_rope(void* X, long long rows, int seq_l
 }
 
 // ---------------------------------------------------------------- attention
-constexpr int AT_NG = 1;               // 16-query groups per wave
+constexpr int AT_NG = 2;               // 16-query groups per wave
 constexpr int AT_Q = 64 * AT_NG;       // queries per workgroup (4 waves)
 constexpr int AT_K = 64;               // keys per tile
 
@@ -388,6 +391,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
     store_tile();
     __syncthreads();
     if (k0 + AT_K < kend) load_tile(k0 + AT_K);
+    if (k0 > wq0 + 16 * AT_NG - 1) continue;  // every key of the tile is after the wave's queries
 
     // S^T for 4 key subtiles of 16: st[gq][t][i] = key k0 + 16 t + 4 g + i, query myq[gq].
     f32x4 st[AT_NG][4];
