@@ -16,7 +16,11 @@
  *                            r x r state and apply W <- W - lr U S V^T
  *                            (Eqs. 6-10, tail of Alg. 3).
  *
- * plus two small helpers for a squared-error loss and the central difference.
+ * plus small helpers for a squared-error loss and the central or forward
+ * difference, and the network a query evaluates (the forward of Eq. 5): a
+ * pre-LN decoder layer of the OPT family and a LLaMA-family layer with every
+ * weight matrix perturbed, with their row norms, rotary positions and causal
+ * attention as entry points of their own.
  *
  * Conventions (all entry points)
  *   - Every tensor argument is DEVICE memory owned by the caller; the library
@@ -288,7 +292,8 @@ int zo_layernorm(long long rows, int d, int dtype, const void* X,
  *
  * Row-wise RMS normalisation: Y = X / sqrt(mean(X^2) + eps) * gamma per row of d
  * elements, statistics in fp32.  X, Y: rows x d (dtype, may alias); gamma:
- * device fp32 [d].  Limits: d % 8 == 0; 16-byte aligned pointers. */
+ * device fp32 [d]; eps finite and >= 0; rows = 0 launches nothing.
+ * Limits: d % 8 == 0; 16-byte aligned pointers. */
 int zo_rmsnorm(long long rows, int d, int dtype, const void* X,
                const float* gamma, float eps, void* Y, void* stream);
 
