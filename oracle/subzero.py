@@ -18,7 +18,7 @@ __all__ = [
     "perturbation", "perturbed_weight", "perturbed_linear", "perturbed_linear_blocks",
     "lora_perturbed_factors", "lora_perturbed_linear", "lora_perturbed_linear_blocks",
     "layer_norm", "causal_attention", "DECODER_MATS", "decoder_layer",
-    "rms_norm", "rope", "silu", "LLAMA_MATS", "llama_layer",
+    "rms_norm", "rope", "silu", "LLAMA_MATS", "llama_layer", "LORA_LAYER_MATS", "llama_lora_layer",
     "sq_loss", "central_estimate", "forward_estimate", "aggregate",
     "adam_direction", "subspace_adam_update", "subspace_sgd_update", "round_bf16", "round_f16", "tiny_run",
 ]
@@ -187,26 +187,30 @@ def layer_norm(X, gamma, beta, eps_ln=1e-5):
     return (X - mu) / np.sqrt(var + eps_ln) * np.asarray(gamma, np.float64) + np.asarray(beta, np.float64)
 
 
-def causal_attention(Q, K, V, heads, seq_len):
+def causal_attention(Q, K, V, heads, seq_len, kv_heads=None):
     """Multi-head causal self-attention of one block of T token rows holding T / seq_len
     sequences one after another: for each sequence and head h (columns h dh .. (h+1) dh - 1,
     dh = d / heads), query t attends to keys t' <= t of its own sequence with weights
-    softmax_t'(q_t . k_t' / sqrt(dh)) and returns the weighted sum of the v_t'."""
+    softmax_t'(q_t . k_t' / sqrt(dh)) and returns the weighted sum of the v_t'.
+    ``kv_heads`` (grouped key/value heads, a divisor of heads): K and V hold kv_heads heads
+    of dh columns, and query head h reads key/value head h // (heads / kv_heads)."""
     Q, K, V = (np.asarray(a, np.float64) for a in (Q, K, V))
     T, d = Q.shape
     dh = d // heads
+    group = heads // (kv_heads or heads)
     O = np.zeros_like(Q)
     future = np.triu(np.ones((seq_len, seq_len), dtype=bool), 1)
     for s0 in range(0, T, seq_len):
         rows = slice(s0, s0 + seq_len)
         for h in range(heads):
             c = slice(h * dh, (h + 1) * dh)
-            S = Q[rows, c] @ K[rows, c].T / math.sqrt(dh)
+            ckv = slice((h // group) * dh, (h // group + 1) * dh)
+            S = Q[rows, c] @ K[rows, ckv].T / math.sqrt(dh)
             S[future] = -np.inf
             S = S - S.max(axis=1, keepdims=True)
             P = np.exp(S)
             P = P / P.sum(axis=1, keepdims=True)
-            O[rows, c] = P @ V[rows, c]
+            O[rows, c] = P @ V[rows, ckv]
     return O
 
 
@@ -301,6 +305,43 @@ def llama_layer(H, layer, sign, eps, j, heads, seq_len, store=None, eps_rms=1e-6
     K = st(rope(st(lin(A, "k")), seq_len, heads, rope_base))
     Vv = st(lin(A, "v"))
     C = st(causal_attention(Q, K, Vv, heads, seq_len))
+    H2 = st(np.asarray(H, np.float64) + lin(C, "o"))
+    A2 = st(rms_norm(H2, layer["rms2_g"], eps_rms))
+    G = st(lin(A2, "gate"))
+    F = st(silu(G) * lin(A2, "up"))
+    if trace is not None:
+        trace.update(A=A, Q=Q, K=K, V=Vv, C=C, H2=H2, A2=A2, G=G, F=F)
+    return st(H2 + lin(F, "down"))
+
+
+LORA_LAYER_MATS = ("q", "k", "v", "o", "gate", "up", "down")
+
+
+def llama_lora_layer(H, layer, sign, eps, j, heads, kv_heads, seq_len, scale, store=None, eps_rms=1e-6,
+                     rope_base=1e6, trace=None):
+    """The LLaMA-family layer of the LoRA scheme (the Qwen models of the experiments): grouped
+    key/value heads (k and v project to kv_heads * dh columns), frozen base weights, and LoRA
+    adapters on q and v whose factors are the perturbed parameters (Eq. 4 on A and B, as in
+    lora_perturbed_linear):
+        A = RMS1(H);   Q = rope(A (Wq + scale B_q' A_q')^T);   K = rope(A Wk^T)
+        V = A (Wv + scale B_v' A_v')^T;   C = attention(Q, K, V; kv_heads)
+        H2 = H + C Wo^T;   A2 = RMS2(H2);   F = silu(A2 Wg^T) * (A2 Wu^T);   H3 = H2 + F Wd^T.
+    layer["q"], layer["v"]: W, A, UA, VA, ZA (q x r x r), B, UB, VB, ZB; the others: W.
+    ``store`` rounds each tensor where a device path stores one (as in llama_layer).
+    READING: rope_base 1e6 (the Qwen2.5 models); no biases, as for the other layers."""
+    st = store if store is not None else (lambda x: x)
+    lin = lambda X, name: np.asarray(X, np.float64) @ np.asarray(layer[name]["W"], np.float64).T
+
+    def lora(X, name):
+        m = layer[name]
+        return lora_perturbed_linear(X, m["W"], m["A"], m["UA"], m["VA"], m["ZA"][j], m["B"], m["UB"], m["VB"],
+                                     m["ZB"][j], sign, eps, scale)
+
+    A = st(rms_norm(H, layer["rms1_g"], eps_rms))
+    Q = st(rope(st(lora(A, "q")), seq_len, heads, rope_base))
+    K = st(rope(st(lin(A, "k")), seq_len, kv_heads, rope_base))
+    Vv = st(lora(A, "v"))
+    C = st(causal_attention(Q, K, Vv, heads, seq_len, kv_heads))
     H2 = st(np.asarray(H, np.float64) + lin(C, "o"))
     A2 = st(rms_norm(H2, layer["rms2_g"], eps_rms))
     G = st(lin(A2, "gate"))

@@ -844,3 +844,90 @@ def test_llama_layer_matches_transformers():
     ref = out.reshape(S * L, d).numpy()
     got = oracle.llama_layer(H, layer, s, eps, j, heads, L)
     np.testing.assert_allclose(got, ref, rtol=2e-6, atol=2e-6 * np.abs(ref).max())
+
+
+def test_grouped_kv_attention():
+    """Grouped key/value heads: kv_heads = heads is the plain multi-head attention bit for bit;
+    in general the result equals multi-head attention on K and V with each key/value head
+    repeated for its group of query heads, and torch's grouped scaled-dot-product attention."""
+    torch = pytest.importorskip("torch")
+    T, L, heads, kv, dh = 24, 12, 6, 2, 8
+    Q = RNG.standard_normal((T, heads * dh))
+    K, V = RNG.standard_normal((T, kv * dh)), RNG.standard_normal((T, kv * dh))
+    Kf, Vf = RNG.standard_normal((T, heads * dh)), RNG.standard_normal((T, heads * dh))
+    np.testing.assert_array_equal(oracle.causal_attention(Q, Kf, Vf, heads, L, heads),
+                                  oracle.causal_attention(Q, Kf, Vf, heads, L))
+    rep = lambda X: np.repeat(X.reshape(T, kv, dh), heads // kv, axis=1).reshape(T, heads * dh)
+    got = oracle.causal_attention(Q, K, V, heads, L, kv)
+    np.testing.assert_array_equal(got, oracle.causal_attention(Q, rep(K), rep(V), heads, L))
+    F = torch.nn.functional
+    sh = lambda X, h: torch.from_numpy(X).reshape(T // L, L, h, dh).transpose(1, 2)
+    ref = F.scaled_dot_product_attention(sh(Q, heads), sh(K, kv), sh(V, kv), is_causal=True, enable_gqa=True)
+    ref = ref.transpose(1, 2).reshape(T, heads * dh).numpy()
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def _lora_layer_params(seed, d, dkv, ffn, rl, r, q):
+    shapes = {"q": (d, d), "k": (dkv, d), "v": (dkv, d), "o": (d, d), "gate": (ffn, d), "up": (ffn, d),
+              "down": (d, ffn)}
+    layer = {}
+    for i, (nm, (m, n)) in enumerate(shapes.items()):
+        layer[nm] = dict(W=zd.draw(seed, "W0", (i, m, n), (m, n), 0.05))
+        if nm in ("q", "v"):
+            orth = lambda rows, k: np.linalg.qr(zd.draw(seed, "OMEGA_U", (i, rows, k), (rows, r)))[0]
+            layer[nm].update(A=zd.draw(seed, "LORA_A", (i,), (rl, n), 0.05), B=zd.draw(seed, "LORA_B", (i,), (m, rl), 0.05),
+                             UA=orth(rl, 0), VA=orth(n, 1), UB=orth(m, 2), VB=orth(rl, 3),
+                             ZA=zd.z_draws(seed, 0, 2 * i, q, r).astype(np.float64),
+                             ZB=zd.z_draws(seed, 0, 2 * i + 1, q, r).astype(np.float64))
+    layer["rms1_g"], layer["rms2_g"] = 1.0 + 0.1 * RNG.standard_normal(d), 1.0 + 0.1 * RNG.standard_normal(d)
+    return layer
+
+
+def test_llama_lora_layer_matches_transformers_qwen2():
+    """The LoRA-scheme layer against transformers' Qwen2DecoderLayer (grouped key/value heads,
+    rotary base 1e6; its q/k/v biases set to zero, the reading of no biases), with q and v
+    given the effective weights W + scale B'A' of Eq. 4 on the adapter factors."""
+    torch = pytest.importorskip("torch")
+    transformers = pytest.importorskip("transformers")
+    mq = pytest.importorskip("transformers.models.qwen2.modeling_qwen2")
+    d, heads, kv, ffn, rl, r, q, L, S = 64, 8, 2, 96, 4, 2, 3, 10, 2
+    dkv = kv * d // heads
+    layer = _lora_layer_params(8, d, dkv, ffn, rl, r, q)
+    H = RNG.standard_normal((S * L, d))
+    s, eps, j, scale = -1.0, 0.1, 1, 2.0
+    Weff = {nm: layer[nm]["W"] for nm in oracle.LORA_LAYER_MATS}
+    for nm in ("q", "v"):
+        m = layer[nm]
+        Ap, Bp = oracle.lora_perturbed_factors(m["A"], m["UA"], m["VA"], m["ZA"][j], m["B"], m["UB"], m["VB"],
+                                               m["ZB"][j], s, eps)
+        Weff[nm] = m["W"] + scale * Bp @ Ap
+    cfg = transformers.Qwen2Config(hidden_size=d, intermediate_size=ffn, num_attention_heads=heads,
+                                   num_key_value_heads=kv, rms_norm_eps=1e-6, rope_theta=1e6,
+                                   hidden_act="silu", max_position_embeddings=4 * L)
+    cfg._attn_implementation = "sdpa"
+    mod = mq.Qwen2DecoderLayer(cfg, 0).double()
+    rot = mq.Qwen2RotaryEmbedding(cfg).double()
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    with torch.no_grad():
+        att, mlp = mod.self_attn, mod.mlp
+        for lin, nm in ((att.q_proj, "q"), (att.k_proj, "k"), (att.v_proj, "v"), (att.o_proj, "o"),
+                        (mlp.gate_proj, "gate"), (mlp.up_proj, "up"), (mlp.down_proj, "down")):
+            lin.weight.copy_(t(Weff[nm]))
+            if lin.bias is not None:
+                lin.bias.zero_()
+        mod.input_layernorm.weight.copy_(t(layer["rms1_g"]))
+        mod.post_attention_layernorm.weight.copy_(t(layer["rms2_g"]))
+        x = t(H).reshape(S, L, d)
+        pos = torch.arange(L).unsqueeze(0).expand(S, L)
+        out = mod(x, attention_mask=None, position_ids=pos, position_embeddings=rot(x, pos))
+        out = out[0] if isinstance(out, tuple) else out
+    ref = out.reshape(S * L, d).numpy()
+    got = oracle.llama_lora_layer(H, layer, s, eps, j, heads, kv, L, scale)
+    np.testing.assert_allclose(got, ref, rtol=2e-6, atol=2e-6 * np.abs(ref).max())
+    # The frozen base alone: eps = 0 and B = 0 leave q and v at their base weights.
+    zeroB = {nm: dict(layer[nm]) for nm in oracle.LORA_LAYER_MATS}
+    zeroB.update(rms1_g=layer["rms1_g"], rms2_g=layer["rms2_g"])
+    for nm in ("q", "v"):
+        zeroB[nm]["B"] = np.zeros_like(layer[nm]["B"])
+    base = oracle.llama_lora_layer(H, zeroB, s, 0.0, j, heads, kv, L, scale)
+    assert np.abs(base - got).max() > 1e-4   # the adapters and their perturbation do act
