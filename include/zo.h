@@ -320,6 +320,16 @@ int zo_causal_attention(int nblk, int T, int seq_len, int d, int heads,
                         int dtype, const void* Q, const void* K, const void* V,
                         void* O, void* stream);
 
+/* The same with grouped key/value heads (the Qwen models of the experiments):
+ * K and V are nblk blocks of T rows x kv_heads dh (dh = d / heads), and query
+ * head h reads key/value head h / (heads / kv_heads).  zo_causal_attention is
+ * this call with kv_heads = heads.  Limits: heads % kv_heads == 0; the rest as
+ * for zo_causal_attention. */
+int zo_causal_attention_gqa(int nblk, int T, int seq_len, int d, int heads,
+                            int kv_heads, int dtype, const void* Q,
+                            const void* K, const void* V, void* O,
+                            void* stream);
+
 /* One perturbed matrix: W (m x n, the layer's dtype), U (m x r), V (n x r)
  * and Z (q x r x r) fp32. */
 typedef struct {
@@ -477,6 +487,66 @@ int zo_combine_central(int q, const double* L, float eps, float* g,
  * query j with sign +1), g device fp32 [q]; float64 arithmetic. */
 int zo_combine_forward(int q, const double* L, float eps, float* g,
                        void* stream);
+
+/* ------------------------------------------------------------------------
+ * The LLaMA-family layer of the LoRA scheme (the Qwen models of the
+ * experiments, Sec. "Experiments"; Eq. 4 / Alg. 2 on the adapter factors):
+ * grouped key/value heads, a frozen base, and LoRA adapters on q and v whose
+ * factors are the perturbed parameters:
+ *
+ *   A = RMS1(H);   Q = rope(A (Wq + scale B_q' A_q')^T);   K = rope(A Wk^T)
+ *   V = A (Wv + scale B_v' A_v')^T;   C = attention(Q, K, V; kv_heads)
+ *   H2 = H + C Wo^T;   A2 = RMS2(H2);   H_out = H2 + (silu(A2 Wg^T) * (A2 Wu^T)) Wd^T
+ *
+ * with A' and B' as for zo_lora_perturbed_linear (each factor in its own
+ * subspace, block b's query and sign).  No biases.
+ * ------------------------------------------------------------------------ */
+/* An adapted matrix: the frozen W (m x n, the layer's dtype) and the adapter
+ * factors with their subspaces and coefficients, as for
+ * zo_lora_perturbed_linear (A rl x n, B m x rl, fp32). */
+typedef struct {
+  const void* W;
+  const float* A;
+  const float* U_A;
+  const float* V_A;
+  const float* Z_A;
+  const float* B;
+  const float* U_B;
+  const float* V_B;
+  const float* Z_B;
+} zo_lora_matrix;
+
+/* q (d x d) and v (kv_heads dh x d) adapted; the frozen k (kv_heads dh x d),
+ * o (d x d), gate, up (ffn x d), down (d x ffn); the RMS norms' gamma. */
+typedef struct {
+  zo_lora_matrix q, v;
+  const void* k;
+  const void* o;
+  const void* gate;
+  const void* up;
+  const void* down;
+  const float* rms1_gamma;
+  const float* rms2_gamma;
+} zo_llama_lora_layer;
+
+/* The layer for all nblk blocks at once; H, h_block_stride, H_out, eps_rms,
+ * rope_base, dtype and the workspace as for zo_llama_layer_forward; rl, r,
+ * scale as for zo_lora_perturbed_linear.  The frozen products run the fused
+ * GEMM without a rank-r segment (the residuals fused into o and down,
+ * silu(gate) * up into up); the adapted ones run it at rank rl + r.
+ * Limits: those of zo_causal_attention_gqa, zo_rope and
+ * zo_lora_perturbed_linear for q and v. */
+size_t zo_llama_lora_layer_workspace(int T, int seq_len, int d, int heads,
+                                     int kv_heads, int ffn, int rl, int r,
+                                     int q, int nblk, int dtype);
+int zo_llama_lora_layer_forward(int T, int seq_len, int d, int heads,
+                                int kv_heads, int ffn, int rl, int r, int q,
+                                int nblk, const int* blk_query,
+                                const int8_t* blk_sign, float eps, float scale,
+                                float eps_rms, float rope_base, int dtype,
+                                const void* H, long long h_block_stride,
+                                const zo_llama_lora_layer* layer, void* H_out,
+                                void* workspace, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -14,6 +14,8 @@ of include/zo.h); this package only binds it.  Entry points:
     rmsnorm, rope, LlamaLayer
                            the same for a LLaMA-family layer (RMS norms, rotary
                            positions, SwiGLU MLP) with all seven matrices perturbed
+    LlamaLoraLayer         the LoRA scheme's layer (grouped key/value heads, frozen
+                           base, perturbed adapters on q and v)
     subspace_adam_update   subspace Adam and W <- W - lr U S V^T (Eqs. 6-10)
     subspace_sgd_update    plain subspace SGD, W <- W - lr U Zbar V^T
     sq_loss, combine_central, combine_forward   loss and estimate helpers (central
@@ -21,12 +23,12 @@ of include/zo.h); this package only binds it.  Entry points:
 """
 from ._lib import (ZO_BF16, ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL, ZO_EPI_SILU_MUL, ZO_F16, ZO_F32, ZO_MAX_BLOCKS,
                    ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH, DecoderLayer, LlamaLayer,
-                   LoraPerturbedLinear, PerturbedLinear, Workspace, ZoError, abi_version, causal_attention, combine_central,
+                   LlamaLoraLayer, LoraPerturbedLinear, PerturbedLinear, Workspace, ZoError, abi_version, causal_attention, combine_central,
                    combine_forward, layernorm, lib, lora_perturbed_linear, perturbed_linear, rmsnorm, rope,
                    sq_loss, subspace_adam_update, subspace_refresh, subspace_sgd_update)
 
 __all__ = ["ZO_BF16", "ZO_EPI_NONE", "ZO_EPI_RELU", "ZO_EPI_RESIDUAL", "ZO_EPI_SILU_MUL", "ZO_F16", "ZO_F32", "ZO_MAX_BLOCKS",
-           "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH", "DecoderLayer", "LlamaLayer", "LoraPerturbedLinear",
+           "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH", "DecoderLayer", "LlamaLayer", "LlamaLoraLayer", "LoraPerturbedLinear",
            "PerturbedLinear", "Workspace", "ZoError", "abi_version", "causal_attention", "combine_central",
            "combine_forward", "layernorm", "lib", "lora_perturbed_linear", "perturbed_linear", "rmsnorm", "rope", "sq_loss",
            "subspace_adam_update", "subspace_refresh", "subspace_sgd_update"]

@@ -38,6 +38,7 @@ ABI_SYMBOLS = (
     "zo_perturbed_linear_apply_ex", "zo_layernorm", "zo_causal_attention",
     "zo_decoder_layer_workspace", "zo_decoder_layer_forward",
     "zo_rmsnorm", "zo_rope", "zo_llama_layer_workspace", "zo_llama_layer_forward",
+    "zo_causal_attention_gqa", "zo_llama_lora_layer_workspace", "zo_llama_lora_layer_forward",
 )
 ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL, ZO_EPI_SILU_MUL = 0, 1, 2, 3
 
@@ -57,6 +58,17 @@ class LlamaLayerDesc(ctypes.Structure):
     """zo_llama_layer: seven perturbed matrices and the two RMS norms' gamma."""
     _fields_ = [(nm, Matrix) for nm in ("q", "k", "v", "o", "gate", "up", "down")] + [
         (nm, ctypes.c_void_p) for nm in ("rms1_gamma", "rms2_gamma")]
+
+
+class LoraMatrix(ctypes.Structure):
+    """zo_lora_matrix: a frozen W and its LoRA factors with their subspaces and coefficients."""
+    _fields_ = [(nm, ctypes.c_void_p) for nm in ("W", "A", "U_A", "V_A", "Z_A", "B", "U_B", "V_B", "Z_B")]
+
+
+class LlamaLoraLayerDesc(ctypes.Structure):
+    """zo_llama_lora_layer: adapted q and v, the frozen k, o, gate, up, down, the RMS gammas."""
+    _fields_ = [("q", LoraMatrix), ("v", LoraMatrix)] + [
+        (nm, ctypes.c_void_p) for nm in ("k", "o", "gate", "up", "down", "rms1_gamma", "rms2_gamma")]
 
 
 class ZoError(RuntimeError):
@@ -171,6 +183,16 @@ def lib() -> ctypes.CDLL:
                                                                 ctypes.POINTER(ctypes.c_int8), c_f, c_f, c_f, c_int,
                                                                 c_vp, c_ll, ctypes.POINTER(LlamaLayerDesc),
                                                                 c_vp, c_vp, c_sz, c_vp])
+            L.zo_causal_attention_gqa.restype = c_int
+            L.zo_causal_attention_gqa.argtypes = [c_int] * 7 + [c_vp] * 5
+            L.zo_llama_lora_layer_workspace.restype = c_sz
+            L.zo_llama_lora_layer_workspace.argtypes = [c_int] * 11
+            L.zo_llama_lora_layer_forward.restype = c_int
+            L.zo_llama_lora_layer_forward.argtypes = ([c_int] * 10 + [ctypes.POINTER(ctypes.c_int),
+                                                                      ctypes.POINTER(ctypes.c_int8), c_f, c_f, c_f,
+                                                                      c_f, c_int, c_vp, c_ll,
+                                                                      ctypes.POINTER(LlamaLoraLayerDesc), c_vp, c_vp,
+                                                                      c_sz, c_vp])
             _lib = L
     return _lib
 
@@ -395,17 +417,25 @@ def rope(X: torch.Tensor, seq_len: int, heads: int, base: float = 10000.0):
 
 
 def causal_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, nblk: int, T: int, seq_len: int,
-                     heads: int, out: Optional[torch.Tensor] = None):
-    """Multi-head causal self-attention of nblk blocks of T rows (T / seq_len sequences each).
-    See zo_causal_attention."""
+                     heads: int, out: Optional[torch.Tensor] = None, kv_heads: Optional[int] = None):
+    """Multi-head causal self-attention of nblk blocks of T rows (T / seq_len sequences each);
+    with kv_heads, K and V hold kv_heads grouped key/value heads.  See zo_causal_attention(_gqa)."""
     d = Q.shape[-1]
-    for nm, t in (("Q", Q), ("K", K), ("V", V)):
-        _need(t, nm, Q.dtype, nblk * T * d)
+    if Q.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {Q.dtype}")
+    dkv = d if kv_heads is None else d // heads * kv_heads
+    _need(Q, "Q", Q.dtype, nblk * T * d)
+    for nm, t in (("K", K), ("V", V)):
+        _need(t, nm, Q.dtype, nblk * T * dkv)
     if out is None:
         out = torch.empty_like(Q)
     _need(out, "out", Q.dtype, nblk * T * d)
-    _check(lib().zo_causal_attention(nblk, T, seq_len, d, heads, _DT[Q.dtype], Q.data_ptr(), K.data_ptr(),
-                                     V.data_ptr(), out.data_ptr(), _stream_handle()))
+    if kv_heads is None:
+        _check(lib().zo_causal_attention(nblk, T, seq_len, d, heads, _DT[Q.dtype], Q.data_ptr(), K.data_ptr(),
+                                         V.data_ptr(), out.data_ptr(), _stream_handle()))
+    else:
+        _check(lib().zo_causal_attention_gqa(nblk, T, seq_len, d, heads, kv_heads, _DT[Q.dtype], Q.data_ptr(),
+                                             K.data_ptr(), V.data_ptr(), out.data_ptr(), _stream_handle()))
     return out
 
 
@@ -546,6 +576,83 @@ class LlamaLayer:
         _check(lib().zo_llama_layer_forward(*self.dims, self.bq, self.bs, self.eps, self.eps_rms, self.base,
                                             self.dt, H.data_ptr(), hs, ctypes.byref(self.desc), out.data_ptr(),
                                             self.ws.data_ptr(), self.ws.numel(), _stream_handle()))
+        return out
+
+
+class LlamaLoraLayer:
+    """The LoRA-scheme LLaMA-family layer (grouped key/value heads, frozen base, adapters on q
+    and v perturbed per block).  See zo_llama_lora_layer_forward.  ``mats`` maps q and v to
+    dicts with W (the layer's dtype), A, UA, VA, ZA, B, UB, VB, ZB (fp32), and k, o, gate, up,
+    down to dicts with W; ``norms`` holds rms1_gamma and rms2_gamma."""
+
+    FROZEN = ("k", "o", "gate", "up", "down")
+
+    def __init__(self, mats: dict, norms: dict, blk_query: Sequence[int], blk_sign: Sequence[int], eps: float,
+                 scale: float, T: int, seq_len: int, heads: int, kv_heads: int, eps_rms: float = 1e-6,
+                 rope_base: float = 1e6, workspace: Optional[torch.Tensor] = None):
+        nblk = len(blk_query)
+        if len(blk_sign) != nblk:
+            raise ValueError("blk_query and blk_sign differ in length")
+        Wq = mats["q"]["W"]
+        d, dt = Wq.shape[0], Wq.dtype
+        if dt not in _DT:
+            raise TypeError(f"unsupported dtype {dt}")
+        dkv = d // heads * kv_heads
+        ffn = mats["gate"]["W"].shape[0]
+        rl, r = mats["q"]["A"].shape[0], mats["q"]["UA"].shape[1]
+        q = mats["q"]["ZA"].shape[0]
+        desc = LlamaLoraLayerDesc()
+        for nm, m in (("q", d), ("v", dkv)):
+            mt = mats[nm]
+            _need(mt["W"], f"{nm}.W", dt, m * d)
+            for key, numel in (("A", rl * d), ("UA", rl * r), ("VA", d * r), ("ZA", q * r * r), ("B", m * rl),
+                               ("UB", m * r), ("VB", rl * r), ("ZB", q * r * r)):
+                _need(mt[key], f"{nm}.{key}", torch.float32, numel)
+            setattr(desc, nm, LoraMatrix(*[mt[k].data_ptr() for k in ("W", "A", "UA", "VA", "ZA", "B", "UB", "VB",
+                                                                      "ZB")]))
+        shapes = {"k": (dkv, d), "o": (d, d), "gate": (ffn, d), "up": (ffn, d), "down": (d, ffn)}
+        for nm in self.FROZEN:
+            m, n = shapes[nm]
+            _need(mats[nm]["W"], f"{nm}.W", dt, m * n)
+            setattr(desc, nm, mats[nm]["W"].data_ptr())
+        for nm in ("rms1_gamma", "rms2_gamma"):
+            _need(norms[nm], nm, torch.float32, d)
+            setattr(desc, nm, norms[nm].data_ptr())
+        self.desc, self.keep = desc, (mats, norms)
+        self.dims = (T, seq_len, d, heads, kv_heads, ffn, rl, r, q, nblk)
+        self.bq = (ctypes.c_int * nblk)(*[int(v) for v in blk_query])
+        self.bs = (ctypes.c_int8 * nblk)(*[int(v) for v in blk_sign])
+        self.eps, self.scale, self.eps_rms, self.base = float(eps), float(scale), float(eps_rms), float(rope_base)
+        self.dt, self.dtype = _DT[dt], dt
+        need = lib().zo_llama_lora_layer_workspace(*self.dims, self.dt)
+        if need == 0:
+            _check(lib().zo_llama_lora_layer_forward(*self.dims, self.bq, self.bs, self.eps, self.scale, self.eps_rms,
+                                                     self.base, self.dt, None, 0, ctypes.byref(self.desc), None, None,
+                                                     0, None))
+        if workspace is None:
+            workspace = Workspace.get(need)
+        _need(workspace, "workspace", torch.uint8)
+        if workspace.numel() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, {need} needed")
+        self.ws = workspace
+
+    def __call__(self, H: torch.Tensor, out: Optional[torch.Tensor] = None):
+        """H: one T x d input shared by all blocks, or nblk blocks; returns nblk blocks of T x d."""
+        T, d, nblk = self.dims[0], self.dims[2], self.dims[9]
+        _need(H, "H", self.dtype)
+        if H.numel() == T * d:
+            hs = 0
+        elif H.numel() == nblk * T * d:
+            hs = T * d
+        else:
+            raise ValueError("H must hold T*d or nblk*T*d elements")
+        if out is None:
+            out = torch.empty((nblk * T, d), dtype=self.dtype, device=H.device)
+        _need(out, "out", self.dtype, nblk * T * d)
+        _check(lib().zo_llama_lora_layer_forward(*self.dims, self.bq, self.bs, self.eps, self.scale, self.eps_rms,
+                                                 self.base, self.dt, H.data_ptr(), hs, ctypes.byref(self.desc),
+                                                 out.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+                                                 _stream_handle()))
         return out
 
 

@@ -351,10 +351,14 @@ int zo_rope(long long rows, int seq_len, int d, int heads, int dtype, void* X, f
   return zo_rope_launch(rows, seq_len, d, heads, dtype, X, base, (hipStream_t)stream);
 }
 
-static int check_attention(int nblk, int T, int seq_len, int d, int heads, int dtype) {
+// kv_heads < 0: as many key/value heads as query heads (plain multi-head attention).
+static int check_attention(int nblk, int T, int seq_len, int d, int heads, int dtype, int kv_heads = -1) {
   ZO_CHECK(nblk >= 1 && T >= 1 && seq_len >= 1 && T % seq_len == 0,
            "attention: nblk = %d, T = %d, seq_len = %d (need T %% seq_len == 0)", nblk, T, seq_len);
   ZO_CHECK(heads >= 1 && d % heads == 0, "attention: d = %d not a multiple of heads = %d", d, heads);
+  if (kv_heads < 0) kv_heads = heads;
+  ZO_CHECK(kv_heads >= 1 && heads % kv_heads == 0, "attention: heads = %d not a multiple of kv_heads = %d",
+           heads, kv_heads);
   if (dtype != ZO_BF16 && dtype != ZO_F16) {
     zo_set_error("attention: dtype %d unsupported (bf16 or fp16)", dtype);
     return ZO_ERR_UNSUPPORTED;
@@ -375,7 +379,18 @@ int zo_causal_attention(int nblk, int T, int seq_len, int d, int heads, int dtyp
   ZO_CHECK(Q && K && V && O, "attention: NULL tensor argument");
   ZO_CHECK(aligned(Q, 16) && aligned(K, 16) && aligned(V, 16) && aligned(O, 16),
            "attention: Q, K, V, O must be 16-byte aligned");
-  return zo_attention_launch(nblk, T, seq_len, d, heads, dtype, Q, K, V, O, (hipStream_t)stream);
+  return zo_attention_launch(nblk, T, seq_len, d, heads, heads, dtype, Q, K, V, O, (hipStream_t)stream);
+}
+
+int zo_causal_attention_gqa(int nblk, int T, int seq_len, int d, int heads, int kv_heads, int dtype,
+                            const void* Q, const void* K, const void* V, void* O, void* stream) {
+  ZO_CHECK(kv_heads >= 1, "attention: kv_heads = %d must be >= 1", kv_heads);
+  int st = check_attention(nblk, T, seq_len, d, heads, dtype, kv_heads);
+  if (st != ZO_OK) return st;
+  ZO_CHECK(Q && K && V && O, "attention: NULL tensor argument");
+  ZO_CHECK(aligned(Q, 16) && aligned(K, 16) && aligned(V, 16) && aligned(O, 16),
+           "attention: Q, K, V, O must be 16-byte aligned");
+  return zo_attention_launch(nblk, T, seq_len, d, heads, kv_heads, dtype, Q, K, V, O, (hipStream_t)stream);
 }
 
 namespace {
@@ -515,7 +530,7 @@ int zo_decoder_layer_forward(int T, int seq_len, int d, int heads, int ffn, int 
                         w.lin, w.grp, s)) != ZO_OK)
       return st;
   }
-  if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
+  if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
     return st;
   // H2 = H + C Wo'^T;  A = LN2(H2);  F = relu(A W1'^T);  H_out = H2 + F W2'^T.
   if ((st = lin(&layer->o, d, d, w.C, Td, w.H2, ZO_EPI_RESIDUAL, H, h_block_stride)) != ZO_OK) return st;
@@ -621,7 +636,7 @@ int zo_llama_layer_forward(int T, int seq_len, int d, int heads, int ffn, int r,
   }
   if ((st = zo_rope_launch(rows, seq_len, d, heads, dtype, w.Qb, rope_base, s)) != ZO_OK) return st;
   if ((st = zo_rope_launch(rows, seq_len, d, heads, dtype, w.Kb, rope_base, s)) != ZO_OK) return st;
-  if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
+  if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
     return st;
   // H2 = H + C Wo'^T;  A = RMS2(H2);  G = A Wg'^T;  F = silu(G) * (A Wu'^T);  H_out = H2 + F Wd'^T.
   if ((st = lin(&layer->o, d, d, w.C, Td, w.H2, ZO_EPI_RESIDUAL, H, h_block_stride)) != ZO_OK) return st;
@@ -638,6 +653,132 @@ int zo_llama_layer_forward(int T, int seq_len, int d, int heads, int ffn, int r,
       return st;
   }
   return lin(&layer->down, d, ffn, w.F, Tf, H_out, ZO_EPI_RESIDUAL, w.H2, Td);
+}
+
+// ------------------------------------------------------- LoRA-scheme LLaMA-family layer
+namespace {
+struct LoraLayerWs {
+  char *A, *Qb, *Kb, *Vb, *C, *H2, *G, *F, *lin;
+  size_t total;
+};
+static LoraLayerWs lora_layer_ws(int T, int d, int dkv, int ffn, int rl, int r, int q, int nblk, int dtype,
+                                 void* base) {
+  const size_t es = 2;
+  const size_t act = zo_align256((size_t)nblk * T * d * es), kv = zo_align256((size_t)nblk * T * dkv * es);
+  const size_t wide = zo_align256((size_t)nblk * T * ffn * es);
+  size_t lin = 0;
+  for (int m : {d, dkv}) {
+    PlinearPlan p;
+    zo_plinear_plan(&p, T, m, d, rl + r, q, nblk, (long long)T * d, dtype, dtype);
+    lin = p.ws_total > lin ? p.ws_total : lin;
+  }
+  WsCarver wc(base);
+  LoraLayerWs w;
+  w.A = (char*)wc.take(act);
+  w.Qb = (char*)wc.take(act);
+  w.Kb = (char*)wc.take(kv);
+  w.Vb = (char*)wc.take(kv);
+  w.C = (char*)wc.take(act);
+  w.H2 = (char*)wc.take(act);
+  w.G = (char*)wc.take(wide);
+  w.F = (char*)wc.take(wide);
+  w.lin = (char*)wc.take(lin);
+  w.total = wc.off;
+  return w;
+}
+static int check_lora_layer(int T, int seq_len, int d, int heads, int kv_heads, int ffn, int rl, int r, int q,
+                            int nblk, int dtype) {
+  ZO_CHECK(kv_heads >= 1, "lora layer: kv_heads = %d must be >= 1", kv_heads);
+  int st = check_attention(nblk, T, seq_len, d, heads, dtype, kv_heads);
+  if (st != ZO_OK) return st;
+  const int dkv = d / heads * kv_heads;
+  ZO_CHECK(ffn >= 8 && ffn % 8 == 0, "lora layer: ffn = %d must be a positive multiple of 8", ffn);
+  if ((st = check_lora(T, d, d, rl, r, q, nblk, (long long)T * d, dtype)) != ZO_OK) return st;
+  if ((st = check_lora(T, dkv, d, rl, r, q, nblk, (long long)T * d, dtype)) != ZO_OK) return st;
+  if ((st = check_plinear(T, ffn, d, 1, q, nblk, (long long)T * d, dtype)) != ZO_OK) return st;
+  return check_plinear(T, d, ffn, 1, q, nblk, (long long)T * ffn, dtype);
+}
+}  // namespace
+
+size_t zo_llama_lora_layer_workspace(int T, int seq_len, int d, int heads, int kv_heads, int ffn, int rl,
+                                     int r, int q, int nblk, int dtype) {
+  if (check_lora_layer(T, seq_len, d, heads, kv_heads, ffn, rl, r, q, nblk, dtype) != ZO_OK) return 0;
+  if (check_rope((long long)nblk * T, seq_len, d, heads, dtype, 1e6f) != ZO_OK) return 0;
+  return lora_layer_ws(T, d, d / heads * kv_heads, ffn, rl, r, q, nblk, dtype, nullptr).total;
+}
+
+int zo_llama_lora_layer_forward(int T, int seq_len, int d, int heads, int kv_heads, int ffn, int rl, int r,
+                                int q, int nblk, const int* blk_query, const int8_t* blk_sign, float eps,
+                                float scale, float eps_rms, float rope_base, int dtype, const void* H,
+                                long long h_block_stride, const zo_llama_lora_layer* layer, void* H_out,
+                                void* workspace, size_t ws_bytes, void* stream) {
+  int st = check_lora_layer(T, seq_len, d, heads, kv_heads, ffn, rl, r, q, nblk, dtype);
+  if (st != ZO_OK) return st;
+  const int dkv = d / heads * kv_heads;
+  if ((st = check_rope((long long)nblk * T, seq_len, d, heads, dtype, rope_base)) != ZO_OK) return st;
+  ZO_CHECK(layer && H && H_out, "lora layer: NULL argument (layer, H or H_out)");
+  ZO_CHECK(h_block_stride == 0 || h_block_stride == (long long)T * d,
+           "lora layer: h_block_stride = %lld must be 0 (one H for every block) or T*d", h_block_stride);
+  ZO_CHECK(isfinite(eps_rms) && eps_rms >= 0.f, "lora layer: eps_rms must be finite and >= 0");
+  const zo_lora_matrix* ad[2] = {&layer->q, &layer->v};
+  for (int i = 0; i < 2; ++i) {
+    if ((st = check_lora_factors(q, nblk, blk_query, blk_sign, eps, scale, ad[i]->A, ad[i]->U_A, ad[i]->V_A,
+                                 ad[i]->Z_A, ad[i]->B, ad[i]->U_B, ad[i]->V_B, ad[i]->Z_B)) != ZO_OK)
+      return st;
+    ZO_CHECK(ad[i]->W && aligned(ad[i]->W, 16), "lora layer: %s W is NULL or not 16-byte aligned",
+             i ? "v" : "q");
+  }
+  const void* frozen[5] = {layer->k, layer->o, layer->gate, layer->up, layer->down};
+  for (int i = 0; i < 5; ++i)
+    ZO_CHECK(frozen[i] && aligned(frozen[i], 16), "lora layer: a frozen weight is NULL or not 16-byte aligned");
+  ZO_CHECK(layer->rms1_gamma && layer->rms2_gamma && aligned(layer->rms1_gamma, 16) &&
+               aligned(layer->rms2_gamma, 16),
+           "lora layer: RMS-norm parameters NULL or not 16-byte aligned");
+  ZO_CHECK(aligned(H, 16) && aligned(H_out, 16), "lora layer: H and H_out must be 16-byte aligned");
+  const LoraLayerWs need = lora_layer_ws(T, d, dkv, ffn, rl, r, q, nblk, dtype, nullptr);
+  if (!workspace || ws_bytes < need.total) {
+    zo_set_error("lora layer: workspace %zu bytes < required %zu", ws_bytes, need.total);
+    return ZO_ERR_WORKSPACE;
+  }
+  ZO_CHECK(aligned(workspace, 256), "lora layer: workspace not 256-byte aligned");
+  const LoraLayerWs w = lora_layer_ws(T, d, dkv, ffn, rl, r, q, nblk, dtype, workspace);
+  hipStream_t s = (hipStream_t)stream;
+  const long long Td = (long long)T * d, Tf = (long long)T * ffn;
+  const long long rows = (long long)nblk * T;
+  const bool shared = h_block_stride == 0;
+  const long long as = shared ? 0 : Td;
+  // An adapted matrix: both factors perturbed (X_b [A^T | V_A] times scale [B' | s eps B' U_A Z_A]).
+  auto lora = [&](const zo_lora_matrix* mt, int m, void* Y) -> int {
+    PlinearPlan p;
+    zo_plinear_plan(&p, T, m, d, rl + r, q, nblk, as, dtype, dtype);
+    int e = zo_lora_prepare(p, rl, r, blk_query, blk_sign, eps, scale, w.A, mt->A, mt->U_A, mt->V_A, mt->Z_A,
+                            mt->B, mt->U_B, mt->V_B, mt->Z_B, w.lin, s);
+    if (e != ZO_OK) return e;
+    return zo_plinear_apply(p, w.A, mt->W, Y, w.lin, s);
+  };
+  // A = RMS1(H): once when every block shares H.
+  if ((st = zo_layernorm_launch(shared ? T : rows, d, dtype, H, layer->rms1_gamma, nullptr, eps_rms, w.A, s,
+                                true)) != ZO_OK)
+    return st;
+  if ((st = lora(&layer->q, d, w.Qb)) != ZO_OK) return st;
+  if ((st = zo_gemm_plain(T, dkv, d, nblk, dtype, w.A, as, layer->k, w.Kb, ZO_EPI_NONE, nullptr, 0, s)) != ZO_OK)
+    return st;
+  if ((st = lora(&layer->v, dkv, w.Vb)) != ZO_OK) return st;
+  if ((st = zo_rope_launch(rows, seq_len, d, heads, dtype, w.Qb, rope_base, s)) != ZO_OK) return st;
+  if ((st = zo_rope_launch(rows, seq_len, dkv, kv_heads, dtype, w.Kb, rope_base, s)) != ZO_OK) return st;
+  if ((st = zo_attention_launch(nblk, T, seq_len, d, heads, kv_heads, dtype, w.Qb, w.Kb, w.Vb, w.C, s)) != ZO_OK)
+    return st;
+  // H2 = H + C Wo^T;  A = RMS2(H2);  G = A Wg^T;  F = silu(G) * (A Wu^T);  H_out = H2 + F Wd^T.
+  if ((st = zo_gemm_plain(T, d, d, nblk, dtype, w.C, Td, layer->o, w.H2, ZO_EPI_RESIDUAL, H, h_block_stride, s)) !=
+      ZO_OK)
+    return st;
+  if ((st = zo_layernorm_launch(rows, d, dtype, w.H2, layer->rms2_gamma, nullptr, eps_rms, w.A, s, true)) != ZO_OK)
+    return st;
+  if ((st = zo_gemm_plain(T, ffn, d, nblk, dtype, w.A, Td, layer->gate, w.G, ZO_EPI_NONE, nullptr, 0, s)) != ZO_OK)
+    return st;
+  if ((st = zo_gemm_plain(T, ffn, d, nblk, dtype, w.A, Td, layer->up, w.F, ZO_EPI_SILU_MUL, w.G, Tf, s)) != ZO_OK)
+    return st;
+  return zo_gemm_plain(T, d, ffn, nblk, dtype, w.F, Tf, layer->down, H_out, ZO_EPI_RESIDUAL, w.H2, Td, s);
 }
 
 // ------------------------------------------------------------------ update

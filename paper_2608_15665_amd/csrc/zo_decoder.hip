@@ -264,6 +264,7 @@ struct AttnArgs {
   const void* V;
   void* O;
   int T, seq_len, d, heads, qtiles;  // qtiles = ceil(seq_len / AT_Q)
+  int dkv, group;                    // K/V row length (kv_heads dh); query heads per K/V head
   float scale_log2;                  // log2(e) / sqrt(dh)
 };
 
@@ -332,6 +333,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
   const int blk = w / nseq;
   const long long row0 = (long long)blk * a.T + (long long)seq * a.seq_len;  // first row of the sequence
   const int col0 = head * DH;
+  const int col0kv = (head / a.group) * DH;  // the key/value head of this query head
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
   const int q0 = qt * AT_Q;  // first query of the tile (within the sequence)
@@ -370,7 +372,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < KCH; ++c) {
       const int x = tid + 256 * c;
-      const size_t off = (size_t)(row0 + min(k0 + x / C8, a.seq_len - 1)) * a.d + col0 + 8 * (x % C8);
+      const size_t off = (size_t)(row0 + min(k0 + x / C8, a.seq_len - 1)) * a.dkv + col0kv + 8 * (x % C8);
       kreg[c] = *(const u32x4*)(Kg + off);
       vreg[c] = *(const u32x4*)(Vg + off);
     }
@@ -553,8 +555,8 @@ int zo_rope_launch(long long rows, int seq_len, int d, int heads, int dtype, voi
   return zo_hip_status(hipGetLastError(), "k_rope");
 }
 
-int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int dtype, const void* Q,
-                        const void* K, const void* V, void* O, hipStream_t stream) {
+int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int kv_heads, int dtype,
+                        const void* Q, const void* K, const void* V, void* O, hipStream_t stream) {
   AttnArgs a;
   a.Q = Q;
   a.K = K;
@@ -564,6 +566,8 @@ int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int dtyp
   a.seq_len = seq_len;
   a.d = d;
   a.heads = heads;
+  a.dkv = d / heads * kv_heads;
+  a.group = heads / kv_heads;
   a.qtiles = (seq_len + AT_Q - 1) / AT_Q;
   const int dh = d / heads;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)dh);

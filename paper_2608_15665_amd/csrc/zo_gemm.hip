@@ -970,6 +970,30 @@ int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_
   return zo_hip_status(hipGetLastError(), "k_gemm_f32 (projection)");
 }
 
+int zo_gemm_plain(int T, int m, int n, int nblk, int dtype, const void* X, long long x_block_stride,
+                  const void* W, void* Y, int epi, const void* R, long long r_block_stride,
+                  hipStream_t stream) {
+  GemmArgs h{};
+  h.A = (const bf16_t*)W;
+  h.B = (const bf16_t*)X;
+  h.b_block_stride = x_block_stride;
+  h.rows_a = m;
+  h.rows_b = T;
+  h.K = n;
+  h.nblk = nblk;
+  h.rc = 0;
+  h.Y = Y;
+  h.y_block_stride = (long long)T * m;
+  h.ldy = m;
+  h.out_dtype = dtype;
+  h.epi = epi;
+  h.R = R;
+  h.r_block_stride = r_block_stride;
+  const bool f16 = dtype == ZO_F16;
+  if (n % 32 == 0) return launch_gemm_main(h, f16, stream);
+  return f16 ? launch_gemm_bf16<2, 4, 4, 2, true>(h, stream) : launch_gemm_bf16<2, 4, 4, 2, false>(h, stream);
+}
+
 int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
                      hipStream_t stream, int epi, const void* R, long long r_block_stride) {
   const PlinearWs w = zo_plinear_ws(p, ws);

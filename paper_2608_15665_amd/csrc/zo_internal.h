@@ -133,6 +133,11 @@ int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t*
 // separate prepares (every projection tile covers one matrix's rows).  fp32 plans, or
 // count < 2, take the separate prepares.
 size_t zo_plinear_group_ws(const PlinearPlan& p, int count);
+// X_b W^T for every block with no perturbation (a frozen matrix): the fused GEMM without its
+// rank-r segment, with the same epilogues.  16-bit inputs and outputs of one type.
+int zo_gemm_plain(int T, int m, int n, int nblk, int dtype, const void* X, long long x_block_stride,
+                  const void* W, void* Y, int epi, const void* R, long long r_block_stride,
+                  hipStream_t stream);
 int zo_plinear_prepare_group(const PlinearPlan* plans, int count, const int* blk_query,
                              const int8_t* blk_sign, float eps, const void* X, const float* const* U,
                              const float* const* V, const float* const* Z, void* const* ws, void* gws,
@@ -142,8 +147,8 @@ int zo_layernorm_launch(long long rows, int d, int dtype, const void* X, const f
                         const float* beta, float eps_ln, void* Y, hipStream_t stream, bool rms = false);
 int zo_rope_launch(long long rows, int seq_len, int d, int heads, int dtype, void* X, float base,
                    hipStream_t stream);
-int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int dtype, const void* Q,
-                        const void* K, const void* V, void* O, hipStream_t stream);
+int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int kv_heads, int dtype,
+                        const void* Q, const void* K, const void* V, void* O, hipStream_t stream);
 int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
                      hipStream_t stream, int epi = ZO_EPI_NONE, const void* R = nullptr,
                      long long r_block_stride = 0);

@@ -87,7 +87,7 @@ def ulp16(x, dt):
     return np.ldexp(1.0, np.maximum(e - 11, -24)) if dt == "f16" else np.ldexp(1.0, e - 8)
 
 
-def check_attention(got, Q, K, V, heads, seq_len, dt, what):
+def check_attention(got, Q, K, V, heads, seq_len, dt, what, kv_heads=None):
     """Causal attention held to the bar its arithmetic sets.  P enters the P V product as a
     hi + lo pair of 16-bit values (relative error <= 2^-17 for bf16 pairs, less for fp16), and
     the fp32 logits carry an absolute error of a few 2^-24 |q| |k|, which moves P by under
@@ -95,8 +95,8 @@ def check_attention(got, Q, K, V, heads, seq_len, dt, what):
     2^-14 softmax(S) |V| (the same average taken of |V|, with margin) of the exact one, and
     after it within one ulp more; blockwise it keeps the normwise bar of a single rounding."""
     import oracle
-    ref = oracle.causal_attention(Q, K, V, heads, seq_len)
-    mag = oracle.causal_attention(Q, K, np.abs(V), heads, seq_len)
+    ref = oracle.causal_attention(Q, K, V, heads, seq_len, kv_heads)
+    mag = oracle.causal_attention(Q, K, np.abs(V), heads, seq_len, kv_heads)
     assert normwise(got, ref) <= 2e-3, what
     bound = ulp16(ref, dt) + 2.0 ** -14 * mag
     err = np.abs(np.asarray(got, np.float64) - ref)

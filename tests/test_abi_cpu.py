@@ -285,6 +285,33 @@ def test_llama_entry_points_validation():
     assert st == 1 and "eps_rms" in _detail()
 
 
+def test_lora_layer_and_grouped_attention_validation():
+    """Grouped attention and the LoRA-scheme layer reject bad arguments before launching."""
+    L = zo.lib()
+    fake = 1 << 20
+    assert L.zo_causal_attention_gqa(1, 128, 64, 512, 4, 3, 1, fake, fake, fake, fake, None) == 1
+    assert "kv_heads" in _detail()
+    assert L.zo_causal_attention_gqa(1, 128, 64, 512, 4, 0, 1, fake, fake, fake, fake, None) == 1
+    assert L.zo_causal_attention_gqa(1, 128, 64, 512, 4, -1, 1, fake, fake, fake, fake, None) == 1
+    assert L.zo_llama_lora_layer_workspace(128, 64, 256, 2, 0, 512, 4, 4, 2, 4, 1) == 0
+    assert L.zo_causal_attention_gqa(1, 128, 64, 512, 4, 2, 0, fake, fake, fake, fake, None) == 2  # fp32
+    assert L.zo_causal_attention_gqa(1, 128, 64, 512, 4, 2, 1, fake, None, fake, fake, None) == 1
+    args = (128, 64, 256, 2, 1, 512, 4, 4, 2, 4)
+    assert L.zo_llama_lora_layer_workspace(*args, 1) > 0
+    assert L.zo_llama_lora_layer_workspace(*args, 0) == 0                       # fp32: no attention kernel
+    assert L.zo_llama_lora_layer_workspace(128, 64, 256, 2, 3, 512, 4, 4, 2, 4, 1) == 0   # heads % kv_heads
+    assert L.zo_llama_lora_layer_workspace(128, 64, 256, 2, 1, 512, 100, 40, 2, 4, 1) == 0  # rl + r > 128
+    layer = zo._lib.LlamaLoraLayerDesc()
+    bq4 = (ctypes.c_int * 4)(0, 0, 1, 1)
+    bs4 = (ctypes.c_int8 * 4)(1, -1, 1, -1)
+    st = L.zo_llama_lora_layer_forward(*args, bq4, bs4, 1e-3, 2.0, 1e-6, 1e6, 1, fake, 0, ctypes.byref(layer), fake,
+                                       fake, 1 << 40, None)
+    assert st == 1 and "NULL" in _detail()
+    st = L.zo_llama_lora_layer_forward(*args, bq4, bs4, 1e-3, 2.0, 1e-6, 1e6, 1, fake, 7, ctypes.byref(layer), fake,
+                                       fake, 1 << 40, None)
+    assert st == 1 and "h_block_stride" in _detail()
+
+
 def test_empty_calls_are_no_ops():
     """count = 0 refreshes and updates, and zero-row layer norms, succeed without launching."""
     L = zo.lib()

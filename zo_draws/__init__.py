@@ -192,7 +192,9 @@ CONFIGS = {
                             [("q", 5120, 5120), ("k", 1024, 5120), ("v", 1024, 5120),
                              ("o", 5120, 5120), ("gate", 27648, 5120), ("up", 27648, 5120),
                              ("down", 5120, 27648)],
-                            T=4096, r=4, q=4, lr=1e-2),
+                            T=4096, r=4, q=4, lr=1e-2,
+                            decoder=dict(d=5120, heads=40, kv_heads=8, ffn=27648, seq_len=256,  # 16 x 256
+                                         family="llama-lora", rope_base=1e6)),
 }
 QWEN_LORA_RANK = 8
 QWEN_LORA_ALPHA = 16
