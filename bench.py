@@ -212,6 +212,8 @@ def run_decoder(args):
     if not dec:
         print(f"bench.py: --model decoder has no layer shape for {args.config}", file=sys.stderr)
         sys.exit(2)
+    if dec.get("family") == "llama-lora":
+        return run_decoder_lora(args, cfg, dec)
     llama = dec.get("family") == "llama"
     T, r, q = cfg["T"], cfg["r"], cfg["q"]
     if args.queries:
@@ -377,6 +379,181 @@ def run_decoder(args):
     print(json.dumps(out), flush=True)
 
 
+def run_decoder_lora(args, cfg, dec):
+    """The decoder step of the LoRA scheme (Qwen-shaped LLaMA-family layers with grouped
+    key/value heads): refresh of every adapter factor's subspace (t mod F == 0), the forward of
+    all 2q blocks through every layer (zo_llama_lora_layer_forward: frozen k, o, gate, up, down;
+    adapted q and v with both factors perturbed), the loss and estimate, and the subspace Adam
+    update of the adapter factors (fp32)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_15665_amd as zo
+    import zo_draws as zd
+
+    T, r, q = cfg["T"], cfg["r"], cfg["q"]
+    if args.queries:
+        q = args.queries
+    if args.rank:
+        r = args.rank
+    d, heads, kv, ffn, L = dec["d"], dec["heads"], dec["kv_heads"], dec["ffn"], dec["seq_len"]
+    dkv = d // heads * kv
+    rl, scale = zd.QWEN_LORA_RANK, zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
+    layers = cfg["layers"]
+    forward = args.estimator == "forward"
+    if forward:
+        bq, bs = [0] + list(range(q)), [0] + [1] * q
+    else:
+        bq, bs = [b // 2 for b in range(2 * q)], [1 if b % 2 == 0 else -1 for b in range(2 * q)]
+    nblk = len(bq)
+    nsigned = sum(1 for v in bs if v != 0)
+    eps, lr, b1, b2, ea, F = cfg["eps"], cfg["lr"], cfg["beta1"], cfg["beta2"], cfg["eps_adam"], cfg["F"]
+    seed, dev = args.seed, "cuda"
+    f16 = args.dtype == "fp16"
+    dt16 = torch.float16 if f16 else torch.bfloat16
+    t_setup = time.perf_counter()
+
+    def to16(a64):
+        if f16:
+            return torch.from_numpy(zd.as_f16_values(a64)[0]).to(dev)
+        return torch.from_numpy(zd.bf16_bits(zd.f32(a64)).view(np.int16)).view(dt16).to(dev)
+
+    f32dev = lambda a64: torch.from_numpy(zd.f32(a64)).to(dev)
+    shapes = {"q": (d, d), "k": (dkv, d), "v": (dkv, d), "o": (d, d), "gate": (ffn, d), "up": (ffn, d),
+              "down": (d, ffn)}
+    Wbase = {sh: to16(zd.draw(seed, "W0", sh, sh, 0.02)) for sh in set(shapes.values())}
+    Obase = {rw: f32dev(zd.draw(seed, "OMEGA_U", (rw, r), (rw, r))) for rw in sorted({d, dkv, rl})}
+    zeros_rr = lambda: torch.zeros((r, r), dtype=torch.float32, device=dev)
+    nsteps = args.warmup + args.steps
+    mats, factors, omegas, qouts, norms = [], [], [], [], []
+    for l in range(layers):
+        lm = {nm: dict(W=torch.roll(Wbase[sh], l, 0).contiguous()) for nm, sh in shapes.items()}
+        for nm in ("q", "v"):
+            m = shapes[nm][0]
+            u = lm[nm]
+            k = len(factors)
+            u["A"] = f32dev(zd.draw(seed, "LORA_A", (l, nm == "v"), (rl, d), 0.02))
+            u["B"] = torch.zeros((m, rl), dtype=torch.float32, device=dev)  # the usual LoRA start
+            for key, rw in (("UA", rl), ("VA", d), ("UB", m), ("VB", rl)):
+                omegas.append(torch.roll(Obase[rw], len(omegas), 0).contiguous())
+                u[key] = torch.empty((rw, r), dtype=torch.float32, device=dev)
+                qouts.append(u[key])
+            factors.append(dict(W=u["A"], U=u["UA"], V=u["VA"], M1=zeros_rr(), M2=zeros_rr(), m=rl, n=d, z=k))
+            factors.append(dict(W=u["B"], U=u["UB"], V=u["VB"], M1=zeros_rr(), M2=zeros_rr(), m=m, n=rl, z=k + 1))
+            u["zi"] = k
+        mats.append(lm)
+        g = f32dev(1.0 + 0.05 * zd.draw(seed, "W0", (l, 1), (2, d)))
+        norms.append(dict(rms1_gamma=g[0].contiguous(), rms2_gamma=g[1].contiguous()))
+    del Wbase, Obase
+    Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(len(factors))])
+                                   for t in range(nsteps)])).to(dev)  # [step, factor, q, r, r]
+    H0 = to16(zd.draw(seed, "X", (T, d, 0), (T, d)))
+    Ystar = to16(zd.draw(seed, "X", (T, d, 1), (T, d)))
+    Hbuf = [torch.empty((nblk * T, d), dtype=dt16, device=dev) for _ in range(2)]
+    ws = None
+
+    def layer_obj(t, l):
+        nonlocal ws
+        lm = {}
+        for nm, u in mats[l].items():
+            if nm in ("q", "v"):
+                lm[nm] = dict(W=u["W"], A=u["A"], UA=u["UA"], VA=u["VA"], ZA=Z[t, u["zi"]], B=u["B"], UB=u["UB"],
+                              VB=u["VB"], ZB=Z[t, u["zi"] + 1])
+            else:
+                lm[nm] = dict(W=u["W"])
+        o = zo.LlamaLoraLayer(lm, norms[l], bq, bs, eps, scale, T, L, heads, kv, rope_base=dec["rope_base"],
+                              workspace=ws)
+        ws = o.ws
+        return o
+
+    decs = [[layer_obj(t, l) for l in range(layers)] for t in range(nsteps)]
+    items = [[dict(W=f["W"], U=f["U"], V=f["V"], Z=Z[t, f["z"]], M1=f["M1"], M2=f["M2"]) for f in factors]
+             for t in range(nsteps)]
+    torch.cuda.synchronize()
+    log(f"setup {time.perf_counter() - t_setup:.1f} s; {layers} LoRA-scheme layers; "
+        f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB on device")
+    Ev = lambda: torch.cuda.Event(enable_timing=True)
+    recs = []
+
+    def step(t, s):
+        rec = {"layers": [], "upd": None, "refresh": None}
+        if t % F == 0:
+            e0, e1 = Ev(), Ev()
+            e0.record()
+            zo.subspace_refresh(omegas, r, out=qouts)
+            e1.record()
+            rec["refresh"] = (e0, e1)
+        H = H0
+        for l in range(layers):
+            e0, e1 = Ev(), Ev()
+            e0.record()
+            H = decs[s][l](H, out=Hbuf[l % 2])
+            e1.record()
+            rec["layers"].append((e0, e1))
+        Lb = zo.sq_loss(H, Ystar, nblk, T)
+        g = zo.combine_forward(Lb, eps) if forward else zo.combine_central(Lb, eps)
+        e0, e1 = Ev(), Ev()
+        e0.record()
+        zo.subspace_adam_update(items[s], g, t + 1, lr, b1, b2, ea)
+        e1.record()
+        rec["upd"] = (e0, e1)
+        return rec
+
+    for s in range(args.warmup):
+        step(s, s)
+        torch.cuda.synchronize()
+        log(f"warmup step {s} done")
+    for f in factors:
+        f["M1"].zero_()
+        f["M2"].zero_()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        recs.append(step(k, args.warmup + k))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"timed {args.steps} steps in {t1 - t0:.2f} s")
+
+    lin_layer = (lora_flops(T, d, d, rl, r, q, nblk, nsigned) + lora_flops(T, dkv, d, rl, r, q, nblk, nsigned)
+                 + sum(nblk * 2 * T * m * n for nm, (m, n) in shapes.items() if nm not in ("q", "v")))
+    att_layer = attention_flops(T, L, heads, d // heads, nblk)
+    value = lin_layer * layers * args.steps / (t1 - t0) / 1e12
+    layer_ms = [a.elapsed_time(b) for rc in recs for a, b in rc["layers"]]
+    avg_layer = sum(layer_ms) / len(layer_ms)
+    achieved = (lin_layer + att_layer) / (avg_layer * 1e-3) / 1e12
+    upd_ms = sum(rc["upd"][0].elapsed_time(rc["upd"][1]) for rc in recs)
+    upd_bytes = sum(update_bytes(f["m"], f["n"], r, q, 4) for f in factors) * args.steps
+    upd_gbps = upd_bytes / (upd_ms * 1e-3) / 1e9
+    ref_ms = [rc["refresh"][0].elapsed_time(rc["refresh"][1]) for rc in recs if rc["refresh"]]
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round((t1 - t0) / args.steps * 1e3, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": args.dtype, "data": "synthetic",
+        "config": {"workload": (f"{args.config}-shaped decoder: {layers} LLaMA-family layers of the LoRA scheme "
+                                f"(RMS norm, rotary positions base {dec['rope_base']:g}, d={d}, {heads} query heads "
+                                f"over {kv} key/value heads of {d // heads}, ffn={ffn}, SwiGLU), frozen k, o, gate, up, "
+                                f"down, adapters r_L={rl} (scale {scale:g}) on q and v with both factors perturbed; "
+                                + (f"{nblk} blocks (baseline + q={q} forward queries)" if forward
+                                   else f"{nblk} query blocks (q={q}, +/-)")
+                                + f" of T={T} tokens ({T // L} sequences x {L}); r={r}; {args.dtype}; value counts "
+                                  "the linear-layer FLOPs of the step (adapted at rank r_L + r, frozen plain)"),
+                   "layers": layers, "d": d, "heads": heads, "kv_heads": kv, "ffn": ffn, "seq_len": L, "T": T,
+                   "lora_rank": rl, "r": r, "q": q, "blocks": nblk, "estimator": args.estimator, "refresh_every": F},
+        "roofline": {"kernel": "zo_llama_lora_layer_forward (one layer: 2 RMS norms, 2 rotations, 2 adapted and 5 "
+                               "frozen fused GEMMs, grouped causal attention)", "bound": "mfma",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "launches": len(layer_ms), "avg_launch_ms": round(avg_layer, 4),
+                     "flops_per_launch_avg": lin_layer + att_layer},
+        "attention_flops_per_layer": att_layer,
+        "update": {"kernel": "zo_subspace_adam_update on the fp32 adapter factors (latency-bound)", "bound": "hbm",
+                   "achieved": round(upd_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                   "frac": round(upd_gbps / PEAK_HBM_GBPS, 4), "ms_per_step": round(upd_ms / args.steps, 3)},
+        "refresh_ms": round(ref_ms[0], 3) if ref_ms else None,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -392,7 +569,8 @@ def main():
     ap.add_argument("--model", default="stack", choices=["stack", "decoder"],
                     help="stack: the perturbed linears of every matrix on synthetic activations; decoder: "
                          "real decoder-layer forwards (OPT: layer norm, causal attention, ReLU MLP; llama-7b: "
-                         "RMS norm, rotary positions, causal attention, SwiGLU MLP; residuals)")
+                         "RMS norm, rotary positions, causal attention, SwiGLU MLP; qwen-32b-lora: the same with "
+                         "grouped key/value heads, a frozen base and perturbed adapters on q and v; residuals)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
