@@ -680,15 +680,25 @@ def main():
     else:
         ws_need = max(zo.lib().zo_perturbed_linear_workspace(T, m, n, r, q, nblk, T * n, zdt)
                       for m, n in shapes)
-    ws = torch.empty(ws_need, dtype=torch.uint8, device=dev)
+    # q, k and v of a layer read the same input: their prepares run as one group (one pass
+    # over X), so each keeps its own workspace until its apply.
+    grouped = not lora and [nm for nm, _, _ in unit_mats][:3] == ["q", "k", "v"]
+    wsets = [torch.empty(ws_need, dtype=torch.uint8, device=dev) for _ in range(3 if grouped else 1)]
+    ws = wsets[0]
+    gws = None
+    if grouped:
+        gneed = zo.lib().zo_perturbed_linear_group_workspace(3, T, unit_mats[0][2], r, q, nblk, T * unit_mats[0][2], zdt)
+        gws = torch.empty(max(gneed, 1), dtype=torch.uint8, device=dev)
 
     def make_layer(t, i, u):
         if lora:
             return zo.LoraPerturbedLinear(X[u["n"]], u["W"], u["A"], u["UA"], u["VA"], Z[t, 2 * i], u["B"], u["UB"],
                                           u["VB"], Z[t, 2 * i + 1], bq, bs, eps, scale, T,
                                           x_block_stride=T * u["n"], Y=Y[u["m"]], workspace=ws)
+        k = i % len(unit_mats)
         return zo.PerturbedLinear(X[u["n"]], u["W"], u["U"], u["V"], Z[t, i], bq, bs, eps, T,
-                                  x_block_stride=T * u["n"], Y=Y[u["m"]], workspace=ws)
+                                  x_block_stride=T * u["n"], Y=Y[u["m"]],
+                                  workspace=wsets[k] if grouped and k < 3 else ws)
 
     def make_items(t, i, u):
         if lora:
@@ -716,16 +726,25 @@ def main():
             zo.subspace_refresh(omegas, r, out=qouts)
             e1.record()
             rec["refresh"] = (e0, e1)
-        for i, mt in enumerate(units):
-            pl = plins[s][i]
-            e0, e1, e2 = Ev(), Ev(), Ev()
+        i = 0
+        while i < len(units):
+            g = 3 if grouped and i % len(unit_mats) == 0 else 1
+            e0, e1 = Ev(), Ev()
             e0.record()
-            pl.prepare()
+            if g == 3:
+                zo.prepare_group(plins[s][i:i + 3], gws)
+            else:
+                plins[s][i].prepare()
             e1.record()
-            pl.apply()
-            e2.record()
             rec["prep"].append((e0, e1))
-            rec["gemm"].append((e1, e2, mt["m"], mt["n"]))
+            for k in range(i, i + g):
+                mt = units[k]
+                a0, a1 = Ev(), Ev()
+                a0.record()
+                plins[s][k].apply()
+                a1.record()
+                rec["gemm"].append((a0, a1, mt["m"], mt["n"]))
+            i += g
         Lb = zo.sq_loss(Y[m_last], Ystar, nblk, T)
         g = zo.combine_forward(Lb, eps) if forward else zo.combine_central(Lb, eps)
         e0, e1 = Ev(), Ev()

@@ -55,6 +55,7 @@ extern "C" {
 #define ZO_MAX_QR_RANK 128 /* r limit of zo_subspace_refresh                 */
 #define ZO_MAX_BLOCKS 256 /* nblk limit of zo_perturbed_linear               */
 #define ZO_MAX_QUERIES 256
+#define ZO_MAX_GROUP 8    /* count limit of zo_perturbed_linear_prepare_group   */
 
 typedef enum {
   ZO_OK = 0,
@@ -175,6 +176,33 @@ int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk,
                               long long x_block_stride, const void* W,
                               int out_dtype, void* Y, void* workspace,
                               size_t ws_bytes, void* stream);
+
+/* prepare for count perturbed linears that read the same X (a layer's q, k
+ * and v): one projection pass reads X once for all of them, against their
+ * stacked V factors.  Matrix i has m[i] rows, its own U[i], V[i], Z[i] and its
+ * own workspace[i] (ws_bytes[i] bytes, as for zo_perturbed_linear_prepare);
+ * T, n, r, q, nblk, the blocks, eps, in_dtype, X and x_block_stride are
+ * shared.  group_ws: device scratch of zo_perturbed_linear_group_workspace
+ * bytes (0 for fp32 inputs or count = 1, when the call runs the separate
+ * prepares; group_ws may then be NULL).  The prepared operands are bitwise
+ * those of separate prepares; each matrix is then applied with
+ * zo_perturbed_linear_apply(_ex) and its own workspace.
+ * Limits: 1 <= count <= ZO_MAX_GROUP; those of zo_perturbed_linear. */
+size_t zo_perturbed_linear_group_workspace(int count, int T, int n, int r, int q,
+                                           int nblk, long long x_block_stride,
+                                           int in_dtype);
+int zo_perturbed_linear_prepare_group(int count, const int* m, int T, int n,
+                                      int r, int q, int nblk,
+                                      const int* blk_query,
+                                      const int8_t* blk_sign, float eps,
+                                      int in_dtype, const void* X,
+                                      long long x_block_stride,
+                                      const float* const* U,
+                                      const float* const* V,
+                                      const float* const* Z,
+                                      void* const* workspace,
+                                      const size_t* ws_bytes, void* group_ws,
+                                      size_t group_ws_bytes, void* stream);
 
 /* apply with a fused epilogue on the fp32 result, before its one rounding to
  * out_dtype -- the operations that follow a linear inside the decoder layer

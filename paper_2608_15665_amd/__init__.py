@@ -5,7 +5,8 @@ of include/zo.h); this package only binds it.  Entry points:
 
     subspace_refresh       Haar factors of Gaussian panels (Eq. 11, Alg. 1)
     perturbed_linear       X_b (W +- eps U Z_j V^T)^T for all query blocks (Eq. 4);
-                           PerturbedLinear.apply takes a fused ReLU or residual epilogue
+                           PerturbedLinear.apply takes a fused ReLU or residual epilogue;
+                           prepare_group prepares a layer's q, k, v in one pass over X
     lora_perturbed_linear  the same for a LoRA-adapted layer: both adapter factors
                            perturbed in their own subspaces
     layernorm, causal_attention, DecoderLayer
@@ -24,11 +25,11 @@ of include/zo.h); this package only binds it.  Entry points:
 from ._lib import (ZO_BF16, ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL, ZO_EPI_SILU_MUL, ZO_F16, ZO_F32, ZO_MAX_BLOCKS,
                    ZO_MAX_QR_RANK, ZO_MAX_RANK, ABI_SYMBOLS, LIB_PATH, DecoderLayer, LlamaLayer,
                    LlamaLoraLayer, LoraPerturbedLinear, PerturbedLinear, Workspace, ZoError, abi_version, causal_attention, combine_central,
-                   combine_forward, layernorm, lib, lora_perturbed_linear, perturbed_linear, rmsnorm, rope,
+                   combine_forward, layernorm, lib, lora_perturbed_linear, perturbed_linear, prepare_group, rmsnorm, rope,
                    sq_loss, subspace_adam_update, subspace_refresh, subspace_sgd_update)
 
 __all__ = ["ZO_BF16", "ZO_EPI_NONE", "ZO_EPI_RELU", "ZO_EPI_RESIDUAL", "ZO_EPI_SILU_MUL", "ZO_F16", "ZO_F32", "ZO_MAX_BLOCKS",
            "ZO_MAX_QR_RANK", "ZO_MAX_RANK", "ABI_SYMBOLS", "LIB_PATH", "DecoderLayer", "LlamaLayer", "LlamaLoraLayer", "LoraPerturbedLinear",
            "PerturbedLinear", "Workspace", "ZoError", "abi_version", "causal_attention", "combine_central",
-           "combine_forward", "layernorm", "lib", "lora_perturbed_linear", "perturbed_linear", "rmsnorm", "rope", "sq_loss",
+           "combine_forward", "layernorm", "lib", "lora_perturbed_linear", "perturbed_linear", "prepare_group", "rmsnorm", "rope", "sq_loss",
            "subspace_adam_update", "subspace_refresh", "subspace_sgd_update"]

@@ -39,6 +39,7 @@ ABI_SYMBOLS = (
     "zo_decoder_layer_workspace", "zo_decoder_layer_forward",
     "zo_rmsnorm", "zo_rope", "zo_llama_layer_workspace", "zo_llama_layer_forward",
     "zo_causal_attention_gqa", "zo_llama_lora_layer_workspace", "zo_llama_lora_layer_forward",
+    "zo_perturbed_linear_group_workspace", "zo_perturbed_linear_prepare_group",
 )
 ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL, ZO_EPI_SILU_MUL = 0, 1, 2, 3
 
@@ -183,6 +184,12 @@ def lib() -> ctypes.CDLL:
                                                                 ctypes.POINTER(ctypes.c_int8), c_f, c_f, c_f, c_int,
                                                                 c_vp, c_ll, ctypes.POINTER(LlamaLayerDesc),
                                                                 c_vp, c_vp, c_sz, c_vp])
+            L.zo_perturbed_linear_group_workspace.restype = c_sz
+            L.zo_perturbed_linear_group_workspace.argtypes = [c_int] * 6 + [c_ll, c_int]
+            L.zo_perturbed_linear_prepare_group.restype = c_int
+            L.zo_perturbed_linear_prepare_group.argtypes = [c_int, ctypes.POINTER(c_int)] + [c_int] * 5 + [
+                ctypes.POINTER(c_int), ctypes.POINTER(ctypes.c_int8), c_f, c_int, c_vp, c_ll] + [
+                ctypes.POINTER(c_vp)] * 4 + [ctypes.POINTER(c_sz), c_vp, c_sz, c_vp]
             L.zo_causal_attention_gqa.restype = c_int
             L.zo_causal_attention_gqa.argtypes = [c_int] * 7 + [c_vp] * 5
             L.zo_llama_lora_layer_workspace.restype = c_sz
@@ -359,6 +366,33 @@ class PerturbedLinear:
                                          self.odt, self.Y.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
                                          _stream_handle()))
         return self.Y
+
+
+def prepare_group(plins: Sequence["PerturbedLinear"], group_ws: Optional[torch.Tensor] = None):
+    """zo_perturbed_linear_prepare_group for PerturbedLinear objects that read the same X (a
+    layer's q, k, v): one projection pass for all of them, each keeping its own workspace."""
+    p0 = plins[0]
+    T, n, r, q, nblk = p0.dims[0], p0.dims[2], p0.dims[3], p0.dims[4], p0.dims[5]
+    for p in plins:
+        if (p.dims[0], p.dims[2], p.dims[3], p.dims[4], p.dims[5]) != (T, n, r, q, nblk) or p.dt != p0.dt \
+                or p.X.data_ptr() != p0.X.data_ptr() or p.xs != p0.xs:
+            raise ValueError("prepare_group: the linears must share T, n, r, q, nblk, dtype and X")
+        if list(p.bq) != list(p0.bq) or list(p.bs) != list(p0.bs) or p.eps != p0.eps:
+            raise ValueError("prepare_group: the linears must share their blocks and eps")
+    cnt = len(plins)
+    need = lib().zo_perturbed_linear_group_workspace(cnt, T, n, r, q, nblk, p0.xs, p0.dt)
+    if need and group_ws is None:
+        group_ws = torch.empty(need, dtype=torch.uint8, device=p0.X.device)
+    if need and group_ws.numel() < need:
+        raise ValueError(f"group workspace holds {group_ws.numel()} bytes, {need} needed")
+    arr = lambda vals: (ctypes.c_void_p * cnt)(*vals)
+    _check(lib().zo_perturbed_linear_prepare_group(
+        cnt, (ctypes.c_int * cnt)(*[p.dims[1] for p in plins]), T, n, r, q, nblk, p0.bq, p0.bs, p0.eps, p0.dt,
+        p0.X.data_ptr(), p0.xs, arr([p.U.data_ptr() for p in plins]), arr([p.V.data_ptr() for p in plins]),
+        arr([p.Z.data_ptr() for p in plins]), arr([p.ws.data_ptr() for p in plins]),
+        (ctypes.c_size_t * cnt)(*[p.ws.numel() for p in plins]), group_ws.data_ptr() if need else None,
+        group_ws.numel() if need else 0, _stream_handle()))
+    return group_ws
 
 
 def perturbed_linear(X: torch.Tensor, W: torch.Tensor, U: torch.Tensor, V: torch.Tensor, Z: torch.Tensor,

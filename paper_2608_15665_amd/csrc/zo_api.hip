@@ -196,6 +196,45 @@ int zo_perturbed_linear_prepare(int T, int m, int n, int r, int q, int nblk,
   return zo_plinear_prepare(p, blk_query, blk_sign, eps, X, U, V, Z, workspace, (hipStream_t)stream);
 }
 
+size_t zo_perturbed_linear_group_workspace(int count, int T, int n, int r, int q, int nblk,
+                                           long long x_block_stride, int in_dtype) {
+  if (count < 1 || count > ZO_MAX_GROUP) return 0;
+  if (check_plinear(T, 8, n, r, q, nblk, x_block_stride, in_dtype) != ZO_OK) return 0;
+  PlinearPlan p;
+  zo_plinear_plan(&p, T, 8, n, r, q, nblk, x_block_stride, in_dtype, in_dtype);
+  return zo_plinear_group_ws(p, count);
+}
+
+int zo_perturbed_linear_prepare_group(int count, const int* m, int T, int n, int r, int q, int nblk,
+                                      const int* blk_query, const int8_t* blk_sign, float eps, int in_dtype,
+                                      const void* X, long long x_block_stride, const float* const* U,
+                                      const float* const* V, const float* const* Z, void* const* workspace,
+                                      const size_t* ws_bytes, void* group_ws, size_t group_ws_bytes,
+                                      void* stream) {
+  ZO_CHECK(count >= 1 && count <= ZO_MAX_GROUP, "prepare_group: count = %d outside [1, %d]", count,
+           ZO_MAX_GROUP);
+  ZO_CHECK(m && U && V && Z && workspace && ws_bytes, "prepare_group: NULL descriptor array");
+  PlinearPlan plans[ZO_MAX_GROUP];
+  int st;
+  for (int i = 0; i < count; ++i) {
+    if ((st = check_plinear(T, m[i], n, r, q, nblk, x_block_stride, in_dtype)) != ZO_OK) return st;
+    if ((st = check_blocks(q, nblk, blk_query, blk_sign, eps, U[i], V[i], Z[i])) != ZO_OK) return st;
+    if ((st = check_plinear_call(T, m[i], n, r, q, nblk, x_block_stride, in_dtype, in_dtype, X, nullptr, nullptr,
+                                 workspace[i], ws_bytes[i], &plans[i])) != ZO_OK)
+      return st;
+  }
+  const size_t need = zo_plinear_group_ws(plans[0], count);
+  if (need > 0) {
+    if (!group_ws || group_ws_bytes < need) {
+      zo_set_error("prepare_group: group workspace %zu bytes < required %zu", group_ws_bytes, need);
+      return ZO_ERR_WORKSPACE;
+    }
+    ZO_CHECK(aligned(group_ws, 256), "prepare_group: group workspace not 256-byte aligned");
+  }
+  return zo_plinear_prepare_group(plans, count, blk_query, blk_sign, eps, X, U, V, Z, workspace, group_ws,
+                                  (hipStream_t)stream);
+}
+
 int zo_perturbed_linear_apply_ex(int T, int m, int n, int r, int q, int nblk, int in_dtype,
                                  const void* X, long long x_block_stride, const void* W,
                                  int out_dtype, void* Y, int epilogue, const void* R,

@@ -312,6 +312,31 @@ def test_lora_layer_and_grouped_attention_validation():
     assert st == 1 and "h_block_stride" in _detail()
 
 
+def test_prepare_group_validation():
+    """The grouped prepare rejects bad counts, NULL descriptors and a short group workspace."""
+    L = zo.lib()
+    fake = 1 << 20
+    assert L.zo_perturbed_linear_group_workspace(3, 64, 256, 8, 2, 4, 64 * 256, 1) > 0
+    assert L.zo_perturbed_linear_group_workspace(3, 64, 256, 8, 2, 4, 64 * 256, 0) == 0   # fp32: separate
+    assert L.zo_perturbed_linear_group_workspace(1, 64, 256, 8, 2, 4, 64 * 256, 1) == 0   # one matrix
+    assert L.zo_perturbed_linear_group_workspace(9, 64, 256, 8, 2, 4, 64 * 256, 1) == 0
+    bq = (ctypes.c_int * 2)(0, 0)
+    bs = (ctypes.c_int8 * 2)(1, -1)
+    m = (ctypes.c_int * 2)(64, 64)
+    ptrs = (ctypes.c_void_p * 2)(fake, fake)
+    need = L.zo_perturbed_linear_workspace(16, 64, 64, 4, 1, 2, 0, 1)
+    sizes = (ctypes.c_size_t * 2)(need, need)
+    st = L.zo_perturbed_linear_prepare_group(0, m, 16, 64, 4, 1, 2, bq, bs, 1e-3, 1, fake, 0, ptrs, ptrs, ptrs,
+                                             ptrs, sizes, fake, 1 << 30, None)
+    assert st == 1 and "count" in _detail()
+    st = L.zo_perturbed_linear_prepare_group(2, m, 16, 64, 4, 1, 2, bq, bs, 1e-3, 1, fake, 0, None, ptrs, ptrs,
+                                             ptrs, sizes, fake, 1 << 30, None)
+    assert st == 1 and "NULL" in _detail()
+    st = L.zo_perturbed_linear_prepare_group(2, m, 16, 64, 4, 1, 2, bq, bs, 1e-3, 1, fake, 0, ptrs, ptrs, ptrs,
+                                             ptrs, sizes, fake, 16, None)
+    assert st == 6 and "group workspace" in _detail()
+
+
 def test_empty_calls_are_no_ops():
     """count = 0 refreshes and updates, and zero-row layer norms, succeed without launching."""
     L = zo.lib()

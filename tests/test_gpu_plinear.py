@@ -16,7 +16,7 @@ import torch
 import oracle
 import paper_2608_15665_amd as zo
 import zo_draws as zd
-from _common import dev_bf16, dev_f16, dev_f32, ferr, host, normwise, orth
+from _common import cast, dev_bf16, dev_f16, dev_f32, ferr, host, normwise, orth
 
 pytestmark = pytest.mark.gpu
 
@@ -282,3 +282,32 @@ def test_forward_difference_layout_at_paper_k():
         assert ferr(Y[b], ref[b], 1.0) <= 1e-4, b
     # the baseline block is the plain product X W^T
     np.testing.assert_allclose(Y[0], c["X0v"] @ c["Wv"].T, rtol=0, atol=1e-4 * np.abs(Y[0]).max())
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
+@pytest.mark.parametrize("shared", [False, True])
+def test_prepare_group_equals_separate(dt, shared):
+    """zo_perturbed_linear_prepare_group (one projection pass for matrices that read the same X,
+    of different heights) then each apply: bitwise the separate prepares and applies."""
+    T, n, r, q, nblk = 200, 264, 20, 2, 4
+    ms = [256, 128, 72]
+    xs = 0 if shared else T * n
+    Xd, _ = cast(zd.draw(31, "X", (T, n), ((1 if shared else nblk) * T, n)), dt)
+    bq, bs = [b // 2 for b in range(nblk)], [1, -1] * (nblk // 2)
+    plins, refs = [], []
+    for i, m in enumerate(ms):
+        Wd, _ = cast(zd.draw(31, "W0", (i, m, n), (m, n), 0.05), dt)
+        U, V = orth(31, (i, 1, m), m, r), orth(31, (i, 2, n), n, r)
+        Z = zd.z_draws(31, 0, i, q, r)
+        args = (Xd, Wd, dev_f32(U), dev_f32(V), dev_f32(Z), bq, bs, 1e-2, T)
+        ws = torch.empty(zo.lib().zo_perturbed_linear_workspace(T, m, n, r, q, nblk, xs, zo._lib._DT[Xd.dtype]),
+                         dtype=torch.uint8, device="cuda")
+        plins.append(zo.PerturbedLinear(*args, x_block_stride=xs, workspace=ws))
+        ref = zo.PerturbedLinear(*args, x_block_stride=xs)
+        ref.prepare()
+        refs.append(ref.apply().clone())
+    zo.prepare_group(plins)
+    for p, ref in zip(plins, refs):
+        Y = p.apply()
+        torch.cuda.synchronize()
+        assert torch.equal(Y.view(torch.uint8), ref.view(torch.uint8))
