@@ -15,8 +15,8 @@
 // by each pass from L1/L2 (k_layernorm).  Both do the same operations in the
 // same order, so their results are identical.
 //
-// k_attention<F16, DH>: one workgroup (4 waves) per (block, sequence, head,
-// tile of 64 AT_NG queries); keys in tiles of 64 through LDS (loaded into
+// k_attention<F16, DH, W>: one workgroup (W = 4 or 8 waves) per (block, sequence,
+// head, tile of 32 W queries); keys in tiles of 64 through LDS (loaded into
 // registers a tile ahead, both K and V stored row-major), online softmax in
 // fp32.  Each wave owns AT_NG = 2 groups of 16 queries that share every K and
 // V fragment it reads from LDS (two groups measured 9-18 % faster than one once
@@ -255,7 +255,9 @@ __global__ __launch_bounds__(256) void k_rope(void* X, long long rows, int seq_l
 
 // ---------------------------------------------------------------- attention
 constexpr int AT_NG = 2;               // 16-query groups per wave
-constexpr int AT_Q = 64 * AT_NG;       // queries per workgroup (4 waves)
+// Waves per workgroup: 4, or 8 for sequences of 512 or more (the K/V tile a workgroup loads
+// then serves 256 queries; at 256 keys per sequence the causal tiles 8 waves would walk in
+// step cost more than that saves).
 constexpr int AT_K = 64;               // keys per tile
 
 struct AttnArgs {
@@ -263,7 +265,7 @@ struct AttnArgs {
   const void* K;
   const void* V;
   void* O;
-  int T, seq_len, d, heads, qtiles;  // qtiles = ceil(seq_len / AT_Q)
+  int T, seq_len, d, heads, qtiles;  // qtiles = ceil(seq_len / queries per workgroup)
   int dkv, group;                    // K/V row length (kv_heads dh); query heads per K/V head
   float scale_log2;                  // log2(e) / sqrt(dh)
 };
@@ -309,16 +311,18 @@ __device__ __forceinline__ u32x2 ds_read_tr(const uint16_t* p) {
   return __builtin_bit_cast(u32x2, v);
 }
 
-template <bool F16, int DH>
-__global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
+template <bool F16, int DH, int W>
+__global__ __launch_bounds__(64 * W) void k_attention(AttnArgs a) {
+  constexpr int NT = 64 * W;              // threads
+  constexpr int AT_Q = 16 * AT_NG * W;    // queries per workgroup
   constexpr int KS = DH / 32;         // 32-deep k steps of Q K^T
   constexpr int DT = DH / 16;         // 16-dim tiles of the output
   constexpr int KROW = DH + 8;        // LDS row of the K tile (elements), padded
   constexpr int VROW = DH + 16;       // LDS row of the V tile (elements): 16 rows of a
                                       // transposed read fall on distinct banks
   constexpr int C8 = DH / 8;          // 16-byte chunks per head row
-  constexpr int KCH = AT_K * C8 / 256;    // K (and V) chunks per thread per tile
-  static_assert(KCH * 256 == AT_K * C8, "tile / thread mismatch");
+  constexpr int KCH = AT_K * C8 / NT;    // K (and V) chunks per thread per tile
+  static_assert(KCH * NT == AT_K * C8, "tile / thread mismatch");
   __shared__ __attribute__((aligned(16))) uint16_t Ks[AT_K * KROW];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[AT_K * VROW];
 
@@ -364,14 +368,14 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
     lsum[gq] = 0.f;     // this lane's part of the running sum
   }
 
-  // K and V tiles are loaded into registers a tile ahead: chunk x = tid + 256 c is key x / C8,
+  // K and V tiles are loaded into registers a tile ahead: chunk x = tid + NT c is key x / C8,
   // dims 8 (x % C8); both are stored row-major (V is read transposed by ds_read_tr).  Rows
   // past the sequence are clamped to its last row (their keys are masked).
   u32x4 kreg[KCH], vreg[KCH];
   auto load_tile = [&](int k0) {
 #pragma unroll
     for (int c = 0; c < KCH; ++c) {
-      const int x = tid + 256 * c;
+      const int x = tid + NT * c;
       const size_t off = (size_t)(row0 + min(k0 + x / C8, a.seq_len - 1)) * a.dkv + col0kv + 8 * (x % C8);
       kreg[c] = *(const u32x4*)(Kg + off);
       vreg[c] = *(const u32x4*)(Vg + off);
@@ -380,7 +384,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a) {
   auto store_tile = [&]() {
 #pragma unroll
     for (int c = 0; c < KCH; ++c) {
-      const int x = tid + 256 * c;
+      const int x = tid + NT * c;
       *(u32x4*)&Ks[(x / C8) * KROW + 8 * (x % C8)] = kreg[c];
       *(u32x4*)&Vs[(x / C8) * VROW + 8 * (x % C8)] = vreg[c];
     }
@@ -568,7 +572,9 @@ int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int kv_h
   a.heads = heads;
   a.dkv = d / heads * kv_heads;
   a.group = heads / kv_heads;
-  a.qtiles = (seq_len + AT_Q - 1) / AT_Q;
+  const int W = seq_len >= 512 ? 8 : 4;
+  const int qpw = 16 * AT_NG * W;
+  a.qtiles = (seq_len + qpw - 1) / qpw;
   const int dh = d / heads;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
   const long long wg = (long long)nblk * (T / seq_len) * heads * a.qtiles;
@@ -577,18 +583,22 @@ int zo_attention_launch(int nblk, int T, int seq_len, int d, int heads, int kv_h
     zo_set_error("attention: too many workgroups (%lld)", wg);
     return ZO_ERR_UNSUPPORTED;
   }
-  const dim3 grid((unsigned)wg), block(256);
+  const dim3 grid((unsigned)wg), block(64 * W);
   const bool f16 = dtype == ZO_F16;
-  if (dh == 64) {
-    if (f16)
-      hipLaunchKernelGGL((k_attention<true, 64>), grid, block, 0, stream, a);
-    else
-      hipLaunchKernelGGL((k_attention<false, 64>), grid, block, 0, stream, a);
+#define ZO_ATTN(F, D, WW) hipLaunchKernelGGL((k_attention<F, D, WW>), grid, block, 0, stream, a)
+  if (W == 8) {
+    if (dh == 64) {
+      if (f16) ZO_ATTN(true, 64, 8); else ZO_ATTN(false, 64, 8);
+    } else {
+      if (f16) ZO_ATTN(true, 128, 8); else ZO_ATTN(false, 128, 8);
+    }
   } else {
-    if (f16)
-      hipLaunchKernelGGL((k_attention<true, 128>), grid, block, 0, stream, a);
-    else
-      hipLaunchKernelGGL((k_attention<false, 128>), grid, block, 0, stream, a);
+    if (dh == 64) {
+      if (f16) ZO_ATTN(true, 64, 4); else ZO_ATTN(false, 64, 4);
+    } else {
+      if (f16) ZO_ATTN(true, 128, 4); else ZO_ATTN(false, 128, 4);
+    }
   }
+#undef ZO_ATTN
   return zo_hip_status(hipGetLastError(), "k_attention");
 }
