@@ -112,6 +112,26 @@ size_t zo_subspace_refresh_workspace(int count, const zo_panel* panels, int r);
 int zo_subspace_refresh(int count, const zo_panel* panels, int r, int* info,
                         void* workspace, size_t ws_bytes, void* stream);
 
+/* zo_subspace_refresh without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, arithmetic, results
+ * (bitwise) and errors as zo_subspace_refresh; its scratch is a static device
+ * array of ZO_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds
+ * until the process ends (its address is looked up on the first call on each
+ * device, with that device current).  The call allocates nothing.
+ *   - A call whose zo_subspace_refresh_workspace size exceeds
+ *     ZO_NOALLOC_SCRATCH_BYTES returns ZO_ERR_WORKSPACE and launches nothing;
+ *     split its panels over several calls.  (Each panel of r <= 64 needs about
+ *     (ceil(rows / 1024) + 3) * 32 KiB; of 64 < r <= 128 about
+ *     ceil(rows / 1024) * 66 KiB + 384 KiB.)
+ *   - Every call on one GPU uses the same scratch: calls that overlap on one
+ *     GPU (on different streams, or from different threads without ordering)
+ *     race and give wrong results.  Calls enqueued on one stream are ordered
+ *     and safe.  Nothing the scratch holds from an earlier call is read. */
+#define ZO_NOALLOC_SCRATCH_BYTES (64u << 20)
+int zo_subspace_refresh_noalloc(int count, const zo_panel* panels, int r,
+                                int* info, void* stream);
+
 /* ------------------------------------------------------------------------
  * Perturbed linear -- Eq. 4 inside the forward of Eq. 5 (Alg. 2 + Alg. 3).
  *

@@ -40,7 +40,9 @@ ABI_SYMBOLS = (
     "zo_rmsnorm", "zo_rope", "zo_llama_layer_workspace", "zo_llama_layer_forward",
     "zo_causal_attention_gqa", "zo_llama_lora_layer_workspace", "zo_llama_lora_layer_forward",
     "zo_perturbed_linear_group_workspace", "zo_perturbed_linear_prepare_group",
+    "zo_subspace_refresh_noalloc",
 )
+ZO_NOALLOC_SCRATCH_BYTES = 64 << 20
 ZO_EPI_NONE, ZO_EPI_RELU, ZO_EPI_RESIDUAL, ZO_EPI_SILU_MUL = 0, 1, 2, 3
 
 
@@ -116,6 +118,8 @@ def lib() -> ctypes.CDLL:
             L.zo_subspace_refresh_workspace.argtypes = [c_int, ctypes.POINTER(Panel), c_int]
             L.zo_subspace_refresh.restype = c_int
             L.zo_subspace_refresh.argtypes = [c_int, ctypes.POINTER(Panel), c_int, c_vp, c_vp, c_sz, c_vp]
+            L.zo_subspace_refresh_noalloc.restype = c_int
+            L.zo_subspace_refresh_noalloc.argtypes = [c_int, ctypes.POINTER(Panel), c_int, c_vp, c_vp]
             L.zo_perturbed_linear_workspace.restype = c_sz
             L.zo_perturbed_linear_workspace.argtypes = [c_int] * 6 + [c_ll, c_int]
             L.zo_perturbed_linear.restype = c_int
@@ -286,6 +290,28 @@ def subspace_refresh(omegas: Sequence[torch.Tensor], r: int, out: Optional[Seque
         _check(L.zo_subspace_refresh(n, arr, r, None, None, 0, None))  # raises with the reason
     ws = Workspace.get(ws_n)
     _check(L.zo_subspace_refresh(n, arr, r, _ptr(info), ws.data_ptr(), ws.numel(), _stream_handle()))
+    return out
+
+
+def subspace_refresh_noalloc(omegas: Sequence[torch.Tensor], r: int, out: Sequence[torch.Tensor],
+                             r_diag: Optional[Sequence[torch.Tensor]] = None,
+                             info: Optional[torch.Tensor] = None):
+    """subspace_refresh through zo_subspace_refresh_noalloc: the library's static per-GPU scratch
+    instead of a workspace, so nothing is allocated here either (out is required)."""
+    n = len(omegas)
+    arr = (Panel * max(n, 1))()
+    for p, om in enumerate(omegas):
+        _need(om, f"omega[{p}]", torch.float32)
+        if om.dim() != 2 or om.shape[1] != r:
+            raise ValueError(f"omega[{p}] must be rows x {r}")
+        _need(out[p], f"out[{p}]", torch.float32, om.numel())
+        rd = None
+        if r_diag is not None:
+            rd = _need(r_diag[p], f"r_diag[{p}]", torch.float32, r)
+        arr[p] = Panel(int(om.shape[0]), om.data_ptr(), out[p].data_ptr(), _ptr(rd))
+    if info is not None:
+        _need(info, "info", torch.int32, n)
+    _check(lib().zo_subspace_refresh_noalloc(n, arr, r, _ptr(info), _stream_handle()))
     return out
 
 

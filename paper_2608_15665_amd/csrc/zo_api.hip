@@ -93,6 +93,24 @@ int zo_subspace_refresh(int count, const zo_panel* panels, int r, int* info, voi
                            nullptr);
 }
 
+int zo_subspace_refresh_noalloc(int count, const zo_panel* panels, int r, int* info, void* stream) {
+  int st = check_refresh(count, panels, r);
+  if (st != ZO_OK) return st;
+  if (count == 0) return ZO_OK;
+  size_t need = 0;
+  zo_refresh_launch(count, panels, r, nullptr, nullptr, 0, nullptr, &need);
+  if (need > (size_t)ZO_NOALLOC_SCRATCH_BYTES) {
+    zo_set_error("refresh_noalloc: these %d panels need %zu bytes of scratch, more than the %zu-byte "
+                 "static scratch; refresh them over several calls", count, need,
+                 (size_t)ZO_NOALLOC_SCRATCH_BYTES);
+    return ZO_ERR_WORKSPACE;
+  }
+  void* scratch = nullptr;
+  if ((st = zo_refresh_scratch(&scratch)) != ZO_OK) return st;
+  return zo_refresh_launch(count, panels, r, info, scratch, (size_t)ZO_NOALLOC_SCRATCH_BYTES,
+                           (hipStream_t)stream, nullptr);
+}
+
 // --------------------------------------------------------- perturbed linear
 static int check_plinear(int T, int m, int n, int r, int q, int nblk, long long xs, int in_dtype) {
   ZO_CHECK(T >= 1 && m >= 1 && n >= 1, "perturbed_linear: T, m, n must be >= 1 (got %d, %d, %d)",

@@ -163,6 +163,9 @@ int zo_update_launch(int count, const zo_update_item* items, int w_dtype, int r,
 // Subspace refresh, CholeskyQR2 (zo_qr.hip).
 int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void* ws,
                       size_t ws_bytes, hipStream_t stream, size_t* ws_needed);
+// Device address of the current device's static refresh scratch (ZO_NOALLOC_SCRATCH_BYTES),
+// looked up on the first call per device and cached.
+int zo_refresh_scratch(void** ptr);
 
 // Loss helpers (zo_loss.hip).
 int zo_sq_loss_launch(int nblk, int T, int m, int dtype, const void* Y, const void* Ystar,

@@ -26,6 +26,7 @@
 // column is zero, and the other columns are formed as if it were absent.
 #include "zo_internal.h"
 
+#include <mutex>
 #include <vector>
 
 namespace {
@@ -582,5 +583,44 @@ int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void*
     }
     if (st != ZO_OK) return st;
   }
+  return ZO_OK;
+}
+
+// ---------------------------------------------------------------- no-allocation variant
+// The scratch of zo_subspace_refresh_noalloc: a static device array, one copy per GPU the
+// library runs on, held until the process ends.  The row passes write every partial Gram
+// entry the Cholesky launch reads, and the Cholesky launch writes all of R1, X1 and M, so
+// nothing in it has to start at zero and what an earlier call left there is never read.
+// In host code the array's name is a stand-in, not a device address: the device address is
+// looked up once per device (hipGetSymbolAddress, with that device current) and only that
+// pointer is handed to kernels.
+static __device__ __align__(256) char scratch[ZO_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES];
+}  // namespace
+
+int zo_refresh_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return zo_hip_status(e, "refresh_noalloc: hipGetDevice");
+  if (dev < 0 || dev >= MAX_DEVICES) {
+    zo_set_error("refresh_noalloc: device %d outside [0, %d)", dev, MAX_DEVICES);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return zo_hip_status(e, "refresh_noalloc: hipGetSymbolAddress");
+    if (!p || (uintptr_t)p % 256 != 0) {
+      zo_set_error("refresh_noalloc: scratch address %p unusable", p);
+      return ZO_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
   return ZO_OK;
 }

@@ -348,3 +348,20 @@ def test_empty_calls_are_no_ops():
     assert L.zo_layernorm(0, 64, 1, None, None, None, 1e-5, None, None) == 0
     assert L.zo_rmsnorm(0, 64, 1, None, None, 1e-6, None, None) == 0
     assert L.zo_rope(0, 64, 256, 2, 1, None, 1e4, None) == 0
+
+
+def test_refresh_noalloc_validation():
+    """The no-allocation refresh validates like zo_subspace_refresh and rejects, before touching
+    any device, a call whose scratch need exceeds the static scratch."""
+    L = zo.lib()
+    fake = 1 << 20
+    arr = (Panel * 2)(Panel(10, fake, fake, None), Panel(3, fake, fake, None))
+    assert L.zo_subspace_refresh_noalloc(2, arr, 4, None, None) == 1
+    assert "rows = 3 < r = 4" in _detail()
+    assert L.zo_subspace_refresh_noalloc(1, arr, 129, None, None) == 1
+    assert L.zo_subspace_refresh_noalloc(0, None, 4, None, None) == 0
+    big = (Panel * 1)(Panel(1 << 26, fake, fake, None))
+    need = L.zo_subspace_refresh_workspace(1, big, 64)
+    assert need > zo.ZO_NOALLOC_SCRATCH_BYTES
+    assert L.zo_subspace_refresh_noalloc(1, big, 64, None, None) == 6
+    assert "static scratch" in _detail() and str(need) in _detail()
