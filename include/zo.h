@@ -57,6 +57,10 @@ extern "C" {
 #define ZO_MAX_QUERIES 256
 #define ZO_MAX_GROUP 8    /* count limit of zo_perturbed_linear_prepare_group   */
 
+/* ZO_ERR_RANK_DEFICIENT and ZO_ERR_NONFINITE are reserved: no call returns
+ * them.  Both conditions arise on the device after the call has returned
+ * (every call is asynchronous), so they are reported through device memory
+ * instead: the refresh's info array and the update's nonfinite_flag. */
 typedef enum {
   ZO_OK = 0,
   ZO_ERR_INVALID_ARG = 1,
@@ -86,16 +90,23 @@ const char* zo_last_error_detail(void);
  * Haar distributed.  Computed in float64 by CholeskyQR2 (R1 = chol(O^T O),
  * Q1 = O R1^-1, R2 = chol(Q1^T Q1), Q = Q1 R2^-1), whose Cholesky factors
  * have a positive diagonal, so the sign correction is built in; outputs
- * rounded once to float32.  Accurate to working precision while
- * cond(Omega)^2 * 1e-16 << 1, which Gaussian panels with rows >= r meet
- * with overwhelming probability.  Bitwise reproducible.
+ * rounded once to float32.  Bitwise reproducible.  Accuracy: Q within 1e-5
+ * of the exact factor (tested against a float64 Householder QR) on panels
+ * whose columns are not nearly dependent -- column scaling does not matter
+ * (tested to condition 1e9); nearly collinear columns are tested to
+ * condition 2e7 - 4e7.  From condition ~1e8 of that kind the Cholesky pivots
+ * fall to the rounding noise of the Gram matrix: a pivot that comes out not
+ * positive is reported through info, one that comes out positive is not and
+ * the result is then inaccurate.  Gaussian panels with rows >= 2 r (every
+ * configuration here) reach such a condition with probability below 1e-30.
  *
  *   omega   device, rows x r fp32, row-major; read only.
  *   q       device, rows x r fp32 output; may alias omega.
  *   r_diag  device, r fp32 output (diag of the corrected R, > 0); nullable.
  *   info    device, `count` ints, nullable: info[p] = 0, or k+1 when the
  *           first Cholesky pivot that is not positive is at column k
- *           (Omega_p rank deficient; an exactly zero column gives this).
+ *           (Omega_p rank deficient, or numerically so; an exactly zero
+ *           column gives this).
  *           R_kk is then reported as 0, the Q column is zero and the other
  *           columns are formed as if column k were absent.
  * Limits: 1 <= r <= ZO_MAX_QR_RANK, rows <= 2^26.  Panels of one call share
@@ -204,7 +215,8 @@ int zo_perturbed_linear_apply(int T, int m, int n, int r, int q, int nblk,
  * T, n, r, q, nblk, the blocks, eps, in_dtype, X and x_block_stride are
  * shared.  group_ws: device scratch of zo_perturbed_linear_group_workspace
  * bytes (0 for fp32 inputs or count = 1, when the call runs the separate
- * prepares; group_ws may then be NULL).  The prepared operands are bitwise
+ * prepares; group_ws may then be NULL).  The count workspaces and group_ws
+ * must be pairwise disjoint (ZO_ERR_INVALID_ARG otherwise).  The prepared operands are bitwise
  * those of separate prepares; each matrix is then applied with
  * zo_perturbed_linear_apply(_ex) and its own workspace.
  * Limits: 1 <= count <= ZO_MAX_GROUP; those of zo_perturbed_linear. */

@@ -462,7 +462,7 @@ def round_f16(x):
 # ---------------------------------------------------------------------------
 # Tiny configuration end to end (Alg. 3 with the central estimate)
 # ---------------------------------------------------------------------------
-def tiny_run(inputs, omega_fn, z_fn, cfg, g_override=None, f32_state=False, estimator="central"):
+def tiny_run(inputs, omega_fn, z_fn, cfg, g_override=None, estimator="central"):
     """Alg. 3 on the one-layer Tiny problem, float64.
 
     inputs: dict(W, X, Ystar) arrays.  omega_fn(t) -> (Omega_U, Omega_V) for a

@@ -249,6 +249,20 @@ int zo_perturbed_linear_prepare_group(int count, const int* m, int T, int n, int
     }
     ZO_CHECK(aligned(group_ws, 256), "prepare_group: group workspace not 256-byte aligned");
   }
+  // Each matrix keeps its prepared operands in its own workspace until its apply, and the group
+  // scratch is read after every matrix's part has been written: no two of the regions the call
+  // writes may overlap (a shared buffer would hand every apply the last matrix's operands).
+  auto overlap = [](const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return na > 0 && nb > 0 && x < y + nb && y < x + na;
+  };
+  for (int i = 0; i < count; ++i) {
+    for (int j = i + 1; j < count; ++j)
+      ZO_CHECK(!overlap(workspace[i], plans[i].ws_total, workspace[j], plans[j].ws_total),
+               "prepare_group: workspaces of matrices %d and %d overlap; each matrix needs its own", i, j);
+    ZO_CHECK(!overlap(workspace[i], plans[i].ws_total, group_ws, need),
+             "prepare_group: the group workspace overlaps matrix %d's workspace", i);
+  }
   return zo_plinear_prepare_group(plans, count, blk_query, blk_sign, eps, X, U, V, Z, workspace, group_ws,
                                   (hipStream_t)stream);
 }

@@ -5,7 +5,8 @@
 // Launches per call (bf16 inputs):
 //   1. k_transpose_v : V (n x r fp32) -> Vt2 (2 rp x n bf16): rows [0, rp) the
 //                      high bf16 part of V^T, rows [rp, 2 rp) the low part
-//                      (V = hi + lo to ~16 bits); rp = r rounded up to 16.
+//                      (V = hi + lo to ~16 bits); rp = r rounded up to 32
+//                      (16 for fp32 inputs).
 //   2. P2 = X_x Vt2^T: the n -> rp projection of every distinct X block, as
 //                      two fp32 halves (one GEMM launch, narrow A operand).
 //   3. k_pcombine    : P = P2_hi + P2_lo, written as the K segment

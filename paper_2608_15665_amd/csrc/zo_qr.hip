@@ -7,10 +7,12 @@
 // Nakatsukasa, Yanagisawa, Yamamoto, 2014): R1 = chol(Omega^T Omega),
 // Q1 = Omega R1^-1, R2 = chol(Q1^T Q1), Q = Q1 R2^-1, R = R2 R1.  A Cholesky
 // factor has a positive diagonal, so the sign correction is built in.  The
-// second pass restores orthogonality to working precision whenever
-// cond(Omega)^2 u << 1, which Gaussian panels with rows >= r satisfy with
-// overwhelming probability (their condition number is about
-// (sqrt(rows) + sqrt(r)) / (sqrt(rows) - sqrt(r))).
+// second pass restores orthogonality to working precision.  What limits the
+// method is a pivot of the first factorisation sinking into the rounding noise
+// of the Gram matrix, which takes a column within ~1e-8 of the span of the
+// earlier ones (column scaling alone does not: the relative pivots are scale
+// free).  Gaussian panels, whose condition number is about
+// (sqrt(rows) + sqrt(r)) / (sqrt(rows) - sqrt(r)), essentially never get there.
 //
 // Five launches per batch of panels, all float64 with fixed-order sums (the
 // result is bitwise reproducible):

@@ -101,3 +101,44 @@ def check_attention(got, Q, K, V, heads, seq_len, dt, what, kv_heads=None):
     bound = ulp16(ref, dt) + 2.0 ** -14 * mag
     err = np.abs(np.asarray(got, np.float64) - ref)
     assert np.all(err <= bound), (what, float(np.max(err / bound)))
+
+
+def spacing32(y):
+    """Spacing of float32 values at |y| (one ulp)."""
+    return np.spacing(np.abs(np.asarray(y, np.float64)).astype(np.float32)).astype(np.float64)
+
+
+def estimate_noise_bar(Yplus, Yminus, Ystar, eps, r, T, g, k=6.0, rel=1e-5):
+    """Per-query bar on |g_gpu - g_exact| / max(|g_exact|, rms(g_exact)) for estimates formed
+    from fp32 outputs of the fp32 perturbed linear.
+
+    Yplus[j] is the exact output of query j's + block (the oracle's).  Central estimate,
+    g_j = (L(Y+_j) - L(Y-_j)) / (2 eps): Yminus[j] is the exact output of its - block.
+    Forward estimate, g_j = (L(Y+_j) - L(Y_0)) / eps: Yminus is None (the baseline block
+    adds exact zeros as its rank-r term, so its output carries no rounding that the + block
+    does not share).  L = 0.5 sum (Y - Y*)^2 / T is accumulated in fp64, so its own error is
+    negligible; what moves g is the rounding of Y.  The two sides of a difference share
+    X W^T bit for bit (same X, same W, same summation order); the rank-r term is then added
+    by r fused multiply-adds, each rounding at the scale of |Y| with an error uniform in
+    +-ulp/2 (variance ulp^2 / 12), independently for the two sides.  The shared error of
+    X W^T enters only through Y+ - Y- = O(eps), and W, U, V differ from the oracle's
+    float64 ones by fp32 rounding: both are covered by the `rel` term.  So
+
+        var(T * delta(L+_j - L-_j)) = sum_i (Y+_ji - Y*_i)^2 r ulp(Y+_ji)^2 / 12
+                                      + the same for Y-_j (central only)
+
+    and the bar is k = 6 standard deviations plus rel |g_j|, over the floored |g_j|."""
+    Ystar = np.asarray(Ystar, np.float64)
+    g = np.asarray(g, np.float64)
+    floor = np.maximum(np.abs(g), np.sqrt(np.mean(g * g)))
+
+    def var(Y):
+        Y = np.asarray(Y, np.float64)
+        return np.sum((Y - Ystar) ** 2 * r * spacing32(Y) ** 2 / 12.0)
+
+    out = []
+    for j, Yp in enumerate(Yplus):
+        v = var(Yp) + (var(Yminus[j]) if Yminus is not None else 0.0)
+        sigma = np.sqrt(v) / (T * (2.0 * eps if Yminus is not None else eps))
+        out.append((k * sigma + rel * abs(g[j])) / floor[j])
+    return np.array(out)

@@ -335,6 +335,17 @@ def test_prepare_group_validation():
     st = L.zo_perturbed_linear_prepare_group(2, m, 16, 64, 4, 1, 2, bq, bs, 1e-3, 1, fake, 0, ptrs, ptrs, ptrs,
                                              ptrs, sizes, fake, 16, None)
     assert st == 6 and "group workspace" in _detail()
+    # Aliased workspaces (one shared buffer for both matrices) are rejected before any launch.
+    gneed = L.zo_perturbed_linear_group_workspace(2, 16, 64, 4, 1, 2, 0, 1)
+    ws = (ctypes.c_void_p * 2)(1 << 30, (1 << 30) + need // 2)
+    gws = 1 << 34
+    st = L.zo_perturbed_linear_prepare_group(2, m, 16, 64, 4, 1, 2, bq, bs, 1e-3, 1, fake, 0, ptrs, ptrs, ptrs,
+                                             ws, sizes, gws, gneed, None)
+    assert st == 1 and "overlap" in _detail()
+    ws = (ctypes.c_void_p * 2)(1 << 30, 1 << 31)
+    st = L.zo_perturbed_linear_prepare_group(2, m, 16, 64, 4, 1, 2, bq, bs, 1e-3, 1, fake, 0, ptrs, ptrs, ptrs,
+                                             ws, sizes, (1 << 31) + 256, gneed, None)
+    assert st == 1 and "group workspace overlaps" in _detail()
 
 
 def test_empty_calls_are_no_ops():

@@ -61,6 +61,7 @@ def attn_case(seed, nblk, T, d, dt):
     (1, 200, 100, 128, 2),    # dh = 64, sequences not a multiple of the 64-query tile
     (3, 64, 64, 512, 4),      # one tile per sequence
     (1, 1024, 512, 256, 2),   # the OPT-13B sequence length
+    (1, 1024, 512, 128, 2),   # dh = 64 at a sequence length that takes the 8-wave workgroups
 ])
 def test_attention_parity(dt, nblk, T, seq_len, d, heads):
     (Qd, Qv), (Kd, Kv), (Vd, Vv) = attn_case(9, nblk, T, d, dt)

@@ -28,6 +28,8 @@ pytestmark = pytest.mark.gpu
     (2, 256, 128, 512, 4, 1),    # dh = 128, one key/value head for four query heads
     (1, 200, 100, 256, 4, 2),    # dh = 64, ragged query tiles
     (2, 512, 256, 1280, 10, 2),  # the Qwen-32B ratio (5 query heads per key/value head)
+    (1, 1024, 512, 512, 4, 2),   # dh = 128, sequences of 512 (8-wave workgroups)
+    (1, 1024, 512, 256, 4, 2),   # dh = 64, sequences of 512 (8-wave workgroups)
 ])
 def test_grouped_attention_parity(dt, nblk, T, seq_len, d, heads, kv):
     dkv = d // heads * kv

@@ -211,17 +211,18 @@ FULL_SIZE = [(name, m, n) for name in ("opt-1.3b", "llama-7b", "opt-13b")
 
 
 FULL_SIZE_R128 = [("opt-13b", m, n, 128, "bf16") for m, n in _distinct_shapes(zd.CONFIGS["opt-13b"])]
+FULL_SIZE_R24 = [("opt-13b", m, n, 24, "bf16") for m, n in _distinct_shapes(zd.CONFIGS["opt-13b"])]
 FULL_SIZE_F16 = [("opt-13b", m, n, None, "f16") for m, n in _distinct_shapes(zd.CONFIGS["opt-13b"])]
 
 
 @pytest.mark.parametrize("name,m,n,rank,dt", [(*x, None, "bf16") for x in FULL_SIZE] + FULL_SIZE_R128
-                         + FULL_SIZE_F16)
+                         + FULL_SIZE_R24 + FULL_SIZE_F16)
 def test_full_size_sampled(name, m, n, rank, dt):
     """Every distinct matrix shape of the OPT-1.3B, LLaMA-7B and OPT-13B stacks at full size
     (T tokens per block, 2q blocks, the config's r; the OPT-13B shapes also at the paper's
-    full-tuning rank r = 128 and in fp16, the paper's precision) in the launch configuration
-    the benchmark times; sampled token rows of several blocks checked against the oracle row
-    by row."""
+    full-tuning rank r = 128, at its r = 24 and in fp16, the paper's precision) in the launch
+    configuration the benchmark times; sampled token rows of several blocks checked against
+    the oracle row by row."""
     cfg = zd.CONFIGS[name]
     T, q = cfg["T"], cfg["q"]
     r = rank or cfg["r"]
@@ -266,6 +267,50 @@ def test_max_blocks_and_queries():
     ref = run_oracle(c, 1e-1)
     for b in range(nblk):
         assert ferr(Y[b], ref[b], 1.0) <= 1e-4, b
+
+
+def test_forward_difference_paper_k_full_size_sampled():
+    """The paper's K = 99 queries and a baseline block at the OPT-13B shape and token count
+    (nblk = 100, T = 8192: M = 819200 rows, 5120 x 5120 W, r = 64, distinct activations per
+    block) in the launch configuration the benchmark's forward-difference run times; sampled
+    rows of the baseline, the first, a middle and the last query block against the oracle,
+    and the baseline block against the plain product."""
+    cfg = zd.CONFIGS["opt-13b"]
+    T, m, n, r, q = cfg["T"], 5120, 5120, cfg["r"], 99
+    nblk = q + 1
+    c = make_case(T, m, n, r, q, nblk, False, bf16=True)
+    c["bq"] = [0] + list(range(q))
+    c["bs"] = [0] + [1] * q
+    Y = zo.perturbed_linear(c["Xd"], c["Wd"], c["Ud"], c["Vd"], c["Zd"], c["bq"], c["bs"], 1e-3, T,
+                            x_block_stride=c["xs"])
+    torch.cuda.synchronize()
+    del c["Xd"]
+    rows = np.array([0, 1, 255, 256, T // 2 + 1, T - 1])
+    Yh = Y.view(nblk, T, m)
+    for b in (0, 1, 50, 99):
+        got = host(Yh[b][torch.from_numpy(rows).cuda()])
+        ref = run_oracle(c, 1e-3, blocks=[b], rows=rows)[0]
+        assert ferr(got, ref, 1e-3) <= 1e-2, b
+        assert normwise(got, ref) <= 1e-2, b
+        if b == 0:
+            plain = xblock(c, 0, rows) @ c["Wv"].T
+            assert ferr(got, plain, 1e-3) <= 1e-2
+
+
+def test_prepare_group_rejects_shared_workspace():
+    """Linears that would share one workspace (the default per-stream buffer) cannot be prepared
+    as a group: each must keep its own prepared operands until its apply."""
+    T, n, r, q, nblk = 64, 256, 8, 2, 4
+    Xd, _ = cast(zd.draw(32, "X", (T, n), (nblk * T, n)), "bf16")
+    plins = []
+    for i in range(2):
+        Wd, _ = cast(zd.draw(32, "W0", (i, n), (128, n), 0.05), "bf16")
+        U, V, Z = orth(32, (i, 1), 128, r), orth(32, (i, 2), n, r), zd.z_draws(32, 0, i, q, r)
+        plins.append(zo.PerturbedLinear(Xd, Wd, dev_f32(U), dev_f32(V), dev_f32(Z), [0, 0, 1, 1], [1, -1, 1, -1],
+                                        1e-2, T, x_block_stride=T * n))
+    assert plins[0].ws.data_ptr() == plins[1].ws.data_ptr()
+    with pytest.raises(zo.ZoError, match="overlap"):
+        zo.prepare_group(plins)
 
 
 def test_forward_difference_layout_at_paper_k():

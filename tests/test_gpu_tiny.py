@@ -6,9 +6,12 @@ refresh -> perturbed linear (8 blocks, shared X) -> squared loss -> central
 difference -> subspace Adam update.
 
 The loss differences cancel catastrophically (L ~ 6.4 while L+ - L- ~ 1e-4), so
-g carries ~1e-3 relative fp32 noise.  Teacher forcing (both sides use the
-oracle's g) checks the rest of the step at the fp32 bar; the free-running run
-is checked with bounds derived from that noise.
+g carries up to ~3e-4 relative noise from the fp32 rounding of the outputs.  The
+GPU's own g is held, every step, to six standard deviations of that rounding
+noise (estimate_noise_bar: 2.6e-4 to 1.5e-3 over the 20 steps, under the 1e-2
+bar of the build target).  Teacher forcing (both sides use the oracle's g)
+checks the rest of the step at the fp32 bar; the free-running run is checked
+with bounds derived from that noise.
 """
 import numpy as np
 import pytest
@@ -17,7 +20,7 @@ import torch
 import oracle
 import paper_2608_15665_amd as zo
 import zo_draws as zd
-from _common import dev_f32, ferr, host
+from _common import dev_f32, estimate_noise_bar, ferr, host
 
 pytestmark = pytest.mark.gpu
 
@@ -77,6 +80,29 @@ def f32cfg():
     return c
 
 
+def query_outputs(inp, rec, sign):
+    """The exact outputs of every query's block of sign `sign` at step rec (the oracle's)."""
+    X = inp["X"].astype(np.float64)
+    eps = f32cfg()["eps"]
+    return [oracle.perturbed_linear(X, rec["W_before"], rec["U"], rec["V"], rec["Z"][j], sign, eps)
+            for j in range(C["q"])]
+
+
+def g_bar(inp, rec, forward=False):
+    """Per-query bar on the GPU's own g at this step (fp32 output rounding noise, 6 sigma)."""
+    minus = None if forward else query_outputs(inp, rec, -1.0)
+    bar = estimate_noise_bar(query_outputs(inp, rec, +1.0), minus, inp["Ystar"], f32cfg()["eps"], C["r"],
+                             C["T"], rec["g"])
+    assert np.all(bar <= 1e-2), bar  # the derived bar stays inside the build target's 1e-2
+    return bar
+
+
+def g_err(g, g_ref):
+    """Per-query floored relative error |g - g_ref| / max(|g_ref|, rms(g_ref))."""
+    g_ref = np.asarray(g_ref, np.float64)
+    return np.abs(np.asarray(g, np.float64) - g_ref) / np.maximum(np.abs(g_ref), np.sqrt(np.mean(g_ref ** 2)))
+
+
 def test_tiny_teacher_forced():
     inp = zd.tiny_inputs(C["seed"])
     recs = oracle.tiny_run(inp, omega, zdraw, f32cfg())
@@ -85,8 +111,9 @@ def test_tiny_teacher_forced():
         L, g = gpu.step(t, g_override=rec["g"].astype(np.float32))
         Lp, Lm = L[0::2], L[1::2]
         assert ferr(Lp, rec["Lp"], 1.0) <= 1e-5 and ferr(Lm, rec["Lm"], 1.0) <= 1e-5, t
-        # The GPU's own estimate differs from the oracle's by the fp32 cancellation noise only.
-        assert ferr(g, rec["g"], 1.0) <= 5e-2, t
+        # The GPU's own estimate differs from the oracle's by the fp32 rounding noise only.
+        e, bar = g_err(g, rec["g"]), g_bar(inp, rec)
+        assert np.all(e <= bar), (t, e, bar)
         W = host(gpu.W)
         assert ferr(W, rec["W"], 1.0) <= 1e-5, t
 
@@ -132,7 +159,8 @@ def test_tiny_forward_teacher_forced():
     for t, rec in enumerate(recs):
         L, g = gpu.step(t, g_override=rec["g"].astype(np.float32))
         assert ferr(L[:1], [rec["L0"]], 1.0) <= 1e-5 and ferr(L[1:], rec["Lp"], 1.0) <= 1e-5, t
-        assert ferr(g, rec["g"], 1.0) <= 5e-2, t
+        e, bar = g_err(g, rec["g"]), g_bar(inp, rec, forward=True)
+        assert np.all(e <= bar), (t, e, bar)
         assert ferr(host(gpu.W), rec["W"], 1.0) <= 1e-5, t
 
 

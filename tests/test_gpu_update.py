@@ -8,7 +8,10 @@ that bound is below half an ulp; (iii) normwise <= 2e-3.  The fraction of
 1-ulp flips is reported (and held below 1% for bf16).  fp16 W: the same bars
 with fp16 rounding and ulp; its ulp is 8x finer, so the 1-ulp bar applies to
 fewer entries (where the delta cancels W, the split's ~2^-17 of sum |L||V| can
-reach a few fp16 ulps).  The moments are fp32 state: relative 1e-6.
+reach a few fp16 ulps).  The 1-ulp bar must cover at least half of the entries
+(bf16 at every learning rate tested; fp16 at the full-tuning rate 1e-3, where it
+covers 70-100%; at 1e-2 it covers 1-99% and the first two bars carry the check).
+The moments are fp32 state: relative 1e-6.
 """
 import numpy as np
 import pytest
@@ -68,11 +71,12 @@ def update_bound(U, V, S, lr, W_exact):
     return (3 * 2.0 ** -18 + (3 * rp + r + 4) * 2.0 ** -24) * A + 2.0 ** -23 * np.abs(W_exact)
 
 
-def check_bf16_storage(got_w, got_hook, W_exact, E, f16=False):
+def check_bf16_storage(got_w, got_hook, W_exact, E, f16=False, min_held=0.5):
     """Stored 16-bit W (bf16, or fp16 with f16=True): the hook within E of W_exact everywhere;
     the stored value exactly RNE of the hook; within 1 ulp of the exactly rounded W_exact
     wherever E is below half an ulp (where E is not, the first two already bound the stored
-    value by E + half an ulp); returns the fraction of 1-ulp flips."""
+    value by E + half an ulp), which must hold for at least min_held of the entries (None: no
+    floor); returns the fraction of 1-ulp flips."""
     rnd = oracle.round_f16 if f16 else oracle.round_bf16
     assert np.all(np.abs(got_hook - W_exact) <= E)
     assert np.array_equal(got_w, rnd(got_hook))
@@ -80,15 +84,16 @@ def check_bf16_storage(got_w, got_hook, W_exact, E, f16=False):
     e = np.frexp(rne)[1]
     ulp = np.ldexp(1.0, np.maximum(e - 11, -24)) if f16 else np.ldexp(1.0, e - 8)
     held = ulp >= 2 * E
-    if not f16:
+    print(f"1-ulp bar covers {np.mean(held):.3f} of the entries")
+    if min_held is not None:
         # bf16's ulp leaves E far below half an ulp almost everywhere; fp16's is 8x finer, and
         # where the delta cancels W the split's ~2^-17 of sum|L||V| can reach a few fp16 ulps.
-        assert np.mean(held) > 0.5
+        assert np.mean(held) >= min_held
     assert np.all((np.abs(got_w - rne) <= ulp * (1 + 1e-12))[held])
     return float(np.mean(got_w != rne))
 
 
-def check_item(it, ref, bf16, lr):
+def check_item(it, ref, bf16, lr, min_held=0.5):
     got_hook = host(it["dev"]["w_f32_out"])
     got_w = host(it["dev"]["W"])
     # Our own bound, tighter than the 2e-3 bar: the hi+lo bf16 split keeps ~2^-16 of the delta.
@@ -96,7 +101,7 @@ def check_item(it, ref, bf16, lr):
     if bf16:
         assert ferr(got_hook, ref["W"], 1.0) <= 2e-3
         E = update_bound(it["U"], it["V"], ref["S"], lr, ref["W"])
-        flips = check_bf16_storage(got_w, got_hook, ref["W"], E, it["f16"])
+        flips = check_bf16_storage(got_w, got_hook, ref["W"], E, it["f16"], min_held)
         assert normwise(got_w, ref["W"]) <= 2e-3
         print(f"16-bit storage flips vs exact rounding: {flips:.2e}")
         if not it["f16"]:
@@ -133,16 +138,20 @@ def test_bf16_update_parity(m, n, r, q, t, moments):
     (256, 512, 128, 4, 2, True),
     (17, 8, 4, 4, 1, False),
 ])
-def test_f16_update_parity(m, n, r, q, t, moments):
+@pytest.mark.parametrize("lr", [1e-3, 1e-2])
+def test_f16_update_parity(m, n, r, q, t, moments, lr):
     """fp16 W (the paper's precision): the same kernel with fp16 conversions of W; stored values
-    RNE to fp16 of the fp32 hook, held to the fp16 ulp."""
+    RNE to fp16 of the fp32 hook, held to the fp16 ulp.  At the full-tuning learning rate 1e-3
+    the 1-ulp bar covers at least half of the entries; at 1e-2 the update's rounding bound
+    exceeds half an fp16 ulp on most entries (down to 1% covered at r = 128), so there the
+    hook bound and the exact rounding of the hook carry the check."""
     it = make_item(21, (m, n, r), m, n, r, q, False, moments, f16=True)
     g = zd.f32(zd.draw(21, "G", (m, n, r), (q,), 1e-2))
-    lr, b1, b2, ea = 1e-2, 0.9, 0.95, 1e-8
+    b1, b2, ea = 0.9, 0.95, 1e-8
     ref = expected(it, g.astype(np.float64), t, lr, b1, b2, ea)
     zo.subspace_adam_update([it["dev"]], dev_f32(g), t, lr, b1, b2, ea)
     torch.cuda.synchronize()
-    check_item(it, ref, True, lr)
+    check_item(it, ref, True, lr, min_held=0.5 if lr <= 1e-3 else None)
 
 
 @pytest.mark.parametrize("m,n,r,q", [(256, 512, 4, 4), (33, 71, 5, 3), (1, 1, 1, 1), (200, 264, 128, 2)])

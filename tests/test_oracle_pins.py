@@ -584,6 +584,56 @@ def test_tiny_loop_decreases_loss():
     np.testing.assert_allclose(rec["g"], exact, rtol=1e-6, atol=1e-9)
 
 
+@pytest.mark.parametrize("estimator", ["central", "forward"])
+def test_tiny_run_state_carried_across_steps_and_refreshes(estimator):
+    """The 20-step loop's state from step to step, pinned against things other than the loop:
+    - torch.optim.Adam (betas and eps of the run), stepped once per loop step with the run's own
+      Zbar_t as the gradient of an r x r parameter, moves that parameter by exactly the run's
+      subspace coordinates of the weight change, U_t^T (W_{t+1} - W_t) V_t = -lr S_t (Eq. 10
+      with orthonormal U, V).  Torch keeps its moments across every step and refresh and
+      counts steps from 1, so moments that were reset, not carried, or bias-corrected with the
+      wrong index fail here;
+    - W carries over: step t + 1 starts from step t's W;
+    - the subspace is the sign-corrected LAPACK QR of Omega(t) at t mod F = 0 and unchanged in
+      between (an off-by-one in the refresh cadence fails);
+    - Zbar_t = (1/q) sum_j g_j Z_j;
+    - each g_j is the exact directional derivative of the quadratic loss at W_t (central), or
+      that plus eps/2 ||X P_j^T||^2 / T (forward, P_j = U Z_j V^T)."""
+    torch = pytest.importorskip("torch")
+    c = zd.TINY
+    inp = zd.tiny_inputs(0)
+    om = lambda t: zd.omega_pair(0, t, 0, c["m"], c["n"], c["r"])
+    recs = oracle.tiny_run(inp, om, lambda t: zd.z_draws(0, t, 0, c["q"], c["r"]), c, estimator=estimator)
+    assert len(recs) == c["steps"]
+    r, X, Ys = c["r"], inp["X"].astype(np.float64), inp["Ystar"]
+    p = torch.zeros((r, r), dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([p], lr=c["lr"], betas=(c["beta1"], c["beta2"]), eps=c["eps_adam"])
+    W_prev = inp["W"].astype(np.float64)
+    for t, rec in enumerate(recs):
+        np.testing.assert_array_equal(rec["W_before"], W_prev)
+        if t % c["F"] == 0:
+            for got, omega in zip((rec["U"], rec["V"]), om(t)):
+                Q, R = np.linalg.qr(np.asarray(omega, np.float64))
+                np.testing.assert_allclose(got, Q * np.sign(np.diag(R))[None, :], rtol=0, atol=1e-12)
+        else:
+            np.testing.assert_array_equal(rec["U"], recs[t - 1]["U"])
+            np.testing.assert_array_equal(rec["V"], recs[t - 1]["V"])
+        np.testing.assert_allclose(rec["Zbar"], np.tensordot(rec["g"], rec["Z"], axes=1) / c["q"],
+                                   rtol=1e-13, atol=1e-16)
+        grad = (X @ rec["W_before"].T - Ys).T @ X / X.shape[0]
+        P = [rec["U"] @ Z @ rec["V"].T for Z in rec["Z"]]
+        exact = np.array([np.sum(grad * Pj) for Pj in P])
+        if estimator == "forward":
+            exact += np.array([0.5 * c["eps"] * np.sum((X @ Pj.T) ** 2) / X.shape[0] for Pj in P])
+        np.testing.assert_allclose(rec["g"], exact, rtol=1e-6, atol=1e-9)
+        before = p.detach().clone().numpy()
+        p.grad = torch.from_numpy(np.array(rec["Zbar"], np.float64))
+        opt.step()
+        moved = rec["U"].T @ (rec["W"] - rec["W_before"]) @ rec["V"]
+        np.testing.assert_allclose(moved, p.detach().numpy() - before, rtol=1e-8, atol=1e-13)
+        W_prev = rec["W"]
+
+
 # ---------------------------------------------------------------------------
 # The decoder layer the queries run through (Eq. 5 inside Alg. 3)
 # ---------------------------------------------------------------------------
