@@ -80,7 +80,7 @@ def source_hash():
     parts = [_region(gemm, "struct GemmArgs {", "};"),
              _region(gemm, "template <int OUT>\n__device__ __forceinline__ void store4(", "\n}\n"),
              _region(gemm, "__device__ __forceinline__ f32x16 mfma32(", "\n}\n"),
-             _region(gemm, "__device__ __forceinline__ int g4(int r)", 'hipGetLastError(), "k_gemm_main");\n}'),
+             _region(gemm, "constexpr int MAIN_RB = 128;", 'hipGetLastError(), "k_gemm_main");\n}'),
              _region(inc, "__device__ __forceinline__ bf16_t f32_to_bf16(", "\n}\n"),
              _region(inc, "__device__ __forceinline__ uint32_t pack_bf16x2(", "\n}\n"),
              _region(inc, "__device__ __forceinline__ uint16_t f32_to_f16(", "\n}\n"),

@@ -581,100 +581,145 @@ int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
 //
 // 256 x 256 output tile per workgroup of 4 waves (one per SIMD), each wave a
 // 128 x 128 sub-tile held in 16 accumulators of the 32x32x16 MFMA (256 AGPRs).
-// K is walked in tiles of 32 (64-byte LDS rows) through a 4-stage LDS ring
-// filled by direct global->LDS loads (global_load_lds_dwordx4: 16 rows x 64 B
-// per instruction, 8 per wave per tile).  Row r of a tile keeps its 16-byte
-// chunk c at position c ^ g(r), g(r) = ((r >> 2) ^ (r & 2)) & 3, which makes the
-// fragment reads conflict free for 8- and 16-lane LDS passes.
 //
-// One barrier per k-tile, in its middle: before it each wave has waited for
-// its own loads of tile kt+1 and its own reads of tile kt; after it, the
-// loads of tile kt+4 start into tile kt's stage (half right away, half in the
-// next iteration's first half, so load issue is spread over the loop) and
-// the first fragments of tile kt+1 are read while the second half of tile
-// kt's MFMAs run.  Loads therefore have three iterations to land.  The tail
-// re-issues the last tile into its own stage (identical bytes), which keeps
-// the loop body free of data-dependent branches so the instruction scheduler
-// follows the sched_group_barrier interleave of MFMAs, LDS reads and loads.
+// K is walked in tiles of 64, so every LDS row holds 128 bytes: one whole cache
+// line per row, which the load path moves ~1.6x faster than 64-byte half lines
+// (measured with load-only kernels of the same traffic).  Tiles are brought in by
+// direct global->LDS buffer loads (buffer_load_dwordx4 ... lds: 8 rows x 128 B per
+// instruction, a per-lane row offset fixed for the whole loop and the k offset in a
+// scalar register, so the loop has no address arithmetic).  Row r keeps its 16-byte
+// chunk c at position c ^ f(r), f(r) = (r >> 1) & 7: the fragment reads (16
+// consecutive rows at one chunk per 16-lane pass) are conflict free.
 //
-// The rank-rc correction is rc/32 more k-tiles through the same pipeline,
-// with the A operand taken from ca (per block, rows_a x rc) and the B operand
-// from cb (per block, rows_b x rc).  Rows past rows_a / rows_b are loaded
-// from the last valid row (never stored).  F16: the main k-tiles run the fp16
-// MFMA and the correction k-tiles (bf16 hi/lo operands) the bf16 MFMA, as two
-// loops over the same body; the loads do not depend on the element type.
-// OUT (zo_dtype of Y) and EPI (zo_epilogue) are template parameters: with all
-// 256 accumulators live, one store path per instantiation keeps the epilogue
-// free of per-store branches (a run-time choice there made the compiler keep
-// spilled VGPR copies of the accumulators, one of which it stored wrongly).
-__device__ __forceinline__ int g4(int r) { return ((r >> 2) ^ (r & 2)) & 3; }
+// LDS ring: the 160 KB as 5 slots of 32 KB, one per part of a tile (part A = the
+// 256 W rows, part B = the 256 X rows): A(t) in slot 2t % 5, B(t) in slot (2t+1) % 5.
+// One barrier per tile, barrier(k), after the wave's last fragment reads of tile k:
+// every wave has finished with tile k, and tile k+1 has landed.  Tile k's two slots
+// are then refilled with B(k+2) and A(k+3).  The loads are spread evenly over the
+// tile's four 16-deep substeps (one load per four MFMAs): B(k+2) half in the last
+// substep of tile k and half in the first of tile k+1, A(k+3) in the next two.
+// Issued in bursts they would fill the address unit's queue and block the wave's
+// MFMA issue behind them; spread out they hide under the MFMAs.  So a B part has a
+// tile-time to land and an A part two; at barrier(k) only A(k+2), the last 8 loads
+// issued, may be outstanding.  Fragments for the next substep are read while the
+// current one's MFMAs run; scheduling fences keep each substep's MFMAs, reads and
+// loads in that interleave.
+//
+// The rank-rc correction is rc/64 more k-tiles through the same pipeline, with the
+// A operand taken from ca (per block, rows_a x rc) and the B operand from cb (per
+// block, rows_b x rc).  The last tile of a segment whose length is an odd multiple
+// of 32 holds 32 valid columns: only its first two substeps are computed (the other
+// half of its rows is loaded but never read).  So every accumulator sees its k terms
+// in ascending order, 16 at a time, whatever the tiling.  Rows past rows_a / rows_b
+// are loaded from the last valid row (never stored).  F16: the main tiles run the
+// fp16 MFMA and the correction tiles (bf16 hi/lo operands) the bf16 MFMA.  OUT
+// (zo_dtype of Y) and EPI (zo_epilogue) are template parameters: with all 256
+// accumulators live, one store path per instantiation keeps the epilogue free of
+// per-store branches (a run-time choice there made the compiler keep spilled VGPR
+// copies of the accumulators, one of which it stored wrongly).
+//
+// Each operand's buffer descriptor spans its rows x K (or rc) elements, so the host
+// takes this kernel only when every such span is below 2^32 bytes.
+constexpr int MAIN_RB = 128;               // bytes per LDS row (64 bf16)
+constexpr int MAIN_PART = 256 * MAIN_RB;   // one part of a tile: 32 KB
+constexpr int MAIN_SLOTS = 5;
+
+__device__ __forceinline__ int f8(int r) { return (r >> 1) & 7; }
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)bytes, 0x00020000);
+}
 
 template <bool F16, int OUT, int EPI>
 __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
-  constexpr int STAGES = 4;
-  constexpr int BM = 256, BN = 256, RB = 64;               // RB: bytes per LDS row (32 bf16)
-  constexpr int TILE_BYTES = (BM + BN) * RB;                // 32 KB per stage
-  __shared__ __attribute__((aligned(1024))) char lds[STAGES * TILE_BYTES];
+  constexpr int RB = MAIN_RB, PART = MAIN_PART;
+  __shared__ __attribute__((aligned(1024))) char lds[MAIN_SLOTS * PART];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
 
+  // XCD-aware tile order (each XCD a contiguous range), grouped 8 token tiles deep.
   const int w = blockIdx.x;
   const int nt = a.total_tiles;
   const int xcd = w & 7, widx = w >> 3;
   const int lt = xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
   constexpr int GROUP = 8;
-  const int total_bt = a.nblk * a.tiles_b;
-  const int per_group = GROUP * a.tiles_a;
-  const int grp = lt / per_group;
-  const int first = grp * GROUP;
-  const int gsize = min(GROUP, total_bt - first);
-  const int rem = lt - grp * per_group;
-  const int bt = first + rem % gsize;
-  const int at = rem / gsize;
-  const int blk = bt / a.tiles_b;
-  const int t0 = (bt % a.tiles_b) * BN;
-  const int m0 = at * BM;
+  const int per_group = GROUP * a.tiles_a, grp = lt / per_group, first = grp * GROUP;
+  const int gsize = min(GROUP, a.nblk * a.tiles_b - first), rem = lt - grp * per_group;
+  const int bt = first + rem % gsize, at = rem / gsize;
+  // The decode is uniform but its divisions run on the VALU: pin the results to scalar
+  // registers, so the buffer descriptors built from them are scalar too.
+  const int blk = __builtin_amdgcn_readfirstlane(bt / a.tiles_b);
+  const int t0 = __builtin_amdgcn_readfirstlane((bt % a.tiles_b) * 256);
+  const int m0 = __builtin_amdgcn_readfirstlane(at * 256);
 
-  const int NKM = a.K / 32;
-  const int NTK = NKM + a.rc / 32;
-  const bf16_t* Bblk = a.B + (long long)blk * a.b_block_stride;
-  const bf16_t* Cblk = a.ca + (long long)blk * a.ca_block_stride;
-  const bf16_t* Dblk = a.cb + (long long)blk * a.cb_block_stride;
-  // DMA lane mapping: row 16 (wave + 4 i) + lane/4, physical chunk lane%4.
-  const int dr = lane >> 2;
-  const int dkc = (lane & 3) ^ g4(dr);
-  int ra[4], rb[4];  // clamped source rows of this lane's four A and four B loads
+  // Tiles: main segment [0, NTM) over K, rank-rc segment [NTM, NT) over rc.
+  const int NTM = (a.K + 63) / 64, NT = NTM + (a.rc + 63) / 64;
+  const bool halfM = (a.K & 63) != 0, halfR = (a.rc & 63) != 0;
+  const bf16_t* const Bblk = a.B + (long long)blk * a.b_block_stride;
+  const bf16_t* const Cblk = a.ca + (long long)blk * a.ca_block_stride;
+  const bf16_t* const Dblk = a.cb + (long long)blk * a.cb_block_stride;
+  const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (unsigned)a.rows_a * a.K * 2);
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(Bblk, (unsigned)a.rows_b * a.K * 2);
+  // DMA: load i (0..7) of a wave writes rows 8 (wave + 4 i) .. + 7 of a part; lane l writes row
+  // l / 8 at physical chunk l % 8, which holds logical chunk (l % 8) ^ f(row) (f(row) does not
+  // depend on i).  Per-lane byte offsets of the four operands at k = 0.
+  const int drow = lane >> 3;
+  const int lch = (lane & 7) ^ f8(8 * wave + drow);
+  unsigned voA[8], voB[8], voC[8], voD[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 16 * (wave + 4 * i) + dr;
-    ra[i] = min(m0 + row, a.rows_a - 1);
-    rb[i] = min(t0 + row, a.rows_b - 1);
+  for (int i = 0; i < 8; ++i) {
+    const int row = 8 * (wave + 4 * i) + drow;
+    const unsigned ra = (unsigned)min(m0 + row, a.rows_a - 1), rb = (unsigned)min(t0 + row, a.rows_b - 1);
+    voA[i] = ra * (unsigned)a.K * 2u + lch * 16u;
+    voB[i] = rb * (unsigned)a.K * 2u + lch * 16u;
+    voC[i] = ra * (unsigned)a.rc * 2u + lch * 16u;
+    voD[i] = rb * (unsigned)a.rc * 2u + lch * 16u;
   }
-  // One half of a tile's loads: part 0 the A rows (W, or the rank-r operand of W's side),
-  // part 1 the B rows (X, or the rank-r operand of X's side); 4 loads per lane each.
-  auto issue_part = [&](int kt, int part) {
-    char* st = lds + (kt % STAGES) * TILE_BYTES + 16 * wave * RB + part * BM * RB;
-    const bool main = kt < NKM;
-    const bf16_t* base = part ? (main ? Bblk : Dblk) : (main ? a.A : Cblk);
-    const int* rr = part ? rb : ra;
-    const int ld = main ? a.K : a.rc;
-    const int ko = (main ? kt : kt - NKM) * 32 + dkc * 8;
+  char* const ldsw = lds + 8 * wave * RB;
+  // Loads i in [I0, I1) of part A (W rows) or B (X rows) of tile t into slot sl; tiles past the
+  // end are not loaded.  MAIN: t is known to be a main-segment tile.  The rank segment's
+  // descriptor is built after its base is chosen (a scalar select), so it stays in scalar
+  // registers.
+  auto load_A = [&](int sl, int t, auto MAIN, auto I0, auto I1) {
+    const bool m = decltype(MAIN)::value || t < NTM;
+    if (!m && t >= NT) return;
+    char* d = ldsw + sl * PART;
+    const __amdgpu_buffer_rsrc_t r = m ? rsA : make_rsrc(Cblk, (unsigned)a.rows_a * a.rc * 2);
+    const unsigned so = (unsigned)(m ? t : t - NTM) * 128u;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(base + (size_t)rr[i] * ld + ko),
-                                       (lds_ptr_t)(st + 64 * i * RB), 16, 0, 0);
+    for (int i = decltype(I0)::value; i < decltype(I1)::value; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(d + 32 * RB * i), 16, m ? voA[i] : voC[i], so, 0, 0);
   };
+  auto load_B = [&](int sl, int t, auto MAIN, auto I0, auto I1) {
+    const bool m = decltype(MAIN)::value || t < NTM;
+    if (!m && t >= NT) return;
+    char* d = ldsw + sl * PART;
+    const __amdgpu_buffer_rsrc_t r = m ? rsB : make_rsrc(Dblk, (unsigned)a.rows_b * a.rc * 2);
+    const unsigned so = (unsigned)(m ? t : t - NTM) * 128u;
+#pragma unroll
+    for (int i = decltype(I0)::value; i < decltype(I1)::value; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(d + 32 * RB * i), 16, m ? voB[i] : voD[i], so, 0, 0);
+  };
+  using Main = std::true_type;
+  using Any = std::false_type;
+  using I0 = std::integral_constant<int, 0>;
+  using I4 = std::integral_constant<int, 4>;
+  using I8 = std::integral_constant<int, 8>;
+
   const int fr = lane & 31, fh = lane >> 5;
-  const int fg = g4(fr);
-  const int offA = (wm * 128 + fr) * RB, offB = BM * RB + (wn * 128 + fr) * RB;
-  auto frags = [&](int kt, int s, bf16x8* fa, bf16x8* fb) {
-    const char* st = lds + (kt % STAGES) * TILE_BYTES;
-    const int ch = ((2 * s + fh) ^ fg) * 16;
+  const int ff = f8(fr);  // f of every fragment row (they differ from fr by multiples of 32)
+  const int offA = (wm * 128 + fr) * RB, offB = (wn * 128 + fr) * RB;
+  bf16x8 F0a[4], F0b[4], F1a[4], F1b[4];
+  // Fragments of substep s (k 16 s .. 16 s + 15 of the tile) from the slots sa (A) and sb (B).
+  auto frags = [&](int sa, int sb, int s, bf16x8* fa, bf16x8* fb) {
+    const int ch = ((2 * s + fh) ^ ff) * 16;
+    const char* pa = lds + sa * PART + offA + ch;
+    const char* pb = lds + sb * PART + offB + ch;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) fa[i] = *(const bf16x8*)(st + offA + i * 32 * RB + ch);
+    for (int i = 0; i < 4; ++i) fa[i] = *(const bf16x8*)(pa + i * 32 * RB);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)(st + offB + j * 32 * RB + ch);
+    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)(pb + j * 32 * RB);
   };
   f32x16 acc[4][4];
 #pragma unroll
@@ -689,52 +734,101 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = mfma32<decltype(f16)::value>(fa[i], fb[j], acc[i][j]);
   };
-
-  // Prologue: tiles 0..3 issued in full; wait for tile 0.
-  for (int t = 0; t < 4; ++t) {
-    issue_part(min(t, NTK - 1), 0);
-    issue_part(min(t, NTK - 1), 1);
-  }
-  asm volatile("s_waitcnt vmcnt(24)" ::: "memory");  // this wave's loads of tile 0 landed
-  __syncthreads();                                    // ... and every wave's
-  bf16x8 f0a[4], f0b[4], f1a[4], f1b[4];
-  frags(0, 0, f0a, f0b);
-  // Tile kt+4 reuses tile kt's stage: its part 0 is issued right after barrier(kt) (every wave
-  // has finished reading tile kt: each waits for its own reads before the barrier), its part 1
-  // in the first half of iteration kt+1.  So at barrier(kt) the loads outstanding are, in issue
-  // order, tile kt+1, kt+2, kt+3 (8 each): waiting down to 16 leaves tile kt+1 complete.
-  auto body = [&](int kt, auto f16) {
-    frags(kt, 1, f1a, f1b);
-    if (kt >= 1) issue_part(min(kt + 3, NTK - 1), 1);
-    mma(f0a, f0b, f16);
-    for (int i = 0; i < 4; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // 2 LDS reads
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 global->LDS load
+  // One substep's 16 MFMAs: the next substep's 8 fragment reads after the first 8 of them, its
+  // nvm loads spread evenly over all 16; then a fence so nothing moves across substeps.
+  auto sub_sched = [&](int nvm) {
+    const int every = nvm > 0 ? 16 / nvm : 17;
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                     // MFMA
+      if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);          // LDS read
+      if (i % every == 1 % every && i / every < nvm)
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                   // global->LDS load
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");                      // no memory access moves across
-    issue_part(min(kt + 4, NTK - 1), 0);
-    frags(kt + 1, 0, f0a, f0b);
-    mma(f1a, f1b, f16);
-    for (int i = 0; i < 4; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 global->LDS load
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // 2 LDS reads
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 12, 0);
+    __builtin_amdgcn_sched_barrier(0);
   };
-  if constexpr (F16) {
-    int kt = 0;
-    for (; kt < NKM; ++kt) body(kt, std::true_type{});
-    for (; kt < NTK; ++kt) body(kt, std::false_type{});
-  } else {
-    for (int kt = 0; kt < NTK; ++kt) body(kt, std::false_type{});
+
+  // Prologue: A0, B0, A1 and the first half of B1 (what the last substep of tile -1 would have
+  // issued); tile 0 then issues the rest of B1 and A2.
+  load_A(0, 0, Any{}, I0{}, I8{});
+  load_B(1, 0, Any{}, I0{}, I8{});
+  load_A(2, 1, Any{}, I0{}, I8{});
+  load_B(3, 1, Any{}, I0{}, I4{});
+  if (NT > 1)
+    asm volatile("s_waitcnt vmcnt(12)" ::: "memory");  // this wave's loads of tile 0 landed
+  else
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  frags(0, 1, 0, F0a, F0b);
+
+  // Tile k, a full main tile with main tiles k+1 and k+2 after it; K5 = k % 5 makes every slot a
+  // compile-time constant.  Loads: the rest of B(k+1) in substep 0, A(k+2) in substeps 1 and 2
+  // (both into tile k-1's slots, free since barrier(k-1)), the first half of B(k+2) in substep 3
+  // (into tile k's A slot, free after barrier(k)).
+  auto body_main = [&](int k, auto K5, auto f16) {
+    constexpr int k5 = decltype(K5)::value;
+    constexpr int sa = (2 * k5) % 5, sb = (2 * k5 + 1) % 5;                       // tile k
+    constexpr int na = (2 * k5 + 2) % 5, nb = (2 * k5 + 3) % 5, a2 = (2 * k5 + 4) % 5;  // k+1, A(k+2)
+    frags(sa, sb, 1, F1a, F1b);
+    load_B(nb, k + 1, Main{}, I4{}, I8{});
+    mma(F0a, F0b, f16);
+    sub_sched(4);
+    frags(sa, sb, 2, F0a, F0b);
+    load_A(a2, k + 2, Main{}, I0{}, I4{});
+    mma(F1a, F1b, f16);
+    sub_sched(4);
+    frags(sa, sb, 3, F1a, F1b);
+    load_A(a2, k + 2, Main{}, I4{}, I8{});
+    mma(F0a, F0b, f16);
+    sub_sched(4);
+    asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");  // all but A(k+2)
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    frags(na, nb, 0, F0a, F0b);
+    load_B(sa, k + 2, Main{}, I0{}, I4{});
+    mma(F1a, F1b, f16);
+    sub_sched(4);
+  };
+  // Any tile (run-time slots, loads of either segment or none, half tiles).  The loads go out
+  // together here: only the last few tiles take this path.
+  auto body_any = [&](int k, auto f16) {
+    const int sa = (2 * k) % 5, sb = (2 * k + 1) % 5, na = (2 * k + 2) % 5, nb = (2 * k + 3) % 5;
+    const int a2 = (2 * k + 4) % 5;
+    const bool half = k == NTM - 1 ? halfM : (k == NT - 1 ? halfR : false);
+    load_B(nb, k + 1, Any{}, I4{}, I8{});
+    load_A(a2, k + 2, Any{}, I0{}, I8{});
+    frags(sa, sb, 1, F1a, F1b);
+    mma(F0a, F0b, f16);
+    if (!half) {
+      frags(sa, sb, 2, F0a, F0b);
+      mma(F1a, F1b, f16);
+      frags(sa, sb, 3, F1a, F1b);
+      mma(F0a, F0b, f16);
+    }
+    // The last loads issued are A(k+2)'s when it exists; otherwise none may stay outstanding.
+    if (k + 2 < NT)
+      asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (k + 1 < NT) frags(na, nb, 0, F0a, F0b);
+    load_B(sa, k + 2, Any{}, I0{}, I4{});
+    mma(F1a, F1b, f16);
+  };
+  using MT = std::integral_constant<bool, F16>;
+  // body_main needs k + 2 <= NTM - 1 (main-segment loads) and tile k full: k <= NTM - 3.
+  const int P = NTM >= 3 ? (NTM - 2) / 5 * 5 : 0;
+  int k = 0;
+  for (; k < P; k += 5) {
+    body_main(k, std::integral_constant<int, 0>{}, MT{});
+    body_main(k + 1, std::integral_constant<int, 1>{}, MT{});
+    body_main(k + 2, std::integral_constant<int, 2>{}, MT{});
+    body_main(k + 3, std::integral_constant<int, 3>{}, MT{});
+    body_main(k + 4, std::integral_constant<int, 4>{}, MT{});
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain the tail loads before exit
+  for (; k < NTM; ++k) body_any(k, MT{});
+  for (; k < NT; ++k) body_any(k, std::false_type{});
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain before the stores and exit
 
   char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (OUT == ZO_F32 ? 4 : 2);
   const char* Rb = (const char*)a.R + (long long)blk * a.r_block_stride * (OUT == ZO_F32 ? 4 : 2);
@@ -765,6 +859,15 @@ void launch_main_epi(const GemmArgs& a, dim3 grid, hipStream_t stream) {
     hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_SILU_MUL>), grid, dim3(256), 0, stream, a);
   else
     hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_NONE>), grid, dim3(256), 0, stream, a);
+}
+
+// Whether k_gemm_main can take a call: K a multiple of 32 and every operand's buffer descriptor
+// span (rows x K, rows x rc elements of 2 bytes) below 2^32 bytes.
+bool main_gemm_fits(const GemmArgs& a) {
+  const unsigned long long lim = (1ull << 32) - 256;
+  return a.K % 32 == 0 && (unsigned long long)a.rows_a * a.K * 2 <= lim &&
+         (unsigned long long)a.rows_b * a.K * 2 <= lim && (unsigned long long)a.rows_a * a.rc * 2 <= lim &&
+         (unsigned long long)a.rows_b * a.rc * 2 <= lim;
 }
 
 int launch_gemm_main(GemmArgs a, bool f16, hipStream_t stream) {
@@ -991,7 +1094,7 @@ int zo_gemm_plain(int T, int m, int n, int nblk, int dtype, const void* X, long 
   h.R = R;
   h.r_block_stride = r_block_stride;
   const bool f16 = dtype == ZO_F16;
-  if (n % 32 == 0) return launch_gemm_main(h, f16, stream);
+  if (main_gemm_fits(h)) return launch_gemm_main(h, f16, stream);
   return f16 ? launch_gemm_bf16<2, 4, 4, 2, true>(h, stream) : launch_gemm_bf16<2, 4, 4, 2, false>(h, stream);
 }
 
@@ -1023,7 +1126,7 @@ int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y
     h.R = R;
     h.r_block_stride = r_block_stride;
     const bool f16 = p.in_dtype == ZO_F16;
-    if (p.n % 32 == 0) return launch_gemm_main(h, f16, stream);
+    if (main_gemm_fits(h)) return launch_gemm_main(h, f16, stream);
     return f16 ? launch_gemm_bf16<2, 4, 4, 2, true>(h, stream) : launch_gemm_bf16<2, 4, 4, 2, false>(h, stream);
   }
   F32Args h{};
