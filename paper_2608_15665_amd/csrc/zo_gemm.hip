@@ -734,17 +734,37 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = mfma32<decltype(f16)::value>(fa[i], fb[j], acc[i][j]);
   };
-  // One substep's 16 MFMAs: the next substep's 8 fragment reads after the first 8 of them, its
-  // nvm loads spread evenly over all 16; then a fence so nothing moves across substeps.
-  auto sub_sched = [&](int nvm) {
-    const int every = nvm > 0 ? 16 / nvm : 17;
-    for (int i = 0; i < 16; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                     // MFMA
-      if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);          // LDS read
-      if (i % every == 1 % every && i / every < nvm)
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                   // global->LDS load
+  // Fragment x (0..3: A fragment x, 4..7: B fragment x - 4) of substep s from slots sa / sb.
+  auto frag1 = [&](int sa, int sb, int s, int x, bf16x8* fa, bf16x8* fb) {
+    const int ch = ((2 * s + fh) ^ ff) * 16;
+    if (x < 4)
+      fa[x] = *(const bf16x8*)(lds + sa * PART + offA + ch + x * 32 * RB);
+    else
+      fb[x - 4] = *(const bf16x8*)(lds + sb * PART + offB + ch + (x - 4) * 32 * RB);
+  };
+  // One load (i of 8) of part A / B of main-segment tile t into slot sl.
+  auto load1_A = [&](int sl, int t, int i) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_ptr_t)(ldsw + sl * PART + 32 * RB * i), 16, voA[i],
+                                             (unsigned)t * 128u, 0, 0);
+  };
+  auto load1_B = [&](int sl, int t, int i) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_ptr_t)(ldsw + sl * PART + 32 * RB * i), 16, voB[i],
+                                             (unsigned)t * 128u, 0, 0);
+  };
+  // One steady-state substep, written out in issue order: MFMA x (x = 0..15, accumulator
+  // x / 4, x % 4), then the next substep's fragment read x (x < 8, fragments (ra, rb, rs) into
+  // na / nb), then load ld(x / 4) after MFMAs 1, 5, 9, 13, each group fenced so the compiler
+  // keeps the interleave (left to itself it bunches the reads and loads, and the wave's MFMA
+  // issue stalls behind them).
+  auto substep = [&](const bf16x8* fa, const bf16x8* fb, int ra, int rb, int rs, bf16x8* na, bf16x8* nb,
+                     auto ld, auto f16) {
+#pragma unroll
+    for (int x = 0; x < 16; ++x) {
+      acc[x >> 2][x & 3] = mfma32<decltype(f16)::value>(fa[x >> 2], fb[x & 3], acc[x >> 2][x & 3]);
+      if (x < 8) frag1(ra, rb, rs, x, na, nb);
+      if (x % 4 == 1) ld(x / 4);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);
   };
 
   // Prologue: A0, B0, A1 and the first half of B1 (what the last substep of tile -1 would have
@@ -768,25 +788,13 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     constexpr int k5 = decltype(K5)::value;
     constexpr int sa = (2 * k5) % 5, sb = (2 * k5 + 1) % 5;                       // tile k
     constexpr int na = (2 * k5 + 2) % 5, nb = (2 * k5 + 3) % 5, a2 = (2 * k5 + 4) % 5;  // k+1, A(k+2)
-    frags(sa, sb, 1, F1a, F1b);
-    load_B(nb, k + 1, Main{}, I4{}, I8{});
-    mma(F0a, F0b, f16);
-    sub_sched(4);
-    frags(sa, sb, 2, F0a, F0b);
-    load_A(a2, k + 2, Main{}, I0{}, I4{});
-    mma(F1a, F1b, f16);
-    sub_sched(4);
-    frags(sa, sb, 3, F1a, F1b);
-    load_A(a2, k + 2, Main{}, I4{}, I8{});
-    mma(F0a, F0b, f16);
-    sub_sched(4);
+    substep(F0a, F0b, sa, sb, 1, F1a, F1b, [&](int i) { load1_B(nb, k + 1, 4 + i); }, f16);
+    substep(F1a, F1b, sa, sb, 2, F0a, F0b, [&](int i) { load1_A(a2, k + 2, i); }, f16);
+    substep(F0a, F0b, sa, sb, 3, F1a, F1b, [&](int i) { load1_A(a2, k + 2, 4 + i); }, f16);
     asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");  // all but A(k+2)
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    frags(na, nb, 0, F0a, F0b);
-    load_B(sa, k + 2, Main{}, I0{}, I4{});
-    mma(F1a, F1b, f16);
-    sub_sched(4);
+    substep(F1a, F1b, na, nb, 0, F0a, F0b, [&](int i) { load1_B(sa, k + 2, i); }, f16);
   };
   // Any tile (run-time slots, loads of either segment or none, half tiles).  The loads go out
   // together here: only the last few tiles take this path.
