@@ -79,6 +79,8 @@ def source_hash():
     inc = open(os.path.join(CSRC, "zo_internal.h")).read()
     parts = [_region(gemm, "struct GemmArgs {", "};"),
              _region(gemm, "template <int OUT>\n__device__ __forceinline__ void store4(", "\n}\n"),
+             _region(gemm, "template <int OUT>\n__device__ __forceinline__ void load8(", "\n}\n"),
+             _region(gemm, "template <int OUT>\n__device__ __forceinline__ void store8(", "\n}\n"),
              _region(gemm, "__device__ __forceinline__ f32x16 mfma32(", "\n}\n"),
              _region(gemm, "constexpr int MAIN_RB = 128;", 'hipGetLastError(), "k_gemm_main");\n}'),
              _region(inc, "__device__ __forceinline__ bf16_t f32_to_bf16(", "\n}\n"),
@@ -89,6 +91,190 @@ def source_hash():
     for p in parts:
         h.update(p.encode())
     return h.hexdigest()[:16]
+
+
+class ZFeed:
+    """The per-step coefficients Z_j of every perturbed factor (Alg. 3: one Gaussian r x r draw
+    per query and matrix, keyed by step), drawn on the host inside the timed window.
+
+    A worker thread draws step s + 1 into a pinned host buffer while the GPU runs step s; the
+    copy to the device runs on a side stream, and the compute stream waits for it before the
+    step's first use.  Two device slots alternate: the copy into a slot waits until the compute
+    stream has finished the step that last read it, and the host buffer of a slot is refilled
+    only after its previous copy has landed."""
+
+    def __init__(self, seed, nfac, q, r, dev):
+        import threading  # noqa: F401  (the executor below runs one worker thread)
+        from concurrent.futures import ThreadPoolExecutor
+
+        import torch
+        self.seed, self.nfac, self.q, self.r = seed, nfac, q, r
+        shape = (nfac, q, r, r)
+        self.dev = [torch.empty(shape, dtype=torch.float32, device=dev) for _ in range(2)]
+        self.host = [torch.empty(shape, dtype=torch.float32, pin_memory=True) for _ in range(2)]
+        self.copy_stream = torch.cuda.Stream()
+        self.copied = [None, None]
+        self.freed = [None, None]
+        self.pool = ThreadPoolExecutor(max_workers=1)
+        self.pending = {}
+        self.draw_s = {}
+        self.h2d = {}
+        self.nbytes = 4 * nfac * q * r * r
+
+    def _draw(self, s, slot):
+        import zo_draws as zd
+        ev = self.copied[slot]
+        if ev is not None:
+            ev.synchronize()
+        t0 = time.perf_counter()
+        h = self.host[slot].numpy()
+        for i in range(self.nfac):
+            h[i] = zd.z_draws(self.seed, s, i, self.q, self.r)
+        self.draw_s[s] = time.perf_counter() - t0
+
+    def request(self, s):
+        if s not in self.pending:
+            self.pending[s] = self.pool.submit(self._draw, s, s % 2)
+
+    def acquire(self, s):
+        """Device slot holding step s's Z, ordered before the compute stream's next work; starts
+        the host draw of step s + 1."""
+        import torch
+        slot = s % 2
+        self.request(s)
+        self.pending.pop(s).result()
+        cs = self.copy_stream
+        if self.freed[slot] is not None:
+            cs.wait_event(self.freed[slot])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(cs):
+            e0.record(cs)
+            self.dev[slot].copy_(self.host[slot], non_blocking=True)
+            e1.record(cs)
+        self.copied[slot] = e1
+        torch.cuda.current_stream().wait_event(e1)
+        self.h2d[s] = (e0, e1)
+        self.request(s + 1)
+        return slot
+
+    def release(self, slot):
+        """The compute stream's work on this slot is enqueued: the next copy into it waits for it."""
+        import torch
+        ev = torch.cuda.Event()
+        ev.record()
+        self.freed[slot] = ev
+
+    def report(self, steps):
+        """Host draw and copy time of the given steps (ms per step)."""
+        d = [self.draw_s[s] * 1e3 for s in steps if s in self.draw_s]
+        c = [self.h2d[s][0].elapsed_time(self.h2d[s][1]) for s in steps if s in self.h2d]
+        self.pool.shutdown(wait=True)
+        return {"z_bytes_per_step": self.nbytes,
+                "z_host_draw_ms_per_step": round(sum(d) / max(1, len(d)), 2),
+                "z_h2d_ms_per_step": round(sum(c) / max(1, len(c)), 3),
+                "z_h2d_gbs": round(self.nbytes * len(c) / max(1e-9, sum(c) * 1e-3) / 1e9, 1) if c else None,
+                "in_timed_window": True,
+                "how": "worker thread draws step s+1 on the host while step s runs; pinned buffer; "
+                       "copy on a side stream; the compute stream waits for it"}
+
+
+def omega_host_draw(seed, panels, r, F, sample=6):
+    """Host time of drawing one refresh's Gaussian panel inputs (Alg. 1 first step), estimated
+    from the first `sample` panels (float64 draws, cast to fp32) scaled by element count; the
+    timed steps build their panels on the device instead (rolled copies of one draw per row
+    count), so this is reported, not timed in the window."""
+    import zo_draws as zd
+    rows = list(panels)
+    tot = sum(rows) * r
+    take = rows[:sample]
+    t0 = time.perf_counter()
+    for k, rw in enumerate(take):
+        zd.f32(zd.draw(seed, "OMEGA_U", (999, k), (rw, r)))
+    dt = time.perf_counter() - t0
+    est = dt * tot / max(1, sum(take) * r)
+    return {"panels": len(rows), "elements": tot, "fp32_bytes": 4 * tot,
+            "host_draw_s_per_refresh_est": round(est, 3), "amortised_ms_per_step": round(est / F * 1e3, 2),
+            "sample": f"{len(take)} panels drawn, scaled by element count"}
+
+
+class ClockSampler:
+    """Graphics clock of GPU 0 sampled from the power-management firmware's metrics table (the
+    amdsmi library) every `period` seconds while `active` is set; None when the table cannot be
+    read."""
+
+    def __init__(self, period=0.2):
+        import threading
+        self.period = period
+        self.samples = []
+        self.active = threading.Event()
+        self.stop = threading.Event()
+        self.source = None
+        self.h = None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            hs = amdsmi.amdsmi_get_processor_handles()
+            self.h = hs[0] if hs else None
+            self.amdsmi = amdsmi
+        except Exception as e:  # pragma: no cover - depends on the machine
+            self.source = f"unavailable ({type(e).__name__})"
+        self.th = threading.Thread(target=self._run, daemon=True)
+        if self.h is not None:
+            self.th.start()
+
+    def _read(self):
+        a = self.amdsmi
+        try:
+            mt = a.amdsmi_get_gpu_metrics_info(self.h)
+            cl = mt.get("current_gfxclks")
+            vals = [v for v in (cl if isinstance(cl, (list, tuple)) else []) if isinstance(v, (int, float))
+                    and 0 < v < 10000]
+            if vals:
+                self.source = "amdsmi gpu_metrics current_gfxclks (mean over XCDs)"
+                return sum(vals) / len(vals)
+            for key in ("current_gfxclk", "average_gfxclk_frequency"):
+                v = mt.get(key)
+                if isinstance(v, (int, float)) and 0 < v < 10000:
+                    self.source = f"amdsmi gpu_metrics {key}"
+                    return float(v)
+        except Exception:
+            pass
+        try:
+            v = a.amdsmi_get_clock_info(self.h, a.AmdSmiClkType.GFX).get("clk")
+            if isinstance(v, (int, float)) and 0 < v < 10000:
+                self.source = "amdsmi clock_info GFX"
+                return float(v)
+        except Exception:
+            pass
+        return None
+
+    def _run(self):
+        while not self.stop.is_set():
+            if self.active.is_set():
+                v = self._read()
+                if v is not None:
+                    self.samples.append(v)
+            time.sleep(self.period)
+
+    def result(self):
+        self.stop.set()
+        if self.h is not None:
+            self.th.join(timeout=2)
+        if not self.samples:
+            return {"median_mhz": None, "samples": 0, "source": self.source}
+        s = sorted(self.samples)
+        return {"median_mhz": round(s[len(s) // 2], 1), "min_mhz": round(s[0], 1), "max_mhz": round(s[-1], 1),
+                "samples": len(s), "period_s": self.period, "source": self.source}
+
+
+def clock_fields(achieved, sclk):
+    """The MFMA peak at the observed clock (the datasheet figure is at 2.4 GHz) and the fraction
+    of it reached."""
+    mhz = sclk.get("median_mhz")
+    if not mhz:
+        return {}
+    peak = PEAK_BF16_TFLOPS * mhz / 2400.0
+    return {"peak_at_observed_sclk": round(peak, 1), "frac_at_observed_sclk": round(achieved / peak, 4)}
 
 
 def copy_calibration():
@@ -141,51 +327,107 @@ def practical_peaks(M, m, n, dt16):
             "inplace_rmw_2gib_gbs": round(2 * nbytes / ms_rmw / 1e6, 1)}
 
 
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        return 1
+
+
 def cpu_baseline(cfg, seed, budget_s, mat, lora, r, f16=False):
-    """The float64 oracle on a bounded sample of the same workload, on this host's cores."""
+    """The float64 oracle on bounded samples of the same workload, on this host's cores: the
+    perturbed linear (the metric's unit), the update (GB/s) and the refresh QR (ms per panel),
+    each also with one BLAS thread."""
     import numpy as np
     import oracle
     import zo_draws as zd
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
+        from threadpoolctl import threadpool_limits
     except Exception:  # pragma: no cover
-        threads = 1
+        threadpool_limits = None
+    threads = _blas_threads()
     T, q = cfg["T"], cfg["q"]
     m, n = mat[1], mat[2]
     rl, scale = zd.QWEN_LORA_RANK, zd.QWEN_LORA_ALPHA / zd.QWEN_LORA_RANK
     S = 256
     cast = zd.as_f16_values if f16 else zd.as_bf16_values
+    rnd = oracle.round_f16 if f16 else oracle.round_bf16
     W = cast(zd.draw(seed, "W0", (m, n), (m, n), 0.02))[1]
     X0 = cast(zd.draw(seed, "X", (T, n, 0), (S, n)))[1]
-    U, _ = np.linalg.qr(zd.draw(seed, "OMEGA_U", (0, m), (m, r)))
-    V, _ = np.linalg.qr(zd.draw(seed, "OMEGA_V", (0, n), (n, r)))
+    Om_U = zd.draw(seed, "OMEGA_U", (0, m), (m, r))
+    Om_V = zd.draw(seed, "OMEGA_V", (0, n), (n, r))
+    U, V = oracle.haar_qr(Om_U)[0], oracle.haar_qr(Om_V)[0]
     Z = zd.z_draws(seed, 0, 0, q, r).astype(np.float64)
-    flops = 0.0
-    nb = 0
-    t0 = time.perf_counter()
+    g = zd.draw(seed, "G", (0,), (q,))
     if lora:
         A = zd.f32(zd.draw(seed, "LORA_A", (0,), (rl, n), 0.02)).astype(np.float64)
         B = np.zeros((m, rl))
-        UA, _ = np.linalg.qr(zd.draw(seed, "OMEGA_U", (1, rl), (rl, r)))
-        VB, _ = np.linalg.qr(zd.draw(seed, "OMEGA_V", (1, rl), (rl, r)))
-    while time.perf_counter() - t0 < budget_s and nb < 4096:
-        j, s = (nb // 2) % q, (1 if nb % 2 == 0 else -1)
-        if lora:
-            oracle.lora_perturbed_linear(X0, W, A, UA, V, Z[j], B, U, VB, Z[(j + 1) % q], s, 1e-3, scale)
-            re = rl + r
-            flops += 2 * S * m * n + 2 * S * n * re + 2 * S * re * m + 2 * m * (2 * r * rl + 2 * rl * r)
-        else:
-            oracle.perturbed_linear(X0, W, U, V, Z[j], s, 1e-3)
-            flops += 2 * S * m * n + 2 * S * n * r + 2 * S * r * m + 2 * m * r * r
-        nb += 1
-    dt = time.perf_counter() - t0
+        UA = oracle.haar_qr(zd.draw(seed, "OMEGA_U", (1, rl), (rl, r)))[0]
+        VB = oracle.haar_qr(zd.draw(seed, "OMEGA_V", (1, rl), (rl, r)))[0]
+
+    def plinear_leg(budget, cap):
+        flops, nb = 0.0, 0
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < budget and nb < cap:
+            j, s = (nb // 2) % q, (1 if nb % 2 == 0 else -1)
+            if lora:
+                oracle.lora_perturbed_linear(X0, W, A, UA, V, Z[j], B, U, VB, Z[(j + 1) % q], s, 1e-3, scale)
+                re = rl + r
+                flops += 2 * S * m * n + 2 * S * n * re + 2 * S * re * m + 2 * m * (2 * r * rl + 2 * rl * r)
+            else:
+                oracle.perturbed_linear(X0, W, U, V, Z[j], s, 1e-3)
+                flops += 2 * S * m * n + 2 * S * n * r + 2 * S * r * m + 2 * m * r * r
+            nb += 1
+        return flops / (time.perf_counter() - t0) / 1e12, nb
+
+    M1 = np.zeros((r, r))
+    M2 = np.zeros((r, r))
+    if lora:  # the updated matrices are the fp32 adapter factors; A (rl x n) stands for them
+        Wu, Uu, Vu, ubytes = A, UA, V, update_bytes(rl, n, r, q, 4)
+        rnd = zd.f32
+    else:
+        Wu, Uu, Vu, ubytes = W, U, V, update_bytes(m, n, r, q)
+
+    def update_leg(budget):
+        k = 0
+        t0 = time.perf_counter()
+        while k < 1 or time.perf_counter() - t0 < budget:
+            out = oracle.subspace_adam_update(Wu, Uu, Vu, Z, g, M1, M2, 1, 1e-3, 0.9, 0.95, 1e-8)
+            rnd(out["W"])
+            k += 1
+        return ubytes * k / (time.perf_counter() - t0) / 1e9, k
+
+    def qr_leg(budget):
+        k = 0
+        t0 = time.perf_counter()
+        while k < 2 or time.perf_counter() - t0 < budget:
+            oracle.haar_qr(Om_U if k % 2 == 0 else Om_V)
+            k += 1
+        return (time.perf_counter() - t0) / k * 1e3, k
+
+    pl, nb = plinear_leg(budget_s * 0.45, 4096)
+    ug, nu = update_leg(budget_s * 0.15)
+    qm, nq = qr_leg(budget_s * 0.1)
+    one = None
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1, user_api="blas"):
+            pl1, nb1 = plinear_leg(budget_s * 0.15, 4096)
+            ug1, nu1 = update_leg(budget_s * 0.08)
+            qm1, nq1 = qr_leg(budget_s * 0.07)
+        one = {"value": pl1, "update_gbs": round(ug1, 3), "qr_ms_per_panel": round(qm1, 2),
+               "sample": f"{nb1} query blocks, {nu1} updates, {nq1} panels"}
     what = ("materialised A', B' and W + scale B' A', then X W'^T" if lora
             else "materialised W + s eps U Z V^T, then X W'^T")
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"float64 oracle ({what}) on {nb} query blocks "
-                      f"x {S} token rows of the {m}x{n} layer; algorithmic FLOPs of that sample / {dt:.1f} s; "
-                      f"{len(os.sched_getaffinity(0))} host cores visible"}
+    return {"value": pl, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "cores_visible": len(os.sched_getaffinity(0)),
+            "update_gbs": round(ug, 3), "qr_ms_per_panel": round(qm, 2),
+            "one_thread": one,
+            "sample": f"float64 oracle: perturbed linear ({what}) on {nb} query blocks x {S} token rows of "
+                      f"the {m}x{n} layer, algorithmic FLOPs / time; update (Zbar, Adam, W - lr U S V^T, "
+                      f"rounding to the stored type) of {'the ' + str(rl) + 'x' + str(n) + ' adapter factor A' if lora else 'that matrix'} {nu} times, algorithmic bytes {ubytes} each / time; "
+                      f"Householder QR with sign fix of the {m}x{r} and {n}x{r} panels, {nq} panels; "
+                      f"cores = BLAS threads used; one_thread = the same legs with one BLAS thread"}
 
 
 def attention_flops(T, seq_len, heads, dh, nblk):
@@ -273,22 +515,22 @@ def run_decoder(args):
                             ln2_gamma=g[2].contiguous(), ln2_beta=(g[3] - 1.0).contiguous()))
     del Wbase, Obase
     nmat = nper * layers
-    Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(nmat)])
-                                   for t in range(nsteps)])).to(dev)  # [step, matrix, q, r, r]
+    zfeed = ZFeed(seed, nmat, q, r, dev)
+    Z = zfeed.dev  # [slot][matrix, q, r, r]
     H0 = to16(zd.draw(seed, "X", (T, d, 0), (T, d)))
     Ystar = to16(zd.draw(seed, "X", (T, d, 1), (T, d)))
     Hbuf = [torch.empty((nblk * T, d), dtype=dt16, device=dev) for _ in range(2)]
 
     def layer_obj(t, l):
-        lm = {nm: dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, nper * l + i])
+        lm = {nm: dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t][nper * l + i])
               for i, (nm, u) in enumerate(mats[l].items())}
         if llama:
             return zo.LlamaLayer(lm, lns[l], bq, bs, eps, T, L, heads)
         return zo.DecoderLayer(lm, lns[l], bq, bs, eps, T, L, heads)
 
-    decs = [[layer_obj(t, l) for l in range(layers)] for t in range(nsteps)]
-    items = [[dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, nper * l + i], M1=u["M1"], M2=u["M2"])
-              for l in range(layers) for i, u in enumerate(mats[l].values())] for t in range(nsteps)]
+    decs = [[layer_obj(sl, l) for l in range(layers)] for sl in range(2)]
+    items = [[dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[sl][nper * l + i], M1=u["M1"], M2=u["M2"])
+              for l in range(layers) for i, u in enumerate(mats[l].values())] for sl in range(2)]
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s; {layers} decoder layers; "
         f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB on device")
@@ -297,6 +539,7 @@ def run_decoder(args):
 
     def step(t, s):
         rec = {"layers": [], "upd": None, "refresh": None}
+        s = zfeed.acquire(s)
         if t % F == 0:
             e0, e1 = Ev(), Ev()
             e0.record()
@@ -316,6 +559,7 @@ def run_decoder(args):
         e0.record()
         zo.subspace_adam_update(items[s], g, t + 1, lr, b1, b2, ea)
         e1.record()
+        zfeed.release(s)
         rec["upd"] = (e0, e1)
         return rec
 
@@ -327,13 +571,18 @@ def run_decoder(args):
         for u in lm.values():
             u["M1"].zero_()
             u["M2"].zero_()
+    zfeed.request(args.warmup)
     torch.cuda.synchronize()
+    args.clk.active.set()
     t0 = time.perf_counter()
     for k in range(args.steps):
         recs.append(step(k, args.warmup + k))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    args.clk.active.clear()
     log(f"timed {args.steps} steps in {t1 - t0:.2f} s")
+    sclk = args.clk.result()
+    draws = zfeed.report(range(args.warmup, args.warmup + args.steps))
 
     lin_layer = sum(plinear_flops(T, m, n, r, q, nblk, nsigned) for m, n in shapes.values())
     att_layer = attention_flops(T, L, heads, d // heads, nblk)
@@ -369,7 +618,9 @@ def run_decoder(args):
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "launches": len(layer_ms), "avg_launch_ms": round(avg_layer, 4),
-                     "flops_per_launch_avg": lin_layer + att_layer},
+                     "flops_per_launch_avg": lin_layer + att_layer, **clock_fields(achieved, sclk)},
+        "sclk_timed_window": sclk,
+        "host_draws": draws,
         "attention_flops_per_layer": att_layer,
         "update": {"kernel": "zo_subspace_adam_update (k_adam_rr + k_us + k_update_bf16)", "bound": "hbm",
                    "achieved": round(upd_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
@@ -445,8 +696,8 @@ def run_decoder_lora(args, cfg, dec):
         g = f32dev(1.0 + 0.05 * zd.draw(seed, "W0", (l, 1), (2, d)))
         norms.append(dict(rms1_gamma=g[0].contiguous(), rms2_gamma=g[1].contiguous()))
     del Wbase, Obase
-    Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(len(factors))])
-                                   for t in range(nsteps)])).to(dev)  # [step, factor, q, r, r]
+    zfeed = ZFeed(seed, len(factors), q, r, dev)
+    Z = zfeed.dev  # [slot][factor, q, r, r]
     H0 = to16(zd.draw(seed, "X", (T, d, 0), (T, d)))
     Ystar = to16(zd.draw(seed, "X", (T, d, 1), (T, d)))
     Hbuf = [torch.empty((nblk * T, d), dtype=dt16, device=dev) for _ in range(2)]
@@ -457,8 +708,8 @@ def run_decoder_lora(args, cfg, dec):
         lm = {}
         for nm, u in mats[l].items():
             if nm in ("q", "v"):
-                lm[nm] = dict(W=u["W"], A=u["A"], UA=u["UA"], VA=u["VA"], ZA=Z[t, u["zi"]], B=u["B"], UB=u["UB"],
-                              VB=u["VB"], ZB=Z[t, u["zi"] + 1])
+                lm[nm] = dict(W=u["W"], A=u["A"], UA=u["UA"], VA=u["VA"], ZA=Z[t][u["zi"]], B=u["B"], UB=u["UB"],
+                              VB=u["VB"], ZB=Z[t][u["zi"] + 1])
             else:
                 lm[nm] = dict(W=u["W"])
         o = zo.LlamaLoraLayer(lm, norms[l], bq, bs, eps, scale, T, L, heads, kv, rope_base=dec["rope_base"],
@@ -466,9 +717,9 @@ def run_decoder_lora(args, cfg, dec):
         ws = o.ws
         return o
 
-    decs = [[layer_obj(t, l) for l in range(layers)] for t in range(nsteps)]
-    items = [[dict(W=f["W"], U=f["U"], V=f["V"], Z=Z[t, f["z"]], M1=f["M1"], M2=f["M2"]) for f in factors]
-             for t in range(nsteps)]
+    decs = [[layer_obj(sl, l) for l in range(layers)] for sl in range(2)]
+    items = [[dict(W=f["W"], U=f["U"], V=f["V"], Z=Z[sl][f["z"]], M1=f["M1"], M2=f["M2"]) for f in factors]
+             for sl in range(2)]
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s; {layers} LoRA-scheme layers; "
         f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB on device")
@@ -477,6 +728,7 @@ def run_decoder_lora(args, cfg, dec):
 
     def step(t, s):
         rec = {"layers": [], "upd": None, "refresh": None}
+        s = zfeed.acquire(s)
         if t % F == 0:
             e0, e1 = Ev(), Ev()
             e0.record()
@@ -496,6 +748,7 @@ def run_decoder_lora(args, cfg, dec):
         e0.record()
         zo.subspace_adam_update(items[s], g, t + 1, lr, b1, b2, ea)
         e1.record()
+        zfeed.release(s)
         rec["upd"] = (e0, e1)
         return rec
 
@@ -506,13 +759,18 @@ def run_decoder_lora(args, cfg, dec):
     for f in factors:
         f["M1"].zero_()
         f["M2"].zero_()
+    zfeed.request(args.warmup)
     torch.cuda.synchronize()
+    args.clk.active.set()
     t0 = time.perf_counter()
     for k in range(args.steps):
         recs.append(step(k, args.warmup + k))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    args.clk.active.clear()
     log(f"timed {args.steps} steps in {t1 - t0:.2f} s")
+    sclk = args.clk.result()
+    draws = zfeed.report(range(args.warmup, args.warmup + args.steps))
 
     lin_layer = (lora_flops(T, d, d, rl, r, q, nblk, nsigned) + lora_flops(T, dkv, d, rl, r, q, nblk, nsigned)
                  + sum(nblk * 2 * T * m * n for nm, (m, n) in shapes.items() if nm not in ("q", "v")))
@@ -544,7 +802,9 @@ def run_decoder_lora(args, cfg, dec):
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "launches": len(layer_ms), "avg_launch_ms": round(avg_layer, 4),
-                     "flops_per_launch_avg": lin_layer + att_layer},
+                     "flops_per_launch_avg": lin_layer + att_layer, **clock_fields(achieved, sclk)},
+        "sclk_timed_window": sclk,
+        "host_draws": draws,
         "attention_flops_per_layer": att_layer,
         "update": {"kernel": "zo_subspace_adam_update on the fp32 adapter factors (latency-bound)", "bound": "hbm",
                    "achieved": round(upd_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
@@ -595,6 +855,7 @@ def main():
         return
     torch.cuda.set_device(0)
     zo.lib()
+    args.clk = clk = ClockSampler()
     if args.model == "decoder":
         run_decoder(args)
         return
@@ -668,10 +929,9 @@ def main():
                 u["mom"] = [(zeros_rr(), zeros_rr())]
             units.append(u)
     del Wbase, Obase
-    nsteps = args.warmup + args.steps
     zper = 2 if lora else 1  # coefficient sets per unit (one per perturbed factor)
-    Z = torch.from_numpy(np.stack([np.stack([zd.z_draws(seed, t, i, q, r) for i in range(zper * len(units))])
-                                   for t in range(nsteps)])).to(dev)  # [step, factor, q, r, r]
+    zfeed = ZFeed(seed, zper * len(units), q, r, dev)
+    Z = zfeed.dev  # [slot][factor, q, r, r]
     m_last = unit_mats[-1][1]
     Ystar = to_bf16(zd.draw(seed, "X", (T, m_last, 1), (T, m_last)))
     if lora:
@@ -692,24 +952,24 @@ def main():
 
     def make_layer(t, i, u):
         if lora:
-            return zo.LoraPerturbedLinear(X[u["n"]], u["W"], u["A"], u["UA"], u["VA"], Z[t, 2 * i], u["B"], u["UB"],
-                                          u["VB"], Z[t, 2 * i + 1], bq, bs, eps, scale, T,
+            return zo.LoraPerturbedLinear(X[u["n"]], u["W"], u["A"], u["UA"], u["VA"], Z[t][2 * i], u["B"], u["UB"],
+                                          u["VB"], Z[t][2 * i + 1], bq, bs, eps, scale, T,
                                           x_block_stride=T * u["n"], Y=Y[u["m"]], workspace=ws)
         k = i % len(unit_mats)
-        return zo.PerturbedLinear(X[u["n"]], u["W"], u["U"], u["V"], Z[t, i], bq, bs, eps, T,
+        return zo.PerturbedLinear(X[u["n"]], u["W"], u["U"], u["V"], Z[t][i], bq, bs, eps, T,
                                   x_block_stride=T * u["n"], Y=Y[u["m"]],
                                   workspace=wsets[k] if grouped and k < 3 else ws)
 
     def make_items(t, i, u):
         if lora:
             (a1, a2), (c1, c2) = u["mom"]
-            return [dict(W=u["A"], U=u["UA"], V=u["VA"], Z=Z[t, 2 * i], M1=a1, M2=a2),
-                    dict(W=u["B"], U=u["UB"], V=u["VB"], Z=Z[t, 2 * i + 1], M1=c1, M2=c2)]
+            return [dict(W=u["A"], U=u["UA"], V=u["VA"], Z=Z[t][2 * i], M1=a1, M2=a2),
+                    dict(W=u["B"], U=u["UB"], V=u["VB"], Z=Z[t][2 * i + 1], M1=c1, M2=c2)]
         (m1, m2), = u["mom"]
-        return [dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t, i], M1=m1, M2=m2)]
+        return [dict(W=u["W"], U=u["U"], V=u["V"], Z=Z[t][i], M1=m1, M2=m2)]
 
-    plins = [[make_layer(t, i, u) for i, u in enumerate(units)] for t in range(nsteps)]
-    items = [[it for i, u in enumerate(units) for it in make_items(t, i, u)] for t in range(nsteps)]
+    plins = [[make_layer(sl, i, u) for i, u in enumerate(units)] for sl in range(2)]
+    items = [[it for i, u in enumerate(units) for it in make_items(sl, i, u)] for sl in range(2)]
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s; {len(units)} perturbed layers; "
         f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB on device")
@@ -718,8 +978,9 @@ def main():
     recs = []
 
     def step(t, s):
-        """One SubZero+ step; s indexes the pre-drawn Z (step t of the run)."""
+        """One SubZero+ step; s keys the step's Z draws (step t of the run)."""
         rec = {"gemm": [], "prep": [], "upd": None, "refresh": None}
+        s = zfeed.acquire(s)
         if t % F == 0:
             e0, e1 = Ev(), Ev()
             e0.record()
@@ -751,6 +1012,7 @@ def main():
         e0.record()
         zo.subspace_adam_update(items[s], g, t + 1, lr, b1, b2, ea)
         e1.record()
+        zfeed.release(s)
         rec["upd"] = (e0, e1)
         return rec
 
@@ -764,13 +1026,19 @@ def main():
         for m1, m2 in u["mom"]:
             m1.zero_()
             m2.zero_()
+    zfeed.request(args.warmup)
     torch.cuda.synchronize()
+    clk.active.set()
     t0 = time.perf_counter()
     for k in range(args.steps):
         recs.append(step(k, args.warmup + k))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    clk.active.clear()
     log(f"timed {args.steps} steps in {t1 - t0:.2f} s")
+    sclk = clk.result()
+    draws = zfeed.report(range(args.warmup, args.warmup + args.steps))
+    draws["omega"] = omega_host_draw(seed, [rw for o in omegas for rw in [o.shape[0]]], r, F)
 
     if lora:
         layer_flops = lambda m, n: lora_flops(T, m, n, rl, r, q, nblk, nsigned)
@@ -822,7 +1090,9 @@ def main():
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "launches": n_gemm, "avg_launch_ms": round(gemm_ms / n_gemm, 4),
-                     "flops_per_launch_avg": gemm_flops / n_gemm},
+                     "flops_per_launch_avg": gemm_flops / n_gemm, **clock_fields(achieved, sclk)},
+        "sclk_timed_window": sclk,
+        "host_draws": draws,
         "update": {"kernel": "zo_subspace_adam_update (k_adam_rr + k_us + "
                              + ("k_update_f32, fp32 adapter factors)" if lora else "k_update_bf16)"), "bound": "hbm",
                    "achieved": round(upd_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",

@@ -845,9 +845,10 @@ def subspace_adam_update(items: Sequence[dict], g: torch.Tensor, t: int, lr: flo
         _need(nonfinite_flag, "nonfinite_flag", torch.int32, 1)
     L = lib()
     ws_n = L.zo_subspace_adam_update_workspace(n, arr, r, q, dt)
-    if ws_n == 0:
+    if ws_n == 0:  # the arguments failed validation: the call (which launches nothing) says why
         _check(L.zo_subspace_adam_update(n, arr, dt, r, q, g.data_ptr(), t, lr, beta1, beta2,
                                          eps_adam, None, None, 0, None))
+        return
     ws = Workspace.get(ws_n)
     _check(L.zo_subspace_adam_update(n, arr, dt, r, q, g.data_ptr(), int(t), float(lr), float(beta1),
                                      float(beta2), float(eps_adam), _ptr(nonfinite_flag), ws.data_ptr(),
@@ -866,8 +867,9 @@ def subspace_sgd_update(items: Sequence[dict], g: torch.Tensor, lr: float,
         _need(nonfinite_flag, "nonfinite_flag", torch.int32, 1)
     L = lib()
     ws_n = L.zo_subspace_sgd_update_workspace(n, arr, r, q, dt)
-    if ws_n == 0:
+    if ws_n == 0:  # the arguments failed validation: the call (which launches nothing) says why
         _check(L.zo_subspace_sgd_update(n, arr, dt, r, q, g.data_ptr(), lr, None, None, 0, None))
+        return
     ws = Workspace.get(ws_n)
     _check(L.zo_subspace_sgd_update(n, arr, dt, r, q, g.data_ptr(), float(lr), _ptr(nonfinite_flag),
                                     ws.data_ptr(), ws.numel(), _stream_handle()))

@@ -122,6 +122,43 @@ __device__ __forceinline__ void mul4_silu(const char* base, size_t idx, float& v
 
 // The fused epilogue on four fp32 accumulator values, then the store: ReLU, the residual R
 // (same layout as Y) added, or the product with silu(R), before the single rounding to OUT.
+// Eight OUT-typed values at element idx.. as fp32 (16-bit: one 16-byte load; fp32: element
+// loads, since an fp32 R need only be 4-byte aligned).
+template <int OUT>
+__device__ __forceinline__ void load8(const char* base, size_t idx, float* v) {
+  if constexpr (OUT == ZO_F32) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = ((const float*)base)[idx + e];
+  } else {
+    const u32x4 r = *(const u32x4*)(base + idx * 2);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (OUT == ZO_BF16) {
+        v[2 * e] = bf16_to_f32((bf16_t)r[e]);
+        v[2 * e + 1] = bf16_to_f32((bf16_t)(r[e] >> 16));
+      } else {
+        v[2 * e] = f16_to_f32((uint16_t)r[e]);
+        v[2 * e + 1] = f16_to_f32((uint16_t)(r[e] >> 16));
+      }
+    }
+  }
+}
+
+// Eight fp32 values stored as OUT at element idx.. (idx a multiple of 8, 16-byte aligned rows).
+template <int OUT>
+__device__ __forceinline__ void store8(char* base, size_t idx, const float* v) {
+  if constexpr (OUT == ZO_F32) {
+    *(f32x4*)(base + idx * 4) = (f32x4){v[0], v[1], v[2], v[3]};
+    *(f32x4*)(base + idx * 4 + 16) = (f32x4){v[4], v[5], v[6], v[7]};
+  } else if constexpr (OUT == ZO_BF16) {
+    *(u32x4*)(base + idx * 2) = (u32x4){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                        pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+  } else {
+    *(u32x4*)(base + idx * 2) = (u32x4){pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3]),
+                                        pack_f16x2(v[4], v[5]), pack_f16x2(v[6], v[7])};
+  }
+}
+
 template <int OUT, int EPI>
 __device__ __forceinline__ void finish4(char* Yb, const char* Rb, size_t idx, float v0, float v1,
                                         float v2, float v3) {
@@ -796,8 +833,37 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     __builtin_amdgcn_sched_barrier(0);
     substep(F1a, F1b, na, nb, 0, F0a, F0b, [&](int i) { load1_B(sa, k + 2, i); }, f16);
   };
+  // One load (i of 8) of part A / B of tile t (either segment; t < NT) into slot sl.  The
+  // segment is a uniform choice: scalar selects of the descriptor and k offset, one VALU select
+  // of the row offset.
+  const __amdgpu_buffer_rsrc_t rsC = make_rsrc(Cblk, (unsigned)a.rows_a * a.rc * 2);
+  const __amdgpu_buffer_rsrc_t rsD = make_rsrc(Dblk, (unsigned)a.rows_b * a.rc * 2);
+  auto load1g_A = [&](int sl, int t, int i) {
+    const bool m = t < NTM;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(m ? rsA : rsC, (lds_ptr_t)(ldsw + sl * PART + 32 * RB * i), 16,
+                                             m ? voA[i] : voC[i], (unsigned)(m ? t : t - NTM) * 128u, 0, 0);
+  };
+  auto load1g_B = [&](int sl, int t, int i) {
+    const bool m = t < NTM;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(m ? rsB : rsD, (lds_ptr_t)(ldsw + sl * PART + 32 * RB * i), 16,
+                                             m ? voB[i] : voD[i], (unsigned)(m ? t : t - NTM) * 128u, 0, 0);
+  };
+  // Tile k as body_main, with run-time slots and loads from either segment: the tiles that
+  // follow the unrolled main loop (the last main tiles and the rank segment), up to NT - 3.
+  // Needs tile k full and tiles k + 1, k + 2 to exist.
+  auto body_rt = [&](int k, auto f16) {
+    const int sa = (2 * k) % 5, sb = (2 * k + 1) % 5;
+    const int na = (2 * k + 2) % 5, nb = (2 * k + 3) % 5, a2 = (2 * k + 4) % 5;
+    substep(F0a, F0b, sa, sb, 1, F1a, F1b, [&](int i) { load1g_B(nb, k + 1, 4 + i); }, f16);
+    substep(F1a, F1b, sa, sb, 2, F0a, F0b, [&](int i) { load1g_A(a2, k + 2, i); }, f16);
+    substep(F0a, F0b, sa, sb, 3, F1a, F1b, [&](int i) { load1g_A(a2, k + 2, 4 + i); }, f16);
+    asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");  // all but A(k+2)
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    substep(F1a, F1b, na, nb, 0, F0a, F0b, [&](int i) { load1g_B(sa, k + 2, i); }, f16);
+  };
   // Any tile (run-time slots, loads of either segment or none, half tiles).  The loads go out
-  // together here: only the last few tiles take this path.
+  // together here: only the last two tiles and half tiles take this path.
   auto body_any = [&](int k, auto f16) {
     const int sa = (2 * k) % 5, sb = (2 * k + 1) % 5, na = (2 * k + 2) % 5, nb = (2 * k + 3) % 5;
     const int a2 = (2 * k + 4) % 5;
@@ -834,24 +900,101 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     body_main(k + 3, std::integral_constant<int, 3>{}, MT{});
     body_main(k + 4, std::integral_constant<int, 4>{}, MT{});
   }
+  // The rest: body_rt while the tile is full and two more follow, else body_any (only a
+  // segment's last tile can be a half tile).
+  const int e1 = min(halfM ? NTM - 1 : NTM, NT - 2);
+  for (; k < e1; ++k) body_rt(k, MT{});
   for (; k < NTM; ++k) body_any(k, MT{});
+  for (; k < NT - 2; ++k) body_rt(k, std::false_type{});
   for (; k < NT; ++k) body_any(k, std::false_type{});
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain before the stores and exit
 
+  // Epilogue through LDS.  The accumulator layout gives each lane 4 adjacent outputs of one
+  // token, so stores straight from the registers would touch 32 token rows per instruction
+  // with 16 bytes each; staged through the (now free) ring, every lane writes 16 contiguous
+  // bytes and a wave's store covers 8 rows x 128 bytes.  16-bit outputs without R are rounded
+  // once and staged as stored (256 token rows of 512 bytes); otherwise the fp32 values are
+  // staged in two halves of 128 token rows of 1 KB, and R is applied to them before the single
+  // rounding.  Rows are padded by 16 bytes (pitch 528 / 1040), so the read-back (8 consecutive
+  // rows at one 16-byte chunk) is conflict free and every lane's staging addresses are one base
+  // register plus immediates.
   char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (OUT == ZO_F32 ? 4 : 2);
   const char* Rb = (const char*)a.R + (long long)blk * a.r_block_stride * (OUT == ZO_F32 ? 4 : 2);
+  const int lr8 = lane & 7, lc8 = lane >> 3;
+  __syncthreads();  // every wave is past its last fragment reads: the ring is free
+  __builtin_amdgcn_sched_barrier(0);  // nothing of the epilogue moves above the barrier
+  if constexpr (OUT != ZO_F32 && (EPI == ZO_EPI_NONE || EPI == ZO_EPI_RELU)) {
+    constexpr int PITCH = 528;
+    // Token row wn 128 + 32 j + fr, columns wm 128 + 32 i + 8 q4 + 4 fh .. + 3.
+    char* const wb = lds + (wn * 128 + fr) * PITCH + wm * 256 + fh * 8;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int tok = t0 + wn * 128 + j * 32 + fr;
-    if (tok >= a.rows_b) continue;
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int col = m0 + wm * 128 + i * 32 + q4 * 8 + fh * 4;
-        if (col >= a.rows_a) continue;
-        finish4<OUT, EPI>(Yb, Rb, (size_t)tok * a.ldy + col, acc[i][j][q4 * 4 + 0],
-                          acc[i][j][q4 * 4 + 1], acc[i][j][q4 * 4 + 2], acc[i][j][q4 * 4 + 3]);
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = acc[i][j][q4 * 4 + e];
+            if constexpr (EPI == ZO_EPI_RELU) v[e] = fmaxf(v[e], 0.f);
+          }
+          *(u32x2*)(wb + j * 32 * PITCH + (i * 4 + q4) * 16) =
+              OUT == ZO_BF16 ? (u32x2){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])}
+                             : (u32x2){pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3])};
+        }
+    __syncthreads();
+    // Pass it of wave w: rows 8 it + lr8, 16-byte chunk 8 w + lc8 (columns 64 w + 8 lc8 ..).
+    const char* const rb = lds + lr8 * PITCH + (wave * 8 + lc8) * 16;
+    const int col = m0 + (wave * 8 + lc8) * 8;
+#pragma unroll 8
+    for (int it = 0; it < 32; ++it) {
+      const u32x4 v = *(const u32x4*)(rb + it * 8 * PITCH);
+      const int tok = t0 + it * 8 + lr8;
+      if (tok < a.rows_b && col < a.rows_a) *(u32x4*)(Yb + ((size_t)tok * a.ldy + col) * 2) = v;
+    }
+  } else {
+    constexpr int PITCH = 1040;
+    // Half h holds j = 2 h, 2 h + 1: staging row wn 64 + 32 (j % 2) + fr is tile token
+    // wn 128 + 32 j + fr; 16-byte chunk wm 32 + 8 i + 2 q4 + fh holds its columns 4 chunk .. + 3.
+    char* const wb = lds + (wn * 64 + fr) * PITCH + wm * 512 + fh * 16;
+    // Read-back pass it of wave w: staging rows 8 it + lr8, columns 64 w + 8 lc8 .. + 7.
+    const char* const rb = lds + lr8 * PITCH + (wave * 8 + lc8) * 32;
+    const int col = m0 + (wave * 8 + lc8) * 8;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h) __syncthreads();  // the first half's read-back is done
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const f32x16& c = acc[i][2 * h + jj];
+            *(f32x4*)(wb + jj * 32 * PITCH + (i * 8 + q4 * 2) * 16) =
+                (f32x4){c[q4 * 4 + 0], c[q4 * 4 + 1], c[q4 * 4 + 2], c[q4 * 4 + 3]};
+          }
+      __syncthreads();
+#pragma unroll 4
+      for (int it = 0; it < 16; ++it) {
+        const int sr = it * 8 + lr8;
+        const f32x4 lo = *(const f32x4*)(rb + it * 8 * PITCH);
+        const f32x4 hi = *(const f32x4*)(rb + it * 8 * PITCH + 16);
+        const int tok = t0 + (sr >> 6) * 128 + h * 64 + (sr & 63);
+        if (tok >= a.rows_b || col >= a.rows_a) continue;
+        const size_t idx = (size_t)tok * a.ldy + col;
+        float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        if constexpr (EPI != ZO_EPI_NONE) {
+          float rv[8];
+          if constexpr (EPI == ZO_EPI_RESIDUAL || EPI == ZO_EPI_SILU_MUL) load8<OUT>(Rb, idx, rv);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if constexpr (EPI == ZO_EPI_RELU) v[e] = fmaxf(v[e], 0.f);
+            else if constexpr (EPI == ZO_EPI_RESIDUAL) v[e] += rv[e];
+            else v[e] *= silu(rv[e]);
+          }
+        }
+        store8<OUT>(Yb, idx, v);
       }
     }
   }
