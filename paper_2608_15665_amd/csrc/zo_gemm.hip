@@ -912,12 +912,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   // Epilogue through LDS.  The accumulator layout gives each lane 4 adjacent outputs of one
   // token, so stores straight from the registers would touch 32 token rows per instruction
   // with 16 bytes each; staged through the (now free) ring, every lane writes 16 contiguous
-  // bytes and a wave's store covers 8 rows x 128 bytes.  16-bit outputs without R are rounded
+  // bytes and a wave's store covers whole rows.  16-bit outputs without R are rounded
   // once and staged as stored (256 token rows of 512 bytes); otherwise the fp32 values are
   // staged in two halves of 128 token rows of 1 KB, and R is applied to them before the single
-  // rounding.  Rows are padded by 16 bytes (pitch 528 / 1040), so the read-back (8 consecutive
-  // rows at one 16-byte chunk) is conflict free and every lane's staging addresses are one base
-  // register plus immediates.
+  // rounding.  Rows are padded by 16 bytes (pitch 528 / 1040), so that the writes (8 consecutive
+  // rows at one chunk per 8 lanes) spread over the banks and every lane's staging addresses are
+  // one base register plus immediates.
   char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (OUT == ZO_F32 ? 4 : 2);
   const char* Rb = (const char*)a.R + (long long)blk * a.r_block_stride * (OUT == ZO_F32 ? 4 : 2);
   const int lr8 = lane & 7, lc8 = lane >> 3;
@@ -944,13 +944,15 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
                              : (u32x2){pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3])};
         }
     __syncthreads();
-    // Pass it of wave w: rows 8 it + lr8, 16-byte chunk 8 w + lc8 (columns 64 w + 8 lc8 ..).
-    const char* const rb = lds + lr8 * PITCH + (wave * 8 + lc8) * 16;
-    const int col = m0 + (wave * 8 + lc8) * 8;
+    // Pass it of wave w: rows 8 it + 2 w + lane / 32, whole (512 bytes each), 16-byte chunk
+    // lane % 32 (columns 8 (lane % 32) ..).
+    const int half = lane >> 5, ch = lane & 31;
+    const char* const rb = lds + (2 * wave + half) * PITCH + ch * 16;
+    const int col = m0 + ch * 8;
 #pragma unroll 8
     for (int it = 0; it < 32; ++it) {
       const u32x4 v = *(const u32x4*)(rb + it * 8 * PITCH);
-      const int tok = t0 + it * 8 + lr8;
+      const int tok = t0 + it * 8 + 2 * wave + half;
       if (tok < a.rows_b && col < a.rows_a) *(u32x4*)(Yb + ((size_t)tok * a.ldy + col) * 2) = v;
     }
   } else {
