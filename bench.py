@@ -290,6 +290,61 @@ def copy_calibration():
                       "launches": 3}))
 
 
+def shared_x_report(seed, T, m, n, r, q, nblk, dt, label, reps=5):
+    """The shared-X variant (one X read by every block: the first layer's q, k, v, or the Tiny
+    layer): X W^T once, then each block's rank-r term.  Timed as prepare + apply, and the apply
+    alone against the two-term roofline max(MFMA time of one X W^T at the datasheet peak, HBM
+    time of X, W and the nblk outputs at 8 TB/s).  For comparison, the same problem with X
+    copied into every block (the per-block path, X W^T nblk times)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_15665_amd as zo
+    import zo_draws as zd
+    dev = "cuda"
+    es = 4 if dt == torch.float32 else 2
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    X = torch.randn(T, n, device=dev, generator=g).to(dt)
+    W = (0.02 * torch.randn(m, n, device=dev, generator=g)).to(dt)
+    U = torch.linalg.qr(torch.randn(m, r, device=dev, generator=g))[0].contiguous()
+    V = torch.linalg.qr(torch.randn(n, r, device=dev, generator=g))[0].contiguous()
+    Z = torch.from_numpy(zd.z_draws(seed, 0, 0, q, r)).to(dev)
+    bq, bs = [b // 2 for b in range(nblk)], [1 if b % 2 == 0 else -1 for b in range(nblk)]
+    Xr = X.repeat(nblk, 1).contiguous()
+
+    def timed(pl, what):
+        pl.prepare()
+        pl.apply()
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record()
+        for _ in range(reps):
+            pl.prepare()
+        e[1].record()
+        for _ in range(reps):
+            pl.apply()
+        e[2].record()
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / reps, e[1].elapsed_time(e[2]) / reps
+
+    shared = zo.PerturbedLinear(X, W, U, V, Z, bq, bs, 1e-3, T, x_block_stride=0)
+    prep_ms, app_ms = timed(shared, "shared")
+    per_block = zo.PerturbedLinear(Xr, W, U, V, Z, bq, bs, 1e-3, T, x_block_stride=T * n)
+    pb_prep, pb_app = timed(per_block, "per-block")
+    peak = PEAK_BF16_TFLOPS if es == 2 else 157.3
+    flops = 2.0 * T * m * n + 2.0 * T * n * r + nblk * 2.0 * T * r * m
+    nbytes = es * (T * n + m * n + nblk * T * m)
+    ideal_ms = max(2.0 * T * m * n / (peak * 1e9), nbytes / (PEAK_HBM_GBPS * 1e6))
+    del X, W, Xr, shared, per_block
+    torch.cuda.empty_cache()
+    return {"shape": f"{label}: T={T} x m={m} x n={n}, r={r}, {nblk} blocks, {'fp32' if es == 4 else 'bf16'}",
+            "apply_ms": round(app_ms, 4), "prepare_ms": round(prep_ms, 4),
+            "two_term_ideal_ms": round(ideal_ms, 4), "frac_of_two_term": round(ideal_ms / app_ms, 4),
+            "algorithmic_tflops": round(flops / (app_ms * 1e-3) / 1e12, 2),
+            "per_block_path_apply_ms": round(pb_app, 4), "speedup_vs_per_block": round(pb_app / app_ms, 2)}
+
+
 def practical_peaks(M, m, n, dt16):
     """What library kernels reach on this GPU in the same run: a plain GEMM of one of the
     workload's shapes (torch.matmul, i.e. hipBLASLt), a 2 GiB device copy and a 2 GiB in-place
@@ -1107,6 +1162,12 @@ def main():
     if not args.no_peaks:
         _, m0, n0 = unit_mats[0]
         out["practical_peaks"] = practical_peaks(nblk * T, m0, n0, dt16)
+        if not lora:
+            tc = zd.TINY
+            out["shared_x"] = [
+                shared_x_report(seed, T, m0, n0, r, q, nblk, dt16, "first layer's q/k/v shape"),
+                shared_x_report(seed, tc["T"], tc["m"], tc["n"], tc["r"], tc["q"], 2 * tc["q"], torch.float32,
+                                "Tiny layer")]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, seed, args.cpu_budget, unit_mats[0], lora, r, f16)
     print(json.dumps(out), flush=True)

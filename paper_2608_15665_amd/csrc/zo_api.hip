@@ -469,14 +469,17 @@ struct DecoderWs {
   char *A, *Qb, *Kb, *Vb, *C, *H2, *F, *lin[3], *grp;
   size_t total;
 };
-// The largest perturbed-linear workspace of the layer's six matrices.
+// The largest perturbed-linear workspace of the layer's six matrices (the first layer's q, k, v
+// read one shared input: their plans hold the fp32 base of the shared-X path).
 static size_t decoder_lin_ws(int T, int d, int ffn, int r, int q, int nblk, int dtype) {
   const int shapes[3][2] = {{d, d}, {ffn, d}, {d, ffn}};
   size_t need = 0;
   for (const auto& sh : shapes) {
-    PlinearPlan p;
-    zo_plinear_plan(&p, T, sh[0], sh[1], r, q, nblk, (long long)T * sh[1], dtype, dtype);
-    need = p.ws_total > need ? p.ws_total : need;
+    for (const long long xs : {(long long)T * sh[1], 0LL}) {
+      PlinearPlan p;
+      zo_plinear_plan(&p, T, sh[0], sh[1], r, q, nblk, xs, dtype, dtype);
+      need = p.ws_total > need ? p.ws_total : need;
+    }
   }
   return need;
 }
@@ -739,9 +742,11 @@ static LoraLayerWs lora_layer_ws(int T, int d, int dkv, int ffn, int rl, int r, 
   const size_t wide = zo_align256((size_t)nblk * T * ffn * es);
   size_t lin = 0;
   for (int m : {d, dkv}) {
-    PlinearPlan p;
-    zo_plinear_plan(&p, T, m, d, rl + r, q, nblk, (long long)T * d, dtype, dtype);
-    lin = p.ws_total > lin ? p.ws_total : lin;
+    for (const long long xs : {(long long)T * d, 0LL}) {  // per-block or shared input
+      PlinearPlan p;
+      zo_plinear_plan(&p, T, m, d, rl + r, q, nblk, xs, dtype, dtype);
+      lin = p.ws_total > lin ? p.ws_total : lin;
+    }
   }
   WsCarver wc(base);
   LoraLayerWs w;

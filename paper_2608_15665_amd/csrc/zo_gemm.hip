@@ -44,6 +44,11 @@ namespace {
 
 constexpr int BK = 64;  // bf16 elements per K tile = 128 bytes per LDS row
 
+// Internal epilogues of the shared-X fan-out (beyond zo_epilogue's values): R is an fp32 T x m
+// base X W^T shared by every block, added to the block's rank-r term before the rounding.
+constexpr int EPI_BASE = 16;       // Y_b = base + result
+constexpr int EPI_BASE_RELU = 17;  // Y_b = max(base + result, 0)
+
 // Swizzle of the 16-byte chunk index within a 128-byte LDS row; conflict free
 // for ds_read_b128 of 8 or 16 consecutive rows at one logical chunk.
 __device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ ((row & 1) << 2)) & 7; }
@@ -65,6 +70,7 @@ struct GemmArgs {
   const void* R;               // ZO_EPI_RESIDUAL / SILU_MUL: same type and layout as Y (ldy)
   long long r_block_stride;    // elements; 0 = one R shared by all blocks
   int tiles_a, tiles_b, total_tiles;
+  int blk_inner;               // k_gemm_main: 1 = the blocks of one output tile run consecutively
 };
 
 // Four fp32 accumulator values as element idx.. of an OUT-typed (zo_dtype) array.
@@ -389,6 +395,7 @@ struct F32Args {
   int epi;                    // zo_epilogue
   const float* R;             // ZO_EPI_RESIDUAL: added to Y (same layout)
   long long r_block_stride;
+  const float* base;          // nullptr, or a rows_b x ldy matrix added before the epilogue
 };
 
 __global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
@@ -451,6 +458,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
       const int col = c0 + tx * 4 + j;
       if (col >= a.rows_a) continue;
       float v = acc[i][j];
+      if (a.base) v += a.base[(size_t)tok * a.ldy + col];
       if (a.epi == ZO_EPI_RELU) v = fmaxf(v, 0.f);
       if (a.epi == ZO_EPI_RESIDUAL) v += R[(size_t)tok * a.ldy + col];
       if (a.epi == ZO_EPI_SILU_MUL) v *= silu(R[(size_t)tok * a.ldy + col]);
@@ -675,18 +683,22 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
 
-  // XCD-aware tile order (each XCD a contiguous range), grouped 8 token tiles deep.
+  // XCD-aware tile order (each XCD a contiguous range), grouped 8 token tiles deep.  With
+  // blk_inner the block index runs fastest (the shared-X fan-out: the blocks of one tile read
+  // the same base tile, which then comes from the XCD's L2).
   const int w = blockIdx.x;
   const int nt = a.total_tiles;
   const int xcd = w & 7, widx = w >> 3;
-  const int lt = xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
+  const int lt0 = xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
+  const int lt = a.blk_inner ? lt0 / a.nblk : lt0;
+  const int nbt = a.blk_inner ? a.tiles_b : a.nblk * a.tiles_b;  // (block, token tile) pairs in the raster
   constexpr int GROUP = 8;
   const int per_group = GROUP * a.tiles_a, grp = lt / per_group, first = grp * GROUP;
-  const int gsize = min(GROUP, a.nblk * a.tiles_b - first), rem = lt - grp * per_group;
+  const int gsize = min(GROUP, nbt - first), rem = lt - grp * per_group;
   const int bt = first + rem % gsize, at = rem / gsize;
   // The decode is uniform but its divisions run on the VALU: pin the results to scalar
   // registers, so the buffer descriptors built from them are scalar too.
-  const int blk = __builtin_amdgcn_readfirstlane(bt / a.tiles_b);
+  const int blk = __builtin_amdgcn_readfirstlane(a.blk_inner ? lt0 % a.nblk : bt / a.tiles_b);
   const int t0 = __builtin_amdgcn_readfirstlane((bt % a.tiles_b) * 256);
   const int m0 = __builtin_amdgcn_readfirstlane(at * 256);
 
@@ -920,13 +932,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   // one base register plus immediates.
   char* Yb = (char*)a.Y + (long long)blk * a.y_block_stride * (OUT == ZO_F32 ? 4 : 2);
   const char* Rb = (const char*)a.R + (long long)blk * a.r_block_stride * (OUT == ZO_F32 ? 4 : 2);
-  const int lr8 = lane & 7, lc8 = lane >> 3;
   __syncthreads();  // every wave is past its last fragment reads: the ring is free
   __builtin_amdgcn_sched_barrier(0);  // nothing of the epilogue moves above the barrier
+  // The lane index again, from the lane masks rather than the work-item id: the compiler then
+  // recomputes these few values here instead of keeping (and spilling) the loop's copies.
+  const int el = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const int efr = el & 31, efh = el >> 5;
   if constexpr (OUT != ZO_F32 && (EPI == ZO_EPI_NONE || EPI == ZO_EPI_RELU)) {
     constexpr int PITCH = 528;
     // Token row wn 128 + 32 j + fr, columns wm 128 + 32 i + 8 q4 + 4 fh .. + 3.
-    char* const wb = lds + (wn * 128 + fr) * PITCH + wm * 256 + fh * 8;
+    char* const wb = lds + (wn * 128 + efr) * PITCH + wm * 256 + efh * 8;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -946,26 +961,51 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     __syncthreads();
     // Pass it of wave w: rows 8 it + 2 w + lane / 32, whole (512 bytes each), 16-byte chunk
     // lane % 32 (columns 8 (lane % 32) ..).
-    const int half = lane >> 5, ch = lane & 31;
-    const char* const rb = lds + (2 * wave + half) * PITCH + ch * 16;
-    const int col = m0 + ch * 8;
+    const char* const rb = lds + (2 * wave + efh) * PITCH + efr * 16;
+    const int col = m0 + efr * 8;
 #pragma unroll 8
     for (int it = 0; it < 32; ++it) {
       const u32x4 v = *(const u32x4*)(rb + it * 8 * PITCH);
-      const int tok = t0 + it * 8 + 2 * wave + half;
+      const int tok = t0 + it * 8 + 2 * wave + efh;
       if (tok < a.rows_b && col < a.rows_a) *(u32x4*)(Yb + ((size_t)tok * a.ldy + col) * 2) = v;
     }
   } else {
     constexpr int PITCH = 1040;
     // Half h holds j = 2 h, 2 h + 1: staging row wn 64 + 32 (j % 2) + fr is tile token
     // wn 128 + 32 j + fr; 16-byte chunk wm 32 + 8 i + 2 q4 + fh holds its columns 4 chunk .. + 3.
-    char* const wb = lds + (wn * 64 + fr) * PITCH + wm * 512 + fh * 16;
+    char* const wb = lds + (wn * 64 + efr) * PITCH + wm * 512 + efh * 16;
     // Read-back pass it of wave w: staging rows 8 it + lr8, columns 64 w + 8 lc8 .. + 7.
+    const int lr8 = el & 7, lc8 = el >> 3;
     const char* const rb = lds + lr8 * PITCH + (wave * 8 + lc8) * 32;
     const int col = m0 + (wave * 8 + lc8) * 8;
+    // R of the half's read-back passes is requested before its staging writes, so that its
+    // latency overlaps them (one load chain per half instead of one per few passes).
+    constexpr bool HAS_R = EPI == ZO_EPI_RESIDUAL || EPI == ZO_EPI_SILU_MUL || EPI == EPI_BASE ||
+                           EPI == EPI_BASE_RELU;
+    constexpr bool R32 = EPI == EPI_BASE || EPI == EPI_BASE_RELU;  // the fp32 base
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       if (h) __syncthreads();  // the first half's read-back is done
+      u32x4 rpre[HAS_R ? 16 : 1][R32 || OUT == ZO_F32 ? 2 : 1];
+      if constexpr (HAS_R) {
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+          const int sr = it * 8 + lr8;
+          const int tok = t0 + (sr >> 6) * 128 + h * 64 + (sr & 63);
+          const size_t idx = (size_t)min(tok, a.rows_b - 1) * a.ldy + min(col, a.rows_a - 8);
+          if constexpr (R32) {  // 32-byte aligned rows
+            rpre[it][0] = *(const u32x4*)(Rb + idx * 4);
+            rpre[it][1] = *(const u32x4*)(Rb + idx * 4 + 16);
+          } else if constexpr (OUT == ZO_F32) {  // an fp32 R need only be 4-byte aligned
+            float r8[8];
+            load8<ZO_F32>(Rb, idx, r8);
+            rpre[it][0] = __builtin_bit_cast(u32x4, (f32x4){r8[0], r8[1], r8[2], r8[3]});
+            rpre[it][1] = __builtin_bit_cast(u32x4, (f32x4){r8[4], r8[5], r8[6], r8[7]});
+          } else {
+            rpre[it][0] = *(const u32x4*)(Rb + idx * 2);
+          }
+        }
+      }
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
@@ -977,7 +1017,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
                 (f32x4){c[q4 * 4 + 0], c[q4 * 4 + 1], c[q4 * 4 + 2], c[q4 * 4 + 3]};
           }
       __syncthreads();
-#pragma unroll 4
+#pragma unroll
       for (int it = 0; it < 16; ++it) {
         const int sr = it * 8 + lr8;
         const f32x4 lo = *(const f32x4*)(rb + it * 8 * PITCH);
@@ -988,11 +1028,30 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
         float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         if constexpr (EPI != ZO_EPI_NONE) {
           float rv[8];
-          if constexpr (EPI == ZO_EPI_RESIDUAL || EPI == ZO_EPI_SILU_MUL) load8<OUT>(Rb, idx, rv);
+          if constexpr (HAS_R) {
+            if constexpr (R32 || OUT == ZO_F32) {
+              const f32x4 r0 = __builtin_bit_cast(f32x4, rpre[it][0]), r1 = __builtin_bit_cast(f32x4, rpre[it][1]);
+              rv[0] = r0[0]; rv[1] = r0[1]; rv[2] = r0[2]; rv[3] = r0[3];
+              rv[4] = r1[0]; rv[5] = r1[1]; rv[6] = r1[2]; rv[7] = r1[3];
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t u = rpre[it][0][e];
+                if constexpr (OUT == ZO_BF16) {
+                  rv[2 * e] = bf16_to_f32((bf16_t)u);
+                  rv[2 * e + 1] = bf16_to_f32((bf16_t)(u >> 16));
+                } else {
+                  rv[2 * e] = f16_to_f32((uint16_t)u);
+                  rv[2 * e + 1] = f16_to_f32((uint16_t)(u >> 16));
+                }
+              }
+            }
+          }
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             if constexpr (EPI == ZO_EPI_RELU) v[e] = fmaxf(v[e], 0.f);
-            else if constexpr (EPI == ZO_EPI_RESIDUAL) v[e] += rv[e];
+            else if constexpr (EPI == ZO_EPI_RESIDUAL || EPI == EPI_BASE) v[e] += rv[e];
+            else if constexpr (EPI == EPI_BASE_RELU) v[e] = fmaxf(v[e] + rv[e], 0.f);
             else v[e] *= silu(rv[e]);
           }
         }
@@ -1004,7 +1063,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
 
 template <bool F16, int OUT>
 void launch_main_epi(const GemmArgs& a, dim3 grid, hipStream_t stream) {
-  if (a.epi == ZO_EPI_RELU)
+  if (a.epi == EPI_BASE)
+    hipLaunchKernelGGL((k_gemm_main<F16, OUT, EPI_BASE>), grid, dim3(256), 0, stream, a);
+  else if (a.epi == EPI_BASE_RELU)
+    hipLaunchKernelGGL((k_gemm_main<F16, OUT, EPI_BASE_RELU>), grid, dim3(256), 0, stream, a);
+  else if (a.epi == ZO_EPI_RELU)
     hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_RELU>), grid, dim3(256), 0, stream, a);
   else if (a.epi == ZO_EPI_RESIDUAL)
     hipLaunchKernelGGL((k_gemm_main<F16, OUT, ZO_EPI_RESIDUAL>), grid, dim3(256), 0, stream, a);
@@ -1076,7 +1139,9 @@ int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
     p->ws_p = zo_align256(rows * p->rp * 4);
     p->ws_bp = zo_align256((size_t)nblk * m * p->rp * 4);
   }
-  p->ws_total = p->ws_vt + p->ws_p2 + p->ws_p + p->ws_bp;
+  p->fan = p->nx == 1 && nblk > 1;
+  p->ws_base = p->fan ? zo_align256((size_t)T * m * 4) : 0;
+  p->ws_total = p->ws_vt + p->ws_p2 + p->ws_p + p->ws_bp + p->ws_base;
   return ZO_OK;
 }
 
@@ -1093,6 +1158,7 @@ PlinearWs zo_plinear_ws(const PlinearPlan& p, void* ws) {
   w.p2 = p.ws_p2 ? wc.take(p.ws_p2) : nullptr;
   w.pp = wc.take(p.ws_p);
   w.bp = wc.take(p.ws_bp);
+  w.base = p.ws_base ? wc.take(p.ws_base) : nullptr;
   return w;
 }
 
@@ -1251,12 +1317,69 @@ int zo_gemm_plain(int T, int m, int n, int nblk, int dtype, const void* X, long 
   return f16 ? launch_gemm_bf16<2, 4, 4, 2, true>(h, stream) : launch_gemm_bf16<2, 4, 4, 2, false>(h, stream);
 }
 
+// Shared X (one X for every block): X W^T once into the fp32 base, then per block only the
+// rank-r term, added to the base before the epilogue (plain or ReLU; the others take the
+// per-block path).  The MFMA work drops from nblk products to one.
+static int apply_fan(const PlinearPlan& p, const PlinearWs& w, const void* X, const void* W, void* Y,
+                     hipStream_t stream, int epi) {
+  const bool f16 = p.in_dtype == ZO_F16;
+  GemmArgs b{};
+  b.A = (const bf16_t*)W;
+  b.B = (const bf16_t*)X;
+  b.rows_a = p.m;
+  b.rows_b = p.T;
+  b.K = p.n;
+  b.nblk = 1;
+  b.Y = w.base;
+  b.ldy = p.m;
+  b.out_dtype = ZO_F32;
+  b.epi = ZO_EPI_NONE;
+  GemmArgs h{};
+  h.A = (const bf16_t*)W;
+  h.B = (const bf16_t*)X;
+  h.rows_a = p.m;
+  h.rows_b = p.T;
+  h.K = 0;
+  h.nblk = p.nblk;
+  h.ca = (const bf16_t*)w.bp;
+  h.ca_block_stride = (long long)p.m * 3 * p.rp;
+  h.cb = (const bf16_t*)w.pp;
+  h.cb_block_stride = 0;
+  h.rc = 3 * p.rp;
+  h.Y = Y;
+  h.y_block_stride = (long long)p.T * p.m;
+  h.ldy = p.m;
+  h.out_dtype = p.out_dtype;
+  h.epi = epi == ZO_EPI_RELU ? EPI_BASE_RELU : EPI_BASE;
+  h.R = w.base;
+  h.r_block_stride = 0;
+  h.blk_inner = 1;
+  int st = launch_gemm_main(b, f16, stream);
+  if (st != ZO_OK) return st;
+  // No main-segment tiles here (K = 0): f16 only selects the fp16 output type.
+  return launch_gemm_main(h, f16, stream);
+}
+
+static bool fan_fits(const PlinearPlan& p, int epi) {
+  if (!p.fan || !p.in16 || (epi != ZO_EPI_NONE && epi != ZO_EPI_RELU)) return false;
+  GemmArgs b{};
+  b.rows_a = p.m;
+  b.rows_b = p.T;
+  b.K = p.n;
+  GemmArgs h{};
+  h.rows_a = p.m;
+  h.rows_b = p.T;
+  h.rc = 3 * p.rp;
+  return main_gemm_fits(b) && main_gemm_fits(h);
+}
+
 int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y, void* ws,
                      hipStream_t stream, int epi, const void* R, long long r_block_stride) {
   const PlinearWs w = zo_plinear_ws(p, ws);
   void* pp = w.pp;
   void* bp = w.bp;
   const long long xs = p.x_block_stride;
+  if (fan_fits(p, epi)) return apply_fan(p, w, X, W, Y, stream, epi);
   if (p.in16) {
     GemmArgs h{};
     h.A = (const bf16_t*)W;
@@ -1300,6 +1423,21 @@ int zo_plinear_apply(const PlinearPlan& p, const void* X, const void* W, void* Y
   h.epi = epi;
   h.R = (const float*)R;
   h.r_block_stride = r_block_stride;
+  if (p.fan) {
+    // Shared X: X W^T once into the base, then each block's rank-r term added to it.
+    F32Args b = h;
+    b.rc = 0;
+    b.Y = (float*)w.base;
+    b.y_block_stride = 0;
+    b.epi = ZO_EPI_NONE;
+    b.R = nullptr;
+    b.r_block_stride = 0;
+    hipLaunchKernelGGL(k_gemm_f32, dim3((p.m + 63) / 64, (p.T + 63) / 64, 1), dim3(256), 0, stream, b);
+    int st = zo_hip_status(hipGetLastError(), "k_gemm_f32 (shared X)");
+    if (st != ZO_OK) return st;
+    h.K = 0;
+    h.base = (const float*)w.base;
+  }
   dim3 grid((p.m + 63) / 64, (p.T + 63) / 64, p.nblk);
   hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, stream, h);
   return zo_hip_status(hipGetLastError(), "k_gemm_f32");

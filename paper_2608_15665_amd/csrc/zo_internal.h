@@ -96,7 +96,8 @@ struct PlinearPlan {
   long long x_block_stride;
   int in16;                 // 16-bit inputs (bf16 or fp16): MFMA path
   int in_dtype, out_dtype;  // zo_dtype values
-  size_t ws_vt, ws_p2, ws_p, ws_bp;  // bytes of each workspace region
+  int fan;                  // one X shared by nblk > 1 blocks: X W^T once, then the blocks' terms
+  size_t ws_vt, ws_p2, ws_p, ws_bp, ws_base;  // bytes of each workspace region
   size_t ws_total;
 };
 int zo_plinear_plan(PlinearPlan* p, int T, int m, int n, int r, int q, int nblk,
@@ -107,6 +108,7 @@ struct PlinearWs {
   void* p2;  // bf16 inputs: X_b Vt^T in fp32, 2 rp wide (nullptr for fp32)
   void* pp;  // left correction operand per X block: bf16 [P_hi | P_hi | P_lo]; fp32 rp wide
   void* bp;  // right correction operand per block: bf16 [B_hi | B_lo | B_hi]; fp32 rp wide
+  void* base;  // shared X only: X W^T in fp32, T x m (nullptr otherwise)
 };
 PlinearWs zo_plinear_ws(const PlinearPlan& p, void* ws);
 // Query table of a call: j(b) and s(b) packed as j | (s + 1) << 16.
