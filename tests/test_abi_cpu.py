@@ -102,6 +102,22 @@ def test_perturbed_linear_rejects_small_workspace_and_nulls():
         assert st == 2 and "out_dtype" in _detail()
 
 
+def test_shared_x_workspace_holds_the_base():
+    """With one X shared by several blocks the workspace also holds the fp32 T x m product
+    X W^T that every block's output starts from; a single block, or per-block X, does not."""
+    L = zo.lib()
+    T, m, n, r, q = 300, 264, 200, 16, 2
+    for dt in (0, 1, 2):
+        one = L.zo_perturbed_linear_workspace(T, m, n, r, q, 1, 0, dt)
+        shared = L.zo_perturbed_linear_workspace(T, m, n, r, q, 4, 0, dt)
+        per_block = L.zo_perturbed_linear_workspace(T, m, n, r, q, 4, T * n, dt)
+        rp = (r + 31) // 32 * 32 if dt else (r + 15) // 16 * 16
+        bp_growth = 3 * m * (3 * rp * 2 if dt else rp * 4)  # the three more blocks' right factors
+        assert shared - one >= T * m * 4 + bp_growth - 1024, dt
+        assert shared - one <= T * m * 4 + bp_growth + 1024, dt
+        assert per_block > one
+
+
 def test_lora_validation_and_workspace():
     """The LoRA entry points share the full-tuning plan at rank rl + r and reject bad ranks,
     non-finite scale and NULL adapter tensors before launching anything."""

@@ -356,3 +356,71 @@ def test_prepare_group_equals_separate(dt, shared):
         Y = p.apply()
         torch.cuda.synchronize()
         assert torch.equal(Y.view(torch.uint8), ref.view(torch.uint8))
+
+
+def _epi_ref(y, epi, R):
+    if epi == zo.ZO_EPI_RELU:
+        return np.maximum(y, 0.0)
+    if epi == zo.ZO_EPI_RESIDUAL:
+        return y + R
+    if epi == zo.ZO_EPI_SILU_MUL:
+        return y * oracle.silu(R)
+    return y
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("epi", ["none", "relu", "residual", "silu_mul"])
+def test_shared_x_epilogues(dt, epi):
+    """One X shared by every block (x_block_stride = 0): X W^T is computed once and each block
+    adds its rank-r term (plain and ReLU epilogues), or the blocks take the per-block path
+    (residual and gated epilogues, R per block).  Several tiles with ragged edges in tokens and
+    output columns; every block against the oracle with the epilogue applied in float64."""
+    T, m, n, r, q, nblk = 600, 520, 136, 24, 3, 6
+    c = make_case(T, m, n, r, q, nblk, True, bf16=dt == "bf16", f16=dt == "f16")
+    code = {"none": zo.ZO_EPI_NONE, "relu": zo.ZO_EPI_RELU, "residual": zo.ZO_EPI_RESIDUAL,
+            "silu_mul": zo.ZO_EPI_SILU_MUL}[epi]
+    R64 = Rd = None
+    if code in (zo.ZO_EPI_RESIDUAL, zo.ZO_EPI_SILU_MUL):
+        Rd, R64 = cast(zd.draw(5, "X", (T, m, 3), (nblk * T, m)), dt)
+    pl = zo.PerturbedLinear(c["Xd"], c["Wd"], c["Ud"], c["Vd"], c["Zd"], c["bq"], c["bs"], 1e-3, T, x_block_stride=0)
+    pl.prepare()
+    Y = host(pl.apply(code, Rd)).reshape(nblk, T, m)
+    ref = run_oracle(c, 1e-3)
+    for b in range(nblk):
+        Rb = None if R64 is None else R64.reshape(nblk, T, m)[b]
+        want = _epi_ref(ref[b], code, Rb)
+        assert ferr(Y[b], want, 1e-3) <= 1e-2, b
+        assert normwise(Y[b], want) <= (2e-3 if dt == "f16" else 1e-2), b
+
+
+@pytest.mark.parametrize("name", ["opt-13b", "llama-7b"])
+def test_shared_x_full_size_sampled(name):
+    """The first layer's q/k/v shape at full size with one shared X (T tokens, 2q blocks, the
+    config's r), in the launch configuration the benchmark's shared-X report times; sampled token
+    rows of several blocks against the oracle, and the difference of the two blocks of a query
+    (the correction channel, X W^T cancels exactly) against (X V)(eps U Z_j)^T in fp32 output."""
+    cfg = zd.CONFIGS[name]
+    T, q, r = cfg["T"], cfg["q"], cfg["r"]
+    m = n = cfg["mats"][0][1]
+    nblk = 2 * q
+    c = make_case(T, m, n, r, q, nblk, True, bf16=True)
+    rows = np.array([0, 1, 255, 256, T // 2 + 1, T - 1])
+    blocks = sorted({0, 1, nblk // 2 - 1, nblk - 1})
+    for out in (None, torch.float32):
+        Y = zo.perturbed_linear(c["Xd"], c["Wd"], c["Ud"], c["Vd"], c["Zd"], c["bq"], c["bs"], 1e-3, T,
+                                x_block_stride=0, out_dtype=out)
+        torch.cuda.synchronize()
+        Yh = Y.view(nblk, T, m)
+        got = {b: host(Yh[b][torch.from_numpy(rows).cuda()]) for b in blocks}
+        refs = {b: run_oracle(c, 1e-3, blocks=[b], rows=rows)[0] for b in blocks}
+        for b in blocks:
+            if out is None:
+                assert ferr(got[b], refs[b], 1e-3) <= 1e-2, b
+                assert normwise(got[b], refs[b]) <= 1e-2, b
+            else:
+                assert ferr(got[b], refs[b], 1.0) <= 1e-4, b
+        if out is not None:  # blocks 0 and 1: query 0, + and -
+            d = (got[0] - got[1]) / 2e-3
+            xv = xblock(c, 0, rows) @ c["V"].astype(np.float64)
+            want = xv @ (c["U"].astype(np.float64) @ c["Z"][0].astype(np.float64)).T
+            assert ferr(d, want, 1.0) <= 2e-2
