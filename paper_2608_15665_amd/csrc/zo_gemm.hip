@@ -1213,11 +1213,15 @@ static int launch_projection(const PlinearPlan& p, const void* X, const void* vt
   g.y_block_stride = (long long)p.T * rows_a;
   g.ldy = rows_a;
   g.out_dtype = ZO_F32;
-  // 64 x 256 tiles; 64 x 128 when that leaves fewer than two workgroups per CU (this pass
-  // streams X once, so it needs the whole chip's loads in flight).  Tile shapes change no
+  // From 128 rows on, the main GEMM's pipeline (256 x 256 tiles: the 2 rp = 128 rows of one
+  // r = 64 factor fill half a tile, a stacked q, k, v projection 384 of 512 rows): it keeps the X
+  // stream and the MFMAs overlapped better than the register-staged kernel even with the idle
+  // rows (OPT-13B-shaped stack: prepare 130 -> 103 ms per step).  Otherwise 64 x 256 tiles;
+  // 64 x 128 when that leaves fewer than two workgroups per CU.  Tile shapes change no
   // element's arithmetic.
-  const long long tiles = (long long)p.nx * ((p.T + 255) / 256) * ((rows_a + 63) / 64);
   const bool f16 = p.in_dtype == ZO_F16;
+  if (rows_a >= 128 && main_gemm_fits(g)) return launch_gemm_main(g, f16, stream);
+  const long long tiles = (long long)p.nx * ((p.T + 255) / 256) * ((rows_a + 63) / 64);
   if (tiles < 512)
     return f16 ? launch_gemm_bf16<1, 4, 2, 1, true>(g, stream) : launch_gemm_bf16<1, 4, 2, 1, false>(g, stream);
   return f16 ? launch_gemm_bf16<1, 4, 2, 2, true>(g, stream) : launch_gemm_bf16<1, 4, 2, 2, false>(g, stream);
