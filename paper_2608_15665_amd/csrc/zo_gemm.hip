@@ -212,6 +212,18 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// 16x16x32 MFMA on 16-byte fragments of eight 16-bit values: fp16 or bf16.  Lane l holds row
+// l % 16 of A (and of B's transpose) at k (l / 16) 8 .. + 7; the result's lane l holds rows
+// 4 (l / 16) .. + 3 of column l % 16.
+template <bool F16>
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 template <int WM, int WN, int TM, int TN, bool F16>
 __global__ __launch_bounds__(WM* WN * 64) void k_gemm_bf16(GemmArgs a) {
   constexpr int NT = WM * WN * 64;
@@ -671,6 +683,12 @@ constexpr int MAIN_SLOTS = 5;
 
 __device__ __forceinline__ int f8(int r) { return (r >> 1) & 7; }
 
+// Byte offset of a lane's DMA row (clamped to the operand's last row) at k = 0 in an operand of
+// the given width (elements per row), its 16-byte chunk lch.
+__device__ __forceinline__ unsigned dma_off(int row, int rows, int width, int lch) {
+  return (unsigned)min(row, rows - 1) * (unsigned)width * 2u + (unsigned)lch * 16u;
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
   return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)bytes, 0x00020000);
 }
@@ -715,16 +733,18 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   // depend on i).  Per-lane byte offsets of the four operands at k = 0.
   const int drow = lane >> 3;
   const int lch = (lane & 7) ^ f8(8 * wave + drow);
-  unsigned voA[8], voB[8], voC[8], voD[8];
+  unsigned voA[8], voB[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const int row = 8 * (wave + 4 * i) + drow;
     const unsigned ra = (unsigned)min(m0 + row, a.rows_a - 1), rb = (unsigned)min(t0 + row, a.rows_b - 1);
     voA[i] = ra * (unsigned)a.K * 2u + lch * 16u;
     voB[i] = rb * (unsigned)a.K * 2u + lch * 16u;
-    voC[i] = ra * (unsigned)a.rc * 2u + lch * 16u;
-    voD[i] = rb * (unsigned)a.rc * 2u + lch * 16u;
   }
+  // The rank segment's row offsets are formed where its few tiles load (a couple of VALU
+  // instructions each) rather than kept through the main loop.
+#define voC(i) dma_off(m0 + 8 * (wave + 4 * (i)) + drow, a.rows_a, a.rc, lch)
+#define voD(i) dma_off(t0 + 8 * (wave + 4 * (i)) + drow, a.rows_b, a.rc, lch)
   char* const ldsw = lds + 8 * wave * RB;
   // Loads i in [I0, I1) of part A (W rows) or B (X rows) of tile t into slot sl; tiles past the
   // end are not loaded.  MAIN: t is known to be a main-segment tile.  The rank segment's
@@ -738,7 +758,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     const unsigned so = (unsigned)(m ? t : t - NTM) * 128u;
 #pragma unroll
     for (int i = decltype(I0)::value; i < decltype(I1)::value; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(d + 32 * RB * i), 16, m ? voA[i] : voC[i], so, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(d + 32 * RB * i), 16, m ? voA[i] : voC(i), so, 0, 0);
   };
   auto load_B = [&](int sl, int t, auto MAIN, auto I0, auto I1) {
     const bool m = decltype(MAIN)::value || t < NTM;
@@ -748,7 +768,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     const unsigned so = (unsigned)(m ? t : t - NTM) * 128u;
 #pragma unroll
     for (int i = decltype(I0)::value; i < decltype(I1)::value; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(d + 32 * RB * i), 16, m ? voB[i] : voD[i], so, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(d + 32 * RB * i), 16, m ? voB[i] : voD(i), so, 0, 0);
   };
   using Main = std::true_type;
   using Any = std::false_type;
@@ -756,40 +776,48 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   using I4 = std::integral_constant<int, 4>;
   using I8 = std::integral_constant<int, 8>;
 
-  const int fr = lane & 31, fh = lane >> 5;
-  const int ff = f8(fr);  // f of every fragment row (they differ from fr by multiples of 32)
+  // Fragments (16x16x32): lane l reads row (16 i + l % 16) of its wave's 128 rows of a part at
+  // k-quarter l / 16 of a 32-deep substep, i.e. logical chunk 4 s + l / 16 of the row.  The
+  // rows of one fragment start at a multiple of 16, so f of a fragment row is f(l % 16).
+  const int fr = lane & 15, fq = lane >> 4;
+  const int ff = f8(fr);
   const int offA = (wm * 128 + fr) * RB, offB = (wn * 128 + fr) * RB;
-  bf16x8 F0a[4], F0b[4], F1a[4], F1b[4];
-  // Fragments of substep s (k 16 s .. 16 s + 15 of the tile) from the slots sa (A) and sb (B).
+  bf16x8 F0a[8], F0b[8], F1a[8], F1b[8];
+  // Fragments of substep s (k 32 s .. 32 s + 31 of the tile) from the slots sa (A) and sb (B).
   auto frags = [&](int sa, int sb, int s, bf16x8* fa, bf16x8* fb) {
-    const int ch = ((2 * s + fh) ^ ff) * 16;
+    const int ch = ((4 * s + fq) ^ ff) * 16;
     const char* pa = lds + sa * PART + offA + ch;
     const char* pb = lds + sb * PART + offB + ch;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) fa[i] = *(const bf16x8*)(pa + i * 32 * RB);
+    for (int i = 0; i < 8; ++i) fa[i] = *(const bf16x8*)(pa + i * 16 * RB);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)(pb + j * 32 * RB);
+    for (int j = 0; j < 8; ++j) fb[j] = *(const bf16x8*)(pb + j * 16 * RB);
   };
-  f32x16 acc[4][4];
+  // acc[i][j]: output columns (A rows) 16 i + 4 (l / 16) .. + 3, token (B row) 16 j + l % 16 of
+  // the wave's 128 x 128.
+  f32x4 acc[8][8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 8; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.f;
   auto mma = [&](const bf16x8* fa, const bf16x8* fb, auto f16) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32<decltype(f16)::value>(fa[i], fb[j], acc[i][j]);
+      for (int j = 0; j < 8; ++j) acc[i][j] = mfma16<decltype(f16)::value>(fa[i], fb[j], acc[i][j]);
   };
-  // Fragment x (0..3: A fragment x, 4..7: B fragment x - 4) of substep s from slots sa / sb.
-  auto frag1 = [&](int sa, int sb, int s, int x, bf16x8* fa, bf16x8* fb) {
-    const int ch = ((2 * s + fh) ^ ff) * 16;
-    if (x < 4)
-      fa[x] = *(const bf16x8*)(lds + sa * PART + offA + ch + x * 32 * RB);
-    else
-      fb[x - 4] = *(const bf16x8*)(lds + sb * PART + offB + ch + (x - 4) * 32 * RB);
+  // The n-th fragment read of substep s from slots sa / sb, in the order the next substep first
+  // uses them: A0 (MFMA 0), B0..B7 (MFMAs 0..7), then A1..A7 (MFMAs 8, 16, ..., 56).
+  auto frag1 = [&](int sa, int sb, int s, int n, bf16x8* fa, bf16x8* fb) {
+    const int ch = ((4 * s + fq) ^ ff) * 16;
+    if (n >= 1 && n <= 8)
+      fb[n - 1] = *(const bf16x8*)(lds + sb * PART + offB + ch + (n - 1) * 16 * RB);
+    else {
+      const int x = n == 0 ? 0 : n - 8;
+      fa[x] = *(const bf16x8*)(lds + sa * PART + offA + ch + x * 16 * RB);
+    }
   };
   // One load (i of 8) of part A / B of main-segment tile t into slot sl.
   auto load1_A = [&](int sl, int t, int i) {
@@ -800,46 +828,46 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_ptr_t)(ldsw + sl * PART + 32 * RB * i), 16, voB[i],
                                              (unsigned)t * 128u, 0, 0);
   };
-  // One steady-state substep, written out in issue order: MFMA x (x = 0..15, accumulator
-  // x / 4, x % 4), then the next substep's fragment read x (x < 8, fragments (ra, rb, rs) into
-  // na / nb), then load ld(x / 4) after MFMAs 1, 5, 9, 13, each group fenced so the compiler
-  // keeps the interleave (left to itself it bunches the reads and loads, and the wave's MFMA
-  // issue stalls behind them).
+  // One steady-state substep, written out in issue order: MFMA x (x = 0..63, accumulator
+  // x / 8, x % 8), the next substep's fragment read x / 4 after every fourth MFMA (fragments
+  // (ra, rb, rs) into na / nb, in frag1's order: the B fragments, which the next substep's first
+  // eight MFMAs all use, are read early), and load ld(x / 8) after every eighth, each group fenced so the
+  // compiler keeps the interleave (left to itself it bunches the reads and loads, and the wave's
+  // MFMA issue stalls behind them).
   auto substep = [&](const bf16x8* fa, const bf16x8* fb, int ra, int rb, int rs, bf16x8* na, bf16x8* nb,
                      auto ld, auto f16) {
 #pragma unroll
-    for (int x = 0; x < 16; ++x) {
-      acc[x >> 2][x & 3] = mfma32<decltype(f16)::value>(fa[x >> 2], fb[x & 3], acc[x >> 2][x & 3]);
-      if (x < 8) frag1(ra, rb, rs, x, na, nb);
-      if (x % 4 == 1) ld(x / 4);
+    for (int x = 0; x < 64; ++x) {
+      acc[x >> 3][x & 7] = mfma16<decltype(f16)::value>(fa[x >> 3], fb[x & 7], acc[x >> 3][x & 7]);
+      if (x % 4 == 0) frag1(ra, rb, rs, x / 4, na, nb);
+      if (x % 8 == 3) ld(x / 8);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // Prologue: A0, B0, A1 and the first half of B1 (what the last substep of tile -1 would have
-  // issued); tile 0 then issues the rest of B1 and A2.
+  // Prologue: A0, B0, A1 and B1.  Tile k then issues A(k+2) before its barrier (into the slot
+  // tile k-1's B part vacated) and B(k+2) after it (into tile k's A slot), so every part has a
+  // whole tile or more to land.
   load_A(0, 0, Any{}, I0{}, I8{});
   load_B(1, 0, Any{}, I0{}, I8{});
   load_A(2, 1, Any{}, I0{}, I8{});
-  load_B(3, 1, Any{}, I0{}, I4{});
+  load_B(3, 1, Any{}, I0{}, I8{});
   if (NT > 1)
-    asm volatile("s_waitcnt vmcnt(12)" ::: "memory");  // this wave's loads of tile 0 landed
+    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");  // this wave's loads of tile 0 landed
   else
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   frags(0, 1, 0, F0a, F0b);
 
   // Tile k, a full main tile with main tiles k+1 and k+2 after it; K5 = k % 5 makes every slot a
-  // compile-time constant.  Loads: the rest of B(k+1) in substep 0, A(k+2) in substeps 1 and 2
-  // (both into tile k-1's slots, free since barrier(k-1)), the first half of B(k+2) in substep 3
-  // (into tile k's A slot, free after barrier(k)).
+  // compile-time constant.  Substep 0 (MFMAs of k-half 0, reads of half 1) issues A(k+2); the
+  // barrier follows the last reads of tile k; substep 1 (MFMAs of half 1, reads of tile k+1's
+  // half 0) issues B(k+2) into tile k's A slot.
   auto body_main = [&](int k, auto K5, auto f16) {
     constexpr int k5 = decltype(K5)::value;
     constexpr int sa = (2 * k5) % 5, sb = (2 * k5 + 1) % 5;                       // tile k
     constexpr int na = (2 * k5 + 2) % 5, nb = (2 * k5 + 3) % 5, a2 = (2 * k5 + 4) % 5;  // k+1, A(k+2)
-    substep(F0a, F0b, sa, sb, 1, F1a, F1b, [&](int i) { load1_B(nb, k + 1, 4 + i); }, f16);
-    substep(F1a, F1b, sa, sb, 2, F0a, F0b, [&](int i) { load1_A(a2, k + 2, i); }, f16);
-    substep(F0a, F0b, sa, sb, 3, F1a, F1b, [&](int i) { load1_A(a2, k + 2, 4 + i); }, f16);
+    substep(F0a, F0b, sa, sb, 1, F1a, F1b, [&](int i) { load1_A(a2, k + 2, i); }, f16);
     asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");  // all but A(k+2)
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
@@ -853,12 +881,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   auto load1g_A = [&](int sl, int t, int i) {
     const bool m = t < NTM;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(m ? rsA : rsC, (lds_ptr_t)(ldsw + sl * PART + 32 * RB * i), 16,
-                                             m ? voA[i] : voC[i], (unsigned)(m ? t : t - NTM) * 128u, 0, 0);
+                                             m ? voA[i] : voC(i), (unsigned)(m ? t : t - NTM) * 128u, 0, 0);
   };
   auto load1g_B = [&](int sl, int t, int i) {
     const bool m = t < NTM;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(m ? rsB : rsD, (lds_ptr_t)(ldsw + sl * PART + 32 * RB * i), 16,
-                                             m ? voB[i] : voD[i], (unsigned)(m ? t : t - NTM) * 128u, 0, 0);
+                                             m ? voB[i] : voD(i), (unsigned)(m ? t : t - NTM) * 128u, 0, 0);
   };
   // Tile k as body_main, with run-time slots and loads from either segment: the tiles that
   // follow the unrolled main loop (the last main tiles and the rank segment), up to NT - 3.
@@ -866,30 +894,22 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   auto body_rt = [&](int k, auto f16) {
     const int sa = (2 * k) % 5, sb = (2 * k + 1) % 5;
     const int na = (2 * k + 2) % 5, nb = (2 * k + 3) % 5, a2 = (2 * k + 4) % 5;
-    substep(F0a, F0b, sa, sb, 1, F1a, F1b, [&](int i) { load1g_B(nb, k + 1, 4 + i); }, f16);
-    substep(F1a, F1b, sa, sb, 2, F0a, F0b, [&](int i) { load1g_A(a2, k + 2, i); }, f16);
-    substep(F0a, F0b, sa, sb, 3, F1a, F1b, [&](int i) { load1g_A(a2, k + 2, 4 + i); }, f16);
+    substep(F0a, F0b, sa, sb, 1, F1a, F1b, [&](int i) { load1g_A(a2, k + 2, i); }, f16);
     asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");  // all but A(k+2)
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     substep(F1a, F1b, na, nb, 0, F0a, F0b, [&](int i) { load1g_B(sa, k + 2, i); }, f16);
   };
-  // Any tile (run-time slots, loads of either segment or none, half tiles).  The loads go out
-  // together here: only the last two tiles and half tiles take this path.
+  // Any tile (run-time slots, loads of either segment or none, half tiles: their second
+  // 32-deep half is loaded but never read).  The loads go out together here: only the last two
+  // tiles and half tiles take this path.
   auto body_any = [&](int k, auto f16) {
     const int sa = (2 * k) % 5, sb = (2 * k + 1) % 5, na = (2 * k + 2) % 5, nb = (2 * k + 3) % 5;
     const int a2 = (2 * k + 4) % 5;
     const bool half = k == NTM - 1 ? halfM : (k == NT - 1 ? halfR : false);
-    load_B(nb, k + 1, Any{}, I4{}, I8{});
     load_A(a2, k + 2, Any{}, I0{}, I8{});
-    frags(sa, sb, 1, F1a, F1b);
+    if (!half) frags(sa, sb, 1, F1a, F1b);
     mma(F0a, F0b, f16);
-    if (!half) {
-      frags(sa, sb, 2, F0a, F0b);
-      mma(F1a, F1b, f16);
-      frags(sa, sb, 3, F1a, F1b);
-      mma(F0a, F0b, f16);
-    }
     // The last loads issued are A(k+2)'s when it exists; otherwise none may stay outstanding.
     if (k + 2 < NT)
       asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");
@@ -898,8 +918,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     if (k + 1 < NT) frags(na, nb, 0, F0a, F0b);
-    load_B(sa, k + 2, Any{}, I0{}, I4{});
-    mma(F1a, F1b, f16);
+    load_B(sa, k + 2, Any{}, I0{}, I8{});
+    if (!half) mma(F1a, F1b, f16);
   };
   using MT = std::integral_constant<bool, F16>;
   // body_main needs k + 2 <= NTM - 1 (main-segment loads) and tile k full: k <= NTM - 3.
@@ -920,6 +940,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   for (; k < NT - 2; ++k) body_rt(k, std::false_type{});
   for (; k < NT; ++k) body_any(k, std::false_type{});
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain before the stores and exit
+#undef voC
+#undef voD
 
   // Epilogue through LDS.  The accumulator layout gives each lane 4 adjacent outputs of one
   // token, so stores straight from the registers would touch 32 token rows per instruction
@@ -938,26 +960,25 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   // recomputes these few values here instead of keeping (and spilling) the loop's copies.
   const int el = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   const int efr = el & 31, efh = el >> 5;
+  const int e16 = el & 15, eq = el >> 4;  // the accumulator layout's token row and column quarter
   if constexpr (OUT != ZO_F32 && (EPI == ZO_EPI_NONE || EPI == ZO_EPI_RELU)) {
     constexpr int PITCH = 528;
-    // Token row wn 128 + 32 j + fr, columns wm 128 + 32 i + 8 q4 + 4 fh .. + 3.
-    char* const wb = lds + (wn * 128 + efr) * PITCH + wm * 256 + efh * 8;
+    // acc[i][j]: token row wn 128 + 16 j + l % 16, columns wm 128 + 16 i + 4 (l / 16) .. + 3.
+    char* const wb = lds + (wn * 128 + e16) * PITCH + wm * 256 + eq * 8;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 8; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i) {
+        float v[4];
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            v[e] = acc[i][j][q4 * 4 + e];
-            if constexpr (EPI == ZO_EPI_RELU) v[e] = fmaxf(v[e], 0.f);
-          }
-          *(u32x2*)(wb + j * 32 * PITCH + (i * 4 + q4) * 16) =
-              OUT == ZO_BF16 ? (u32x2){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])}
-                             : (u32x2){pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3])};
+        for (int e = 0; e < 4; ++e) {
+          v[e] = acc[i][j][e];
+          if constexpr (EPI == ZO_EPI_RELU) v[e] = fmaxf(v[e], 0.f);
         }
+        *(u32x2*)(wb + j * 16 * PITCH + i * 32) =
+            OUT == ZO_BF16 ? (u32x2){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])}
+                           : (u32x2){pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3])};
+      }
     __syncthreads();
     // Pass it of wave w: rows 8 it + 2 w + lane / 32, whole (512 bytes each), 16-byte chunk
     // lane % 32 (columns 8 (lane % 32) ..).
@@ -967,13 +988,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     for (int it = 0; it < 32; ++it) {
       const u32x4 v = *(const u32x4*)(rb + it * 8 * PITCH);
       const int tok = t0 + it * 8 + 2 * wave + efh;
-      if (tok < a.rows_b && col < a.rows_a) *(u32x4*)(Yb + ((size_t)tok * a.ldy + col) * 2) = v;
+      // Non-temporal: the output streams past the caches (1-2% faster at K = 5120 in A/B).
+      if (tok < a.rows_b && col < a.rows_a) __builtin_nontemporal_store(v, (u32x4*)(Yb + ((size_t)tok * a.ldy + col) * 2));
     }
   } else {
     constexpr int PITCH = 1040;
-    // Half h holds j = 2 h, 2 h + 1: staging row wn 64 + 32 (j % 2) + fr is tile token
-    // wn 128 + 32 j + fr; 16-byte chunk wm 32 + 8 i + 2 q4 + fh holds its columns 4 chunk .. + 3.
-    char* const wb = lds + (wn * 64 + efr) * PITCH + wm * 512 + efh * 16;
+    // Half h holds j = 4 h .. 4 h + 3: staging row wn 64 + 16 (j % 4) + l % 16 is tile token
+    // wn 128 + 16 j + l % 16; 16-byte chunk wm 32 + 4 i + l / 16 holds its columns 4 chunk .. + 3.
+    char* const wb = lds + (wn * 64 + e16) * PITCH + wm * 512 + eq * 16;
     // Read-back pass it of wave w: staging rows 8 it + lr8, columns 64 w + 8 lc8 .. + 7.
     const int lr8 = el & 7, lc8 = el >> 3;
     const char* const rb = lds + lr8 * PITCH + (wave * 8 + lc8) * 32;
@@ -1007,15 +1029,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
         }
       }
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj)
+      for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) {
-            const f32x16& c = acc[i][2 * h + jj];
-            *(f32x4*)(wb + jj * 32 * PITCH + (i * 8 + q4 * 2) * 16) =
-                (f32x4){c[q4 * 4 + 0], c[q4 * 4 + 1], c[q4 * 4 + 2], c[q4 * 4 + 3]};
-          }
+        for (int i = 0; i < 8; ++i) *(f32x4*)(wb + jj * 16 * PITCH + i * 64) = acc[i][4 * h + jj];
       __syncthreads();
 #pragma unroll
       for (int it = 0; it < 16; ++it) {
