@@ -158,7 +158,12 @@ int zo_subspace_refresh_noalloc(int count, const zo_panel* panels, int r,
  *   T            rows (tokens) per block; m, n: W is m x n (out x in).
  *   X            device, block b starts at X + b * x_block_stride elements,
  *                each block T x n.  x_block_stride = 0: all blocks share one
- *                X (the first layer of a network); otherwise >= T*n.
+ *                X (the first layer of a network); otherwise >= T*n.  With
+ *                a shared X and nblk > 1, X W^T is computed once (into an
+ *                fp32 T x m region of the workspace, which the workspace size
+ *                includes) and each block adds its own rank-r term to it
+ *                before the single rounding (plain and ReLU epilogues; the
+ *                residual and gated ones compute every block in full).
  *   W            device, m x n.  in_dtype ZO_BF16, ZO_F16 or ZO_F32 for X
  *                and W.
  *   U, V         device fp32, m x r and n x r (column-orthonormal).
