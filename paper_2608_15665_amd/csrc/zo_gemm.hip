@@ -212,16 +212,24 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// 16x16x32 MFMA on 16-byte fragments of eight 16-bit values: fp16 or bf16.  Lane l holds row
-// l % 16 of A (and of B's transpose) at k (l / 16) 8 .. + 7; the result's lane l holds rows
-// 4 (l / 16) .. + 3 of column l % 16.
+// 16x16x32 MFMA on 16-byte fragments of eight 16-bit values, fp16 or bf16, accumulating in place
+// into c.  Lane l holds row l % 16 of A (and of B's transpose) at k (l / 16) 8 .. + 7; the
+// result's lane l holds rows 4 (l / 16) .. + 3 of column l % 16.
+//
+// Written as inline assembly with c tied to the destination in AGPRs.  With the builtin, a
+// kernel holding 64 such accumulators next to 128 fragment registers (every VGPR and AGPR in
+// use) gets the untied form for part of its MFMAs: those write a fresh AGPR quad, and each
+// trip round the loop then starts with ~300 AGPR/VGPR copies that put the accumulators back.
+// The hazard recognizer does not look inside inline assembly, so the caller provides what it
+// would: 2 wait states between a VALU write of c and the first MFMA reading it, and 12 (8
+// passes + 4) between the last MFMA and any other instruction reading or writing c.  Fragment
+// registers are only ever sources A and B, which need no wait before being overwritten.
 template <bool F16>
-__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+__device__ __forceinline__ void mfma16(f32x4& c, bf16x8 a, bf16x8 b) {
   if constexpr (F16)
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
-                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+    asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
   else
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
 }
 
 template <int WM, int WN, int TM, int TN, bool F16>
@@ -636,47 +644,43 @@ int launch_gemm_bf16(GemmArgs a, hipStream_t stream) {
 // ---------------------------------------------------------------------------
 // Main GEMM for K % 32 == 0: the kernel every model-shaped call takes.
 //
-// 256 x 256 output tile per workgroup of 4 waves (one per SIMD), each wave a
-// 128 x 128 sub-tile held in 16 accumulators of the 32x32x16 MFMA (256 AGPRs).
+// 256 x 256 output tile per workgroup of 4 waves (one per SIMD), each wave a 128 x 128
+// sub-tile held in 64 accumulators of the 16x16x32 MFMA (256 AGPRs, updated in place).
 //
-// K is walked in tiles of 64, so every LDS row holds 128 bytes: one whole cache
-// line per row, which the load path moves ~1.6x faster than 64-byte half lines
-// (measured with load-only kernels of the same traffic).  Tiles are brought in by
-// direct global->LDS buffer loads (buffer_load_dwordx4 ... lds: 8 rows x 128 B per
-// instruction, a per-lane row offset fixed for the whole loop and the k offset in a
-// scalar register, so the loop has no address arithmetic).  Row r keeps its 16-byte
-// chunk c at position c ^ f(r), f(r) = (r >> 1) & 7: the fragment reads (16
-// consecutive rows at one chunk per 16-lane pass) are conflict free.
+// K is walked in tiles of 64, so every LDS row holds 128 bytes: one whole cache line per row,
+// which the load path moves ~1.6x faster than 64-byte half lines (measured with load-only
+// kernels of the same traffic).  Tiles are brought in by direct global->LDS buffer loads
+// (buffer_load_dwordx4 ... lds: 8 rows x 128 B per instruction, a per-lane row offset fixed for
+// the whole loop and the k offset in a scalar register, so the loop has no address arithmetic).
+// Row r keeps its 16-byte chunk c at position c ^ f(r), f(r) = (r >> 1) & 7: the fragment reads
+// (16 consecutive rows at one chunk per 16-lane group) are conflict free.
 //
-// LDS ring: the 160 KB as 5 slots of 32 KB, one per part of a tile (part A = the
-// 256 W rows, part B = the 256 X rows): A(t) in slot 2t % 5, B(t) in slot (2t+1) % 5.
-// One barrier per tile, barrier(k), after the wave's last fragment reads of tile k:
-// every wave has finished with tile k, and tile k+1 has landed.  Tile k's two slots
-// are then refilled with B(k+2) and A(k+3).  The loads are spread evenly over the
-// tile's four 16-deep substeps (one load per four MFMAs): B(k+2) half in the last
-// substep of tile k and half in the first of tile k+1, A(k+3) in the next two.
-// Issued in bursts they would fill the address unit's queue and block the wave's
-// MFMA issue behind them; spread out they hide under the MFMAs.  So a B part has a
-// tile-time to land and an A part two; at barrier(k) only A(k+2), the last 8 loads
-// issued, may be outstanding.  Fragments for the next substep are read while the
-// current one's MFMAs run; scheduling fences keep each substep's MFMAs, reads and
-// loads in that interleave.
+// LDS ring: the 160 KB as 5 slots of 32 KB, one per part of a tile (part A = the 256 W rows,
+// part B = the 256 X rows): A(t) in slot 2t % 5, B(t) in slot (2t+1) % 5.  A tile is two
+// 32-deep substeps of 64 MFMAs each, with one barrier between them.  Substep 0 runs the MFMAs of
+// the tile's first half, reads the fragments of its second half and issues A(k+2) (into the
+// slot B(k-1) vacated); then the wave waits for everything but A(k+2) and meets the others at
+// the barrier: every wave is done reading tile k and tile k+1 has landed.  Substep 1 runs the
+// second half, reads tile k+1's first half and issues B(k+2) into tile k's A slot.  So every
+// part has a whole tile or more to land.  The loads are spread one per eight MFMAs and the
+// fragment reads one per four, in the order the next substep first uses them; scheduling
+// fences after every MFMA keep that interleave (left to itself the compiler bunches the reads
+// and loads, and the wave's MFMA issue stalls behind them).
 //
-// The rank-rc correction is rc/64 more k-tiles through the same pipeline, with the
-// A operand taken from ca (per block, rows_a x rc) and the B operand from cb (per
-// block, rows_b x rc).  The last tile of a segment whose length is an odd multiple
-// of 32 holds 32 valid columns: only its first two substeps are computed (the other
-// half of its rows is loaded but never read).  So every accumulator sees its k terms
-// in ascending order, 16 at a time, whatever the tiling.  Rows past rows_a / rows_b
-// are loaded from the last valid row (never stored).  F16: the main tiles run the
-// fp16 MFMA and the correction tiles (bf16 hi/lo operands) the bf16 MFMA.  OUT
-// (zo_dtype of Y) and EPI (zo_epilogue) are template parameters: with all 256
-// accumulators live, one store path per instantiation keeps the epilogue free of
-// per-store branches (a run-time choice there made the compiler keep spilled VGPR
-// copies of the accumulators, one of which it stored wrongly).
+// The rank-rc correction is rc/64 more k-tiles through the same pipeline, with the A operand
+// taken from ca (per block, rows_a x rc) and the B operand from cb (per block, rows_b x rc).
+// The last tile of a segment whose length is an odd multiple of 32 holds 32 valid columns: only
+// its first substep is computed (the other half of its rows is loaded but never read).  So
+// every accumulator sees its k terms in ascending order, 32 at a time, whatever the tiling.
+// Rows past rows_a / rows_b are loaded from the last valid row (never stored).  F16: the main
+// tiles run the fp16 MFMA and the correction tiles (bf16 hi/lo operands) the bf16 MFMA.  OUT
+// (zo_dtype of Y) and EPI (zo_epilogue) are template parameters: with all 256 accumulators
+// live, one store path per instantiation keeps the epilogue free of per-store branches (a
+// run-time choice there made the compiler keep spilled VGPR copies of the accumulators, one of
+// which it stored wrongly).
 //
-// Each operand's buffer descriptor spans its rows x K (or rc) elements, so the host
-// takes this kernel only when every such span is below 2^32 bytes.
+// Each operand's buffer descriptor spans its rows x K (or rc) elements, so the host takes this
+// kernel only when every such span is below 2^32 bytes.
 constexpr int MAIN_RB = 128;               // bytes per LDS row (64 bf16)
 constexpr int MAIN_PART = 256 * MAIN_RB;   // one part of a tile: 32 KB
 constexpr int MAIN_SLOTS = 5;
@@ -802,11 +806,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
     for (int j = 0; j < 8; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.f;
+  // The zeros are in place (in AGPRs) at least 2 wait states before any MFMA reads them.
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    asm volatile("s_nop 1" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]),
+                 "+a"(acc[i][4]), "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7]));
   auto mma = [&](const bf16x8* fa, const bf16x8* fb, auto f16) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[i][j] = mfma16<decltype(f16)::value>(fa[i], fb[j], acc[i][j]);
+      for (int j = 0; j < 8; ++j) mfma16<decltype(f16)::value>(acc[i][j], fa[i], fb[j]);
   };
   // The n-th fragment read of substep s from slots sa / sb, in the order the next substep first
   // uses them: A0 (MFMA 0), B0..B7 (MFMAs 0..7), then A1..A7 (MFMAs 8, 16, ..., 56).
@@ -838,7 +847,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
                      auto ld, auto f16) {
 #pragma unroll
     for (int x = 0; x < 64; ++x) {
-      acc[x >> 3][x & 7] = mfma16<decltype(f16)::value>(fa[x >> 3], fb[x & 7], acc[x >> 3][x & 7]);
+      mfma16<decltype(f16)::value>(acc[x >> 3][x & 7], fa[x >> 3], fb[x & 7]);
       if (x % 4 == 0) frag1(ra, rb, rs, x / 4, na, nb);
       if (x % 8 == 3) ld(x / 8);
       __builtin_amdgcn_sched_barrier(0);
@@ -940,6 +949,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   for (; k < NT - 2; ++k) body_rt(k, std::false_type{});
   for (; k < NT; ++k) body_any(k, std::false_type{});
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // drain before the stores and exit
+  // 24 wait states after the last MFMA before the accumulators are read.  They then pass
+  // through empty statements ordered after the wait, so no read or copy of them can be placed
+  // ahead of it.
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    asm volatile("" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]), "+a"(acc[i][4]),
+                 "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7]));
 #undef voC
 #undef voD
 
