@@ -1094,6 +1094,179 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   }
 }
 
+// Projection of the prepare pass with the combine fused: for every X block and every factor f
+// of a stack of `count` (each 2 RP rows of Vt2: the hi rows, then the lo rows),
+//   P = (X_b Vt2_hi^T + X_b Vt2_lo^T) * unscale,  written as [P_hi | P_hi | P_lo] (bf16, 3 RP),
+// which is the left operand of the fused GEMM's rank-r segment.  The projection reads every X
+// block once and is bound by that stream, so the tile is narrow: 256 tokens x 128 factor rows
+// per workgroup, the 4 waves side by side along the tokens (64 tokens x 128 rows each, 8 x 4
+// accumulators of the 16x16x32 MFMA), so a k-tile's MFMAs (1024 cycles per wave) take less time
+// than its 32 KB of X takes to arrive.  A factor's hi and lo rows lie in the same tile and the
+// same lane (accumulators i and i + RP / 16), so the combine, the hi/lo split and the rounding
+// happen in registers and the fp32 projection never goes to memory.  Every accumulator sums
+// its k terms in ascending order, 32 at a time, as in the main GEMM: the values are those of
+// the unfused projection followed by the separate combine.
+//
+// K is walked in tiles of 64 through a 3-stage LDS ring (X part 32 KB, factor part 16 KB per
+// stage; rows swizzled as in the main GEMM), filled by direct global->LDS loads two tiles ahead,
+// with one barrier per tile.  Rows past T or past the stack are loaded from the last valid row
+// and not stored.
+constexpr int PJ_XPART = 256 * 128;
+constexpr int PJ_STAGE = PJ_XPART + 128 * 128;
+
+struct ProjArgs {
+  const bf16_t* V;           // rows_v x K: the stacked Vt2 of `count` factors
+  const bf16_t* X;           // per block T x K
+  long long x_block_stride;  // elements
+  int rows_v, T, K, count;
+  int tiles_t, tiles_c, total_tiles;
+  float unscale;             // 1, or 1/256 for fp16 (whose Vt2 holds 256 V)
+  bf16_t* pc[ZO_MAX_GROUP];  // factor f's output: (nx T) x 3 RP
+};
+
+template <bool F16, int RP>
+__global__ __launch_bounds__(256, 1) void k_proj(ProjArgs a) {
+  static_assert(RP == 32 || RP == 64, "factors of 64 or 128 rows");
+  constexpr int NF = 128 / (2 * RP);  // factors per tile
+  constexpr int R16 = RP / 16;
+  __shared__ __attribute__((aligned(1024))) char lds[3 * PJ_STAGE];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // XCD-aware order; the factor tiles of one token tile are adjacent, so its X tile comes
+  // from the XCD's L2 after the first of them.
+  const int w = blockIdx.x, nt = a.total_tiles;
+  const int xcd = w & 7, widx = w >> 3;
+  const int lt = xcd * (nt >> 3) + min(xcd, nt & 7) + widx;
+  const int ct = __builtin_amdgcn_readfirstlane(lt % a.tiles_c);
+  const int bt = lt / a.tiles_c;
+  const int blk = __builtin_amdgcn_readfirstlane(bt / a.tiles_t);
+  const int t0 = __builtin_amdgcn_readfirstlane((bt % a.tiles_t) * 256);
+  const int c0 = ct * 128;
+  const __amdgpu_buffer_rsrc_t rsX =
+      make_rsrc(a.X + (long long)blk * a.x_block_stride, (unsigned)a.T * a.K * 2);
+  const __amdgpu_buffer_rsrc_t rsV = make_rsrc(a.V, (unsigned)a.rows_v * a.K * 2);
+  // DMA: load i of a wave writes rows 8 (wave + 4 i) .. + 7 of a part (8 loads for the 256 X
+  // rows, 4 for the 128 factor rows); lane l writes row l / 8 at physical chunk l % 8.
+  const int drow = lane >> 3;
+  const int lch = (lane & 7) ^ f8(8 * wave + drow);
+  unsigned voX[8], voV[4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) voX[i] = dma_off(t0 + 8 * (wave + 4 * i) + drow, a.T, a.K, lch);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) voV[i] = dma_off(c0 + 8 * (wave + 4 * i) + drow, a.rows_v, a.K, lch);
+  char* const ldsw = lds + 8 * wave * 128;
+  auto load = [&](int st, int t) {
+    char* d = ldsw + st * PJ_STAGE;
+    const unsigned so = (unsigned)t * 128u;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsX, (lds_ptr_t)(d + 32 * 128 * i), 16, voX[i], so, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsV, (lds_ptr_t)(d + PJ_XPART + 32 * 128 * i), 16, voV[i], so,
+                                               0, 0);
+  };
+  // Fragments of substep s: factor rows 16 i + l % 16 (A operand, i < 8) and the wave's tokens
+  // 64 wave + 16 j + l % 16 (B operand, j < 4), chunk 4 s + l / 16.
+  const int fr = lane & 15, fq = lane >> 4;
+  const int ff = f8(fr);
+  auto frags = [&](int st, int s, bf16x8* fa, bf16x8* fb) {
+    const int ch = ((4 * s + fq) ^ ff) * 16;
+    const char* pv = lds + st * PJ_STAGE + PJ_XPART + fr * 128 + ch;
+    const char* px = lds + st * PJ_STAGE + (wave * 64 + fr) * 128 + ch;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) fa[i] = *(const bf16x8*)(pv + i * 16 * 128);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)(px + j * 16 * 128);
+  };
+  // acc[i][j]: factor rows 16 i + 4 (l / 16) .. + 3 of the tile, token 64 wave + 16 j + l % 16.
+  f32x4 acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)  // the zeros in place 2 wait states before the first MFMA
+    asm volatile("s_nop 1" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]));
+  auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mfma16<F16>(acc[i][j], fa[i], fb[j]);
+  };
+
+  const int NT = (a.K + 63) / 64;
+  const bool half = (a.K & 63) != 0;  // the last tile holds 32 valid columns
+  load(0, 0);
+  if (NT > 1) {
+    load(1, 1);
+    asm volatile("s_waitcnt vmcnt(12)" ::: "memory");  // this wave's loads of tile 0 landed
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  // Tile t (both 32-deep substeps, or only the first for the last tile of an odd K / 32).
+  auto tile = [&](int t, bool two) {
+    const int st = t % 3;
+    if (t + 2 < NT) load((t + 2) % 3, t + 2);  // into the stage tile t - 1 vacated
+    bf16x8 fa[8], fb[4], ga[8], gb[4];
+    frags(st, 0, fa, fb);
+    if (two) frags(st, 1, ga, gb);
+    mma(fa, fb);
+    if (two) mma(ga, gb);
+    // Tile t + 1 landed (only tile t + 2's loads may be in flight) and this wave's reads of
+    // stage st are done; after the barrier every wave may overwrite it.
+    if (t + 2 < NT)
+      asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  const int NTF = half ? NT - 1 : NT;
+  for (int t = 0; t < NTF; ++t) tile(t, true);
+  if (half) tile(NT - 1, false);
+  // 24 wait states after the last MFMA, then the accumulators pass through tied empty
+  // statements so that no read of them is placed ahead of the wait.
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    asm volatile("" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]));
+
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int gf = ct * NF + f;
+    if (gf >= a.count) break;
+    bf16_t* const pc = a.pc[gf];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tok = t0 + wave * 64 + 16 * j + fr;
+      if (tok >= a.T) continue;
+      bf16_t* const o = pc + ((long long)blk * a.T + tok) * (3 * RP) + 4 * fq;
+#pragma unroll
+      for (int ii = 0; ii < R16; ++ii) {
+        const int ih = f * 2 * R16 + ii, il = ih + R16;
+        float hv[4], lv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float pv = (acc[ih][j][e] + acc[il][j][e]) * a.unscale;
+          const bf16_t h = f32_to_bf16(pv);
+          hv[e] = bf16_to_f32(h);
+          lv[e] = pv - hv[e];
+        }
+        const u32x2 hi = (u32x2){pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3])};
+        const u32x2 lo = (u32x2){pack_bf16x2(lv[0], lv[1]), pack_bf16x2(lv[2], lv[3])};
+        *(u32x2*)(o + 16 * ii) = hi;
+        *(u32x2*)(o + RP + 16 * ii) = hi;
+        *(u32x2*)(o + 2 * RP + 16 * ii) = lo;
+      }
+    }
+  }
+}
+
 template <bool F16, int OUT>
 void launch_main_epi(const GemmArgs& a, dim3 grid, hipStream_t stream) {
   if (a.epi == EPI_BASE)
@@ -1267,6 +1440,49 @@ static int launch_pcombine(const PlinearPlan& p, const float* p2, int ld2, void*
   return zo_hip_status(hipGetLastError(), "k_pcombine");
 }
 
+// The fused projection (k_proj): 16-bit factors of 64 or 128 rows (rp = 32 or 64), each
+// operand's buffer descriptor below 2^32 bytes.
+static bool proj_fused_fits(const PlinearPlan& p, int count) {
+  const unsigned long long lim = (1ull << 32) - 256;
+  return p.in16 && (p.rp == 32 || p.rp == 64) && p.n % 32 == 0 && count >= 1 && count <= ZO_MAX_GROUP &&
+         (unsigned long long)p.T * p.n * 2 <= lim && (unsigned long long)count * 2 * p.rp * p.n * 2 <= lim;
+}
+
+// [P_hi | P_hi | P_lo] of `count` stacked factors (vt: count x 2 rp rows) for every distinct X
+// block, into pc[i] for factor i.
+static int launch_proj_fused(const PlinearPlan& p, const void* X, const void* vt, int count,
+                             bf16_t* const* pc, hipStream_t stream) {
+  ProjArgs a{};
+  a.V = (const bf16_t*)vt;
+  a.X = (const bf16_t*)X;
+  a.x_block_stride = p.x_block_stride;
+  a.rows_v = count * 2 * p.rp;
+  a.T = p.T;
+  a.K = p.n;
+  a.count = count;
+  a.tiles_t = (p.T + 255) / 256;
+  a.tiles_c = (a.rows_v + 127) / 128;
+  const long long total = (long long)p.nx * a.tiles_t * a.tiles_c;
+  if (total <= 0) return ZO_OK;
+  if (total > 0x7fffffffLL) {
+    zo_set_error("perturbed linear: too many projection tiles (%lld)", total);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  a.total_tiles = (int)total;
+  a.unscale = p.in_dtype == ZO_F16 ? 1.f / ZO_F16_RSCALE : 1.f;
+  for (int i = 0; i < count; ++i) a.pc[i] = pc[i];
+  const dim3 grid((unsigned)total);
+  const bool f16 = p.in_dtype == ZO_F16;
+  if (p.rp == 32) {
+    if (f16) hipLaunchKernelGGL((k_proj<true, 32>), grid, dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL((k_proj<false, 32>), grid, dim3(256), 0, stream, a);
+  } else {
+    if (f16) hipLaunchKernelGGL((k_proj<true, 64>), grid, dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL((k_proj<false, 64>), grid, dim3(256), 0, stream, a);
+  }
+  return zo_hip_status(hipGetLastError(), "k_proj");
+}
+
 size_t zo_plinear_group_ws(const PlinearPlan& p, int count) {
   if (!p.in16 || count < 2) return 0;
   return zo_align256((size_t)count * 2 * p.rp * p.n * 2) +
@@ -1295,6 +1511,14 @@ int zo_plinear_prepare_group(const PlinearPlan* plans, int count, const int* blk
     if ((st = launch_transpose_v(plans[i], V[i], gvt + (size_t)i * w2 * p0.n * 2, stream)) != ZO_OK) return st;
     if ((st = launch_bprime(plans[i], tab, eps, U[i], Z[i], w.bp, stream)) != ZO_OK) return st;
   }
+  // A stack of several factors stays on the main GEMM's 256-row tiles (two factors of 128 rows
+  // per X tile: the stacked q, k, v run 0.50 ms there against 0.72 ms in three 128-row tiles),
+  // with the separate combine; only a 64-row pair shares one 128-row tile.
+  if (2 * p0.rp * count <= 128 && proj_fused_fits(p0, count)) {
+    bf16_t* pc[ZO_MAX_GROUP];
+    for (int i = 0; i < count; ++i) pc[i] = (bf16_t*)zo_plinear_ws(plans[i], ws[i]).pp;
+    return launch_proj_fused(p0, X, gvt, count, pc, stream);
+  }
   if ((st = launch_projection(p0, X, gvt, count * w2, gp2, stream)) != ZO_OK) return st;
   for (int i = 0; i < count; ++i)
     if ((st = launch_pcombine(plans[i], gp2 + (size_t)i * w2, count * w2, zo_plinear_ws(plans[i], ws[i]).pp,
@@ -1311,6 +1535,10 @@ int zo_plinear_project(const PlinearPlan& p, const void* X, void* ws, hipStream_
   int st;
   const long long xs = p.x_block_stride;
   if (p.in16) {
+    if (proj_fused_fits(p, 1)) {
+      bf16_t* pc = (bf16_t*)pp;
+      return launch_proj_fused(p, X, vt, 1, &pc, stream);
+    }
     if ((st = launch_projection(p, X, vt, 2 * p.rp, p2, stream)) != ZO_OK) return st;
     return launch_pcombine(p, (const float*)p2, 2 * p.rp, pp, stream);
   }

@@ -1,8 +1,9 @@
-"""The main GEMM's accumulators stay in place and its inline-asm MFMAs keep their wait states.
+"""The GEMM kernels' accumulators stay in place and their inline-asm MFMAs keep their wait states.
 
-k_gemm_main issues its MFMAs as inline assembly with the accumulator tied to the destination
-(the builtin's untied form made the register allocator rotate the accumulators through fresh
-AGPRs and copy them back on every trip round the loop).  The hazard recognizer does not see
+k_gemm_main (the fused GEMM) and k_proj (the prepare's projection) issue their MFMAs as inline
+assembly with the accumulator tied to the destination (the builtin's untied form made the
+register allocator rotate the accumulators through fresh AGPRs and copy them back on every trip
+round the loop).  The hazard recognizer does not see
 inside inline assembly, so the kernel orders the accumulators through its own fences: zeros
 written, then `s_nop 1` (2 wait states) before the first MFMA; after the last MFMA, three
 `s_nop 7` (24 wait states) before anything else touches them.  This reads the gfx950 assembly
@@ -51,17 +52,18 @@ def _functions(text, pattern):
     return funcs
 
 
-def test_main_gemm_mfma_in_place_and_fenced(tmp_path):
+@pytest.mark.parametrize("kernel,min_kernels,min_mfma", [("k_gemm_main", 12, 256), ("k_proj", 4, 64)])
+def test_mfma_in_place_and_fenced(tmp_path, kernel, min_kernels, min_mfma):
     try:
         _build.hipcc()
     except RuntimeError:
         pytest.skip("hipcc not available")
     text = _asm(os.path.join(_build.CSRC, "zo_gemm.hip"), str(tmp_path))
-    funcs = _functions(text, r"k_gemm_main")
-    assert len(funcs) >= 12
+    funcs = _functions(text, kernel + r"I")
+    assert len(funcs) >= min_kernels
     for name, ins in funcs.items():
         mfma = [i for i, t in enumerate(ins) if t.startswith("v_mfma")]
-        assert len(mfma) > 256, name
+        assert len(mfma) >= min_mfma, name
         for i in mfma:
             ops = [o.strip() for o in ins[i].split(None, 1)[1].split(",")]
             assert ops[0] == ops[3], (name, ins[i])  # destination == accumulator source
