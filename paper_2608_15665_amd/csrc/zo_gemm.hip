@@ -48,6 +48,11 @@ constexpr int BK = 64;  // bf16 elements per K tile = 128 bytes per LDS row
 // base X W^T shared by every block, added to the block's rank-r term before the rounding.
 constexpr int EPI_BASE = 16;       // Y_b = base + result
 constexpr int EPI_BASE_RELU = 17;  // Y_b = max(base + result, 0)
+// The prepare's projection of a stack of 16-bit factors (A = the stacked [V_hi; V_lo] rows, 2 rp
+// per factor, rp = 32 or 64): P = (hi part + lo part) * unscale of every factor, written to the
+// factor's own buffer as [P_hi | P_hi | P_lo] (bf16, 3 rp per token); Y is not used.
+constexpr int EPI_PROJ32 = 18;
+constexpr int EPI_PROJ64 = 19;
 
 // Swizzle of the 16-byte chunk index within a 128-byte LDS row; conflict free
 // for ds_read_b128 of 8 or 16 consecutive rows at one logical chunk.
@@ -71,6 +76,11 @@ struct GemmArgs {
   long long r_block_stride;    // elements; 0 = one R shared by all blocks
   int tiles_a, tiles_b, total_tiles;
   int blk_inner;               // k_gemm_main: 1 = the blocks of one output tile run consecutively
+  // EPI_PROJ32 / EPI_PROJ64: factor f's output (nblk x rows_b tokens x 3 rp), the number of
+  // factors, and the scale of the combined projection (1, or 1/256 for fp16 inputs).
+  bf16_t* pc[ZO_MAX_GROUP];
+  int pcount;
+  float unscale;
 };
 
 // Four fp32 accumulator values as element idx.. of an OUT-typed (zo_dtype) array.
@@ -519,105 +529,133 @@ __global__ __launch_bounds__(256) void k_pcombine(const float* __restrict__ P2, 
 // B_b[i][a] = s_b eps sum_c U[i][c] Z_{j(b)}[c][a] (a < r; 0 for r <= a < rp).
 // fp32 output: m x rp per block.  bf16 output: m x 3 rp per block as
 // [B_hi | B_lo | B_hi].
-// One workgroup forms C = eps U Z_j for 128 rows and one query j (U rows and Z_j
-// staged in LDS 32 columns of K at a time; each thread owns 4 rows x rp/8
-// adjacent columns), then writes s_b C for every block b of query j.  The
-// bf16 split is odd in its argument (round to nearest even is symmetric), so
-// the blocks of one query share one product.
-constexpr int BP_ROWS = 128;
+// One workgroup forms C = eps U Z_j for R rows and one query j: Z_j and the
+// workgroup's U rows are staged in LDS, and each thread owns RR rows (R / RR
+// apart) and 8 adjacent columns (K ascending, one fused multiply-add per term,
+// as a plain dot product).
+// It then writes s_b C for every block b of query j, 16 bytes per store, so a
+// wave's three stores of a block cover 8 whole rows of [B_hi | B_lo | B_hi]
+// (3 KB contiguous at rp = 64).  The bf16 split is odd in its argument (round
+// to nearest even is symmetric), so the blocks of one query share one product.
+template <int RPK>
+struct BpShape {
+  static constexpr int RP = 32 * RPK;
+  static constexpr int G = RP / 8;    // column groups of a row
+  // Rows per thread: wider factors take more, so the staged Z_j rows serve more outputs.
+  static constexpr int RR = RPK <= 2 ? 1 : (RPK == 3 ? 2 : 4);
+  static constexpr int RT = 256 / G;  // rows per pass of the 256 threads (RP = 96: 21, 4 idle)
+  static constexpr int R = RR * RT;   // rows per workgroup
+};
 
 template <int RPK>
 __global__ __launch_bounds__(256) void k_bprime(const float* __restrict__ U,
                                                 const float* __restrict__ Z, int m, int r,
                                                 int rp, int nblk, float eps, BlkTable tab,
                                                 void* Bp, int out_bf16) {
-  constexpr int RP = 32 * RPK;
-  constexpr int CPT = RP / 8;
-  __shared__ __attribute__((aligned(16))) float Ut[32][BP_ROWS + 4];
-  __shared__ __attribute__((aligned(16))) float Zl[32][RP];
+  constexpr int RP = BpShape<RPK>::RP, G = BpShape<RPK>::G, RR = BpShape<RPK>::RR;
+  constexpr int RT = BpShape<RPK>::RT, R = BpShape<RPK>::R;
+  constexpr int UL = RP + 4;  // floats per staged U row (rows 4 banks apart)
+  __shared__ __attribute__((aligned(16))) float Zl[32 * RP];  // 32 rows of Z_j at a time
+  __shared__ __attribute__((aligned(16))) float Ul[R * UL];
   const int j = blockIdx.y;
-  const int i0 = blockIdx.x * BP_ROWS;
-  const int tid = threadIdx.x, tr = tid >> 3, tc = tid & 7;
+  const int i0 = blockIdx.x * R;
+  const int tid = threadIdx.x;
   const float* __restrict__ Zj = Z + (size_t)j * r * r;
-  float acc[4][CPT];
+  for (int x = tid; x < R * RP; x += 256) {
+    const int i = x / RP, k = x % RP;
+    Ul[i * UL + k] = (i0 + i < m && k < r) ? U[(size_t)(i0 + i) * r + k] : 0.f;
+  }
+  const int row = tid / G, cg = tid % G;
+  // Threads past the last row still take part in the staging and its barriers.
+  const bool live = row < RT && i0 + row < m;
+  float acc[RR][8];
 #pragma unroll
-  for (int x = 0; x < 4; ++x)
+  for (int q = 0; q < RR; ++q)
 #pragma unroll
-    for (int y = 0; y < CPT; ++y) acc[x][y] = 0.f;
-  for (int kc = 0; kc < RPK; ++kc) {
-    if (kc) __syncthreads();
-    for (int x = tid; x < 32 * BP_ROWS; x += 256) {
-      const int i = x >> 5, kk = x & 31, t = kc * 32 + kk;
-      Ut[kk][i] = (i0 + i < m && t < r) ? U[(size_t)(i0 + i) * r + t] : 0.f;
-    }
-    for (int x = tid; x < 32 * RP; x += 256) {
-      const int kk = x / RP, c = x % RP, t = kc * 32 + kk;
-      Zl[kk][c] = (t < r && c < r) ? Zj[t * r + c] : 0.f;
+    for (int y = 0; y < 8; ++y) acc[q][y] = 0.f;
+  const float* __restrict__ zc = Zl + cg * 8;
+  for (int k0 = 0; k0 < r; k0 += 32) {
+    const int kn = min(32, r - k0);
+    if (k0) __syncthreads();  // every thread is done with the previous rows of Z_j
+    for (int x = tid; x < kn * RP; x += 256) {
+      const int k = x / RP, c = x % RP;
+      Zl[x] = c < r ? Zj[(k0 + k) * r + c] : 0.f;
     }
     __syncthreads();
-#pragma unroll 4
-    for (int kk = 0; kk < 32; ++kk) {
-      const f32x4 u = *(const f32x4*)&Ut[kk][tr * 4];
+    if (live) {
+      const int kn4 = kn & ~3;
+      int k = 0;
+      for (; k < kn4; k += 4) {
+        f32x4 u[RR];
 #pragma unroll
-      for (int y = 0; y < CPT; y += 4) {
-        const f32x4 z = *(const f32x4*)&Zl[kk][tc * CPT + y];
+        for (int q = 0; q < RR; ++q) u[q] = *(const f32x4*)(Ul + (row + q * RT) * UL + k0 + k);
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          acc[x][y] = fmaf(u[x], z[0], acc[x][y]);
-          acc[x][y + 1] = fmaf(u[x], z[1], acc[x][y + 1]);
-          acc[x][y + 2] = fmaf(u[x], z[2], acc[x][y + 2]);
-          acc[x][y + 3] = fmaf(u[x], z[3], acc[x][y + 3]);
+        for (int e = 0; e < 4; ++e) {
+          const f32x4 z0 = *(const f32x4*)(zc + (k + e) * RP);
+          const f32x4 z1 = *(const f32x4*)(zc + (k + e) * RP + 4);
+#pragma unroll
+          for (int q = 0; q < RR; ++q) {
+            acc[q][0] = fmaf(u[q][e], z0[0], acc[q][0]);
+            acc[q][1] = fmaf(u[q][e], z0[1], acc[q][1]);
+            acc[q][2] = fmaf(u[q][e], z0[2], acc[q][2]);
+            acc[q][3] = fmaf(u[q][e], z0[3], acc[q][3]);
+            acc[q][4] = fmaf(u[q][e], z1[0], acc[q][4]);
+            acc[q][5] = fmaf(u[q][e], z1[1], acc[q][5]);
+            acc[q][6] = fmaf(u[q][e], z1[2], acc[q][6]);
+            acc[q][7] = fmaf(u[q][e], z1[3], acc[q][7]);
+          }
+        }
+      }
+      for (; k < kn; ++k) {
+#pragma unroll
+        for (int q = 0; q < RR; ++q) {
+          const float u = Ul[(row + q * RT) * UL + k0 + k];
+#pragma unroll
+          for (int y = 0; y < 8; ++y) acc[q][y] = fmaf(u, zc[k * RP + y], acc[q][y]);
         }
       }
     }
   }
-  // hi / lo of eps C (the sign is applied per block below).
-  uint32_t hp[4][CPT / 2], lp[4][CPT / 2];
-  float v[4][CPT];
+  if (!live) return;
 #pragma unroll
-  for (int x = 0; x < 4; ++x)
+  for (int q = 0; q < RR; ++q) {
+    const int i = i0 + row + q * RT;
+    if (i >= m) break;
+    float v[8];
 #pragma unroll
-    for (int y = 0; y < CPT; ++y) v[x][y] = eps * acc[x][y];
-  if (out_bf16) {
+    for (int y = 0; y < 8; ++y) v[y] = eps * acc[q][y];
+    if (out_bf16) {
+      // hi / lo of eps C (the sign is applied per block below).
+      u32x4 hp, lp;
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-      for (int y = 0; y < CPT; y += 2) {
-        const float a0 = v[x][y], a1 = v[x][y + 1];
-        hp[x][y / 2] = pack_bf16x2(a0, a1);
-        lp[x][y / 2] = pack_bf16x2(a0 - bf16_to_f32(f32_to_bf16(a0)), a1 - bf16_to_f32(f32_to_bf16(a1)));
+      for (int y = 0; y < 4; ++y) {
+        const float a0 = v[2 * y], a1 = v[2 * y + 1];
+        hp[y] = pack_bf16x2(a0, a1);
+        lp[y] = pack_bf16x2(a0 - bf16_to_f32(f32_to_bf16(a0)), a1 - bf16_to_f32(f32_to_bf16(a1)));
       }
-  }
-  for (int b = 0; b < nblk; ++b) {
-    const int code = tab.code[b];
-    if ((code & 0xffff) != j) continue;
-    const int s = (code >> 16) - 1;
-#pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      const int i = i0 + tr * 4 + x;
-      if (i >= m) break;
-      if (out_bf16) {
+      for (int b = 0; b < nblk; ++b) {
+        const int code = tab.code[b];
+        if ((code & 0xffff) != j) continue;
+        const int s = (code >> 16) - 1;
         // Negation flips the sign bits; zero times the sign is +0.
         const uint32_t flip = s < 0 ? 0x80008000u : 0u;
-        bf16_t* o = (bf16_t*)Bp + ((long long)b * m + i) * 3 * rp + tc * CPT;
-#pragma unroll
-        for (int y = 0; y < CPT; y += 4) {
-          uint32_t h0 = hp[x][y / 2], h1 = hp[x][y / 2 + 1], l0 = lp[x][y / 2], l1 = lp[x][y / 2 + 1];
-          if (s == 0) {
-            h0 = h1 = l0 = l1 = 0u;
-          } else {
-            h0 ^= flip; h1 ^= flip; l0 ^= flip; l1 ^= flip;
-          }
-          *(u32x2*)(o + y) = (u32x2){h0, h1};
-          *(u32x2*)(o + rp + y) = (u32x2){l0, l1};
-          *(u32x2*)(o + 2 * rp + y) = (u32x2){h0, h1};
-        }
-      } else {
-        // fp32 keeps rp == round16(r) wide rows; RP may exceed rp.
-        float* o = (float*)Bp + ((long long)b * m + i) * rp;
-#pragma unroll
-        for (int y = 0; y < CPT; ++y)
-          if (tc * CPT + y < rp) o[tc * CPT + y] = (float)s * v[x][y];
+        const u32x4 h = s == 0 ? (u32x4){0u, 0u, 0u, 0u} : (hp ^ flip);
+        const u32x4 l = s == 0 ? (u32x4){0u, 0u, 0u, 0u} : (lp ^ flip);
+        bf16_t* o = (bf16_t*)Bp + ((long long)b * m + i) * 3 * rp + cg * 8;
+        *(u32x4*)o = h;
+        *(u32x4*)(o + rp) = l;
+        *(u32x4*)(o + 2 * rp) = h;
+      }
+    } else {
+      // fp32 keeps rp == round16(r) wide rows; RP may exceed rp (whole groups of 8).
+      if (cg * 8 >= rp) break;
+      for (int b = 0; b < nblk; ++b) {
+        const int code = tab.code[b];
+        if ((code & 0xffff) != j) continue;
+        const float s = (float)((code >> 16) - 1);
+        float* o = (float*)Bp + ((long long)b * m + i) * rp + cg * 8;
+        *(f32x4*)o = (f32x4){s * v[0], s * v[1], s * v[2], s * v[3]};
+        *(f32x4*)(o + 4) = (f32x4){s * v[4], s * v[5], s * v[6], s * v[7]};
       }
     }
   }
@@ -978,7 +1016,41 @@ __global__ __launch_bounds__(256, 1) void k_gemm_main(GemmArgs a) {
   const int el = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   const int efr = el & 31, efh = el >> 5;
   const int e16 = el & 15, eq = el >> 4;  // the accumulator layout's token row and column quarter
-  if constexpr (OUT != ZO_F32 && (EPI == ZO_EPI_NONE || EPI == ZO_EPI_RELU)) {
+  if constexpr (EPI == EPI_PROJ32 || EPI == EPI_PROJ64) {
+    // A wave's 128 A rows hold whole factors (2 rp rows each: the hi rows, then the lo rows), so
+    // a factor column's hi and lo sums are accumulators i and i + rp / 16 of one lane.  Combined,
+    // split and rounded here, they go straight to the factor's buffer (a lane writes 4 adjacent
+    // columns of one token; the output is 3 rp / (2 K) of the bytes read, so no staging).
+    constexpr int RP = EPI == EPI_PROJ32 ? 32 : 64, R16 = RP / 16, NFW = 128 / (2 * RP);
+#pragma unroll
+    for (int f = 0; f < NFW; ++f) {
+      const int gf = (m0 + wm * 128) / (2 * RP) + f;
+      if (gf >= a.pcount) break;
+      bf16_t* const pc = a.pc[gf];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int tok = t0 + wn * 128 + 16 * j + e16;
+        if (tok >= a.rows_b) continue;
+        bf16_t* const o = pc + ((long long)blk * a.rows_b + tok) * (3 * RP) + 4 * eq;
+#pragma unroll
+        for (int ii = 0; ii < R16; ++ii) {
+          const int ih = f * 2 * R16 + ii, il = ih + R16;
+          float hv[4], lv[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float pv = (acc[ih][j][e] + acc[il][j][e]) * a.unscale;
+            hv[e] = bf16_to_f32(f32_to_bf16(pv));
+            lv[e] = pv - hv[e];
+          }
+          const u32x2 hi = (u32x2){pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3])};
+          const u32x2 lo = (u32x2){pack_bf16x2(lv[0], lv[1]), pack_bf16x2(lv[2], lv[3])};
+          *(u32x2*)(o + 16 * ii) = hi;
+          *(u32x2*)(o + RP + 16 * ii) = hi;
+          *(u32x2*)(o + 2 * RP + 16 * ii) = lo;
+        }
+      }
+    }
+  } else if constexpr (OUT != ZO_F32 && (EPI == ZO_EPI_NONE || EPI == ZO_EPI_RELU)) {
     constexpr int PITCH = 528;
     // acc[i][j]: token row wn 128 + 16 j + l % 16, columns wm 128 + 16 i + 4 (l / 16) .. + 3.
     char* const wb = lds + (wn * 128 + e16) * PITCH + wm * 256 + eq * 8;
@@ -1269,6 +1341,16 @@ __global__ __launch_bounds__(256, 1) void k_proj(ProjArgs a) {
 
 template <bool F16, int OUT>
 void launch_main_epi(const GemmArgs& a, dim3 grid, hipStream_t stream) {
+  if constexpr (OUT != ZO_F32) {  // the projection epilogues write bf16 whatever OUT is
+    if (a.epi == EPI_PROJ32) {
+      hipLaunchKernelGGL((k_gemm_main<F16, OUT, EPI_PROJ32>), grid, dim3(256), 0, stream, a);
+      return;
+    }
+    if (a.epi == EPI_PROJ64) {
+      hipLaunchKernelGGL((k_gemm_main<F16, OUT, EPI_PROJ64>), grid, dim3(256), 0, stream, a);
+      return;
+    }
+  }
   if (a.epi == EPI_BASE)
     hipLaunchKernelGGL((k_gemm_main<F16, OUT, EPI_BASE>), grid, dim3(256), 0, stream, a);
   else if (a.epi == EPI_BASE_RELU)
@@ -1377,15 +1459,15 @@ static int launch_transpose_v(const PlinearPlan& p, const float* V, void* vt, hi
 
 static int launch_bprime(const PlinearPlan& p, const BlkTable& tab, float eps, const float* U,
                          const float* Z, void* bp, hipStream_t stream) {
-  const dim3 grid((unsigned)((p.m + BP_ROWS - 1) / BP_ROWS), (unsigned)p.q);
+  auto grid = [&](int rows) { return dim3((unsigned)((p.m + rows - 1) / rows), (unsigned)p.q); };
   switch ((p.r + 31) / 32) {
-    case 1: hipLaunchKernelGGL(k_bprime<1>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+    case 1: hipLaunchKernelGGL(k_bprime<1>, grid(BpShape<1>::R), dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
                                eps, tab, bp, p.in16); break;
-    case 2: hipLaunchKernelGGL(k_bprime<2>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+    case 2: hipLaunchKernelGGL(k_bprime<2>, grid(BpShape<2>::R), dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
                                eps, tab, bp, p.in16); break;
-    case 3: hipLaunchKernelGGL(k_bprime<3>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+    case 3: hipLaunchKernelGGL(k_bprime<3>, grid(BpShape<3>::R), dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
                                eps, tab, bp, p.in16); break;
-    default: hipLaunchKernelGGL(k_bprime<4>, grid, dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
+    default: hipLaunchKernelGGL(k_bprime<4>, grid(BpShape<4>::R), dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
                                 eps, tab, bp, p.in16); break;
   }
   return zo_hip_status(hipGetLastError(), "k_bprime");
@@ -1438,6 +1520,37 @@ static int launch_pcombine(const PlinearPlan& p, const float* p2, int ld2, void*
   hipLaunchKernelGGL(k_pcombine, dim3((unsigned)((prow * p.rp + 255) / 256)), dim3(256), 0, stream, p2,
                      prow, p.rp, ld2, p.in_dtype == ZO_F16 ? 1.f / ZO_F16_RSCALE : 1.f, (bf16_t*)pp);
   return zo_hip_status(hipGetLastError(), "k_pcombine");
+}
+
+// A stack of `count` 16-bit factors (rp = 32 or 64; vt: count x 2 rp rows) projected on the main
+// GEMM with the combine in its epilogue, factor i's [P_hi | P_hi | P_lo] into pc[i].  False when
+// the stack does not fit that kernel (the caller then projects to fp32 and combines apart).
+static bool proj_main_fits(const PlinearPlan& p, int count) {
+  GemmArgs g{};
+  g.rows_a = count * 2 * p.rp;
+  g.rows_b = p.T;
+  g.K = p.n;
+  return p.in16 && (p.rp == 32 || p.rp == 64) && count >= 1 && count <= ZO_MAX_GROUP && g.rows_a >= 128 &&
+         main_gemm_fits(g);
+}
+
+static int launch_proj_main(const PlinearPlan& p, const void* X, const void* vt, int count, bf16_t* const* pc,
+                            hipStream_t stream) {
+  GemmArgs g{};
+  g.A = (const bf16_t*)vt;
+  g.B = (const bf16_t*)X;
+  g.b_block_stride = p.x_block_stride;
+  g.rows_a = count * 2 * p.rp;
+  g.rows_b = p.T;
+  g.K = p.n;
+  g.nblk = p.nx;
+  g.rc = 0;
+  g.out_dtype = p.in_dtype;  // selects the F16 / BF16 instantiation; nothing is written to Y
+  g.epi = p.rp == 32 ? EPI_PROJ32 : EPI_PROJ64;
+  for (int i = 0; i < count; ++i) g.pc[i] = pc[i];
+  g.pcount = count;
+  g.unscale = p.in_dtype == ZO_F16 ? 1.f / ZO_F16_RSCALE : 1.f;
+  return launch_gemm_main(g, p.in_dtype == ZO_F16, stream);
 }
 
 // The fused projection (k_proj): 16-bit factors of 64 or 128 rows (rp = 32 or 64), each
@@ -1512,13 +1625,12 @@ int zo_plinear_prepare_group(const PlinearPlan* plans, int count, const int* blk
     if ((st = launch_bprime(plans[i], tab, eps, U[i], Z[i], w.bp, stream)) != ZO_OK) return st;
   }
   // A stack of several factors stays on the main GEMM's 256-row tiles (two factors of 128 rows
-  // per X tile: the stacked q, k, v run 0.50 ms there against 0.72 ms in three 128-row tiles),
-  // with the separate combine; only a 64-row pair shares one 128-row tile.
-  if (2 * p0.rp * count <= 128 && proj_fused_fits(p0, count)) {
-    bf16_t* pc[ZO_MAX_GROUP];
-    for (int i = 0; i < count; ++i) pc[i] = (bf16_t*)zo_plinear_ws(plans[i], ws[i]).pp;
-    return launch_proj_fused(p0, X, gvt, count, pc, stream);
-  }
+  // per X tile: the stacked q, k, v run 0.50 ms there against 0.72 ms in three 128-row tiles of
+  // k_proj), with the combine in its epilogue; only a 64-row pair shares one 128-row tile.
+  bf16_t* pc[ZO_MAX_GROUP];
+  for (int i = 0; i < count; ++i) pc[i] = (bf16_t*)zo_plinear_ws(plans[i], ws[i]).pp;
+  if (2 * p0.rp * count <= 128 && proj_fused_fits(p0, count)) return launch_proj_fused(p0, X, gvt, count, pc, stream);
+  if (proj_main_fits(p0, count)) return launch_proj_main(p0, X, gvt, count, pc, stream);
   if ((st = launch_projection(p0, X, gvt, count * w2, gp2, stream)) != ZO_OK) return st;
   for (int i = 0; i < count; ++i)
     if ((st = launch_pcombine(plans[i], gp2 + (size_t)i * w2, count * w2, zo_plinear_ws(plans[i], ws[i]).pp,

@@ -331,11 +331,17 @@ def test_forward_difference_layout_at_paper_k():
 
 @pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
 @pytest.mark.parametrize("shared", [False, True])
-def test_prepare_group_equals_separate(dt, shared):
+@pytest.mark.parametrize("T,n,r,ms", [
+    (200, 264, 20, [256, 128, 72]),   # K not a multiple of 32: fp32 projection, then the combine
+    (300, 512, 64, [256, 128, 72]),   # 3 x 128 stacked rows: the main GEMM, combine in its epilogue
+    (260, 320, 24, [64, 200, 136]),   # 3 x 64 rows (rp = 32) on the main GEMM
+    (130, 256, 40, [96, 160]),        # 2 x 128 rows: one whole 256-row tile
+])
+def test_prepare_group_equals_separate(dt, shared, T, n, r, ms):
     """zo_perturbed_linear_prepare_group (one projection pass for matrices that read the same X,
-    of different heights) then each apply: bitwise the separate prepares and applies."""
-    T, n, r, q, nblk = 200, 264, 20, 2, 4
-    ms = [256, 128, 72]
+    of different heights) then each apply: bitwise the separate prepares and applies (a single
+    16-bit factor of 64 or 128 rows projects in k_proj)."""
+    q, nblk = 2, 4
     xs = 0 if shared else T * n
     Xd, _ = cast(zd.draw(31, "X", (T, n), ((1 if shared else nblk) * T, n)), dt)
     bq, bs = [b // 2 for b in range(nblk)], [1, -1] * (nblk // 2)
