@@ -14,28 +14,40 @@
 // free).  Gaussian panels, whose condition number is about
 // (sqrt(rows) + sqrt(r)) / (sqrt(rows) - sqrt(r)), essentially never get there.
 //
-// Five launches per batch of panels, all float64 with fixed-order sums (the
-// result is bitwise reproducible):
+// Five launches per call, each over every panel of the call (the panel
+// descriptors sit in a table in the workspace, written by k_cqr_fill; a row
+// launch's workgroup finds its panel by binary search over the table), all
+// float64 with fixed-order sums (the result is bitwise reproducible):
 //   k_cqr_rows<0>  per chunk of CHUNK rows: partial Omega^T Omega
 //   k_cqr_chol     per panel: sum of the partials, Cholesky -> R1, and
 //                  X1 = R1^-1 (rows of the identity through forward substitution)
 //   k_cqr_rows<1>  per chunk: Q1 = Omega X1, partial Q1^T Q1
 //   k_cqr_chol     per panel: R2, X2 = R2^-1, M = X1 X2; diag(R) = diag(R2) diag(R1); info
 //   k_cqr_rows<2>  per chunk: Q = Omega M, written as fp32
-// The row passes are small dense products (4 x 4 register tiles, operands in LDS).
+// The row passes (r <= 64) run on v_mfma_f64_16x16x4_f64, each wave on its own
+// quarter of the chunk: the Gram matrix as sums of 4-row outer products over
+// its upper 16 x 16 tiles, the products 16 rows at a time.  The product's
+// output registers are, lane for lane, the operands of the Gram MFMAs of its
+// rows (output lane l, register v holds row 4 v + l / 16, column l % 16, the
+// layout an operand's k = l / 16, i = l % 16 asks for), so Q1 never leaves the
+// registers.  The four waves' partial Gram matrices are added in wave order.
 // A pivot that is not positive marks the panel rank deficient at that column
 // (an exactly zero column gives a zero pivot): R's row there is zero, the Q
 // column is zero, and the other columns are formed as if it were absent.
 #include "zo_internal.h"
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
 namespace {
 
-constexpr int ROWS_WG = 128;     // rows held per pass of a workgroup (one per thread)
-constexpr int CHUNK = 1024;      // rows per workgroup (8 passes of ROWS_WG)
-constexpr int PANELS_PER_LAUNCH = 48;
+constexpr int CHUNK = 2048;       // rows per workgroup of the r <= 64 path (CHUNK / 4 per wave)
+constexpr int WROWS = CHUNK / 4;
+constexpr int BIG_CHUNK = 1024;   // rows per workgroup of the r > 64 path
+constexpr int FILL_PANELS = 48;   // descriptors per k_cqr_fill launch (kernel arguments)
+
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 struct CqrPanel {
   const float* omega;
@@ -49,141 +61,158 @@ struct CqrPanel {
   int rows, chunk_begin;
 };
 struct CqrArgs {
-  CqrPanel p[PANELS_PER_LAUNCH];
+  const CqrPanel* p;  // the call's descriptor table (workspace)
   int count, r;
 };
+struct CqrFill {
+  CqrPanel p[FILL_PANELS];
+  CqrPanel* dst;
+  int n;
+};
 
-__device__ __forceinline__ int find_panel(const CqrArgs& a, int wg) {
-  int k = 0;
-  while (k + 1 < a.count && wg >= a.p[k + 1].chunk_begin) ++k;
-  return k;
+// Copies n host descriptors (kernel arguments) into the table, one 32-bit word per thread.
+__global__ __launch_bounds__(256) void k_cqr_fill(CqrFill f) {
+  constexpr int W = (int)(sizeof(CqrPanel) / 4);
+  static_assert(sizeof(CqrPanel) % 4 == 0, "descriptor of whole words");
+  const int x = blockIdx.x * 256 + threadIdx.x;
+  if (x < f.n * W) ((uint32_t*)f.dst)[x] = ((const uint32_t*)f.p)[x];
 }
 
-// Y = X Mx for a block of ROWS_WG rows (X, Y in rowbuf, Mx RP x RP in LDS);
-// each thread owns RK tiles of 4 rows x 4 columns.
-template <int RP>
-__device__ __forceinline__ void block_product(double (*rowbuf)[RP + 1], const double* Mx) {
-  constexpr int CG = RP / 4;                 // column groups
-  constexpr int TPT = ROWS_WG / 4 * CG / ROWS_WG;  // tiles per thread (= RP / 16)
-  const int tid = threadIdx.x;
-  double acc[TPT][4][4];
-#pragma unroll
-  for (int t = 0; t < TPT; ++t)
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc[t][u][v] = 0.0;
-  for (int k = 0; k < RP; ++k) {
-#pragma unroll
-    for (int t = 0; t < TPT; ++t) {
-      const int tile = tid + t * ROWS_WG, rg = tile / CG, cg = tile % CG;
-      double a[4], m[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) a[u] = rowbuf[4 * rg + u][k];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) m[v] = Mx[k * RP + 4 * cg + v];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[t][u][v] = fma(a[u], m[v], acc[t][u][v]);
-    }
+// The panel that row workgroup wg belongs to: the last k with chunk_begin <= wg
+// (chunk_begin is non-decreasing from 0; a panel without rows has no chunks).
+__device__ __forceinline__ int find_panel(const CqrArgs& a, int wg) {
+  int lo = 0, hi = a.count - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.p[mid].chunk_begin <= wg) lo = mid;
+    else hi = mid - 1;
   }
-  __syncthreads();  // every thread has read its rows of X
-#pragma unroll
-  for (int t = 0; t < TPT; ++t) {
-    const int tile = tid + t * ROWS_WG, rg = tile / CG, cg = tile % CG;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) rowbuf[4 * rg + u][4 * cg + v] = acc[t][u][v];
-  }
-  __syncthreads();
+  return lo;
+}
+
+__device__ __forceinline__ f64x4 mfma64(double a, double b, f64x4 c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
 }
 
 // PASS 0: partial Omega^T Omega of this chunk.  PASS 1: partial Q1^T Q1 with
-// Q1 = Omega X1.  PASS 2: Q = Omega M written as fp32.  Rows move between
-// global memory and LDS as contiguous blocks.
+// Q1 = Omega X1.  PASS 2: Q = Omega M written as fp32.  Entries outside the
+// panel's rows x r read as zero.  A Gram tile (ta <= tb) accumulates, per
+// 4-row step, the MFMA of the rows' columns 16 ta + i (A) and 16 tb + j (B):
+// lane l brings row base + l / 16, column 16 t + l % 16 as the operand of
+// tile t.  A product 16 rows x RP takes the row's columns in K steps of 4:
+// step kk, lane l multiplies column c = (l / 16) KS + kk of row base + l % 16
+// with Mx row c (any one-to-one map of (step, lane group) to columns sums the
+// same terms).
 template <int RK, int PASS>
-__global__ __launch_bounds__(ROWS_WG) void k_cqr_rows(CqrArgs a) {
-  constexpr int RP = 16 * RK;
-  constexpr int NB = RP / 4;                  // 4 x 4 blocks per side
-  constexpr int NBLK = NB * (NB + 1) / 2;     // upper-triangular blocks
-  constexpr int BPT = (NBLK + ROWS_WG - 1) / ROWS_WG;
+__global__ __launch_bounds__(256) void k_cqr_rows(CqrArgs a) {
+  constexpr int RP = 16 * RK, KS = RP / 4, NPAIR = RK * (RK + 1) / 2;
   __shared__ double Mx[PASS == 0 ? 1 : RP * RP];
-  __shared__ double rowbuf[ROWS_WG][RP + 1];
-  const CqrPanel& P = a.p[find_panel(a, blockIdx.x)];
+  __shared__ double red[PASS == 2 ? 1 : NPAIR * 256];
+  const CqrPanel P = a.p[find_panel(a, blockIdx.x)];
   const int chunk = blockIdx.x - P.chunk_begin;
-  const int r = a.r, tid = threadIdx.x;
+  const int r = a.r, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
   if (PASS >= 1) {
     const double* src = PASS == 1 ? P.X1 : P.M;
-    for (int x = tid; x < RP * RP; x += ROWS_WG) Mx[x] = src[x];
-  }
-  // Padding columns r .. RP-1 stay zero in every row.
-  for (int x = tid; x < ROWS_WG * (RP - r); x += ROWS_WG) rowbuf[x / (RP - r)][r + x % (RP - r)] = 0.0;
-  // Gram blocks owned by this thread: (bi, bj) with bi <= bj, enumerated row-major.
-  int bi[BPT], bj[BPT];
-  double g[BPT][4][4];
-#pragma unroll
-  for (int t = 0; t < BPT; ++t) {
-    int b = tid + t * ROWS_WG, ii = 0;
-    if (b >= NBLK) b = -1;
-    if (b >= 0) {
-      int rem = b;
-      while (rem >= NB - ii) { rem -= NB - ii; ++ii; }
-      bi[t] = ii;
-      bj[t] = ii + rem;
-    } else {
-      bi[t] = bj[t] = -1;
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) g[t][u][v] = 0.0;
-  }
-  const int row_end = min((chunk + 1) * CHUNK, P.rows);
-  for (int base = chunk * CHUNK; base < row_end; base += ROWS_WG) {
-    const int nrow = min(ROWS_WG, row_end - base);
-    __syncthreads();  // the previous block's rows have been consumed
-    {
-      const float* src = P.omega + (size_t)base * r;
-      for (int x = tid; x < nrow * r; x += ROWS_WG) rowbuf[x / r][x % r] = (double)src[x];
-      // Rows past the panel's end multiply as zeros.
-      for (int x = tid; x < (ROWS_WG - nrow) * r; x += ROWS_WG) rowbuf[nrow + x / r][x % r] = 0.0;
-    }
+    for (int x = tid; x < RP * RP; x += 256) Mx[x] = src[x];
     __syncthreads();
-    if (PASS >= 1) block_product<RP>(rowbuf, Mx);
-    if (PASS == 2) {
-      float* dst = P.q + (size_t)base * r;
-      for (int x = tid; x < nrow * r; x += ROWS_WG) dst[x] = (float)rowbuf[x / r][x % r];
-      continue;
+  }
+  const int row0 = chunk * CHUNK + wave * WROWS;
+  const int nrow = min(WROWS, P.rows - row0);  // this wave's rows (none past the end)
+  auto om = [&](int row, int col) -> double {
+    return (row < P.rows && col < r) ? (double)P.omega[(size_t)row * r + col] : 0.0;
+  };
+  f64x4 acc[NPAIR];
+#pragma unroll
+  for (int p = 0; p < NPAIR; ++p) acc[p] = (f64x4){0.0, 0.0, 0.0, 0.0};
+  // The Gram tiles over 4 rows whose tile-t operands are v[t].
+  auto gram = [&](const double* v) {
+    int p = 0;
+#pragma unroll
+    for (int ta = 0; ta < RK; ++ta)
+#pragma unroll
+      for (int tb = ta; tb < RK; ++tb, ++p) acc[p] = mfma64(v[ta], v[tb], acc[p]);
+  };
+  if (PASS == 0) {
+    // 16 rows per step (four 4-row Gram steps), the next step's loads issued before the MFMAs.
+    double nx[4][RK];
+    auto load = [&](int s) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int t = 0; t < RK; ++t) nx[u][t] = om(row0 + s + 4 * u + g, 16 * t + l16);
+    };
+    if (nrow > 0) load(0);
+    for (int s = 0; s < nrow; s += 16) {
+      double cur[4][RK];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int t = 0; t < RK; ++t) cur[u][t] = nx[u][t];
+      if (s + 16 < nrow) load(s + 16);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) gram(cur[u]);
     }
-    for (int rr = 0; rr < nrow; ++rr) {
-      const double* row = rowbuf[rr];
+  } else {
+    double nx[KS];
+    auto load = [&](int s) {
 #pragma unroll
-      for (int t = 0; t < BPT; ++t) {
-        if (bi[t] < 0) continue;
-        double u[4], v[4];
+      for (int kk = 0; kk < KS; ++kk) nx[kk] = om(row0 + s + l16, g * KS + kk);
+    };
+    if (nrow > 0) load(0);
+    for (int s = 0; s < nrow; s += 16) {
+      double av[KS];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          u[e] = row[4 * bi[t] + e];
-          v[e] = row[4 * bj[t] + e];
+      for (int kk = 0; kk < KS; ++kk) av[kk] = nx[kk];
+      if (s + 16 < nrow) load(s + 16);
+      f64x4 q[RK];
+#pragma unroll
+      for (int t = 0; t < RK; ++t) {
+        q[t] = (f64x4){0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) q[t] = mfma64(av[kk], Mx[(g * KS + kk) * RP + 16 * t + l16], q[t]);
+      }
+      // q[t][v]: row row0 + s + 4 v + g, column 16 t + l16.
+      if (PASS == 1) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          double w[RK];
+#pragma unroll
+          for (int t = 0; t < RK; ++t) w[t] = q[t][v];
+          gram(w);
         }
+      } else {
 #pragma unroll
-        for (int p = 0; p < 4; ++p)
+        for (int v = 0; v < 4; ++v) {
+          const int row = row0 + s + 4 * v + g;
+          if (row >= P.rows) continue;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) g[t][p][q] = fma(u[p], v[q], g[t][p][q]);
+          for (int t = 0; t < RK; ++t)
+            if (16 * t + l16 < r) P.q[(size_t)row * r + 16 * t + l16] = (float)q[t][v];
+        }
       }
     }
   }
   if (PASS == 2) return;
+  // The waves' partials added in wave order, then written as the chunk's upper tiles.
+  for (int w = 0; w < 4; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int p = 0; p < NPAIR; ++p)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          double& d = red[p * 256 + v * 64 + lane];
+          d = w == 0 ? acc[p][v] : d + acc[p][v];
+        }
+    }
+    __syncthreads();
+  }
   double* out = P.part + (size_t)chunk * RP * RP;
-#pragma unroll
-  for (int t = 0; t < BPT; ++t) {
-    if (bi[t] < 0) continue;
-#pragma unroll
-    for (int p = 0; p < 4; ++p)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) out[(size_t)(4 * bi[t] + p) * RP + 4 * bj[t] + q] = g[t][p][q];
+  for (int x = tid; x < NPAIR * 256; x += 256) {
+    int p = x >> 8, ta = 0;
+    while (p >= RK - ta) { p -= RK - ta; ++ta; }
+    const int tb = ta + p, v = (x >> 6) & 3, l = x & 63;
+    out[(size_t)(16 * ta + 4 * v + (l >> 4)) * RP + 16 * tb + (l & 15)] = red[x];
   }
 }
 
@@ -277,15 +306,15 @@ size_t panel_ws(int rows, int RP) {
 template <int RK>
 int run_batch(const CqrArgs& ca, int wg, hipStream_t stream) {
   int st;
-  hipLaunchKernelGGL((k_cqr_rows<RK, 0>), dim3(wg), dim3(ROWS_WG), 0, stream, ca);
+  if (wg > 0) hipLaunchKernelGGL((k_cqr_rows<RK, 0>), dim3(wg), dim3(256), 0, stream, ca);
   if ((st = zo_hip_status(hipGetLastError(), "k_cqr_rows")) != ZO_OK) return st;
   hipLaunchKernelGGL((k_cqr_chol<RK, false>), dim3(ca.count), dim3(256), 0, stream, ca);
   if ((st = zo_hip_status(hipGetLastError(), "k_cqr_chol")) != ZO_OK) return st;
-  hipLaunchKernelGGL((k_cqr_rows<RK, 1>), dim3(wg), dim3(ROWS_WG), 0, stream, ca);
+  if (wg > 0) hipLaunchKernelGGL((k_cqr_rows<RK, 1>), dim3(wg), dim3(256), 0, stream, ca);
   if ((st = zo_hip_status(hipGetLastError(), "k_cqr_rows")) != ZO_OK) return st;
   hipLaunchKernelGGL((k_cqr_chol<RK, true>), dim3(ca.count), dim3(256), 0, stream, ca);
   if ((st = zo_hip_status(hipGetLastError(), "k_cqr_chol")) != ZO_OK) return st;
-  hipLaunchKernelGGL((k_cqr_rows<RK, 2>), dim3(wg), dim3(ROWS_WG), 0, stream, ca);
+  if (wg > 0) hipLaunchKernelGGL((k_cqr_rows<RK, 2>), dim3(wg), dim3(256), 0, stream, ca);
   return zo_hip_status(hipGetLastError(), "k_cqr_rows");
 }
 
@@ -349,8 +378,8 @@ __global__ __launch_bounds__(BIG_NT) void k_cqr_rows_big(CqrArgs a) {
   const int cg = tid & 31, rg0 = tid >> 5;
   const int nkc = (r + BIG_KC - 1) / BIG_KC;
   const double* Msrc = PASS == 1 ? P.X1 : P.M;
-  const int row_end = min((chunk + 1) * CHUNK, P.rows);
-  for (int base = chunk * CHUNK; base < row_end; base += BIG_RW) {
+  const int row_end = min((chunk + 1) * BIG_CHUNK, P.rows);
+  for (int base = chunk * BIG_CHUNK; base < row_end; base += BIG_RW) {
     const int nrow = min(BIG_RW, row_end - base);
     __syncthreads();  // the previous block's rows have been consumed
     {
@@ -443,7 +472,7 @@ __global__ __launch_bounds__(BIG_NT) void k_cqr_chol_big(CqrArgs a) {
   __shared__ double dg[RP];
   const CqrPanel& P = a.p[blockIdx.x];
   const int r = a.r, tid = threadIdx.x;
-  const int nchunk = (P.rows + CHUNK - 1) / CHUNK;
+  const int nchunk = (P.rows + BIG_CHUNK - 1) / BIG_CHUNK;
   for (int x = tid; x < RP * RP; x += BIG_NT) {
     const int i = x / RP, j = x % RP;
     if (i > j) continue;
@@ -522,21 +551,21 @@ __global__ __launch_bounds__(BIG_NT) void k_cqr_chol_big(CqrArgs a) {
 }
 
 size_t panel_ws_big(int rows) {
-  const size_t nchunk = (size_t)(rows + CHUNK - 1) / CHUNK;
+  const size_t nchunk = (size_t)(rows + BIG_CHUNK - 1) / BIG_CHUNK;
   return zo_align256(nchunk * BIG_NBLK * 16 * 8) + 3 * zo_align256((size_t)BIG_RP * BIG_RP * 8);
 }
 
 int run_batch_big(const CqrArgs& ca, int wg, hipStream_t stream) {
   int st;
-  hipLaunchKernelGGL(k_cqr_rows_big<0>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
+  if (wg > 0) hipLaunchKernelGGL(k_cqr_rows_big<0>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
   if ((st = zo_hip_status(hipGetLastError(), "k_cqr_rows_big")) != ZO_OK) return st;
   hipLaunchKernelGGL(k_cqr_chol_big<false>, dim3(ca.count), dim3(BIG_NT), 0, stream, ca);
   if ((st = zo_hip_status(hipGetLastError(), "k_cqr_chol_big")) != ZO_OK) return st;
-  hipLaunchKernelGGL(k_cqr_rows_big<1>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
+  if (wg > 0) hipLaunchKernelGGL(k_cqr_rows_big<1>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
   if ((st = zo_hip_status(hipGetLastError(), "k_cqr_rows_big")) != ZO_OK) return st;
   hipLaunchKernelGGL(k_cqr_chol_big<true>, dim3(ca.count), dim3(BIG_NT), 0, stream, ca);
   if ((st = zo_hip_status(hipGetLastError(), "k_cqr_chol_big")) != ZO_OK) return st;
-  hipLaunchKernelGGL(k_cqr_rows_big<2>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
+  if (wg > 0) hipLaunchKernelGGL(k_cqr_rows_big<2>, dim3(wg), dim3(BIG_NT), 0, stream, ca);
   return zo_hip_status(hipGetLastError(), "k_cqr_rows_big");
 }
 
@@ -547,45 +576,59 @@ int zo_refresh_launch(int count, const zo_panel* panels, int r, int* info, void*
   const bool big = r > 64;
   const int RK = big ? BIG_RP / 16 : (r + 15) / 16;
   const int RP = 16 * RK;
-  size_t need = 0;
+  const int chunk_rows = big ? BIG_CHUNK : CHUNK;
+  size_t need = zo_align256((size_t)count * sizeof(CqrPanel));
   for (int p = 0; p < count; ++p) need += big ? panel_ws_big(panels[p].rows) : panel_ws(panels[p].rows, RP);
   if (ws_needed) *ws_needed = need;
-  if (!ws) return ZO_OK;
+  if (!ws || count == 0) return ZO_OK;
   if (ws_bytes < need) {
     zo_set_error("refresh: workspace %zu bytes < required %zu", ws_bytes, need);
     return ZO_ERR_WORKSPACE;
   }
   WsCarver wc(ws);
-  int st;
-  for (int c0 = 0; c0 < count; c0 += PANELS_PER_LAUNCH) {
-    CqrArgs ca{};
-    ca.r = r;
-    int wg = 0;
-    for (int p = c0; p < count && p < c0 + PANELS_PER_LAUNCH; ++p) {
-      CqrPanel& e = ca.p[ca.count++];
-      const int nchunk = (panels[p].rows + CHUNK - 1) / CHUNK;
-      e.omega = panels[p].omega;
-      e.q = panels[p].q;
-      e.r_diag = panels[p].r_diag;
-      e.info = info ? info + p : nullptr;
-      e.part = (double*)wc.take((size_t)nchunk * (big ? BIG_NBLK * 16 : RP * RP) * 8);
-      e.R1 = (double*)wc.take((size_t)RP * RP * 8);
-      e.X1 = (double*)wc.take((size_t)RP * RP * 8);
-      e.M = (double*)wc.take((size_t)RP * RP * 8);
-      e.rows = panels[p].rows;
-      e.chunk_begin = wg;
-      wg += nchunk;
-    }
-    switch (big ? 0 : RK) {
-      case 0: st = run_batch_big(ca, wg, stream); break;
-      case 1: st = run_batch<1>(ca, wg, stream); break;
-      case 2: st = run_batch<2>(ca, wg, stream); break;
-      case 3: st = run_batch<3>(ca, wg, stream); break;
-      default: st = run_batch<4>(ca, wg, stream); break;
-    }
-    if (st != ZO_OK) return st;
+  CqrPanel* tab = (CqrPanel*)wc.take((size_t)count * sizeof(CqrPanel));
+  std::vector<CqrPanel> host((size_t)count);
+  long long wg = 0;
+  for (int p = 0; p < count; ++p) {
+    CqrPanel& e = host[p];
+    const int nchunk = (panels[p].rows + chunk_rows - 1) / chunk_rows;
+    e.omega = panels[p].omega;
+    e.q = panels[p].q;
+    e.r_diag = panels[p].r_diag;
+    e.info = info ? info + p : nullptr;
+    e.part = (double*)wc.take((size_t)nchunk * (big ? BIG_NBLK * 16 : RP * RP) * 8);
+    e.R1 = (double*)wc.take((size_t)RP * RP * 8);
+    e.X1 = (double*)wc.take((size_t)RP * RP * 8);
+    e.M = (double*)wc.take((size_t)RP * RP * 8);
+    e.rows = panels[p].rows;
+    e.chunk_begin = (int)wg;
+    wg += nchunk;
   }
-  return ZO_OK;
+  if (wg > 0x7fffffffLL) {
+    zo_set_error("refresh: too many row chunks (%lld)", wg);
+    return ZO_ERR_UNSUPPORTED;
+  }
+  int st;
+  for (int c0 = 0; c0 < count; c0 += FILL_PANELS) {
+    CqrFill f{};
+    f.n = std::min(FILL_PANELS, count - c0);
+    for (int i = 0; i < f.n; ++i) f.p[i] = host[c0 + i];
+    f.dst = tab + c0;
+    const int words = f.n * (int)(sizeof(CqrPanel) / 4);
+    hipLaunchKernelGGL(k_cqr_fill, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, stream, f);
+    if ((st = zo_hip_status(hipGetLastError(), "k_cqr_fill")) != ZO_OK) return st;
+  }
+  CqrArgs ca{};
+  ca.p = tab;
+  ca.count = count;
+  ca.r = r;
+  switch (big ? 0 : RK) {
+    case 0: return run_batch_big(ca, (int)wg, stream);
+    case 1: return run_batch<1>(ca, (int)wg, stream);
+    case 2: return run_batch<2>(ca, (int)wg, stream);
+    case 3: return run_batch<3>(ca, (int)wg, stream);
+    default: return run_batch<4>(ca, (int)wg, stream);
+  }
 }
 
 // ---------------------------------------------------------------- no-allocation variant

@@ -48,7 +48,8 @@ def test_noalloc_matches_workspace_refresh(r, first, second):
 
 def test_noalloc_rejects_oversized_call():
     r = 64
-    om = torch.empty((1 << 21, r), dtype=torch.float32, device="cuda")  # 2M rows: ~66 MB of scratch
+    # 4M rows: 2048 row chunks of one 64 x 64 float64 partial each (64 MiB) plus the panel's rest.
+    om = torch.empty((1 << 22, r), dtype=torch.float32, device="cuda")
     out = torch.empty_like(om)
     with pytest.raises(zo.ZoError, match="static scratch"):
         zo.subspace_refresh_noalloc([om], r, [out])
