@@ -119,8 +119,9 @@ __global__ __launch_bounds__(256) void k_cqr_rows(CqrArgs a) {
   }
   const int row0 = chunk * CHUNK + wave * WROWS;
   const int nrow = min(WROWS, P.rows - row0);  // this wave's rows (none past the end)
-  auto om = [&](int row, int col) -> double {
-    return (row < P.rows && col < r) ? (double)P.omega[(size_t)row * r + col] : 0.0;
+  // Omega entries as loaded (fp32, zero outside the panel); widened to float64 at use (exact).
+  auto om = [&](int row, int col) -> float {
+    return (row < P.rows && col < r) ? P.omega[(size_t)row * r + col] : 0.f;
   };
   f64x4 acc[NPAIR];
 #pragma unroll
@@ -134,43 +135,51 @@ __global__ __launch_bounds__(256) void k_cqr_rows(CqrArgs a) {
       for (int tb = ta; tb < RK; ++tb, ++p) acc[p] = mfma64(v[ta], v[tb], acc[p]);
   };
   if (PASS == 0) {
-    // 16 rows per step (four 4-row Gram steps), the next step's loads issued before the MFMAs.
-    double nx[4][RK];
+    // 32 rows per step (eight 4-row Gram steps), the next step's loads issued before the MFMAs.
+    float nx[8][RK];
     auto load = [&](int s) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
         for (int t = 0; t < RK; ++t) nx[u][t] = om(row0 + s + 4 * u + g, 16 * t + l16);
     };
     if (nrow > 0) load(0);
-    for (int s = 0; s < nrow; s += 16) {
-      double cur[4][RK];
+    for (int s = 0; s < nrow; s += 32) {
+      float cur[8][RK];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 8; ++u)
 #pragma unroll
         for (int t = 0; t < RK; ++t) cur[u][t] = nx[u][t];
-      if (s + 16 < nrow) load(s + 16);
+      if (s + 32 < nrow) load(s + 32);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) gram(cur[u]);
+      for (int u = 0; u < 8; ++u) {
+        double v[RK];
+#pragma unroll
+        for (int t = 0; t < RK; ++t) v[t] = (double)cur[u][t];
+        gram(v);
+      }
     }
   } else {
-    double nx[KS];
+    float nx[KS];
     auto load = [&](int s) {
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) nx[kk] = om(row0 + s + l16, g * KS + kk);
     };
     if (nrow > 0) load(0);
     for (int s = 0; s < nrow; s += 16) {
-      double av[KS];
+      float av[KS];
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) av[kk] = nx[kk];
       if (s + 16 < nrow) load(s + 16);
+      // The RK product chains interleaved (each still sums its K steps in order).
       f64x4 q[RK];
 #pragma unroll
-      for (int t = 0; t < RK; ++t) {
-        q[t] = (f64x4){0.0, 0.0, 0.0, 0.0};
+      for (int t = 0; t < RK; ++t) q[t] = (f64x4){0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) q[t] = mfma64(av[kk], Mx[(g * KS + kk) * RP + 16 * t + l16], q[t]);
+      for (int kk = 0; kk < KS; ++kk) {
+        const double x = (double)av[kk];
+#pragma unroll
+        for (int t = 0; t < RK; ++t) q[t] = mfma64(x, Mx[(g * KS + kk) * RP + 16 * t + l16], q[t]);
       }
       // q[t][v]: row row0 + s + 4 v + g, column 16 t + l16.
       if (PASS == 1) {
@@ -228,17 +237,30 @@ __global__ __launch_bounds__(256) void k_cqr_chol(CqrArgs a) {
   constexpr int RP = 16 * RK;
   __shared__ double G[RP * RP];
   __shared__ double X[RP * RP];
+  __shared__ double X1s[FINAL ? RP * RP : 1];
   __shared__ double inv[RP];
   const CqrPanel& P = a.p[blockIdx.x];
   const int r = a.r, tid = threadIdx.x;
   const int nchunk = (P.rows + CHUNK - 1) / CHUNK;
-  for (int x = tid; x < RP * RP; x += 256) {
-    const int i = x / RP, j = x % RP;
-    double s = 0.0;
-    if (i <= j && j < r)
-      for (int c = 0; c < nchunk; ++c) s += P.part[(size_t)c * RP * RP + x];
-    G[x] = s;
+  // Entry x = tid + 256 e of G: the chunks' partials added in chunk order, the loads of one
+  // chunk for all of a thread's entries in flight together.
+  constexpr int EPT = RP * RP / 256;
+  double gs[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) gs[e] = 0.0;
+  for (int c = 0; c < nchunk; ++c) {
+    const double* pc = P.part + (size_t)c * RP * RP;
+    double v[EPT];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int x = tid + 256 * e, i = x / RP, j = x % RP;
+      v[e] = (i <= j && j < r) ? pc[x] : 0.0;
+    }
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) gs[e] += v[e];
   }
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) G[tid + 256 * e] = gs[e];
   __syncthreads();
   for (int k = 0; k < r; ++k) {
     if (tid == 0) {
@@ -281,10 +303,13 @@ __global__ __launch_bounds__(256) void k_cqr_chol(CqrArgs a) {
     }
     return;
   }
+  // M = X1 X2, X1 staged in LDS.
+  for (int x = tid; x < RP * RP; x += 256) X1s[x] = P.X1[x];
+  __syncthreads();
   for (int x = tid; x < RP * RP; x += 256) {
     const int i = x / RP, j = x % RP;
     double s = 0.0;
-    for (int k = 0; k < RP; ++k) s = fma(P.X1[i * RP + k], X[k * RP + j], s);
+    for (int k = 0; k < RP; ++k) s = fma(X1s[i * RP + k], X[k * RP + j], s);
     P.M[x] = s;
   }
   if (tid == 0) {
