@@ -97,7 +97,8 @@ class ZFeed:
     """The per-step coefficients Z_j of every perturbed factor (Alg. 3: one Gaussian r x r draw
     per query and matrix, keyed by step), drawn on the host inside the timed window.
 
-    A worker thread draws step s + 1 into a pinned host buffer while the GPU runs step s; the
+    A worker thread draws step s + 1 into a pinned host buffer while the GPU runs step s (it is
+    started once step s is enqueued); the
     copy to the device runs on a side stream, and the compute stream waits for it before the
     step's first use.  Two device slots alternate: the copy into a slot waits until the compute
     stream has finished the step that last read it, and the host buffer of a slot is refilled
@@ -120,6 +121,7 @@ class ZFeed:
         self.draw_s = {}
         self.h2d = {}
         self.nbytes = 4 * nfac * q * r * r
+        self.cur = -1
 
     def _draw(self, s, slot):
         import zo_draws as zd
@@ -137,8 +139,7 @@ class ZFeed:
             self.pending[s] = self.pool.submit(self._draw, s, s % 2)
 
     def acquire(self, s):
-        """Device slot holding step s's Z, ordered before the compute stream's next work; starts
-        the host draw of step s + 1."""
+        """Device slot holding step s's Z, ordered before the compute stream's next work."""
         import torch
         slot = s % 2
         self.request(s)
@@ -154,15 +155,22 @@ class ZFeed:
         self.copied[slot] = e1
         torch.cuda.current_stream().wait_event(e1)
         self.h2d[s] = (e0, e1)
-        self.request(s + 1)
+        self.cur = s
         return slot
 
     def release(self, slot):
-        """The compute stream's work on this slot is enqueued: the next copy into it waits for it."""
+        """The compute stream's work on this slot is enqueued: the next copy into it waits for it.
+        Then starts the host draw of the next step.  The draw is requested only now, once the
+        whole step is enqueued: a draw loop running beside the enqueue holds the interpreter lock
+        in slices, and the enqueuing thread, which gives the lock up in every library call, waits
+        out a slice each time (a 1.1 ms refresh call took up to 1.3 s beside a looping draw, and
+        15 ms of GPU idling at a step's start in the benchmark).  This thread then blocks in the
+        next acquire while the GPU runs the step just enqueued."""
         import torch
         ev = torch.cuda.Event()
         ev.record()
         self.freed[slot] = ev
+        self.request(self.cur + 1)
 
     def report(self, steps):
         """Host draw and copy time of the given steps (ms per step)."""
@@ -174,8 +182,8 @@ class ZFeed:
                 "z_h2d_ms_per_step": round(sum(c) / max(1, len(c)), 3),
                 "z_h2d_gbs": round(self.nbytes * len(c) / max(1e-9, sum(c) * 1e-3) / 1e9, 1) if c else None,
                 "in_timed_window": True,
-                "how": "worker thread draws step s+1 on the host while step s runs; pinned buffer; "
-                       "copy on a side stream; the compute stream waits for it"}
+                "how": "worker thread draws step s+1 on the host while step s runs (requested once step s "
+                       "is enqueued); pinned buffer; copy on a side stream; the compute stream waits for it"}
 
 
 def omega_host_draw(seed, panels, r, F, sample=6):
