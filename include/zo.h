@@ -133,8 +133,9 @@ int zo_subspace_refresh(int count, const zo_panel* panels, int r, int* info,
  *   - A call whose zo_subspace_refresh_workspace size exceeds
  *     ZO_NOALLOC_SCRATCH_BYTES returns ZO_ERR_WORKSPACE and launches nothing;
  *     split its panels over several calls.  (Each panel of r <= 64 needs about
- *     (ceil(rows / 1024) + 3) * 32 KiB; of 64 < r <= 128 about
- *     ceil(rows / 1024) * 66 KiB + 384 KiB.)
+ *     (ceil(rows / 2048) + 3) * 32 KiB; of 64 < r <= 128 about
+ *     ceil(rows / 1024) * 66 KiB + 384 KiB; plus 72 bytes per panel for the
+ *     call's descriptor table.)
  *   - Every call on one GPU uses the same scratch: calls that overlap on one
  *     GPU (on different streams, or from different threads without ordering)
  *     race and give wrong results.  Calls enqueued on one stream are ordered

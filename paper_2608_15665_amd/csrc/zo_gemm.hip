@@ -7,13 +7,15 @@
 //                      high bf16 part of V^T, rows [rp, 2 rp) the low part
 //                      (V = hi + lo to ~16 bits); rp = r rounded up to 32
 //                      (16 for fp32 inputs).
-//   2. P2 = X_x Vt2^T: the n -> rp projection of every distinct X block, as
-//                      two fp32 halves (one GEMM launch, narrow A operand).
-//   3. k_pcombine    : P = P2_hi + P2_lo, written as the K segment
-//                      [P_hi | P_hi | P_lo] (bf16, 3 rp wide).
-//   4. k_bprime      : B_b = s_b eps U Z_{j(b)} (fp32) written as the K segment
+//   2. k_bprime      : B_b = s_b eps U Z_{j(b)} (fp32) written as the K segment
 //                      [B_hi | B_lo | B_hi] (bf16, 3 rp wide), every block.
-//   5. main GEMM     : Y_b = X_b W^T + P_{x(b)} B_b^T, the rank-r term added as
+//   3. projection    : P = X_x Vt2_hi^T + X_x Vt2_lo^T of every distinct X block,
+//                      written as the K segment [P_hi | P_hi | P_lo] (bf16,
+//                      3 rp wide).  k_proj for one factor of 64 or 128 rows
+//                      (or a pair of 64), the main GEMM with the EPI_PROJ
+//                      epilogues for a stack of factors that read the same X;
+//                      otherwise an fp32 projection followed by k_pcombine.
+//   4. main GEMM     : Y_b = X_b W^T + P_{x(b)} B_b^T, the rank-r term added as
 //                      one more 3 rp-deep K segment into the same fp32
 //                      accumulators: hi*hi + hi*lo + lo*hi, so the correction
 //                      carries ~2^-16 relative error instead of the 2^-8 of
@@ -26,16 +28,15 @@
 // 1/sqrt(n) then stay normal); k_pcombine multiplies by 1/256 (exact).
 // fp32 inputs: Vt (rp x n), P = X Vt^T and B_b in fp32, fp32 FMA throughout.
 //
-// bf16 GEMM: one workgroup computes a BM x BN tile of Y_b^T (BM output
-// columns, BN tokens) with v_mfma_f32_32x32x16_bf16.  The A operand is the
-// W tile (rows = output columns), the B operand the X tile (rows = tokens);
-// both are K-contiguous, staged through LDS in 128-byte rows with an XOR
-// swizzle of the 16-byte chunks, double buffered.  Accumulator lane layout of
-// the 32x32 MFMA: lane l holds token (l % 32) and output columns
-// 8a + 4(l / 32) + {0,1,2,3}, a = 0..3, so each lane stores 4 adjacent
-// outputs.  Workgroup ids are remapped so that the tiles one XCD runs
-// concurrently are contiguous, then grouped 8 token tiles deep so the tiles
-// in flight on an XCD share their W and X panels in that XCD's L2.
+// The main GEMM (k_gemm_main) is described where it is defined.  The
+// register-staged GEMM (k_gemm_bf16: the projection of wide factors and the
+// fallback when K is not a multiple of 32) computes a BM x BN tile of Y_b^T
+// with v_mfma_f32_32x32x16_bf16: the A operand is the W tile (rows = output
+// columns), the B operand the X tile (rows = tokens), both K-contiguous and
+// staged through LDS in 128-byte rows with an XOR swizzle of the 16-byte
+// chunks, double buffered.  Workgroup ids are remapped so that the tiles one
+// XCD runs concurrently are contiguous, then grouped 8 token tiles deep so the
+// tiles in flight on an XCD share their W and X panels in that XCD's L2.
 #include "zo_internal.h"
 
 #include <type_traits>

@@ -88,6 +88,7 @@ def run_oracle(c, eps, blocks=None, rows=None):
     (1, 3, 1, 1, 1, 1, False),          # degenerate sizes
     (130, 72, 300, 20, 2, 4, True),
     (64, 200, 300, 128, 2, 4, False),   # r = 128, the paper's full-tuning rank
+    (50, 100, 200, 80, 2, 4, False),    # 64 < r <= 96 (rp = 80 of a 96-column product)
 ])
 def test_fp32_parity(T, m, n, r, q, nblk, shared):
     c = make_case(T, m, n, r, q, nblk, shared, bf16=False)
@@ -105,6 +106,7 @@ def test_fp32_parity(T, m, n, r, q, nblk, shared):
     (8, 8, 8, 1, 1, 1, True),           # smallest legal bf16 shape
     (192, 256, 384, 128, 2, 4, False),  # r = 128, the paper's full-tuning rank
     (100, 136, 264, 100, 3, 6, True),   # r = 100 padded to 128
+    (200, 264, 256, 80, 2, 4, False),   # r = 80 padded to 96
 ])
 @pytest.mark.parametrize("out", ["bf16", "f32"])
 def test_bf16_parity(T, m, n, r, q, nblk, shared, out):
@@ -336,6 +338,7 @@ def test_forward_difference_layout_at_paper_k():
     (300, 512, 64, [256, 128, 72]),   # 3 x 128 stacked rows: the main GEMM, combine in its epilogue
     (260, 320, 24, [64, 200, 136]),   # 3 x 64 rows (rp = 32) on the main GEMM
     (130, 256, 40, [96, 160]),        # 2 x 128 rows: one whole 256-row tile
+    (300, 320, 20, [96, 160]),        # 2 x 64 rows (rp = 32): one k_proj tile holds both factors
 ])
 def test_prepare_group_equals_separate(dt, shared, T, n, r, ms):
     """zo_perturbed_linear_prepare_group (one projection pass for matrices that read the same X,
