@@ -500,13 +500,20 @@ __global__ __launch_bounds__(256) void k_gemm_f32(F32Args a) {
 
 // Vt[a][k] = V[k][a] for a < r, 0 for r <= a < rp.  16-bit: hi part in rows
 // [0, rp), low part (V - hi, rounded) in rows [rp, 2 rp); fp16 splits 256 V.
-__global__ __launch_bounds__(256) void k_transpose_v(const float* __restrict__ V, int n, int r,
-                                                      int rp, void* Vt, int dtype) {
+// Factor blockIdx.y of a group that shares n, r and rp.
+struct TvArgs {
+  const float* V[ZO_MAX_GROUP];
+  void* Vt[ZO_MAX_GROUP];
+  int n, r, rp, dtype;
+};
+__global__ __launch_bounds__(256) void k_transpose_v(TvArgs t) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  const int n = t.n, r = t.r, rp = t.rp;
   if (idx >= (long long)rp * n) return;
+  const float* __restrict__ V = t.V[blockIdx.y];
   const int a = (int)(idx / n), k = (int)(idx % n);
   const float v = a < r ? V[(size_t)k * r + a] : 0.f;
-  put_split(Vt, idx, (long long)rp * n, v, dtype);
+  put_split(t.Vt[blockIdx.y], idx, (long long)rp * n, v, t.dtype);
 }
 
 // P = (P2[:, :rp] + P2[:, rp:]) * unscale (fp32; unscale a power of two; P2 rows ld2 apart),
@@ -548,18 +555,34 @@ struct BpShape {
   static constexpr int R = RR * RT;   // rows per workgroup
 };
 
+// Factor blockIdx.z of a group that shares r, rp, the blocks and eps (one factor: a group of 1);
+// the grid covers the tallest factor.
+struct BpArgs {
+  const float* U[ZO_MAX_GROUP];
+  const float* Z[ZO_MAX_GROUP];
+  void* Bp[ZO_MAX_GROUP];
+  int m[ZO_MAX_GROUP];
+  int r, rp, nblk, out_bf16;
+  float eps;
+  BlkTable tab;
+};
+
 template <int RPK>
-__global__ __launch_bounds__(256) void k_bprime(const float* __restrict__ U,
-                                                const float* __restrict__ Z, int m, int r,
-                                                int rp, int nblk, float eps, BlkTable tab,
-                                                void* Bp, int out_bf16) {
+__global__ __launch_bounds__(256) void k_bprime(BpArgs a) {
   constexpr int RP = BpShape<RPK>::RP, G = BpShape<RPK>::G, RR = BpShape<RPK>::RR;
   constexpr int RT = BpShape<RPK>::RT, R = BpShape<RPK>::R;
   constexpr int UL = RP + 4;  // floats per staged U row (rows 4 banks apart)
   __shared__ __attribute__((aligned(16))) float Zl[32 * RP];  // 32 rows of Z_j at a time
   __shared__ __attribute__((aligned(16))) float Ul[R * UL];
+  const int f = blockIdx.z;
+  const int m = a.m[f], r = a.r, rp = a.rp, nblk = a.nblk, out_bf16 = a.out_bf16;
+  const float eps = a.eps;
+  const float* __restrict__ U = a.U[f];
+  const float* __restrict__ Z = a.Z[f];
+  void* const Bp = a.Bp[f];
   const int j = blockIdx.y;
   const int i0 = blockIdx.x * R;
+  if (i0 >= m) return;  // past a shorter factor: the whole workgroup, before any barrier
   const int tid = threadIdx.x;
   const float* __restrict__ Zj = Z + (size_t)j * r * r;
   for (int x = tid; x < R * RP; x += 256) {
@@ -635,7 +658,7 @@ __global__ __launch_bounds__(256) void k_bprime(const float* __restrict__ U,
         lp[y] = pack_bf16x2(a0 - bf16_to_f32(f32_to_bf16(a0)), a1 - bf16_to_f32(f32_to_bf16(a1)));
       }
       for (int b = 0; b < nblk; ++b) {
-        const int code = tab.code[b];
+        const int code = a.tab.code[b];
         if ((code & 0xffff) != j) continue;
         const int s = (code >> 16) - 1;
         // Negation flips the sign bits; zero times the sign is +0.
@@ -651,7 +674,7 @@ __global__ __launch_bounds__(256) void k_bprime(const float* __restrict__ U,
       // fp32 keeps rp == round16(r) wide rows; RP may exceed rp (whole groups of 8).
       if (cg * 8 >= rp) break;
       for (int b = 0; b < nblk; ++b) {
-        const int code = tab.code[b];
+        const int code = a.tab.code[b];
         if ((code & 0xffff) != j) continue;
         const float s = (float)((code >> 16) - 1);
         float* o = (float*)Bp + ((long long)b * m + i) * rp + cg * 8;
@@ -1451,25 +1474,50 @@ PlinearWs zo_plinear_ws(const PlinearPlan& p, void* ws) {
   return w;
 }
 
-static int launch_transpose_v(const PlinearPlan& p, const float* V, void* vt, hipStream_t stream) {
+// Vt2 of `count` factors that share n, r and rp (plans[i] gives factor i's; V[i] -> vt[i]).
+static int launch_transpose_v(const PlinearPlan* plans, int count, const float* const* V, void* const* vt,
+                              hipStream_t stream) {
+  const PlinearPlan& p = plans[0];
+  TvArgs t{};
+  for (int i = 0; i < count; ++i) {
+    t.V[i] = V[i];
+    t.Vt[i] = vt[i];
+  }
+  t.n = p.n;
+  t.r = p.r;
+  t.rp = p.rp;
+  t.dtype = p.in_dtype;
   const long long total = (long long)p.rp * p.n;
-  hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
-                     V, p.n, p.r, p.rp, vt, p.in_dtype);
+  hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((total + 255) / 256), (unsigned)count), dim3(256), 0, stream,
+                     t);
   return zo_hip_status(hipGetLastError(), "k_transpose_v");
 }
 
-static int launch_bprime(const PlinearPlan& p, const BlkTable& tab, float eps, const float* U,
-                         const float* Z, void* bp, hipStream_t stream) {
-  auto grid = [&](int rows) { return dim3((unsigned)((p.m + rows - 1) / rows), (unsigned)p.q); };
+// B' of `count` factors that share r, rp, the blocks and eps (heights may differ): one launch.
+static int launch_bprime(const PlinearPlan* plans, int count, const BlkTable& tab, float eps,
+                         const float* const* U, const float* const* Z, void* const* bp, hipStream_t stream) {
+  const PlinearPlan& p = plans[0];
+  BpArgs a{};
+  int mmax = 0;
+  for (int i = 0; i < count; ++i) {
+    a.U[i] = U[i];
+    a.Z[i] = Z[i];
+    a.Bp[i] = bp[i];
+    a.m[i] = plans[i].m;
+    mmax = std::max(mmax, plans[i].m);
+  }
+  a.r = p.r;
+  a.rp = p.rp;
+  a.nblk = p.nblk;
+  a.out_bf16 = p.in16;
+  a.eps = eps;
+  a.tab = tab;
+  auto grid = [&](int rows) { return dim3((unsigned)((mmax + rows - 1) / rows), (unsigned)p.q, (unsigned)count); };
   switch ((p.r + 31) / 32) {
-    case 1: hipLaunchKernelGGL(k_bprime<1>, grid(BpShape<1>::R), dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                               eps, tab, bp, p.in16); break;
-    case 2: hipLaunchKernelGGL(k_bprime<2>, grid(BpShape<2>::R), dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                               eps, tab, bp, p.in16); break;
-    case 3: hipLaunchKernelGGL(k_bprime<3>, grid(BpShape<3>::R), dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                               eps, tab, bp, p.in16); break;
-    default: hipLaunchKernelGGL(k_bprime<4>, grid(BpShape<4>::R), dim3(256), 0, stream, U, Z, p.m, p.r, p.rp, p.nblk,
-                                eps, tab, bp, p.in16); break;
+    case 1: hipLaunchKernelGGL(k_bprime<1>, grid(BpShape<1>::R), dim3(256), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL(k_bprime<2>, grid(BpShape<2>::R), dim3(256), 0, stream, a); break;
+    case 3: hipLaunchKernelGGL(k_bprime<3>, grid(BpShape<3>::R), dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL(k_bprime<4>, grid(BpShape<4>::R), dim3(256), 0, stream, a); break;
   }
   return zo_hip_status(hipGetLastError(), "k_bprime");
 }
@@ -1479,8 +1527,10 @@ int zo_plinear_prepare(const PlinearPlan& p, const int* blk_query, const int8_t*
                        void* ws, hipStream_t stream) {
   const PlinearWs w = zo_plinear_ws(p, ws);
   int st;
-  if ((st = launch_transpose_v(p, V, w.vt, stream)) != ZO_OK) return st;
-  if ((st = launch_bprime(p, zo_blk_table(p.nblk, blk_query, blk_sign), eps, U, Z, w.bp, stream)) != ZO_OK)
+  void* vt = w.vt;
+  void* bp = w.bp;
+  if ((st = launch_transpose_v(&p, 1, &V, &vt, stream)) != ZO_OK) return st;
+  if ((st = launch_bprime(&p, 1, zo_blk_table(p.nblk, blk_query, blk_sign), eps, &U, &Z, &bp, stream)) != ZO_OK)
     return st;
   return zo_plinear_project(p, X, ws, stream);
 }
@@ -1620,11 +1670,15 @@ int zo_plinear_prepare_group(const PlinearPlan* plans, int count, const int* blk
   char* gvt = (char*)gws;
   float* gp2 = (float*)(gvt + zo_align256((size_t)count * w2 * p0.n * 2));
   const BlkTable tab = zo_blk_table(p0.nblk, blk_query, blk_sign);
+  // Vt2 and B' of every factor of the group: one launch each.
+  void* vts[ZO_MAX_GROUP];
+  void* bps[ZO_MAX_GROUP];
   for (int i = 0; i < count; ++i) {
-    const PlinearWs w = zo_plinear_ws(plans[i], ws[i]);
-    if ((st = launch_transpose_v(plans[i], V[i], gvt + (size_t)i * w2 * p0.n * 2, stream)) != ZO_OK) return st;
-    if ((st = launch_bprime(plans[i], tab, eps, U[i], Z[i], w.bp, stream)) != ZO_OK) return st;
+    vts[i] = gvt + (size_t)i * w2 * p0.n * 2;
+    bps[i] = zo_plinear_ws(plans[i], ws[i]).bp;
   }
+  if ((st = launch_transpose_v(plans, count, V, vts, stream)) != ZO_OK) return st;
+  if ((st = launch_bprime(plans, count, tab, eps, U, Z, bps, stream)) != ZO_OK) return st;
   // A stack of several factors stays on the main GEMM's 256-row tiles (two factors of 128 rows
   // per X tile: the stacked q, k, v run 0.50 ms there against 0.72 ms in three 128-row tiles of
   // k_proj), with the combine in its epilogue; only a 64-row pair shares one 128-row tile.
