@@ -57,9 +57,12 @@ def test_refresh_parity(rows, r):
     check(Q[0], rd[0], Om)
 
 
-def test_refresh_batched_mixed_rows_inplace():
-    r = 16
-    rows = [16, 100, 2048, 4097, 333] * 8  # 40 panels: more than one launch holds
+@pytest.mark.parametrize("r", [16, 64])
+def test_refresh_batched_mixed_rows_inplace(r):
+    """104 panels in one call: the descriptor table takes three fill launches and each pass one
+    launch over all panels; rows on both sides of the 2048-row chunks and the 512-row wave
+    quarters, computed in place."""
+    rows = [r, 100, 2048, 2049, 4097, 333, 511, 6000] * 13
     Oms = [zd.f32(zd.draw(1, "OMEGA_V", (i,), (rw, r))) for i, rw in enumerate(rows)]
     Q, rd, info = run(Oms, r, inplace=True)
     assert np.all(info == 0)
@@ -68,7 +71,7 @@ def test_refresh_batched_mixed_rows_inplace():
 
 
 def test_refresh_batched_wide_rank():
-    """r = 128 over 50 panels of mixed rows (two launches of the wide kernels)."""
+    """r = 128 over 50 panels of mixed rows (the wide kernels; two fill launches)."""
     r = 128
     rows = [128, 300, 2048, 1100, 129] * 10
     Oms = [zd.f32(zd.draw(4, "OMEGA_V", (i,), (rw, r))) for i, rw in enumerate(rows)]
