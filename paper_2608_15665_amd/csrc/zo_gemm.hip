@@ -25,7 +25,7 @@
 // smallest normal, and bf16 has fp32's range) on the bf16 MFMA, as more
 // k-tiles of the same pipeline.  The projection X_x Vt2^T runs on the fp16
 // MFMA with Vt2 the fp16 hi/lo split of 256 V (the low parts of entries near
-// 1/sqrt(n) then stay normal); k_pcombine multiplies by 1/256 (exact).
+// 1/sqrt(n) then stay normal); the combine multiplies by 1/256 (exact).
 // fp32 inputs: Vt (rp x n), P = X Vt^T and B_b in fp32, fp32 FMA throughout.
 //
 // The main GEMM (k_gemm_main) is described where it is defined.  The

@@ -156,6 +156,20 @@ def test_refresh_validation():
     assert L.zo_subspace_refresh(1, arr, 4, None, fake, 16, None) == 6
 
 
+def test_refresh_workspace_size():
+    """The refresh workspace as zo.h states it: 72 bytes per panel for the call's descriptor table,
+    then per panel of r <= 64 one float64 r_p x r_p partial Gram matrix per 2048-row chunk and three
+    r_p x r_p float64 factors (r_p = r rounded up to 16); each piece 256-byte aligned."""
+    L = zo.lib()
+    fake = 1 << 20
+    al = lambda b: (b + 255) // 256 * 256
+    for r, rows in ((64, [5000, 64, 2048, 2049]), (4, [8, 27648]), (24, [24, 100])):
+        rp = (r + 15) // 16 * 16
+        arr = (Panel * len(rows))(*[Panel(rw, fake, fake, None) for rw in rows])
+        want = al(72 * len(rows)) + sum(al(-(-rw // 2048) * rp * rp * 8) + 3 * al(rp * rp * 8) for rw in rows)
+        assert L.zo_subspace_refresh_workspace(len(rows), arr, r) == want, (r, rows)
+
+
 def test_update_validation():
     L = zo.lib()
     fake = 1 << 20
