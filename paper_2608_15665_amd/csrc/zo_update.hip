@@ -260,11 +260,17 @@ __global__ __launch_bounds__(256) void k_us(USArgs a) {
       const int row = k0 + x / G, c0 = (x % G) * 8;
       if (row >= it.n) break;
       float v[8], lo[8];
+      const float* vr = it.V + (size_t)row * r + c0;
+      if (r % 4 == 0 && c0 + 8 <= r && (uintptr_t)it.V % 16 == 0) {  // two 16-byte loads
+        const f32x4 a0 = *(const f32x4*)vr, a1 = *(const f32x4*)(vr + 4);
+        v[0] = a0[0]; v[1] = a0[1]; v[2] = a0[2]; v[3] = a0[3];
+        v[4] = a1[0]; v[5] = a1[1]; v[6] = a1[2]; v[7] = a1[3];
+      } else {
 #pragma unroll
-      for (int z = 0; z < 8; ++z) {
-        v[z] = c0 + z < r ? it.V[(size_t)row * r + c0 + z] : 0.f;
-        lo[z] = v[z] - bf16_to_f32(f32_to_bf16(v[z]));
+        for (int z = 0; z < 8; ++z) v[z] = c0 + z < r ? vr[z] : 0.f;
       }
+#pragma unroll
+      for (int z = 0; z < 8; ++z) lo[z] = v[z] - bf16_to_f32(f32_to_bf16(v[z]));
       *(u32x4*)(Vh + (size_t)row * RP + c0) = (u32x4){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
                                                       pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
       *(u32x4*)(Vl + (size_t)row * RP + c0) =
